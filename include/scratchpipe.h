@@ -1,0 +1,195 @@
+/*
+ * scratchpipe.h - C ABI of an MI355X embedding-training scratchpad.
+ *
+ * The library trains embedding tables that live in pinned host memory through
+ * a GPU-resident cache (the "scratchpad": Storage plus Hit-Map, Sec. IV-D).
+ * Because the sparse IDs of upcoming mini-batches are already known from the
+ * training data (Sec. IV-A), every batch is planned before it is trained: its
+ * missing rows are brought in and victims are chosen only among slots that no
+ * batch of the look-forward window uses (Sec. IV-C), so forward and backward
+ * always hit in HBM.  One training step is
+ *
+ *     sp_plan(window)  ->  sp_forward(ticket)  ->  sp_backward_update(ticket)
+ *
+ * and sp_flush() makes the host tables authoritative again.
+ *
+ * Conventions shared by every call:
+ *  - Batches are table-major CSR: ids[] holds table 0's row IDs, then table
+ *    1's, ...; bag g = t*B + b spans ids[bag_off[g] .. bag_off[g+1]); row IDs
+ *    are local to their table; bag_off has T*B+1 entries, bag_off[0] = 0 and
+ *    bag_off[T*B] = nnz.
+ *  - Pooled outputs and their gradients are fp32 [T][B][D] in device memory
+ *    owned by the caller (row g = t*B + b).
+ *  - Return value: SP_OK (0) or a negative sp_status.  After SP_ERR_HIP the
+ *    context is unusable and only sp_destroy is valid.  sp_last_error()
+ *    describes the last failure.
+ *  - One context is used from one host thread at a time.
+ */
+#ifndef SCRATCHPIPE_H
+#define SCRATCHPIPE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t sp_status;
+#define SP_OK 0
+#define SP_ERR_INVALID_ARG (-1) /* bad config, bad IDs or offsets, bad pointer        */
+#define SP_ERR_OOM (-2)         /* device or pinned allocation failed                  */
+#define SP_ERR_CAPACITY (-3)    /* some table has more misses than unheld slots        */
+#define SP_ERR_SEQUENCE (-4)    /* call out of plan -> forward -> backward order       */
+#define SP_ERR_HIP (-5)         /* a HIP runtime call failed (sticky)                  */
+#define SP_ERR_STATE (-6)       /* context unusable (after SP_ERR_HIP) or null handle  */
+
+/* sp_config.flags */
+#define SP_FLAG_DEBUG_SYNC 0x1u /* synchronise the device at the end of every call     */
+#define SP_FLAG_TIMING 0x2u     /* time forward/backward/plan/fill kernels with events */
+
+typedef struct sp_ctx *sp_handle;
+
+typedef struct {
+    int32_t num_tables;         /* T, 1..64                                            */
+    const int64_t *rows;        /* [T] rows per table, 1 .. 2^25                       */
+    int32_t dim;                /* D, fp32 elements per row; multiple of 4, <= 256     */
+    const int64_t *slots;       /* [T] scratchpad slots per table, 1 .. rows[t]         */
+    int32_t lookahead;          /* L >= 0: successor batches a plan may hold           */
+    float *const *host_tables;  /* [T] row-major [rows][D] fp32 tables in pinned host
+                                   memory from sp_host_alloc (or hipHostMalloc with the
+                                   mapped flag); caller-owned, must outlive the context;
+                                   read on misses, written on evictions and flush      */
+    int32_t max_batch;          /* largest B any batch will have                       */
+    int64_t max_ids;            /* largest nnz any batch will have (all tables)        */
+    uint32_t flags;             /* SP_FLAG_*                                           */
+    int32_t device;             /* HIP device ordinal                                  */
+} sp_config;
+
+typedef struct {
+    int32_t batch;              /* B, 0 .. max_batch                                   */
+    int64_t nnz;                /* number of IDs, 0 .. max_ids                          */
+    const int32_t *ids;         /* [nnz] row IDs, table-major                          */
+    const int32_t *bag_off;     /* [T*B+1] bag offsets                                 */
+    int32_t on_device;          /* 0: ids/bag_off are host memory; 1: device memory    */
+} sp_batch;
+
+typedef struct {
+    int64_t plans;              /* plans committed                                     */
+    int64_t updates;            /* backward updates issued                              */
+    int64_t lookups;            /* IDs planned (sum of nnz)                             */
+    int64_t unique;             /* unique (table,row) keys planned                      */
+    int64_t hits, misses;       /* unique keys found / not found in the Hit-Map         */
+    int64_t evictions;          /* misses placed in a slot that held a row              */
+    int64_t bytes_fill;         /* host -> HBM bytes of miss fills                      */
+    int64_t bytes_writeback;    /* HBM -> host bytes of evicted rows                    */
+    int64_t hash_rebuilds;
+    int64_t min_capacity_margin;/* min over plans and tables of unheld slots - misses  */
+    int64_t device_bytes;       /* device memory held by the context                    */
+    int64_t pinned_bytes;       /* pinned staging held by the context                   */
+    /* SP_FLAG_TIMING only: summed kernel time in ms and number of timed calls */
+    double ms_forward, ms_backward, ms_plan, ms_fill;
+    int64_t timed_forward, timed_backward, timed_plan, timed_fill;
+} sp_stats;
+
+/* Per-plan decisions copied to the host for checking.  The caller allocates
+ * every array with room for the planned batch's nnz entries.  Slots are global
+ * (table t's slots follow tables 0..t-1).  Filled fields:
+ *   u_table,u_row,hit,slot_u [n_unique]  the batch's unique keys, ascending
+ *                                        (table,row); hit=1 if it was cached;
+ *                                        slot_u = its slot after the plan
+ *   inv,slot_of [nnz]                    index into u_*, slot of ids[j]
+ *   m_table,m_row,v_slot,v_old_row,v_old_use [n_miss]
+ *                                        misses in ascending (table,row), the
+ *                                        slot each one gets, the row evicted
+ *                                        from it (-1 if none) and that slot's
+ *                                        previous last-use plan index (-1 if
+ *                                        never used) */
+typedef struct {
+    int32_t *u_table, *u_row, *inv, *m_table, *m_row, *v_slot, *v_old_row, *v_old_use;
+    int32_t *slot_u, *slot_of;
+    uint8_t *hit;
+    int64_t n_unique, n_miss, n_evict, nnz;
+} sp_plan_dump;
+
+/*
+ * Create a context: allocates Storage (sum(slots) x D fp32), the Hit-Map hash,
+ * per-slot metadata, the window ring and staging buffers on config->device,
+ * and two library streams at default priority.  Nothing is cached initially.
+ * Errors: SP_ERR_INVALID_ARG (config out of range, host table not pinned and
+ * mapped), SP_ERR_OOM, SP_ERR_HIP.  *out is set only on success.
+ * (Sec. IV-D "GPU scratchpad design": Storage and Hit-Map.)
+ */
+sp_status sp_create(const sp_config *config, sp_handle *out);
+
+/*
+ * Plan the next mini-batch.  window[0] is the batch to plan (ticket k = number
+ * of plans so far) and window[1..n-1] are the batches that follow it, n-1 <=
+ * lookahead; the same batch must be passed with the same content every time
+ * it appears.  Batches enter the device window ring once (sorted and
+ * deduplicated on arrival); window buffers may be reused when the call
+ * returns.  The plan queries the Hit-Map for window[0]'s unique keys, holds
+ * every cached slot used by any window batch, takes for each table's misses
+ * the least-recently-used unheld slots (oldest first, ties by slot; the
+ * ascending misses take them in that order), updates Hit-Map, slot keys and
+ * last-use, and enqueues the evicted rows' write-back and the misses' fill
+ * (Sec. IV-C "Putting everything together", Sec. IV-D Algorithm 1; LRU from
+ * Sec. VI-E).  The host waits once for per-table counts.
+ * Requires the previous ticket's sp_backward_update to have been issued.
+ * Transactional: on SP_ERR_INVALID_ARG (ID out of range, bad offsets, sizes
+ * above the config) or SP_ERR_CAPACITY (misses > unheld slots in some table)
+ * the scratchpad state is unchanged and the same ticket can be planned again.
+ */
+sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int64_t *ticket);
+
+/*
+ * Pooled forward of a planned batch: d_out[t*B+b][:] = sum of the Storage rows
+ * of bag (t,b) (Sec. II-B "Forward propagation", sum reduction; empty bag ->
+ * zeros).  Enqueued on `stream` (a hipStream_t; NULL = default stream) after
+ * the ticket's fill.  `ticket` must be the latest plan, not yet forwarded.
+ * d_out: caller-owned device fp32 [T][B][D].  Errors: SP_ERR_SEQUENCE,
+ * SP_ERR_INVALID_ARG (null d_out with B*T > 0).
+ */
+sp_status sp_forward(sp_handle h, int64_t ticket, float *d_out, void *stream);
+
+/*
+ * Backward and update of a forwarded batch: every unique row gets the sum of
+ * the gradients of the bags that gathered it, positions in ascending order,
+ * and Storage[row] -= lr * sum in place (Sec. II-B "Backpropagation"; plain
+ * SGD).  d_grad: device fp32 [T][B][D].  Enqueued on `stream`.
+ * Errors: SP_ERR_SEQUENCE, SP_ERR_INVALID_ARG.
+ */
+sp_status sp_backward_update(sp_handle h, int64_t ticket, const float *d_grad, float lr,
+                             void *stream);
+
+/*
+ * Synchronise everything and write every cached row back to its host table;
+ * afterwards the host tables hold the trained model.  The scratchpad keeps
+ * its contents, so training may continue.  (Evicted entries are dirty and must
+ * be written back, Sec. IV-B; flush applies that to all entries.)
+ */
+sp_status sp_flush(sp_handle h);
+
+/* Counters since sp_create (synchronises pending timing events). */
+sp_status sp_get_stats(sp_handle h, sp_stats *out);
+
+/* Copy the decisions of the most recent plan (ticket must equal it) to host
+ * arrays; for checking against a reference.  Synchronises the library stream. */
+sp_status sp_debug_plan(sp_handle h, int64_t ticket, sp_plan_dump *out);
+
+/* Wait for all work, join the write-back thread, free everything.  NULL is ok. */
+void sp_destroy(sp_handle h);
+
+/* Text of the last error on this context (or of the last failed sp_create
+ * when h is NULL).  Valid until the next call on the context. */
+const char *sp_last_error(sp_handle h);
+
+/* Pinned, device-mapped host memory for host tables (hipHostMalloc with the
+ * mapped and portable flags; exact size).  *ptr is set on SP_OK. */
+sp_status sp_host_alloc(size_t bytes, void **ptr);
+void sp_host_free(void *ptr);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SCRATCHPIPE_H */

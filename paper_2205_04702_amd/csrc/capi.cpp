@@ -1,0 +1,910 @@
+// C ABI of the scratchpad: context, window ring, plan/forward/backward state
+// machine, write-back thread and flush.  Kernels live in k_*.hip.
+//
+// Streams.  The caller's stream runs forward and backward.  The library's
+// plan stream runs window ingest, the plan and the miss fill; its copy stream
+// runs the device-to-host copy of evicted rows, which a host thread then
+// scatters into the host tables ([Collect] / [Exchange] / [Insert] of
+// Sec. IV-B, with the CPU-side insert done off the critical path).
+//
+// Ordering (the RAW dependences of Sec. IV-B, for one plan k in flight while
+// batch k-1 trains):
+//  1  update(k-1) -> forward(k): forward(k) waits for update(k-1)'s event.
+//  2/3 update or fill -> victim read: a victim last used by batch k-1 is packed
+//     and refilled only after update(k-1); other victims after update(k-2).
+//     The plan itself never evicts a slot any window batch uses.
+//  4  host write-back -> later fill of the same row: a row evicted by plan p is
+//     not in batches p..p+n_p-1 (the hold window), so before the fill of plan k
+//     the host joins every write-back job with p + n_p <= k.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <condition_variable>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <deque>
+#include <mutex>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "../../include/scratchpipe.h"
+#include "sp_internal.h"
+
+using namespace sp;
+
+namespace {
+
+int bits_for(uint64_t v)  // bits needed to represent v (0 -> 0)
+{
+    int b = 0;
+    while (v) ++b, v >>= 1;
+    return b;
+}
+
+struct Timer {
+    static constexpr int N = 8;
+    hipEvent_t b[N]{}, e[N]{};
+    bool used[N]{};
+    int next = 0;
+    double ms = 0;
+    int64_t count = 0;
+    hipError_t init()
+    {
+        for (int i = 0; i < N; ++i) {
+            hipError_t r = hipEventCreate(&b[i]);
+            if (r != hipSuccess) return r;
+            r = hipEventCreate(&e[i]);
+            if (r != hipSuccess) return r;
+        }
+        return hipSuccess;
+    }
+    hipError_t harvest(int i)
+    {
+        if (!used[i]) return hipSuccess;
+        hipError_t r = hipEventSynchronize(e[i]);
+        if (r != hipSuccess) return r;
+        float x = 0;
+        r = hipEventElapsedTime(&x, b[i], e[i]);
+        if (r != hipSuccess) return r;
+        ms += x;
+        ++count;
+        used[i] = false;
+        return hipSuccess;
+    }
+    hipError_t begin(hipStream_t s)
+    {
+        hipError_t r = harvest(next);
+        return r != hipSuccess ? r : hipEventRecord(b[next], s);
+    }
+    hipError_t end(hipStream_t s)
+    {
+        hipError_t r = hipEventRecord(e[next], s);
+        used[next] = true;
+        next = (next + 1) % N;
+        return r;
+    }
+    hipError_t flush()
+    {
+        for (int i = 0; i < N; ++i) {
+            hipError_t r = harvest(i);
+            if (r != hipSuccess) return r;
+        }
+        return hipSuccess;
+    }
+    void destroy()
+    {
+        for (int i = 0; i < N; ++i) {
+            if (b[i]) hipEventDestroy(b[i]);
+            if (e[i]) hipEventDestroy(e[i]);
+        }
+    }
+};
+
+struct Job {
+    int64_t ticket = 0;
+    hipEvent_t ev = nullptr;
+    const float *rows = nullptr;
+    const int32_t *keys = nullptr;
+    int64_t n = 0;
+};
+
+struct TicketHost {
+    int64_t nnz = 0, n_unique = 0, n_chunks = 0, n_miss = 0;
+    int32_t B = 0;
+    int ring = 0;
+    int nwin = 0;
+};
+
+thread_local std::string g_create_error;
+
+}  // namespace
+
+struct sp_ctx {
+    // configuration
+    int T = 0, D = 0, L = 0, device = 0;
+    uint32_t flags = 0;
+    int32_t max_batch = 0;
+    int64_t max_ids = 0;
+    int key_bits = 0, chunk = 0;
+    Tables tb{};
+    int64_t slots[MAX_TABLES]{}, total_slots = 0, maxS = 0;
+    float *host[MAX_TABLES]{}, *host_dev[MAX_TABLES]{};
+
+    // device state
+    float *storage = nullptr;
+    int32_t *key_of_slot = nullptr, *last_use = nullptr, *held = nullptr;
+    uint64_t *hash = nullptr;
+    uint32_t hash_mask = 0;
+    int64_t hash_used = 0;
+
+    // window ring
+    int nring = 0;
+    std::vector<BatchDev> ring;
+    std::vector<int64_t> ring_batch, ring_nnz, ring_B;
+    std::vector<hipEvent_t> ring_free;
+    int64_t ingested = 0;
+
+    // tickets
+    TicketDev tk[TICKETS]{};
+    TicketHost tkh[TICKETS]{};
+    hipEvent_t ev_filled[TICKETS]{}, ev_upd[TICKETS]{};
+    int64_t planned = 0, forwarded = 0, updated = 0;
+    int32_t stamp = 0;
+
+    // scratch
+    uint32_t *tmp_k = nullptr, *tmp_v = nullptr, *hist = nullptr;
+    void *scan_tmp = nullptr;
+    int32_t *sel_state = nullptr, *sel_hist = nullptr;
+    uint32_t *vk0 = nullptr, *vv0 = nullptr, *vk1 = nullptr;
+    float *partial = nullptr;
+    DevCounters *cnt = nullptr, *h_cnt = nullptr;
+
+    // write-back staging (two in flight)
+    int64_t stage_rows = 0;
+    float *stage_dev[2]{}, *stage_host[2]{};
+    int32_t *stage_keys[2]{};
+    hipEvent_t ev_d2h[2]{};
+
+    hipStream_t s_plan = nullptr, s_copy = nullptr;
+
+    // write-back thread
+    std::thread worker;
+    std::mutex mu;
+    std::condition_variable cv, cv_done;
+    std::deque<Job> jobs;
+    int64_t done_upto = -1;
+    bool stop = false;
+    hipError_t worker_err = hipSuccess;
+    std::deque<std::pair<int64_t, int64_t>> deadlines;  // (ticket, first plan that may refill)
+    int64_t wb_evictions = 0, wb_bytes = 0;
+
+    // bookkeeping
+    sp_stats st{};
+    Timer t_fwd, t_bwd, t_plan, t_fill;
+    int64_t dev_bytes = 0, pinned_bytes = 0;
+    std::vector<void *> dev_allocs, pinned_allocs;
+    std::string err;
+    bool broken = false;
+};
+
+// ---------------------------------------------------------------- error helpers
+
+static sp_status fail(sp_ctx *h, sp_status code, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    if (h) {
+        h->err = buf;
+        if (code == SP_ERR_HIP) h->broken = true;
+    } else {
+        g_create_error = buf;
+    }
+    return code;
+}
+
+#define HIPCHK(h, call)                                                                        \
+    do {                                                                                       \
+        hipError_t _e = (call);                                                                \
+        if (_e != hipSuccess)                                                                  \
+            return fail((h), SP_ERR_HIP, "%s failed: %s (%s:%d)", #call, hipGetErrorString(_e), \
+                        __FILE__, __LINE__);                                                   \
+    } while (0)
+
+#define CHECK_LAUNCH(h) HIPCHK(h, hipGetLastError())
+
+static sp_status usable(sp_ctx *h)
+{
+    if (!h) return SP_ERR_STATE;
+    if (h->broken) return fail(h, SP_ERR_STATE, "context unusable after an earlier HIP error");
+    hipError_t e = hipSetDevice(h->device);
+    if (e != hipSuccess) return fail(h, SP_ERR_HIP, "hipSetDevice: %s", hipGetErrorString(e));
+    return SP_OK;
+}
+
+template <typename T>
+static sp_status dalloc(sp_ctx *h, T **p, int64_t count)
+{
+    size_t bytes = (size_t)std::max<int64_t>(count, 1) * sizeof(T);
+    hipError_t e = hipMalloc((void **)p, bytes);
+    if (e != hipSuccess) {
+        *p = nullptr;
+        (void)hipGetLastError();
+        return fail(h, SP_ERR_OOM, "hipMalloc(%zu) failed: %s", bytes, hipGetErrorString(e));
+    }
+    h->dev_allocs.push_back((void *)*p);
+    h->dev_bytes += (int64_t)bytes;
+    return SP_OK;
+}
+
+template <typename T>
+static sp_status palloc(sp_ctx *h, T **p, int64_t count)
+{
+    size_t bytes = (size_t)std::max<int64_t>(count, 1) * sizeof(T);
+    hipError_t e = hipHostMalloc((void **)p, bytes, hipHostMallocDefault);
+    if (e != hipSuccess) {
+        *p = nullptr;
+        (void)hipGetLastError();
+        return fail(h, SP_ERR_OOM, "hipHostMalloc(%zu) failed: %s", bytes, hipGetErrorString(e));
+    }
+    h->pinned_allocs.push_back((void *)*p);
+    h->pinned_bytes += (int64_t)bytes;
+    return SP_OK;
+}
+
+#define TRY(x)                          \
+    do {                                \
+        sp_status _s = (x);             \
+        if (_s != SP_OK) return _s;     \
+    } while (0)
+
+// ---------------------------------------------------------------- write-back thread
+
+static void worker_main(sp_ctx *h)
+{
+    (void)hipSetDevice(h->device);
+    const int rb = h->tb.row_bits;
+    const uint32_t mask = (1u << rb) - 1u;
+    const size_t row_bytes = sizeof(float) * (size_t)h->D;
+    for (;;) {
+        Job j;
+        {
+            std::unique_lock<std::mutex> lk(h->mu);
+            h->cv.wait(lk, [&] { return !h->jobs.empty() || h->stop; });
+            if (h->jobs.empty()) return;
+            j = h->jobs.front();
+        }
+        int64_t ev = 0;
+        if (j.n > 0) {
+            hipError_t e = hipEventSynchronize(j.ev);
+            if (e != hipSuccess) {
+                std::lock_guard<std::mutex> lk(h->mu);
+                h->worker_err = e;
+            } else {
+                for (int64_t i = 0; i < j.n; ++i) {
+                    const int32_t key = j.keys[i];
+                    if (key < 0) continue;
+                    const int t = key >> rb;
+                    const int64_t row = key & mask;
+                    memcpy(h->host[t] + row * h->D, j.rows + i * h->D, row_bytes);
+                    ++ev;
+                }
+            }
+        }
+        {
+            std::lock_guard<std::mutex> lk(h->mu);
+            h->jobs.pop_front();
+            h->done_upto = j.ticket;
+            h->wb_evictions += ev;
+            h->wb_bytes += ev * (int64_t)row_bytes;
+        }
+        h->cv_done.notify_all();
+    }
+}
+
+static sp_status join_jobs(sp_ctx *h, int64_t upto)
+{
+    std::unique_lock<std::mutex> lk(h->mu);
+    h->cv_done.wait(lk, [&] { return h->done_upto >= upto || h->worker_err != hipSuccess; });
+    if (h->worker_err != hipSuccess)
+        return fail(h, SP_ERR_HIP, "write-back thread: %s", hipGetErrorString(h->worker_err));
+    return SP_OK;
+}
+
+// ---------------------------------------------------------------- create / destroy
+
+static void release(sp_ctx *h)
+{
+    if (!h) return;
+    if (h->worker.joinable()) {
+        {
+            std::lock_guard<std::mutex> lk(h->mu);
+            h->stop = true;
+        }
+        h->cv.notify_all();
+        h->worker.join();
+    }
+    (void)hipDeviceSynchronize();
+    for (auto &e : h->ring_free)
+        if (e) hipEventDestroy(e);
+    for (int i = 0; i < TICKETS; ++i) {
+        if (h->ev_filled[i]) hipEventDestroy(h->ev_filled[i]);
+        if (h->ev_upd[i]) hipEventDestroy(h->ev_upd[i]);
+    }
+    for (int i = 0; i < 2; ++i)
+        if (h->ev_d2h[i]) hipEventDestroy(h->ev_d2h[i]);
+    h->t_fwd.destroy();
+    h->t_bwd.destroy();
+    h->t_plan.destroy();
+    h->t_fill.destroy();
+    if (h->s_plan) hipStreamDestroy(h->s_plan);
+    if (h->s_copy) hipStreamDestroy(h->s_copy);
+    for (void *p : h->dev_allocs) hipFree(p);
+    for (void *p : h->pinned_allocs) hipHostFree(p);
+    delete h;
+}
+
+static sp_status build(sp_ctx *h, const sp_config *c)
+{
+    const int T = c->num_tables;
+    h->T = T;
+    h->D = c->dim;
+    h->L = c->lookahead;
+    h->device = c->device;
+    h->flags = c->flags;
+    h->max_batch = c->max_batch;
+    h->max_ids = c->max_ids;
+    h->chunk = chunk_positions(h->D);
+    int64_t max_rows = 1;
+    h->tb.T = T;
+    h->tb.slot_base[0] = 0;
+    for (int t = 0; t < T; ++t) {
+        h->tb.rows[t] = c->rows[t];
+        h->slots[t] = c->slots[t];
+        h->tb.slot_base[t + 1] = h->tb.slot_base[t] + c->slots[t];
+        max_rows = std::max<int64_t>(max_rows, c->rows[t]);
+        h->maxS = std::max<int64_t>(h->maxS, c->slots[t]);
+    }
+    h->total_slots = h->tb.slot_base[T];
+    h->tb.row_bits = std::max(1, bits_for((uint64_t)(max_rows - 1)));
+    h->key_bits = bits_for((uint64_t)(T - 1)) + h->tb.row_bits;
+    if (h->key_bits > 31) return fail(nullptr, SP_ERR_INVALID_ARG, "tables x rows need %d key bits (max 31)", h->key_bits);
+
+    HIPCHK(nullptr, hipSetDevice(h->device));
+    for (int t = 0; t < T; ++t) {
+        h->host[t] = c->host_tables[t];
+        hipPointerAttribute_t attr;
+        hipError_t e = hipPointerGetAttributes(&attr, (const void *)c->host_tables[t]);
+        void *dp = nullptr;
+        if (e == hipSuccess) e = hipHostGetDevicePointer(&dp, (void *)c->host_tables[t], 0);
+        if (e != hipSuccess || !dp) {
+            (void)hipGetLastError();
+            return fail(nullptr, SP_ERR_INVALID_ARG,
+                        "host table %d is not pinned, device-mapped memory (use sp_host_alloc)", t);
+        }
+        h->host_dev[t] = (float *)dp;
+    }
+
+    const int64_t S = h->total_slots, N = h->max_ids, TB1 = (int64_t)T * h->max_batch + 1;
+    const int64_t nchunk_max = N + N / h->chunk + 1;
+    TRY(dalloc(h, &h->storage, S * h->D));
+    TRY(dalloc(h, &h->key_of_slot, S));
+    TRY(dalloc(h, &h->last_use, S));
+    TRY(dalloc(h, &h->held, S));
+    int64_t cap = 1024;
+    while (cap < 2 * S) cap <<= 1;
+    if (cap > (int64_t)1 << 32) return fail(nullptr, SP_ERR_INVALID_ARG, "too many slots");
+    h->hash_mask = (uint32_t)(cap - 1);
+    TRY(dalloc(h, &h->hash, cap));
+
+    h->nring = h->L + 3;
+    h->ring.resize(h->nring);
+    h->ring_batch.assign(h->nring, -1);
+    h->ring_nnz.assign(h->nring, 0);
+    h->ring_B.assign(h->nring, 0);
+    h->ring_free.assign(h->nring, nullptr);
+    for (int r = 0; r < h->nring; ++r) {
+        BatchDev &b = h->ring[r];
+        TRY(dalloc(h, &b.ids, N));
+        TRY(dalloc(h, &b.bag_off, TB1));
+        TRY(dalloc(h, &b.bag_of, N));
+        TRY(dalloc(h, &b.skeys, N));
+        TRY(dalloc(h, &b.perm, N));
+        TRY(dalloc(h, &b.sbag, N));
+        TRY(dalloc(h, &b.ukeys, N));
+        TRY(dalloc(h, &b.inv, N));
+        TRY(dalloc(h, &b.seg_off, N + 1));
+        TRY(dalloc(h, &b.seg_chunk0, N));
+        TRY(dalloc(h, &b.chunk_seg, nchunk_max));
+        TRY(dalloc(h, &b.scal, T + 3));
+        HIPCHK(nullptr, hipEventCreateWithFlags(&h->ring_free[r], hipEventDisableTiming));
+    }
+    for (int k = 0; k < TICKETS; ++k) {
+        TicketDev &t = h->tk[k];
+        TRY(dalloc(h, &t.hit, N));
+        TRY(dalloc(h, &t.slot_u, N));
+        TRY(dalloc(h, &t.slot_of, N));
+        TRY(dalloc(h, &t.m_key, N));
+        TRY(dalloc(h, &t.m_uidx, N));
+        TRY(dalloc(h, &t.v_slot, N));
+        TRY(dalloc(h, &t.v_old_key, N));
+        TRY(dalloc(h, &t.v_old_lu, N));
+        HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_filled[k], hipEventDisableTiming));
+        HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_upd[k], hipEventDisableTiming));
+    }
+    TRY(dalloc(h, &h->tmp_k, N));
+    TRY(dalloc(h, &h->tmp_v, N));
+    TRY(dalloc(h, &h->vk0, N));
+    TRY(dalloc(h, &h->vv0, N));
+    TRY(dalloc(h, &h->vk1, N));
+    TRY(dalloc(h, &h->hist, radix_hist_entries(N)));
+    const int64_t scan_entries = MAX_TABLES * (h->maxS / 2048 + 2) + N / 2048 + 1024;
+    TRY(dalloc(h, (uint64_t **)&h->scan_tmp, scan_entries));
+    TRY(dalloc(h, &h->sel_state, 2 * MAX_TABLES));
+    TRY(dalloc(h, &h->sel_hist, (int64_t)MAX_TABLES * SEL_BINS));
+    TRY(dalloc(h, &h->partial, nchunk_max * h->D));
+    TRY(dalloc(h, &h->cnt, 1));
+    h->stage_rows = std::min<int64_t>(N, S);
+    for (int i = 0; i < 2; ++i) {
+        TRY(dalloc(h, &h->stage_dev[i], h->stage_rows * h->D));
+        TRY(palloc(h, &h->stage_host[i], h->stage_rows * h->D));
+        TRY(palloc(h, &h->stage_keys[i], h->stage_rows));
+        HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_d2h[i], hipEventDisableTiming));
+    }
+    TRY(palloc(h, &h->h_cnt, 1));
+
+    HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_plan, hipStreamNonBlocking));
+    HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_copy, hipStreamNonBlocking));
+    HIPCHK(nullptr, h->t_fwd.init());
+    HIPCHK(nullptr, h->t_bwd.init());
+    HIPCHK(nullptr, h->t_plan.init());
+    HIPCHK(nullptr, h->t_fill.init());
+
+    // initial state: nothing cached
+    HIPCHK(nullptr, hipMemsetAsync(h->key_of_slot, 0xFF, sizeof(int32_t) * S, h->s_plan));
+    HIPCHK(nullptr, hipMemsetAsync(h->last_use, 0xFF, sizeof(int32_t) * S, h->s_plan));
+    HIPCHK(nullptr, hipMemsetAsync(h->held, 0, sizeof(int32_t) * S, h->s_plan));
+    HIPCHK(nullptr, hipMemsetAsync(h->hash, 0xFF, sizeof(uint64_t) * cap, h->s_plan));
+    HIPCHK(nullptr, hipMemsetAsync(h->storage, 0, sizeof(float) * S * h->D, h->s_plan));
+    HIPCHK(nullptr, hipMemsetAsync(h->sel_hist, 0, sizeof(int32_t) * MAX_TABLES * SEL_BINS, h->s_plan));
+    HIPCHK(nullptr, hipStreamSynchronize(h->s_plan));
+    h->st.min_capacity_margin = INT64_MAX;
+    h->worker = std::thread(worker_main, h);
+    return SP_OK;
+}
+
+extern "C" sp_status sp_create(const sp_config *c, sp_handle *out)
+{
+    if (!c || !out) return fail(nullptr, SP_ERR_INVALID_ARG, "null config or output");
+    const int T = c->num_tables;
+    if (T < 1 || T > MAX_TABLES) return fail(nullptr, SP_ERR_INVALID_ARG, "num_tables %d not in 1..%d", T, MAX_TABLES);
+    if (!c->rows || !c->slots || !c->host_tables) return fail(nullptr, SP_ERR_INVALID_ARG, "null rows/slots/host_tables");
+    const int D = c->dim;
+    if (D < 4 || D > 256 || (D & (D - 1)) != 0)
+        return fail(nullptr, SP_ERR_INVALID_ARG, "dim %d must be a power of two in 4..256", D);
+    if (c->lookahead < 0 || c->lookahead >= MAX_WINDOW)
+        return fail(nullptr, SP_ERR_INVALID_ARG, "lookahead %d not in 0..%d", c->lookahead, MAX_WINDOW - 1);
+    if (c->max_batch < 0 || c->max_ids < 0 || c->max_ids > INT32_MAX - 1)
+        return fail(nullptr, SP_ERR_INVALID_ARG, "bad max_batch / max_ids");
+    if ((int64_t)T * c->max_batch + 1 > INT32_MAX) return fail(nullptr, SP_ERR_INVALID_ARG, "too many bags");
+    int64_t total = 0;
+    for (int t = 0; t < T; ++t) {
+        if (c->rows[t] < 1 || c->rows[t] > ((int64_t)1 << 25))
+            return fail(nullptr, SP_ERR_INVALID_ARG, "rows[%d]=%lld not in 1..2^25", t, (long long)c->rows[t]);
+        if (c->slots[t] < 1 || c->slots[t] > c->rows[t])
+            return fail(nullptr, SP_ERR_INVALID_ARG, "slots[%d]=%lld not in 1..rows", t, (long long)c->slots[t]);
+        if (!c->host_tables[t]) return fail(nullptr, SP_ERR_INVALID_ARG, "host_tables[%d] is null", t);
+        total += c->slots[t];
+    }
+    if (total > INT32_MAX) return fail(nullptr, SP_ERR_INVALID_ARG, "total slots exceed 2^31-1");
+    if (c->flags & ~(SP_FLAG_DEBUG_SYNC | SP_FLAG_TIMING)) return fail(nullptr, SP_ERR_INVALID_ARG, "unknown flags");
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || c->device < 0 || c->device >= ndev) {
+        (void)hipGetLastError();
+        return fail(nullptr, SP_ERR_INVALID_ARG, "device %d not available (%d devices)", c->device, ndev);
+    }
+    sp_ctx *h = new sp_ctx();
+    sp_status s = build(h, c);
+    if (s != SP_OK) {
+        if (!h->err.empty()) g_create_error = h->err;
+        release(h);
+        return s;
+    }
+    *out = h;
+    return SP_OK;
+}
+
+extern "C" void sp_destroy(sp_handle h)
+{
+    if (!h) return;
+    (void)hipSetDevice(h->device);
+    release(h);
+}
+
+extern "C" const char *sp_last_error(sp_handle h)
+{
+    return h ? h->err.c_str() : g_create_error.c_str();
+}
+
+extern "C" sp_status sp_host_alloc(size_t bytes, void **ptr)
+{
+    if (!ptr || bytes == 0) return fail(nullptr, SP_ERR_INVALID_ARG, "bad sp_host_alloc arguments");
+    hipError_t e = hipHostMalloc(ptr, bytes, hipHostMallocMapped | hipHostMallocPortable);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        *ptr = nullptr;
+        return fail(nullptr, SP_ERR_OOM, "hipHostMalloc(%zu): %s", bytes, hipGetErrorString(e));
+    }
+    return SP_OK;
+}
+
+extern "C" void sp_host_free(void *ptr)
+{
+    if (ptr) (void)hipHostFree(ptr);
+}
+
+// ---------------------------------------------------------------- plan
+
+static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
+{
+    const int r = (int)(q % h->nring);
+    BatchDev &b = h->ring[r];
+    // the previous occupant (batch q - nring) must be done with its backward
+    HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ring_free[r], 0));
+    const int64_t nbags = (int64_t)h->T * bt.batch;
+    const hipMemcpyKind kind = bt.on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
+    if (bt.nnz > 0) HIPCHK(h, hipMemcpyAsync(b.ids, bt.ids, sizeof(int32_t) * bt.nnz, kind, h->s_plan));
+    HIPCHK(h, hipMemcpyAsync(b.bag_off, bt.bag_off, sizeof(int32_t) * (nbags + 1), kind, h->s_plan));
+    launch_ingest(h->tb, b, bt.batch, bt.nnz, h->key_bits, h->chunk, h->tmp_k, h->tmp_v, h->hist,
+                  h->scan_tmp, h->cnt, h->s_plan);
+    CHECK_LAUNCH(h);
+    h->ring_batch[r] = q;
+    h->ring_nnz[r] = bt.nnz;
+    h->ring_B[r] = bt.batch;
+    return SP_OK;
+}
+
+extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int64_t *ticket)
+{
+    TRY(usable(h));
+    if (h->updated != h->planned)
+        return fail(h, SP_ERR_SEQUENCE, "plan %lld requested before backward of ticket %lld",
+                    (long long)h->planned, (long long)h->planned - 1);
+    if (!window || n < 1 || n > h->L + 1)
+        return fail(h, SP_ERR_INVALID_ARG, "window of %d batches (1..%d allowed)", n, h->L + 1);
+    for (int w = 0; w < n; ++w) {
+        const sp_batch &b = window[w];
+        if (b.batch < 0 || b.batch > h->max_batch || b.nnz < 0 || b.nnz > h->max_ids || !b.bag_off ||
+            (b.nnz > 0 && !b.ids) || (b.batch == 0 && b.nnz != 0))
+            return fail(h, SP_ERR_INVALID_ARG, "window[%d]: batch %d / nnz %lld outside the config or null pointer",
+                        w, b.batch, (long long)b.nnz);
+    }
+    const int64_t k = h->planned;
+    const int32_t u = (int32_t)k;
+    const int e = (int)(k % TICKETS);
+    TicketDev &tk = h->tk[e];
+    TicketHost &th = h->tkh[e];
+    const bool timing = h->flags & SP_FLAG_TIMING;
+    if (timing) HIPCHK(h, h->t_plan.begin(h->s_plan));
+
+    // the ticket buffers being reused belonged to ticket k - TICKETS
+    if (k >= TICKETS) HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ev_upd[e], 0));
+    launch_zero_i32((int32_t *)h->cnt, sizeof(DevCounters) / sizeof(int32_t), h->s_plan);
+
+    // ---- phase 1: ingest new window batches, query, hold (read-only on the scratchpad)
+    const uint32_t *ukeys[MAX_WINDOW];
+    const int32_t *nuniq[MAX_WINDOW];
+    int64_t max_nnz = 0;
+    for (int w = 0; w < n; ++w) {
+        const int64_t q = k + w;
+        const int r = (int)(q % h->nring);
+        if (q >= h->ingested || h->ring_batch[r] != q) {
+            TRY(ingest(h, window[w], q));
+        } else if (h->ring_nnz[r] != window[w].nnz || h->ring_B[r] != window[w].batch) {
+            return fail(h, SP_ERR_INVALID_ARG, "batch %lld changed shape between windows", (long long)q);
+        }
+        ukeys[w] = h->ring[r].ukeys;
+        nuniq[w] = h->ring[r].scal;
+        max_nnz = std::max(max_nnz, window[w].nnz);
+    }
+    const int r0 = (int)(k % h->nring);
+    const int stamp = ++h->stamp;
+    launch_probe_hold(h->tb, h->hash, h->hash_mask, ukeys, nuniq, n, max_nnz, h->held, stamp, tk,
+                      h->cnt, h->ring[r0].scal, h->s_plan);
+    CHECK_LAUNCH(h);
+    HIPCHK(h, hipMemcpyAsync(h->h_cnt, h->cnt, sizeof(DevCounters), hipMemcpyDeviceToHost, h->s_plan));
+    HIPCHK(h, hipStreamSynchronize(h->s_plan));
+    const DevCounters c = *h->h_cnt;
+    if (c.err & (ERR_ID_RANGE | ERR_OFFSETS))
+        return fail(h, SP_ERR_INVALID_ARG, "%s in the window",
+                    (c.err & ERR_ID_RANGE) ? "row ID out of range" : "malformed bag offsets");
+    if (c.err & (ERR_HASH_FULL | ERR_PLAN))
+        return fail(h, SP_ERR_HIP, "internal planner inconsistency (flags %d) in an earlier plan", c.err);
+    int64_t n_miss = 0, margin = INT64_MAX;
+    for (int t = 0; t < h->T; ++t) {
+        const int64_t free_slots = h->slots[t] - c.held[t];
+        margin = std::min<int64_t>(margin, free_slots - c.miss[t]);
+        if (c.miss[t] > free_slots)
+            return fail(h, SP_ERR_CAPACITY,
+                        "table %d: %d misses but only %lld unheld slots (plan %lld)", t, c.miss[t],
+                        (long long)free_slots, (long long)k);
+        n_miss += c.miss[t];
+    }
+
+    // ---- phase 2: commit
+    h->ingested = std::max<int64_t>(h->ingested, k + n);
+    const BatchDev &b0 = h->ring[r0];
+    th.nnz = h->ring_nnz[r0];
+    th.B = (int32_t)h->ring_B[r0];
+    th.n_unique = c.n_unique;
+    th.n_chunks = c.n_chunks;
+    th.n_miss = n_miss;
+    th.ring = r0;
+    th.nwin = n;
+
+    if (n_miss > 0) {
+        const int64_t cap = (int64_t)h->hash_mask + 1;
+        if (h->hash_used + n_miss > cap * 7 / 10) {
+            launch_hash_rebuild(h->hash, h->hash_mask, h->key_of_slot, h->total_slots, h->cnt, h->s_plan);
+            h->hash_used = h->total_slots;
+            ++h->st.hash_rebuilds;
+        }
+        h->hash_used += n_miss;
+        launch_miss_compact(b0.ukeys, th.n_unique, tk, h->scan_tmp, h->s_plan);
+        SelArgs a{};
+        int32_t vb = 0;
+        int64_t maxS = 0;
+        for (int t = 0; t < h->T; ++t) {
+            if (c.miss[t] > 0) {
+                int y = a.nact++;
+                a.t[y] = t;
+                a.k[y] = c.miss[t];
+                a.base[y] = h->tb.slot_base[t];
+                a.S[y] = h->slots[t];
+                a.vbase[y] = vb;
+                maxS = std::max<int64_t>(maxS, h->slots[t]);
+            }
+            vb += c.miss[t];
+        }
+        const int nb = std::max(1, bits_for((uint64_t)u));
+        a.lu_bits = nb;
+        a.act_bits = bits_for((uint64_t)(a.nact - 1));
+        a.stamp = stamp;
+        const int levels = (nb + SEL_BITS - 1) / SEL_BITS;
+        launch_select_victims(a, levels, maxS, h->held, h->last_use, h->sel_state, h->sel_hist, h->vk0,
+                              h->vv0, h->vk1, (uint32_t *)nullptr, n_miss, h->hist, h->scan_tmp,
+                              tk.v_slot, h->s_plan);
+        launch_commit(h->tb, h->hash, h->hash_mask, tk, n_miss, th.n_unique, h->key_of_slot,
+                      h->last_use, h->cnt, h->s_plan);
+    }
+    launch_touch_remap(tk, b0, th.n_unique, th.nnz, h->total_slots, h->last_use, u, h->s_plan);
+    CHECK_LAUNCH(h);
+    if (timing) HIPCHK(h, h->t_plan.end(h->s_plan));
+
+    // ---- mover: write-back of evicted rows and fill of misses
+    // RAW-4: rows evicted by plan p may be refilled from plan p + n_p on
+    int64_t need = -1;
+    for (const auto &d : h->deadlines)
+        if (d.second <= k) need = std::max(need, d.first);
+    if (need >= 0) {
+        TRY(join_jobs(h, need));
+        while (!h->deadlines.empty() && h->deadlines.front().first <= need) h->deadlines.pop_front();
+    }
+    const int sl = (int)(k & 1);
+    if (k >= 2) {
+        TRY(join_jobs(h, k - 2));  // host staging of plan k-2 is free again
+        HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ev_d2h[sl], 0));
+    }
+    if (timing) HIPCHK(h, h->t_fill.begin(h->s_plan));
+    if (n_miss > 0) {
+        if (k >= 2) HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ev_upd[(k - 2) % TICKETS], 0));
+        launch_pack(h->storage, h->D, h->total_slots, tk, n_miss, u, 0, h->stage_dev[sl], h->s_plan);
+        launch_fill(h->storage, h->D, h->tb, h->host_dev, tk, n_miss, u, 0, h->s_plan);
+        if (k >= 1) HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ev_upd[(k - 1) % TICKETS], 0));
+        launch_pack(h->storage, h->D, h->total_slots, tk, n_miss, u, 1, h->stage_dev[sl], h->s_plan);
+        launch_fill(h->storage, h->D, h->tb, h->host_dev, tk, n_miss, u, 1, h->s_plan);
+        CHECK_LAUNCH(h);
+    }
+    HIPCHK(h, hipEventRecord(h->ev_filled[e], h->s_plan));
+    if (timing) HIPCHK(h, h->t_fill.end(h->s_plan));
+    Job job;
+    job.ticket = k;
+    if (n_miss > 0) {
+        HIPCHK(h, hipStreamWaitEvent(h->s_copy, h->ev_filled[e], 0));
+        HIPCHK(h, hipMemcpyAsync(h->stage_host[sl], h->stage_dev[sl], sizeof(float) * n_miss * h->D,
+                                 hipMemcpyDeviceToHost, h->s_copy));
+        HIPCHK(h, hipMemcpyAsync(h->stage_keys[sl], tk.v_old_key, sizeof(int32_t) * n_miss,
+                                 hipMemcpyDeviceToHost, h->s_copy));
+        HIPCHK(h, hipEventRecord(h->ev_d2h[sl], h->s_copy));
+        job.ev = h->ev_d2h[sl];
+        job.rows = h->stage_host[sl];
+        job.keys = h->stage_keys[sl];
+        job.n = n_miss;
+    }
+    {
+        std::lock_guard<std::mutex> lk(h->mu);
+        h->jobs.push_back(job);
+    }
+    h->cv.notify_one();
+    h->deadlines.emplace_back(k, k + n);
+
+    h->planned = k + 1;
+    h->st.plans += 1;
+    h->st.lookups += th.nnz;
+    h->st.unique += th.n_unique;
+    h->st.misses += n_miss;
+    h->st.hits += th.n_unique - n_miss;
+    h->st.bytes_fill += n_miss * h->D * (int64_t)sizeof(float);
+    h->st.min_capacity_margin = std::min(h->st.min_capacity_margin, margin);
+    if (ticket) *ticket = k;
+    if (h->flags & SP_FLAG_DEBUG_SYNC) HIPCHK(h, hipDeviceSynchronize());
+    return SP_OK;
+}
+
+// ---------------------------------------------------------------- forward / backward
+
+extern "C" sp_status sp_forward(sp_handle h, int64_t ticket, float *d_out, void *stream)
+{
+    TRY(usable(h));
+    if (ticket != h->planned - 1 || h->forwarded != ticket)
+        return fail(h, SP_ERR_SEQUENCE, "forward of ticket %lld out of order (planned %lld, forwarded %lld)",
+                    (long long)ticket, (long long)h->planned, (long long)h->forwarded);
+    const int e = (int)(ticket % TICKETS);
+    const TicketHost &th = h->tkh[e];
+    const int64_t nbags = (int64_t)h->T * th.B;
+    if (nbags > 0 && !d_out) return fail(h, SP_ERR_INVALID_ARG, "null d_out");
+    hipStream_t s = (hipStream_t)stream;
+    HIPCHK(h, hipStreamWaitEvent(s, h->ev_filled[e], 0));
+    if (ticket >= 1) HIPCHK(h, hipStreamWaitEvent(s, h->ev_upd[(ticket - 1) % TICKETS], 0));
+    const bool timing = h->flags & SP_FLAG_TIMING;
+    if (timing) HIPCHK(h, h->t_fwd.begin(s));
+    launch_forward(h->storage, h->D, h->total_slots, h->tk[e].slot_of, h->ring[th.ring].bag_off,
+                   nbags, d_out, s);
+    CHECK_LAUNCH(h);
+    if (timing) HIPCHK(h, h->t_fwd.end(s));
+    h->forwarded = ticket + 1;
+    if (h->flags & SP_FLAG_DEBUG_SYNC) HIPCHK(h, hipDeviceSynchronize());
+    return SP_OK;
+}
+
+extern "C" sp_status sp_backward_update(sp_handle h, int64_t ticket, const float *d_grad, float lr,
+                                        void *stream)
+{
+    TRY(usable(h));
+    if (ticket != h->forwarded - 1 || h->updated != ticket)
+        return fail(h, SP_ERR_SEQUENCE, "backward of ticket %lld out of order (forwarded %lld, updated %lld)",
+                    (long long)ticket, (long long)h->forwarded, (long long)h->updated);
+    const int e = (int)(ticket % TICKETS);
+    const TicketHost &th = h->tkh[e];
+    if (th.nnz > 0 && !d_grad) return fail(h, SP_ERR_INVALID_ARG, "null d_grad");
+    hipStream_t s = (hipStream_t)stream;
+    const bool timing = h->flags & SP_FLAG_TIMING;
+    if (timing) HIPCHK(h, h->t_bwd.begin(s));
+    launch_backward(h->storage, h->D, h->total_slots, h->ring[th.ring], h->tk[e].slot_u,
+                    th.n_unique, th.n_chunks, h->chunk, d_grad, (int64_t)h->T * th.B, lr,
+                    h->partial, s);
+    CHECK_LAUNCH(h);
+    if (timing) HIPCHK(h, h->t_bwd.end(s));
+    HIPCHK(h, hipEventRecord(h->ev_upd[e], s));
+    HIPCHK(h, hipEventRecord(h->ring_free[th.ring], s));
+    h->updated = ticket + 1;
+    h->st.updates += 1;
+    if (h->flags & SP_FLAG_DEBUG_SYNC) HIPCHK(h, hipDeviceSynchronize());
+    return SP_OK;
+}
+
+// ---------------------------------------------------------------- flush / stats / debug
+
+extern "C" sp_status sp_flush(sp_handle h)
+{
+    TRY(usable(h));
+    HIPCHK(h, hipDeviceSynchronize());
+    TRY(join_jobs(h, h->planned - 1));
+    h->deadlines.clear();
+    std::vector<int32_t> keys((size_t)h->total_slots);
+    HIPCHK(h, hipMemcpy(keys.data(), h->key_of_slot, sizeof(int32_t) * h->total_slots,
+                        hipMemcpyDeviceToHost));
+    const int rb = h->tb.row_bits;
+    const uint32_t mask = (1u << rb) - 1u;
+    const size_t row_bytes = sizeof(float) * (size_t)h->D;
+    for (int64_t s0 = 0; s0 < h->total_slots; s0 += h->stage_rows) {
+        const int64_t cnt = std::min(h->stage_rows, h->total_slots - s0);
+        bool any = false;
+        for (int64_t i = 0; i < cnt && !any; ++i) any = keys[s0 + i] >= 0;
+        if (!any) continue;
+        HIPCHK(h, hipMemcpy(h->stage_host[0], h->storage + s0 * h->D, row_bytes * cnt,
+                            hipMemcpyDeviceToHost));
+        for (int64_t i = 0; i < cnt; ++i) {
+            const int32_t key = keys[s0 + i];
+            if (key < 0) continue;
+            memcpy(h->host[key >> rb] + (int64_t)(key & mask) * h->D, h->stage_host[0] + i * h->D,
+                   row_bytes);
+        }
+    }
+    return SP_OK;
+}
+
+extern "C" sp_status sp_get_stats(sp_handle h, sp_stats *out)
+{
+    TRY(usable(h));
+    if (!out) return fail(h, SP_ERR_INVALID_ARG, "null stats");
+    HIPCHK(h, hipDeviceSynchronize());
+    HIPCHK(h, h->t_fwd.flush());
+    HIPCHK(h, h->t_bwd.flush());
+    HIPCHK(h, h->t_plan.flush());
+    HIPCHK(h, h->t_fill.flush());
+    sp_stats s = h->st;
+    {
+        std::lock_guard<std::mutex> lk(h->mu);
+        s.evictions = h->wb_evictions;
+        s.bytes_writeback = h->wb_bytes;
+    }
+    if (s.min_capacity_margin == INT64_MAX) s.min_capacity_margin = -1;
+    s.device_bytes = h->dev_bytes;
+    s.pinned_bytes = h->pinned_bytes;
+    s.ms_forward = h->t_fwd.ms;
+    s.ms_backward = h->t_bwd.ms;
+    s.ms_plan = h->t_plan.ms;
+    s.ms_fill = h->t_fill.ms;
+    s.timed_forward = h->t_fwd.count;
+    s.timed_backward = h->t_bwd.count;
+    s.timed_plan = h->t_plan.count;
+    s.timed_fill = h->t_fill.count;
+    *out = s;
+    return SP_OK;
+}
+
+extern "C" sp_status sp_debug_plan(sp_handle h, int64_t ticket, sp_plan_dump *d)
+{
+    TRY(usable(h));
+    if (!d) return fail(h, SP_ERR_INVALID_ARG, "null dump");
+    if (ticket != h->planned - 1 || ticket < 0)
+        return fail(h, SP_ERR_SEQUENCE, "only the latest plan (%lld) can be dumped", (long long)h->planned - 1);
+    HIPCHK(h, hipStreamSynchronize(h->s_plan));
+    const TicketHost &th = h->tkh[ticket % TICKETS];
+    const TicketDev &tk = h->tk[ticket % TICKETS];
+    const BatchDev &b = h->ring[th.ring];
+    const int rb = h->tb.row_bits;
+    const uint32_t mask = (1u << rb) - 1u;
+    const int64_t nu = th.n_unique, nm = th.n_miss, nnz = th.nnz;
+    std::vector<uint32_t> keys((size_t)std::max<int64_t>(nu, nm) + 1);
+    std::vector<int32_t> tmp((size_t)std::max<int64_t>(nu, nm) + 1);
+    d->n_unique = nu;
+    d->n_miss = nm;
+    d->nnz = nnz;
+    if (nu > 0) {
+        HIPCHK(h, hipMemcpy(keys.data(), b.ukeys, sizeof(uint32_t) * nu, hipMemcpyDeviceToHost));
+        for (int64_t i = 0; i < nu; ++i) {
+            d->u_table[i] = (int32_t)(keys[i] >> rb);
+            d->u_row[i] = (int32_t)(keys[i] & mask);
+        }
+        HIPCHK(h, hipMemcpy(tmp.data(), tk.hit, sizeof(int32_t) * nu, hipMemcpyDeviceToHost));
+        for (int64_t i = 0; i < nu; ++i) d->hit[i] = (uint8_t)(tmp[i] != 0);
+        HIPCHK(h, hipMemcpy(d->slot_u, tk.slot_u, sizeof(int32_t) * nu, hipMemcpyDeviceToHost));
+    }
+    if (nnz > 0) {
+        HIPCHK(h, hipMemcpy(d->inv, b.inv, sizeof(int32_t) * nnz, hipMemcpyDeviceToHost));
+        HIPCHK(h, hipMemcpy(d->slot_of, tk.slot_of, sizeof(int32_t) * nnz, hipMemcpyDeviceToHost));
+    }
+    int64_t nev = 0;
+    if (nm > 0) {
+        HIPCHK(h, hipMemcpy(keys.data(), tk.m_key, sizeof(uint32_t) * nm, hipMemcpyDeviceToHost));
+        for (int64_t i = 0; i < nm; ++i) {
+            d->m_table[i] = (int32_t)(keys[i] >> rb);
+            d->m_row[i] = (int32_t)(keys[i] & mask);
+        }
+        HIPCHK(h, hipMemcpy(d->v_slot, tk.v_slot, sizeof(int32_t) * nm, hipMemcpyDeviceToHost));
+        HIPCHK(h, hipMemcpy(tmp.data(), tk.v_old_key, sizeof(int32_t) * nm, hipMemcpyDeviceToHost));
+        for (int64_t i = 0; i < nm; ++i) {
+            d->v_old_row[i] = tmp[i] < 0 ? -1 : (int32_t)((uint32_t)tmp[i] & mask);
+            nev += tmp[i] >= 0;
+        }
+        HIPCHK(h, hipMemcpy(d->v_old_use, tk.v_old_lu, sizeof(int32_t) * nm, hipMemcpyDeviceToHost));
+    }
+    d->n_evict = nev;
+    return SP_OK;
+}

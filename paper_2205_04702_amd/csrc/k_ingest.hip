@@ -1,0 +1,275 @@
+// Window ingest: a batch that becomes visible to the planner is turned into
+// sorted (table,row) keys, its unique keys, the inverse map and the runs of
+// equal keys that the backward pass coalesces (gradient duplication and
+// coalescing, Sec. II-B).  Everything here runs once per batch, when the batch
+// enters the look-forward window.
+#include "sp_device.h"
+#include "sp_internal.h"
+
+namespace sp {
+
+// ---------------------------------------------------------------- small fills
+
+__global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+void launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s)
+{
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_fill_i32, dim3((unsigned)((n + BLOCK - 1) / BLOCK)), dim3(BLOCK), 0, s,
+                       p, n, v);
+}
+
+void launch_zero_i32(int32_t *p, int64_t n, hipStream_t s) { launch_fill_i32(p, n, 0, s); }
+
+// ---------------------------------------------------------------- keys and bags
+
+// key = table << row_bits | row; the table of position j is the one whose
+// span [bag_off[t*B], bag_off[(t+1)*B]) contains j.  Out-of-range rows raise
+// ERR_ID_RANGE and are clamped so that nothing downstream reads out of bounds.
+__global__ void __launch_bounds__(BLOCK) k_build_keys(Tables tb, const int32_t *ids,
+                                                      const int32_t *bag_off, int32_t B,
+                                                      int64_t nnz, uint32_t *keys,
+                                                      uint32_t *pos, int32_t *err)
+{
+    int64_t j = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    if (j >= nnz) return;
+    int lo = 0, hi = tb.T - 1;  // largest t with bag_off[t*B] <= j
+    while (lo < hi) {
+        int mid = (lo + hi + 1) >> 1;
+        if ((int64_t)bag_off[(int64_t)mid * B] <= j) lo = mid; else hi = mid - 1;
+    }
+    int32_t row = ids[j];
+    if (row < 0 || (int64_t)row >= tb.rows[lo]) {
+        atomicOr(err, ERR_ID_RANGE);
+        row = 0;
+    }
+    keys[j] = ((uint32_t)lo << tb.row_bits) | (uint32_t)row;
+    pos[j] = (uint32_t)j;
+}
+
+// bag_of[j] = bag containing position j.  Offsets are validated on the way:
+// non-decreasing, starting at 0 and ending at nnz (ERR_OFFSETS otherwise, with
+// the ranges clamped into [0, nnz)).
+__global__ void __launch_bounds__(BLOCK) k_bag_of(const int32_t *bag_off, int64_t nbags,
+                                                  int64_t nnz, int32_t *bag_of, int32_t *err)
+{
+    int64_t g = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    if (g >= nbags) return;
+    int64_t lo = bag_off[g], hi = bag_off[g + 1];
+    bool bad = lo > hi || lo < 0 || hi > nnz || (g == 0 && lo != 0) || (g == nbags - 1 && hi != nnz);
+    if (bad) {
+        atomicOr(err, ERR_OFFSETS);
+        lo = lo < 0 ? 0 : (lo > nnz ? nnz : lo);
+        hi = hi < lo ? lo : (hi > nnz ? nnz : hi);
+    }
+    for (int64_t j = lo; j < hi; ++j) bag_of[j] = (int32_t)g;
+}
+
+// ---------------------------------------------------------------- LSD radix sort
+//
+// 8-bit digits, stable.  Per pass: tile histograms (digit-major), one scan of
+// the histogram table, then a scatter in which every tile ranks its keys per
+// digit with wave ballots, round by round, so equal digits keep input order.
+
+constexpr int RS_ITEMS = 8;
+constexpr int RS_TILE = BLOCK * RS_ITEMS;
+
+int64_t radix_hist_entries(int64_t n) { return 256 * ((n + RS_TILE - 1) / RS_TILE + 1); }
+
+__global__ void __launch_bounds__(BLOCK) k_radix_hist(const uint32_t *keys, int64_t n, int shift,
+                                                      uint32_t *hist, int tiles)
+{
+    __shared__ uint32_t h[256];
+    h[threadIdx.x] = 0;
+    __syncthreads();
+    int64_t base = (int64_t)blockIdx.x * RS_TILE;
+    for (int r = 0; r < RS_ITEMS; ++r) {
+        int64_t i = base + (int64_t)r * BLOCK + threadIdx.x;
+        if (i < n) atomicAdd(&h[(keys[i] >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    hist[(int64_t)threadIdx.x * tiles + blockIdx.x] = h[threadIdx.x];
+}
+
+__global__ void __launch_bounds__(BLOCK) k_radix_scatter(const uint32_t *kin, const uint32_t *vin,
+                                                         int64_t n, int shift,
+                                                         const uint32_t *offs, int tiles,
+                                                         uint32_t *kout, uint32_t *vout)
+{
+    __shared__ uint32_t base[256];
+    __shared__ uint32_t wc[BLOCK / WAVE][256];
+    const int tid = threadIdx.x, w = wave_id();
+    const uint64_t lt = lanemask_lt();
+    base[tid] = offs[(int64_t)tid * tiles + blockIdx.x];
+    const int64_t tbase = (int64_t)blockIdx.x * RS_TILE;
+    for (int r = 0; r < RS_ITEMS; ++r) {
+        int64_t i = tbase + (int64_t)r * BLOCK + tid;
+        bool valid = i < n;
+        uint32_t k = valid ? kin[i] : 0u;
+        uint32_t v = valid ? vin[i] : 0u;
+        uint32_t d = (k >> shift) & 255u;
+        uint64_t peers = __ballot(valid);
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+            uint32_t bit = (d >> b) & 1u;
+            uint64_t bb = __ballot(bit);
+            peers &= bit ? bb : ~bb;
+        }
+#pragma unroll
+        for (int q = 0; q < BLOCK / WAVE; ++q) wc[q][tid] = 0;
+        __syncthreads();
+        if (valid && (peers & lt) == 0) wc[w][d] = (uint32_t)__popcll(peers);
+        __syncthreads();
+        {
+            uint32_t run = base[tid];
+#pragma unroll
+            for (int q = 0; q < BLOCK / WAVE; ++q) {
+                uint32_t c = wc[q][tid];
+                wc[q][tid] = run;
+                run += c;
+            }
+            base[tid] = run;
+        }
+        __syncthreads();
+        if (valid) {
+            uint32_t p = wc[w][d] + (uint32_t)__popcll(peers & lt);
+            kout[p] = k;
+            vout[p] = v;
+        }
+        __syncthreads();
+    }
+}
+
+struct ValU32 {
+    const uint32_t *p;
+    __device__ uint32_t operator()(int64_t i, int) const { return p[i]; }
+};
+struct OutU32 {
+    uint32_t *p;
+    __device__ void operator()(int64_t i, uint32_t e, uint32_t, int) const { p[i] = e; }
+};
+
+// Sorts (k0, v0) by key; k1/v1 are scratch of the same size.  *in_k1 tells
+// where the result ends up.
+void launch_radix_sort(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *v1, int64_t n,
+                       int bits, uint32_t *hist, void *scan_tmp, bool *in_k1, hipStream_t s)
+{
+    *in_k1 = false;
+    if (n <= 1 || bits <= 0) return;
+    const int passes = (bits + 7) / 8;
+    const int tiles = (int)((n + RS_TILE - 1) / RS_TILE);
+    uint32_t *ki = k0, *vi = v0, *ko = k1, *vo = v1;
+    for (int p = 0; p < passes; ++p) {
+        int shift = 8 * p;
+        hipLaunchKernelGGL(k_radix_hist, dim3(tiles), dim3(BLOCK), 0, s, ki, n, shift, hist, tiles);
+        seg_scan(SegN{(int64_t)256 * tiles}, 1, (int64_t)256 * tiles, ValU32{hist}, OutU32{hist},
+                 (uint32_t *)scan_tmp, (uint32_t *)nullptr, s);
+        hipLaunchKernelGGL(k_radix_scatter, dim3(tiles), dim3(BLOCK), 0, s, ki, vi, n, shift,
+                           hist, tiles, ko, vo);
+        uint32_t *t;
+        t = ki, ki = ko, ko = t;
+        t = vi, vi = vo, vo = t;
+    }
+    *in_k1 = (ki == k1);
+}
+
+// ---------------------------------------------------------------- unique keys
+
+struct HeadFlag {
+    const uint32_t *k;
+    __device__ uint32_t operator()(int64_t i, int) const { return i == 0 || k[i] != k[i - 1]; }
+};
+
+// Segment (run of equal keys) bookkeeping for sorted position i.
+struct UniqueOut {
+    const uint32_t *skeys, *perm;
+    const int32_t *bag_of;
+    uint32_t *ukeys;
+    int32_t *inv, *seg_off, *sbag, *scal;
+    int64_t n;
+    __device__ void operator()(int64_t i, uint32_t e, uint32_t f, int) const
+    {
+        uint32_t seg = e + f - 1;
+        uint32_t p = perm[i];
+        if (f) {
+            ukeys[seg] = skeys[i];
+            seg_off[seg] = (int32_t)i;
+        }
+        inv[p] = (int32_t)seg;
+        sbag[i] = bag_of[p];
+        if (i == n - 1) {
+            scal[0] = (int32_t)(seg + 1);
+            seg_off[seg + 1] = (int32_t)n;
+        }
+    }
+};
+
+// Backward work split: a run of len positions becomes ceil(len / chunk) chunks.
+struct ChunkCount {
+    const int32_t *seg_off;
+    int32_t chunk;
+    __device__ uint32_t operator()(int64_t s, int) const
+    {
+        int32_t len = seg_off[s + 1] - seg_off[s];
+        return (uint32_t)((len + chunk - 1) / chunk);
+    }
+};
+struct ChunkOut {
+    int32_t *seg_chunk0, *chunk_seg, *scal;
+    __device__ void operator()(int64_t s, uint32_t e, uint32_t v, int) const
+    {
+        seg_chunk0[s] = (int32_t)e;
+        for (uint32_t c = 0; c < v; ++c) chunk_seg[e + c] = (int32_t)s;
+        if (s == scal[0] - 1) scal[1] = (int32_t)(e + v);
+    }
+};
+
+// scal[2+t] = first unique index of table t (lower bound of t << row_bits).
+__global__ void k_table_starts(const uint32_t *ukeys, int32_t *scal, int T, int row_bits)
+{
+    int t = threadIdx.x;
+    if (t > T) return;
+    uint32_t key = (uint32_t)t << row_bits;
+    int32_t lo = 0, hi = scal[0];
+    while (lo < hi) {
+        int32_t mid = lo + (hi - lo) / 2;
+        if (ukeys[mid] < key) lo = mid + 1; else hi = mid;
+    }
+    scal[2 + t] = lo;
+}
+
+void launch_ingest(const Tables &tb, const BatchDev &b, int32_t B, int64_t nnz, int key_bits,
+                   int chunk, uint32_t *tmp_k, uint32_t *tmp_v, uint32_t *hist,
+                   void *scan_tmp, DevCounters *cnt, hipStream_t s)
+{
+    const int64_t nbags = (int64_t)tb.T * B;
+    launch_zero_i32(b.scal, 2 + tb.T + 1, s);
+    if (nbags > 0)
+        hipLaunchKernelGGL(k_bag_of, dim3((unsigned)((nbags + BLOCK - 1) / BLOCK)), dim3(BLOCK), 0,
+                           s, b.bag_off, nbags, nnz, b.bag_of, &cnt->err);
+    if (nnz > 0) {
+        // place the keys so that the final sort pass lands in skeys/perm
+        const int passes = nnz > 1 ? (key_bits + 7) / 8 : 0;
+        uint32_t *k0 = (passes & 1) ? tmp_k : b.skeys, *v0 = (passes & 1) ? tmp_v : b.perm;
+        uint32_t *k1 = (passes & 1) ? b.skeys : tmp_k, *v1 = (passes & 1) ? b.perm : tmp_v;
+        hipLaunchKernelGGL(k_build_keys, dim3((unsigned)((nnz + BLOCK - 1) / BLOCK)), dim3(BLOCK),
+                           0, s, tb, b.ids, b.bag_off, B, nnz, k0, v0, &cnt->err);
+        bool in_k1 = false;
+        launch_radix_sort(k0, v0, k1, v1, nnz, key_bits, hist, scan_tmp, &in_k1, s);
+        seg_scan(SegN{nnz}, 1, nnz, HeadFlag{b.skeys},
+                 UniqueOut{b.skeys, b.perm, b.bag_of, b.ukeys, b.inv, b.seg_off, b.sbag, b.scal,
+                           nnz},
+                 (uint32_t *)scan_tmp, (uint32_t *)nullptr, s);
+        seg_scan(SegDevN{b.scal}, 1, nnz, ChunkCount{b.seg_off, chunk},
+                 ChunkOut{b.seg_chunk0, b.chunk_seg, b.scal}, (uint32_t *)scan_tmp,
+                 (uint32_t *)nullptr, s);
+    }
+    hipLaunchKernelGGL(k_table_starts, dim3(1), dim3(MAX_TABLES + 1), 0, s, b.ukeys, b.scal, tb.T,
+                       tb.row_bits);
+}
+
+}  // namespace sp

@@ -1,0 +1,370 @@
+// Planner kernels: Hit-Map query, hold marking over the look-forward window,
+// LRU victim choice among unheld slots, and the Hit-Map / slot-metadata commit
+// (Sec. IV-C "Putting everything together", Sec. IV-D Algorithm 1; LRU is the
+// default replacement policy of Sec. VI-E).
+#include "sp_device.h"
+#include "sp_internal.h"
+
+namespace sp {
+
+// ---------------------------------------------------------------- query + hold
+
+struct ProbeArgs {
+    const uint32_t *uk[MAX_WINDOW];
+    const int32_t *nu[MAX_WINDOW];
+};
+
+// blockIdx.y = window batch.  Every cached key of a window batch stamps its
+// slot as held for this plan (held[slot] = stamp) and counts it once per
+// table; batch 0 (the planned one) also records hit / slot and counts misses.
+__global__ void __launch_bounds__(BLOCK) k_probe_hold(int32_t row_bits, const uint64_t *hash,
+                                                      uint32_t mask, ProbeArgs pa, int32_t *held,
+                                                      int32_t stamp, int32_t *hit,
+                                                      int32_t *slot_u, DevCounters *cnt)
+{
+    const int w = blockIdx.y;
+    const int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    if (i >= *pa.nu[w]) return;
+    const uint32_t key = pa.uk[w][i];
+    const int t = (int)(key >> row_bits);
+    const int32_t slot = hash_find(hash, mask, key);
+    if (w == 0) {
+        hit[i] = slot >= 0;
+        slot_u[i] = slot;
+        if (slot < 0) atomicAdd(&cnt->miss[t], 1);
+    }
+    if (slot >= 0) {
+        int32_t old = atomicExch(&held[slot], stamp);
+        if (old != stamp) atomicAdd(&cnt->held[t], 1);
+    }
+}
+
+__global__ void k_collect(DevCounters *cnt, const int32_t *scal0)
+{
+    if (threadIdx.x == 0) {
+        cnt->n_unique = scal0[0];
+        cnt->n_chunks = scal0[1];
+    }
+}
+
+void launch_probe_hold(const Tables &tb, const uint64_t *hash, uint32_t mask,
+                       const uint32_t *const *ukeys, const int32_t *const *nuniq, int nwin,
+                       int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk,
+                       DevCounters *cnt, const int32_t *scal0, hipStream_t s)
+{
+    ProbeArgs pa{};
+    for (int w = 0; w < nwin; ++w) pa.uk[w] = ukeys[w], pa.nu[w] = nuniq[w];
+    if (max_unique > 0)
+        hipLaunchKernelGGL(k_probe_hold, dim3((unsigned)((max_unique + BLOCK - 1) / BLOCK), nwin),
+                           dim3(BLOCK), 0, s, tb.row_bits, hash, mask, pa, held, stamp, tk.hit,
+                           tk.slot_u, cnt);
+    hipLaunchKernelGGL(k_collect, dim3(1), dim3(64), 0, s, cnt, scal0);
+}
+
+// ---------------------------------------------------------------- hash rebuild
+
+__global__ void k_hash_clear(uint64_t *hash, int64_t n)
+{
+    int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    if (i < n) hash[i] = ENTRY_EMPTY;
+}
+
+__global__ void k_hash_reinsert(uint64_t *hash, uint32_t mask, const int32_t *key_of_slot,
+                                int64_t nslots, int32_t *err)
+{
+    int64_t s = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    if (s >= nslots) return;
+    int32_t k = key_of_slot[s];
+    if (k >= 0 && !hash_insert(hash, mask, (uint32_t)k, (int32_t)s)) atomicOr(err, ERR_HASH_FULL);
+}
+
+void launch_hash_rebuild(uint64_t *hash, uint32_t mask, const int32_t *key_of_slot, int64_t nslots,
+                         DevCounters *cnt, hipStream_t s)
+{
+    int64_t cap = (int64_t)mask + 1;
+    hipLaunchKernelGGL(k_hash_clear, dim3((unsigned)((cap + BLOCK - 1) / BLOCK)), dim3(BLOCK), 0, s,
+                       hash, cap);
+    if (nslots > 0)
+        hipLaunchKernelGGL(k_hash_reinsert, dim3((unsigned)((nslots + BLOCK - 1) / BLOCK)),
+                           dim3(BLOCK), 0, s, hash, mask, key_of_slot, nslots, &cnt->err);
+}
+
+// ---------------------------------------------------------------- misses
+
+struct MissFlag {
+    const int32_t *hit;
+    __device__ uint32_t operator()(int64_t i, int) const { return hit[i] == 0; }
+};
+struct MissOut {
+    const uint32_t *ukeys;
+    uint32_t *m_key;
+    int32_t *m_uidx;
+    __device__ void operator()(int64_t i, uint32_t e, uint32_t v, int) const
+    {
+        if (v) {
+            m_key[e] = ukeys[i];
+            m_uidx[e] = (int32_t)i;
+        }
+    }
+};
+
+// Misses in ascending key order (the unique keys are sorted), so table t's
+// misses start at the sum of the miss counts of tables < t.
+void launch_miss_compact(const uint32_t *ukeys, int64_t n_unique, TicketDev tk, void *scan_tmp,
+                         hipStream_t s)
+{
+    seg_scan(SegN{n_unique}, 1, n_unique, MissFlag{tk.hit}, MissOut{ukeys, tk.m_key, tk.m_uidx},
+             (uint32_t *)scan_tmp, (uint32_t *)nullptr, s);
+}
+
+// ---------------------------------------------------------------- LRU victims
+//
+// For each table with k misses: the k smallest (last_use + 1, slot) among its
+// unheld slots (last_use = -1 for a never-used slot, so those go first).
+// A radix select on last_use + 1 (SEL_BITS per level, most significant first)
+// finds the threshold value v* and how many slots equal to v* to take (r); a
+// segmented scan then compacts, in slot order, every unheld slot below v* and
+// the first r equal to it; a stable radix sort on (table, last_use + 1) puts
+// them in LRU order with ties in slot order.  sel_state[2a] = v* prefix,
+// sel_state[2a+1] = slots still to take at the current level.
+
+constexpr int SEL_ITEMS = 16;
+constexpr int SEL_CHUNK = BLOCK * SEL_ITEMS;
+
+__global__ void k_sel_init(SelArgs a, int32_t *st, int32_t *hist)
+{
+    for (int i = threadIdx.x; i < a.nact; i += blockDim.x) {
+        st[2 * i] = 0;
+        st[2 * i + 1] = a.k[i];
+    }
+    (void)hist;
+}
+
+__global__ void __launch_bounds__(BLOCK) k_sel_hist(SelArgs a, int shift, const int32_t *held,
+                                                    const int32_t *last_use, const int32_t *st,
+                                                    int32_t *hist)
+{
+    __shared__ int32_t h[SEL_BINS];
+    for (int b = threadIdx.x; b < SEL_BINS; b += BLOCK) h[b] = 0;
+    __syncthreads();
+    const int ai = blockIdx.y;
+    const int64_t S = a.S[ai];
+    const int64_t s0 = (int64_t)blockIdx.x * SEL_CHUNK;
+    if (s0 < S) {
+        const uint64_t want = (uint64_t)(uint32_t)st[2 * ai] >> (shift + SEL_BITS);
+        const int64_t base = a.base[ai];
+        for (int r = 0; r < SEL_ITEMS; ++r) {
+            int64_t s = s0 + (int64_t)r * BLOCK + threadIdx.x;
+            if (s < S) {
+                int64_t g = base + s;
+                if (held[g] != a.stamp) {
+                    uint32_t key = (uint32_t)(last_use[g] + 1);
+                    if (((uint64_t)key >> (shift + SEL_BITS)) == want)
+                        atomicAdd(&h[(key >> shift) & (SEL_BINS - 1)], 1);
+                }
+            }
+        }
+    }
+    __syncthreads();
+    int32_t *out = hist + (int64_t)ai * SEL_BINS;
+    for (int b = threadIdx.x; b < SEL_BINS; b += BLOCK)
+        if (h[b]) atomicAdd(&out[b], h[b]);
+}
+
+// One block per active table: fix the next SEL_BITS of v*.
+__global__ void __launch_bounds__(BLOCK) k_sel_pick(int shift, int32_t *st, int32_t *hist)
+{
+    __shared__ int32_t lds[BLOCK / WAVE];
+    constexpr int PER = SEL_BINS / BLOCK;
+    const int ai = blockIdx.x;
+    int32_t *h = hist + (int64_t)ai * SEL_BINS;
+    const int32_t krem = st[2 * ai + 1];
+    int32_t c[PER], sum = 0;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+        c[q] = h[threadIdx.x * PER + q];
+        sum += c[q];
+    }
+    int32_t total;
+    int32_t excl = block_excl_scan(sum, lds, total);
+    if (excl < krem && krem <= excl + sum) {
+        int32_t cum = excl;
+#pragma unroll
+        for (int q = 0; q < PER; ++q) {
+            if (cum + c[q] >= krem) {
+                st[2 * ai] |= (threadIdx.x * PER + q) << shift;
+                st[2 * ai + 1] = krem - cum;
+                break;
+            }
+            cum += c[q];
+        }
+    }
+    __syncthreads();
+    // leave the histogram zeroed for the next level
+#pragma unroll
+    for (int q = 0; q < PER; ++q) h[threadIdx.x * PER + q] = 0;
+}
+
+struct SegAct {
+    int64_t base[MAX_TABLES], S[MAX_TABLES];
+    __device__ int64_t beg(int y) const { return base[y]; }
+    __device__ int64_t end(int y) const { return base[y] + S[y]; }
+};
+
+// (below v*) << 32 | (equal to v*) for an unheld slot, 0 for a held one.
+struct VictimFlag {
+    const int32_t *held, *last_use, *st;
+    int32_t stamp;
+    __device__ uint64_t operator()(int64_t g, int y) const
+    {
+        if (held[g] == stamp) return 0;
+        uint32_t key = (uint32_t)(last_use[g] + 1), vstar = (uint32_t)st[2 * y];
+        if (key < vstar) return 1ull << 32;
+        return key == vstar ? 1ull : 0ull;
+    }
+};
+
+struct VictimOut {
+    const int32_t *last_use, *st;
+    int32_t vbase[MAX_TABLES], k[MAX_TABLES];
+    int32_t lu_bits;
+    uint32_t *vk, *vv;
+    __device__ void operator()(int64_t g, uint64_t e, uint64_t v, int y) const
+    {
+        if (!v) return;
+        const uint32_t below = (uint32_t)(e >> 32), eq = (uint32_t)e, r = (uint32_t)st[2 * y + 1];
+        uint32_t pos;
+        if (v >> 32) pos = below + (eq < r ? eq : r);
+        else if (eq < r) pos = below + eq;
+        else return;
+        if (pos >= (uint32_t)k[y]) return;  // never write past the table's victims
+        const int64_t idx = vbase[y] + pos;
+        vk[idx] = ((uint32_t)y << lu_bits) | (uint32_t)(last_use[g] + 1);
+        vv[idx] = (uint32_t)g;
+    }
+};
+
+void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int32_t *held,
+                           const int32_t *last_use, int32_t *sel_state, int32_t *sel_hist,
+                           uint32_t *vk0, uint32_t *vv0, uint32_t *vk1, uint32_t *vv1,
+                           int64_t n_victims, uint32_t *hist, void *scan_tmp, int32_t *v_slot,
+                           hipStream_t s)
+{
+    if (a.nact <= 0 || n_victims <= 0) return;
+    hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(64), 0, s, a, sel_state, sel_hist);
+    const unsigned chunks = (unsigned)((maxS + SEL_CHUNK - 1) / SEL_CHUNK);
+    for (int l = 0; l < levels; ++l) {
+        int shift = (levels - 1 - l) * SEL_BITS;
+        hipLaunchKernelGGL(k_sel_hist, dim3(chunks, a.nact), dim3(BLOCK), 0, s, a, shift, held,
+                           last_use, (const int32_t *)sel_state, sel_hist);
+        hipLaunchKernelGGL(k_sel_pick, dim3(a.nact), dim3(BLOCK), 0, s, shift, sel_state, sel_hist);
+    }
+    // compaction lands where the sort's last pass will end in v_slot
+    const int bits = a.act_bits + a.lu_bits;
+    const int passes = n_victims > 1 ? (bits + 7) / 8 : 0;
+    uint32_t *ck = (passes & 1) ? vk0 : vk1;
+    uint32_t *cv = (passes & 1) ? vv0 : (uint32_t *)v_slot;
+    uint32_t *ok = (passes & 1) ? vk1 : vk0;
+    uint32_t *ov = (passes & 1) ? (uint32_t *)v_slot : vv0;
+    SegAct seg;
+    VictimOut out;
+    for (int y = 0; y < a.nact; ++y) {
+        seg.base[y] = a.base[y];
+        seg.S[y] = a.S[y];
+        out.vbase[y] = a.vbase[y];
+        out.k[y] = a.k[y];
+    }
+    // holes (none if the selection is consistent) read as an invalid slot
+    launch_fill_i32((int32_t *)cv, n_victims, -1, s);
+    out.last_use = last_use;
+    out.st = sel_state;
+    out.lu_bits = a.lu_bits;
+    out.vk = ck;
+    out.vv = cv;
+    seg_scan(seg, a.nact, maxS, VictimFlag{held, last_use, sel_state, a.stamp}, out,
+             (uint64_t *)scan_tmp, (uint64_t *)nullptr, s);
+    bool in_k1 = false;
+    launch_radix_sort(ck, cv, ok, ov, n_victims, bits, hist, scan_tmp, &in_k1, s);
+}
+
+// ---------------------------------------------------------------- commit
+
+// Record each victim's previous occupant and erase it from the Hit-Map.
+__global__ void __launch_bounds__(BLOCK) k_evict(uint64_t *hash, uint32_t mask, TicketDev tk,
+                                                 int64_t n, int64_t nslots,
+                                                 const int32_t *key_of_slot,
+                                                 const int32_t *last_use, int32_t *err)
+{
+    int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    if (i >= n) return;
+    const int32_t v = tk.v_slot[i];
+    if ((uint32_t)v >= (uint64_t)nslots) {
+        atomicOr(err, ERR_PLAN);
+        tk.v_old_key[i] = -1;
+        tk.v_old_lu[i] = -1;
+        return;
+    }
+    const int32_t old = key_of_slot[v];
+    tk.v_old_key[i] = old;
+    tk.v_old_lu[i] = last_use[v];
+    if (old >= 0) hash_erase(hash, mask, (uint32_t)old);
+}
+
+// Place miss i in victim slot i and enter it in the Hit-Map.
+__global__ void __launch_bounds__(BLOCK) k_insert(uint64_t *hash, uint32_t mask, TicketDev tk,
+                                                  int64_t n, int64_t nslots, int64_t n_unique,
+                                                  int32_t *key_of_slot, int32_t *err)
+{
+    int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    if (i >= n) return;
+    const int32_t v = tk.v_slot[i];
+    const int32_t ui = tk.m_uidx[i];
+    if ((uint32_t)v >= (uint64_t)nslots || (uint32_t)ui >= (uint64_t)n_unique) {
+        atomicOr(err, ERR_PLAN);
+        return;
+    }
+    const uint32_t key = tk.m_key[i];
+    key_of_slot[v] = (int32_t)key;
+    if (!hash_insert(hash, mask, key, v)) atomicOr(err, ERR_HASH_FULL);
+    tk.slot_u[ui] = v;
+}
+
+void launch_commit(const Tables &tb, uint64_t *hash, uint32_t mask, TicketDev tk, int64_t n_miss,
+                   int64_t n_unique, int32_t *key_of_slot, int32_t *last_use, DevCounters *cnt,
+                   hipStream_t s)
+{
+    if (n_miss <= 0) return;
+    const int64_t nslots = tb.slot_base[tb.T];
+    dim3 g((unsigned)((n_miss + BLOCK - 1) / BLOCK));
+    hipLaunchKernelGGL(k_evict, g, dim3(BLOCK), 0, s, hash, mask, tk, n_miss, nslots,
+                       (const int32_t *)key_of_slot, (const int32_t *)last_use, &cnt->err);
+    hipLaunchKernelGGL(k_insert, g, dim3(BLOCK), 0, s, hash, mask, tk, n_miss, nslots, n_unique,
+                       key_of_slot, &cnt->err);
+}
+
+// last_use = u for every slot the batch uses; slot_of[j] = slot of position j.
+__global__ void __launch_bounds__(BLOCK) k_touch_remap(TicketDev tk, const int32_t *inv,
+                                                       int64_t n_unique, int64_t nnz,
+                                                       int64_t nslots, int32_t *last_use, int32_t u)
+{
+    int64_t j = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    if (j < n_unique) {
+        const int32_t v = tk.slot_u[j];
+        if ((uint32_t)v < (uint64_t)nslots) last_use[v] = u;
+    }
+    if (j < nnz) {
+        const int32_t i = inv[j];
+        tk.slot_of[j] = (uint32_t)i < (uint64_t)n_unique ? tk.slot_u[i] : -1;
+    }
+}
+
+void launch_touch_remap(TicketDev tk, const BatchDev &b, int64_t n_unique, int64_t nnz,
+                        int64_t nslots, int32_t *last_use, int32_t u, hipStream_t s)
+{
+    int64_t n = nnz > n_unique ? nnz : n_unique;
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_touch_remap, dim3((unsigned)((n + BLOCK - 1) / BLOCK)), dim3(BLOCK), 0, s,
+                       tk, (const int32_t *)b.inv, n_unique, nnz, nslots, last_use, u);
+}
+
+}  // namespace sp

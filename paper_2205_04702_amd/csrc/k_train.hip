@@ -1,0 +1,271 @@
+// Data movement and training kernels over the scratchpad Storage.
+//
+// Row layout: Storage is fp32 [slots][D] in HBM; a row is D/4 float4 words
+// and LPR = D/4 lanes cover one row, so one wave64 touches 64/LPR rows per
+// pass with fully coalesced 16-byte loads.
+#include "sp_device.h"
+#include "sp_internal.h"
+
+namespace sp {
+
+struct HostRows {
+    const float4 *p[MAX_TABLES];  // device-visible pointers to the pinned host tables
+};
+
+__device__ __forceinline__ float4 f4_add(float4 a, float4 b)
+{
+    return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+}
+
+__device__ __forceinline__ float4 f4_xor(float4 a, int o)
+{
+    return make_float4(__shfl_xor(a.x, o, WAVE), __shfl_xor(a.y, o, WAVE), __shfl_xor(a.z, o, WAVE),
+                       __shfl_xor(a.w, o, WAVE));
+}
+
+// Sum the per-subgroup partial rows of a wave (lane groups of LPR lanes).
+template <int LPR>
+__device__ __forceinline__ float4 reduce_rows(float4 acc)
+{
+#pragma unroll
+    for (int o = LPR; o < WAVE; o <<= 1) acc = f4_add(acc, f4_xor(acc, o));
+    return acc;
+}
+
+// Sum of the rows src[idx[k]] for k in [beg, end), one wave, idx read 64 at a
+// time (coalesced) and broadcast by shuffles; each lane group takes every
+// RPP-th row in order and UNROLL rows are in flight per lane.
+template <int LPR, int UNROLL>
+__device__ __forceinline__ float4 gather_sum(const float4 *__restrict__ src, int64_t nrows,
+                                             const int32_t *__restrict__ idx, int64_t beg,
+                                             int64_t end)
+{
+    constexpr int RPP = WAVE / LPR;
+    const int lane = lane_id(), sub = lane / LPR, c = lane % LPR;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int64_t base = beg; base < end; base += WAVE) {
+        const int n = (int)((end - base) < WAVE ? (end - base) : WAVE);
+        const int32_t my = lane < n ? idx[base + lane] : 0;
+        for (int k0 = 0; k0 < n; k0 += RPP * UNROLL) {
+            float4 v[UNROLL];
+#pragma unroll
+            for (int q = 0; q < UNROLL; ++q) {
+                const int k = k0 + q * RPP + sub;
+                int32_t r = __shfl(my, k < n ? k : 0, WAVE);
+                r = (uint32_t)r < (uint64_t)nrows ? r : 0;  // never leave the array
+                v[q] = k < n ? src[(int64_t)r * LPR + c] : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+#pragma unroll
+            for (int q = 0; q < UNROLL; ++q) acc = f4_add(acc, v[q]);
+        }
+    }
+    return acc;
+}
+
+// ---------------------------------------------------------------- forward
+
+// out[g] = sum of Storage[slot_of[j]] over the positions j of bag g
+// (Sec. II-B, gather then element-wise reduction per table).  One wave per bag.
+template <int LPR>
+__global__ void __launch_bounds__(BLOCK) k_forward(const float4 *__restrict__ storage,
+                                                   const int32_t *__restrict__ slot_of,
+                                                   const int32_t *__restrict__ bag_off,
+                                                   int64_t nbags, int64_t nslots,
+                                                   float4 *__restrict__ out)
+{
+    const int64_t g = (int64_t)blockIdx.x * (BLOCK / WAVE) + wave_id();
+    if (g >= nbags) return;
+    float4 acc = gather_sum<LPR, 4>(storage, nslots, slot_of, bag_off[g], bag_off[g + 1]);
+    acc = reduce_rows<LPR>(acc);
+    const int lane = lane_id();
+    if (lane < LPR) out[g * LPR + lane] = acc;
+}
+
+// ---------------------------------------------------------------- backward + SGD
+
+// One wave per chunk of a run of equal keys: sum the gradients of the bags at
+// the chunk's sorted positions (ascending position order within each lane
+// group).  A run that fits one chunk updates its Storage row directly
+// (W -= lr * g); longer runs leave per-chunk partial sums for k_bwd_combine.
+template <int LPR>
+__global__ void __launch_bounds__(BLOCK) k_bwd_chunks(float4 *__restrict__ storage,
+                                                      const int32_t *__restrict__ seg_off,
+                                                      const int32_t *__restrict__ seg_chunk0,
+                                                      const int32_t *__restrict__ chunk_seg,
+                                                      const int32_t *__restrict__ sbag,
+                                                      const int32_t *__restrict__ slot_u,
+                                                      int64_t n_chunks, int chunk,
+                                                      const float4 *__restrict__ grad,
+                                                      int64_t nbags, int64_t nslots, float lr,
+                                                      float4 *__restrict__ partial)
+{
+    const int64_t ch = (int64_t)blockIdx.x * (BLOCK / WAVE) + wave_id();
+    if (ch >= n_chunks) return;
+    const int32_t s = chunk_seg[ch];
+    const int64_t s0 = seg_off[s], s1 = seg_off[s + 1];
+    const int64_t p0 = s0 + (ch - seg_chunk0[s]) * (int64_t)chunk;
+    const int64_t p1 = (p0 + chunk) < s1 ? (p0 + chunk) : s1;
+    float4 acc = gather_sum<LPR, 4>(grad, nbags, sbag, p0, p1);
+    acc = reduce_rows<LPR>(acc);
+    const int lane = lane_id();
+    if (lane >= LPR) return;
+    const int64_t nch = (s1 - s0 + chunk - 1) / chunk;
+    if (nch == 1) {
+        const int32_t slot = slot_u[s];
+        if ((uint32_t)slot >= (uint64_t)nslots) return;
+        float4 *w = storage + (int64_t)slot * LPR + lane;
+        float4 x = *w;
+        x.x = fmaf(-lr, acc.x, x.x);
+        x.y = fmaf(-lr, acc.y, x.y);
+        x.z = fmaf(-lr, acc.z, x.z);
+        x.w = fmaf(-lr, acc.w, x.w);
+        *w = x;
+    } else {
+        partial[ch * LPR + lane] = acc;
+    }
+}
+
+// Runs split over several chunks: add the chunk partials in chunk order and
+// update.  LPR threads per run.
+template <int LPR>
+__global__ void __launch_bounds__(BLOCK) k_bwd_combine(float4 *__restrict__ storage,
+                                                       const int32_t *__restrict__ seg_off,
+                                                       const int32_t *__restrict__ seg_chunk0,
+                                                       const int32_t *__restrict__ slot_u,
+                                                       int64_t n_unique, int chunk,
+                                                       const float4 *__restrict__ partial,
+                                                       int64_t nslots, float lr)
+{
+    const int64_t tid = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    const int64_t s = tid / LPR;
+    const int c = (int)(tid % LPR);
+    if (s >= n_unique) return;
+    const int64_t len = seg_off[s + 1] - seg_off[s];
+    const int64_t nch = (len + chunk - 1) / chunk;
+    if (nch <= 1) return;
+    const int64_t c0 = seg_chunk0[s];
+    float4 acc = partial[c0 * LPR + c];
+    for (int64_t q = 1; q < nch; ++q) acc = f4_add(acc, partial[(c0 + q) * LPR + c]);
+    const int32_t slot = slot_u[s];
+    if ((uint32_t)slot >= (uint64_t)nslots) return;
+    float4 *w = storage + (int64_t)slot * LPR + c;
+    float4 x = *w;
+    x.x = fmaf(-lr, acc.x, x.x);
+    x.y = fmaf(-lr, acc.y, x.y);
+    x.z = fmaf(-lr, acc.z, x.z);
+    x.w = fmaf(-lr, acc.w, x.w);
+    *w = x;
+}
+
+// ---------------------------------------------------------------- evict / fill
+
+// Copy the rows of occupied victim slots of one class into the staging rows
+// (row i of stage = victim i).  Class 1 = slots last used by the batch just
+// before this plan (their update may still be running), class 0 = the rest.
+template <int LPR>
+__global__ void __launch_bounds__(BLOCK) k_pack(const float4 *__restrict__ storage, TicketDev tk,
+                                                int64_t n, int64_t nslots, int32_t u, int cls,
+                                                float4 *__restrict__ stage)
+{
+    const int64_t t = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    const int64_t i = t / LPR;
+    const int c = (int)(t % LPR);
+    if (i >= n) return;
+    if (tk.v_old_key[i] < 0) return;
+    const int32_t lu = tk.v_old_lu[i];
+    if ((int)(lu >= 0 && lu == u - 1) != cls) return;
+    const int32_t v = tk.v_slot[i];
+    if ((uint32_t)v >= (uint64_t)nslots) return;
+    stage[i * LPR + c] = storage[(int64_t)v * LPR + c];
+}
+
+// Fill victim slot i with the missing row m_key[i] read straight from the
+// pinned host table (zero-copy over the host link).
+template <int LPR>
+__global__ void __launch_bounds__(BLOCK) k_fill(float4 *__restrict__ storage, Tables tb,
+                                                HostRows hr, TicketDev tk, int64_t n, int64_t nslots,
+                                                int32_t u, int cls)
+{
+    const int64_t t = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    const int64_t i = t / LPR;
+    const int c = (int)(t % LPR);
+    if (i >= n) return;
+    const int32_t lu = tk.v_old_lu[i];
+    if ((int)(lu >= 0 && lu == u - 1) != cls) return;
+    const uint32_t key = tk.m_key[i];
+    const int tab = (int)(key >> tb.row_bits);
+    const int64_t row = key & ((1u << tb.row_bits) - 1u);
+    const int32_t v = tk.v_slot[i];
+    if (tab >= tb.T || row >= tb.rows[tab] || (uint32_t)v >= (uint64_t)nslots) return;
+    storage[(int64_t)v * LPR + c] = hr.p[tab][row * LPR + c];
+}
+
+// ---------------------------------------------------------------- dispatch
+
+#define SP_DISPATCH_LPR(D4, KERNEL, GRID, ...)                                                   \
+    switch (D4) {                                                                                \
+    case 1: hipLaunchKernelGGL(KERNEL<1>, GRID, dim3(BLOCK), 0, s, __VA_ARGS__); break;          \
+    case 2: hipLaunchKernelGGL(KERNEL<2>, GRID, dim3(BLOCK), 0, s, __VA_ARGS__); break;          \
+    case 4: hipLaunchKernelGGL(KERNEL<4>, GRID, dim3(BLOCK), 0, s, __VA_ARGS__); break;          \
+    case 8: hipLaunchKernelGGL(KERNEL<8>, GRID, dim3(BLOCK), 0, s, __VA_ARGS__); break;          \
+    case 16: hipLaunchKernelGGL(KERNEL<16>, GRID, dim3(BLOCK), 0, s, __VA_ARGS__); break;        \
+    case 32: hipLaunchKernelGGL(KERNEL<32>, GRID, dim3(BLOCK), 0, s, __VA_ARGS__); break;        \
+    default: hipLaunchKernelGGL(KERNEL<64>, GRID, dim3(BLOCK), 0, s, __VA_ARGS__); break;        \
+    }
+
+static dim3 grid_rows(int64_t n, int D4)
+{
+    int64_t threads = n * D4;
+    return dim3((unsigned)((threads + BLOCK - 1) / BLOCK));
+}
+
+static dim3 grid_waves(int64_t n)
+{
+    return dim3((unsigned)((n + BLOCK / WAVE - 1) / (BLOCK / WAVE)));
+}
+
+void launch_pack(const float *storage, int dim, int64_t nslots, TicketDev tk, int64_t n_miss,
+                 int32_t u, int cls, float *stage, hipStream_t s)
+{
+    if (n_miss <= 0) return;
+    const int D4 = dim / 4;
+    SP_DISPATCH_LPR(D4, k_pack, grid_rows(n_miss, D4), (const float4 *)storage, tk, n_miss, nslots,
+                    u, cls, (float4 *)stage);
+}
+
+void launch_fill(float *storage, int dim, const Tables &tb, float *const *host_dev, TicketDev tk,
+                 int64_t n_miss, int32_t u, int cls, hipStream_t s)
+{
+    if (n_miss <= 0) return;
+    const int D4 = dim / 4;
+    HostRows hr{};
+    for (int t = 0; t < tb.T; ++t) hr.p[t] = (const float4 *)host_dev[t];
+    SP_DISPATCH_LPR(D4, k_fill, grid_rows(n_miss, D4), (float4 *)storage, tb, hr, tk, n_miss,
+                    tb.slot_base[tb.T], u, cls);
+}
+
+void launch_forward(const float *storage, int dim, int64_t nslots, const int32_t *slot_of,
+                    const int32_t *bag_off, int64_t nbags, float *out, hipStream_t s)
+{
+    if (nbags <= 0) return;
+    SP_DISPATCH_LPR(dim / 4, k_forward, grid_waves(nbags), (const float4 *)storage, slot_of,
+                    bag_off, nbags, nslots, (float4 *)out);
+}
+
+void launch_backward(float *storage, int dim, int64_t nslots, const BatchDev &b,
+                     const int32_t *slot_u, int64_t n_unique, int64_t n_chunks, int chunk,
+                     const float *grad, int64_t nbags, float lr, float *partial, hipStream_t s)
+{
+    if (n_chunks <= 0) return;
+    const int D4 = dim / 4;
+    SP_DISPATCH_LPR(D4, k_bwd_chunks, grid_waves(n_chunks), (float4 *)storage,
+                    (const int32_t *)b.seg_off, (const int32_t *)b.seg_chunk0,
+                    (const int32_t *)b.chunk_seg, (const int32_t *)b.sbag, slot_u, n_chunks, chunk,
+                    (const float4 *)grad, nbags, nslots, lr, (float4 *)partial);
+    if (n_chunks > n_unique)
+        SP_DISPATCH_LPR(D4, k_bwd_combine, grid_rows(n_unique, D4), (float4 *)storage,
+                        (const int32_t *)b.seg_off, (const int32_t *)b.seg_chunk0, slot_u, n_unique,
+                        chunk, (const float4 *)partial, nslots, lr);
+}
+
+}  // namespace sp

@@ -1,0 +1,115 @@
+// Host-side declarations shared by the scratchpad library's translation units.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sp {
+
+constexpr int MAX_TABLES = 64;
+constexpr int MAX_WINDOW = 16;   // batches one plan may look at (lookahead <= 15)
+constexpr int TICKETS = 4;       // ticket ring depth
+constexpr int SEL_BITS = 11;     // digit width of the LRU radix select
+constexpr int SEL_BINS = 1 << SEL_BITS;
+
+// Per-table constants passed by value to kernels.
+struct Tables {
+    int32_t T;
+    int32_t row_bits;            // key = table << row_bits | row
+    int64_t rows[MAX_TABLES];
+    int64_t slot_base[MAX_TABLES + 1];
+};
+
+// Counters written by the planning kernels and copied to the host once per plan.
+struct DevCounters {
+    int32_t err;                 // ERR_* bits
+    int32_t n_unique;            // unique keys of the planned batch
+    int32_t n_chunks;            // backward work chunks of the planned batch
+    int32_t pad;
+    int32_t miss[MAX_TABLES];
+    int32_t held[MAX_TABLES];
+};
+constexpr int32_t ERR_ID_RANGE = 1, ERR_OFFSETS = 2, ERR_HASH_FULL = 4, ERR_PLAN = 8;
+
+// One window-ring entry: a batch as it arrived plus its sort/dedup products.
+struct BatchDev {
+    int32_t *ids, *bag_off, *bag_of;  // raw CSR, bag of each position
+    uint32_t *skeys, *perm;          // keys sorted ascending, position of each sorted key
+    int32_t *sbag;                   // bag of each sorted position
+    uint32_t *ukeys;                 // unique keys ascending
+    int32_t *inv;                    // [nnz] index of each position's key in ukeys
+    int32_t *seg_off;                // [n_unique+1] start of each key's run in skeys
+    int32_t *seg_chunk0;             // [n_unique] first backward chunk of each run
+    int32_t *chunk_seg;              // [n_chunks] run of each chunk
+    int32_t *scal;                   // [0] n_unique, [1] n_chunks, [2..T+2] table starts in ukeys
+};
+
+// Per-plan device buffers.
+struct TicketDev {
+    int32_t *hit, *slot_u;           // [n_unique]
+    int32_t *slot_of;                // [nnz]
+    uint32_t *m_key;                 // [n_miss] missing keys ascending
+    int32_t *m_uidx;                 // [n_miss] their index in ukeys
+    int32_t *v_slot;                 // [n_miss] slot given to each miss
+    int32_t *v_old_key, *v_old_lu;   // [n_miss] previous occupant / last use of that slot
+};
+
+// Victim selection arguments (active tables = those with misses).
+struct SelArgs {
+    int32_t nact;
+    int32_t lu_bits;                 // bits of (last_use + 1) values
+    int32_t act_bits;                // bits of the active-table index in sort keys
+    int32_t stamp;
+    int32_t t[MAX_TABLES];
+    int32_t k[MAX_TABLES];           // misses
+    int64_t base[MAX_TABLES];        // first global slot of the table
+    int64_t S[MAX_TABLES];           // slots of the table
+    int32_t vbase[MAX_TABLES];       // first victim index of the table
+};
+
+constexpr int CHUNK_WAVES_ROWS = 8;  // backward chunk = 8 passes of a wave over rows
+
+inline int chunk_positions(int dim) { return CHUNK_WAVES_ROWS * (64 / (dim / 4)); }
+
+// ---------------------------------------------------------------- launchers
+// k_ingest.hip
+void launch_zero_i32(int32_t *p, int64_t n, hipStream_t s);
+void launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
+void launch_ingest(const Tables &tb, const BatchDev &b, int32_t B, int64_t nnz, int key_bits,
+                   int chunk, uint32_t *tmp_k, uint32_t *tmp_v, uint32_t *hist,
+                   void *scan_tmp, DevCounters *cnt, hipStream_t s);
+void launch_radix_sort(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *v1, int64_t n,
+                       int bits, uint32_t *hist, void *scan_tmp, bool *in_k1, hipStream_t s);
+int64_t radix_hist_entries(int64_t n);
+
+// k_plan.hip
+void launch_probe_hold(const Tables &tb, const uint64_t *hash, uint32_t mask,
+                       const uint32_t *const *ukeys, const int32_t *const *nuniq, int nwin,
+                       int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk,
+                       DevCounters *cnt, const int32_t *scal0, hipStream_t s);
+void launch_hash_rebuild(uint64_t *hash, uint32_t mask, const int32_t *key_of_slot, int64_t nslots,
+                         DevCounters *cnt, hipStream_t s);
+void launch_miss_compact(const uint32_t *ukeys, int64_t n_unique, TicketDev tk, void *scan_tmp,
+                         hipStream_t s);
+void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int32_t *held,
+                           const int32_t *last_use, int32_t *sel_state, int32_t *sel_hist,
+                           uint32_t *vk0, uint32_t *vv0, uint32_t *vk1, uint32_t *vv1,
+                           int64_t n_victims, uint32_t *hist, void *scan_tmp, int32_t *v_slot,
+                           hipStream_t s);
+void launch_commit(const Tables &tb, uint64_t *hash, uint32_t mask, TicketDev tk, int64_t n_miss,
+                   int64_t n_unique, int32_t *key_of_slot, int32_t *last_use, DevCounters *cnt,
+                   hipStream_t s);
+void launch_touch_remap(TicketDev tk, const BatchDev &b, int64_t n_unique, int64_t nnz,
+                        int64_t nslots, int32_t *last_use, int32_t u, hipStream_t s);
+
+// k_train.hip
+void launch_pack(const float *storage, int dim, int64_t nslots, TicketDev tk, int64_t n_miss,
+                 int32_t u, int cls, float *stage, hipStream_t s);
+void launch_fill(float *storage, int dim, const Tables &tb, float *const *host_dev, TicketDev tk,
+                 int64_t n_miss, int32_t u, int cls, hipStream_t s);
+void launch_forward(const float *storage, int dim, int64_t nslots, const int32_t *slot_of,
+                    const int32_t *bag_off, int64_t nbags, float *out, hipStream_t s);
+void launch_backward(float *storage, int dim, int64_t nslots, const BatchDev &b,
+                     const int32_t *slot_u, int64_t n_unique, int64_t n_chunks, int chunk,
+                     const float *grad, int64_t nbags, float lr, float *partial, hipStream_t s);
+
+}  // namespace sp

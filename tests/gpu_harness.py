@@ -1,0 +1,110 @@
+"""Drive the HIP scratchpad and the CPU oracle side by side on the same inputs."""
+from __future__ import annotations
+
+import numpy as np
+
+from oracle import oracle
+from paper_2205_04702_amd import workload as wl
+from paper_2205_04702_amd.scratchpipe import HostTables, ScratchPipe
+
+PLAN_FIELDS = ("u_table", "u_row", "inv", "hit", "m_table", "m_row", "v_slot", "v_old_row",
+               "v_old_use", "slot_u", "slot_of")
+REL_TOL = 1e-5  # per-row max |gpu - ref| / max |ref|
+
+
+def row_rel_err(got: np.ndarray, ref: np.ndarray) -> np.ndarray:
+    """Per row: infinity-norm of the difference over infinity-norm of the reference."""
+    got = got.reshape(ref.shape[0], -1).astype(np.float64)
+    ref = ref.reshape(ref.shape[0], -1).astype(np.float64)
+    den = np.abs(ref).max(axis=1)
+    num = np.abs(got - ref).max(axis=1)
+    return np.where(den > 0, num / np.where(den > 0, den, 1), num)
+
+
+def compare_plan(step, dump, ref, T, B):
+    for f in PLAN_FIELDS:
+        a = np.asarray(dump[f])
+        b = np.asarray(getattr(ref, f))
+        if f == "hit":
+            a, b = a.astype(np.uint8), b.astype(np.uint8)
+        assert a.shape == b.shape, f"step {step}: {f} shape {a.shape} vs {b.shape}"
+        if not np.array_equal(a, b):
+            bad = np.nonzero(a != b)[0][:5]
+            raise AssertionError(f"step {step}: plan field {f} differs at {bad.tolist()}: "
+                                 f"gpu {a[bad].tolist()} oracle {b[bad].tolist()}")
+    assert dump["n_evict"] == ref.n_evict, f"step {step}: evictions {dump['n_evict']} vs {ref.n_evict}"
+
+
+def make_inputs(w, steps=None, ragged=None):
+    n = w.steps if steps is None else steps
+    if ragged:
+        batches = [wl.ragged_batch(w, s, ragged) for s in range(n)]
+    else:
+        batches = [wl.batch(w, s) for s in range(n)]
+    return batches
+
+
+def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all", flags=0,
+               device_ids=False, ref_tables=None, sync_each_step=True, compare_tables=True,
+               return_tables=False, steps=None):
+    """Train w on the GPU and with the oracle; assert parity; return a summary."""
+    import torch
+    dev = torch.device("cuda:0")
+    if batches is None:
+        batches = make_inputs(w, steps)
+    n = len(batches)
+    T, B, D, L = w.tables, w.batch, w.dim, w.lookahead
+    max_ids = max(int(b[0].size) for b in batches)
+    host = HostTables(w.rows, D)
+    for t in range(T):
+        wl.init_table(w, t, out=host[t])
+    ref = ref_tables if ref_tables is not None else [wl.init_table(w, t) for t in range(T)]
+    planner = oracle.Planner(w.rows, w.slots)
+    touched = [np.zeros(r, bool) for r in w.rows]
+    dev_batches = None
+    if device_ids:
+        dev_batches = [(torch.from_numpy(i).to(dev), torch.from_numpy(o).to(dev)) for i, o in batches]
+    plan_set = set(range(n)) if check_plan_steps == "all" else set(check_plan_steps)
+    fwd_set = set(range(n)) if check_fwd_steps == "all" else set(check_fwd_steps)
+    worst_fwd = 0.0
+    sp = ScratchPipe(w.rows, D, w.slots, L, host, max_batch=B, max_ids=max(max_ids, 1), flags=flags)
+    try:
+        out = torch.zeros((T * B, D), dtype=torch.float32, device=dev)
+        for u in range(n):
+            win_idx = list(range(u, min(u + L, n - 1) + 1))
+            src = dev_batches if device_ids else batches
+            ticket = sp.plan([src[q] for q in win_idx])
+            assert ticket == u
+            p = planner.plan([batches[q] for q in win_idx], B)
+            if u in plan_set:
+                compare_plan(u, sp.debug_plan(ticket, max(int(batches[u][0].size), 1)), p, T, B)
+            sp.forward(ticket, out)
+            g = wl.grads(w, u)
+            gd = torch.from_numpy(g).to(dev)
+            sp.backward_update(ticket, gd, w.lr)
+            ids, off = batches[u]
+            o_ref = oracle.train_step(ref, ids, off, B, g, w.lr, want_out=u in fwd_set)
+            for t in range(T):
+                touched[t][ids[off[t * B]:off[(t + 1) * B]]] = True
+            if u in fwd_set:
+                torch.cuda.synchronize()
+                e = row_rel_err(out.cpu().numpy(), o_ref)
+                worst_fwd = max(worst_fwd, float(e.max(initial=0.0)))
+                assert e.max(initial=0.0) <= REL_TOL, f"step {u}: forward rel err {e.max()}"
+            elif sync_each_step:
+                torch.cuda.synchronize()
+        sp.flush()
+        stats = sp.stats()
+    finally:
+        sp.close()
+    worst_tab = 0.0
+    if compare_tables:
+        for t in range(T):
+            got, exp = host[t], ref[t]
+            assert np.array_equal(got[~touched[t]], exp[~touched[t]]), f"table {t}: untouched rows changed"
+            e = row_rel_err(got[touched[t]], exp[touched[t]])
+            worst_tab = max(worst_tab, float(e.max(initial=0.0)))
+            assert e.max(initial=0.0) <= REL_TOL, f"table {t}: row rel err {e.max()}"
+    tables = [host[t].copy() for t in range(T)] if return_tables else None
+    host.close()
+    return {"stats": stats, "worst_fwd": worst_fwd, "worst_table": worst_tab, "tables": tables}

@@ -1,0 +1,218 @@
+"""Embedding-training throughput of the HIP scratchpad on one MI355X.
+
+One step = sp_plan (window ingest, dedup, Hit-Map query, hold, LRU victims,
+commit, miss fill and evicted-row write-back) + sp_forward (pooled gather) +
+sp_backward_update (gradient coalescing and in-place SGD) for one mini-batch
+of the synthetic workload.  Batch IDs and upstream gradients are generated
+before timing and are resident in HBM when the timed region starts; the
+embedding tables live in pinned host memory and only the scratchpad is in HBM.
+
+Prints one JSON line (rank 0).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_bytes(w, n_unique: float, n_chunks: float) -> dict:
+    """Algorithmic HBM bytes per launch of the forward and backward kernels.
+
+    forward  (unique-bound): each unique row read once, slot_of, bag offsets,
+             pooled output written.
+    backward: each unique row read and written once, each bag gradient read
+             once, sorted bag index per position, per-run offsets / first
+             chunk / slot, chunk->run map.
+    """
+    T, B, D = w.tables, w.batch, w.dim
+    nnz = w.nnz
+    row = 4 * D
+    fwd = n_unique * row + nnz * 4 + (T * B + 1) * 4 + T * B * row
+    fwd_req = nnz * row + nnz * 4 + (T * B + 1) * 4 + T * B * row
+    bwd = 2 * n_unique * row + T * B * row + nnz * 4 + n_unique * 12 + n_chunks * 4
+    return {"forward": fwd, "forward_requested": fwd_req, "backward": bwd}
+
+
+def traffic_from_profile(kernel: str, src_hash: str, workload: str):
+    """HBM bytes per launch measured by rocprofv3 counters, if a summary for the
+    current kernel source exists under profiles/."""
+    p = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        d = json.load(open(p))
+        e = d.get(workload, {}).get(kernel)
+        if e and e.get("source_sha256") == src_hash:
+            return float(e["bytes_per_launch"])
+    except Exception:
+        return None
+    return None
+
+
+def cpu_baseline(w, seconds: float = 15.0, max_steps: int | None = None) -> dict:
+    """The uncached CPU oracle trainer on the same inputs, bounded in time."""
+    from oracle import oracle
+    from paper_2205_04702_amd import workload as wl
+    tables = [wl.init_table(w, t) for t in range(w.tables)]
+    cores = min(oracle.max_threads(), w.tables)
+    # one step to size the sample
+    ids, off = wl.batch(w, 0)
+    g = wl.grads(w, 0)
+    t0 = time.perf_counter()
+    oracle.train_step(tables, ids, off, w.batch, g, w.lr, want_out=True)
+    one = time.perf_counter() - t0
+    n = max(1, min(int(seconds / max(one, 1e-6)), max_steps or w.steps))
+    inputs = [(wl.batch(w, s), wl.grads(w, s)) for s in range(1, n + 1)]
+    t0 = time.perf_counter()
+    for (ids, off), g in inputs:
+        oracle.train_step(tables, ids, off, w.batch, g, w.lr, want_out=True)
+    dt = time.perf_counter() - t0
+    return {"value": round(w.batch * n / dt, 1), "unit": "samples/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"steps 1..{n} of {w.name} (forward + coalesced SGD, fp64 accumulation, "
+                      f"OpenMP over tables), input generation excluded"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="zipf-8x1M")
+    ap.add_argument("--host-ids", action="store_true",
+                    help="hand the batch IDs over from host memory (PCIe-inclusive variant)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-timing", action="store_true", help="do not time kernels with events")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: the scratchpad path has no multi-GPU mode "
+              "(tables would shard across GPUs, one context per GPU)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2205_04702_amd import workload as wl
+    from paper_2205_04702_amd import scratchpipe as sp
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    w = wl.get_workload(args.workload)
+    W, K, L = args.warmup, args.steps, w.lookahead
+    nb = W + K + L + 1  # the window of the last step plus the batch prepared after it
+    log(f"[bench] workload {w.name}: generating {nb} batches and {W + K} gradient tensors")
+    t0 = time.perf_counter()
+    host_batches = [wl.batch(w, s) for s in range(nb)]
+    if args.host_ids:
+        batches = host_batches
+    else:
+        batches = [(torch.from_numpy(i).to(dev), torch.from_numpy(o).to(dev)) for i, o in host_batches]
+    grads = [torch.from_numpy(wl.grads(w, s)).to(dev) for s in range(W + K)]
+    host = sp.HostTables(w.rows, w.dim)
+    for t in range(w.tables):
+        wl.init_table(w, t, out=host[t])
+    log(f"[bench] inputs ready in {time.perf_counter() - t0:.1f}s")
+
+    flags = 0 if args.no_timing else sp.SP_FLAG_TIMING
+    ctx = sp.ScratchPipe(w.rows, w.dim, w.slots, L, host, max_batch=w.batch, max_ids=w.nnz,
+                         flags=flags)
+    out = torch.empty((w.tables * w.batch, w.dim), dtype=torch.float32, device=dev)
+
+    def step(u):
+        # hold window u..u+L, plus batch u+L+1 handed over early for sorting
+        tk = ctx.plan([batches[q] for q in range(u, min(u + L + 1, nb - 1) + 1)])
+        ctx.forward(tk, out)
+        ctx.backward_update(tk, grads[u], w.lr)
+
+    for u in range(W):
+        step(u)
+    torch.cuda.synchronize()
+    s0 = ctx.stats()
+    log(f"[bench] warmup {W} steps done")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for u in range(W, W + K):
+        step(u)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    s1 = ctx.stats()
+    ctx.close()
+    host.close()
+    log(f"[bench] timed {K} steps in {dt:.3f}s")
+
+    d = {k: s1[k] - s0[k] for k in s1 if isinstance(s1[k], (int, float))}
+    n_unique = d["unique"] / max(d["plans"], 1)
+    samples_per_s = w.batch * K / dt
+    res = {
+        "metric": "embedding-train samples/sec at 1 MI355X; achieved HBM GB/s vs peak",
+        "value": round(samples_per_s, 1),
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(dt * 1e3 / K, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {**w.describe(), "ids": "host" if args.host_ids else "hbm"},
+    }
+    detail = {"miss_rate": round(d["misses"] / max(d["unique"], 1), 4),
+              "unique_per_step": round(n_unique, 1),
+              "evictions_per_step": round(d["evictions"] / K, 1),
+              "fill_GBps": round(d["bytes_fill"] / dt / 1e9, 3),
+              "writeback_GBps": round(d["bytes_writeback"] / dt / 1e9, 3)}
+    if not args.no_timing and d["timed_forward"] > 0:
+        # kernel execution times from start/stop events of the launches themselves
+        fwd_ms = d["ms_forward"] / d["timed_forward"]
+        bwd_ms = d["ms_backward"] / max(d["timed_backward"], 1)
+        cmb_ms = d["ms_combine"] / max(d["timed_combine"], 1)
+        n_chunks = d["chunks"] / max(d["updates"], 1)
+        kb = kernel_bytes(w, n_unique, n_chunks)
+        fwd_gbs = kb["forward"] / (fwd_ms * 1e-3) / 1e9
+        bwd_gbs = kb["backward"] / (bwd_ms * 1e-3) / 1e9
+        detail.update({"forward_ms": round(fwd_ms, 5), "backward_chunks_ms": round(bwd_ms, 5),
+                       "backward_combine_ms": round(cmb_ms, 5),
+                       "combine_launches": d["timed_combine"],
+                       "plan_ms": round(d["ms_plan"] / max(d["timed_plan"], 1), 5),
+                       "fill_ms": round(d["ms_fill"] / max(d["timed_fill"], 1), 5),
+                       "chunks_per_step": round(n_chunks, 1),
+                       "forward_GBps_unique": round(fwd_gbs, 1),
+                       "forward_GBps_requested": round(kb["forward_requested"] / (fwd_ms * 1e-3) / 1e9, 1),
+                       "backward_GBps": round(bwd_gbs, 1)})
+        src = open(os.path.join(ROOT, "paper_2205_04702_amd", "csrc", "k_train.hip"), "rb").read()
+        src_hash = hashlib.sha256(src).hexdigest()
+        dom = "forward" if fwd_ms >= bwd_ms else "backward"
+        ach = fwd_gbs if dom == "forward" else bwd_gbs
+        name = "k_forward" if dom == "forward" else "k_bwd_chunks"
+        tr = traffic_from_profile(name, src_hash, w.name)
+        res["roofline"] = {"bound": "hbm", "kernel": name,
+                           "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                           "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": tr,
+                           "bytes_per_launch": int(kb[dom]),
+                           "ms_per_launch": round(fwd_ms if dom == "forward" else bwd_ms, 5)}
+    res["detail"] = detail
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle")
+        res["cpu_baseline"] = cpu_baseline(w, seconds=args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

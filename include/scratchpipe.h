@@ -84,12 +84,15 @@ typedef struct {
     int64_t bytes_fill;         /* host -> HBM bytes of miss fills                      */
     int64_t bytes_writeback;    /* HBM -> host bytes of evicted rows                    */
     int64_t hash_rebuilds;
+    int64_t chunks;             /* backward work chunks processed                       */
     int64_t min_capacity_margin;/* min over plans and tables of unheld slots - misses  */
     int64_t device_bytes;       /* device memory held by the context                    */
     int64_t pinned_bytes;       /* pinned staging held by the context                   */
-    /* SP_FLAG_TIMING only: summed kernel time in ms and number of timed calls */
-    double ms_forward, ms_backward, ms_plan, ms_fill;
-    int64_t timed_forward, timed_backward, timed_plan, timed_fill;
+    /* SP_FLAG_TIMING only: summed time in ms and number of timed calls.  forward,
+     * backward (per-chunk kernel) and combine (multi-chunk runs) are kernel
+     * execution times; plan and fill span their whole launch sequences. */
+    double ms_forward, ms_backward, ms_combine, ms_plan, ms_fill;
+    int64_t timed_forward, timed_backward, timed_combine, timed_plan, timed_fill;
 } sp_stats;
 
 /* Per-plan decisions copied to the host for checking.  The caller allocates
@@ -124,11 +127,15 @@ sp_status sp_create(const sp_config *config, sp_handle *out);
 
 /*
  * Plan the next mini-batch.  window[0] is the batch to plan (ticket k = number
- * of plans so far) and window[1..n-1] are the batches that follow it, n-1 <=
- * lookahead; the same batch must be passed with the same content every time
- * it appears.  Batches enter the device window ring once (sorted and
- * deduplicated on arrival); window buffers may be reused when the call
- * returns.  The plan queries the Hit-Map for window[0]'s unique keys, holds
+ * of plans so far) and window[1..] are the batches that follow it.  The first
+ * min(n, lookahead+1) batches form the hold window; if n = lookahead+2 the
+ * last one is only sorted and deduplicated ahead of time (not held), which
+ * takes that work off the next plan's path.  Batches enter the device window
+ * ring once, when first seen, and are not read again: the same batch must be
+ * passed with the same content every time it appears (after a failed plan
+ * all of that call's batches are read again on the next call).  Window
+ * buffers may be reused when the call returns.  The plan queries the Hit-Map
+ * for window[0]'s unique keys, holds
  * every cached slot used by any window batch, takes for each table's misses
  * the least-recently-used unheld slots (oldest first, ties by slot; the
  * ascending misses take them in that order), updates Hit-Map, slot keys and

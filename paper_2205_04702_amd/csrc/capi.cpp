@@ -85,6 +85,16 @@ struct Timer {
         next = (next + 1) % N;
         return r;
     }
+    // Event pair for a launch that records its own start/stop (kernel time only).
+    hipError_t take(hipEvent_t *b0, hipEvent_t *e0)
+    {
+        hipError_t r = harvest(next);
+        *b0 = b[next];
+        *e0 = e[next];
+        used[next] = true;
+        next = (next + 1) % N;
+        return r;
+    }
     hipError_t flush()
     {
         for (int i = 0; i < N; ++i) {
@@ -139,35 +149,40 @@ struct sp_ctx {
     uint32_t hash_mask = 0;
     int64_t hash_used = 0;
 
-    // window ring
+    // window ring: batch q lives in entry q % nring (ring_batch[r] = q, -1 if none)
     int nring = 0;
     std::vector<BatchDev> ring;
     std::vector<int64_t> ring_batch, ring_nnz, ring_B;
-    std::vector<hipEvent_t> ring_free;
-    int64_t ingested = 0;
+    std::vector<hipEvent_t> ring_free;      // backward of the entry's batch issued
+    std::vector<hipEvent_t> ring_ready;     // ingest of the entry's batch finished
 
     // tickets
     TicketDev tk[TICKETS]{};
     TicketHost tkh[TICKETS]{};
-    hipEvent_t ev_filled[TICKETS]{}, ev_upd[TICKETS]{};
+    hipEvent_t ev_planned[TICKETS]{}, ev_filled[TICKETS]{}, ev_upd[TICKETS]{};
     int64_t planned = 0, forwarded = 0, updated = 0;
     int32_t stamp = 0;
 
-    // scratch
+    // scratch of the plan stream and of the ingest stream
     uint32_t *tmp_k = nullptr, *tmp_v = nullptr, *hist = nullptr;
     void *scan_tmp = nullptr;
+    uint32_t *itmp_k = nullptr, *itmp_v = nullptr, *ihist = nullptr;
+    void *iscan_tmp = nullptr;
     int32_t *sel_state = nullptr, *sel_hist = nullptr;
     uint32_t *vk0 = nullptr, *vv0 = nullptr, *vk1 = nullptr;
     float *partial = nullptr;
-    DevCounters *cnt = nullptr, *h_cnt = nullptr;
+    DevCounters *cnt = nullptr;
+    DevCounters *h_cnt = nullptr, *h_cnt_dev = nullptr;  // host-coherent copy and its device address
 
     // write-back staging (two in flight)
     int64_t stage_rows = 0;
-    float *stage_dev[2]{}, *stage_host[2]{};
-    int32_t *stage_keys[2]{};
+    float *stage_dev[2]{}, *stage_host[2]{};  // n rows, then their n previous keys
     hipEvent_t ev_d2h[2]{};
 
-    hipStream_t s_plan = nullptr, s_copy = nullptr;
+    // plan stream: query, hold, victims, commit; ingest stream: sorting and
+    // deduplicating batches as they become visible; move stream: write-back
+    // packing and miss fills; copy stream: device-to-host of evicted rows
+    hipStream_t s_plan = nullptr, s_ingest = nullptr, s_move = nullptr, s_copy = nullptr;
 
     // write-back thread
     std::thread worker;
@@ -182,7 +197,7 @@ struct sp_ctx {
 
     // bookkeeping
     sp_stats st{};
-    Timer t_fwd, t_bwd, t_plan, t_fill;
+    Timer t_fwd, t_bwd, t_cmb, t_plan, t_fill;
     int64_t dev_bytes = 0, pinned_bytes = 0;
     std::vector<void *> dev_allocs, pinned_allocs;
     std::string err;
@@ -331,7 +346,10 @@ static void release(sp_ctx *h)
     (void)hipDeviceSynchronize();
     for (auto &e : h->ring_free)
         if (e) hipEventDestroy(e);
+    for (auto &e : h->ring_ready)
+        if (e) hipEventDestroy(e);
     for (int i = 0; i < TICKETS; ++i) {
+        if (h->ev_planned[i]) hipEventDestroy(h->ev_planned[i]);
         if (h->ev_filled[i]) hipEventDestroy(h->ev_filled[i]);
         if (h->ev_upd[i]) hipEventDestroy(h->ev_upd[i]);
     }
@@ -339,9 +357,12 @@ static void release(sp_ctx *h)
         if (h->ev_d2h[i]) hipEventDestroy(h->ev_d2h[i]);
     h->t_fwd.destroy();
     h->t_bwd.destroy();
+    h->t_cmb.destroy();
     h->t_plan.destroy();
     h->t_fill.destroy();
     if (h->s_plan) hipStreamDestroy(h->s_plan);
+    if (h->s_ingest) hipStreamDestroy(h->s_ingest);
+    if (h->s_move) hipStreamDestroy(h->s_move);
     if (h->s_copy) hipStreamDestroy(h->s_copy);
     for (void *p : h->dev_allocs) hipFree(p);
     for (void *p : h->pinned_allocs) hipHostFree(p);
@@ -401,12 +422,14 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     h->hash_mask = (uint32_t)(cap - 1);
     TRY(dalloc(h, &h->hash, cap));
 
-    h->nring = h->L + 3;
+    // batches k-1 (training) .. k+L+1 (prepared ahead) plus one of slack
+    h->nring = h->L + 4;
     h->ring.resize(h->nring);
     h->ring_batch.assign(h->nring, -1);
     h->ring_nnz.assign(h->nring, 0);
     h->ring_B.assign(h->nring, 0);
     h->ring_free.assign(h->nring, nullptr);
+    h->ring_ready.assign(h->nring, nullptr);
     for (int r = 0; r < h->nring; ++r) {
         BatchDev &b = h->ring[r];
         TRY(dalloc(h, &b.ids, N));
@@ -422,6 +445,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
         TRY(dalloc(h, &b.chunk_seg, nchunk_max));
         TRY(dalloc(h, &b.scal, T + 3));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ring_free[r], hipEventDisableTiming));
+        HIPCHK(nullptr, hipEventCreateWithFlags(&h->ring_ready[r], hipEventDisableTiming));
     }
     for (int k = 0; k < TICKETS; ++k) {
         TicketDev &t = h->tk[k];
@@ -433,34 +457,53 @@ static sp_status build(sp_ctx *h, const sp_config *c)
         TRY(dalloc(h, &t.v_slot, N));
         TRY(dalloc(h, &t.v_old_key, N));
         TRY(dalloc(h, &t.v_old_lu, N));
+        HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_planned[k], hipEventDisableTiming));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_filled[k], hipEventDisableTiming));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_upd[k], hipEventDisableTiming));
     }
     TRY(dalloc(h, &h->tmp_k, N));
     TRY(dalloc(h, &h->tmp_v, N));
+    TRY(dalloc(h, &h->itmp_k, N));
+    TRY(dalloc(h, &h->itmp_v, N));
     TRY(dalloc(h, &h->vk0, N));
     TRY(dalloc(h, &h->vv0, N));
     TRY(dalloc(h, &h->vk1, N));
     TRY(dalloc(h, &h->hist, radix_hist_entries(N)));
+    TRY(dalloc(h, &h->ihist, radix_hist_entries(N)));
     const int64_t scan_entries = MAX_TABLES * (h->maxS / 2048 + 2) + N / 2048 + 1024;
     TRY(dalloc(h, (uint64_t **)&h->scan_tmp, scan_entries));
+    TRY(dalloc(h, (uint64_t **)&h->iscan_tmp, scan_entries));
     TRY(dalloc(h, &h->sel_state, 2 * MAX_TABLES));
     TRY(dalloc(h, &h->sel_hist, (int64_t)MAX_TABLES * SEL_BINS));
     TRY(dalloc(h, &h->partial, nchunk_max * h->D));
     TRY(dalloc(h, &h->cnt, 1));
     h->stage_rows = std::min<int64_t>(N, S);
     for (int i = 0; i < 2; ++i) {
-        TRY(dalloc(h, &h->stage_dev[i], h->stage_rows * h->D));
-        TRY(palloc(h, &h->stage_host[i], h->stage_rows * h->D));
-        TRY(palloc(h, &h->stage_keys[i], h->stage_rows));
+        TRY(dalloc(h, &h->stage_dev[i], h->stage_rows * (h->D + 1)));
+        TRY(palloc(h, &h->stage_host[i], h->stage_rows * (h->D + 1)));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_d2h[i], hipEventDisableTiming));
     }
-    TRY(palloc(h, &h->h_cnt, 1));
+    {
+        void *p = nullptr;
+        hipError_t e = hipHostMalloc(&p, sizeof(DevCounters),
+                                     hipHostMallocMapped | hipHostMallocCoherent);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(h, SP_ERR_OOM, "hipHostMalloc(counters): %s", hipGetErrorString(e));
+        }
+        h->pinned_allocs.push_back(p);
+        h->h_cnt = (DevCounters *)p;
+        memset(p, 0, sizeof(DevCounters));
+        HIPCHK(nullptr, hipHostGetDevicePointer((void **)&h->h_cnt_dev, p, 0));
+    }
 
     HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_plan, hipStreamNonBlocking));
+    HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_ingest, hipStreamNonBlocking));
+    HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_move, hipStreamNonBlocking));
     HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_copy, hipStreamNonBlocking));
     HIPCHK(nullptr, h->t_fwd.init());
     HIPCHK(nullptr, h->t_bwd.init());
+    HIPCHK(nullptr, h->t_cmb.init());
     HIPCHK(nullptr, h->t_plan.init());
     HIPCHK(nullptr, h->t_fill.init());
 
@@ -471,6 +514,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     HIPCHK(nullptr, hipMemsetAsync(h->hash, 0xFF, sizeof(uint64_t) * cap, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->storage, 0, sizeof(float) * S * h->D, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->sel_hist, 0, sizeof(int32_t) * MAX_TABLES * SEL_BINS, h->s_plan));
+    HIPCHK(nullptr, hipMemsetAsync(h->cnt, 0, sizeof(DevCounters), h->s_plan));
     HIPCHK(nullptr, hipStreamSynchronize(h->s_plan));
     h->st.min_capacity_margin = INT64_MAX;
     h->worker = std::thread(worker_main, h);
@@ -554,14 +598,22 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
     const int r = (int)(q % h->nring);
     BatchDev &b = h->ring[r];
     // the previous occupant (batch q - nring) must be done with its backward
-    HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ring_free[r], 0));
+    HIPCHK(h, hipStreamWaitEvent(h->s_ingest, h->ring_free[r], 0));
     const int64_t nbags = (int64_t)h->T * bt.batch;
-    const hipMemcpyKind kind = bt.on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
-    if (bt.nnz > 0) HIPCHK(h, hipMemcpyAsync(b.ids, bt.ids, sizeof(int32_t) * bt.nnz, kind, h->s_plan));
-    HIPCHK(h, hipMemcpyAsync(b.bag_off, bt.bag_off, sizeof(int32_t) * (nbags + 1), kind, h->s_plan));
-    launch_ingest(h->tb, b, bt.batch, bt.nnz, h->key_bits, h->chunk, h->tmp_k, h->tmp_v, h->hist,
-                  h->scan_tmp, h->cnt, h->s_plan);
+    const int32_t *ids = bt.ids, *off = bt.bag_off;
+    if (!bt.on_device) {  // host arrays: copy into the ring first
+        if (bt.nnz > 0)
+            HIPCHK(h, hipMemcpyAsync(b.ids, bt.ids, sizeof(int32_t) * bt.nnz, hipMemcpyHostToDevice,
+                                     h->s_ingest));
+        HIPCHK(h, hipMemcpyAsync(b.bag_off, bt.bag_off, sizeof(int32_t) * (nbags + 1),
+                                 hipMemcpyHostToDevice, h->s_ingest));
+        ids = b.ids;
+        off = b.bag_off;
+    }
+    launch_ingest(h->tb, b, ids, off, bt.batch, bt.nnz, h->key_bits, h->chunk, h->itmp_k,
+                  h->itmp_v, h->ihist, h->iscan_tmp, h->s_ingest);
     CHECK_LAUNCH(h);
+    HIPCHK(h, hipEventRecord(h->ring_ready[r], h->s_ingest));
     h->ring_batch[r] = q;
     h->ring_nnz[r] = bt.nnz;
     h->ring_B[r] = bt.batch;
@@ -574,8 +626,8 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     if (h->updated != h->planned)
         return fail(h, SP_ERR_SEQUENCE, "plan %lld requested before backward of ticket %lld",
                     (long long)h->planned, (long long)h->planned - 1);
-    if (!window || n < 1 || n > h->L + 1)
-        return fail(h, SP_ERR_INVALID_ARG, "window of %d batches (1..%d allowed)", n, h->L + 1);
+    if (!window || n < 1 || n > h->L + 2)
+        return fail(h, SP_ERR_INVALID_ARG, "window of %d batches (1..%d allowed)", n, h->L + 2);
     for (int w = 0; w < n; ++w) {
         const sp_batch &b = window[w];
         if (b.batch < 0 || b.batch > h->max_batch || b.nnz < 0 || b.nnz > h->max_ids || !b.bag_off ||
@@ -586,57 +638,69 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     const int64_t k = h->planned;
     const int32_t u = (int32_t)k;
     const int e = (int)(k % TICKETS);
+    const int nhold = std::min<int>(n, h->L + 1);  // window[L+1], if given, is only prepared
     TicketDev &tk = h->tk[e];
     TicketHost &th = h->tkh[e];
     const bool timing = h->flags & SP_FLAG_TIMING;
-    if (timing) HIPCHK(h, h->t_plan.begin(h->s_plan));
 
-    // the ticket buffers being reused belonged to ticket k - TICKETS
-    if (k >= TICKETS) HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ev_upd[e], 0));
-    launch_zero_i32((int32_t *)h->cnt, sizeof(DevCounters) / sizeof(int32_t), h->s_plan);
-
-    // ---- phase 1: ingest new window batches, query, hold (read-only on the scratchpad)
-    const uint32_t *ukeys[MAX_WINDOW];
-    const int32_t *nuniq[MAX_WINDOW];
-    int64_t max_nnz = 0;
+    // ---- ingest (own stream): every window batch not in the ring yet; with a
+    // prepared-ahead batch this is normally just that one, off the plan's path
     for (int w = 0; w < n; ++w) {
         const int64_t q = k + w;
         const int r = (int)(q % h->nring);
-        if (q >= h->ingested || h->ring_batch[r] != q) {
+        if (h->ring_batch[r] != q) {
             TRY(ingest(h, window[w], q));
         } else if (h->ring_nnz[r] != window[w].nnz || h->ring_B[r] != window[w].batch) {
             return fail(h, SP_ERR_INVALID_ARG, "batch %lld changed shape between windows", (long long)q);
         }
+    }
+
+    // ---- phase 1: query and hold (read-only on the scratchpad)
+    if (timing) HIPCHK(h, h->t_plan.begin(h->s_plan));
+    // the ticket buffers being reused belonged to ticket k - TICKETS
+    if (k >= TICKETS) HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ev_upd[e], 0));
+    const uint32_t *ukeys[MAX_WINDOW];
+    const int32_t *nuniq[MAX_WINDOW];
+    int64_t max_nnz = 0;
+    for (int w = 0; w < nhold; ++w) {
+        const int r = (int)((k + w) % h->nring);
+        HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ring_ready[r], 0));
         ukeys[w] = h->ring[r].ukeys;
         nuniq[w] = h->ring[r].scal;
         max_nnz = std::max(max_nnz, window[w].nnz);
     }
+    launch_zero_i32((int32_t *)h->cnt, COUNTERS_CLEARED, h->s_plan);
     const int r0 = (int)(k % h->nring);
     const int stamp = ++h->stamp;
-    launch_probe_hold(h->tb, h->hash, h->hash_mask, ukeys, nuniq, n, max_nnz, h->held, stamp, tk,
-                      h->cnt, h->ring[r0].scal, h->s_plan);
+    launch_probe_hold(h->tb, h->hash, h->hash_mask, ukeys, nuniq, nhold, max_nnz, h->held, stamp,
+                      tk, h->cnt, h->ring[r0].scal, h->s_plan);
+    launch_publish(h->cnt, h->h_cnt_dev, h->s_plan);
     CHECK_LAUNCH(h);
-    HIPCHK(h, hipMemcpyAsync(h->h_cnt, h->cnt, sizeof(DevCounters), hipMemcpyDeviceToHost, h->s_plan));
     HIPCHK(h, hipStreamSynchronize(h->s_plan));
-    const DevCounters c = *h->h_cnt;
-    if (c.err & (ERR_ID_RANGE | ERR_OFFSETS))
+    DevCounters c;
+    memcpy(&c, (const void *)h->h_cnt, sizeof c);
+    if (c.err & (ERR_ID_RANGE | ERR_OFFSETS)) {
+        for (int w = 0; w < n; ++w) h->ring_batch[(k + w) % h->nring] = -1;  // re-read on retry
         return fail(h, SP_ERR_INVALID_ARG, "%s in the window",
                     (c.err & ERR_ID_RANGE) ? "row ID out of range" : "malformed bag offsets");
-    if (c.err & (ERR_HASH_FULL | ERR_PLAN))
-        return fail(h, SP_ERR_HIP, "internal planner inconsistency (flags %d) in an earlier plan", c.err);
+    }
+    if (c.err_sticky)
+        return fail(h, SP_ERR_HIP, "internal planner inconsistency (flags %d) in an earlier plan",
+                    c.err_sticky);
     int64_t n_miss = 0, margin = INT64_MAX;
     for (int t = 0; t < h->T; ++t) {
         const int64_t free_slots = h->slots[t] - c.held[t];
         margin = std::min<int64_t>(margin, free_slots - c.miss[t]);
-        if (c.miss[t] > free_slots)
+        if (c.miss[t] > free_slots) {
+            for (int w = 0; w < n; ++w) h->ring_batch[(k + w) % h->nring] = -1;  // re-read on retry
             return fail(h, SP_ERR_CAPACITY,
                         "table %d: %d misses but only %lld unheld slots (plan %lld)", t, c.miss[t],
                         (long long)free_slots, (long long)k);
+        }
         n_miss += c.miss[t];
     }
 
     // ---- phase 2: commit
-    h->ingested = std::max<int64_t>(h->ingested, k + n);
     const BatchDev &b0 = h->ring[r0];
     th.nnz = h->ring_nnz[r0];
     th.B = (int32_t)h->ring_B[r0];
@@ -644,7 +708,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     th.n_chunks = c.n_chunks;
     th.n_miss = n_miss;
     th.ring = r0;
-    th.nwin = n;
+    th.nwin = nhold;
 
     if (n_miss > 0) {
         const int64_t cap = (int64_t)h->hash_mask + 1;
@@ -683,9 +747,11 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     }
     launch_touch_remap(tk, b0, th.n_unique, th.nnz, h->total_slots, h->last_use, u, h->s_plan);
     CHECK_LAUNCH(h);
+    HIPCHK(h, hipEventRecord(h->ev_planned[e], h->s_plan));
     if (timing) HIPCHK(h, h->t_plan.end(h->s_plan));
 
-    // ---- mover: write-back of evicted rows and fill of misses
+    // ---- mover (own stream): write-back of evicted rows and fill of misses;
+    // the next plan's query does not wait for it
     // RAW-4: rows evicted by plan p may be refilled from plan p + n_p on
     int64_t need = -1;
     for (const auto &d : h->deadlines)
@@ -695,34 +761,34 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
         while (!h->deadlines.empty() && h->deadlines.front().first <= need) h->deadlines.pop_front();
     }
     const int sl = (int)(k & 1);
+    HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_planned[e], 0));
     if (k >= 2) {
         TRY(join_jobs(h, k - 2));  // host staging of plan k-2 is free again
-        HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ev_d2h[sl], 0));
+        HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_d2h[sl], 0));
     }
-    if (timing) HIPCHK(h, h->t_fill.begin(h->s_plan));
+    if (timing) HIPCHK(h, h->t_fill.begin(h->s_move));
     if (n_miss > 0) {
-        if (k >= 2) HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ev_upd[(k - 2) % TICKETS], 0));
-        launch_pack(h->storage, h->D, h->total_slots, tk, n_miss, u, 0, h->stage_dev[sl], h->s_plan);
-        launch_fill(h->storage, h->D, h->tb, h->host_dev, tk, n_miss, u, 0, h->s_plan);
-        if (k >= 1) HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ev_upd[(k - 1) % TICKETS], 0));
-        launch_pack(h->storage, h->D, h->total_slots, tk, n_miss, u, 1, h->stage_dev[sl], h->s_plan);
-        launch_fill(h->storage, h->D, h->tb, h->host_dev, tk, n_miss, u, 1, h->s_plan);
+        if (k >= 2) HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_upd[(k - 2) % TICKETS], 0));
+        launch_pack(h->storage, h->D, h->total_slots, tk, n_miss, u, 0, h->stage_dev[sl], h->s_move);
+        launch_fill(h->storage, h->D, h->tb, h->host_dev, tk, n_miss, u, 0, h->s_move);
+        if (k >= 1) HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_upd[(k - 1) % TICKETS], 0));
+        launch_pack(h->storage, h->D, h->total_slots, tk, n_miss, u, 1, h->stage_dev[sl], h->s_move);
+        launch_fill(h->storage, h->D, h->tb, h->host_dev, tk, n_miss, u, 1, h->s_move);
         CHECK_LAUNCH(h);
     }
-    HIPCHK(h, hipEventRecord(h->ev_filled[e], h->s_plan));
-    if (timing) HIPCHK(h, h->t_fill.end(h->s_plan));
+    HIPCHK(h, hipEventRecord(h->ev_filled[e], h->s_move));
+    if (timing) HIPCHK(h, h->t_fill.end(h->s_move));
     Job job;
     job.ticket = k;
     if (n_miss > 0) {
         HIPCHK(h, hipStreamWaitEvent(h->s_copy, h->ev_filled[e], 0));
-        HIPCHK(h, hipMemcpyAsync(h->stage_host[sl], h->stage_dev[sl], sizeof(float) * n_miss * h->D,
-                                 hipMemcpyDeviceToHost, h->s_copy));
-        HIPCHK(h, hipMemcpyAsync(h->stage_keys[sl], tk.v_old_key, sizeof(int32_t) * n_miss,
-                                 hipMemcpyDeviceToHost, h->s_copy));
+        HIPCHK(h, hipMemcpyAsync(h->stage_host[sl], h->stage_dev[sl],
+                                 sizeof(float) * n_miss * (h->D + 1), hipMemcpyDeviceToHost,
+                                 h->s_copy));
         HIPCHK(h, hipEventRecord(h->ev_d2h[sl], h->s_copy));
         job.ev = h->ev_d2h[sl];
         job.rows = h->stage_host[sl];
-        job.keys = h->stage_keys[sl];
+        job.keys = (const int32_t *)(h->stage_host[sl] + n_miss * h->D);
         job.n = n_miss;
     }
     {
@@ -730,7 +796,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
         h->jobs.push_back(job);
     }
     h->cv.notify_one();
-    h->deadlines.emplace_back(k, k + n);
+    h->deadlines.emplace_back(k, k + nhold);
 
     h->planned = k + 1;
     h->st.plans += 1;
@@ -760,12 +826,11 @@ extern "C" sp_status sp_forward(sp_handle h, int64_t ticket, float *d_out, void 
     hipStream_t s = (hipStream_t)stream;
     HIPCHK(h, hipStreamWaitEvent(s, h->ev_filled[e], 0));
     if (ticket >= 1) HIPCHK(h, hipStreamWaitEvent(s, h->ev_upd[(ticket - 1) % TICKETS], 0));
-    const bool timing = h->flags & SP_FLAG_TIMING;
-    if (timing) HIPCHK(h, h->t_fwd.begin(s));
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if ((h->flags & SP_FLAG_TIMING) && nbags > 0) HIPCHK(h, h->t_fwd.take(&e0, &e1));
     launch_forward(h->storage, h->D, h->total_slots, h->tk[e].slot_of, h->ring[th.ring].bag_off,
-                   nbags, d_out, s);
+                   nbags, d_out, s, e0, e1);
     CHECK_LAUNCH(h);
-    if (timing) HIPCHK(h, h->t_fwd.end(s));
     h->forwarded = ticket + 1;
     if (h->flags & SP_FLAG_DEBUG_SYNC) HIPCHK(h, hipDeviceSynchronize());
     return SP_OK;
@@ -782,17 +847,19 @@ extern "C" sp_status sp_backward_update(sp_handle h, int64_t ticket, const float
     const TicketHost &th = h->tkh[e];
     if (th.nnz > 0 && !d_grad) return fail(h, SP_ERR_INVALID_ARG, "null d_grad");
     hipStream_t s = (hipStream_t)stream;
-    const bool timing = h->flags & SP_FLAG_TIMING;
-    if (timing) HIPCHK(h, h->t_bwd.begin(s));
+    hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+    if ((h->flags & SP_FLAG_TIMING) && th.n_chunks > 0) HIPCHK(h, h->t_bwd.take(&ev[0], &ev[1]));
+    if ((h->flags & SP_FLAG_TIMING) && th.n_chunks > th.n_unique)
+        HIPCHK(h, h->t_cmb.take(&ev[2], &ev[3]));
     launch_backward(h->storage, h->D, h->total_slots, h->ring[th.ring], h->tk[e].slot_u,
                     th.n_unique, th.n_chunks, h->chunk, d_grad, (int64_t)h->T * th.B, lr,
-                    h->partial, s);
+                    h->partial, s, ev);
     CHECK_LAUNCH(h);
-    if (timing) HIPCHK(h, h->t_bwd.end(s));
     HIPCHK(h, hipEventRecord(h->ev_upd[e], s));
     HIPCHK(h, hipEventRecord(h->ring_free[th.ring], s));
     h->updated = ticket + 1;
     h->st.updates += 1;
+    h->st.chunks += th.n_chunks;
     if (h->flags & SP_FLAG_DEBUG_SYNC) HIPCHK(h, hipDeviceSynchronize());
     return SP_OK;
 }
@@ -835,6 +902,7 @@ extern "C" sp_status sp_get_stats(sp_handle h, sp_stats *out)
     HIPCHK(h, hipDeviceSynchronize());
     HIPCHK(h, h->t_fwd.flush());
     HIPCHK(h, h->t_bwd.flush());
+    HIPCHK(h, h->t_cmb.flush());
     HIPCHK(h, h->t_plan.flush());
     HIPCHK(h, h->t_fill.flush());
     sp_stats s = h->st;
@@ -848,10 +916,12 @@ extern "C" sp_status sp_get_stats(sp_handle h, sp_stats *out)
     s.pinned_bytes = h->pinned_bytes;
     s.ms_forward = h->t_fwd.ms;
     s.ms_backward = h->t_bwd.ms;
+    s.ms_combine = h->t_cmb.ms;
     s.ms_plan = h->t_plan.ms;
     s.ms_fill = h->t_fill.ms;
     s.timed_forward = h->t_fwd.count;
     s.timed_backward = h->t_bwd.count;
+    s.timed_combine = h->t_cmb.count;
     s.timed_plan = h->t_plan.count;
     s.timed_fill = h->t_fill.count;
     *out = s;

@@ -27,46 +27,51 @@ void launch_zero_i32(int32_t *p, int64_t n, hipStream_t s) { launch_fill_i32(p, 
 
 // ---------------------------------------------------------------- keys and bags
 
-// key = table << row_bits | row; the table of position j is the one whose
-// span [bag_off[t*B], bag_off[(t+1)*B]) contains j.  Out-of-range rows raise
-// ERR_ID_RANGE and are clamped so that nothing downstream reads out of bounds.
-__global__ void __launch_bounds__(BLOCK) k_build_keys(Tables tb, const int32_t *ids,
-                                                      const int32_t *bag_off, int32_t B,
-                                                      int64_t nnz, uint32_t *keys,
-                                                      uint32_t *pos, int32_t *err)
+// One launch over max(nnz, nbags) threads, two independent jobs:
+//  * position j < nnz: key = table << row_bits | row, where the table is the
+//    one whose span [bag_off[t*B], bag_off[(t+1)*B]) contains j; rows out of
+//    range raise ERR_ID_RANGE and are clamped so nothing downstream leaves
+//    its array;
+//  * bag g < nbags: validate the offsets (non-decreasing, from 0 to nnz;
+//    ERR_OFFSETS otherwise, ranges clamped into [0, nnz)), write bag_of[j] = g
+//    for the bag's positions and copy the offsets into the window ring (when
+//    they are read from the caller's device memory).
+__global__ void __launch_bounds__(BLOCK) k_prepare(Tables tb, const int32_t *ids,
+                                                   const int32_t *bag_off, int32_t *bag_off_copy,
+                                                   int32_t B, int64_t nnz, int64_t nbags,
+                                                   uint32_t *keys, uint32_t *pos, int32_t *bag_of,
+                                                   int32_t *err)
 {
-    int64_t j = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
-    if (j >= nnz) return;
-    int lo = 0, hi = tb.T - 1;  // largest t with bag_off[t*B] <= j
-    while (lo < hi) {
-        int mid = (lo + hi + 1) >> 1;
-        if ((int64_t)bag_off[(int64_t)mid * B] <= j) lo = mid; else hi = mid - 1;
+    const int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    if (i < nnz) {
+        int lo = 0, hi = tb.T - 1;  // largest t with bag_off[t*B] <= i
+        while (lo < hi) {
+            int mid = (lo + hi + 1) >> 1;
+            if ((int64_t)bag_off[(int64_t)mid * B] <= i) lo = mid; else hi = mid - 1;
+        }
+        int32_t row = ids[i];
+        if (row < 0 || (int64_t)row >= tb.rows[lo]) {
+            atomicOr(err, ERR_ID_RANGE);
+            row = 0;
+        }
+        keys[i] = ((uint32_t)lo << tb.row_bits) | (uint32_t)row;
+        pos[i] = (uint32_t)i;
     }
-    int32_t row = ids[j];
-    if (row < 0 || (int64_t)row >= tb.rows[lo]) {
-        atomicOr(err, ERR_ID_RANGE);
-        row = 0;
+    if (i < nbags) {
+        int64_t lo = bag_off[i], hi = bag_off[i + 1];
+        if (bag_off_copy != bag_off) {
+            bag_off_copy[i] = (int32_t)lo;
+            if (i == nbags - 1) bag_off_copy[i + 1] = (int32_t)hi;
+        }
+        bool bad = lo > hi || lo < 0 || hi > nnz || (i == 0 && lo != 0) ||
+                   (i == nbags - 1 && hi != nnz);
+        if (bad) {
+            atomicOr(err, ERR_OFFSETS);
+            lo = lo < 0 ? 0 : (lo > nnz ? nnz : lo);
+            hi = hi < lo ? lo : (hi > nnz ? nnz : hi);
+        }
+        for (int64_t j = lo; j < hi; ++j) bag_of[j] = (int32_t)i;
     }
-    keys[j] = ((uint32_t)lo << tb.row_bits) | (uint32_t)row;
-    pos[j] = (uint32_t)j;
-}
-
-// bag_of[j] = bag containing position j.  Offsets are validated on the way:
-// non-decreasing, starting at 0 and ending at nnz (ERR_OFFSETS otherwise, with
-// the ranges clamped into [0, nnz)).
-__global__ void __launch_bounds__(BLOCK) k_bag_of(const int32_t *bag_off, int64_t nbags,
-                                                  int64_t nnz, int32_t *bag_of, int32_t *err)
-{
-    int64_t g = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
-    if (g >= nbags) return;
-    int64_t lo = bag_off[g], hi = bag_off[g + 1];
-    bool bad = lo > hi || lo < 0 || hi > nnz || (g == 0 && lo != 0) || (g == nbags - 1 && hi != nnz);
-    if (bad) {
-        atomicOr(err, ERR_OFFSETS);
-        lo = lo < 0 ? 0 : (lo > nnz ? nnz : lo);
-        hi = hi < lo ? lo : (hi > nnz ? nnz : hi);
-    }
-    for (int64_t j = lo; j < hi; ++j) bag_of[j] = (int32_t)g;
 }
 
 // ---------------------------------------------------------------- LSD radix sort
@@ -167,7 +172,7 @@ void launch_radix_sort(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *v1, i
         int shift = 8 * p;
         hipLaunchKernelGGL(k_radix_hist, dim3(tiles), dim3(BLOCK), 0, s, ki, n, shift, hist, tiles);
         seg_scan(SegN{(int64_t)256 * tiles}, 1, (int64_t)256 * tiles, ValU32{hist}, OutU32{hist},
-                 (uint32_t *)scan_tmp, (uint32_t *)nullptr, s);
+                 (uint32_t *)scan_tmp, (uint32_t *)nullptr, s, true);
         hipLaunchKernelGGL(k_radix_scatter, dim3(tiles), dim3(BLOCK), 0, s, ki, vi, n, shift,
                            hist, tiles, ko, vo);
         uint32_t *t;
@@ -228,36 +233,28 @@ struct ChunkOut {
     }
 };
 
-// scal[2+t] = first unique index of table t (lower bound of t << row_bits).
-__global__ void k_table_starts(const uint32_t *ukeys, int32_t *scal, int T, int row_bits)
-{
-    int t = threadIdx.x;
-    if (t > T) return;
-    uint32_t key = (uint32_t)t << row_bits;
-    int32_t lo = 0, hi = scal[0];
-    while (lo < hi) {
-        int32_t mid = lo + (hi - lo) / 2;
-        if (ukeys[mid] < key) lo = mid + 1; else hi = mid;
-    }
-    scal[2 + t] = lo;
-}
-
-void launch_ingest(const Tables &tb, const BatchDev &b, int32_t B, int64_t nnz, int key_bits,
-                   int chunk, uint32_t *tmp_k, uint32_t *tmp_v, uint32_t *hist,
-                   void *scan_tmp, DevCounters *cnt, hipStream_t s)
+// Sort, deduplicate and split into backward chunks one batch of the window.
+// ids / bag_off may be the caller's device arrays (read once, here) or the
+// ring's own copies; the ring always ends up with the offsets.  Input errors
+// are recorded in the batch's own scal[2].
+void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, const int32_t *bag_off,
+                   int32_t B, int64_t nnz, int key_bits, int chunk, uint32_t *tmp_k,
+                   uint32_t *tmp_v, uint32_t *hist, void *scan_tmp, hipStream_t s)
 {
     const int64_t nbags = (int64_t)tb.T * B;
-    launch_zero_i32(b.scal, 2 + tb.T + 1, s);
-    if (nbags > 0)
-        hipLaunchKernelGGL(k_bag_of, dim3((unsigned)((nbags + BLOCK - 1) / BLOCK)), dim3(BLOCK), 0,
-                           s, b.bag_off, nbags, nnz, b.bag_of, &cnt->err);
+    launch_zero_i32(b.scal, 3, s);
+    // place the keys so that the final sort pass lands in skeys/perm
+    const int passes = nnz > 1 ? (key_bits + 7) / 8 : 0;
+    uint32_t *k0 = (passes & 1) ? tmp_k : b.skeys, *v0 = (passes & 1) ? tmp_v : b.perm;
+    uint32_t *k1 = (passes & 1) ? b.skeys : tmp_k, *v1 = (passes & 1) ? b.perm : tmp_v;
+    const int64_t nthr = nnz > nbags ? nnz : nbags;
+    if (nthr > 0)
+        hipLaunchKernelGGL(k_prepare, dim3((unsigned)((nthr + BLOCK - 1) / BLOCK)), dim3(BLOCK), 0,
+                           s, tb, ids, bag_off, b.bag_off, B, nnz, nbags, k0, v0, b.bag_of,
+                           b.scal + 2);
+    else if (bag_off != b.bag_off)
+        hipMemcpyAsync(b.bag_off, bag_off, sizeof(int32_t), hipMemcpyDeviceToDevice, s);
     if (nnz > 0) {
-        // place the keys so that the final sort pass lands in skeys/perm
-        const int passes = nnz > 1 ? (key_bits + 7) / 8 : 0;
-        uint32_t *k0 = (passes & 1) ? tmp_k : b.skeys, *v0 = (passes & 1) ? tmp_v : b.perm;
-        uint32_t *k1 = (passes & 1) ? b.skeys : tmp_k, *v1 = (passes & 1) ? b.perm : tmp_v;
-        hipLaunchKernelGGL(k_build_keys, dim3((unsigned)((nnz + BLOCK - 1) / BLOCK)), dim3(BLOCK),
-                           0, s, tb, b.ids, b.bag_off, B, nnz, k0, v0, &cnt->err);
         bool in_k1 = false;
         launch_radix_sort(k0, v0, k1, v1, nnz, key_bits, hist, scan_tmp, &in_k1, s);
         seg_scan(SegN{nnz}, 1, nnz, HeadFlag{b.skeys},
@@ -268,8 +265,23 @@ void launch_ingest(const Tables &tb, const BatchDev &b, int32_t B, int64_t nnz, 
                  ChunkOut{b.seg_chunk0, b.chunk_seg, b.scal}, (uint32_t *)scan_tmp,
                  (uint32_t *)nullptr, s);
     }
-    hipLaunchKernelGGL(k_table_starts, dim3(1), dim3(MAX_TABLES + 1), 0, s, b.ukeys, b.scal, tb.T,
-                       tb.row_bits);
+}
+
+// Copy the plan counters to pinned, device-mapped, host-coherent memory with
+// plain stores, so the host reads them after one stream synchronisation
+// without a separate copy command.
+__global__ void k_publish(const DevCounters *cnt, DevCounters *host_mapped)
+{
+    constexpr int N = (int)(sizeof(DevCounters) / sizeof(int32_t));
+    const int32_t *src = reinterpret_cast<const int32_t *>(cnt);
+    int32_t *dst = reinterpret_cast<int32_t *>(host_mapped);
+    for (int i = threadIdx.x; i < N; i += blockDim.x) dst[i] = src[i];
+    __threadfence_system();
+}
+
+void launch_publish(const DevCounters *cnt, DevCounters *host_mapped, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_publish, dim3(1), dim3(BLOCK), 0, s, cnt, host_mapped);
 }
 
 }  // namespace sp

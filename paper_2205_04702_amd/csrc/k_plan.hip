@@ -17,33 +17,49 @@ struct ProbeArgs {
 // blockIdx.y = window batch.  Every cached key of a window batch stamps its
 // slot as held for this plan (held[slot] = stamp) and counts it once per
 // table; batch 0 (the planned one) also records hit / slot and counts misses.
+// Per-table counts are summed across the wave first (keys are sorted, so a
+// wave nearly always covers one table) and added with one atomic per table
+// per wave.
 __global__ void __launch_bounds__(BLOCK) k_probe_hold(int32_t row_bits, const uint64_t *hash,
                                                       uint32_t mask, ProbeArgs pa, int32_t *held,
                                                       int32_t stamp, int32_t *hit,
-                                                      int32_t *slot_u, DevCounters *cnt)
+                                                      int32_t *slot_u, DevCounters *cnt,
+                                                      const int32_t *scal0)
 {
     const int w = blockIdx.y;
     const int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
-    if (i >= *pa.nu[w]) return;
-    const uint32_t key = pa.uk[w][i];
-    const int t = (int)(key >> row_bits);
-    const int32_t slot = hash_find(hash, mask, key);
-    if (w == 0) {
-        hit[i] = slot >= 0;
-        slot_u[i] = slot;
-        if (slot < 0) atomicAdd(&cnt->miss[t], 1);
-    }
-    if (slot >= 0) {
-        int32_t old = atomicExch(&held[slot], stamp);
-        if (old != stamp) atomicAdd(&cnt->held[t], 1);
-    }
-}
-
-__global__ void k_collect(DevCounters *cnt, const int32_t *scal0)
-{
-    if (threadIdx.x == 0) {
+    if (w == 0 && i == 0) {
         cnt->n_unique = scal0[0];
         cnt->n_chunks = scal0[1];
+    }
+    if (i == 0 && pa.nu[w][2]) atomicOr(&cnt->err, pa.nu[w][2]);  // the batch's input errors
+    const bool valid = i < *pa.nu[w];
+    int t = 0;
+    bool miss = false, fresh = false;
+    if (valid) {
+        const uint32_t key = pa.uk[w][i];
+        t = (int)(key >> row_bits);
+        const int32_t slot = hash_find(hash, mask, key);
+        if (w == 0) {
+            hit[i] = slot >= 0;
+            slot_u[i] = slot;
+            miss = slot < 0;
+        }
+        if (slot >= 0) fresh = atomicExch(&held[slot], stamp) != stamp;
+    }
+    uint64_t todo = __ballot(valid);
+    while (todo) {
+        const int leader = __ffsll((unsigned long long)todo) - 1;
+        const int tl = __shfl(t, leader, WAVE);
+        const bool mine = valid && t == tl;
+        const uint64_t same = __ballot(mine);
+        const int nm = __popcll(__ballot(mine && miss));
+        const int nh = __popcll(__ballot(mine && fresh));
+        if (lane_id() == leader) {
+            if (nm) atomicAdd(&cnt->miss[tl], nm);
+            if (nh) atomicAdd(&cnt->held[tl], nh);
+        }
+        todo &= ~same;
     }
 }
 
@@ -54,11 +70,11 @@ void launch_probe_hold(const Tables &tb, const uint64_t *hash, uint32_t mask,
 {
     ProbeArgs pa{};
     for (int w = 0; w < nwin; ++w) pa.uk[w] = ukeys[w], pa.nu[w] = nuniq[w];
-    if (max_unique > 0)
-        hipLaunchKernelGGL(k_probe_hold, dim3((unsigned)((max_unique + BLOCK - 1) / BLOCK), nwin),
-                           dim3(BLOCK), 0, s, tb.row_bits, hash, mask, pa, held, stamp, tk.hit,
-                           tk.slot_u, cnt);
-    hipLaunchKernelGGL(k_collect, dim3(1), dim3(64), 0, s, cnt, scal0);
+    // at least one block per batch so that every batch's error word is read
+    const int64_t n = max_unique > 0 ? max_unique : 1;
+    hipLaunchKernelGGL(k_probe_hold, dim3((unsigned)((n + BLOCK - 1) / BLOCK), nwin), dim3(BLOCK),
+                       0, s, tb.row_bits, hash, mask, pa, held, stamp, tk.hit, tk.slot_u, cnt,
+                       scal0);
 }
 
 // ---------------------------------------------------------------- hash rebuild
@@ -86,7 +102,7 @@ void launch_hash_rebuild(uint64_t *hash, uint32_t mask, const int32_t *key_of_sl
                        hash, cap);
     if (nslots > 0)
         hipLaunchKernelGGL(k_hash_reinsert, dim3((unsigned)((nslots + BLOCK - 1) / BLOCK)),
-                           dim3(BLOCK), 0, s, hash, mask, key_of_slot, nslots, &cnt->err);
+                           dim3(BLOCK), 0, s, hash, mask, key_of_slot, nslots, &cnt->err_sticky);
 }
 
 // ---------------------------------------------------------------- misses
@@ -131,18 +147,9 @@ void launch_miss_compact(const uint32_t *ukeys, int64_t n_unique, TicketDev tk, 
 constexpr int SEL_ITEMS = 16;
 constexpr int SEL_CHUNK = BLOCK * SEL_ITEMS;
 
-__global__ void k_sel_init(SelArgs a, int32_t *st, int32_t *hist)
-{
-    for (int i = threadIdx.x; i < a.nact; i += blockDim.x) {
-        st[2 * i] = 0;
-        st[2 * i + 1] = a.k[i];
-    }
-    (void)hist;
-}
-
-__global__ void __launch_bounds__(BLOCK) k_sel_hist(SelArgs a, int shift, const int32_t *held,
-                                                    const int32_t *last_use, const int32_t *st,
-                                                    int32_t *hist)
+__global__ void __launch_bounds__(BLOCK) k_sel_hist(SelArgs a, int shift, int first,
+                                                    const int32_t *held, const int32_t *last_use,
+                                                    const int32_t *st, int32_t *hist)
 {
     __shared__ int32_t h[SEL_BINS];
     for (int b = threadIdx.x; b < SEL_BINS; b += BLOCK) h[b] = 0;
@@ -151,7 +158,7 @@ __global__ void __launch_bounds__(BLOCK) k_sel_hist(SelArgs a, int shift, const 
     const int64_t S = a.S[ai];
     const int64_t s0 = (int64_t)blockIdx.x * SEL_CHUNK;
     if (s0 < S) {
-        const uint64_t want = (uint64_t)(uint32_t)st[2 * ai] >> (shift + SEL_BITS);
+        const uint64_t want = first ? 0 : (uint64_t)(uint32_t)st[2 * ai] >> (shift + SEL_BITS);
         const int64_t base = a.base[ai];
         for (int r = 0; r < SEL_ITEMS; ++r) {
             int64_t s = s0 + (int64_t)r * BLOCK + threadIdx.x;
@@ -171,14 +178,17 @@ __global__ void __launch_bounds__(BLOCK) k_sel_hist(SelArgs a, int shift, const 
         if (h[b]) atomicAdd(&out[b], h[b]);
 }
 
-// One block per active table: fix the next SEL_BITS of v*.
-__global__ void __launch_bounds__(BLOCK) k_sel_pick(int shift, int32_t *st, int32_t *hist)
+// One block per active table: fix the next SEL_BITS of v*.  The first level
+// starts from k misses still to place and an empty prefix.
+__global__ void __launch_bounds__(BLOCK) k_sel_pick(SelArgs a, int shift, int first, int32_t *st,
+                                                    int32_t *hist)
 {
     __shared__ int32_t lds[BLOCK / WAVE];
     constexpr int PER = SEL_BINS / BLOCK;
     const int ai = blockIdx.x;
     int32_t *h = hist + (int64_t)ai * SEL_BINS;
-    const int32_t krem = st[2 * ai + 1];
+    const int32_t krem = first ? a.k[ai] : st[2 * ai + 1];
+    const int32_t prefix = first ? 0 : st[2 * ai];
     int32_t c[PER], sum = 0;
 #pragma unroll
     for (int q = 0; q < PER; ++q) {
@@ -192,7 +202,7 @@ __global__ void __launch_bounds__(BLOCK) k_sel_pick(int shift, int32_t *st, int3
 #pragma unroll
         for (int q = 0; q < PER; ++q) {
             if (cum + c[q] >= krem) {
-                st[2 * ai] |= (threadIdx.x * PER + q) << shift;
+                st[2 * ai] = prefix | ((threadIdx.x * PER + q) << shift);
                 st[2 * ai + 1] = krem - cum;
                 break;
             }
@@ -251,13 +261,13 @@ void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int
                            hipStream_t s)
 {
     if (a.nact <= 0 || n_victims <= 0) return;
-    hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(64), 0, s, a, sel_state, sel_hist);
     const unsigned chunks = (unsigned)((maxS + SEL_CHUNK - 1) / SEL_CHUNK);
     for (int l = 0; l < levels; ++l) {
         int shift = (levels - 1 - l) * SEL_BITS;
-        hipLaunchKernelGGL(k_sel_hist, dim3(chunks, a.nact), dim3(BLOCK), 0, s, a, shift, held,
-                           last_use, (const int32_t *)sel_state, sel_hist);
-        hipLaunchKernelGGL(k_sel_pick, dim3(a.nact), dim3(BLOCK), 0, s, shift, sel_state, sel_hist);
+        hipLaunchKernelGGL(k_sel_hist, dim3(chunks, a.nact), dim3(BLOCK), 0, s, a, shift, (int)(l == 0),
+                           held, last_use, (const int32_t *)sel_state, sel_hist);
+        hipLaunchKernelGGL(k_sel_pick, dim3(a.nact), dim3(BLOCK), 0, s, a, shift, (int)(l == 0),
+                           sel_state, sel_hist);
     }
     // compaction lands where the sort's last pass will end in v_slot
     const int bits = a.act_bits + a.lu_bits;
@@ -289,16 +299,21 @@ void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int
 
 // ---------------------------------------------------------------- commit
 
-// Record each victim's previous occupant and erase it from the Hit-Map.
-__global__ void __launch_bounds__(BLOCK) k_evict(uint64_t *hash, uint32_t mask, TicketDev tk,
-                                                 int64_t n, int64_t nslots,
-                                                 const int32_t *key_of_slot,
-                                                 const int32_t *last_use, int32_t *err)
+// Miss i goes to victim slot i: record the slot's previous occupant and its
+// last use, erase that key from the Hit-Map, enter the new key.  Erases and
+// inserts may interleave across threads: inserts only claim EMPTY or erased
+// entries, so they never disturb a live key another thread is erasing, and
+// the keys inserted are known to be absent.
+__global__ void __launch_bounds__(BLOCK) k_commit(uint64_t *hash, uint32_t mask, TicketDev tk,
+                                                  int64_t n, int64_t nslots, int64_t n_unique,
+                                                  int32_t *key_of_slot, const int32_t *last_use,
+                                                  int32_t *err)
 {
     int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
     if (i >= n) return;
     const int32_t v = tk.v_slot[i];
-    if ((uint32_t)v >= (uint64_t)nslots) {
+    const int32_t ui = tk.m_uidx[i];
+    if ((uint32_t)v >= (uint64_t)nslots || (uint32_t)ui >= (uint64_t)n_unique) {
         atomicOr(err, ERR_PLAN);
         tk.v_old_key[i] = -1;
         tk.v_old_lu[i] = -1;
@@ -308,21 +323,6 @@ __global__ void __launch_bounds__(BLOCK) k_evict(uint64_t *hash, uint32_t mask, 
     tk.v_old_key[i] = old;
     tk.v_old_lu[i] = last_use[v];
     if (old >= 0) hash_erase(hash, mask, (uint32_t)old);
-}
-
-// Place miss i in victim slot i and enter it in the Hit-Map.
-__global__ void __launch_bounds__(BLOCK) k_insert(uint64_t *hash, uint32_t mask, TicketDev tk,
-                                                  int64_t n, int64_t nslots, int64_t n_unique,
-                                                  int32_t *key_of_slot, int32_t *err)
-{
-    int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
-    if (i >= n) return;
-    const int32_t v = tk.v_slot[i];
-    const int32_t ui = tk.m_uidx[i];
-    if ((uint32_t)v >= (uint64_t)nslots || (uint32_t)ui >= (uint64_t)n_unique) {
-        atomicOr(err, ERR_PLAN);
-        return;
-    }
     const uint32_t key = tk.m_key[i];
     key_of_slot[v] = (int32_t)key;
     if (!hash_insert(hash, mask, key, v)) atomicOr(err, ERR_HASH_FULL);
@@ -335,11 +335,9 @@ void launch_commit(const Tables &tb, uint64_t *hash, uint32_t mask, TicketDev tk
 {
     if (n_miss <= 0) return;
     const int64_t nslots = tb.slot_base[tb.T];
-    dim3 g((unsigned)((n_miss + BLOCK - 1) / BLOCK));
-    hipLaunchKernelGGL(k_evict, g, dim3(BLOCK), 0, s, hash, mask, tk, n_miss, nslots,
-                       (const int32_t *)key_of_slot, (const int32_t *)last_use, &cnt->err);
-    hipLaunchKernelGGL(k_insert, g, dim3(BLOCK), 0, s, hash, mask, tk, n_miss, nslots, n_unique,
-                       key_of_slot, &cnt->err);
+    hipLaunchKernelGGL(k_commit, dim3((unsigned)((n_miss + BLOCK - 1) / BLOCK)), dim3(BLOCK), 0, s,
+                       hash, mask, tk, n_miss, nslots, n_unique, key_of_slot,
+                       (const int32_t *)last_use, &cnt->err_sticky);
 }
 
 // last_use = u for every slot the batch uses; slot_of[j] = slot of position j.

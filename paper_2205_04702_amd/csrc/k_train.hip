@@ -3,6 +3,8 @@
 // Row layout: Storage is fp32 [slots][D] in HBM; a row is D/4 float4 words
 // and LPR = D/4 lanes cover one row, so one wave64 touches 64/LPR rows per
 // pass with fully coalesced 16-byte loads.
+#include <hip/hip_ext.h>
+
 #include "sp_device.h"
 #include "sp_internal.h"
 
@@ -162,6 +164,8 @@ __global__ void __launch_bounds__(BLOCK) k_bwd_combine(float4 *__restrict__ stor
 // Copy the rows of occupied victim slots of one class into the staging rows
 // (row i of stage = victim i).  Class 1 = slots last used by the batch just
 // before this plan (their update may still be running), class 0 = the rest.
+// The class-0 launch also stores every victim's previous key after the n rows,
+// so that rows and keys leave the device in one copy.
 template <int LPR>
 __global__ void __launch_bounds__(BLOCK) k_pack(const float4 *__restrict__ storage, TicketDev tk,
                                                 int64_t n, int64_t nslots, int32_t u, int cls,
@@ -171,7 +175,9 @@ __global__ void __launch_bounds__(BLOCK) k_pack(const float4 *__restrict__ stora
     const int64_t i = t / LPR;
     const int c = (int)(t % LPR);
     if (i >= n) return;
-    if (tk.v_old_key[i] < 0) return;
+    const int32_t old = tk.v_old_key[i];
+    if (cls == 0 && c == 0) reinterpret_cast<int32_t *>(stage + n * LPR)[i] = old;
+    if (old < 0) return;
     const int32_t lu = tk.v_old_lu[i];
     if ((int)(lu >= 0 && lu == u - 1) != cls) return;
     const int32_t v = tk.v_slot[i];
@@ -244,28 +250,44 @@ void launch_fill(float *storage, int dim, const Tables &tb, float *const *host_d
                     tb.slot_base[tb.T], u, cls);
 }
 
+// Launches that may carry start/stop events: the events then time the kernel's
+// own execution on stream s (null events = plain launch).
+#define SP_DISPATCH_LPR_EV(D4, KERNEL, GRID, E0, E1, ...)                                        \
+    switch (D4) {                                                                                \
+    case 1: hipExtLaunchKernelGGL(KERNEL<1>, GRID, dim3(BLOCK), 0, s, E0, E1, 0, __VA_ARGS__); break;   \
+    case 2: hipExtLaunchKernelGGL(KERNEL<2>, GRID, dim3(BLOCK), 0, s, E0, E1, 0, __VA_ARGS__); break;   \
+    case 4: hipExtLaunchKernelGGL(KERNEL<4>, GRID, dim3(BLOCK), 0, s, E0, E1, 0, __VA_ARGS__); break;   \
+    case 8: hipExtLaunchKernelGGL(KERNEL<8>, GRID, dim3(BLOCK), 0, s, E0, E1, 0, __VA_ARGS__); break;   \
+    case 16: hipExtLaunchKernelGGL(KERNEL<16>, GRID, dim3(BLOCK), 0, s, E0, E1, 0, __VA_ARGS__); break; \
+    case 32: hipExtLaunchKernelGGL(KERNEL<32>, GRID, dim3(BLOCK), 0, s, E0, E1, 0, __VA_ARGS__); break; \
+    default: hipExtLaunchKernelGGL(KERNEL<64>, GRID, dim3(BLOCK), 0, s, E0, E1, 0, __VA_ARGS__); break; \
+    }
+
 void launch_forward(const float *storage, int dim, int64_t nslots, const int32_t *slot_of,
-                    const int32_t *bag_off, int64_t nbags, float *out, hipStream_t s)
+                    const int32_t *bag_off, int64_t nbags, float *out, hipStream_t s,
+                    hipEvent_t e0, hipEvent_t e1)
 {
     if (nbags <= 0) return;
-    SP_DISPATCH_LPR(dim / 4, k_forward, grid_waves(nbags), (const float4 *)storage, slot_of,
-                    bag_off, nbags, nslots, (float4 *)out);
+    SP_DISPATCH_LPR_EV(dim / 4, k_forward, grid_waves(nbags), e0, e1, (const float4 *)storage,
+                       slot_of, bag_off, nbags, nslots, (float4 *)out);
 }
 
 void launch_backward(float *storage, int dim, int64_t nslots, const BatchDev &b,
                      const int32_t *slot_u, int64_t n_unique, int64_t n_chunks, int chunk,
-                     const float *grad, int64_t nbags, float lr, float *partial, hipStream_t s)
+                     const float *grad, int64_t nbags, float lr, float *partial, hipStream_t s,
+                     hipEvent_t ev[4])
 {
     if (n_chunks <= 0) return;
     const int D4 = dim / 4;
-    SP_DISPATCH_LPR(D4, k_bwd_chunks, grid_waves(n_chunks), (float4 *)storage,
-                    (const int32_t *)b.seg_off, (const int32_t *)b.seg_chunk0,
-                    (const int32_t *)b.chunk_seg, (const int32_t *)b.sbag, slot_u, n_chunks, chunk,
-                    (const float4 *)grad, nbags, nslots, lr, (float4 *)partial);
+    SP_DISPATCH_LPR_EV(D4, k_bwd_chunks, grid_waves(n_chunks), ev[0], ev[1], (float4 *)storage,
+                       (const int32_t *)b.seg_off, (const int32_t *)b.seg_chunk0,
+                       (const int32_t *)b.chunk_seg, (const int32_t *)b.sbag, slot_u, n_chunks,
+                       chunk, (const float4 *)grad, nbags, nslots, lr, (float4 *)partial);
     if (n_chunks > n_unique)
-        SP_DISPATCH_LPR(D4, k_bwd_combine, grid_rows(n_unique, D4), (float4 *)storage,
-                        (const int32_t *)b.seg_off, (const int32_t *)b.seg_chunk0, slot_u, n_unique,
-                        chunk, (const float4 *)partial, nslots, lr);
+        SP_DISPATCH_LPR_EV(D4, k_bwd_combine, grid_rows(n_unique, D4), ev[2], ev[3],
+                           (float4 *)storage, (const int32_t *)b.seg_off,
+                           (const int32_t *)b.seg_chunk0, slot_u, n_unique, chunk,
+                           (const float4 *)partial, nslots, lr);
 }
 
 }  // namespace sp

@@ -1,6 +1,7 @@
 // Host-side declarations shared by the scratchpad library's translation units.
 #pragma once
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 namespace sp {
@@ -20,14 +21,19 @@ struct Tables {
 };
 
 // Counters written by the planning kernels and copied to the host once per plan.
+// Everything before err_sticky is cleared at the start of each plan;
+// err_sticky collects errors of later plan stages and is never cleared.
 struct DevCounters {
-    int32_t err;                 // ERR_* bits
+    int32_t err;                 // ERR_* bits of this plan's window (ids, offsets)
     int32_t n_unique;            // unique keys of the planned batch
     int32_t n_chunks;            // backward work chunks of the planned batch
     int32_t pad;
     int32_t miss[MAX_TABLES];
     int32_t held[MAX_TABLES];
+    int32_t err_sticky;          // ERR_HASH_FULL / ERR_PLAN from any earlier commit
+    int32_t pad2[3];
 };
+constexpr int COUNTERS_CLEARED = (int)(offsetof(DevCounters, err_sticky) / sizeof(int32_t));
 constexpr int32_t ERR_ID_RANGE = 1, ERR_OFFSETS = 2, ERR_HASH_FULL = 4, ERR_PLAN = 8;
 
 // One window-ring entry: a batch as it arrived plus its sort/dedup products.
@@ -40,7 +46,7 @@ struct BatchDev {
     int32_t *seg_off;                // [n_unique+1] start of each key's run in skeys
     int32_t *seg_chunk0;             // [n_unique] first backward chunk of each run
     int32_t *chunk_seg;              // [n_chunks] run of each chunk
-    int32_t *scal;                   // [0] n_unique, [1] n_chunks, [2..T+2] table starts in ukeys
+    int32_t *scal;                   // [0] n_unique, [1] n_chunks, [2] ERR_* bits of the batch
 };
 
 // Per-plan device buffers.
@@ -74,9 +80,10 @@ inline int chunk_positions(int dim) { return CHUNK_WAVES_ROWS * (64 / (dim / 4))
 // k_ingest.hip
 void launch_zero_i32(int32_t *p, int64_t n, hipStream_t s);
 void launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
-void launch_ingest(const Tables &tb, const BatchDev &b, int32_t B, int64_t nnz, int key_bits,
-                   int chunk, uint32_t *tmp_k, uint32_t *tmp_v, uint32_t *hist,
-                   void *scan_tmp, DevCounters *cnt, hipStream_t s);
+void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, const int32_t *bag_off,
+                   int32_t B, int64_t nnz, int key_bits, int chunk, uint32_t *tmp_k,
+                   uint32_t *tmp_v, uint32_t *hist, void *scan_tmp, hipStream_t s);
+void launch_publish(const DevCounters *cnt, DevCounters *host_mapped, hipStream_t s);
 void launch_radix_sort(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *v1, int64_t n,
                        int bits, uint32_t *hist, void *scan_tmp, bool *in_k1, hipStream_t s);
 int64_t radix_hist_entries(int64_t n);
@@ -107,9 +114,11 @@ void launch_pack(const float *storage, int dim, int64_t nslots, TicketDev tk, in
 void launch_fill(float *storage, int dim, const Tables &tb, float *const *host_dev, TicketDev tk,
                  int64_t n_miss, int32_t u, int cls, hipStream_t s);
 void launch_forward(const float *storage, int dim, int64_t nslots, const int32_t *slot_of,
-                    const int32_t *bag_off, int64_t nbags, float *out, hipStream_t s);
+                    const int32_t *bag_off, int64_t nbags, float *out, hipStream_t s,
+                    hipEvent_t e0, hipEvent_t e1);
 void launch_backward(float *storage, int dim, int64_t nslots, const BatchDev &b,
                      const int32_t *slot_u, int64_t n_unique, int64_t n_chunks, int chunk,
-                     const float *grad, int64_t nbags, float lr, float *partial, hipStream_t s);
+                     const float *grad, int64_t nbags, float lr, float *partial, hipStream_t s,
+                     hipEvent_t ev[4]);
 
 }  // namespace sp

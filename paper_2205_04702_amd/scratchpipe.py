@@ -49,10 +49,10 @@ class sp_batch(C.Structure):
 
 
 _STAT_I64 = ["plans", "updates", "lookups", "unique", "hits", "misses", "evictions", "bytes_fill",
-             "bytes_writeback", "hash_rebuilds", "min_capacity_margin", "device_bytes",
+             "bytes_writeback", "hash_rebuilds", "chunks", "min_capacity_margin", "device_bytes",
              "pinned_bytes"]
-_STAT_F64 = ["ms_forward", "ms_backward", "ms_plan", "ms_fill"]
-_STAT_CNT = ["timed_forward", "timed_backward", "timed_plan", "timed_fill"]
+_STAT_F64 = ["ms_forward", "ms_backward", "ms_combine", "ms_plan", "ms_fill"]
+_STAT_CNT = ["timed_forward", "timed_backward", "timed_combine", "timed_plan", "timed_fill"]
 
 
 class sp_stats(C.Structure):

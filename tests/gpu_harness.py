@@ -35,6 +35,37 @@ def compare_plan(step, dump, ref, T, B):
     assert dump["n_evict"] == ref.n_evict, f"step {step}: evictions {dump['n_evict']} vs {ref.n_evict}"
 
 
+def run_gpu(w, batches, host, first=0, last=None, flags=0, prepare_ahead=False):
+    """Train batches[first:last] on the GPU only (fresh context over `host`), then flush."""
+    import torch
+    dev = torch.device("cuda:0")
+    n = len(batches)
+    last = n if last is None else last
+    T, B, D, L = w.tables, w.batch, w.dim, w.lookahead
+    max_ids = max(int(b[0].size) for b in batches)
+    sp = ScratchPipe(w.rows, D, w.slots, L, host, max_batch=B, max_ids=max(max_ids, 1), flags=flags)
+    try:
+        out = torch.zeros((T * B, D), dtype=torch.float32, device=dev)
+        for u in range(first, last):
+            idx = list(range(u, min(u + L, last - 1) + 1))
+            if prepare_ahead and u + L + 1 < last:
+                idx.append(u + L + 1)
+            ticket = sp.plan([batches[q] for q in idx])
+            sp.forward(ticket, out)
+            sp.backward_update(ticket, torch.from_numpy(wl.grads(w, u)).to(dev), w.lr)
+        sp.flush()
+        return sp.stats()
+    finally:
+        sp.close()
+
+
+def fresh_host(w):
+    host = HostTables(w.rows, w.dim)
+    for t in range(w.tables):
+        wl.init_table(w, t, out=host[t])
+    return host
+
+
 def make_inputs(w, steps=None, ragged=None):
     n = w.steps if steps is None else steps
     if ragged:
@@ -46,8 +77,11 @@ def make_inputs(w, steps=None, ragged=None):
 
 def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all", flags=0,
                device_ids=False, ref_tables=None, sync_each_step=True, compare_tables=True,
-               return_tables=False, steps=None):
-    """Train w on the GPU and with the oracle; assert parity; return a summary."""
+               return_tables=False, steps=None, prepare_ahead=False):
+    """Train w on the GPU and with the oracle; assert parity; return a summary.
+
+    prepare_ahead: also hand the GPU the batch after the window (prepared in
+    advance, not held); the oracle always sees the plain window."""
     import torch
     dev = torch.device("cuda:0")
     if batches is None:
@@ -73,7 +107,8 @@ def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all"
         for u in range(n):
             win_idx = list(range(u, min(u + L, n - 1) + 1))
             src = dev_batches if device_ids else batches
-            ticket = sp.plan([src[q] for q in win_idx])
+            gpu_idx = win_idx + ([u + L + 1] if prepare_ahead and u + L + 1 < n else [])
+            ticket = sp.plan([src[q] for q in gpu_idx])
             assert ticket == u
             p = planner.plan([batches[q] for q in win_idx], B)
             if u in plan_set:

@@ -81,6 +81,19 @@ def test_single_table_single_slot_pressure(harness):
     harness.run_parity(w)
 
 
+@pytest.mark.parametrize("device_ids", [False, True])
+def test_prepared_ahead_batch_changes_nothing(harness, device_ids):
+    """Passing the batch after the window (prepared early, not held) gives the
+    same plans and tables as the plain window."""
+    w = wl.custom(rows=[2500, 4000], dim=64, batch=40, pooling=[4, 2], slots=[500, 600],
+                  lookahead=2, steps=20, dist=("zipf", 1.0), seed=21)
+    _say(f"case prepared-ahead device_ids={device_ids}")
+    a = harness.run_parity(w, return_tables=True)
+    b = harness.run_parity(w, prepare_ahead=True, device_ids=device_ids, return_tables=True)
+    for x, y in zip(a["tables"], b["tables"]):
+        assert np.array_equal(x, y)
+
+
 def test_device_resident_ids_match_host_ids(harness):
     w = wl.custom(rows=[3000, 3000], dim=32, batch=48, pooling=3, slots=[700, 700], lookahead=2,
                   steps=15, dist=("zipf", 1.0), seed=12)

@@ -133,11 +133,20 @@ def main():
                          flags=flags)
     out = torch.empty((w.tables * w.batch, w.dim), dtype=torch.float32, device=dev)
 
+    host_s = [0.0, 0.0, 0.0]  # host time inside plan / forward / backward calls
+
     def step(u):
         # hold window u..u+L, plus batch u+L+1 handed over early for sorting
+        t0 = time.perf_counter()
         tk = ctx.plan([batches[q] for q in range(u, min(u + L + 1, nb - 1) + 1)])
+        t1 = time.perf_counter()
         ctx.forward(tk, out)
+        t2 = time.perf_counter()
         ctx.backward_update(tk, grads[u], w.lr)
+        t3 = time.perf_counter()
+        host_s[0] += t1 - t0
+        host_s[1] += t2 - t1
+        host_s[2] += t3 - t2
 
     for u in range(W):
         step(u)
@@ -145,6 +154,7 @@ def main():
     s0 = ctx.stats()
     log(f"[bench] warmup {W} steps done")
     torch.cuda.synchronize()
+    host_s[:] = [0.0, 0.0, 0.0]
     t0 = time.perf_counter()
     for u in range(W, W + K):
         step(u)
@@ -177,18 +187,20 @@ def main():
               "unique_per_step": round(n_unique, 1),
               "evictions_per_step": round(d["evictions"] / K, 1),
               "fill_GBps": round(d["bytes_fill"] / dt / 1e9, 3),
-              "writeback_GBps": round(d["bytes_writeback"] / dt / 1e9, 3)}
+              "writeback_GBps": round(d["bytes_writeback"] / dt / 1e9, 3),
+              "host_ms_per_step": {"plan": round(host_s[0] * 1e3 / K, 4),
+                                   "forward": round(host_s[1] * 1e3 / K, 4),
+                                   "backward": round(host_s[2] * 1e3 / K, 4)}}
     if not args.no_timing and d["timed_forward"] > 0:
         # kernel execution times from start/stop events of the launches themselves
         fwd_ms = d["ms_forward"] / d["timed_forward"]
         bwd_ms = d["ms_backward"] / max(d["timed_backward"], 1)
-        cmb_ms = d["ms_combine"] / max(d["timed_combine"], 1)
         n_chunks = d["chunks"] / max(d["updates"], 1)
         kb = kernel_bytes(w, n_unique, n_chunks)
         fwd_gbs = kb["forward"] / (fwd_ms * 1e-3) / 1e9
         bwd_gbs = kb["backward"] / (bwd_ms * 1e-3) / 1e9
-        detail.update({"forward_ms": round(fwd_ms, 5), "backward_chunks_ms": round(bwd_ms, 5),
-                       "backward_combine_ms": round(cmb_ms, 5),
+        detail.update({"forward_ms": round(fwd_ms, 5), "backward_ms": round(bwd_ms, 5),
+                       "combine_ms": round(d["ms_combine"] / max(d["timed_combine"], 1), 5),
                        "combine_launches": d["timed_combine"],
                        "plan_ms": round(d["ms_plan"] / max(d["timed_plan"], 1), 5),
                        "fill_ms": round(d["ms_fill"] / max(d["timed_fill"], 1), 5),
@@ -200,7 +212,7 @@ def main():
         src_hash = hashlib.sha256(src).hexdigest()
         dom = "forward" if fwd_ms >= bwd_ms else "backward"
         ach = fwd_gbs if dom == "forward" else bwd_gbs
-        name = "k_forward" if dom == "forward" else "k_bwd_chunks"
+        name = "k_forward" if dom == "forward" else "k_backward"
         tr = traffic_from_profile(name, src_hash, w.name)
         res["roofline"] = {"bound": "hbm", "kernel": name,
                            "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",

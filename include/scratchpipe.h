@@ -88,9 +88,10 @@ typedef struct {
     int64_t min_capacity_margin;/* min over plans and tables of unheld slots - misses  */
     int64_t device_bytes;       /* device memory held by the context                    */
     int64_t pinned_bytes;       /* pinned staging held by the context                   */
-    /* SP_FLAG_TIMING only: summed time in ms and number of timed calls.  forward,
-     * backward (per-chunk kernel) and combine (multi-chunk runs) are kernel
-     * execution times; plan and fill span their whole launch sequences. */
+    /* SP_FLAG_TIMING only: summed time in ms and number of timed launches.
+     * forward, backward (per-chunk kernel) and combine (runs split over several
+     * chunks, launched only when there are any) are kernel execution times;
+     * plan and fill span their whole launch sequences. */
     double ms_forward, ms_backward, ms_combine, ms_plan, ms_fill;
     int64_t timed_forward, timed_backward, timed_combine, timed_plan, timed_fill;
 } sp_stats;

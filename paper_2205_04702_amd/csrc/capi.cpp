@@ -121,13 +121,102 @@ struct Job {
 };
 
 struct TicketHost {
-    int64_t nnz = 0, n_unique = 0, n_chunks = 0, n_miss = 0;
+    int64_t nnz = 0, n_unique = 0, n_chunks = 0, n_multi = 0, n_miss = 0;
     int32_t B = 0;
     int ring = 0;
     int nwin = 0;
 };
 
 thread_local std::string g_create_error;
+
+// Host threads that copy evicted rows from the pinned staging buffer into the
+// host tables (the CPU-side [Insert] of Sec. IV-B).  Rows land at random
+// places in tables far larger than any cache, so the copy is latency-bound
+// and spreads over several threads.
+class ScatterPool {
+  public:
+    void start(int nthreads, float *const *tables, int dim, int row_bits)
+    {
+        tables_ = tables;
+        dim_ = dim;
+        row_bits_ = row_bits;
+        for (int i = 0; i < nthreads; ++i) threads_.emplace_back([this, i, nthreads] { loop(i, nthreads); });
+    }
+    // Scatter n staged rows (row i goes to the table row named by keys[i];
+    // negative keys are skipped).  Returns the number of rows written.
+    int64_t run(const float *rows, const int32_t *keys, int64_t n)
+    {
+        if (threads_.empty() || n < 2048) return slice(rows, keys, 0, n);
+        std::unique_lock<std::mutex> lk(m_);
+        rows_ = rows;
+        keys_ = keys;
+        n_ = n;
+        written_ = 0;
+        pending_ = (int)threads_.size();
+        ++gen_;
+        cv_start_.notify_all();
+        cv_done_.wait(lk, [&] { return pending_ == 0; });
+        return written_;
+    }
+    void stop()
+    {
+        {
+            std::lock_guard<std::mutex> lk(m_);
+            stop_ = true;
+        }
+        cv_start_.notify_all();
+        for (auto &t : threads_) t.join();
+        threads_.clear();
+    }
+
+  private:
+    int64_t slice(const float *rows, const int32_t *keys, int64_t b, int64_t e) const
+    {
+        const uint32_t mask = (1u << row_bits_) - 1u;
+        const size_t row_bytes = sizeof(float) * (size_t)dim_;
+        int64_t w = 0;
+        for (int64_t i = b; i < e; ++i) {
+            const int32_t key = keys[i];
+            if (key < 0) continue;
+            memcpy(tables_[key >> row_bits_] + (int64_t)(key & mask) * dim_, rows + i * dim_,
+                   row_bytes);
+            ++w;
+        }
+        return w;
+    }
+    void loop(int id, int nthreads)
+    {
+        int64_t seen = 0;
+        for (;;) {
+            const float *rows;
+            const int32_t *keys;
+            int64_t n;
+            {
+                std::unique_lock<std::mutex> lk(m_);
+                cv_start_.wait(lk, [&] { return gen_ != seen || stop_; });
+                if (stop_) return;
+                seen = gen_;
+                rows = rows_;
+                keys = keys_;
+                n = n_;
+            }
+            const int64_t w = slice(rows, keys, n * id / nthreads, n * (id + 1) / nthreads);
+            std::lock_guard<std::mutex> lk(m_);
+            written_ += w;
+            if (--pending_ == 0) cv_done_.notify_one();
+        }
+    }
+    std::vector<std::thread> threads_;
+    std::mutex m_;
+    std::condition_variable cv_start_, cv_done_;
+    float *const *tables_ = nullptr;
+    int dim_ = 0, row_bits_ = 0;
+    const float *rows_ = nullptr;
+    const int32_t *keys_ = nullptr;
+    int64_t n_ = 0, written_ = 0, gen_ = 0;
+    int pending_ = 0;
+    bool stop_ = false;
+};
 
 }  // namespace
 
@@ -194,6 +283,7 @@ struct sp_ctx {
     hipError_t worker_err = hipSuccess;
     std::deque<std::pair<int64_t, int64_t>> deadlines;  // (ticket, first plan that may refill)
     int64_t wb_evictions = 0, wb_bytes = 0;
+    ScatterPool scatter;
 
     // bookkeeping
     sp_stats st{};
@@ -282,8 +372,6 @@ static sp_status palloc(sp_ctx *h, T **p, int64_t count)
 static void worker_main(sp_ctx *h)
 {
     (void)hipSetDevice(h->device);
-    const int rb = h->tb.row_bits;
-    const uint32_t mask = (1u << rb) - 1u;
     const size_t row_bytes = sizeof(float) * (size_t)h->D;
     for (;;) {
         Job j;
@@ -300,14 +388,7 @@ static void worker_main(sp_ctx *h)
                 std::lock_guard<std::mutex> lk(h->mu);
                 h->worker_err = e;
             } else {
-                for (int64_t i = 0; i < j.n; ++i) {
-                    const int32_t key = j.keys[i];
-                    if (key < 0) continue;
-                    const int t = key >> rb;
-                    const int64_t row = key & mask;
-                    memcpy(h->host[t] + row * h->D, j.rows + i * h->D, row_bytes);
-                    ++ev;
-                }
+                ev = h->scatter.run(j.rows, j.keys, j.n);
             }
         }
         {
@@ -343,6 +424,7 @@ static void release(sp_ctx *h)
         h->cv.notify_all();
         h->worker.join();
     }
+    h->scatter.stop();
     (void)hipDeviceSynchronize();
     for (auto &e : h->ring_free)
         if (e) hipEventDestroy(e);
@@ -443,6 +525,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
         TRY(dalloc(h, &b.seg_off, N + 1));
         TRY(dalloc(h, &b.seg_chunk0, N));
         TRY(dalloc(h, &b.chunk_seg, nchunk_max));
+        TRY(dalloc(h, &b.multi, N / (h->chunk + 1) + 2));
         TRY(dalloc(h, &b.scal, T + 3));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ring_free[r], hipEventDisableTiming));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ring_ready[r], hipEventDisableTiming));
@@ -517,6 +600,8 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     HIPCHK(nullptr, hipMemsetAsync(h->cnt, 0, sizeof(DevCounters), h->s_plan));
     HIPCHK(nullptr, hipStreamSynchronize(h->s_plan));
     h->st.min_capacity_margin = INT64_MAX;
+    const unsigned hw = std::thread::hardware_concurrency();
+    h->scatter.start((int)std::min(8u, std::max(1u, hw / 2)), h->host, h->D, h->tb.row_bits);
     h->worker = std::thread(worker_main, h);
     return SP_OK;
 }
@@ -706,6 +791,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     th.B = (int32_t)h->ring_B[r0];
     th.n_unique = c.n_unique;
     th.n_chunks = c.n_chunks;
+    th.n_multi = c.n_multi;
     th.n_miss = n_miss;
     th.ring = r0;
     th.nwin = nhold;
@@ -849,10 +935,10 @@ extern "C" sp_status sp_backward_update(sp_handle h, int64_t ticket, const float
     hipStream_t s = (hipStream_t)stream;
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
     if ((h->flags & SP_FLAG_TIMING) && th.n_chunks > 0) HIPCHK(h, h->t_bwd.take(&ev[0], &ev[1]));
-    if ((h->flags & SP_FLAG_TIMING) && th.n_chunks > th.n_unique)
+    if ((h->flags & SP_FLAG_TIMING) && th.n_chunks > 0 && th.n_multi > 0)
         HIPCHK(h, h->t_cmb.take(&ev[2], &ev[3]));
     launch_backward(h->storage, h->D, h->total_slots, h->ring[th.ring], h->tk[e].slot_u,
-                    th.n_unique, th.n_chunks, h->chunk, d_grad, (int64_t)h->T * th.B, lr,
+                    th.n_chunks, th.n_multi, h->chunk, d_grad, (int64_t)h->T * th.B, lr,
                     h->partial, s, ev);
     CHECK_LAUNCH(h);
     HIPCHK(h, hipEventRecord(h->ev_upd[e], s));

@@ -224,11 +224,12 @@ struct ChunkCount {
     }
 };
 struct ChunkOut {
-    int32_t *seg_chunk0, *chunk_seg, *scal;
+    int32_t *seg_chunk0, *chunk_seg, *multi, *scal;
     __device__ void operator()(int64_t s, uint32_t e, uint32_t v, int) const
     {
         seg_chunk0[s] = (int32_t)e;
         for (uint32_t c = 0; c < v; ++c) chunk_seg[e + c] = (int32_t)s;
+        if (v > 1) multi[atomicAdd(scal + 3, 1)] = (int32_t)s;  // list order is irrelevant
         if (s == scal[0] - 1) scal[1] = (int32_t)(e + v);
     }
 };
@@ -242,7 +243,7 @@ void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, cons
                    uint32_t *tmp_v, uint32_t *hist, void *scan_tmp, hipStream_t s)
 {
     const int64_t nbags = (int64_t)tb.T * B;
-    launch_zero_i32(b.scal, 3, s);
+    launch_zero_i32(b.scal, 4, s);
     // place the keys so that the final sort pass lands in skeys/perm
     const int passes = nnz > 1 ? (key_bits + 7) / 8 : 0;
     uint32_t *k0 = (passes & 1) ? tmp_k : b.skeys, *v0 = (passes & 1) ? tmp_v : b.perm;
@@ -262,7 +263,7 @@ void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, cons
                            nnz},
                  (uint32_t *)scan_tmp, (uint32_t *)nullptr, s);
         seg_scan(SegDevN{b.scal}, 1, nnz, ChunkCount{b.seg_off, chunk},
-                 ChunkOut{b.seg_chunk0, b.chunk_seg, b.scal}, (uint32_t *)scan_tmp,
+                 ChunkOut{b.seg_chunk0, b.chunk_seg, b.multi, b.scal}, (uint32_t *)scan_tmp,
                  (uint32_t *)nullptr, s);
     }
 }

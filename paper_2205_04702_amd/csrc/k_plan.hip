@@ -31,6 +31,7 @@ __global__ void __launch_bounds__(BLOCK) k_probe_hold(int32_t row_bits, const ui
     if (w == 0 && i == 0) {
         cnt->n_unique = scal0[0];
         cnt->n_chunks = scal0[1];
+        cnt->n_multi = scal0[3];
     }
     if (i == 0 && pa.nu[w][2]) atomicOr(&cnt->err, pa.nu[w][2]);  // the batch's input errors
     const bool valid = i < *pa.nu[w];

@@ -85,78 +85,98 @@ __global__ void __launch_bounds__(BLOCK) k_forward(const float4 *__restrict__ st
 
 // ---------------------------------------------------------------- backward + SGD
 
-// One wave per chunk of a run of equal keys: sum the gradients of the bags at
-// the chunk's sorted positions (ascending position order within each lane
-// group).  A run that fits one chunk updates its Storage row directly
-// (W -= lr * g); longer runs leave per-chunk partial sums for k_bwd_combine.
-template <int LPR>
-__global__ void __launch_bounds__(BLOCK) k_bwd_chunks(float4 *__restrict__ storage,
-                                                      const int32_t *__restrict__ seg_off,
-                                                      const int32_t *__restrict__ seg_chunk0,
-                                                      const int32_t *__restrict__ chunk_seg,
-                                                      const int32_t *__restrict__ sbag,
-                                                      const int32_t *__restrict__ slot_u,
-                                                      int64_t n_chunks, int chunk,
-                                                      const float4 *__restrict__ grad,
-                                                      int64_t nbags, int64_t nslots, float lr,
-                                                      float4 *__restrict__ partial)
+__device__ __forceinline__ void sgd_row(float4 *w, float4 g, float lr)
 {
-    const int64_t ch = (int64_t)blockIdx.x * (BLOCK / WAVE) + wave_id();
-    if (ch >= n_chunks) return;
+    float4 x = *w;
+    x.x = fmaf(-lr, g.x, x.x);
+    x.y = fmaf(-lr, g.y, x.y);
+    x.z = fmaf(-lr, g.z, x.z);
+    x.w = fmaf(-lr, g.w, x.w);
+    *w = x;
+}
+
+// Gradient coalescing and SGD (Sec. II-B "Backpropagation").  The sorted
+// positions of one batch form runs of equal keys; each run is cut into chunks
+// of at most `chunk` positions.  One group of LPR lanes (one row width) takes
+// one chunk, so a wave works on 64/LPR chunks at once: it sums the gradient
+// rows of the bags at its positions in ascending position order.
+//  * a run of one chunk updates its Storage row directly: W -= lr * g;
+//  * a longer run stores per-chunk partial sums, which k_bwd_combine adds in
+//    chunk order before updating the row (the kernel boundary orders the two).
+template <int LPR>
+__global__ void __launch_bounds__(BLOCK) k_backward(float4 *__restrict__ storage,
+                                                    const int32_t *__restrict__ seg_off,
+                                                    const int32_t *__restrict__ seg_chunk0,
+                                                    const int32_t *__restrict__ chunk_seg,
+                                                    const int32_t *__restrict__ sbag,
+                                                    const int32_t *__restrict__ slot_u,
+                                                    int64_t n_chunks, int chunk,
+                                                    const float4 *__restrict__ grad,
+                                                    int64_t nbags, int64_t nslots, float lr,
+                                                    float4 *__restrict__ partial)
+{
+    const int64_t t = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    const int64_t ch = t / LPR;
+    const int c = (int)(t % LPR);
+    if (ch >= n_chunks) return;  // whole lane groups leave together
     const int32_t s = chunk_seg[ch];
     const int64_t s0 = seg_off[s], s1 = seg_off[s + 1];
-    const int64_t p0 = s0 + (ch - seg_chunk0[s]) * (int64_t)chunk;
+    const int64_t c0 = seg_chunk0[s];
+    const int32_t slot = slot_u[s];
+    const int64_t p0 = s0 + (ch - c0) * (int64_t)chunk;
     const int64_t p1 = (p0 + chunk) < s1 ? (p0 + chunk) : s1;
-    float4 acc = gather_sum<LPR, 4>(grad, nbags, sbag, p0, p1);
-    acc = reduce_rows<LPR>(acc);
-    const int lane = lane_id();
-    if (lane >= LPR) return;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    int64_t p = p0;
+    for (; p + 4 <= p1; p += 4) {
+        int32_t b[4];
+        float4 v[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            b[q] = sbag[p + q];
+            b[q] = (uint32_t)b[q] < (uint64_t)nbags ? b[q] : 0;
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] = grad[(int64_t)b[q] * LPR + c];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc = f4_add(acc, v[q]);
+    }
+    for (; p < p1; ++p) {
+        int32_t b = sbag[p];
+        b = (uint32_t)b < (uint64_t)nbags ? b : 0;
+        acc = f4_add(acc, grad[(int64_t)b * LPR + c]);
+    }
     const int64_t nch = (s1 - s0 + chunk - 1) / chunk;
-    if (nch == 1) {
-        const int32_t slot = slot_u[s];
-        if ((uint32_t)slot >= (uint64_t)nslots) return;
-        float4 *w = storage + (int64_t)slot * LPR + lane;
-        float4 x = *w;
-        x.x = fmaf(-lr, acc.x, x.x);
-        x.y = fmaf(-lr, acc.y, x.y);
-        x.z = fmaf(-lr, acc.z, x.z);
-        x.w = fmaf(-lr, acc.w, x.w);
-        *w = x;
-    } else {
-        partial[ch * LPR + lane] = acc;
+    if (nch > 1) {
+        partial[ch * LPR + c] = acc;
+    } else if ((uint32_t)slot < (uint64_t)nslots) {
+        sgd_row(storage + (int64_t)slot * LPR + c, acc, lr);
     }
 }
 
-// Runs split over several chunks: add the chunk partials in chunk order and
-// update.  LPR threads per run.
+// Runs longer than one chunk (listed in `multi`, any order): add the chunk
+// partials in chunk order and update the row.  One lane group per run.
 template <int LPR>
 __global__ void __launch_bounds__(BLOCK) k_bwd_combine(float4 *__restrict__ storage,
+                                                       const int32_t *__restrict__ multi,
+                                                       int64_t n_multi,
                                                        const int32_t *__restrict__ seg_off,
                                                        const int32_t *__restrict__ seg_chunk0,
                                                        const int32_t *__restrict__ slot_u,
-                                                       int64_t n_unique, int chunk,
+                                                       int chunk,
                                                        const float4 *__restrict__ partial,
                                                        int64_t nslots, float lr)
 {
-    const int64_t tid = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
-    const int64_t s = tid / LPR;
-    const int c = (int)(tid % LPR);
-    if (s >= n_unique) return;
-    const int64_t len = seg_off[s + 1] - seg_off[s];
-    const int64_t nch = (len + chunk - 1) / chunk;
-    if (nch <= 1) return;
+    const int64_t t = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    const int64_t m = t / LPR;
+    const int c = (int)(t % LPR);
+    if (m >= n_multi) return;
+    const int32_t s = multi[m];
+    const int64_t nch = (seg_off[s + 1] - seg_off[s] + chunk - 1) / chunk;
     const int64_t c0 = seg_chunk0[s];
-    float4 acc = partial[c0 * LPR + c];
-    for (int64_t q = 1; q < nch; ++q) acc = f4_add(acc, partial[(c0 + q) * LPR + c]);
     const int32_t slot = slot_u[s];
-    if ((uint32_t)slot >= (uint64_t)nslots) return;
-    float4 *w = storage + (int64_t)slot * LPR + c;
-    float4 x = *w;
-    x.x = fmaf(-lr, acc.x, x.x);
-    x.y = fmaf(-lr, acc.y, x.y);
-    x.z = fmaf(-lr, acc.z, x.z);
-    x.w = fmaf(-lr, acc.w, x.w);
-    *w = x;
+    float4 sum = partial[c0 * LPR + c];
+    for (int64_t q = 1; q < nch; ++q) sum = f4_add(sum, partial[(c0 + q) * LPR + c]);
+    if ((uint32_t)slot < (uint64_t)nslots) sgd_row(storage + (int64_t)slot * LPR + c, sum, lr);
 }
 
 // ---------------------------------------------------------------- evict / fill
@@ -273,21 +293,21 @@ void launch_forward(const float *storage, int dim, int64_t nslots, const int32_t
 }
 
 void launch_backward(float *storage, int dim, int64_t nslots, const BatchDev &b,
-                     const int32_t *slot_u, int64_t n_unique, int64_t n_chunks, int chunk,
+                     const int32_t *slot_u, int64_t n_chunks, int64_t n_multi, int chunk,
                      const float *grad, int64_t nbags, float lr, float *partial, hipStream_t s,
                      hipEvent_t ev[4])
 {
     if (n_chunks <= 0) return;
     const int D4 = dim / 4;
-    SP_DISPATCH_LPR_EV(D4, k_bwd_chunks, grid_waves(n_chunks), ev[0], ev[1], (float4 *)storage,
+    SP_DISPATCH_LPR_EV(D4, k_backward, grid_rows(n_chunks, D4), ev[0], ev[1], (float4 *)storage,
                        (const int32_t *)b.seg_off, (const int32_t *)b.seg_chunk0,
                        (const int32_t *)b.chunk_seg, (const int32_t *)b.sbag, slot_u, n_chunks,
                        chunk, (const float4 *)grad, nbags, nslots, lr, (float4 *)partial);
-    if (n_chunks > n_unique)
-        SP_DISPATCH_LPR_EV(D4, k_bwd_combine, grid_rows(n_unique, D4), ev[2], ev[3],
-                           (float4 *)storage, (const int32_t *)b.seg_off,
-                           (const int32_t *)b.seg_chunk0, slot_u, n_unique, chunk,
-                           (const float4 *)partial, nslots, lr);
+    if (n_multi > 0)
+        SP_DISPATCH_LPR_EV(D4, k_bwd_combine, grid_rows(n_multi, D4), ev[2], ev[3],
+                           (float4 *)storage, (const int32_t *)b.multi, n_multi,
+                           (const int32_t *)b.seg_off, (const int32_t *)b.seg_chunk0, slot_u,
+                           chunk, (const float4 *)partial, nslots, lr);
 }
 
 }  // namespace sp

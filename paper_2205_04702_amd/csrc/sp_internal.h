@@ -27,7 +27,7 @@ struct DevCounters {
     int32_t err;                 // ERR_* bits of this plan's window (ids, offsets)
     int32_t n_unique;            // unique keys of the planned batch
     int32_t n_chunks;            // backward work chunks of the planned batch
-    int32_t pad;
+    int32_t n_multi;             // its runs longer than one chunk
     int32_t miss[MAX_TABLES];
     int32_t held[MAX_TABLES];
     int32_t err_sticky;          // ERR_HASH_FULL / ERR_PLAN from any earlier commit
@@ -46,7 +46,8 @@ struct BatchDev {
     int32_t *seg_off;                // [n_unique+1] start of each key's run in skeys
     int32_t *seg_chunk0;             // [n_unique] first backward chunk of each run
     int32_t *chunk_seg;              // [n_chunks] run of each chunk
-    int32_t *scal;                   // [0] n_unique, [1] n_chunks, [2] ERR_* bits of the batch
+    int32_t *multi;                  // [n_multi] runs longer than one chunk (any order)
+    int32_t *scal;                   // [0] n_unique, [1] n_chunks, [2] ERR_* bits, [3] n_multi
 };
 
 // Per-plan device buffers.
@@ -72,9 +73,9 @@ struct SelArgs {
     int32_t vbase[MAX_TABLES];       // first victim index of the table
 };
 
-constexpr int CHUNK_WAVES_ROWS = 8;  // backward chunk = 8 passes of a wave over rows
-
-inline int chunk_positions(int dim) { return CHUNK_WAVES_ROWS * (64 / (dim / 4)); }
+// Positions per backward chunk: one lane group sums at most this many
+// gradient rows before a run is split across groups.
+inline int chunk_positions(int /*dim*/) { return 16; }
 
 // ---------------------------------------------------------------- launchers
 // k_ingest.hip
@@ -117,7 +118,7 @@ void launch_forward(const float *storage, int dim, int64_t nslots, const int32_t
                     const int32_t *bag_off, int64_t nbags, float *out, hipStream_t s,
                     hipEvent_t e0, hipEvent_t e1);
 void launch_backward(float *storage, int dim, int64_t nslots, const BatchDev &b,
-                     const int32_t *slot_u, int64_t n_unique, int64_t n_chunks, int chunk,
+                     const int32_t *slot_u, int64_t n_chunks, int64_t n_multi, int chunk,
                      const float *grad, int64_t nbags, float lr, float *partial, hipStream_t s,
                      hipEvent_t ev[4]);
 

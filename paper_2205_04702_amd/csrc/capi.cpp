@@ -244,6 +244,7 @@ struct sp_ctx {
     std::vector<int64_t> ring_batch, ring_nnz, ring_B;
     std::vector<hipEvent_t> ring_free;      // backward of the entry's batch issued
     std::vector<hipEvent_t> ring_ready;     // ingest of the entry's batch finished
+    hipEvent_t ev_consumed = nullptr;       // last ingest has read the caller's arrays
 
     // tickets
     TicketDev tk[TICKETS]{};
@@ -430,6 +431,7 @@ static void release(sp_ctx *h)
         if (e) hipEventDestroy(e);
     for (auto &e : h->ring_ready)
         if (e) hipEventDestroy(e);
+    if (h->ev_consumed) hipEventDestroy(h->ev_consumed);
     for (int i = 0; i < TICKETS; ++i) {
         if (h->ev_planned[i]) hipEventDestroy(h->ev_planned[i]);
         if (h->ev_filled[i]) hipEventDestroy(h->ev_filled[i]);
@@ -524,7 +526,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
         TRY(dalloc(h, &b.inv, N));
         TRY(dalloc(h, &b.seg_off, N + 1));
         TRY(dalloc(h, &b.seg_chunk0, N));
-        TRY(dalloc(h, &b.chunk_seg, nchunk_max));
+        TRY(dalloc(h, &b.chunk_desc, nchunk_max));
         TRY(dalloc(h, &b.multi, N / (h->chunk + 1) + 2));
         TRY(dalloc(h, &b.scal, T + 3));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ring_free[r], hipEventDisableTiming));
@@ -580,6 +582,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
         HIPCHK(nullptr, hipHostGetDevicePointer((void **)&h->h_cnt_dev, p, 0));
     }
 
+    HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_consumed, hipEventDisableTiming));
     HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_plan, hipStreamNonBlocking));
     HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_ingest, hipStreamNonBlocking));
     HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_move, hipStreamNonBlocking));
@@ -696,7 +699,7 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
         off = b.bag_off;
     }
     launch_ingest(h->tb, b, ids, off, bt.batch, bt.nnz, h->key_bits, h->chunk, h->itmp_k,
-                  h->itmp_v, h->ihist, h->iscan_tmp, h->s_ingest);
+                  h->itmp_v, h->ihist, h->iscan_tmp, h->ev_consumed, h->s_ingest);
     CHECK_LAUNCH(h);
     HIPCHK(h, hipEventRecord(h->ring_ready[r], h->s_ingest));
     h->ring_batch[r] = q;
@@ -728,15 +731,27 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     TicketHost &th = h->tkh[e];
     const bool timing = h->flags & SP_FLAG_TIMING;
 
-    // ---- ingest (own stream): every window batch not in the ring yet; with a
-    // prepared-ahead batch this is normally just that one, off the plan's path
+    // ---- ingest (own stream): held batches not in the ring yet (normally
+    // none once batches are handed over one step early) go now, before the
+    // query that needs them; the prepared-ahead batch goes after the query
+    // has been enqueued, so its launches overlap the query on the GPU
+    bool consumed = false;
+    struct ConsumedGuard {  // the window buffers are the caller's again when we return
+        sp_ctx *h;
+        const bool *flag;
+        ~ConsumedGuard()
+        {
+            if (*flag) (void)hipEventSynchronize(h->ev_consumed);
+        }
+    } guard{h, &consumed};
     for (int w = 0; w < n; ++w) {
         const int64_t q = k + w;
         const int r = (int)(q % h->nring);
-        if (h->ring_batch[r] != q) {
-            TRY(ingest(h, window[w], q));
-        } else if (h->ring_nnz[r] != window[w].nnz || h->ring_B[r] != window[w].batch) {
+        if (h->ring_batch[r] == q && (h->ring_nnz[r] != window[w].nnz || h->ring_B[r] != window[w].batch))
             return fail(h, SP_ERR_INVALID_ARG, "batch %lld changed shape between windows", (long long)q);
+        if (w < nhold && h->ring_batch[r] != q) {
+            TRY(ingest(h, window[w], q));
+            consumed = true;
         }
     }
 
@@ -761,6 +776,10 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
                       tk, h->cnt, h->ring[r0].scal, h->s_plan);
     launch_publish(h->cnt, h->h_cnt_dev, h->s_plan);
     CHECK_LAUNCH(h);
+    if (n > nhold && h->ring_batch[(k + nhold) % h->nring] != k + nhold) {
+        TRY(ingest(h, window[nhold], k + nhold));
+        consumed = true;
+    }
     HIPCHK(h, hipStreamSynchronize(h->s_plan));
     DevCounters c;
     memcpy(&c, (const void *)h->h_cnt, sizeof c);

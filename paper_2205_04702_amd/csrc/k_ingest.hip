@@ -80,70 +80,161 @@ __global__ void __launch_bounds__(BLOCK) k_prepare(Tables tb, const int32_t *ids
 // the histogram table, then a scatter in which every tile ranks its keys per
 // digit with wave ballots, round by round, so equal digits keep input order.
 
+// Digits are up to RS_MAXBITS wide; a key of b bits takes ceil(b / 11) passes
+// of ceil(b / passes) bits each.
 constexpr int RS_ITEMS = 8;
 constexpr int RS_TILE = BLOCK * RS_ITEMS;
+constexpr int RS_MAXBITS = 11;
+constexpr int RS_MAXBINS = 1 << RS_MAXBITS;
+// One-launch passes when every block can afford to read the whole
+// (bins x tiles) histogram table.
+constexpr int64_t RS_FUSED_TABLE = 16384;
 
-int64_t radix_hist_entries(int64_t n) { return 256 * ((n + RS_TILE - 1) / RS_TILE + 1); }
-
-__global__ void __launch_bounds__(BLOCK) k_radix_hist(const uint32_t *keys, int64_t n, int shift,
-                                                      uint32_t *hist, int tiles)
+int radix_passes(int64_t n, int bits)
 {
-    __shared__ uint32_t h[256];
-    h[threadIdx.x] = 0;
-    __syncthreads();
-    int64_t base = (int64_t)blockIdx.x * RS_TILE;
-    for (int r = 0; r < RS_ITEMS; ++r) {
-        int64_t i = base + (int64_t)r * BLOCK + threadIdx.x;
-        if (i < n) atomicAdd(&h[(keys[i] >> shift) & 255u], 1u);
-    }
-    __syncthreads();
-    hist[(int64_t)threadIdx.x * tiles + blockIdx.x] = h[threadIdx.x];
+    return (n <= 1 || bits <= 0) ? 0 : (bits + RS_MAXBITS - 1) / RS_MAXBITS;
 }
 
-__global__ void __launch_bounds__(BLOCK) k_radix_scatter(const uint32_t *kin, const uint32_t *vin,
-                                                         int64_t n, int shift,
-                                                         const uint32_t *offs, int tiles,
-                                                         uint32_t *kout, uint32_t *vout)
+int64_t radix_hist_entries(int64_t n)
 {
-    __shared__ uint32_t base[256];
-    __shared__ uint32_t wc[BLOCK / WAVE][256];
-    const int tid = threadIdx.x, w = wave_id();
-    const uint64_t lt = lanemask_lt();
-    base[tid] = offs[(int64_t)tid * tiles + blockIdx.x];
-    const int64_t tbase = (int64_t)blockIdx.x * RS_TILE;
+    const int64_t tiles = (n + RS_TILE - 1) / RS_TILE + 1;
+    const int64_t big = (int64_t)RS_MAXBINS * tiles;
+    return big > 4 * RS_FUSED_TABLE ? big : 4 * RS_FUSED_TABLE;
+}
+
+// hist[d * tiles + tile] = keys of the tile with digit d.  With zero_from /
+// zero_n, also clears a range (the histograms later passes accumulate into).
+__global__ void __launch_bounds__(BLOCK) k_radix_hist(const uint32_t *keys, int64_t n, int shift,
+                                                      int dbits, uint32_t *hist, int tiles,
+                                                      uint32_t *zero_from, int64_t zero_n)
+{
+    __shared__ uint32_t h[RS_MAXBINS];
+    const int bins = 1 << dbits;
+    const uint32_t mask = (uint32_t)bins - 1u;
+    for (int d = threadIdx.x; d < bins; d += BLOCK) h[d] = 0;
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * RS_TILE;
     for (int r = 0; r < RS_ITEMS; ++r) {
-        int64_t i = tbase + (int64_t)r * BLOCK + tid;
-        bool valid = i < n;
-        uint32_t k = valid ? kin[i] : 0u;
-        uint32_t v = valid ? vin[i] : 0u;
-        uint32_t d = (k >> shift) & 255u;
+        const int64_t i = base + (int64_t)r * BLOCK + threadIdx.x;
+        if (i < n) atomicAdd(&h[(keys[i] >> shift) & mask], 1u);
+    }
+    __syncthreads();
+    for (int d = threadIdx.x; d < bins; d += BLOCK) hist[(int64_t)d * tiles + blockIdx.x] = h[d];
+    for (int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x; i < zero_n;
+         i += (int64_t)gridDim.x * BLOCK)
+        zero_from[i] = 0;
+}
+
+// Stable scatter of one tile by one digit.  Keys are ranked round by round
+// (256 keys per round, in input order): lanes of a wave with the same digit
+// find each other with one ballot per digit bit; the lowest of them records
+// the wave's count for that digit, stamped with the round, so stale counts of
+// earlier rounds read as zero and nothing has to be cleared between rounds.
+// base[d] is where the tile's next key of digit d goes.
+//  FUSED: base comes from the raw per-tile histogram table (this block sums
+//  its column prefix and the digit totals), and the scatter adds each key to
+//  the next pass's histogram at its output tile, so a pass is one launch.
+//  Otherwise base comes from a scanned (exclusive, digit-major) table.
+template <bool FUSED>
+__global__ void __launch_bounds__(BLOCK) k_radix_scatter(const uint32_t *kin, const uint32_t *vin,
+                                                         int64_t n, int shift, int dbits,
+                                                         const uint32_t *table, int tiles,
+                                                         uint32_t *kout, uint32_t *vout,
+                                                         uint32_t *hist_next, int shift_next,
+                                                         int dbits_next)
+{
+    __shared__ uint32_t base[RS_MAXBINS];
+    __shared__ uint32_t wc[BLOCK / WAVE][RS_MAXBINS];
+    __shared__ uint32_t lds[BLOCK / WAVE];
+    const int tid = threadIdx.x, w = wave_id(), lane = lane_id();
+    const int bins = 1 << dbits;
+    const uint32_t mask = (uint32_t)bins - 1u;
+    const int tile = blockIdx.x;
+    if (FUSED) {
+        // digit totals into wc[0], this tile's column prefix into base
+        for (int d = tid; d < bins; d += BLOCK) {
+            const uint32_t *row = table + (int64_t)d * tiles;
+            uint32_t before = 0, total = 0;
+            for (int t = 0; t < tiles; ++t) {
+                const uint32_t x = row[t];
+                before += t < tile ? x : 0u;
+                total += x;
+            }
+            base[d] = before;
+            wc[0][d] = total;
+        }
+        __syncthreads();
+        // exclusive scan of the digit totals: thread tid owns bins/BLOCK
+        // consecutive digits (or one digit when bins < BLOCK)
+        const int per = bins >= BLOCK ? bins / BLOCK : 1;
+        const int d0 = tid * per;
+        uint32_t mine = 0;
+        for (int q = 0; q < per; ++q)
+            if (d0 + q < bins) mine += wc[0][d0 + q];
+        uint32_t total;
+        uint32_t run = block_excl_scan(mine, lds, total);
+        for (int q = 0; q < per; ++q)
+            if (d0 + q < bins) {
+                const uint32_t x = wc[0][d0 + q];
+                base[d0 + q] += run;
+                run += x;
+            }
+    } else {
+        for (int d = tid; d < bins; d += BLOCK) base[d] = table[(int64_t)d * tiles + tile];
+    }
+    __syncthreads();
+    for (int q = 0; q < BLOCK / WAVE; ++q)
+        for (int d = tid; d < bins; d += BLOCK) wc[q][d] = 0;
+    __syncthreads();
+
+    const uint64_t lt = lanemask_lt();
+    const int64_t tbase = (int64_t)tile * RS_TILE;
+    const int tiles_out = (int)((n + RS_TILE - 1) / RS_TILE);
+    const uint32_t mask_next = (1u << dbits_next) - 1u;
+    for (int r = 0; r < RS_ITEMS; ++r) {
+        const uint32_t stamp = (uint32_t)(r + 1) << 16;
+        const int64_t i = tbase + (int64_t)r * BLOCK + tid;
+        const bool valid = i < n;
+        const uint32_t k = valid ? kin[i] : 0u;
+        const uint32_t v = valid ? vin[i] : 0u;
+        const uint32_t d = (k >> shift) & mask;
         uint64_t peers = __ballot(valid);
-#pragma unroll
-        for (int b = 0; b < 8; ++b) {
-            uint32_t bit = (d >> b) & 1u;
-            uint64_t bb = __ballot(bit);
+        for (int b = 0; b < dbits; ++b) {
+            const uint32_t bit = (d >> b) & 1u;
+            const uint64_t bb = __ballot(bit);
             peers &= bit ? bb : ~bb;
         }
-#pragma unroll
-        for (int q = 0; q < BLOCK / WAVE; ++q) wc[q][tid] = 0;
+        const int leader = valid ? __ffsll((unsigned long long)peers) - 1 : lane;
+        const bool is_leader = valid && leader == lane;
+        if (is_leader) wc[w][d] = stamp | (uint32_t)__popcll(peers);
         __syncthreads();
-        if (valid && (peers & lt) == 0) wc[w][d] = (uint32_t)__popcll(peers);
-        __syncthreads();
-        {
-            uint32_t run = base[tid];
-#pragma unroll
+        uint32_t start = 0;
+        bool last_wave = false;
+        uint32_t total = 0;
+        if (is_leader) {
+            uint32_t before = 0;
+            last_wave = true;
             for (int q = 0; q < BLOCK / WAVE; ++q) {
-                uint32_t c = wc[q][tid];
-                wc[q][tid] = run;
-                run += c;
+                const uint32_t e = wc[q][d];
+                const uint32_t c = (e & 0xFFFF0000u) == stamp ? (e & 0xFFFFu) : 0u;
+                if (q < w) before += c;
+                if (q > w && c) last_wave = false;
+                total += c;
             }
-            base[tid] = run;
+            start = base[d] + before;
         }
-        __syncthreads();
+        start = __shfl(start, leader, WAVE);
+        __syncthreads();  // every leader has read base[d]
+        if (is_leader && last_wave) base[d] += total;
         if (valid) {
-            uint32_t p = wc[w][d] + (uint32_t)__popcll(peers & lt);
+            uint32_t p = start + (uint32_t)__popcll(peers & lt);
+            p = p < (uint64_t)n ? p : (uint32_t)(n - 1);  // never write past the output
             kout[p] = k;
             vout[p] = v;
+            if (FUSED && hist_next)
+                atomicAdd(&hist_next[(int64_t)((k >> shift_next) & mask_next) * tiles_out +
+                                     p / RS_TILE],
+                          1u);
         }
         __syncthreads();
     }
@@ -158,26 +249,45 @@ struct OutU32 {
     __device__ void operator()(int64_t i, uint32_t e, uint32_t, int) const { p[i] = e; }
 };
 
-// Sorts (k0, v0) by key; k1/v1 are scratch of the same size.  *in_k1 tells
-// where the result ends up.
+// Sorts (k0, v0) by key (LSD, stable); k1/v1 are scratch of the same size.
+// The result is in k1/v1 when radix_passes(n, bits) is odd (*in_k1).
 void launch_radix_sort(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *v1, int64_t n,
                        int bits, uint32_t *hist, void *scan_tmp, bool *in_k1, hipStream_t s)
 {
     *in_k1 = false;
-    if (n <= 1 || bits <= 0) return;
-    const int passes = (bits + 7) / 8;
+    const int passes = radix_passes(n, bits);
+    if (passes == 0) return;
+    const int dbits = (bits + passes - 1) / passes;
+    const int bins = 1 << dbits;
     const int tiles = (int)((n + RS_TILE - 1) / RS_TILE);
+    const int64_t table = (int64_t)bins * tiles;
     uint32_t *ki = k0, *vi = v0, *ko = k1, *vo = v1;
-    for (int p = 0; p < passes; ++p) {
-        int shift = 8 * p;
-        hipLaunchKernelGGL(k_radix_hist, dim3(tiles), dim3(BLOCK), 0, s, ki, n, shift, hist, tiles);
-        seg_scan(SegN{(int64_t)256 * tiles}, 1, (int64_t)256 * tiles, ValU32{hist}, OutU32{hist},
-                 (uint32_t *)scan_tmp, (uint32_t *)nullptr, s, true);
-        hipLaunchKernelGGL(k_radix_scatter, dim3(tiles), dim3(BLOCK), 0, s, ki, vi, n, shift,
-                           hist, tiles, ko, vo);
-        uint32_t *t;
-        t = ki, ki = ko, ko = t;
-        t = vi, vi = vo, vo = t;
+    if (table <= RS_FUSED_TABLE) {
+        // hist + P one-launch passes; pass p reads table p and fills table p+1
+        hipLaunchKernelGGL(k_radix_hist, dim3(tiles), dim3(BLOCK), 0, s, ki, n, 0, dbits, hist,
+                           tiles, hist + table, table * (passes - 1));
+        for (int p = 0; p < passes; ++p) {
+            uint32_t *next = p + 1 < passes ? hist + table * (p + 1) : nullptr;
+            hipLaunchKernelGGL(k_radix_scatter<true>, dim3(tiles), dim3(BLOCK), 0, s, ki, vi, n,
+                               dbits * p, dbits, hist + table * p, tiles, ko, vo, next,
+                               dbits * (p + 1), dbits);
+            uint32_t *t;
+            t = ki, ki = ko, ko = t;
+            t = vi, vi = vo, vo = t;
+        }
+    } else {
+        for (int p = 0; p < passes; ++p) {
+            const int shift = dbits * p;
+            hipLaunchKernelGGL(k_radix_hist, dim3(tiles), dim3(BLOCK), 0, s, ki, n, shift, dbits,
+                               hist, tiles, (uint32_t *)nullptr, (int64_t)0);
+            seg_scan(SegN{table}, 1, table, ValU32{hist}, OutU32{hist}, (uint32_t *)scan_tmp,
+                     (uint32_t *)nullptr, s, true);
+            hipLaunchKernelGGL(k_radix_scatter<false>, dim3(tiles), dim3(BLOCK), 0, s, ki, vi, n,
+                               shift, dbits, hist, tiles, ko, vo, (uint32_t *)nullptr, 0, dbits);
+            uint32_t *t;
+            t = ki, ki = ko, ko = t;
+            t = vi, vi = vo, vo = t;
+        }
     }
     *in_k1 = (ki == k1);
 }
@@ -223,12 +333,23 @@ struct ChunkCount {
         return (uint32_t)((len + chunk - 1) / chunk);
     }
 };
+// Chunk c of run s gets the descriptor {first position, end position, s,
+// chunks of s}; runs with more than one chunk are also listed in `multi`.
 struct ChunkOut {
-    int32_t *seg_chunk0, *chunk_seg, *multi, *scal;
+    const int32_t *seg_off;
+    int32_t chunk;
+    int32_t *seg_chunk0;
+    int4 *chunk_desc;
+    int32_t *multi, *scal;
     __device__ void operator()(int64_t s, uint32_t e, uint32_t v, int) const
     {
         seg_chunk0[s] = (int32_t)e;
-        for (uint32_t c = 0; c < v; ++c) chunk_seg[e + c] = (int32_t)s;
+        const int32_t s0 = seg_off[s], s1 = seg_off[s + 1];
+        for (uint32_t c = 0; c < v; ++c) {
+            const int32_t p0 = s0 + (int32_t)c * chunk;
+            chunk_desc[e + c] = make_int4(p0, p0 + chunk < s1 ? p0 + chunk : s1, (int32_t)s,
+                                          (int32_t)v);
+        }
         if (v > 1) multi[atomicAdd(scal + 3, 1)] = (int32_t)s;  // list order is irrelevant
         if (s == scal[0] - 1) scal[1] = (int32_t)(e + v);
     }
@@ -240,12 +361,13 @@ struct ChunkOut {
 // are recorded in the batch's own scal[2].
 void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, const int32_t *bag_off,
                    int32_t B, int64_t nnz, int key_bits, int chunk, uint32_t *tmp_k,
-                   uint32_t *tmp_v, uint32_t *hist, void *scan_tmp, hipStream_t s)
+                   uint32_t *tmp_v, uint32_t *hist, void *scan_tmp, hipEvent_t consumed,
+                   hipStream_t s)
 {
     const int64_t nbags = (int64_t)tb.T * B;
     launch_zero_i32(b.scal, 4, s);
     // place the keys so that the final sort pass lands in skeys/perm
-    const int passes = nnz > 1 ? (key_bits + 7) / 8 : 0;
+    const int passes = radix_passes(nnz, key_bits);
     uint32_t *k0 = (passes & 1) ? tmp_k : b.skeys, *v0 = (passes & 1) ? tmp_v : b.perm;
     uint32_t *k1 = (passes & 1) ? b.skeys : tmp_k, *v1 = (passes & 1) ? b.perm : tmp_v;
     const int64_t nthr = nnz > nbags ? nnz : nbags;
@@ -255,6 +377,7 @@ void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, cons
                            b.scal + 2);
     else if (bag_off != b.bag_off)
         hipMemcpyAsync(b.bag_off, bag_off, sizeof(int32_t), hipMemcpyDeviceToDevice, s);
+    hipEventRecord(consumed, s);  // the caller's arrays are not read after this point
     if (nnz > 0) {
         bool in_k1 = false;
         launch_radix_sort(k0, v0, k1, v1, nnz, key_bits, hist, scan_tmp, &in_k1, s);
@@ -263,7 +386,8 @@ void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, cons
                            nnz},
                  (uint32_t *)scan_tmp, (uint32_t *)nullptr, s);
         seg_scan(SegDevN{b.scal}, 1, nnz, ChunkCount{b.seg_off, chunk},
-                 ChunkOut{b.seg_chunk0, b.chunk_seg, b.multi, b.scal}, (uint32_t *)scan_tmp,
+                 ChunkOut{b.seg_off, chunk, b.seg_chunk0, b.chunk_desc, b.multi, b.scal},
+                 (uint32_t *)scan_tmp,
                  (uint32_t *)nullptr, s);
     }
 }

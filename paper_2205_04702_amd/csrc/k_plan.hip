@@ -272,7 +272,7 @@ void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int
     }
     // compaction lands where the sort's last pass will end in v_slot
     const int bits = a.act_bits + a.lu_bits;
-    const int passes = n_victims > 1 ? (bits + 7) / 8 : 0;
+    const int passes = radix_passes(n_victims, bits);
     uint32_t *ck = (passes & 1) ? vk0 : vk1;
     uint32_t *cv = (passes & 1) ? vv0 : (uint32_t *)v_slot;
     uint32_t *ok = (passes & 1) ? vk1 : vk0;

@@ -105,12 +105,10 @@ __device__ __forceinline__ void sgd_row(float4 *w, float4 g, float lr)
 //    chunk order before updating the row (the kernel boundary orders the two).
 template <int LPR>
 __global__ void __launch_bounds__(BLOCK) k_backward(float4 *__restrict__ storage,
-                                                    const int32_t *__restrict__ seg_off,
-                                                    const int32_t *__restrict__ seg_chunk0,
-                                                    const int32_t *__restrict__ chunk_seg,
+                                                    const int4 *__restrict__ chunk_desc,
                                                     const int32_t *__restrict__ sbag,
                                                     const int32_t *__restrict__ slot_u,
-                                                    int64_t n_chunks, int chunk,
+                                                    int64_t n_chunks,
                                                     const float4 *__restrict__ grad,
                                                     int64_t nbags, int64_t nslots, float lr,
                                                     float4 *__restrict__ partial)
@@ -119,12 +117,10 @@ __global__ void __launch_bounds__(BLOCK) k_backward(float4 *__restrict__ storage
     const int64_t ch = t / LPR;
     const int c = (int)(t % LPR);
     if (ch >= n_chunks) return;  // whole lane groups leave together
-    const int32_t s = chunk_seg[ch];
-    const int64_t s0 = seg_off[s], s1 = seg_off[s + 1];
-    const int64_t c0 = seg_chunk0[s];
-    const int32_t slot = slot_u[s];
-    const int64_t p0 = s0 + (ch - c0) * (int64_t)chunk;
-    const int64_t p1 = (p0 + chunk) < s1 ? (p0 + chunk) : s1;
+    const int4 d = chunk_desc[ch];  // first position, end position, run, chunks of the run
+    const int64_t p0 = d.x, p1 = d.y;
+    const int32_t slot = slot_u[d.z];
+    const int64_t nch = d.w;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     int64_t p = p0;
     for (; p + 4 <= p1; p += 4) {
@@ -145,7 +141,6 @@ __global__ void __launch_bounds__(BLOCK) k_backward(float4 *__restrict__ storage
         b = (uint32_t)b < (uint64_t)nbags ? b : 0;
         acc = f4_add(acc, grad[(int64_t)b * LPR + c]);
     }
-    const int64_t nch = (s1 - s0 + chunk - 1) / chunk;
     if (nch > 1) {
         partial[ch * LPR + c] = acc;
     } else if ((uint32_t)slot < (uint64_t)nslots) {
@@ -153,29 +148,44 @@ __global__ void __launch_bounds__(BLOCK) k_backward(float4 *__restrict__ storage
     }
 }
 
-// Runs longer than one chunk (listed in `multi`, any order): add the chunk
-// partials in chunk order and update the row.  One lane group per run.
+// Runs longer than one chunk (listed in `multi`, any order), one block per
+// run: the block's G lane groups add the run's chunk partials in a fixed
+// strided order (group g takes chunks g, g+G, ...), four loads in flight per
+// lane; group 0 then adds the G group sums in order and updates the row.
 template <int LPR>
 __global__ void __launch_bounds__(BLOCK) k_bwd_combine(float4 *__restrict__ storage,
                                                        const int32_t *__restrict__ multi,
                                                        int64_t n_multi,
-                                                       const int32_t *__restrict__ seg_off,
                                                        const int32_t *__restrict__ seg_chunk0,
+                                                       const int4 *__restrict__ chunk_desc,
                                                        const int32_t *__restrict__ slot_u,
-                                                       int chunk,
                                                        const float4 *__restrict__ partial,
                                                        int64_t nslots, float lr)
 {
-    const int64_t t = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
-    const int64_t m = t / LPR;
-    const int c = (int)(t % LPR);
-    if (m >= n_multi) return;
+    constexpr int G = BLOCK / LPR;
+    __shared__ float4 red[G][LPR];
+    const int64_t m = blockIdx.x;
+    if (m >= n_multi) return;  // uniform per block
+    const int g = threadIdx.x / LPR, c = threadIdx.x % LPR;
     const int32_t s = multi[m];
-    const int64_t nch = (seg_off[s + 1] - seg_off[s] + chunk - 1) / chunk;
     const int64_t c0 = seg_chunk0[s];
+    const int64_t nch = chunk_desc[c0].w;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    int64_t q = g;
+    for (; q + 3 * G < nch; q += 4 * G) {
+        float4 v[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = partial[(c0 + q + k * G) * LPR + c];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) acc = f4_add(acc, v[k]);
+    }
+    for (; q < nch; q += G) acc = f4_add(acc, partial[(c0 + q) * LPR + c]);
+    red[g][c] = acc;
+    __syncthreads();
+    if (g != 0) return;
+    float4 sum = red[0][c];
+    for (int k = 1; k < G; ++k) sum = f4_add(sum, red[k][c]);
     const int32_t slot = slot_u[s];
-    float4 sum = partial[c0 * LPR + c];
-    for (int64_t q = 1; q < nch; ++q) sum = f4_add(sum, partial[(c0 + q) * LPR + c]);
     if ((uint32_t)slot < (uint64_t)nslots) sgd_row(storage + (int64_t)slot * LPR + c, sum, lr);
 }
 
@@ -299,15 +309,15 @@ void launch_backward(float *storage, int dim, int64_t nslots, const BatchDev &b,
 {
     if (n_chunks <= 0) return;
     const int D4 = dim / 4;
+    (void)chunk;
     SP_DISPATCH_LPR_EV(D4, k_backward, grid_rows(n_chunks, D4), ev[0], ev[1], (float4 *)storage,
-                       (const int32_t *)b.seg_off, (const int32_t *)b.seg_chunk0,
-                       (const int32_t *)b.chunk_seg, (const int32_t *)b.sbag, slot_u, n_chunks,
-                       chunk, (const float4 *)grad, nbags, nslots, lr, (float4 *)partial);
+                       (const int4 *)b.chunk_desc, (const int32_t *)b.sbag, slot_u, n_chunks,
+                       (const float4 *)grad, nbags, nslots, lr, (float4 *)partial);
     if (n_multi > 0)
-        SP_DISPATCH_LPR_EV(D4, k_bwd_combine, grid_rows(n_multi, D4), ev[2], ev[3],
+        SP_DISPATCH_LPR_EV(D4, k_bwd_combine, dim3((unsigned)n_multi), ev[2], ev[3],
                            (float4 *)storage, (const int32_t *)b.multi, n_multi,
-                           (const int32_t *)b.seg_off, (const int32_t *)b.seg_chunk0, slot_u,
-                           chunk, (const float4 *)partial, nslots, lr);
+                           (const int32_t *)b.seg_chunk0, (const int4 *)b.chunk_desc, slot_u,
+                           (const float4 *)partial, nslots, lr);
 }
 
 }  // namespace sp

@@ -45,7 +45,7 @@ struct BatchDev {
     int32_t *inv;                    // [nnz] index of each position's key in ukeys
     int32_t *seg_off;                // [n_unique+1] start of each key's run in skeys
     int32_t *seg_chunk0;             // [n_unique] first backward chunk of each run
-    int32_t *chunk_seg;              // [n_chunks] run of each chunk
+    int4 *chunk_desc;                // [n_chunks] first pos, end pos, run, chunks of the run
     int32_t *multi;                  // [n_multi] runs longer than one chunk (any order)
     int32_t *scal;                   // [0] n_unique, [1] n_chunks, [2] ERR_* bits, [3] n_multi
 };
@@ -83,11 +83,13 @@ void launch_zero_i32(int32_t *p, int64_t n, hipStream_t s);
 void launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
 void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, const int32_t *bag_off,
                    int32_t B, int64_t nnz, int key_bits, int chunk, uint32_t *tmp_k,
-                   uint32_t *tmp_v, uint32_t *hist, void *scan_tmp, hipStream_t s);
+                   uint32_t *tmp_v, uint32_t *hist, void *scan_tmp, hipEvent_t consumed,
+                   hipStream_t s);
 void launch_publish(const DevCounters *cnt, DevCounters *host_mapped, hipStream_t s);
 void launch_radix_sort(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *v1, int64_t n,
                        int bits, uint32_t *hist, void *scan_tmp, bool *in_k1, hipStream_t s);
 int64_t radix_hist_entries(int64_t n);
+int radix_passes(int64_t n, int bits);  // passes launch_radix_sort makes (result in k1 if odd)
 
 // k_plan.hip
 void launch_probe_hold(const Tables &tb, const uint64_t *hash, uint32_t mask,

@@ -248,7 +248,13 @@ class ScratchPipe:
                         lookahead=lookahead, host_tables=self._tabs, max_batch=max_batch,
                         max_ids=max_ids, flags=flags, device=device)
         self.handle = sp_create(cfg)
-        self._keep = []
+        self._desc_cache = {}
+
+    def _describe(self, ids, off) -> sp_batch:
+        B = (len(off) - 1) // self.T
+        nnz = int(ids.shape[0])
+        return sp_batch(batch=B, nnz=nnz, ids=_ptr(ids) if nnz else None, bag_off=_ptr(off),
+                        on_device=_on_device(ids))
 
     def plan(self, window) -> int:
         """window: [(ids, bag_off), ...] as int32 numpy arrays or int32 device tensors."""
@@ -256,14 +262,22 @@ class ScratchPipe:
         arr = (sp_batch * n)()
         keep = []
         for i, (ids, off) in enumerate(window):
-            if not hasattr(ids, "data_ptr"):
+            if hasattr(ids, "data_ptr"):
+                # device tensors: descriptors cached per tensor pair (the cache
+                # holds the tensors, so their addresses stay valid)
+                key = (id(ids), id(off))
+                hit = self._desc_cache.get(key)
+                if hit is None:
+                    if len(self._desc_cache) >= 64:
+                        self._desc_cache.pop(next(iter(self._desc_cache)))
+                    hit = (self._describe(ids, off), ids, off)
+                    self._desc_cache[key] = hit
+                arr[i] = hit[0]
+            else:
                 ids = np.ascontiguousarray(ids, dtype=np.int32)
                 off = np.ascontiguousarray(off, dtype=np.int32)
-            keep.append((ids, off))
-            B = (len(off) - 1) // self.T
-            nnz = int(ids.shape[0])
-            arr[i] = sp_batch(batch=B, nnz=nnz, ids=_ptr(ids) if nnz else None, bag_off=_ptr(off),
-                              on_device=_on_device(ids))
+                keep.append((ids, off))
+                arr[i] = self._describe(ids, off)
         return sp_plan(self.handle, arr, n)
 
     def forward(self, ticket: int, out, stream=None) -> None:

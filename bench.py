@@ -134,15 +134,16 @@ def main():
     out = torch.empty((w.tables * w.batch, w.dim), dtype=torch.float32, device=dev)
 
     host_s = [0.0, 0.0, 0.0]  # host time inside plan / forward / backward calls
+    stream = torch.cuda.current_stream().cuda_stream  # forward and backward run here
 
     def step(u):
         # hold window u..u+L, plus batch u+L+1 handed over early for sorting
         t0 = time.perf_counter()
         tk = ctx.plan([batches[q] for q in range(u, min(u + L + 1, nb - 1) + 1)])
         t1 = time.perf_counter()
-        ctx.forward(tk, out)
+        ctx.forward(tk, out, stream)
         t2 = time.perf_counter()
-        ctx.backward_update(tk, grads[u], w.lr)
+        ctx.backward_update(tk, grads[u], w.lr, stream)
         t3 = time.perf_counter()
         host_s[0] += t1 - t0
         host_s[1] += t2 - t1
@@ -190,7 +191,8 @@ def main():
               "writeback_GBps": round(d["bytes_writeback"] / dt / 1e9, 3),
               "host_ms_per_step": {"plan": round(host_s[0] * 1e3 / K, 4),
                                    "forward": round(host_s[1] * 1e3 / K, 4),
-                                   "backward": round(host_s[2] * 1e3 / K, 4)}}
+                                   "backward": round(host_s[2] * 1e3 / K, 4),
+                                   **{k[8:]: round(d[k] / K, 4) for k in d if k.startswith("host_ms_")}}}
     if not args.no_timing and d["timed_forward"] > 0:
         # kernel execution times from start/stop events of the launches themselves
         fwd_ms = d["ms_forward"] / d["timed_forward"]

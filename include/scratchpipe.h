@@ -94,6 +94,10 @@ typedef struct {
      * plan and fill span their whole launch sequences. */
     double ms_forward, ms_backward, ms_combine, ms_plan, ms_fill;
     int64_t timed_forward, timed_backward, timed_combine, timed_plan, timed_fill;
+    /* host time spent inside sp_plan, in ms: enqueueing ingest, enqueueing the
+     * query, waiting for its counts, enqueueing the commit, and the mover
+     * (including waits for the write-back thread) */
+    double host_ms_ingest, host_ms_query, host_ms_wait, host_ms_commit, host_ms_mover;
 } sp_stats;
 
 /* Per-plan decisions copied to the host for checking.  The caller allocates

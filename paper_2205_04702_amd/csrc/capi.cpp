@@ -19,6 +19,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <chrono>
 #include <condition_variable>
 #include <cstdarg>
 #include <cstdio>
@@ -35,6 +36,13 @@
 using namespace sp;
 
 namespace {
+
+double host_ms()
+{
+    return std::chrono::duration<double, std::milli>(
+               std::chrono::steady_clock::now().time_since_epoch())
+        .count();
+}
 
 int bits_for(uint64_t v)  // bits needed to represent v (0 -> 0)
 {
@@ -252,6 +260,7 @@ struct sp_ctx {
     hipEvent_t ev_planned[TICKETS]{}, ev_filled[TICKETS]{}, ev_upd[TICKETS]{};
     int64_t planned = 0, forwarded = 0, updated = 0;
     int32_t stamp = 0;
+    hipStream_t last_update_stream = nullptr;
 
     // scratch of the plan stream and of the ingest stream
     uint32_t *tmp_k = nullptr, *tmp_v = nullptr, *hist = nullptr;
@@ -290,6 +299,7 @@ struct sp_ctx {
     sp_stats st{};
     Timer t_fwd, t_bwd, t_cmb, t_plan, t_fill;
     int64_t dev_bytes = 0, pinned_bytes = 0;
+    double host_ms[5] = {0, 0, 0, 0, 0};  // ingest, query, wait, commit, mover (sp_plan)
     std::vector<void *> dev_allocs, pinned_allocs;
     std::string err;
     bool broken = false;
@@ -735,6 +745,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     // none once batches are handed over one step early) go now, before the
     // query that needs them; the prepared-ahead batch goes after the query
     // has been enqueued, so its launches overlap the query on the GPU
+    double tA = host_ms();
     bool consumed = false;
     struct ConsumedGuard {  // the window buffers are the caller's again when we return
         sp_ctx *h;
@@ -755,6 +766,8 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
         }
     }
 
+    double tB = host_ms();
+    h->host_ms[0] += tB - tA;
     // ---- phase 1: query and hold (read-only on the scratchpad)
     if (timing) HIPCHK(h, h->t_plan.begin(h->s_plan));
     // the ticket buffers being reused belonged to ticket k - TICKETS
@@ -776,11 +789,17 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
                       tk, h->cnt, h->ring[r0].scal, h->s_plan);
     launch_publish(h->cnt, h->h_cnt_dev, h->s_plan);
     CHECK_LAUNCH(h);
+    double tC = host_ms();
+    h->host_ms[1] += tC - tB;
     if (n > nhold && h->ring_batch[(k + nhold) % h->nring] != k + nhold) {
         TRY(ingest(h, window[nhold], k + nhold));
         consumed = true;
     }
+    double tD = host_ms();
+    h->host_ms[0] += tD - tC;
     HIPCHK(h, hipStreamSynchronize(h->s_plan));
+    double tE = host_ms();
+    h->host_ms[2] += tE - tD;
     DevCounters c;
     memcpy(&c, (const void *)h->h_cnt, sizeof c);
     if (c.err & (ERR_ID_RANGE | ERR_OFFSETS)) {
@@ -855,6 +874,8 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     HIPCHK(h, hipEventRecord(h->ev_planned[e], h->s_plan));
     if (timing) HIPCHK(h, h->t_plan.end(h->s_plan));
 
+    double tF = host_ms();
+    h->host_ms[3] += tF - tE;
     // ---- mover (own stream): write-back of evicted rows and fill of misses;
     // the next plan's query does not wait for it
     // RAW-4: rows evicted by plan p may be refilled from plan p + n_p on
@@ -874,11 +895,11 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     if (timing) HIPCHK(h, h->t_fill.begin(h->s_move));
     if (n_miss > 0) {
         if (k >= 2) HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_upd[(k - 2) % TICKETS], 0));
-        launch_pack(h->storage, h->D, h->total_slots, tk, n_miss, u, 0, h->stage_dev[sl], h->s_move);
-        launch_fill(h->storage, h->D, h->tb, h->host_dev, tk, n_miss, u, 0, h->s_move);
+        launch_move(h->storage, h->D, h->tb, h->host_dev, tk, n_miss, u, 0, h->stage_dev[sl],
+                    h->s_move);
         if (k >= 1) HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_upd[(k - 1) % TICKETS], 0));
-        launch_pack(h->storage, h->D, h->total_slots, tk, n_miss, u, 1, h->stage_dev[sl], h->s_move);
-        launch_fill(h->storage, h->D, h->tb, h->host_dev, tk, n_miss, u, 1, h->s_move);
+        launch_move(h->storage, h->D, h->tb, h->host_dev, tk, n_miss, u, 1, h->stage_dev[sl],
+                    h->s_move);
         CHECK_LAUNCH(h);
     }
     HIPCHK(h, hipEventRecord(h->ev_filled[e], h->s_move));
@@ -903,6 +924,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     h->cv.notify_one();
     h->deadlines.emplace_back(k, k + nhold);
 
+    h->host_ms[4] += host_ms() - tF;
     h->planned = k + 1;
     h->st.plans += 1;
     h->st.lookups += th.nnz;
@@ -930,7 +952,9 @@ extern "C" sp_status sp_forward(sp_handle h, int64_t ticket, float *d_out, void 
     if (nbags > 0 && !d_out) return fail(h, SP_ERR_INVALID_ARG, "null d_out");
     hipStream_t s = (hipStream_t)stream;
     HIPCHK(h, hipStreamWaitEvent(s, h->ev_filled[e], 0));
-    if (ticket >= 1) HIPCHK(h, hipStreamWaitEvent(s, h->ev_upd[(ticket - 1) % TICKETS], 0));
+    // RAW-1: the previous update must land first (implicit on the same stream)
+    if (ticket >= 1 && s != h->last_update_stream)
+        HIPCHK(h, hipStreamWaitEvent(s, h->ev_upd[(ticket - 1) % TICKETS], 0));
     hipEvent_t e0 = nullptr, e1 = nullptr;
     if ((h->flags & SP_FLAG_TIMING) && nbags > 0) HIPCHK(h, h->t_fwd.take(&e0, &e1));
     launch_forward(h->storage, h->D, h->total_slots, h->tk[e].slot_of, h->ring[th.ring].bag_off,
@@ -962,6 +986,7 @@ extern "C" sp_status sp_backward_update(sp_handle h, int64_t ticket, const float
     CHECK_LAUNCH(h);
     HIPCHK(h, hipEventRecord(h->ev_upd[e], s));
     HIPCHK(h, hipEventRecord(h->ring_free[th.ring], s));
+    h->last_update_stream = s;
     h->updated = ticket + 1;
     h->st.updates += 1;
     h->st.chunks += th.n_chunks;
@@ -1027,6 +1052,11 @@ extern "C" sp_status sp_get_stats(sp_handle h, sp_stats *out)
     s.timed_forward = h->t_fwd.count;
     s.timed_backward = h->t_bwd.count;
     s.timed_combine = h->t_cmb.count;
+    s.host_ms_ingest = h->host_ms[0];
+    s.host_ms_query = h->host_ms[1];
+    s.host_ms_wait = h->host_ms[2];
+    s.host_ms_commit = h->host_ms[3];
+    s.host_ms_mover = h->host_ms[4];
     s.timed_plan = h->t_plan.count;
     s.timed_fill = h->t_fill.count;
     *out = s;

@@ -150,8 +150,8 @@ struct SegN {
     __device__ int64_t end(int) const { return n; }
 };
 
-// Small single ranges: one 1024-thread block, each thread scanning SS_ITEMS
-// consecutive values in registers, block-wide scan of the thread sums.
+// Small segments: one 1024-thread block per segment, each thread scanning
+// SS_ITEMS consecutive values in registers, block-wide scan of the thread sums.
 constexpr int SS_THREADS = 1024;
 constexpr int SS_ITEMS = 16;
 constexpr int64_t SMALL_SCAN = (int64_t)SS_THREADS * SS_ITEMS * 8;
@@ -161,7 +161,8 @@ __global__ void __launch_bounds__(SS_THREADS) k_scan_single(Seg seg, Val val, Ou
 {
     __shared__ T lds[SS_THREADS / WAVE];
     __shared__ T carry_s;
-    const int64_t beg = seg.beg(0), end = seg.end(0);
+    const int y = blockIdx.x;
+    const int64_t beg = seg.beg(y), end = seg.end(y);
     if (threadIdx.x == 0) carry_s = 0;
     __syncthreads();
     for (int64_t base = beg; base < end; base += (int64_t)SS_THREADS * SS_ITEMS) {
@@ -171,7 +172,7 @@ __global__ void __launch_bounds__(SS_THREADS) k_scan_single(Seg seg, Val val, Ou
 #pragma unroll
         for (int q = 0; q < SS_ITEMS; ++q) {
             const int64_t i = i0 + q;
-            v[q] = i < end ? val(i, 0) : T(0);
+            v[q] = i < end ? val(i, y) : T(0);
             sum += v[q];
         }
         const T incl = wave_incl_scan(sum);
@@ -188,7 +189,7 @@ __global__ void __launch_bounds__(SS_THREADS) k_scan_single(Seg seg, Val val, Ou
 #pragma unroll
         for (int q = 0; q < SS_ITEMS; ++q) {
             const int64_t i = i0 + q;
-            if (i < end) out(i, run, v[q], 0);
+            if (i < end) out(i, run, v[q], y);
             run += v[q];
         }
         __syncthreads();
@@ -199,17 +200,17 @@ __global__ void __launch_bounds__(SS_THREADS) k_scan_single(Seg seg, Val val, Ou
 
 // Launch the scan.  max_len bounds every segment's length; tile_sums needs
 // nseg * ceil(max_len / SCAN_TILE) entries; totals (optional) gets each
-// segment's sum (multi-block path only).  With one_block, a single range of at
-// most SMALL_SCAN values takes the one-block path: one launch instead of
-// three, worth it only when val/out are cheap (no dependent global loads).
+// segment's sum (multi-block path only).  With one_block, segments of at most
+// SMALL_SCAN values take the one-block-per-segment path: one launch instead
+// of three, worth it only when val/out are cheap (no dependent global loads).
 template <class Seg, class Val, class Out, typename T>
 inline void seg_scan(Seg seg, int nseg, int64_t max_len, Val val, Out out, T *tile_sums,
                      T *totals, hipStream_t s, bool one_block = false)
 {
     if (nseg <= 0 || max_len <= 0) return;
-    if (one_block && nseg == 1 && max_len <= SMALL_SCAN && totals == nullptr) {
-        hipLaunchKernelGGL((k_scan_single<Seg, Val, Out, T>), dim3(1), dim3(SS_THREADS), 0, s, seg,
-                           val, out);
+    if (one_block && max_len <= SMALL_SCAN && totals == nullptr) {
+        hipLaunchKernelGGL((k_scan_single<Seg, Val, Out, T>), dim3(nseg), dim3(SS_THREADS), 0, s,
+                           seg, val, out);
         return;
     }
     int tiles = (int)((max_len + SCAN_TILE - 1) / SCAN_TILE);

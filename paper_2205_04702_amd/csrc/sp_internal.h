@@ -112,10 +112,8 @@ void launch_touch_remap(TicketDev tk, const BatchDev &b, int64_t n_unique, int64
                         int64_t nslots, int32_t *last_use, int32_t u, hipStream_t s);
 
 // k_train.hip
-void launch_pack(const float *storage, int dim, int64_t nslots, TicketDev tk, int64_t n_miss,
-                 int32_t u, int cls, float *stage, hipStream_t s);
-void launch_fill(float *storage, int dim, const Tables &tb, float *const *host_dev, TicketDev tk,
-                 int64_t n_miss, int32_t u, int cls, hipStream_t s);
+void launch_move(float *storage, int dim, const Tables &tb, float *const *host_dev, TicketDev tk,
+                 int64_t n_miss, int32_t u, int cls, float *stage, hipStream_t s);
 void launch_forward(const float *storage, int dim, int64_t nslots, const int32_t *slot_of,
                     const int32_t *bag_off, int64_t nbags, float *out, hipStream_t s,
                     hipEvent_t e0, hipEvent_t e1);

@@ -99,6 +99,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-timing", action="store_true", help="do not time kernels with events")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="after the timed region, run a plain elementwise copy (torch.neg) of MIB "
+                         "MiB three times: the reference kernel for scaling HBM byte counters")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -162,6 +165,13 @@ def main():
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     s1 = ctx.stats()
+    if args.calibrate_copy > 0:
+        x = torch.ones(args.calibrate_copy << 18, dtype=torch.float32, device=dev)
+        y = torch.empty_like(x)
+        for _ in range(3):
+            torch.neg(x, out=y)  # reads and writes MIB MiB
+        torch.cuda.synchronize()
+        del x, y
     ctx.close()
     host.close()
     log(f"[bench] timed {K} steps in {dt:.3f}s")

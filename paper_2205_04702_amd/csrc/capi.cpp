@@ -250,23 +250,31 @@ struct sp_ctx {
     int nring = 0;
     std::vector<BatchDev> ring;
     std::vector<int64_t> ring_batch, ring_nnz, ring_B;
-    std::vector<hipEvent_t> ring_free;      // backward of the entry's batch issued
     std::vector<hipEvent_t> ring_ready;     // ingest of the entry's batch finished
+    std::vector<char> ring_seen;            // the plan stream has waited for ring_ready
     hipEvent_t ev_consumed = nullptr;       // last ingest has read the caller's arrays
 
     // tickets
-    TicketDev tk[TICKETS]{};
-    TicketHost tkh[TICKETS]{};
-    hipEvent_t ev_planned[TICKETS]{}, ev_filled[TICKETS]{}, ev_upd[TICKETS]{};
+    // tickets: plan k uses entry k % nring, like its batch in the window ring,
+    // so ev_upd[r] (backward of the entry's ticket issued) also frees ring[r]
+    std::vector<TicketDev> tk;
+    std::vector<TicketHost> tkh;
+    std::vector<hipEvent_t> ev_planned, ev_filled, ev_upd;
+    std::vector<hipStream_t> upd_stream;    // stream each ticket's backward ran on
     int64_t planned = 0, forwarded = 0, updated = 0;
     int32_t stamp = 0;
+    // query of plan spec_ticket over spec_nhold batches, issued early by the
+    // plan before it (-1: none); its hold marks carry spec_stamp
+    int64_t spec_ticket = -1;
+    int spec_nhold = 0;
+    int32_t spec_stamp = 0;
     hipStream_t last_update_stream = nullptr;
 
     // scratch of the plan stream and of the ingest stream
     uint32_t *tmp_k = nullptr, *tmp_v = nullptr, *hist = nullptr;
-    void *scan_tmp = nullptr;
+    ScanWs ws_plan;
     uint32_t *itmp_k = nullptr, *itmp_v = nullptr, *ihist = nullptr;
-    void *iscan_tmp = nullptr;
+    ScanWs ws_ingest;
     int32_t *sel_state = nullptr, *sel_hist = nullptr;
     uint32_t *vk0 = nullptr, *vv0 = nullptr, *vk1 = nullptr;
     float *partial = nullptr;
@@ -280,8 +288,8 @@ struct sp_ctx {
 
     // plan stream: query, hold, victims, commit; ingest stream: sorting and
     // deduplicating batches as they become visible; move stream: write-back
-    // packing and miss fills; copy stream: device-to-host of evicted rows
-    hipStream_t s_plan = nullptr, s_ingest = nullptr, s_move = nullptr, s_copy = nullptr;
+    // staging, miss fills and the device-to-host copy of evicted rows
+    hipStream_t s_plan = nullptr, s_ingest = nullptr, s_move = nullptr;
 
     // write-back thread
     std::thread worker;
@@ -437,16 +445,10 @@ static void release(sp_ctx *h)
     }
     h->scatter.stop();
     (void)hipDeviceSynchronize();
-    for (auto &e : h->ring_free)
-        if (e) hipEventDestroy(e);
-    for (auto &e : h->ring_ready)
-        if (e) hipEventDestroy(e);
+    for (auto *v : {&h->ring_ready, &h->ev_planned, &h->ev_filled, &h->ev_upd})
+        for (auto &e : *v)
+            if (e) hipEventDestroy(e);
     if (h->ev_consumed) hipEventDestroy(h->ev_consumed);
-    for (int i = 0; i < TICKETS; ++i) {
-        if (h->ev_planned[i]) hipEventDestroy(h->ev_planned[i]);
-        if (h->ev_filled[i]) hipEventDestroy(h->ev_filled[i]);
-        if (h->ev_upd[i]) hipEventDestroy(h->ev_upd[i]);
-    }
     for (int i = 0; i < 2; ++i)
         if (h->ev_d2h[i]) hipEventDestroy(h->ev_d2h[i]);
     h->t_fwd.destroy();
@@ -457,7 +459,6 @@ static void release(sp_ctx *h)
     if (h->s_plan) hipStreamDestroy(h->s_plan);
     if (h->s_ingest) hipStreamDestroy(h->s_ingest);
     if (h->s_move) hipStreamDestroy(h->s_move);
-    if (h->s_copy) hipStreamDestroy(h->s_copy);
     for (void *p : h->dev_allocs) hipFree(p);
     for (void *p : h->pinned_allocs) hipHostFree(p);
     delete h;
@@ -522,8 +523,14 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     h->ring_batch.assign(h->nring, -1);
     h->ring_nnz.assign(h->nring, 0);
     h->ring_B.assign(h->nring, 0);
-    h->ring_free.assign(h->nring, nullptr);
     h->ring_ready.assign(h->nring, nullptr);
+    h->ring_seen.assign(h->nring, 0);
+    h->tk.assign(h->nring, TicketDev{});
+    h->tkh.assign(h->nring, TicketHost{});
+    h->ev_planned.assign(h->nring, nullptr);
+    h->ev_filled.assign(h->nring, nullptr);
+    h->ev_upd.assign(h->nring, nullptr);
+    h->upd_stream.assign(h->nring, nullptr);
     for (int r = 0; r < h->nring; ++r) {
         BatchDev &b = h->ring[r];
         TRY(dalloc(h, &b.ids, N));
@@ -539,10 +546,9 @@ static sp_status build(sp_ctx *h, const sp_config *c)
         TRY(dalloc(h, &b.chunk_desc, nchunk_max));
         TRY(dalloc(h, &b.multi, N / (h->chunk + 1) + 2));
         TRY(dalloc(h, &b.scal, T + 3));
-        HIPCHK(nullptr, hipEventCreateWithFlags(&h->ring_free[r], hipEventDisableTiming));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ring_ready[r], hipEventDisableTiming));
     }
-    for (int k = 0; k < TICKETS; ++k) {
+    for (int k = 0; k < h->nring; ++k) {
         TicketDev &t = h->tk[k];
         TRY(dalloc(h, &t.hit, N));
         TRY(dalloc(h, &t.slot_u, N));
@@ -565,13 +571,21 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     TRY(dalloc(h, &h->vk1, N));
     TRY(dalloc(h, &h->hist, radix_hist_entries(N)));
     TRY(dalloc(h, &h->ihist, radix_hist_entries(N)));
-    const int64_t scan_entries = MAX_TABLES * (h->maxS / 2048 + 2) + N / 2048 + 1024;
-    TRY(dalloc(h, (uint64_t **)&h->scan_tmp, scan_entries));
-    TRY(dalloc(h, (uint64_t **)&h->iscan_tmp, scan_entries));
+    TRY(dalloc(h, &h->cnt, 1));
+    {
+        // scans: victims (tables x slots per table), misses and batches (N),
+        // radix histogram tables (at most N + 2048 entries)
+        const int64_t tiles = std::max(scan_tiles(T, h->maxS), scan_tiles(1, N + 4096)) + 2;
+        for (ScanWs *ws : {&h->ws_plan, &h->ws_ingest}) {
+            ws->max_tiles = tiles;
+            TRY(dalloc(h, &ws->status, LB_WORDS * tiles));
+            TRY(dalloc(h, &ws->counter, 1));
+            ws->err = &h->cnt->err_sticky;
+        }
+    }
     TRY(dalloc(h, &h->sel_state, 2 * MAX_TABLES));
     TRY(dalloc(h, &h->sel_hist, (int64_t)MAX_TABLES * SEL_BINS));
     TRY(dalloc(h, &h->partial, nchunk_max * h->D));
-    TRY(dalloc(h, &h->cnt, 1));
     h->stage_rows = std::min<int64_t>(N, S);
     for (int i = 0; i < 2; ++i) {
         TRY(dalloc(h, &h->stage_dev[i], h->stage_rows * (h->D + 1)));
@@ -596,7 +610,6 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_plan, hipStreamNonBlocking));
     HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_ingest, hipStreamNonBlocking));
     HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_move, hipStreamNonBlocking));
-    HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_copy, hipStreamNonBlocking));
     HIPCHK(nullptr, h->t_fwd.init());
     HIPCHK(nullptr, h->t_bwd.init());
     HIPCHK(nullptr, h->t_cmb.init());
@@ -611,6 +624,10 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     HIPCHK(nullptr, hipMemsetAsync(h->storage, 0, sizeof(float) * S * h->D, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->sel_hist, 0, sizeof(int32_t) * MAX_TABLES * SEL_BINS, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->cnt, 0, sizeof(DevCounters), h->s_plan));
+    for (ScanWs *ws : {&h->ws_plan, &h->ws_ingest}) {
+        HIPCHK(nullptr, hipMemsetAsync(ws->status, 0, sizeof(uint64_t) * LB_WORDS * ws->max_tiles, h->s_plan));
+        HIPCHK(nullptr, hipMemsetAsync(ws->counter, 0, sizeof(uint32_t), h->s_plan));
+    }
     HIPCHK(nullptr, hipStreamSynchronize(h->s_plan));
     h->st.min_capacity_margin = INT64_MAX;
     const unsigned hw = std::thread::hardware_concurrency();
@@ -696,7 +713,7 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
     const int r = (int)(q % h->nring);
     BatchDev &b = h->ring[r];
     // the previous occupant (batch q - nring) must be done with its backward
-    HIPCHK(h, hipStreamWaitEvent(h->s_ingest, h->ring_free[r], 0));
+    HIPCHK(h, hipStreamWaitEvent(h->s_ingest, h->ev_upd[r], 0));
     const int64_t nbags = (int64_t)h->T * bt.batch;
     const int32_t *ids = bt.ids, *off = bt.bag_off;
     if (!bt.on_device) {  // host arrays: copy into the ring first
@@ -709,12 +726,44 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
         off = b.bag_off;
     }
     launch_ingest(h->tb, b, ids, off, bt.batch, bt.nnz, h->key_bits, h->chunk, h->itmp_k,
-                  h->itmp_v, h->ihist, h->iscan_tmp, h->ev_consumed, h->s_ingest);
+                  h->itmp_v, h->ihist, h->ws_ingest, h->ev_consumed, h->s_ingest);
     CHECK_LAUNCH(h);
+    if (h->ws_ingest.overflow) return fail(h, SP_ERR_HIP, "internal: scan workspace too small");
     HIPCHK(h, hipEventRecord(h->ring_ready[r], h->s_ingest));
+    h->ring_seen[r] = 0;
     h->ring_batch[r] = q;
     h->ring_nnz[r] = bt.nnz;
     h->ring_B[r] = bt.batch;
+    return SP_OK;
+}
+
+// Phase 1 of plan k over window batches k .. k+nhold-1, all ingested or being
+// ingested: hold marks, the planned batch's hits and per-table miss / held
+// counts, published to host-coherent memory (read-only on the scratchpad).
+static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, int32_t *stamp_out)
+{
+    const int e = (int)(k % h->nring);
+    // the ticket buffers being reused belonged to ticket k - nring
+    if (k >= h->nring) HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ev_upd[e], 0));
+    const uint32_t *ukeys[MAX_WINDOW];
+    const int32_t *nuniq[MAX_WINDOW];
+    int64_t max_nnz = 0;
+    for (int w = 0; w < nhold; ++w) {
+        const int r = (int)((k + w) % h->nring);
+        if (!h->ring_seen[r]) {  // later queries are behind this one on the same stream
+            HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ring_ready[r], 0));
+            h->ring_seen[r] = 1;
+        }
+        ukeys[w] = h->ring[r].ukeys;
+        nuniq[w] = h->ring[r].scal;
+        max_nnz = std::max(max_nnz, h->ring_nnz[r]);
+    }
+    const int32_t stamp = ++h->stamp;
+    launch_probe_hold(h->tb, h->hash, h->hash_mask, ukeys, nuniq, nhold, max_nnz, h->held, stamp,
+                      h->tk[e], h->cnt, h->ring[k % h->nring].scal, h->s_plan);
+    launch_publish(h->cnt, h->h_cnt_dev, h->s_plan);  // also clears the counters
+    CHECK_LAUNCH(h);
+    *stamp_out = stamp;
     return SP_OK;
 }
 
@@ -735,7 +784,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     }
     const int64_t k = h->planned;
     const int32_t u = (int32_t)k;
-    const int e = (int)(k % TICKETS);
+    const int e = (int)(k % h->nring);
     const int nhold = std::min<int>(n, h->L + 1);  // window[L+1], if given, is only prepared
     TicketDev &tk = h->tk[e];
     TicketHost &th = h->tkh[e];
@@ -768,27 +817,14 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
 
     double tB = host_ms();
     h->host_ms[0] += tB - tA;
-    // ---- phase 1: query and hold (read-only on the scratchpad)
-    if (timing) HIPCHK(h, h->t_plan.begin(h->s_plan));
-    // the ticket buffers being reused belonged to ticket k - TICKETS
-    if (k >= TICKETS) HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ev_upd[e], 0));
-    const uint32_t *ukeys[MAX_WINDOW];
-    const int32_t *nuniq[MAX_WINDOW];
-    int64_t max_nnz = 0;
-    for (int w = 0; w < nhold; ++w) {
-        const int r = (int)((k + w) % h->nring);
-        HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ring_ready[r], 0));
-        ukeys[w] = h->ring[r].ukeys;
-        nuniq[w] = h->ring[r].scal;
-        max_nnz = std::max(max_nnz, window[w].nnz);
-    }
-    launch_zero_i32((int32_t *)h->cnt, COUNTERS_CLEARED, h->s_plan);
+    // ---- phase 1: query and hold, unless the previous plan already issued it
+    // over this same window (its batches still in place)
+    bool spec = h->spec_ticket == k && h->spec_nhold == nhold;
+    for (int w = 0; w < nhold && spec; ++w) spec = h->ring_batch[(k + w) % h->nring] == k + w;
+    h->spec_ticket = -1;
+    int32_t stamp = h->spec_stamp;
+    if (!spec) TRY(enqueue_query(h, k, nhold, &stamp));
     const int r0 = (int)(k % h->nring);
-    const int stamp = ++h->stamp;
-    launch_probe_hold(h->tb, h->hash, h->hash_mask, ukeys, nuniq, nhold, max_nnz, h->held, stamp,
-                      tk, h->cnt, h->ring[r0].scal, h->s_plan);
-    launch_publish(h->cnt, h->h_cnt_dev, h->s_plan);
-    CHECK_LAUNCH(h);
     double tC = host_ms();
     h->host_ms[1] += tC - tB;
     if (n > nhold && h->ring_batch[(k + nhold) % h->nring] != k + nhold) {
@@ -824,6 +860,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     }
 
     // ---- phase 2: commit
+    if (timing) HIPCHK(h, h->t_plan.begin(h->s_plan));
     const BatchDev &b0 = h->ring[r0];
     th.nnz = h->ring_nnz[r0];
     th.B = (int32_t)h->ring_B[r0];
@@ -842,7 +879,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
             ++h->st.hash_rebuilds;
         }
         h->hash_used += n_miss;
-        launch_miss_compact(b0.ukeys, th.n_unique, tk, h->scan_tmp, h->s_plan);
+        launch_miss_compact(b0.ukeys, th.n_unique, tk, h->ws_plan, h->s_plan);
         SelArgs a{};
         int32_t vb = 0;
         int64_t maxS = 0;
@@ -864,18 +901,27 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
         a.stamp = stamp;
         const int levels = (nb + SEL_BITS - 1) / SEL_BITS;
         launch_select_victims(a, levels, maxS, h->held, h->last_use, h->sel_state, h->sel_hist, h->vk0,
-                              h->vv0, h->vk1, (uint32_t *)nullptr, n_miss, h->hist, h->scan_tmp,
-                              tk.v_slot, h->s_plan);
-        launch_commit(h->tb, h->hash, h->hash_mask, tk, n_miss, th.n_unique, h->key_of_slot,
-                      h->last_use, h->cnt, h->s_plan);
+                              h->vv0, h->vk1, (uint32_t *)nullptr, n_miss, h->hist, h->ws_plan,
+                              tk.v_slot, &h->cnt->err_sticky, h->s_plan);
     }
-    launch_touch_remap(tk, b0, th.n_unique, th.nnz, h->total_slots, h->last_use, u, h->s_plan);
+    launch_commit(h->tb, h->hash, h->hash_mask, tk, b0, n_miss, th.n_unique, th.nnz, h->key_of_slot,
+                  h->last_use, u, h->cnt, h->s_plan);
     CHECK_LAUNCH(h);
+    if (h->ws_plan.overflow) return fail(h, SP_ERR_HIP, "internal: scan workspace too small");
     HIPCHK(h, hipEventRecord(h->ev_planned[e], h->s_plan));
-    if (timing) HIPCHK(h, h->t_plan.end(h->s_plan));
-
     double tF = host_ms();
     h->host_ms[3] += tF - tE;
+    // ---- the next plan's query, when its whole window is known: batches
+    // k+1 .. k+L+1 are all in the ring now; it runs right behind this commit
+    if (n == h->L + 2) {
+        TRY(enqueue_query(h, k + 1, h->L + 1, &h->spec_stamp));
+        h->spec_ticket = k + 1;
+        h->spec_nhold = h->L + 1;
+    }
+    if (timing) HIPCHK(h, h->t_plan.end(h->s_plan));
+    const double tG = host_ms();
+    h->host_ms[1] += tG - tF;
+    tF = tG;
     // ---- mover (own stream): write-back of evicted rows and fill of misses;
     // the next plan's query does not wait for it
     // RAW-4: rows evicted by plan p may be refilled from plan p + n_p on
@@ -887,18 +933,22 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
         while (!h->deadlines.empty() && h->deadlines.front().first <= need) h->deadlines.pop_front();
     }
     const int sl = (int)(k & 1);
+    // host staging of plan k-2 is free again once its rows are scattered; the
+    // device staging is, by stream order (its copy ran on this stream)
+    if (k >= 2) TRY(join_jobs(h, k - 2));
     HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_planned[e], 0));
-    if (k >= 2) {
-        TRY(join_jobs(h, k - 2));  // host staging of plan k-2 is free again
-        HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_d2h[sl], 0));
-    }
     if (timing) HIPCHK(h, h->t_fill.begin(h->s_move));
     if (n_miss > 0) {
-        if (k >= 2) HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_upd[(k - 2) % TICKETS], 0));
-        launch_move(h->storage, h->D, h->tb, h->host_dev, tk, n_miss, u, 0, h->stage_dev[sl],
-                    h->s_move);
-        if (k >= 1) HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_upd[(k - 1) % TICKETS], 0));
-        launch_move(h->storage, h->D, h->tb, h->host_dev, tk, n_miss, u, 1, h->stage_dev[sl],
+        // RAW-2/3: a victim's row is final once the last update that used it
+        // has run.  Updates up to k-4 are behind this stream already (the
+        // ring entries they freed were ingested before this plan's query);
+        // k-3 .. k-1 are waited for, one wait when they share a stream.
+        for (int64_t j = std::max<int64_t>(0, k - 3); j < k; ++j) {
+            const int ej = (int)(j % h->nring);
+            if (j == k - 1 || h->upd_stream[ej] != h->upd_stream[(k - 1) % h->nring])
+                HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_upd[ej], 0));
+        }
+        launch_move(h->storage, h->D, h->tb, h->host_dev, tk, n_miss, u, h->stage_dev[sl],
                     h->s_move);
         CHECK_LAUNCH(h);
     }
@@ -907,11 +957,10 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     Job job;
     job.ticket = k;
     if (n_miss > 0) {
-        HIPCHK(h, hipStreamWaitEvent(h->s_copy, h->ev_filled[e], 0));
         HIPCHK(h, hipMemcpyAsync(h->stage_host[sl], h->stage_dev[sl],
                                  sizeof(float) * n_miss * (h->D + 1), hipMemcpyDeviceToHost,
-                                 h->s_copy));
-        HIPCHK(h, hipEventRecord(h->ev_d2h[sl], h->s_copy));
+                                 h->s_move));
+        HIPCHK(h, hipEventRecord(h->ev_d2h[sl], h->s_move));
         job.ev = h->ev_d2h[sl];
         job.rows = h->stage_host[sl];
         job.keys = (const int32_t *)(h->stage_host[sl] + n_miss * h->D);
@@ -946,7 +995,7 @@ extern "C" sp_status sp_forward(sp_handle h, int64_t ticket, float *d_out, void 
     if (ticket != h->planned - 1 || h->forwarded != ticket)
         return fail(h, SP_ERR_SEQUENCE, "forward of ticket %lld out of order (planned %lld, forwarded %lld)",
                     (long long)ticket, (long long)h->planned, (long long)h->forwarded);
-    const int e = (int)(ticket % TICKETS);
+    const int e = (int)(ticket % h->nring);
     const TicketHost &th = h->tkh[e];
     const int64_t nbags = (int64_t)h->T * th.B;
     if (nbags > 0 && !d_out) return fail(h, SP_ERR_INVALID_ARG, "null d_out");
@@ -954,7 +1003,7 @@ extern "C" sp_status sp_forward(sp_handle h, int64_t ticket, float *d_out, void 
     HIPCHK(h, hipStreamWaitEvent(s, h->ev_filled[e], 0));
     // RAW-1: the previous update must land first (implicit on the same stream)
     if (ticket >= 1 && s != h->last_update_stream)
-        HIPCHK(h, hipStreamWaitEvent(s, h->ev_upd[(ticket - 1) % TICKETS], 0));
+        HIPCHK(h, hipStreamWaitEvent(s, h->ev_upd[(ticket - 1) % h->nring], 0));
     hipEvent_t e0 = nullptr, e1 = nullptr;
     if ((h->flags & SP_FLAG_TIMING) && nbags > 0) HIPCHK(h, h->t_fwd.take(&e0, &e1));
     launch_forward(h->storage, h->D, h->total_slots, h->tk[e].slot_of, h->ring[th.ring].bag_off,
@@ -972,7 +1021,7 @@ extern "C" sp_status sp_backward_update(sp_handle h, int64_t ticket, const float
     if (ticket != h->forwarded - 1 || h->updated != ticket)
         return fail(h, SP_ERR_SEQUENCE, "backward of ticket %lld out of order (forwarded %lld, updated %lld)",
                     (long long)ticket, (long long)h->forwarded, (long long)h->updated);
-    const int e = (int)(ticket % TICKETS);
+    const int e = (int)(ticket % h->nring);
     const TicketHost &th = h->tkh[e];
     if (th.nnz > 0 && !d_grad) return fail(h, SP_ERR_INVALID_ARG, "null d_grad");
     hipStream_t s = (hipStream_t)stream;
@@ -984,8 +1033,8 @@ extern "C" sp_status sp_backward_update(sp_handle h, int64_t ticket, const float
                     th.n_chunks, th.n_multi, h->chunk, d_grad, (int64_t)h->T * th.B, lr,
                     h->partial, s, ev);
     CHECK_LAUNCH(h);
-    HIPCHK(h, hipEventRecord(h->ev_upd[e], s));
-    HIPCHK(h, hipEventRecord(h->ring_free[th.ring], s));
+    HIPCHK(h, hipEventRecord(h->ev_upd[e], s));  // also frees ring entry e of the window
+    h->upd_stream[e] = s;
     h->last_update_stream = s;
     h->updated = ticket + 1;
     h->st.updates += 1;
@@ -1070,8 +1119,8 @@ extern "C" sp_status sp_debug_plan(sp_handle h, int64_t ticket, sp_plan_dump *d)
     if (ticket != h->planned - 1 || ticket < 0)
         return fail(h, SP_ERR_SEQUENCE, "only the latest plan (%lld) can be dumped", (long long)h->planned - 1);
     HIPCHK(h, hipStreamSynchronize(h->s_plan));
-    const TicketHost &th = h->tkh[ticket % TICKETS];
-    const TicketDev &tk = h->tk[ticket % TICKETS];
+    const TicketHost &th = h->tkh[ticket % h->nring];
+    const TicketDev &tk = h->tk[ticket % h->nring];
     const BatchDev &b = h->ring[th.ring];
     const int rb = h->tb.row_bits;
     const uint32_t mask = (1u << rb) - 1u;

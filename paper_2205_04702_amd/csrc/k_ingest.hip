@@ -76,14 +76,14 @@ __global__ void __launch_bounds__(BLOCK) k_prepare(Tables tb, const int32_t *ids
 
 // ---------------------------------------------------------------- LSD radix sort
 //
-// 8-bit digits, stable.  Per pass: tile histograms (digit-major), one scan of
-// the histogram table, then a scatter in which every tile ranks its keys per
-// digit with wave ballots, round by round, so equal digits keep input order.
-
-// Digits are up to RS_MAXBITS wide; a key of b bits takes ceil(b / 11) passes
-// of ceil(b / passes) bits each.
-constexpr int RS_ITEMS = 8;
-constexpr int RS_TILE = BLOCK * RS_ITEMS;
+// Stable.  Per pass: tile histograms (digit-major), one scan of the histogram
+// table, then a scatter in which every tile ranks its keys per digit with wave
+// ballots, round by round (BLOCK keys per round), so equal digits keep input
+// order.  Digits are up to RS_MAXBITS wide; a key of b bits takes
+// ceil(b / 11) passes of ceil(b / passes) bits each.  A tile is `items`
+// rounds: small inputs get short tiles so that more blocks share the work.
+constexpr int RS_ITEMS = 8;                 // most rounds per tile
+constexpr int RS_TILE = BLOCK * RS_ITEMS;   // longest tile
 constexpr int RS_MAXBITS = 11;
 constexpr int RS_MAXBINS = 1 << RS_MAXBITS;
 // One-launch passes when every block can afford to read the whole
@@ -93,6 +93,23 @@ constexpr int64_t RS_FUSED_TABLE = 16384;
 int radix_passes(int64_t n, int bits)
 {
     return (n <= 1 || bits <= 0) ? 0 : (bits + RS_MAXBITS - 1) / RS_MAXBITS;
+}
+
+RadixPlan radix_plan(int64_t n, int bits)
+{
+    RadixPlan p{};
+    p.passes = radix_passes(n, bits);
+    if (p.passes == 0) return p;
+    p.dbits = (bits + p.passes - 1) / p.passes;
+    const int64_t bins = (int64_t)1 << p.dbits;
+    auto tiles_for = [n](int r) { return (n + (int64_t)BLOCK * r - 1) / ((int64_t)BLOCK * r); };
+    p.items = RS_ITEMS;
+    while (p.items > 1 && tiles_for(p.items) < 128 && bins * tiles_for(p.items / 2) <= RS_FUSED_TABLE)
+        p.items /= 2;
+    p.tiles = tiles_for(p.items);
+    p.table = bins * p.tiles;
+    p.fused = p.table <= RS_FUSED_TABLE;
+    return p;
 }
 
 int64_t radix_hist_entries(int64_t n)
@@ -105,16 +122,17 @@ int64_t radix_hist_entries(int64_t n)
 // hist[d * tiles + tile] = keys of the tile with digit d.  With zero_from /
 // zero_n, also clears a range (the histograms later passes accumulate into).
 __global__ void __launch_bounds__(BLOCK) k_radix_hist(const uint32_t *keys, int64_t n, int shift,
-                                                      int dbits, uint32_t *hist, int tiles,
-                                                      uint32_t *zero_from, int64_t zero_n)
+                                                      int dbits, int items, uint32_t *hist,
+                                                      int tiles, uint32_t *zero_from,
+                                                      int64_t zero_n)
 {
     __shared__ uint32_t h[RS_MAXBINS];
     const int bins = 1 << dbits;
     const uint32_t mask = (uint32_t)bins - 1u;
     for (int d = threadIdx.x; d < bins; d += BLOCK) h[d] = 0;
     __syncthreads();
-    const int64_t base = (int64_t)blockIdx.x * RS_TILE;
-    for (int r = 0; r < RS_ITEMS; ++r) {
+    const int64_t base = (int64_t)blockIdx.x * BLOCK * items;
+    for (int r = 0; r < items; ++r) {
         const int64_t i = base + (int64_t)r * BLOCK + threadIdx.x;
         if (i < n) atomicAdd(&h[(keys[i] >> shift) & mask], 1u);
     }
@@ -138,10 +156,10 @@ __global__ void __launch_bounds__(BLOCK) k_radix_hist(const uint32_t *keys, int6
 template <bool FUSED>
 __global__ void __launch_bounds__(BLOCK) k_radix_scatter(const uint32_t *kin, const uint32_t *vin,
                                                          int64_t n, int shift, int dbits,
-                                                         const uint32_t *table, int tiles,
-                                                         uint32_t *kout, uint32_t *vout,
-                                                         uint32_t *hist_next, int shift_next,
-                                                         int dbits_next)
+                                                         int items, const uint32_t *table,
+                                                         int tiles, uint32_t *kout,
+                                                         uint32_t *vout, uint32_t *hist_next,
+                                                         int shift_next, int dbits_next)
 {
     __shared__ uint32_t base[RS_MAXBINS];
     __shared__ uint32_t wc[BLOCK / WAVE][RS_MAXBINS];
@@ -150,11 +168,23 @@ __global__ void __launch_bounds__(BLOCK) k_radix_scatter(const uint32_t *kin, co
     const int bins = 1 << dbits;
     const uint32_t mask = (uint32_t)bins - 1u;
     const int tile = blockIdx.x;
+    const int tile_len = BLOCK * items;
+    const int64_t tbase = (int64_t)tile * tile_len;
+    // the tile's keys and values, all loads in flight at once
+    uint32_t kr[RS_ITEMS], vr[RS_ITEMS];
+#pragma unroll
+    for (int r = 0; r < RS_ITEMS; ++r) {
+        const int64_t i = tbase + (int64_t)r * BLOCK + tid;
+        const bool in = r < items && i < n;
+        kr[r] = in ? kin[i] : 0u;
+        vr[r] = in ? vin[i] : 0u;
+    }
     if (FUSED) {
         // digit totals into wc[0], this tile's column prefix into base
         for (int d = tid; d < bins; d += BLOCK) {
             const uint32_t *row = table + (int64_t)d * tiles;
             uint32_t before = 0, total = 0;
+#pragma unroll 8
             for (int t = 0; t < tiles; ++t) {
                 const uint32_t x = row[t];
                 before += t < tile ? x : 0u;
@@ -188,15 +218,15 @@ __global__ void __launch_bounds__(BLOCK) k_radix_scatter(const uint32_t *kin, co
     __syncthreads();
 
     const uint64_t lt = lanemask_lt();
-    const int64_t tbase = (int64_t)tile * RS_TILE;
-    const int tiles_out = (int)((n + RS_TILE - 1) / RS_TILE);
     const uint32_t mask_next = (1u << dbits_next) - 1u;
+#pragma unroll
     for (int r = 0; r < RS_ITEMS; ++r) {
+        if (r >= items) break;  // uniform
         const uint32_t stamp = (uint32_t)(r + 1) << 16;
         const int64_t i = tbase + (int64_t)r * BLOCK + tid;
         const bool valid = i < n;
-        const uint32_t k = valid ? kin[i] : 0u;
-        const uint32_t v = valid ? vin[i] : 0u;
+        const uint32_t k = kr[r];
+        const uint32_t v = vr[r];
         const uint32_t d = (k >> shift) & mask;
         uint64_t peers = __ballot(valid);
         for (int b = 0; b < dbits; ++b) {
@@ -232,8 +262,8 @@ __global__ void __launch_bounds__(BLOCK) k_radix_scatter(const uint32_t *kin, co
             kout[p] = k;
             vout[p] = v;
             if (FUSED && hist_next)
-                atomicAdd(&hist_next[(int64_t)((k >> shift_next) & mask_next) * tiles_out +
-                                     p / RS_TILE],
+                atomicAdd(&hist_next[(int64_t)((k >> shift_next) & mask_next) * tiles +
+                                     p / (uint32_t)tile_len],
                           1u);
         }
         __syncthreads();
@@ -250,26 +280,31 @@ struct OutU32 {
 };
 
 // Sorts (k0, v0) by key (LSD, stable); k1/v1 are scratch of the same size.
-// The result is in k1/v1 when radix_passes(n, bits) is odd (*in_k1).
+// The result is in k1/v1 when radix_passes(n, bits) is odd (*in_k1).  With
+// prehist (one-launch passes only), the caller has already filled the first
+// pass's table (tile t = keys [t * BLOCK * items, ...)) and zeroed the other
+// passes' tables (radix_plan gives the layout).
 void launch_radix_sort(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *v1, int64_t n,
-                       int bits, uint32_t *hist, void *scan_tmp, bool *in_k1, hipStream_t s)
+                       int bits, uint32_t *hist, ScanWs &ws, bool *in_k1, hipStream_t s,
+                       bool prehist)
 {
     *in_k1 = false;
-    const int passes = radix_passes(n, bits);
+    const RadixPlan rp = radix_plan(n, bits);
+    const int passes = rp.passes;
     if (passes == 0) return;
-    const int dbits = (bits + passes - 1) / passes;
-    const int bins = 1 << dbits;
-    const int tiles = (int)((n + RS_TILE - 1) / RS_TILE);
-    const int64_t table = (int64_t)bins * tiles;
+    const int dbits = rp.dbits, items = rp.items;
+    const int tiles = (int)rp.tiles;
+    const int64_t table = rp.table;
     uint32_t *ki = k0, *vi = v0, *ko = k1, *vo = v1;
-    if (table <= RS_FUSED_TABLE) {
+    if (rp.fused) {
         // hist + P one-launch passes; pass p reads table p and fills table p+1
-        hipLaunchKernelGGL(k_radix_hist, dim3(tiles), dim3(BLOCK), 0, s, ki, n, 0, dbits, hist,
-                           tiles, hist + table, table * (passes - 1));
+        if (!prehist)
+            hipLaunchKernelGGL(k_radix_hist, dim3(tiles), dim3(BLOCK), 0, s, ki, n, 0, dbits, items,
+                               hist, tiles, hist + table, table * (passes - 1));
         for (int p = 0; p < passes; ++p) {
             uint32_t *next = p + 1 < passes ? hist + table * (p + 1) : nullptr;
             hipLaunchKernelGGL(k_radix_scatter<true>, dim3(tiles), dim3(BLOCK), 0, s, ki, vi, n,
-                               dbits * p, dbits, hist + table * p, tiles, ko, vo, next,
+                               dbits * p, dbits, items, hist + table * p, tiles, ko, vo, next,
                                dbits * (p + 1), dbits);
             uint32_t *t;
             t = ki, ki = ko, ko = t;
@@ -279,11 +314,11 @@ void launch_radix_sort(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *v1, i
         for (int p = 0; p < passes; ++p) {
             const int shift = dbits * p;
             hipLaunchKernelGGL(k_radix_hist, dim3(tiles), dim3(BLOCK), 0, s, ki, n, shift, dbits,
-                               hist, tiles, (uint32_t *)nullptr, (int64_t)0);
-            seg_scan(SegN{table}, 1, table, ValU32{hist}, OutU32{hist}, (uint32_t *)scan_tmp,
-                     (uint32_t *)nullptr, s, true);
+                               items, hist, tiles, (uint32_t *)nullptr, (int64_t)0);
+            seg_scan<uint32_t>(SegN{table}, 1, table, ValU32{hist}, OutU32{hist}, ws, s);
             hipLaunchKernelGGL(k_radix_scatter<false>, dim3(tiles), dim3(BLOCK), 0, s, ki, vi, n,
-                               shift, dbits, hist, tiles, ko, vo, (uint32_t *)nullptr, 0, dbits);
+                               shift, dbits, items, hist, tiles, ko, vo, (uint32_t *)nullptr, 0,
+                               dbits);
             uint32_t *t;
             t = ki, ki = ko, ko = t;
             t = vi, vi = vo, vo = t;
@@ -361,7 +396,7 @@ struct ChunkOut {
 // are recorded in the batch's own scal[2].
 void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, const int32_t *bag_off,
                    int32_t B, int64_t nnz, int key_bits, int chunk, uint32_t *tmp_k,
-                   uint32_t *tmp_v, uint32_t *hist, void *scan_tmp, hipEvent_t consumed,
+                   uint32_t *tmp_v, uint32_t *hist, ScanWs &ws, hipEvent_t consumed,
                    hipStream_t s)
 {
     const int64_t nbags = (int64_t)tb.T * B;
@@ -380,31 +415,34 @@ void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, cons
     hipEventRecord(consumed, s);  // the caller's arrays are not read after this point
     if (nnz > 0) {
         bool in_k1 = false;
-        launch_radix_sort(k0, v0, k1, v1, nnz, key_bits, hist, scan_tmp, &in_k1, s);
-        seg_scan(SegN{nnz}, 1, nnz, HeadFlag{b.skeys},
-                 UniqueOut{b.skeys, b.perm, b.bag_of, b.ukeys, b.inv, b.seg_off, b.sbag, b.scal,
-                           nnz},
-                 (uint32_t *)scan_tmp, (uint32_t *)nullptr, s);
-        seg_scan(SegDevN{b.scal}, 1, nnz, ChunkCount{b.seg_off, chunk},
-                 ChunkOut{b.seg_off, chunk, b.seg_chunk0, b.chunk_desc, b.multi, b.scal},
-                 (uint32_t *)scan_tmp,
-                 (uint32_t *)nullptr, s);
+        launch_radix_sort(k0, v0, k1, v1, nnz, key_bits, hist, ws, &in_k1, s, false);
+        seg_scan<uint32_t>(SegN{nnz}, 1, nnz, HeadFlag{b.skeys},
+                           UniqueOut{b.skeys, b.perm, b.bag_of, b.ukeys, b.inv, b.seg_off, b.sbag,
+                                     b.scal, nnz},
+                           ws, s);
+        seg_scan<uint32_t>(SegDevN{b.scal}, 1, nnz, ChunkCount{b.seg_off, chunk},
+                           ChunkOut{b.seg_off, chunk, b.seg_chunk0, b.chunk_desc, b.multi, b.scal},
+                           ws, s);
     }
 }
 
 // Copy the plan counters to pinned, device-mapped, host-coherent memory with
 // plain stores, so the host reads them after one stream synchronisation
-// without a separate copy command.
-__global__ void k_publish(const DevCounters *cnt, DevCounters *host_mapped)
+// without a separate copy command; then clear the per-plan counters for the
+// next query.
+__global__ void k_publish(DevCounters *cnt, DevCounters *host_mapped)
 {
     constexpr int N = (int)(sizeof(DevCounters) / sizeof(int32_t));
-    const int32_t *src = reinterpret_cast<const int32_t *>(cnt);
+    int32_t *src = reinterpret_cast<int32_t *>(cnt);
     int32_t *dst = reinterpret_cast<int32_t *>(host_mapped);
-    for (int i = threadIdx.x; i < N; i += blockDim.x) dst[i] = src[i];
+    for (int i = threadIdx.x; i < N; i += blockDim.x) {
+        dst[i] = src[i];
+        if (i < COUNTERS_CLEARED) src[i] = 0;
+    }
     __threadfence_system();
 }
 
-void launch_publish(const DevCounters *cnt, DevCounters *host_mapped, hipStream_t s)
+void launch_publish(DevCounters *cnt, DevCounters *host_mapped, hipStream_t s)
 {
     hipLaunchKernelGGL(k_publish, dim3(1), dim3(BLOCK), 0, s, cnt, host_mapped);
 }

@@ -127,11 +127,11 @@ struct MissOut {
 
 // Misses in ascending key order (the unique keys are sorted), so table t's
 // misses start at the sum of the miss counts of tables < t.
-void launch_miss_compact(const uint32_t *ukeys, int64_t n_unique, TicketDev tk, void *scan_tmp,
+void launch_miss_compact(const uint32_t *ukeys, int64_t n_unique, TicketDev tk, ScanWs &ws,
                          hipStream_t s)
 {
-    seg_scan(SegN{n_unique}, 1, n_unique, MissFlag{tk.hit}, MissOut{ukeys, tk.m_key, tk.m_uidx},
-             (uint32_t *)scan_tmp, (uint32_t *)nullptr, s);
+    seg_scan<uint32_t>(SegN{n_unique}, 1, n_unique, MissFlag{tk.hit},
+                       MissOut{ukeys, tk.m_key, tk.m_uidx}, ws, s);
 }
 
 // ---------------------------------------------------------------- LRU victims
@@ -145,7 +145,7 @@ void launch_miss_compact(const uint32_t *ukeys, int64_t n_unique, TicketDev tk, 
 // them in LRU order with ties in slot order.  sel_state[2a] = v* prefix,
 // sel_state[2a+1] = slots still to take at the current level.
 
-constexpr int SEL_ITEMS = 16;
+constexpr int SEL_ITEMS = 4;
 constexpr int SEL_CHUNK = BLOCK * SEL_ITEMS;
 
 __global__ void __launch_bounds__(BLOCK) k_sel_hist(SelArgs a, int shift, int first,
@@ -161,15 +161,19 @@ __global__ void __launch_bounds__(BLOCK) k_sel_hist(SelArgs a, int shift, int fi
     if (s0 < S) {
         const uint64_t want = first ? 0 : (uint64_t)(uint32_t)st[2 * ai] >> (shift + SEL_BITS);
         const int64_t base = a.base[ai];
+        int32_t hv[SEL_ITEMS], lv[SEL_ITEMS];
+#pragma unroll
+        for (int r = 0; r < SEL_ITEMS; ++r) {  // all loads in flight together
+            const int64_t s = s0 + (int64_t)r * BLOCK + threadIdx.x;
+            hv[r] = s < S ? held[base + s] : a.stamp;
+            lv[r] = s < S ? last_use[base + s] : 0;
+        }
+#pragma unroll
         for (int r = 0; r < SEL_ITEMS; ++r) {
-            int64_t s = s0 + (int64_t)r * BLOCK + threadIdx.x;
-            if (s < S) {
-                int64_t g = base + s;
-                if (held[g] != a.stamp) {
-                    uint32_t key = (uint32_t)(last_use[g] + 1);
-                    if (((uint64_t)key >> (shift + SEL_BITS)) == want)
-                        atomicAdd(&h[(key >> shift) & (SEL_BINS - 1)], 1);
-                }
+            if (hv[r] != a.stamp) {
+                const uint32_t key = (uint32_t)(lv[r] + 1);
+                if (((uint64_t)key >> (shift + SEL_BITS)) == want)
+                    atomicAdd(&h[(key >> shift) & (SEL_BINS - 1)], 1);
             }
         }
     }
@@ -180,9 +184,12 @@ __global__ void __launch_bounds__(BLOCK) k_sel_hist(SelArgs a, int shift, int fi
 }
 
 // One block per active table: fix the next SEL_BITS of v*.  The first level
-// starts from k misses still to place and an empty prefix.
+// starts from k misses still to place and an empty prefix, marks the table's
+// victim entries invalid (-1) before the compaction fills them, and clears
+// (all blocks together) the n_zero counters the victim sort accumulates into.
 __global__ void __launch_bounds__(BLOCK) k_sel_pick(SelArgs a, int shift, int first, int32_t *st,
-                                                    int32_t *hist)
+                                                    int32_t *hist, int32_t *victims,
+                                                    uint32_t *zero, int64_t n_zero)
 {
     __shared__ int32_t lds[BLOCK / WAVE];
     constexpr int PER = SEL_BINS / BLOCK;
@@ -214,6 +221,11 @@ __global__ void __launch_bounds__(BLOCK) k_sel_pick(SelArgs a, int shift, int fi
     // leave the histogram zeroed for the next level
 #pragma unroll
     for (int q = 0; q < PER; ++q) h[threadIdx.x * PER + q] = 0;
+    if (first) {
+        for (int i = threadIdx.x; i < a.k[ai]; i += BLOCK) victims[a.vbase[ai] + i] = -1;
+        for (int64_t i = (int64_t)ai * BLOCK + threadIdx.x; i < n_zero; i += (int64_t)a.nact * BLOCK)
+            zero[i] = 0;
+    }
 }
 
 struct SegAct {
@@ -240,8 +252,18 @@ struct VictimOut {
     int32_t vbase[MAX_TABLES], k[MAX_TABLES];
     int32_t lu_bits;
     uint32_t *vk, *vv;
+    uint32_t *hist0;                 // first sort pass's counters (digit-major), or null
+    uint32_t digit_mask, tile_len, tiles;
+    int64_t last[MAX_TABLES];        // last slot of each active table
+    int32_t *err;
     __device__ void operator()(int64_t g, uint64_t e, uint64_t v, int y) const
     {
+        if (g == last[y]) {  // every victim entry of the table must get a slot
+            const uint64_t tot = e + v;
+            const uint32_t below = (uint32_t)(tot >> 32), eq = (uint32_t)tot;
+            const uint32_t r = (uint32_t)st[2 * y + 1];
+            if (below + (eq < r ? eq : r) < (uint32_t)k[y]) atomicOr(err, ERR_PLAN);
+        }
         if (!v) return;
         const uint32_t below = (uint32_t)(e >> 32), eq = (uint32_t)e, r = (uint32_t)st[2 * y + 1];
         uint32_t pos;
@@ -250,26 +272,20 @@ struct VictimOut {
         else return;
         if (pos >= (uint32_t)k[y]) return;  // never write past the table's victims
         const int64_t idx = vbase[y] + pos;
-        vk[idx] = ((uint32_t)y << lu_bits) | (uint32_t)(last_use[g] + 1);
+        const uint32_t key = ((uint32_t)y << lu_bits) | (uint32_t)(last_use[g] + 1);
+        vk[idx] = key;
         vv[idx] = (uint32_t)g;
+        if (hist0) atomicAdd(&hist0[(key & digit_mask) * tiles + (uint32_t)idx / tile_len], 1u);
     }
 };
 
 void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int32_t *held,
                            const int32_t *last_use, int32_t *sel_state, int32_t *sel_hist,
                            uint32_t *vk0, uint32_t *vv0, uint32_t *vk1, uint32_t *vv1,
-                           int64_t n_victims, uint32_t *hist, void *scan_tmp, int32_t *v_slot,
-                           hipStream_t s)
+                           int64_t n_victims, uint32_t *hist, ScanWs &ws, int32_t *v_slot,
+                           int32_t *err, hipStream_t s)
 {
     if (a.nact <= 0 || n_victims <= 0) return;
-    const unsigned chunks = (unsigned)((maxS + SEL_CHUNK - 1) / SEL_CHUNK);
-    for (int l = 0; l < levels; ++l) {
-        int shift = (levels - 1 - l) * SEL_BITS;
-        hipLaunchKernelGGL(k_sel_hist, dim3(chunks, a.nact), dim3(BLOCK), 0, s, a, shift, (int)(l == 0),
-                           held, last_use, (const int32_t *)sel_state, sel_hist);
-        hipLaunchKernelGGL(k_sel_pick, dim3(a.nact), dim3(BLOCK), 0, s, a, shift, (int)(l == 0),
-                           sel_state, sel_hist);
-    }
     // compaction lands where the sort's last pass will end in v_slot
     const int bits = a.act_bits + a.lu_bits;
     const int passes = radix_passes(n_victims, bits);
@@ -277,6 +293,19 @@ void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int
     uint32_t *cv = (passes & 1) ? vv0 : (uint32_t *)v_slot;
     uint32_t *ok = (passes & 1) ? vk1 : vk0;
     uint32_t *ov = (passes & 1) ? (uint32_t *)v_slot : vv0;
+    // the compaction counts the sort's first digits when its passes are one
+    // launch each; their counters are cleared by the first pick
+    const RadixPlan rp = radix_plan(n_victims, bits);
+    const bool prehist = rp.passes > 0 && rp.fused;
+    const unsigned chunks = (unsigned)((maxS + SEL_CHUNK - 1) / SEL_CHUNK);
+    for (int l = 0; l < levels; ++l) {
+        int shift = (levels - 1 - l) * SEL_BITS;
+        hipLaunchKernelGGL(k_sel_hist, dim3(chunks, a.nact), dim3(BLOCK), 0, s, a, shift, (int)(l == 0),
+                           held, last_use, (const int32_t *)sel_state, sel_hist);
+        hipLaunchKernelGGL(k_sel_pick, dim3(a.nact), dim3(BLOCK), 0, s, a, shift, (int)(l == 0),
+                           sel_state, sel_hist, (int32_t *)cv, hist,
+                           prehist ? rp.table * rp.passes : (int64_t)0);
+    }
     SegAct seg;
     VictimOut out;
     for (int y = 0; y < a.nact; ++y) {
@@ -284,86 +313,93 @@ void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int
         seg.S[y] = a.S[y];
         out.vbase[y] = a.vbase[y];
         out.k[y] = a.k[y];
+        out.last[y] = a.base[y] + a.S[y] - 1;
     }
-    // holes (none if the selection is consistent) read as an invalid slot
-    launch_fill_i32((int32_t *)cv, n_victims, -1, s);
+    out.err = err;
     out.last_use = last_use;
     out.st = sel_state;
     out.lu_bits = a.lu_bits;
     out.vk = ck;
     out.vv = cv;
-    seg_scan(seg, a.nact, maxS, VictimFlag{held, last_use, sel_state, a.stamp}, out,
-             (uint64_t *)scan_tmp, (uint64_t *)nullptr, s);
+    out.hist0 = prehist ? hist : nullptr;
+    out.digit_mask = prehist ? (1u << rp.dbits) - 1u : 0u;
+    out.tile_len = prehist ? (uint32_t)(BLOCK * rp.items) : 1u;
+    out.tiles = prehist ? (uint32_t)rp.tiles : 0u;
+    seg_scan<uint64_t>(seg, a.nact, maxS, VictimFlag{held, last_use, sel_state, a.stamp}, out, ws,
+                       s);
     bool in_k1 = false;
-    launch_radix_sort(ck, cv, ok, ov, n_victims, bits, hist, scan_tmp, &in_k1, s);
+    launch_radix_sort(ck, cv, ok, ov, n_victims, bits, hist, ws, &in_k1, s, prehist);
 }
 
 // ---------------------------------------------------------------- commit
 
-// Miss i goes to victim slot i: record the slot's previous occupant and its
-// last use, erase that key from the Hit-Map, enter the new key.  Erases and
-// inserts may interleave across threads: inserts only claim EMPTY or erased
-// entries, so they never disturb a live key another thread is erasing, and
-// the keys inserted are known to be absent.
+// Threads [0, n_miss): miss i goes to victim slot v = v_slot[i]: record the
+// slot's previous occupant and its last use, erase that key from the Hit-Map,
+// enter the new key, then touch the slot (last_use = u) and point every
+// position of the key at it.  Erases and inserts may interleave across
+// threads: inserts only claim EMPTY or erased entries, so they never disturb
+// a live key another thread is erasing, and the keys inserted are known to be
+// absent.  Threads [n_miss, n_miss + max(n_unique, nnz)): touch the slots of
+// hits and point the positions of hit keys at them.  Victims are unheld and
+// hits are held, so the two groups never share a slot.
 __global__ void __launch_bounds__(BLOCK) k_commit(uint64_t *hash, uint32_t mask, TicketDev tk,
-                                                  int64_t n, int64_t nslots, int64_t n_unique,
-                                                  int32_t *key_of_slot, const int32_t *last_use,
-                                                  int32_t *err)
+                                                  const int32_t *inv, const int32_t *seg_off,
+                                                  const uint32_t *perm, int64_t n_miss,
+                                                  int64_t n_unique, int64_t nnz, int64_t nslots,
+                                                  int32_t *key_of_slot, int32_t *last_use,
+                                                  int32_t u, int32_t *err)
 {
-    int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
-    if (i >= n) return;
-    const int32_t v = tk.v_slot[i];
-    const int32_t ui = tk.m_uidx[i];
-    if ((uint32_t)v >= (uint64_t)nslots || (uint32_t)ui >= (uint64_t)n_unique) {
-        atomicOr(err, ERR_PLAN);
-        tk.v_old_key[i] = -1;
-        tk.v_old_lu[i] = -1;
+    const int64_t t = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    if (t < n_miss) {
+        const int64_t i = t;
+        const int32_t v = tk.v_slot[i];
+        const int32_t ui = tk.m_uidx[i];
+        if ((uint32_t)v >= (uint64_t)nslots || (uint32_t)ui >= (uint64_t)n_unique) {
+            atomicOr(err, ERR_PLAN);
+            tk.v_old_key[i] = -1;
+            tk.v_old_lu[i] = -1;
+            return;
+        }
+        const int32_t old = key_of_slot[v];
+        tk.v_old_key[i] = old;
+        tk.v_old_lu[i] = last_use[v];
+        if (old >= 0) hash_erase(hash, mask, (uint32_t)old);
+        const uint32_t key = tk.m_key[i];
+        key_of_slot[v] = (int32_t)key;
+        if (!hash_insert(hash, mask, key, v)) atomicOr(err, ERR_HASH_FULL);
+        tk.slot_u[ui] = v;
+        last_use[v] = u;
+        const int32_t p0 = seg_off[ui], p1 = seg_off[ui + 1];
+        for (int32_t p = p0; p < p1; ++p) {
+            const uint32_t j = perm[p];
+            if (j < (uint64_t)nnz) tk.slot_of[j] = v;
+        }
         return;
     }
-    const int32_t old = key_of_slot[v];
-    tk.v_old_key[i] = old;
-    tk.v_old_lu[i] = last_use[v];
-    if (old >= 0) hash_erase(hash, mask, (uint32_t)old);
-    const uint32_t key = tk.m_key[i];
-    key_of_slot[v] = (int32_t)key;
-    if (!hash_insert(hash, mask, key, v)) atomicOr(err, ERR_HASH_FULL);
-    tk.slot_u[ui] = v;
-}
-
-void launch_commit(const Tables &tb, uint64_t *hash, uint32_t mask, TicketDev tk, int64_t n_miss,
-                   int64_t n_unique, int32_t *key_of_slot, int32_t *last_use, DevCounters *cnt,
-                   hipStream_t s)
-{
-    if (n_miss <= 0) return;
-    const int64_t nslots = tb.slot_base[tb.T];
-    hipLaunchKernelGGL(k_commit, dim3((unsigned)((n_miss + BLOCK - 1) / BLOCK)), dim3(BLOCK), 0, s,
-                       hash, mask, tk, n_miss, nslots, n_unique, key_of_slot,
-                       (const int32_t *)last_use, &cnt->err_sticky);
-}
-
-// last_use = u for every slot the batch uses; slot_of[j] = slot of position j.
-__global__ void __launch_bounds__(BLOCK) k_touch_remap(TicketDev tk, const int32_t *inv,
-                                                       int64_t n_unique, int64_t nnz,
-                                                       int64_t nslots, int32_t *last_use, int32_t u)
-{
-    int64_t j = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
-    if (j < n_unique) {
+    const int64_t j = t - n_miss;
+    if (j < n_unique && tk.hit[j]) {
         const int32_t v = tk.slot_u[j];
         if ((uint32_t)v < (uint64_t)nslots) last_use[v] = u;
     }
     if (j < nnz) {
         const int32_t i = inv[j];
-        tk.slot_of[j] = (uint32_t)i < (uint64_t)n_unique ? tk.slot_u[i] : -1;
+        if ((uint32_t)i >= (uint64_t)n_unique) tk.slot_of[j] = -1;
+        else if (tk.hit[i]) tk.slot_of[j] = tk.slot_u[i];
     }
 }
 
-void launch_touch_remap(TicketDev tk, const BatchDev &b, int64_t n_unique, int64_t nnz,
-                        int64_t nslots, int32_t *last_use, int32_t u, hipStream_t s)
+void launch_commit(const Tables &tb, uint64_t *hash, uint32_t mask, TicketDev tk,
+                   const BatchDev &b, int64_t n_miss, int64_t n_unique, int64_t nnz,
+                   int32_t *key_of_slot, int32_t *last_use, int32_t u, DevCounters *cnt,
+                   hipStream_t s)
 {
-    int64_t n = nnz > n_unique ? nnz : n_unique;
+    const int64_t n = n_miss + (nnz > n_unique ? nnz : n_unique);
     if (n <= 0) return;
-    hipLaunchKernelGGL(k_touch_remap, dim3((unsigned)((n + BLOCK - 1) / BLOCK)), dim3(BLOCK), 0, s,
-                       tk, (const int32_t *)b.inv, n_unique, nnz, nslots, last_use, u);
+    const int64_t nslots = tb.slot_base[tb.T];
+    hipLaunchKernelGGL(k_commit, dim3((unsigned)((n + BLOCK - 1) / BLOCK)), dim3(BLOCK), 0, s,
+                       hash, mask, tk, (const int32_t *)b.inv, (const int32_t *)b.seg_off,
+                       (const uint32_t *)b.perm, n_miss, n_unique, nnz, nslots, key_of_slot,
+                       last_use, u, &cnt->err_sticky);
 }
 
 }  // namespace sp

@@ -191,29 +191,23 @@ __global__ void __launch_bounds__(BLOCK) k_bwd_combine(float4 *__restrict__ stor
 
 // ---------------------------------------------------------------- evict / fill
 
-// Copy the rows of occupied victim slots of one class into the staging rows
-// (row i of stage = victim i).  Class 1 = slots last used by the batch just
-// before this plan (their update may still be running), class 0 = the rest.
-// For victim i of the class: copy the row it held (if any) to staging row i
-// for the write-back, then fill the slot with the missing row m_key[i] read
-// straight from the pinned host table (zero-copy over the host link).  The
-// same lanes read the old row before writing the new one.  The class-0
-// launch also stores every victim's previous key after the n staging rows,
-// so rows and keys leave the device in one copy.
+// Victim i: copy the row its slot held (if any) to staging row i for the
+// write-back, then fill the slot with the missing row m_key[i] read straight
+// from the pinned host table (zero-copy over the host link).  The same lanes
+// read the old row before writing the new one.  Every victim's previous key
+// is stored after the n staging rows, so rows and keys leave the device in
+// one copy.
 template <int LPR>
 __global__ void __launch_bounds__(BLOCK) k_move(float4 *__restrict__ storage, Tables tb,
                                                 HostRows hr, TicketDev tk, int64_t n,
-                                                int64_t nslots, int32_t u, int cls,
-                                                float4 *__restrict__ stage)
+                                                int64_t nslots, float4 *__restrict__ stage)
 {
     const int64_t t = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
     const int64_t i = t / LPR;
     const int c = (int)(t % LPR);
     if (i >= n) return;
     const int32_t old = tk.v_old_key[i];
-    if (cls == 0 && c == 0) reinterpret_cast<int32_t *>(stage + n * LPR)[i] = old;
-    const int32_t lu = tk.v_old_lu[i];
-    if ((int)(lu >= 0 && lu == u - 1) != cls) return;
+    if (c == 0) reinterpret_cast<int32_t *>(stage + n * LPR)[i] = old;
     const int32_t v = tk.v_slot[i];
     if ((uint32_t)v >= (uint64_t)nslots) return;
     float4 *slot_row = storage + (int64_t)v * LPR + c;
@@ -250,14 +244,14 @@ static dim3 grid_waves(int64_t n)
 }
 
 void launch_move(float *storage, int dim, const Tables &tb, float *const *host_dev, TicketDev tk,
-                 int64_t n_miss, int32_t u, int cls, float *stage, hipStream_t s)
+                 int64_t n_miss, int32_t u, float *stage, hipStream_t s)
 {
     if (n_miss <= 0) return;
     const int D4 = dim / 4;
     HostRows hr{};
     for (int t = 0; t < tb.T; ++t) hr.p[t] = (const float4 *)host_dev[t];
     SP_DISPATCH_LPR(D4, k_move, grid_rows(n_miss, D4), (float4 *)storage, tb, hr, tk, n_miss,
-                    tb.slot_base[tb.T], u, cls, (float4 *)stage);
+                    tb.slot_base[tb.T], (float4 *)stage);
 }
 
 // Launches that may carry start/stop events: the events then time the kernel's

@@ -3,12 +3,12 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "sp_internal.h"
+
 namespace sp {
 
 constexpr int WAVE = 64;
 constexpr int BLOCK = 256;                 // 4 waves
-constexpr int SCAN_ITEMS = 8;
-constexpr int SCAN_TILE = BLOCK * SCAN_ITEMS;
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (WAVE - 1); }
 __device__ __forceinline__ int wave_id() { return threadIdx.x / WAVE; }
@@ -64,163 +64,162 @@ __device__ __forceinline__ T block_sum(T v, T *lds)
 
 // ---------------------------------------------------------------- segmented scan
 //
-// A segmented exclusive scan over index ranges.  Segment y covers
-// [seg.beg(y), seg.end(y)); blockIdx.y selects the segment, blockIdx.x a tile
-// of SCAN_TILE consecutive indices.  Three launches: tile sums, per-segment
-// scan of tile sums (one block per segment), then per-index exclusive prefixes
-// handed to out(i, prefix, value, y) in index order.  Values come from
-// val(i, y).
+// Segmented exclusive scan over index ranges in one launch (single pass with
+// decoupled look-back).  Segment y covers [seg.beg(y), seg.end(y)); values
+// come from val(i, y) and every index receives out(i, prefix, value, y).
+// Tiles of LB_TILE indices are handed out in launch order through an atomic
+// counter, so every tile a block looks back at belongs to a block that has
+// already started.  A tile publishes its own sum, then its inclusive prefix
+// once known; a successor adds published sums walking backwards until it
+// meets an inclusive prefix.  Published words carry the launch's epoch in
+// their upper half, so nothing is cleared between launches.  Values are one
+// 32-bit counter (uint32_t) or two independent 32-bit counters packed in a
+// uint64_t (low and high half, each sum below 2^32).
 
-template <class Seg, class Val, typename T>
-__global__ void __launch_bounds__(BLOCK) k_seg_tile_sums(Seg seg, Val val, T *tile_sums,
-                                                         int tiles)
-{
-    __shared__ T lds[BLOCK / WAVE];
-    const int y = blockIdx.y;
-    const int64_t beg = seg.beg(y), end = seg.end(y);
-    const int64_t base = beg + (int64_t)blockIdx.x * SCAN_TILE;
-    T acc = 0;
-    for (int r = 0; r < SCAN_ITEMS; ++r) {
-        int64_t i = base + (int64_t)r * BLOCK + threadIdx.x;
-        if (i < end) acc += val(i, y);
-    }
-    T s = block_sum(acc, lds);
-    if (threadIdx.x == 0) tile_sums[(int64_t)y * tiles + blockIdx.x] = s;
-}
-
-template <typename T>
-__global__ void __launch_bounds__(1024) k_seg_scan_tiles(T *tile_sums, int tiles, T *totals)
-{
-    __shared__ T lds[1024 / WAVE];
-    __shared__ T carry_s;
-    T *row = tile_sums + (int64_t)blockIdx.x * tiles;
-    if (threadIdx.x == 0) carry_s = 0;
-    __syncthreads();
-    for (int b = 0; b < tiles; b += 1024) {
-        int i = b + threadIdx.x;
-        T v = i < tiles ? row[i] : T(0);
-        T incl = wave_incl_scan(v);
-        if (lane_id() == WAVE - 1) lds[threadIdx.x / WAVE] = incl;
-        __syncthreads();
-        T base = 0, sum = 0;
-        for (int w = 0; w < 1024 / WAVE; ++w) {
-            T x = lds[w];
-            if (w < (int)(threadIdx.x / WAVE)) base += x;
-            sum += x;
-        }
-        T carry = carry_s;
-        if (i < tiles) row[i] = carry + base + incl - v;
-        __syncthreads();
-        if (threadIdx.x == 0) carry_s = carry + sum;
-        __syncthreads();
-    }
-    if (threadIdx.x == 0 && totals) totals[blockIdx.x] = carry_s;
-}
-
-template <class Seg, class Val, class Out, typename T>
-__global__ void __launch_bounds__(BLOCK) k_seg_apply(Seg seg, Val val, Out out,
-                                                     const T *tile_sums, int tiles)
-{
-    __shared__ T lds[BLOCK / WAVE];
-    const int y = blockIdx.y;
-    const int64_t beg = seg.beg(y), end = seg.end(y);
-    const int64_t base = beg + (int64_t)blockIdx.x * SCAN_TILE;
-    if (base >= end) return;  // uniform per block
-    T carry = tile_sums[(int64_t)y * tiles + blockIdx.x];
-    for (int r = 0; r < SCAN_ITEMS; ++r) {
-        int64_t i = base + (int64_t)r * BLOCK + threadIdx.x;
-        T v = i < end ? val(i, y) : T(0);
-        T total;
-        T e = block_excl_scan(v, lds, total);
-        if (i < end) out(i, carry + e, v, y);
-        carry += total;
-    }
-}
-
-// One contiguous range [0, *n) whose length lives on the device.
-struct SegDevN {
+struct SegDevN {  // one contiguous range [0, *n) whose length lives on the device
     const int32_t *n;
     __device__ int64_t beg(int) const { return 0; }
     __device__ int64_t end(int) const { return *n; }
 };
-// One contiguous range [0, n).
-struct SegN {
+struct SegN {  // one contiguous range [0, n)
     int64_t n;
     __device__ int64_t beg(int) const { return 0; }
     __device__ int64_t end(int) const { return n; }
 };
 
-// Small segments: one 1024-thread block per segment, each thread scanning
-// SS_ITEMS consecutive values in registers, block-wide scan of the thread sums.
-constexpr int SS_THREADS = 1024;
-constexpr int SS_ITEMS = 16;
-constexpr int64_t SMALL_SCAN = (int64_t)SS_THREADS * SS_ITEMS * 8;
+constexpr int LB_ITEMS = LB_TILE / BLOCK;
+static_assert(LB_ITEMS * BLOCK == LB_TILE, "scan tile must be a multiple of the block");
+constexpr int LB_SPIN = 1 << 16;     // polls before a look-back stops waiting
+
+struct ScanDev {
+    uint64_t *status;
+    uint32_t *counter;
+    int32_t *err;
+    uint32_t base, epoch, grid;
+    int32_t tiles;                   // per segment
+};
+
+template <typename T> struct LbHalves;
+template <> struct LbHalves<uint32_t> { static constexpr int N = 1; };
+template <> struct LbHalves<uint64_t> { static constexpr int N = 2; };
+
+template <typename T>
+__device__ __forceinline__ void lb_publish(uint64_t *w, uint32_t epoch, T v)
+{
+#pragma unroll
+    for (int c = 0; c < LbHalves<T>::N; ++c)
+        __hip_atomic_store(w + c, ((uint64_t)epoch << 32) | (uint32_t)((uint64_t)v >> (32 * c)),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Reads one half-set of words: true when every half carries this epoch.
+template <typename T>
+__device__ __forceinline__ bool lb_read(const uint64_t *w, uint32_t epoch, T &v)
+{
+    bool ok = true;
+    uint64_t acc = 0;
+#pragma unroll
+    for (int c = 0; c < LbHalves<T>::N; ++c) {
+        const uint64_t x = __hip_atomic_load(w + c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ok = ok && (uint32_t)(x >> 32) == epoch;
+        acc |= (uint64_t)(uint32_t)x << (32 * c);
+    }
+    v = (T)acc;
+    return ok;
+}
 
 template <class Seg, class Val, class Out, typename T>
-__global__ void __launch_bounds__(SS_THREADS) k_scan_single(Seg seg, Val val, Out out)
+__global__ void __launch_bounds__(BLOCK) k_scan_lookback(Seg seg, Val val, Out out, ScanDev d)
 {
-    __shared__ T lds[SS_THREADS / WAVE];
-    __shared__ T carry_s;
-    const int y = blockIdx.x;
-    const int64_t beg = seg.beg(y), end = seg.end(y);
-    if (threadIdx.x == 0) carry_s = 0;
+    __shared__ T lds[BLOCK / WAVE];
+    __shared__ T prefix_s;
+    __shared__ uint32_t id_s;
+    if (threadIdx.x == 0) id_s = atomicAdd(d.counter, 1u) - d.base;
     __syncthreads();
-    for (int64_t base = beg; base < end; base += (int64_t)SS_THREADS * SS_ITEMS) {
-        const int64_t i0 = base + (int64_t)threadIdx.x * SS_ITEMS;
-        T v[SS_ITEMS];
-        T sum = 0;
+    const uint32_t id = id_s;
+    if (id >= d.grid) {  // the counter and the host disagree: give up loudly
+        if (threadIdx.x == 0) atomicOr(d.err, ERR_PLAN);
+        return;
+    }
+    const int y = (int)(id / (uint32_t)d.tiles), x = (int)(id % (uint32_t)d.tiles);
+    const int64_t beg = seg.beg(y), end = seg.end(y);
+    const int64_t tbase = beg + (int64_t)x * LB_TILE;
+    if (tbase >= end) return;  // whole tile past the segment: no later tile of it needs us
+    const int64_t i0 = tbase + (int64_t)threadIdx.x * LB_ITEMS;
+    T v[LB_ITEMS];
+    T sum = 0;
 #pragma unroll
-        for (int q = 0; q < SS_ITEMS; ++q) {
-            const int64_t i = i0 + q;
-            v[q] = i < end ? val(i, y) : T(0);
-            sum += v[q];
+    for (int q = 0; q < LB_ITEMS; ++q) {
+        v[q] = i0 + q < end ? val(i0 + q, y) : T(0);
+        sum += v[q];
+    }
+    T total;
+    const T excl = block_excl_scan(sum, lds, total);
+    uint64_t *st = d.status + (int64_t)id * LB_WORDS;
+    if (threadIdx.x < WAVE) {
+        const int lane = threadIdx.x;
+        T prefix = 0;
+        if (x == 0) {
+            if (lane == 0) lb_publish(st + 2, d.epoch, total);
+        } else {
+            if (lane == 0) lb_publish(st, d.epoch, total);
+            const int64_t first = (int64_t)id - x;  // the segment's first tile
+            int64_t t = (int64_t)id - 1 - lane;
+            int spins = 0;
+            while (true) {
+                T pv = 0;
+                int state = 2;  // lanes before the segment act as a zero inclusive prefix
+                if (t >= first) {
+                    const uint64_t *w = d.status + t * LB_WORDS;
+                    state = lb_read(w + 2, d.epoch, pv) ? 2 : (lb_read(w, d.epoch, pv) ? 1 : 0);
+                }
+                const uint64_t incl = __ballot(state == 2);
+                const int stop = incl ? __ffsll((unsigned long long)incl) - 1 : WAVE;
+                const uint64_t need = stop >= WAVE - 1 ? ~0ull : ((2ull << stop) - 1ull);
+                if (__ballot(state == 0) & need) {
+                    if (++spins <= LB_SPIN) {
+                        __builtin_amdgcn_s_sleep(1);
+                        continue;
+                    }
+                    if (lane == 0) atomicOr(d.err, ERR_PLAN);  // counted as zero; result flagged wrong
+                }
+                prefix += wave_sum(lane <= stop && state != 0 ? pv : T(0));
+                if (stop < WAVE) break;
+                t -= WAVE;
+            }
+            if (lane == 0) lb_publish(st + 2, d.epoch, prefix + total);
         }
-        const T incl = wave_incl_scan(sum);
-        if (lane_id() == WAVE - 1) lds[threadIdx.x / WAVE] = incl;
-        __syncthreads();
-        T wbase = 0, tot = 0;
-        for (int w = 0; w < SS_THREADS / WAVE; ++w) {
-            const T x = lds[w];
-            if (w < (int)(threadIdx.x / WAVE)) wbase += x;
-            tot += x;
-        }
-        const T carry = carry_s;
-        T run = carry + wbase + incl - sum;
+        if (lane == 0) prefix_s = prefix;
+    }
+    __syncthreads();
+    T run = prefix_s + excl;
 #pragma unroll
-        for (int q = 0; q < SS_ITEMS; ++q) {
-            const int64_t i = i0 + q;
-            if (i < end) out(i, run, v[q], y);
-            run += v[q];
-        }
-        __syncthreads();
-        if (threadIdx.x == 0) carry_s = carry + tot;
-        __syncthreads();
+    for (int q = 0; q < LB_ITEMS; ++q) {
+        if (i0 + q < end) out(i0 + q, run, v[q], y);
+        run += v[q];
     }
 }
 
-// Launch the scan.  max_len bounds every segment's length; tile_sums needs
-// nseg * ceil(max_len / SCAN_TILE) entries; totals (optional) gets each
-// segment's sum (multi-block path only).  With one_block, segments of at most
-// SMALL_SCAN values take the one-block-per-segment path: one launch instead
-// of three, worth it only when val/out are cheap (no dependent global loads).
-template <class Seg, class Val, class Out, typename T>
-inline void seg_scan(Seg seg, int nseg, int64_t max_len, Val val, Out out, T *tile_sums,
-                     T *totals, hipStream_t s, bool one_block = false)
+// Launch the scan on stream s, which must be the only stream using ws.
+template <typename T, class Seg, class Val, class Out>
+inline void seg_scan(Seg seg, int nseg, int64_t max_len, Val val, Out out, ScanWs &ws,
+                     hipStream_t s)
 {
     if (nseg <= 0 || max_len <= 0) return;
-    if (one_block && max_len <= SMALL_SCAN && totals == nullptr) {
-        hipLaunchKernelGGL((k_scan_single<Seg, Val, Out, T>), dim3(nseg), dim3(SS_THREADS), 0, s,
-                           seg, val, out);
+    const int64_t tiles = (max_len + LB_TILE - 1) / LB_TILE;
+    const int64_t grid = tiles * nseg;
+    if (grid > ws.max_tiles) {
+        ws.overflow = true;
         return;
     }
-    int tiles = (int)((max_len + SCAN_TILE - 1) / SCAN_TILE);
-    dim3 grid(tiles, nseg);
-    hipLaunchKernelGGL((k_seg_tile_sums<Seg, Val, T>), grid, dim3(BLOCK), 0, s, seg, val,
-                       tile_sums, tiles);
-    hipLaunchKernelGGL((k_seg_scan_tiles<T>), dim3(nseg), dim3(1024), 0, s, tile_sums, tiles,
-                       totals);
-    hipLaunchKernelGGL((k_seg_apply<Seg, Val, Out, T>), grid, dim3(BLOCK), 0, s, seg, val, out,
-                       (const T *)tile_sums, tiles);
+    if (ws.epoch == 0xFFFFFFFFu) {  // epochs wrapped: forget every published word
+        (void)hipMemsetAsync(ws.status, 0, sizeof(uint64_t) * LB_WORDS * ws.max_tiles, s);
+        ws.epoch = 0;
+    }
+    ScanDev d{ws.status, ws.counter, ws.err, ws.issued, ++ws.epoch, (uint32_t)grid, (int32_t)tiles};
+    ws.issued += (uint32_t)grid;
+    hipLaunchKernelGGL((k_scan_lookback<Seg, Val, Out, T>), dim3((unsigned)grid), dim3(BLOCK), 0,
+                       s, seg, val, out, d);
 }
 
 // ---------------------------------------------------------------- Hit-Map hash

@@ -8,9 +8,28 @@ namespace sp {
 
 constexpr int MAX_TABLES = 64;
 constexpr int MAX_WINDOW = 16;   // batches one plan may look at (lookahead <= 15)
-constexpr int TICKETS = 4;       // ticket ring depth
 constexpr int SEL_BITS = 11;     // digit width of the LRU radix select
 constexpr int SEL_BINS = 1 << SEL_BITS;
+
+// Single-pass scan: indices per tile, published words per tile (sum and
+// inclusive prefix, two 32-bit halves each), tiles of nseg segments.
+constexpr int LB_TILE = 2048;
+constexpr int LB_WORDS = 4;
+inline int64_t scan_tiles(int nseg, int64_t max_len)
+{
+    return (int64_t)nseg * ((max_len + LB_TILE - 1) / LB_TILE);
+}
+
+// Workspace of the single-pass scan; each stream that runs scans owns one.
+struct ScanWs {
+    uint64_t *status = nullptr;   // [4 * max_tiles] tile sums published by the scan, epoch-tagged
+    uint32_t *counter = nullptr;  // tiles handed out so far (wraps)
+    int32_t *err = nullptr;       // gets ERR_PLAN when a look-back stops waiting
+    int64_t max_tiles = 0;
+    uint32_t issued = 0;          // value *counter holds once every launch so far has run
+    uint32_t epoch = 0;           // tag of the last launch
+    bool overflow = false;        // a scan needed more than max_tiles tiles and was skipped
+};
 
 // Per-table constants passed by value to kernels.
 struct Tables {
@@ -21,8 +40,9 @@ struct Tables {
 };
 
 // Counters written by the planning kernels and copied to the host once per plan.
-// Everything before err_sticky is cleared at the start of each plan;
-// err_sticky collects errors of later plan stages and is never cleared.
+// Everything before err_sticky is cleared right after each copy, ready for
+// the next query; err_sticky collects errors of later plan stages and of the
+// scans and is never cleared.
 struct DevCounters {
     int32_t err;                 // ERR_* bits of this plan's window (ids, offsets)
     int32_t n_unique;            // unique keys of the planned batch
@@ -83,13 +103,23 @@ void launch_zero_i32(int32_t *p, int64_t n, hipStream_t s);
 void launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
 void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, const int32_t *bag_off,
                    int32_t B, int64_t nnz, int key_bits, int chunk, uint32_t *tmp_k,
-                   uint32_t *tmp_v, uint32_t *hist, void *scan_tmp, hipEvent_t consumed,
+                   uint32_t *tmp_v, uint32_t *hist, ScanWs &ws, hipEvent_t consumed,
                    hipStream_t s);
-void launch_publish(const DevCounters *cnt, DevCounters *host_mapped, hipStream_t s);
+void launch_publish(DevCounters *cnt, DevCounters *host_mapped, hipStream_t s);
 void launch_radix_sort(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *v1, int64_t n,
-                       int bits, uint32_t *hist, void *scan_tmp, bool *in_k1, hipStream_t s);
+                       int bits, uint32_t *hist, ScanWs &ws, bool *in_k1, hipStream_t s,
+                       bool prehist);
 int64_t radix_hist_entries(int64_t n);
 int radix_passes(int64_t n, int bits);  // passes launch_radix_sort makes (result in k1 if odd)
+// Layout of a sort of n keys of `bits` bits: passes of dbits-wide digits over
+// tiles of BLOCK * items keys; one-launch passes (fused) when the per-pass
+// table of (1 << dbits) x tiles counters has at most 16384 entries.
+struct RadixPlan {
+    int passes, dbits, items;
+    int64_t tiles, table;
+    bool fused;
+};
+RadixPlan radix_plan(int64_t n, int bits);
 
 // k_plan.hip
 void launch_probe_hold(const Tables &tb, const uint64_t *hash, uint32_t mask,
@@ -98,22 +128,23 @@ void launch_probe_hold(const Tables &tb, const uint64_t *hash, uint32_t mask,
                        DevCounters *cnt, const int32_t *scal0, hipStream_t s);
 void launch_hash_rebuild(uint64_t *hash, uint32_t mask, const int32_t *key_of_slot, int64_t nslots,
                          DevCounters *cnt, hipStream_t s);
-void launch_miss_compact(const uint32_t *ukeys, int64_t n_unique, TicketDev tk, void *scan_tmp,
+void launch_miss_compact(const uint32_t *ukeys, int64_t n_unique, TicketDev tk, ScanWs &ws,
                          hipStream_t s);
 void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int32_t *held,
                            const int32_t *last_use, int32_t *sel_state, int32_t *sel_hist,
                            uint32_t *vk0, uint32_t *vv0, uint32_t *vk1, uint32_t *vv1,
-                           int64_t n_victims, uint32_t *hist, void *scan_tmp, int32_t *v_slot,
-                           hipStream_t s);
-void launch_commit(const Tables &tb, uint64_t *hash, uint32_t mask, TicketDev tk, int64_t n_miss,
-                   int64_t n_unique, int32_t *key_of_slot, int32_t *last_use, DevCounters *cnt,
+                           int64_t n_victims, uint32_t *hist, ScanWs &ws, int32_t *v_slot,
+                           int32_t *err, hipStream_t s);
+// Misses into their victim slots, Hit-Map and slot metadata updated, every
+// slot the batch uses touched (last_use = u), slot_of filled.
+void launch_commit(const Tables &tb, uint64_t *hash, uint32_t mask, TicketDev tk,
+                   const BatchDev &b, int64_t n_miss, int64_t n_unique, int64_t nnz,
+                   int32_t *key_of_slot, int32_t *last_use, int32_t u, DevCounters *cnt,
                    hipStream_t s);
-void launch_touch_remap(TicketDev tk, const BatchDev &b, int64_t n_unique, int64_t nnz,
-                        int64_t nslots, int32_t *last_use, int32_t u, hipStream_t s);
 
 // k_train.hip
 void launch_move(float *storage, int dim, const Tables &tb, float *const *host_dev, TicketDev tk,
-                 int64_t n_miss, int32_t u, int cls, float *stage, hipStream_t s);
+                 int64_t n_miss, int32_t u, float *stage, hipStream_t s);
 void launch_forward(const float *storage, int dim, int64_t nslots, const int32_t *slot_of,
                     const int32_t *bag_off, int64_t nbags, float *out, hipStream_t s,
                     hipEvent_t e0, hipEvent_t e1);

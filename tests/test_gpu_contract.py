@@ -133,6 +133,49 @@ def test_rejected_plans_leave_state_unchanged(harness, lookahead):
         host.close()
 
 
+def test_bad_prepared_batch_fails_the_plan_that_holds_it(harness):
+    """A batch handed over early as the prepared-ahead batch is read once.  Bad
+    content in it does not affect the plan it was handed to; the next plan,
+    whose window holds it, is rejected whatever is passed, and a retry with
+    good content re-reads it.  Continuing matches the oracle."""
+    import torch
+    from oracle import oracle
+    w = wl.custom(rows=[1500, 2500], dim=32, batch=24, pooling=[3, 2], slots=[300, 260],
+                  lookahead=2, steps=14, dist=("zipf", 1.0), seed=37)
+    _say("case bad prepared-ahead batch")
+    batches = harness.make_inputs(w)
+    host = harness.fresh_host(w)
+    ref = [wl.init_table(w, t) for t in range(w.tables)]
+    planner = oracle.Planner(w.rows, w.slots)
+    ctx = spm.ScratchPipe(w.rows, w.dim, w.slots, w.lookahead, host, w.batch, 4096)
+    out = torch.zeros((w.tables * w.batch, w.dim), device="cuda:0")
+    L, n = w.lookahead, w.steps
+    try:
+        for u in range(n):
+            held = batches[u:min(u + L, n - 1) + 1]
+            ahead = [batches[u + L + 1]] if u + L + 1 < n else []
+            if u == 4:
+                tail = ahead[0]
+                ahead = [_bad_ids(tail, w, 1, w.rows[1] + 7)]
+            if u == 5:
+                with pytest.raises(spm.SPError) as e:
+                    ctx.plan(held + ahead)
+                assert e.value.status == spm.SP_ERR_INVALID_ARG
+            t = ctx.plan(held + ahead)
+            p = planner.plan(held, w.batch)
+            harness.compare_plan(u, ctx.debug_plan(t, int(held[0][0].size)), p, w.tables, w.batch)
+            ctx.forward(t, out)
+            g = wl.grads(w, u)
+            ctx.backward_update(t, torch.from_numpy(g).to("cuda:0"), w.lr)
+            oracle.train_step(ref, *batches[u], w.batch, g, w.lr)
+        ctx.flush()
+        for t in range(w.tables):
+            assert harness.row_rel_err(host[t], ref[t]).max() <= harness.REL_TOL
+    finally:
+        ctx.close()
+        host.close()
+
+
 def test_overlapped_equals_serialized_bit_for_bit(harness):
     """The overlapped schedule (plan of the next batch while this one trains,
     fills and write-backs on side streams) gives exactly the tables of a run

@@ -216,6 +216,8 @@ def main():
                        "combine_launches": d["timed_combine"],
                        "plan_ms": round(d["ms_plan"] / max(d["timed_plan"], 1), 5),
                        "fill_ms": round(d["ms_fill"] / max(d["timed_fill"], 1), 5),
+                       "ingest_ms": round(d["ms_ingest"] / max(d["timed_ingest"], 1), 5),
+                       "query_ms": round(d["ms_query"] / max(d["timed_query"], 1), 5),
                        "chunks_per_step": round(n_chunks, 1),
                        "forward_GBps_unique": round(fwd_gbs, 1),
                        "forward_GBps_requested": round(kb["forward_requested"] / (fwd_ms * 1e-3) / 1e9, 1),

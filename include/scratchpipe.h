@@ -91,13 +91,19 @@ typedef struct {
     /* SP_FLAG_TIMING only: summed time in ms and number of timed launches.
      * forward, backward (per-chunk kernel) and combine (runs split over several
      * chunks, launched only when there are any) are kernel execution times;
-     * plan and fill span their whole launch sequences. */
+     * plan (the commit sequence: victims, Hit-Map, slot metadata) and fill
+     * (evicted-row staging and miss fill) span their launch sequences. */
     double ms_forward, ms_backward, ms_combine, ms_plan, ms_fill;
     int64_t timed_forward, timed_backward, timed_combine, timed_plan, timed_fill;
     /* host time spent inside sp_plan, in ms: enqueueing ingest, enqueueing the
      * query, waiting for its counts, enqueueing the commit, and the mover
      * (including waits for the write-back thread) */
     double host_ms_ingest, host_ms_query, host_ms_wait, host_ms_commit, host_ms_mover;
+    /* SP_FLAG_TIMING only: ingest of a batch (keys, sort, dedup, backward
+     * chunks) and the query of a plan (hold marks and probe, from the moment
+     * its stream reaches it, waits for ingests included) */
+    double ms_ingest, ms_query;
+    int64_t timed_ingest, timed_query;
 } sp_stats;
 
 /* Per-plan decisions copied to the host for checking.  The caller allocates

@@ -305,7 +305,7 @@ struct sp_ctx {
 
     // bookkeeping
     sp_stats st{};
-    Timer t_fwd, t_bwd, t_cmb, t_plan, t_fill;
+    Timer t_fwd, t_bwd, t_cmb, t_plan, t_fill, t_ing, t_qry;
     int64_t dev_bytes = 0, pinned_bytes = 0;
     double host_ms[5] = {0, 0, 0, 0, 0};  // ingest, query, wait, commit, mover (sp_plan)
     std::vector<void *> dev_allocs, pinned_allocs;
@@ -456,6 +456,8 @@ static void release(sp_ctx *h)
     h->t_cmb.destroy();
     h->t_plan.destroy();
     h->t_fill.destroy();
+    h->t_ing.destroy();
+    h->t_qry.destroy();
     if (h->s_plan) hipStreamDestroy(h->s_plan);
     if (h->s_ingest) hipStreamDestroy(h->s_ingest);
     if (h->s_move) hipStreamDestroy(h->s_move);
@@ -615,6 +617,8 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     HIPCHK(nullptr, h->t_cmb.init());
     HIPCHK(nullptr, h->t_plan.init());
     HIPCHK(nullptr, h->t_fill.init());
+    HIPCHK(nullptr, h->t_ing.init());
+    HIPCHK(nullptr, h->t_qry.init());
 
     // initial state: nothing cached
     HIPCHK(nullptr, hipMemsetAsync(h->key_of_slot, 0xFF, sizeof(int32_t) * S, h->s_plan));
@@ -714,6 +718,8 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
     BatchDev &b = h->ring[r];
     // the previous occupant (batch q - nring) must be done with its backward
     HIPCHK(h, hipStreamWaitEvent(h->s_ingest, h->ev_upd[r], 0));
+    const bool timing = h->flags & SP_FLAG_TIMING;
+    if (timing) HIPCHK(h, h->t_ing.begin(h->s_ingest));
     const int64_t nbags = (int64_t)h->T * bt.batch;
     const int32_t *ids = bt.ids, *off = bt.bag_off;
     if (!bt.on_device) {  // host arrays: copy into the ring first
@@ -730,6 +736,7 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
     CHECK_LAUNCH(h);
     if (h->ws_ingest.overflow) return fail(h, SP_ERR_HIP, "internal: scan workspace too small");
     HIPCHK(h, hipEventRecord(h->ring_ready[r], h->s_ingest));
+    if (timing) HIPCHK(h, h->t_ing.end(h->s_ingest));
     h->ring_seen[r] = 0;
     h->ring_batch[r] = q;
     h->ring_nnz[r] = bt.nnz;
@@ -743,6 +750,8 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
 static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, int32_t *stamp_out)
 {
     const int e = (int)(k % h->nring);
+    const bool timing = h->flags & SP_FLAG_TIMING;
+    if (timing) HIPCHK(h, h->t_qry.begin(h->s_plan));
     // the ticket buffers being reused belonged to ticket k - nring
     if (k >= h->nring) HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ev_upd[e], 0));
     const uint32_t *ukeys[MAX_WINDOW];
@@ -763,6 +772,7 @@ static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, int32_t *stamp_o
                       h->tk[e], h->cnt, h->ring[k % h->nring].scal, h->s_plan);
     launch_publish(h->cnt, h->h_cnt_dev, h->s_plan);  // also clears the counters
     CHECK_LAUNCH(h);
+    if (timing) HIPCHK(h, h->t_qry.end(h->s_plan));
     *stamp_out = stamp;
     return SP_OK;
 }
@@ -909,6 +919,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     CHECK_LAUNCH(h);
     if (h->ws_plan.overflow) return fail(h, SP_ERR_HIP, "internal: scan workspace too small");
     HIPCHK(h, hipEventRecord(h->ev_planned[e], h->s_plan));
+    if (timing) HIPCHK(h, h->t_plan.end(h->s_plan));
     double tF = host_ms();
     h->host_ms[3] += tF - tE;
     // ---- the next plan's query, when its whole window is known: batches
@@ -918,7 +929,6 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
         h->spec_ticket = k + 1;
         h->spec_nhold = h->L + 1;
     }
-    if (timing) HIPCHK(h, h->t_plan.end(h->s_plan));
     const double tG = host_ms();
     h->host_ms[1] += tG - tF;
     tF = tG;
@@ -1084,6 +1094,8 @@ extern "C" sp_status sp_get_stats(sp_handle h, sp_stats *out)
     HIPCHK(h, h->t_cmb.flush());
     HIPCHK(h, h->t_plan.flush());
     HIPCHK(h, h->t_fill.flush());
+    HIPCHK(h, h->t_ing.flush());
+    HIPCHK(h, h->t_qry.flush());
     sp_stats s = h->st;
     {
         std::lock_guard<std::mutex> lk(h->mu);
@@ -1108,6 +1120,10 @@ extern "C" sp_status sp_get_stats(sp_handle h, sp_stats *out)
     s.host_ms_mover = h->host_ms[4];
     s.timed_plan = h->t_plan.count;
     s.timed_fill = h->t_fill.count;
+    s.ms_ingest = h->t_ing.ms;
+    s.ms_query = h->t_qry.ms;
+    s.timed_ingest = h->t_ing.count;
+    s.timed_query = h->t_qry.count;
     *out = s;
     return SP_OK;
 }

@@ -196,27 +196,31 @@ __global__ void __launch_bounds__(BLOCK) k_bwd_combine(float4 *__restrict__ stor
 // from the pinned host table (zero-copy over the host link).  The same lanes
 // read the old row before writing the new one.  Every victim's previous key
 // is stored after the n staging rows, so rows and keys leave the device in
-// one copy.
+// one copy.  The grid is kept small (lane groups stride over the victims):
+// waves waiting on the host link then occupy few compute units, and the
+// kernels running beside this one keep the rest.
+constexpr int MOVE_MAX_BLOCKS = 128;
+
 template <int LPR>
 __global__ void __launch_bounds__(BLOCK) k_move(float4 *__restrict__ storage, Tables tb,
                                                 HostRows hr, TicketDev tk, int64_t n,
                                                 int64_t nslots, float4 *__restrict__ stage)
 {
-    const int64_t t = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
-    const int64_t i = t / LPR;
-    const int c = (int)(t % LPR);
-    if (i >= n) return;
-    const int32_t old = tk.v_old_key[i];
-    if (c == 0) reinterpret_cast<int32_t *>(stage + n * LPR)[i] = old;
-    const int32_t v = tk.v_slot[i];
-    if ((uint32_t)v >= (uint64_t)nslots) return;
-    float4 *slot_row = storage + (int64_t)v * LPR + c;
-    if (old >= 0) stage[i * LPR + c] = *slot_row;
-    const uint32_t key = tk.m_key[i];
-    const int tab = (int)(key >> tb.row_bits);
-    const int64_t row = key & ((1u << tb.row_bits) - 1u);
-    if (tab >= tb.T || row >= tb.rows[tab]) return;
-    *slot_row = hr.p[tab][row * LPR + c];
+    const int c = (int)(threadIdx.x % LPR);
+    const int64_t step = (int64_t)gridDim.x * (BLOCK / LPR);
+    for (int64_t i = ((int64_t)blockIdx.x * BLOCK + threadIdx.x) / LPR; i < n; i += step) {
+        const int32_t old = tk.v_old_key[i];
+        if (c == 0) reinterpret_cast<int32_t *>(stage + n * LPR)[i] = old;
+        const int32_t v = tk.v_slot[i];
+        if ((uint32_t)v >= (uint64_t)nslots) continue;
+        float4 *slot_row = storage + (int64_t)v * LPR + c;
+        if (old >= 0) stage[i * LPR + c] = *slot_row;
+        const uint32_t key = tk.m_key[i];
+        const int tab = (int)(key >> tb.row_bits);
+        const int64_t row = key & ((1u << tb.row_bits) - 1u);
+        if (tab >= tb.T || row >= tb.rows[tab]) continue;
+        *slot_row = hr.p[tab][row * LPR + c];
+    }
 }
 
 // ---------------------------------------------------------------- dispatch
@@ -250,7 +254,9 @@ void launch_move(float *storage, int dim, const Tables &tb, float *const *host_d
     const int D4 = dim / 4;
     HostRows hr{};
     for (int t = 0; t < tb.T; ++t) hr.p[t] = (const float4 *)host_dev[t];
-    SP_DISPATCH_LPR(D4, k_move, grid_rows(n_miss, D4), (float4 *)storage, tb, hr, tk, n_miss,
+    dim3 grid = grid_rows(n_miss, D4);
+    grid.x = grid.x < (unsigned)MOVE_MAX_BLOCKS ? grid.x : (unsigned)MOVE_MAX_BLOCKS;
+    SP_DISPATCH_LPR(D4, k_move, grid, (float4 *)storage, tb, hr, tk, n_miss,
                     tb.slot_base[tb.T], (float4 *)stage);
 }
 

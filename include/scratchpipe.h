@@ -191,6 +191,10 @@ sp_status sp_flush(sp_handle h);
 /* Counters since sp_create (synchronises pending timing events). */
 sp_status sp_get_stats(sp_handle h, sp_stats *out);
 
+/* Replace the context's SP_FLAG_* bits for the calls that follow, e.g. to
+ * time only a sample of the steps.  SP_ERR_INVALID_ARG for unknown bits. */
+sp_status sp_set_flags(sp_handle h, uint32_t flags);
+
 /* Copy the decisions of the most recent plan (ticket must equal it) to host
  * arrays; for checking against a reference.  Synchronises the library stream. */
 sp_status sp_debug_plan(sp_handle h, int64_t ticket, sp_plan_dump *out);

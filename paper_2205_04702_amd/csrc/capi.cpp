@@ -1084,6 +1084,14 @@ extern "C" sp_status sp_flush(sp_handle h)
     return SP_OK;
 }
 
+extern "C" sp_status sp_set_flags(sp_handle h, uint32_t flags)
+{
+    TRY(usable(h));
+    if (flags & ~(SP_FLAG_DEBUG_SYNC | SP_FLAG_TIMING)) return fail(h, SP_ERR_INVALID_ARG, "unknown flags");
+    h->flags = flags;
+    return SP_OK;
+}
+
 extern "C" sp_status sp_get_stats(sp_handle h, sp_stats *out)
 {
     TRY(usable(h));

@@ -92,6 +92,7 @@ def load():
         L.sp_backward_update.argtypes = [h, C.c_int64, C.c_void_p, C.c_float, C.c_void_p]
         L.sp_flush.argtypes = [h]
         L.sp_get_stats.argtypes = [h, C.POINTER(sp_stats)]
+        L.sp_set_flags.argtypes = [h, C.c_uint32]
         L.sp_debug_plan.argtypes = [h, C.c_int64, C.POINTER(sp_plan_dump)]
         L.sp_destroy.argtypes = [h]
         L.sp_destroy.restype = None
@@ -101,7 +102,7 @@ def load():
         L.sp_host_free.argtypes = [C.c_void_p]
         L.sp_host_free.restype = None
         for n in ("sp_create", "sp_plan", "sp_forward", "sp_backward_update", "sp_flush",
-                  "sp_get_stats", "sp_debug_plan", "sp_host_alloc"):
+                  "sp_get_stats", "sp_set_flags", "sp_debug_plan", "sp_host_alloc"):
             getattr(L, n).restype = C.c_int32
         _lib = L
     return _lib
@@ -153,6 +154,10 @@ def sp_get_stats(handle: int) -> dict:
     s = sp_stats()
     _check(load().sp_get_stats(handle, C.byref(s)), handle)
     return {n: getattr(s, n) for n, _ in sp_stats._fields_}
+
+
+def sp_set_flags(handle: int, flags: int) -> None:
+    _check(load().sp_set_flags(handle, flags), handle)
 
 
 def sp_debug_plan(handle: int, ticket: int, nnz_cap: int) -> dict:
@@ -297,6 +302,9 @@ class ScratchPipe:
 
     def stats(self) -> dict:
         return sp_get_stats(self.handle)
+
+    def set_flags(self, flags: int) -> None:
+        sp_set_flags(self.handle, flags)
 
     def debug_plan(self, ticket: int, nnz: int) -> dict:
         return sp_debug_plan(self.handle, ticket, nnz)

@@ -115,6 +115,7 @@ def test_null_handle_calls_report_state_error():
     assert L.sp_forward(None, 0, None, None) == sp.SP_ERR_STATE
     assert L.sp_backward_update(None, 0, None, C.c_float(0.1), None) == sp.SP_ERR_STATE
     assert L.sp_flush(None) == sp.SP_ERR_STATE
+    assert L.sp_set_flags(None, 0) == sp.SP_ERR_STATE
     L.sp_destroy(None)
 
 

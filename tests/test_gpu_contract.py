@@ -248,3 +248,39 @@ def test_stats_account_for_every_lookup(harness):
     assert st["evictions"] <= st["misses"]
     assert st["timed_forward"] == w.steps and st["ms_forward"] > 0
     assert st["min_capacity_margin"] >= 0
+
+
+def test_timing_can_be_sampled_per_step(harness):
+    """sp_set_flags switches kernel timing for the calls that follow; timed
+    launch counts match the sampled steps and the trained tables do not depend
+    on which steps were timed."""
+    import torch
+    w = _small()
+    _say("case sampled timing")
+    batches = harness.make_inputs(w)
+    L = w.lookahead
+    results = []
+    for every in (0, 3):
+        host = harness.fresh_host(w)
+        ctx = spm.ScratchPipe(w.rows, w.dim, w.slots, L, host, w.batch, 4096)
+        out = torch.zeros((w.tables * w.batch, w.dim), device="cuda:0")
+        try:
+            for u in range(w.steps):
+                if every:
+                    ctx.set_flags(spm.SP_FLAG_TIMING if u % every == 0 else 0)
+                t = ctx.plan(batches[u:min(u + L + 1, w.steps - 1) + 1])
+                ctx.forward(t, out)
+                ctx.backward_update(t, torch.from_numpy(wl.grads(w, u)).to("cuda:0"), w.lr)
+            st = ctx.stats()
+            ctx.flush()
+        finally:
+            ctx.close()
+        n_timed = len(range(0, w.steps, every)) if every else 0
+        assert st["timed_forward"] == n_timed and st["timed_backward"] == n_timed
+        assert st["timed_plan"] == n_timed
+        results.append([host[t].copy() for t in range(w.tables)])
+        host.close()
+    with pytest.raises(spm.SPError) as e:
+        spm.sp_set_flags(0, 0)
+    for x, y in zip(*results):
+        assert np.array_equal(x, y)

@@ -94,6 +94,9 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="zipf-8x1M")
+    ap.add_argument("--tables", type=int, default=0, metavar="N",
+                    help="run only the workload's first N tables (one GPU's share when the "
+                         "pinned host tables of the whole workload exceed what one process maps)")
     ap.add_argument("--host-ids", action="store_true",
                     help="hand the batch IDs over from host memory (PCIe-inclusive variant)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -118,6 +121,11 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     w = wl.get_workload(args.workload)
+    if args.tables > 0:
+        import dataclasses
+        n = args.tables
+        w = dataclasses.replace(w, name=f"{w.name}-first{n}", rows=w.rows[:n],
+                                pooling=w.pooling[:n], dist=w.dist[:n], slots=w.slots[:n])
     W, K, L = args.warmup, args.steps, w.lookahead
     nb = W + K + L + 1  # the window of the last step plus the batch prepared after it
     log(f"[bench] workload {w.name}: generating {nb} batches and {W + K} gradient tensors")

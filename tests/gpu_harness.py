@@ -143,3 +143,103 @@ def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all"
     tables = [host[t].copy() for t in range(T)] if return_tables else None
     host.close()
     return {"stats": stats, "worst_fwd": worst_fwd, "worst_table": worst_tab, "tables": tables}
+
+
+# ----------------------------------------------------------------------------- full-size configs
+
+def touched_rows(w, batches, steps):
+    """Per table: sorted unique rows read by batches[0:steps], the only rows training touches."""
+    T, B = w.tables, w.batch
+    out = []
+    for t in range(T):
+        parts = [b[0][int(b[1][t * B]):int(b[1][(t + 1) * B])] for b in batches[:steps]]
+        out.append(np.unique(np.concatenate(parts)) if parts else np.zeros(0, np.int32))
+    return out
+
+
+def row_values(t, rows, dim):
+    """Deterministic values in [-0.05, 0.05) for (table, row, column); cheap to make for a
+    few rows of a huge table (full initialisation of 100+ GB would dominate the test)."""
+    r = np.asarray(rows, dtype=np.int64)[:, None]
+    c = np.arange(dim, dtype=np.int64)[None, :]
+    h = (r * 2654435761 + c * 40503 + (t + 1) * 977) % 2003
+    return ((h - 1001) * (0.05 / 1002)).astype(np.float32)
+
+
+def run_sampled_parity(w, steps, *, check_plan_steps, check_fwd_steps, say=print):
+    """A full-size workload driven as the benchmark drives it (IDs in device memory, the batch
+    after the window handed over early) for `steps` steps.
+
+    Only rows that the trained batches read are initialised (plus sentinel rows elsewhere);
+    the oracle trains compact copies of exactly those rows (uncached training touches no
+    other row, so its arithmetic is the same).  Checks: plans bit-exact against the
+    reference planner at `check_plan_steps`, forward outputs at `check_fwd_steps`, every
+    touched row after flush, and sentinel rows unchanged."""
+    import time
+    import torch
+    dev = torch.device("cuda:0")
+    T, B, D, L = w.tables, w.batch, w.dim, w.lookahead
+    t0 = time.perf_counter()
+    batches = [wl.batch(w, s) for s in range(steps + L + 1)]
+    rows = touched_rows(w, batches, steps)
+    say(f"  inputs {time.perf_counter() - t0:.1f}s, touched rows {sum(r.size for r in rows)}")
+    host = HostTables(w.rows, D)
+    ref = []
+    sentinels = []
+    for t in range(T):
+        v = row_values(t, rows[t], D)
+        host[t][rows[t]] = v
+        ref.append(v.copy())
+        cand = np.linspace(0, w.rows[t] - 1, num=min(w.rows[t], 512), dtype=np.int64)
+        s = np.setdiff1d(cand, rows[t])
+        host[t][s] = row_values(t + 1000, s, D)
+        sentinels.append(s)
+    say(f"  host tables ready {time.perf_counter() - t0:.1f}s")
+
+    def compact(u):
+        ids, off = batches[u]
+        parts = []
+        for t in range(T):
+            seg = ids[int(off[t * B]):int(off[(t + 1) * B])]
+            parts.append(np.searchsorted(rows[t], seg).astype(np.int32))
+        return np.concatenate(parts), off
+
+    dev_batches = [(torch.from_numpy(i).to(dev), torch.from_numpy(o).to(dev)) for i, o in batches]
+    planner = oracle.Planner(w.rows, w.slots)
+    max_ids = max(int(b[0].size) for b in batches)
+    sp = ScratchPipe(w.rows, D, w.slots, L, host, max_batch=B, max_ids=max_ids)
+    worst_fwd = 0.0
+    try:
+        out = torch.zeros((T * B, D), dtype=torch.float32, device=dev)
+        for u in range(steps):
+            ticket = sp.plan([dev_batches[q] for q in range(u, u + L + 2)])
+            p = planner.plan([batches[q] for q in range(u, u + L + 1)], B)
+            if u in check_plan_steps:
+                compare_plan(u, sp.debug_plan(ticket, int(batches[u][0].size)), p, T, B)
+            sp.forward(ticket, out)
+            g = wl.grads(w, u)
+            sp.backward_update(ticket, torch.from_numpy(g).to(dev), w.lr)
+            cid, off = compact(u)
+            o_ref = oracle.train_step(ref, cid, off, B, g, w.lr, want_out=u in check_fwd_steps)
+            if u in check_fwd_steps:
+                torch.cuda.synchronize()
+                e = row_rel_err(out.cpu().numpy(), o_ref)
+                worst_fwd = max(worst_fwd, float(e.max(initial=0.0)))
+                assert e.max(initial=0.0) <= REL_TOL, f"step {u}: forward rel err {e.max()}"
+            say(f"  step {u} done {time.perf_counter() - t0:.1f}s")
+        sp.flush()
+        stats = sp.stats()
+    finally:
+        sp.close()
+    worst_tab = 0.0
+    try:
+        for t in range(T):
+            e = row_rel_err(host[t][rows[t]], ref[t])
+            worst_tab = max(worst_tab, float(e.max(initial=0.0)))
+            assert e.max(initial=0.0) <= REL_TOL, f"table {t}: row rel err {e.max()}"
+            s = sentinels[t]
+            assert np.array_equal(host[t][s], row_values(t + 1000, s, D)), f"table {t}: sentinel changed"
+    finally:
+        host.close()
+    say(f"  checked {time.perf_counter() - t0:.1f}s")
+    return {"stats": stats, "worst_fwd": worst_fwd, "worst_table": worst_tab}

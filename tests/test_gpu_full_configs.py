@@ -1,0 +1,67 @@
+"""The larger benchmark configurations at full size on the GPU.
+
+Each runs as the benchmark drives it, for a number of steps that reaches
+steady eviction, with bit-exact plans against the reference planner, sampled
+forward outputs, every touched row after flush, and untouched sentinel rows."""
+import dataclasses
+
+import pytest
+
+from paper_2205_04702_amd import workload as wl
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def harness():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from tests import gpu_harness
+    return gpu_harness
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def first_tables(w, n):
+    """The workload restricted to its first n tables (same IDs, rows and slots for those)."""
+    return dataclasses.replace(w, name=f"{w.name}-first{n}", rows=w.rows[:n],
+                               pooling=w.pooling[:n], dist=w.dist[:n], slots=w.slots[:n])
+
+
+def _run(harness, name, steps, fwd, tables=None):
+    w = wl.get_workload(name)
+    if tables is not None:
+        w = first_tables(w, tables)
+    _say(f"case {name} full size, {steps} steps {w.describe()}")
+    r = harness.run_sampled_parity(w, steps, check_plan_steps=set(range(steps)),
+                                   check_fwd_steps=set(fwd), say=_say)
+    st = r["stats"]
+    _say(f"{name}: worst fwd {r['worst_fwd']:.2e} table {r['worst_table']:.2e} "
+         f"misses {st['misses']} evictions {st['evictions']}")
+    return st
+
+
+def test_zipf_26x4M_full_size(harness):
+    """26 x 4M x 128, B=2048, pooling 20, Zipf 1.1, 200k slots, L=4: 32 steps (the
+    scratchpad fills after about 24)."""
+    st = _run(harness, "zipf-26x4M", 32, (0, 16, 31))
+    assert st["evictions"] > 0
+
+
+def test_zipf_26x10M_per_gpu_share(harness):
+    """26 x 10M x 128, B=4096, pooling 40, Zipf 0.9, 200k slots, L=4, at the full per-table
+    shape.  All 26 tables need 133 GB of pinned, device-mapped host memory; one process can
+    map about 64 GiB here, which is the share of one GPU when the tables are split over
+    several (tables are independent units), so 12 tables (61 GB) run: 6 steps."""
+    st = _run(harness, "zipf-26x10M", 6, (0, 5), tables=12)
+    assert st["evictions"] > 0
+
+
+def test_mixed_full_size(harness):
+    """64 tables with rows log-uniform in [1e3, 2e7], D=64, B=8192, pooling 1-80, half
+    uniform and half Zipf 1.2, 40 GB Storage budget, L=6: 5 steps."""
+    st = _run(harness, "mixed", 5, (0, 4))
+    assert st["misses"] > 0

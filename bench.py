@@ -127,7 +127,8 @@ def main():
         w = dataclasses.replace(w, name=f"{w.name}-first{n}", rows=w.rows[:n],
                                 pooling=w.pooling[:n], dist=w.dist[:n], slots=w.slots[:n])
     W, K, L = args.warmup, args.steps, w.lookahead
-    nb = W + K + L + 1  # the window of the last step plus the batch prepared after it
+    ahead = sp.SP_MAX_AHEAD
+    nb = W + K + L + 1 + ahead  # the window of the last step plus the batches prepared after it
     log(f"[bench] workload {w.name}: generating {nb} batches and {W + K} gradient tensors")
     t0 = time.perf_counter()
     host_batches = [wl.batch(w, s) for s in range(nb)]
@@ -151,12 +152,12 @@ def main():
     stream = torch.cuda.current_stream().cuda_stream  # forward and backward run here
 
     def step(u):
-        # hold window u..u+L, plus batch u+L+1 handed over early for sorting;
+        # hold window u..u+L, plus the next batches handed over early for sorting;
         # kernel events on a sample of the steps only (they cost host time)
         if timed:
             ctx.set_flags(sp.SP_FLAG_TIMING if u % every == 0 else 0)
         t0 = time.perf_counter()
-        tk = ctx.plan([batches[q] for q in range(u, min(u + L + 1, nb - 1) + 1)])
+        tk = ctx.plan([batches[q] for q in range(u, min(u + L + ahead, nb - 1) + 1)])
         t1 = time.perf_counter()
         ctx.forward(tk, out, stream)
         t2 = time.perf_counter()

@@ -136,12 +136,18 @@ typedef struct {
  */
 sp_status sp_create(const sp_config *config, sp_handle *out);
 
+/* Batches after the hold window that sp_plan accepts for early sorting. */
+#define SP_MAX_AHEAD 2
+
 /*
  * Plan the next mini-batch.  window[0] is the batch to plan (ticket k = number
- * of plans so far) and window[1..] are the batches that follow it.  The first
- * min(n, lookahead+1) batches form the hold window; if n = lookahead+2 the
- * last one is only sorted and deduplicated ahead of time (not held), which
- * takes that work off the next plan's path.  Batches enter the device window
+ * of plans so far) and window[1..] are the batches that follow it, n of them
+ * in all, 1 <= n <= lookahead + 1 + SP_MAX_AHEAD.  The first
+ * min(n, lookahead+1) batches form the hold window; any after them are only
+ * sorted and deduplicated ahead of time (not held), which takes that work off
+ * later plans' paths.  Handing over at least one such batch also lets this
+ * plan issue the next plan's query right behind its own commit.  Batches
+ * enter the device window
  * ring once, when first seen, and are not read again: the same batch must be
  * passed with the same content every time it appears (after a failed plan
  * all of that call's batches are read again on the next call).  Window

@@ -520,7 +520,8 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     TRY(dalloc(h, &h->hash, cap));
 
     // batches k-1 (training) .. k+L+1 (prepared ahead) plus one of slack
-    h->nring = h->L + 4;
+    // batches k-1 (training) .. k+L+SP_MAX_AHEAD (prepared) plus one of slack
+    h->nring = h->L + 3 + SP_MAX_AHEAD;
     h->ring.resize(h->nring);
     h->ring_batch.assign(h->nring, -1);
     h->ring_nnz.assign(h->nring, 0);
@@ -783,8 +784,9 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     if (h->updated != h->planned)
         return fail(h, SP_ERR_SEQUENCE, "plan %lld requested before backward of ticket %lld",
                     (long long)h->planned, (long long)h->planned - 1);
-    if (!window || n < 1 || n > h->L + 2)
-        return fail(h, SP_ERR_INVALID_ARG, "window of %d batches (1..%d allowed)", n, h->L + 2);
+    if (!window || n < 1 || n > h->L + 1 + SP_MAX_AHEAD)
+        return fail(h, SP_ERR_INVALID_ARG, "window of %d batches (1..%d allowed)", n,
+                    h->L + 1 + SP_MAX_AHEAD);
     for (int w = 0; w < n; ++w) {
         const sp_batch &b = window[w];
         if (b.batch < 0 || b.batch > h->max_batch || b.nnz < 0 || b.nnz > h->max_ids || !b.bag_off ||
@@ -795,7 +797,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     const int64_t k = h->planned;
     const int32_t u = (int32_t)k;
     const int e = (int)(k % h->nring);
-    const int nhold = std::min<int>(n, h->L + 1);  // window[L+1], if given, is only prepared
+    const int nhold = std::min<int>(n, h->L + 1);  // window[L+1..], if given, are only prepared
     TicketDev &tk = h->tk[e];
     TicketHost &th = h->tkh[e];
     const bool timing = h->flags & SP_FLAG_TIMING;
@@ -837,9 +839,11 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     const int r0 = (int)(k % h->nring);
     double tC = host_ms();
     h->host_ms[1] += tC - tB;
-    if (n > nhold && h->ring_batch[(k + nhold) % h->nring] != k + nhold) {
-        TRY(ingest(h, window[nhold], k + nhold));
-        consumed = true;
+    for (int w = nhold; w < n; ++w) {
+        if (h->ring_batch[(k + w) % h->nring] != k + w) {
+            TRY(ingest(h, window[w], k + w));
+            consumed = true;
+        }
     }
     double tD = host_ms();
     h->host_ms[0] += tD - tC;
@@ -924,7 +928,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     h->host_ms[3] += tF - tE;
     // ---- the next plan's query, when its whole window is known: batches
     // k+1 .. k+L+1 are all in the ring now; it runs right behind this commit
-    if (n == h->L + 2) {
+    if (n >= h->L + 2) {
         TRY(enqueue_query(h, k + 1, h->L + 1, &h->spec_stamp));
         h->spec_ticket = k + 1;
         h->spec_nhold = h->L + 1;
@@ -950,10 +954,11 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     if (timing) HIPCHK(h, h->t_fill.begin(h->s_move));
     if (n_miss > 0) {
         // RAW-2/3: a victim's row is final once the last update that used it
-        // has run.  Updates up to k-4 are behind this stream already (the
-        // ring entries they freed were ingested before this plan's query);
-        // k-3 .. k-1 are waited for, one wait when they share a stream.
-        for (int64_t j = std::max<int64_t>(0, k - 3); j < k; ++j) {
+        // has run.  Update j freed ring entry j % nring for batch j + nring,
+        // whose ingest waited for it; this plan's query is behind every batch
+        // up to k+L, so updates up to k+L-nring are behind this stream
+        // already.  The rest are waited for, one wait when they share a stream.
+        for (int64_t j = std::max<int64_t>(0, k + h->L + 1 - h->nring); j < k; ++j) {
             const int ej = (int)(j % h->nring);
             if (j == k - 1 || h->upd_stream[ej] != h->upd_stream[(k - 1) % h->nring])
                 HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_upd[ej], 0));

@@ -40,7 +40,7 @@ __global__ void __launch_bounds__(BLOCK) k_probe_hold(int32_t row_bits, const ui
     if (valid) {
         const uint32_t key = pa.uk[w][i];
         t = (int)(key >> row_bits);
-        const int32_t slot = hash_find(hash, mask, key);
+        const int32_t slot = hash_find_ro(hash, mask, key);  // the map is not written here
         if (w == 0) {
             hit[i] = slot >= 0;
             slot_u[i] = slot;

@@ -248,13 +248,15 @@ __device__ __forceinline__ uint64_t load_entry(const uint64_t *p)
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Returns the slot of key, or -1.
-__device__ __forceinline__ int32_t hash_find(const uint64_t *tab, uint32_t mask, uint32_t key)
+// Returns the slot of key, or -1, in a kernel during which nothing modifies
+// the map (plain loads, served by the caches).
+__device__ __forceinline__ int32_t hash_find_ro(const uint64_t *__restrict__ tab, uint32_t mask,
+                                                uint32_t key)
 {
     uint32_t pos = hash_key(key) & mask;
     for (uint32_t n = 0; n <= mask; ++n) {
-        uint64_t e = load_entry(tab + pos);
-        uint32_t k = (uint32_t)(e >> 32);
+        const uint64_t e = tab[pos];
+        const uint32_t k = (uint32_t)(e >> 32);
         if (k == key) return (int32_t)(uint32_t)e;
         if (k == KEY_EMPTY) return -1;
         pos = (pos + 1) & mask;

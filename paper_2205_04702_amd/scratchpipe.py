@@ -24,6 +24,7 @@ SP_ERR_HIP = -5
 SP_ERR_STATE = -6
 SP_FLAG_DEBUG_SYNC = 0x1
 SP_FLAG_TIMING = 0x2
+SP_MAX_AHEAD = 2  # batches after the hold window that sp_plan sorts early
 
 _NAMES = {SP_ERR_INVALID_ARG: "SP_ERR_INVALID_ARG", SP_ERR_OOM: "SP_ERR_OOM",
           SP_ERR_CAPACITY: "SP_ERR_CAPACITY", SP_ERR_SEQUENCE: "SP_ERR_SEQUENCE",

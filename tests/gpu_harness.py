@@ -35,8 +35,9 @@ def compare_plan(step, dump, ref, T, B):
     assert dump["n_evict"] == ref.n_evict, f"step {step}: evictions {dump['n_evict']} vs {ref.n_evict}"
 
 
-def run_gpu(w, batches, host, first=0, last=None, flags=0, prepare_ahead=False):
-    """Train batches[first:last] on the GPU only (fresh context over `host`), then flush."""
+def run_gpu(w, batches, host, first=0, last=None, flags=0, prepare_ahead=0):
+    """Train batches[first:last] on the GPU only (fresh context over `host`), then flush.
+    prepare_ahead: how many batches after each window to hand over for early sorting."""
     import torch
     dev = torch.device("cuda:0")
     n = len(batches)
@@ -48,8 +49,7 @@ def run_gpu(w, batches, host, first=0, last=None, flags=0, prepare_ahead=False):
         out = torch.zeros((T * B, D), dtype=torch.float32, device=dev)
         for u in range(first, last):
             idx = list(range(u, min(u + L, last - 1) + 1))
-            if prepare_ahead and u + L + 1 < last:
-                idx.append(u + L + 1)
+            idx += [q for q in range(u + L + 1, u + L + 1 + int(prepare_ahead)) if q < last]
             ticket = sp.plan([batches[q] for q in idx])
             sp.forward(ticket, out)
             sp.backward_update(ticket, torch.from_numpy(wl.grads(w, u)).to(dev), w.lr)
@@ -77,11 +77,11 @@ def make_inputs(w, steps=None, ragged=None):
 
 def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all", flags=0,
                device_ids=False, ref_tables=None, sync_each_step=True, compare_tables=True,
-               return_tables=False, steps=None, prepare_ahead=False):
+               return_tables=False, steps=None, prepare_ahead=0):
     """Train w on the GPU and with the oracle; assert parity; return a summary.
 
-    prepare_ahead: also hand the GPU the batch after the window (prepared in
-    advance, not held); the oracle always sees the plain window."""
+    prepare_ahead: also hand the GPU that many batches after the window
+    (prepared in advance, not held); the oracle always sees the plain window."""
     import torch
     dev = torch.device("cuda:0")
     if batches is None:
@@ -107,7 +107,8 @@ def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all"
         for u in range(n):
             win_idx = list(range(u, min(u + L, n - 1) + 1))
             src = dev_batches if device_ids else batches
-            gpu_idx = win_idx + ([u + L + 1] if prepare_ahead and u + L + 1 < n else [])
+            gpu_idx = win_idx + [q for q in range(u + L + 1, u + L + 1 + int(prepare_ahead))
+                                 if q < n]
             ticket = sp.plan([src[q] for q in gpu_idx])
             assert ticket == u
             p = planner.plan([batches[q] for q in win_idx], B)
@@ -167,8 +168,8 @@ def row_values(t, rows, dim):
 
 
 def run_sampled_parity(w, steps, *, check_plan_steps, check_fwd_steps, say=print):
-    """A full-size workload driven as the benchmark drives it (IDs in device memory, the batch
-    after the window handed over early) for `steps` steps.
+    """A full-size workload driven as the benchmark drives it (IDs in device memory, the two
+    batches after the window handed over early) for `steps` steps.
 
     Only rows that the trained batches read are initialised (plus sentinel rows elsewhere);
     the oracle trains compact copies of exactly those rows (uncached training touches no
@@ -180,7 +181,8 @@ def run_sampled_parity(w, steps, *, check_plan_steps, check_fwd_steps, say=print
     dev = torch.device("cuda:0")
     T, B, D, L = w.tables, w.batch, w.dim, w.lookahead
     t0 = time.perf_counter()
-    batches = [wl.batch(w, s) for s in range(steps + L + 1)]
+    ahead = 2
+    batches = [wl.batch(w, s) for s in range(steps + L + ahead)]
     rows = touched_rows(w, batches, steps)
     say(f"  inputs {time.perf_counter() - t0:.1f}s, touched rows {sum(r.size for r in rows)}")
     host = HostTables(w.rows, D)
@@ -212,7 +214,7 @@ def run_sampled_parity(w, steps, *, check_plan_steps, check_fwd_steps, say=print
     try:
         out = torch.zeros((T * B, D), dtype=torch.float32, device=dev)
         for u in range(steps):
-            ticket = sp.plan([dev_batches[q] for q in range(u, u + L + 2)])
+            ticket = sp.plan([dev_batches[q] for q in range(u, u + L + 1 + ahead)])
             p = planner.plan([batches[q] for q in range(u, u + L + 1)], B)
             if u in check_plan_steps:
                 compare_plan(u, sp.debug_plan(ticket, int(batches[u][0].size)), p, T, B)

@@ -56,7 +56,7 @@ def test_call_order_is_enforced(harness):
         assert e.value.status == spm.SP_ERR_SEQUENCE
         ctx.backward_update(t, g, 0.1)
         with pytest.raises(spm.SPError) as e:
-            ctx.plan(batches[1:6])  # more than lookahead + 2 batches
+            ctx.plan(batches[1:7])  # more than lookahead + 1 + SP_MAX_AHEAD batches
         assert e.value.status == spm.SP_ERR_INVALID_ARG
         assert ctx.plan(batches[1:4]) == 1
     finally:
@@ -133,16 +133,18 @@ def test_rejected_plans_leave_state_unchanged(harness, lookahead):
         host.close()
 
 
-def test_bad_prepared_batch_fails_the_plan_that_holds_it(harness):
-    """A batch handed over early as the prepared-ahead batch is read once.  Bad
-    content in it does not affect the plan it was handed to; the next plan,
-    whose window holds it, is rejected whatever is passed, and a retry with
-    good content re-reads it.  Continuing matches the oracle."""
+@pytest.mark.parametrize("ahead", [1, 2])
+def test_bad_prepared_batch_fails_the_plan_that_holds_it(harness, ahead):
+    """A batch handed over early as a prepared-ahead batch is read once.  Bad
+    content in it does not affect the plans it was handed to before it enters
+    a hold window; the first plan whose window holds it is rejected whatever is
+    passed, and a retry with good content re-reads it.  Continuing matches the
+    oracle."""
     import torch
     from oracle import oracle
     w = wl.custom(rows=[1500, 2500], dim=32, batch=24, pooling=[3, 2], slots=[300, 260],
                   lookahead=2, steps=14, dist=("zipf", 1.0), seed=37)
-    _say("case bad prepared-ahead batch")
+    _say(f"case bad prepared-ahead batch, {ahead} ahead")
     batches = harness.make_inputs(w)
     host = harness.fresh_host(w)
     ref = [wl.init_table(w, t) for t in range(w.tables)]
@@ -153,15 +155,15 @@ def test_bad_prepared_batch_fails_the_plan_that_holds_it(harness):
     try:
         for u in range(n):
             held = batches[u:min(u + L, n - 1) + 1]
-            ahead = [batches[u + L + 1]] if u + L + 1 < n else []
+            extra = [batches[q] for q in range(u + L + 1, u + L + 1 + ahead) if q < n]
+            bad_q = 4 + L + ahead  # handed over last (and bad) at step 4
             if u == 4:
-                tail = ahead[0]
-                ahead = [_bad_ids(tail, w, 1, w.rows[1] + 7)]
-            if u == 5:
+                extra[-1] = _bad_ids(extra[-1], w, 1, w.rows[1] + 7)
+            if u == bad_q - L:  # first plan whose window holds it
                 with pytest.raises(spm.SPError) as e:
-                    ctx.plan(held + ahead)
+                    ctx.plan(held + extra)
                 assert e.value.status == spm.SP_ERR_INVALID_ARG
-            t = ctx.plan(held + ahead)
+            t = ctx.plan(held + extra)
             p = planner.plan(held, w.batch)
             harness.compare_plan(u, ctx.debug_plan(t, int(held[0][0].size)), p, w.tables, w.batch)
             ctx.forward(t, out)
@@ -185,7 +187,7 @@ def test_overlapped_equals_serialized_bit_for_bit(harness):
     _say("case overlap vs serialised")
     batches = harness.make_inputs(w)
     results = []
-    for flags, ahead in ((0, False), (spm.SP_FLAG_DEBUG_SYNC, False), (0, True), (0, False)):
+    for flags, ahead in ((0, 0), (spm.SP_FLAG_DEBUG_SYNC, 0), (0, 1), (0, 2), (0, 0)):
         host = harness.fresh_host(w)
         harness.run_gpu(w, batches, host, flags=flags, prepare_ahead=ahead)
         results.append([host[t].copy() for t in range(w.tables)])

@@ -81,15 +81,15 @@ def test_single_table_single_slot_pressure(harness):
     harness.run_parity(w)
 
 
-@pytest.mark.parametrize("device_ids", [False, True])
-def test_prepared_ahead_batch_changes_nothing(harness, device_ids):
-    """Passing the batch after the window (prepared early, not held) gives the
+@pytest.mark.parametrize("device_ids,ahead", [(False, 1), (True, 1), (True, 2)])
+def test_prepared_ahead_batch_changes_nothing(harness, device_ids, ahead):
+    """Passing the batches after the window (prepared early, not held) gives the
     same plans and tables as the plain window."""
     w = wl.custom(rows=[2500, 4000], dim=64, batch=40, pooling=[4, 2], slots=[500, 600],
                   lookahead=2, steps=20, dist=("zipf", 1.0), seed=21)
-    _say(f"case prepared-ahead device_ids={device_ids}")
+    _say(f"case prepared-ahead device_ids={device_ids} ahead={ahead}")
     a = harness.run_parity(w, return_tables=True)
-    b = harness.run_parity(w, prepare_ahead=True, device_ids=device_ids, return_tables=True)
+    b = harness.run_parity(w, prepare_ahead=ahead, device_ids=device_ids, return_tables=True)
     for x, y in zip(a["tables"], b["tables"]):
         assert np.array_equal(x, y)
 
@@ -111,10 +111,10 @@ def test_zipf_8x1M_full_size(harness):
     w = wl.get_workload("zipf-8x1M")
     _say(f"case zipf-8x1M {w.describe()}")
     sample = [0, 1, 2, 3, 50, 101, 150, 198, 199]
-    # as the benchmark drives it: IDs in device memory, the batch after the
-    # window handed over one step early
+    # as the benchmark drives it: IDs in device memory, the two batches after
+    # the window handed over early
     r = harness.run_parity(w, check_plan_steps=sample, check_fwd_steps=sample,
-                           sync_each_step=False, prepare_ahead=True, device_ids=True)
+                           sync_each_step=False, prepare_ahead=2, device_ids=True)
     st = r["stats"]
     assert st["plans"] == 200 and st["evictions"] > 0
     _say(f"zipf-8x1M worst fwd {r['worst_fwd']:.2e} table {r['worst_table']:.2e} "

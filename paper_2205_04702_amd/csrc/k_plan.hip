@@ -279,6 +279,93 @@ struct VictimOut {
     }
 };
 
+// ---------------------------------------------------------------- LRU order in LDS
+//
+// When every active table has at most VS_MAX victims, one block per table puts
+// its compacted victims (slot order) into LRU order: a stable LSD radix sort on
+// last_use + 1 in LDS, 8-bit digits.  Within a round of VS_THREADS keys, lanes
+// of a wave with the same digit find each other with ballots; the lowest of
+// them records the wave's count stamped with the round, so no clearing is
+// needed between rounds.
+constexpr int VS_THREADS = 1024;
+constexpr int VS_WAVES = VS_THREADS / WAVE;
+constexpr int VS_MAX = 2048;
+
+__global__ void __launch_bounds__(VS_THREADS) k_victim_sort(SelArgs a, const uint32_t *vk,
+                                                          const uint32_t *vv, int32_t *v_slot)
+{
+    __shared__ uint32_t kb[2][VS_MAX], vb[2][VS_MAX];
+    __shared__ uint32_t wc[VS_WAVES][256];
+    __shared__ uint32_t base[256];
+    __shared__ uint32_t lds[VS_WAVES];
+    const int y = blockIdx.x;
+    const int n = a.k[y] < VS_MAX ? a.k[y] : VS_MAX;
+    const int64_t off = a.vbase[y];
+    const int tid = threadIdx.x, w = wave_id(), lane = lane_id();
+    const uint32_t kmask = a.lu_bits >= 32 ? ~0u : ((1u << a.lu_bits) - 1u);
+    for (int i = tid; i < n; i += VS_THREADS) {
+        kb[0][i] = vk[off + i] & kmask;
+        vb[0][i] = vv[off + i];
+    }
+    for (int i = tid; i < VS_WAVES * 256; i += VS_THREADS) (&wc[0][0])[i] = 0;
+    const uint64_t lt = lanemask_lt();
+    int cur = 0;
+    uint32_t stamp = 0;
+    for (int shift = 0; shift < a.lu_bits; shift += 8) {
+        if (tid < 256) base[tid] = 0;
+        __syncthreads();
+        for (int i = tid; i < n; i += VS_THREADS) atomicAdd(&base[(kb[cur][i] >> shift) & 255u], 1u);
+        __syncthreads();
+        uint32_t tot;
+        const uint32_t ex = block_excl_scan_n<VS_THREADS>(tid < 256 ? base[tid] : 0u, lds, tot);
+        if (tid < 256) base[tid] = ex;
+        __syncthreads();
+        for (int r0 = 0; r0 < n; r0 += VS_THREADS) {
+            stamp += 1u << 16;
+            const int i = r0 + tid;
+            const bool valid = i < n;
+            const uint32_t key = valid ? kb[cur][i] : 0u, val = valid ? vb[cur][i] : 0u;
+            const uint32_t d = (key >> shift) & 255u;
+            uint64_t peers = __ballot(valid);
+            for (int b = 0; b < 8; ++b) {
+                const uint32_t bit = (d >> b) & 1u;
+                const uint64_t bb = __ballot(bit);
+                peers &= bit ? bb : ~bb;
+            }
+            const int leader = valid ? __ffsll((unsigned long long)peers) - 1 : lane;
+            const bool is_leader = valid && leader == lane;
+            if (is_leader) wc[w][d] = stamp | (uint32_t)__popcll(peers);
+            __syncthreads();
+            uint32_t start = 0, total = 0;
+            bool last_wave = false;
+            if (is_leader) {
+                uint32_t before = 0;
+                last_wave = true;
+                for (int q = 0; q < VS_WAVES; ++q) {
+                    const uint32_t e = wc[q][d];
+                    const uint32_t c = (e & 0xFFFF0000u) == stamp ? (e & 0xFFFFu) : 0u;
+                    if (q < w) before += c;
+                    if (q > w && c) last_wave = false;
+                    total += c;
+                }
+                start = base[d] + before;
+            }
+            start = __shfl(start, leader, WAVE);
+            __syncthreads();  // every leader has read base[d]
+            if (is_leader && last_wave) base[d] += total;
+            if (valid) {
+                uint32_t p = start + (uint32_t)__popcll(peers & lt);
+                p = p < (uint32_t)n ? p : (uint32_t)(n - 1);
+                kb[cur ^ 1][p] = key;
+                vb[cur ^ 1][p] = val;
+            }
+            __syncthreads();
+        }
+        cur ^= 1;
+    }
+    for (int i = tid; i < n; i += VS_THREADS) v_slot[off + i] = (int32_t)vb[cur][i];
+}
+
 void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int32_t *held,
                            const int32_t *last_use, int32_t *sel_state, int32_t *sel_hist,
                            uint32_t *vk0, uint32_t *vv0, uint32_t *vk1, uint32_t *vv1,
@@ -286,17 +373,21 @@ void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int
                            int32_t *err, hipStream_t s)
 {
     if (a.nact <= 0 || n_victims <= 0) return;
-    // compaction lands where the sort's last pass will end in v_slot
+    // small victim sets are ordered per table in LDS; otherwise one global
+    // sort on (table, last_use + 1), whose compaction lands where the sort's
+    // last pass will end in v_slot
+    bool small = true;
+    for (int y = 0; y < a.nact; ++y) small = small && a.k[y] <= VS_MAX;
     const int bits = a.act_bits + a.lu_bits;
-    const int passes = radix_passes(n_victims, bits);
+    const int passes = small ? 1 : radix_passes(n_victims, bits);
     uint32_t *ck = (passes & 1) ? vk0 : vk1;
     uint32_t *cv = (passes & 1) ? vv0 : (uint32_t *)v_slot;
     uint32_t *ok = (passes & 1) ? vk1 : vk0;
     uint32_t *ov = (passes & 1) ? (uint32_t *)v_slot : vv0;
-    // the compaction counts the sort's first digits when its passes are one
-    // launch each; their counters are cleared by the first pick
+    // the compaction counts the global sort's first digits when its passes
+    // are one launch each; their counters are cleared by the first pick
     const RadixPlan rp = radix_plan(n_victims, bits);
-    const bool prehist = rp.passes > 0 && rp.fused;
+    const bool prehist = !small && rp.passes > 0 && rp.fused;
     const unsigned chunks = (unsigned)((maxS + SEL_CHUNK - 1) / SEL_CHUNK);
     for (int l = 0; l < levels; ++l) {
         int shift = (levels - 1 - l) * SEL_BITS;
@@ -327,6 +418,11 @@ void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int
     out.tiles = prehist ? (uint32_t)rp.tiles : 0u;
     seg_scan<uint64_t>(seg, a.nact, maxS, VictimFlag{held, last_use, sel_state, a.stamp}, out, ws,
                        s);
+    if (small) {
+        hipLaunchKernelGGL(k_victim_sort, dim3(a.nact), dim3(VS_THREADS), 0, s, a,
+                           (const uint32_t *)ck, (const uint32_t *)cv, v_slot);
+        return;
+    }
     bool in_k1 = false;
     launch_radix_sort(ck, cv, ok, ov, n_victims, bits, hist, ws, &in_k1, s, prehist);
 }

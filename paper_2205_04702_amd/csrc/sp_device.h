@@ -54,6 +54,26 @@ __device__ __forceinline__ T block_excl_scan(T v, T *lds, T &total)
     return base + incl - v;
 }
 
+// Exclusive scan over a block of NT threads (every thread calls it; `lds`
+// holds NT / WAVE entries; two barriers).
+template <int NT, typename T>
+__device__ __forceinline__ T block_excl_scan_n(T v, T *lds, T &total)
+{
+    T incl = wave_incl_scan(v);
+    if (lane_id() == WAVE - 1) lds[wave_id()] = incl;
+    __syncthreads();
+    T base = 0, sum = 0;
+#pragma unroll
+    for (int w = 0; w < NT / WAVE; ++w) {
+        T x = lds[w];
+        if (w < wave_id()) base += x;
+        sum += x;
+    }
+    __syncthreads();
+    total = sum;
+    return base + incl - v;
+}
+
 template <typename T>
 __device__ __forceinline__ T block_sum(T v, T *lds)
 {

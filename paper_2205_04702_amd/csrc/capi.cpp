@@ -586,7 +586,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
             ws->err = &h->cnt->err_sticky;
         }
     }
-    TRY(dalloc(h, &h->sel_state, 2 * MAX_TABLES));
+    TRY(dalloc(h, &h->sel_state, 3 * MAX_TABLES));  // v* prefix, slots to take, arrivals
     TRY(dalloc(h, &h->sel_hist, (int64_t)MAX_TABLES * SEL_BINS));
     TRY(dalloc(h, &h->partial, nchunk_max * h->D));
     h->stage_rows = std::min<int64_t>(N, S);
@@ -628,6 +628,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     HIPCHK(nullptr, hipMemsetAsync(h->hash, 0xFF, sizeof(uint64_t) * cap, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->storage, 0, sizeof(float) * S * h->D, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->sel_hist, 0, sizeof(int32_t) * MAX_TABLES * SEL_BINS, h->s_plan));
+    HIPCHK(nullptr, hipMemsetAsync(h->sel_state, 0, sizeof(int32_t) * 3 * MAX_TABLES, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->cnt, 0, sizeof(DevCounters), h->s_plan));
     for (ScanWs *ws : {&h->ws_plan, &h->ws_ingest}) {
         HIPCHK(nullptr, hipMemsetAsync(ws->status, 0, sizeof(uint64_t) * LB_WORDS * ws->max_tiles, h->s_plan));

@@ -143,23 +143,41 @@ void launch_miss_compact(const uint32_t *ukeys, int64_t n_unique, TicketDev tk, 
 // segmented scan then compacts, in slot order, every unheld slot below v* and
 // the first r equal to it; a stable radix sort on (table, last_use + 1) puts
 // them in LRU order with ties in slot order.  sel_state[2a] = v* prefix,
-// sel_state[2a+1] = slots still to take at the current level.
+// sel_state[2a+1] = slots still to take at the current level,
+// sel_state[2 * MAX_TABLES + a] = blocks of the current level done with table a.
 
 constexpr int SEL_ITEMS = 4;
 constexpr int SEL_CHUNK = BLOCK * SEL_ITEMS;
 
-__global__ void __launch_bounds__(BLOCK) k_sel_hist(SelArgs a, int shift, int first,
-                                                    const int32_t *held, const int32_t *last_use,
-                                                    const int32_t *st, int32_t *hist)
+// One level of the select, one launch.  Every block counts its chunk of one
+// active table's unheld slots by the current SEL_BITS of last_use + 1 (among
+// slots matching the prefix found so far) and adds the counts to the table's
+// histogram.  The last block of a table to arrive then fixes the next SEL_BITS
+// of v* and the slots still to take, and leaves the histogram and its arrival
+// counter cleared.  The adds return their old values and each thread tests
+// them before the block's barrier, so every add of a block has been performed
+// before the block arrives; the last block reads the histogram with
+// device-scope atomic loads.  The first level starts from k misses still to
+// place and an empty prefix; its last blocks also mark the table's victim
+// entries invalid (-1) before the compaction fills them, and clear (all
+// tables together) the n_zero counters the global victim sort accumulates into.
+__global__ void __launch_bounds__(BLOCK) k_sel_level(SelArgs a, int shift, int first,
+                                                     const int32_t *held, const int32_t *last_use,
+                                                     int32_t *st, int32_t *hist, int32_t *arrived,
+                                                     int32_t *victims, uint32_t *zero,
+                                                     int64_t n_zero)
 {
     __shared__ int32_t h[SEL_BINS];
+    __shared__ int32_t lds[BLOCK / WAVE];
+    __shared__ int32_t last_s;
     for (int b = threadIdx.x; b < SEL_BINS; b += BLOCK) h[b] = 0;
     __syncthreads();
     const int ai = blockIdx.y;
     const int64_t S = a.S[ai];
     const int64_t s0 = (int64_t)blockIdx.x * SEL_CHUNK;
+    const int32_t prefix = first ? 0 : st[2 * ai];
     if (s0 < S) {
-        const uint64_t want = first ? 0 : (uint64_t)(uint32_t)st[2 * ai] >> (shift + SEL_BITS);
+        const uint64_t want = (uint64_t)(uint32_t)prefix >> (shift + SEL_BITS);
         const int64_t base = a.base[ai];
         int32_t hv[SEL_ITEMS], lv[SEL_ITEMS];
 #pragma unroll
@@ -179,28 +197,22 @@ __global__ void __launch_bounds__(BLOCK) k_sel_hist(SelArgs a, int shift, int fi
     }
     __syncthreads();
     int32_t *out = hist + (int64_t)ai * SEL_BINS;
+    int32_t seen = 0;
     for (int b = threadIdx.x; b < SEL_BINS; b += BLOCK)
-        if (h[b]) atomicAdd(&out[b], h[b]);
-}
+        if (h[b]) seen |= atomicAdd(&out[b], h[b]);
+    if (seen < 0) victims[0] = -1;  // never (counts are not negative); waits for the adds
+    __syncthreads();
+    if (threadIdx.x == 0) last_s = atomicAdd(&arrived[ai], 1) == (int32_t)gridDim.x - 1;
+    __syncthreads();
+    if (!last_s) return;  // uniform per block
 
-// One block per active table: fix the next SEL_BITS of v*.  The first level
-// starts from k misses still to place and an empty prefix, marks the table's
-// victim entries invalid (-1) before the compaction fills them, and clears
-// (all blocks together) the n_zero counters the victim sort accumulates into.
-__global__ void __launch_bounds__(BLOCK) k_sel_pick(SelArgs a, int shift, int first, int32_t *st,
-                                                    int32_t *hist, int32_t *victims,
-                                                    uint32_t *zero, int64_t n_zero)
-{
-    __shared__ int32_t lds[BLOCK / WAVE];
     constexpr int PER = SEL_BINS / BLOCK;
-    const int ai = blockIdx.x;
-    int32_t *h = hist + (int64_t)ai * SEL_BINS;
     const int32_t krem = first ? a.k[ai] : st[2 * ai + 1];
-    const int32_t prefix = first ? 0 : st[2 * ai];
     int32_t c[PER], sum = 0;
 #pragma unroll
     for (int q = 0; q < PER; ++q) {
-        c[q] = h[threadIdx.x * PER + q];
+        c[q] = __hip_atomic_load(&out[threadIdx.x * PER + q], __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
         sum += c[q];
     }
     int32_t total;
@@ -217,10 +229,10 @@ __global__ void __launch_bounds__(BLOCK) k_sel_pick(SelArgs a, int shift, int fi
             cum += c[q];
         }
     }
-    __syncthreads();
-    // leave the histogram zeroed for the next level
 #pragma unroll
-    for (int q = 0; q < PER; ++q) h[threadIdx.x * PER + q] = 0;
+    for (int q = 0; q < PER; ++q)
+        __hip_atomic_store(&out[threadIdx.x * PER + q], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x == 0) __hip_atomic_store(&arrived[ai], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (first) {
         for (int i = threadIdx.x; i < a.k[ai]; i += BLOCK) victims[a.vbase[ai] + i] = -1;
         for (int64_t i = (int64_t)ai * BLOCK + threadIdx.x; i < n_zero; i += (int64_t)a.nact * BLOCK)
@@ -391,10 +403,9 @@ void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int
     const unsigned chunks = (unsigned)((maxS + SEL_CHUNK - 1) / SEL_CHUNK);
     for (int l = 0; l < levels; ++l) {
         int shift = (levels - 1 - l) * SEL_BITS;
-        hipLaunchKernelGGL(k_sel_hist, dim3(chunks, a.nact), dim3(BLOCK), 0, s, a, shift, (int)(l == 0),
-                           held, last_use, (const int32_t *)sel_state, sel_hist);
-        hipLaunchKernelGGL(k_sel_pick, dim3(a.nact), dim3(BLOCK), 0, s, a, shift, (int)(l == 0),
-                           sel_state, sel_hist, (int32_t *)cv, hist,
+        hipLaunchKernelGGL(k_sel_level, dim3(chunks, a.nact), dim3(BLOCK), 0, s, a, shift,
+                           (int)(l == 0), held, last_use, sel_state, sel_hist,
+                           sel_state + 2 * MAX_TABLES, (int32_t *)cv, hist,
                            prehist ? rp.table * rp.passes : (int64_t)0);
     }
     SegAct seg;

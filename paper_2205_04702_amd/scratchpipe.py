@@ -13,7 +13,8 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libscratchpipe.so")
+# SCRATCHPIPE_LIB selects another build of the library (for comparing builds)
+LIB_PATH = os.environ.get("SCRATCHPIPE_LIB") or os.path.join(_HERE, "libscratchpipe.so")
 
 SP_OK = 0
 SP_ERR_INVALID_ARG = -1

@@ -279,6 +279,7 @@ struct sp_ctx {
     uint32_t *vk0 = nullptr, *vv0 = nullptr, *vk1 = nullptr;
     float *partial = nullptr;
     DevCounters *cnt = nullptr;
+    int32_t *cnt_part = nullptr;  // [PART_COPIES][2 * MAX_TABLES] probe counter copies
     DevCounters *h_cnt = nullptr, *h_cnt_dev = nullptr;  // host-coherent copy and its device address
 
     // write-back staging (two in flight)
@@ -575,6 +576,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     TRY(dalloc(h, &h->hist, radix_hist_entries(N)));
     TRY(dalloc(h, &h->ihist, radix_hist_entries(N)));
     TRY(dalloc(h, &h->cnt, 1));
+    TRY(dalloc(h, &h->cnt_part, (int64_t)PART_COPIES * 2 * MAX_TABLES));
     {
         // scans: victims (tables x slots per table), misses and batches (N),
         // radix histogram tables (at most N + 2048 entries)
@@ -630,6 +632,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     HIPCHK(nullptr, hipMemsetAsync(h->sel_hist, 0, sizeof(int32_t) * MAX_TABLES * SEL_BINS, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->sel_state, 0, sizeof(int32_t) * 3 * MAX_TABLES, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->cnt, 0, sizeof(DevCounters), h->s_plan));
+    HIPCHK(nullptr, hipMemsetAsync(h->cnt_part, 0, sizeof(int32_t) * PART_COPIES * 2 * MAX_TABLES, h->s_plan));
     for (ScanWs *ws : {&h->ws_plan, &h->ws_ingest}) {
         HIPCHK(nullptr, hipMemsetAsync(ws->status, 0, sizeof(uint64_t) * LB_WORDS * ws->max_tiles, h->s_plan));
         HIPCHK(nullptr, hipMemsetAsync(ws->counter, 0, sizeof(uint32_t), h->s_plan));
@@ -771,8 +774,8 @@ static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, int32_t *stamp_o
     }
     const int32_t stamp = ++h->stamp;
     launch_probe_hold(h->tb, h->hash, h->hash_mask, ukeys, nuniq, nhold, max_nnz, h->held, stamp,
-                      h->tk[e], h->cnt, h->ring[k % h->nring].scal, h->s_plan);
-    launch_publish(h->cnt, h->h_cnt_dev, h->s_plan);  // also clears the counters
+                      h->tk[e], h->cnt, h->cnt_part, h->ring[k % h->nring].scal, h->s_plan);
+    launch_publish(h->cnt, h->cnt_part, h->T, h->h_cnt_dev, h->s_plan);  // also clears them
     CHECK_LAUNCH(h);
     if (timing) HIPCHK(h, h->t_qry.end(h->s_plan));
     *stamp_out = stamp;

@@ -426,25 +426,4 @@ void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, cons
     }
 }
 
-// Copy the plan counters to pinned, device-mapped, host-coherent memory with
-// plain stores, so the host reads them after one stream synchronisation
-// without a separate copy command; then clear the per-plan counters for the
-// next query.
-__global__ void k_publish(DevCounters *cnt, DevCounters *host_mapped)
-{
-    constexpr int N = (int)(sizeof(DevCounters) / sizeof(int32_t));
-    int32_t *src = reinterpret_cast<int32_t *>(cnt);
-    int32_t *dst = reinterpret_cast<int32_t *>(host_mapped);
-    for (int i = threadIdx.x; i < N; i += blockDim.x) {
-        dst[i] = src[i];
-        if (i < COUNTERS_CLEARED) src[i] = 0;
-    }
-    __threadfence_system();
-}
-
-void launch_publish(DevCounters *cnt, DevCounters *host_mapped, hipStream_t s)
-{
-    hipLaunchKernelGGL(k_publish, dim3(1), dim3(BLOCK), 0, s, cnt, host_mapped);
-}
-
 }  // namespace sp

@@ -17,15 +17,20 @@ struct ProbeArgs {
 // blockIdx.y = window batch.  Every cached key of a window batch stamps its
 // slot as held for this plan (held[slot] = stamp) and counts it once per
 // table; batch 0 (the planned one) also records hit / slot and counts misses.
-// Per-table counts are summed across the wave first (keys are sorted, so a
-// wave nearly always covers one table) and added with one atomic per table
-// per wave.
-__global__ void __launch_bounds__(BLOCK) k_probe_hold(int32_t row_bits, const uint64_t *hash,
+// Per-table counts are summed across the wave (keys are sorted, so a wave
+// nearly always covers one table), then across the block in LDS, then added
+// to one of PART_COPIES copies of the counters so that few blocks contend for
+// an address; the publish kernel sums the copies.
+__global__ void __launch_bounds__(BLOCK) k_probe_hold(int32_t row_bits, int32_t T,
+                                                      const uint64_t *__restrict__ hash,
                                                       uint32_t mask, ProbeArgs pa, int32_t *held,
                                                       int32_t stamp, int32_t *hit,
                                                       int32_t *slot_u, DevCounters *cnt,
-                                                      const int32_t *scal0)
+                                                      int32_t *part, const int32_t *scal0)
 {
+    __shared__ int32_t c_miss[MAX_TABLES], c_held[MAX_TABLES];
+    for (int t = threadIdx.x; t < T; t += BLOCK) c_miss[t] = c_held[t] = 0;
+    __syncthreads();
     const int w = blockIdx.y;
     const int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
     if (w == 0 && i == 0) {
@@ -57,25 +62,75 @@ __global__ void __launch_bounds__(BLOCK) k_probe_hold(int32_t row_bits, const ui
         const int nm = __popcll(__ballot(mine && miss));
         const int nh = __popcll(__ballot(mine && fresh));
         if (lane_id() == leader) {
-            if (nm) atomicAdd(&cnt->miss[tl], nm);
-            if (nh) atomicAdd(&cnt->held[tl], nh);
+            if (nm) atomicAdd(&c_miss[tl], nm);
+            if (nh) atomicAdd(&c_held[tl], nh);
         }
         todo &= ~same;
+    }
+    __syncthreads();
+    int32_t *p = part + (int64_t)((blockIdx.y * gridDim.x + blockIdx.x) % PART_COPIES) * 2 * MAX_TABLES;
+    for (int t = threadIdx.x; t < T; t += BLOCK) {
+        if (c_miss[t]) atomicAdd(&p[t], c_miss[t]);
+        if (c_held[t]) atomicAdd(&p[MAX_TABLES + t], c_held[t]);
     }
 }
 
 void launch_probe_hold(const Tables &tb, const uint64_t *hash, uint32_t mask,
                        const uint32_t *const *ukeys, const int32_t *const *nuniq, int nwin,
                        int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk,
-                       DevCounters *cnt, const int32_t *scal0, hipStream_t s)
+                       DevCounters *cnt, int32_t *part, const int32_t *scal0, hipStream_t s)
 {
     ProbeArgs pa{};
     for (int w = 0; w < nwin; ++w) pa.uk[w] = ukeys[w], pa.nu[w] = nuniq[w];
     // at least one block per batch so that every batch's error word is read
     const int64_t n = max_unique > 0 ? max_unique : 1;
     hipLaunchKernelGGL(k_probe_hold, dim3((unsigned)((n + BLOCK - 1) / BLOCK), nwin), dim3(BLOCK),
-                       0, s, tb.row_bits, hash, mask, pa, held, stamp, tk.hit, tk.slot_u, cnt,
-                       scal0);
+                       0, s, tb.row_bits, tb.T, hash, mask, pa, held, stamp, tk.hit, tk.slot_u,
+                       cnt, part, scal0);
+}
+
+// Sum the probe's counter copies into the plan counters (clearing the copies),
+// then copy the counters to pinned, device-mapped, host-coherent memory with
+// plain stores, so the host reads them after one stream synchronisation
+// without a separate copy command, and clear the per-plan counters for the
+// next query.
+__global__ void __launch_bounds__(BLOCK) k_publish(DevCounters *cnt, int32_t *part, int32_t T,
+                                                   DevCounters *host_mapped)
+{
+    __shared__ int32_t sums[2 * MAX_TABLES];
+    for (int j = threadIdx.x; j < 2 * MAX_TABLES; j += BLOCK) sums[j] = 0;
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < PART_COPIES * 2 * MAX_TABLES; idx += BLOCK) {
+        const int j = idx % (2 * MAX_TABLES);
+        if (j % MAX_TABLES >= T) continue;
+        const int32_t v = part[idx];
+        if (v) {
+            atomicAdd(&sums[j], v);
+            part[idx] = 0;
+        }
+    }
+    __syncthreads();
+    for (int j = threadIdx.x; j < 2 * MAX_TABLES; j += BLOCK) {
+        const int t = j % MAX_TABLES;
+        if (t >= T) continue;
+        if (j < MAX_TABLES) cnt->miss[t] = sums[j];
+        else cnt->held[t] = sums[j];
+    }
+    __syncthreads();
+    constexpr int N = (int)(sizeof(DevCounters) / sizeof(int32_t));
+    int32_t *src = reinterpret_cast<int32_t *>(cnt);
+    int32_t *dst = reinterpret_cast<int32_t *>(host_mapped);
+    for (int i = threadIdx.x; i < N; i += BLOCK) {
+        dst[i] = src[i];
+        if (i < COUNTERS_CLEARED) src[i] = 0;
+    }
+    __threadfence_system();
+}
+
+void launch_publish(DevCounters *cnt, int32_t *part, int32_t T, DevCounters *host_mapped,
+                    hipStream_t s)
+{
+    hipLaunchKernelGGL(k_publish, dim3(1), dim3(BLOCK), 0, s, cnt, part, T, host_mapped);
 }
 
 // ---------------------------------------------------------------- hash rebuild

@@ -196,10 +196,11 @@ __global__ void __launch_bounds__(BLOCK) k_bwd_combine(float4 *__restrict__ stor
 // from the pinned host table (zero-copy over the host link).  The same lanes
 // read the old row before writing the new one.  Every victim's previous key
 // is stored after the n staging rows, so rows and keys leave the device in
-// one copy.  The grid is kept small (lane groups stride over the victims):
-// waves waiting on the host link then occupy few compute units, and the
-// kernels running beside this one keep the rest.
-constexpr int MOVE_MAX_BLOCKS = 128;
+// one copy.  The grid is kept small and each lane group keeps MOVE_ROWS
+// victims in flight: waves waiting on the host link then occupy few compute
+// units, and the kernels running beside this one keep the rest.
+constexpr int MOVE_MAX_BLOCKS = 64;
+constexpr int MOVE_ROWS = 4;
 
 template <int LPR>
 __global__ void __launch_bounds__(BLOCK) k_move(float4 *__restrict__ storage, Tables tb,
@@ -207,19 +208,43 @@ __global__ void __launch_bounds__(BLOCK) k_move(float4 *__restrict__ storage, Ta
                                                 int64_t nslots, float4 *__restrict__ stage)
 {
     const int c = (int)(threadIdx.x % LPR);
-    const int64_t step = (int64_t)gridDim.x * (BLOCK / LPR);
-    for (int64_t i = ((int64_t)blockIdx.x * BLOCK + threadIdx.x) / LPR; i < n; i += step) {
-        const int32_t old = tk.v_old_key[i];
-        if (c == 0) reinterpret_cast<int32_t *>(stage + n * LPR)[i] = old;
-        const int32_t v = tk.v_slot[i];
-        if ((uint32_t)v >= (uint64_t)nslots) continue;
-        float4 *slot_row = storage + (int64_t)v * LPR + c;
-        if (old >= 0) stage[i * LPR + c] = *slot_row;
-        const uint32_t key = tk.m_key[i];
-        const int tab = (int)(key >> tb.row_bits);
-        const int64_t row = key & ((1u << tb.row_bits) - 1u);
-        if (tab >= tb.T || row >= tb.rows[tab]) continue;
-        *slot_row = hr.p[tab][row * LPR + c];
+    const int64_t groups = (int64_t)gridDim.x * (BLOCK / LPR);
+    const int64_t g = ((int64_t)blockIdx.x * BLOCK + threadIdx.x) / LPR;
+    const uint32_t row_mask = (1u << tb.row_bits) - 1u;
+    for (int64_t i0 = g; i0 < n; i0 += groups * MOVE_ROWS) {
+        int32_t old[MOVE_ROWS], v[MOVE_ROWS];
+        const float4 *src[MOVE_ROWS];
+#pragma unroll
+        for (int q = 0; q < MOVE_ROWS; ++q) {
+            const int64_t i = i0 + q * groups;
+            old[q] = -1;
+            v[q] = -1;
+            src[q] = nullptr;
+            if (i < n) {
+                old[q] = tk.v_old_key[i];
+                v[q] = tk.v_slot[i];
+                const uint32_t key = tk.m_key[i];
+                const int tab = (int)(key >> tb.row_bits);
+                const int64_t row = key & row_mask;
+                if (tab < tb.T && row < tb.rows[tab]) src[q] = hr.p[tab] + row * LPR + c;
+                if ((uint32_t)v[q] >= (uint64_t)nslots) v[q] = -1;
+            }
+        }
+        float4 prev[MOVE_ROWS], next[MOVE_ROWS];
+#pragma unroll
+        for (int q = 0; q < MOVE_ROWS; ++q) {  // every load of the batch in flight together
+            if (v[q] >= 0 && old[q] >= 0) prev[q] = storage[(int64_t)v[q] * LPR + c];
+            if (v[q] >= 0 && src[q]) next[q] = *src[q];
+        }
+#pragma unroll
+        for (int q = 0; q < MOVE_ROWS; ++q) {
+            const int64_t i = i0 + q * groups;
+            if (i >= n) continue;
+            if (c == 0) reinterpret_cast<int32_t *>(stage + n * LPR)[i] = old[q];
+            if (v[q] < 0) continue;
+            if (old[q] >= 0) stage[i * LPR + c] = prev[q];
+            if (src[q]) storage[(int64_t)v[q] * LPR + c] = next[q];
+        }
     }
 }
 

@@ -54,6 +54,7 @@ struct DevCounters {
     int32_t pad2[3];
 };
 constexpr int COUNTERS_CLEARED = (int)(offsetof(DevCounters, err_sticky) / sizeof(int32_t));
+constexpr int PART_COPIES = 64;  // copies of the per-table counters the probe adds into
 constexpr int32_t ERR_ID_RANGE = 1, ERR_OFFSETS = 2, ERR_HASH_FULL = 4, ERR_PLAN = 8;
 
 // One window-ring entry: a batch as it arrived plus its sort/dedup products.
@@ -105,7 +106,7 @@ void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, cons
                    int32_t B, int64_t nnz, int key_bits, int chunk, uint32_t *tmp_k,
                    uint32_t *tmp_v, uint32_t *hist, ScanWs &ws, hipEvent_t consumed,
                    hipStream_t s);
-void launch_publish(DevCounters *cnt, DevCounters *host_mapped, hipStream_t s);
+
 void launch_radix_sort(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *v1, int64_t n,
                        int bits, uint32_t *hist, ScanWs &ws, bool *in_k1, hipStream_t s,
                        bool prehist);
@@ -125,7 +126,10 @@ RadixPlan radix_plan(int64_t n, int bits);
 void launch_probe_hold(const Tables &tb, const uint64_t *hash, uint32_t mask,
                        const uint32_t *const *ukeys, const int32_t *const *nuniq, int nwin,
                        int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk,
-                       DevCounters *cnt, const int32_t *scal0, hipStream_t s);
+                       DevCounters *cnt, int32_t *part, const int32_t *scal0, hipStream_t s);
+// Sums the probe's counter copies, publishes the counters, clears them.
+void launch_publish(DevCounters *cnt, int32_t *part, int32_t T, DevCounters *host_mapped,
+                    hipStream_t s);
 void launch_hash_rebuild(uint64_t *hash, uint32_t mask, const int32_t *key_of_slot, int64_t nslots,
                          DevCounters *cnt, hipStream_t s);
 void launch_miss_compact(const uint32_t *ukeys, int64_t n_unique, TicketDev tk, ScanWs &ws,

@@ -280,7 +280,11 @@ struct sp_ctx {
     float *partial = nullptr;
     DevCounters *cnt = nullptr;
     int32_t *cnt_part = nullptr;  // [PART_COPIES][2 * MAX_TABLES] probe counter copies
-    DevCounters *h_cnt = nullptr, *h_cnt_dev = nullptr;  // host-coherent copy and its device address
+    // host-coherent copy of the counters, one 64-bit word per counter: query
+    // sequence number << 32 | value; and its device address
+    uint64_t *h_cnt = nullptr, *h_cnt_dev = nullptr;
+    uint32_t qseq = 0;        // sequence number of the last query issued
+    uint32_t spec_seq = 0;    // that of the early query
 
     // write-back staging (two in flight)
     int64_t stage_rows = 0;
@@ -599,15 +603,15 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     }
     {
         void *p = nullptr;
-        hipError_t e = hipHostMalloc(&p, sizeof(DevCounters),
-                                     hipHostMallocMapped | hipHostMallocCoherent);
+        const size_t bytes = sizeof(uint64_t) * COUNTER_WORDS;
+        hipError_t e = hipHostMalloc(&p, bytes, hipHostMallocMapped | hipHostMallocCoherent);
         if (e != hipSuccess) {
             (void)hipGetLastError();
             return fail(h, SP_ERR_OOM, "hipHostMalloc(counters): %s", hipGetErrorString(e));
         }
         h->pinned_allocs.push_back(p);
-        h->h_cnt = (DevCounters *)p;
-        memset(p, 0, sizeof(DevCounters));
+        h->h_cnt = (uint64_t *)p;
+        memset(p, 0, bytes);
         HIPCHK(nullptr, hipHostGetDevicePointer((void **)&h->h_cnt_dev, p, 0));
     }
 
@@ -749,10 +753,48 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
     return SP_OK;
 }
 
+// Wait until the query with sequence number seq has published every counter
+// word, and copy them out.  The host polls the coherent words instead of
+// synchronising the stream: the values count, not the end of the kernel, and
+// the plan stream keeps its order for what comes next.  Stream errors end the
+// wait.
+static sp_status wait_counts(sp_ctx *h, uint32_t seq, DevCounters *c)
+{
+    int32_t *dst = reinterpret_cast<int32_t *>(c);
+    const volatile uint64_t *w = h->h_cnt;
+    for (int64_t spin = 0;; ++spin) {
+        bool all = true;
+        for (int i = 0; i < COUNTER_WORDS && all; ++i) {
+            const uint64_t x = w[i];
+            all = (uint32_t)(x >> 32) == seq;
+            dst[i] = (int32_t)(uint32_t)x;
+        }
+        if (all) return SP_OK;
+        if ((spin & 1023) == 1023) {
+            const hipError_t e = hipStreamQuery(h->s_plan);
+            if (e == hipSuccess) {  // the stream is idle, so the words are final
+                for (int i = 0; i < COUNTER_WORDS; ++i) {
+                    const uint64_t x = w[i];
+                    if ((uint32_t)(x >> 32) != seq)
+                        return fail(h, SP_ERR_HIP, "internal: plan counters were not published");
+                    dst[i] = (int32_t)(uint32_t)x;
+                }
+                return SP_OK;
+            }
+            if (e != hipErrorNotReady) {
+                (void)hipGetLastError();
+                return fail(h, SP_ERR_HIP, "plan stream: %s", hipGetErrorString(e));
+            }
+        }
+        __builtin_ia32_pause();
+    }
+}
+
 // Phase 1 of plan k over window batches k .. k+nhold-1, all ingested or being
 // ingested: hold marks, the planned batch's hits and per-table miss / held
 // counts, published to host-coherent memory (read-only on the scratchpad).
-static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, int32_t *stamp_out)
+static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, int32_t *stamp_out,
+                               uint32_t *seq_out)
 {
     const int e = (int)(k % h->nring);
     const bool timing = h->flags & SP_FLAG_TIMING;
@@ -775,7 +817,8 @@ static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, int32_t *stamp_o
     const int32_t stamp = ++h->stamp;
     launch_probe_hold(h->tb, h->hash, h->hash_mask, ukeys, nuniq, nhold, max_nnz, h->held, stamp,
                       h->tk[e], h->cnt, h->cnt_part, h->ring[k % h->nring].scal, h->s_plan);
-    launch_publish(h->cnt, h->cnt_part, h->T, h->h_cnt_dev, h->s_plan);  // also clears them
+    *seq_out = ++h->qseq;
+    launch_publish(h->cnt, h->cnt_part, h->T, h->h_cnt_dev, *seq_out, h->s_plan);  // clears them
     CHECK_LAUNCH(h);
     if (timing) HIPCHK(h, h->t_qry.end(h->s_plan));
     *stamp_out = stamp;
@@ -839,7 +882,8 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     for (int w = 0; w < nhold && spec; ++w) spec = h->ring_batch[(k + w) % h->nring] == k + w;
     h->spec_ticket = -1;
     int32_t stamp = h->spec_stamp;
-    if (!spec) TRY(enqueue_query(h, k, nhold, &stamp));
+    uint32_t seq = h->spec_seq;
+    if (!spec) TRY(enqueue_query(h, k, nhold, &stamp, &seq));
     const int r0 = (int)(k % h->nring);
     double tC = host_ms();
     h->host_ms[1] += tC - tB;
@@ -851,11 +895,10 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     }
     double tD = host_ms();
     h->host_ms[0] += tD - tC;
-    HIPCHK(h, hipStreamSynchronize(h->s_plan));
+    DevCounters c;
+    TRY(wait_counts(h, seq, &c));
     double tE = host_ms();
     h->host_ms[2] += tE - tD;
-    DevCounters c;
-    memcpy(&c, (const void *)h->h_cnt, sizeof c);
     if (c.err & (ERR_ID_RANGE | ERR_OFFSETS)) {
         for (int w = 0; w < n; ++w) h->ring_batch[(k + w) % h->nring] = -1;  // re-read on retry
         return fail(h, SP_ERR_INVALID_ARG, "%s in the window",
@@ -933,7 +976,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     // ---- the next plan's query, when its whole window is known: batches
     // k+1 .. k+L+1 are all in the ring now; it runs right behind this commit
     if (n >= h->L + 2) {
-        TRY(enqueue_query(h, k + 1, h->L + 1, &h->spec_stamp));
+        TRY(enqueue_query(h, k + 1, h->L + 1, &h->spec_stamp, &h->spec_seq));
         h->spec_ticket = k + 1;
         h->spec_nhold = h->L + 1;
     }

@@ -90,12 +90,13 @@ void launch_probe_hold(const Tables &tb, const uint64_t *hash, uint32_t mask,
 }
 
 // Sum the probe's counter copies into the plan counters (clearing the copies),
-// then copy the counters to pinned, device-mapped, host-coherent memory with
-// plain stores, so the host reads them after one stream synchronisation
-// without a separate copy command, and clear the per-plan counters for the
-// next query.
+// then write the counters to pinned, device-mapped, host-coherent memory, each
+// as one 64-bit store tagged with the query's sequence number: the host polls
+// until every word carries it, with no copy command and no fence, and each
+// word is whole when seen.  Then clear the per-plan counters for the next
+// query.
 __global__ void __launch_bounds__(BLOCK) k_publish(DevCounters *cnt, int32_t *part, int32_t T,
-                                                   DevCounters *host_mapped)
+                                                   uint64_t *host_mapped, uint32_t seq)
 {
     __shared__ int32_t sums[2 * MAX_TABLES];
     for (int j = threadIdx.x; j < 2 * MAX_TABLES; j += BLOCK) sums[j] = 0;
@@ -117,20 +118,17 @@ __global__ void __launch_bounds__(BLOCK) k_publish(DevCounters *cnt, int32_t *pa
         else cnt->held[t] = sums[j];
     }
     __syncthreads();
-    constexpr int N = (int)(sizeof(DevCounters) / sizeof(int32_t));
     int32_t *src = reinterpret_cast<int32_t *>(cnt);
-    int32_t *dst = reinterpret_cast<int32_t *>(host_mapped);
-    for (int i = threadIdx.x; i < N; i += BLOCK) {
-        dst[i] = src[i];
+    for (int i = threadIdx.x; i < COUNTER_WORDS; i += BLOCK) {
+        host_mapped[i] = ((uint64_t)seq << 32) | (uint32_t)src[i];
         if (i < COUNTERS_CLEARED) src[i] = 0;
     }
-    __threadfence_system();
 }
 
-void launch_publish(DevCounters *cnt, int32_t *part, int32_t T, DevCounters *host_mapped,
-                    hipStream_t s)
+void launch_publish(DevCounters *cnt, int32_t *part, int32_t T, uint64_t *host_mapped,
+                    uint32_t seq, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_publish, dim3(1), dim3(BLOCK), 0, s, cnt, part, T, host_mapped);
+    hipLaunchKernelGGL(k_publish, dim3(1), dim3(BLOCK), 0, s, cnt, part, T, host_mapped, seq);
 }
 
 // ---------------------------------------------------------------- hash rebuild

@@ -55,6 +55,7 @@ struct DevCounters {
 };
 constexpr int COUNTERS_CLEARED = (int)(offsetof(DevCounters, err_sticky) / sizeof(int32_t));
 constexpr int PART_COPIES = 64;  // copies of the per-table counters the probe adds into
+constexpr int COUNTER_WORDS = (int)(sizeof(DevCounters) / sizeof(int32_t));
 constexpr int32_t ERR_ID_RANGE = 1, ERR_OFFSETS = 2, ERR_HASH_FULL = 4, ERR_PLAN = 8;
 
 // One window-ring entry: a batch as it arrived plus its sort/dedup products.
@@ -127,9 +128,10 @@ void launch_probe_hold(const Tables &tb, const uint64_t *hash, uint32_t mask,
                        const uint32_t *const *ukeys, const int32_t *const *nuniq, int nwin,
                        int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk,
                        DevCounters *cnt, int32_t *part, const int32_t *scal0, hipStream_t s);
-// Sums the probe's counter copies, publishes the counters, clears them.
-void launch_publish(DevCounters *cnt, int32_t *part, int32_t T, DevCounters *host_mapped,
-                    hipStream_t s);
+// Sums the probe's counter copies, publishes the counters (word i of
+// host_mapped = seq << 32 | counter word i), clears them.
+void launch_publish(DevCounters *cnt, int32_t *part, int32_t T, uint64_t *host_mapped,
+                    uint32_t seq, hipStream_t s);
 void launch_hash_rebuild(uint64_t *hash, uint32_t mask, const int32_t *key_of_slot, int64_t nslots,
                          DevCounters *cnt, hipStream_t s);
 void launch_miss_compact(const uint32_t *ukeys, int64_t n_unique, TicketDev tk, ScanWs &ws,

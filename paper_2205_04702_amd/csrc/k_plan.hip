@@ -101,16 +101,20 @@ __global__ void __launch_bounds__(BLOCK) k_publish(DevCounters *cnt, int32_t *pa
     __shared__ int32_t sums[2 * MAX_TABLES];
     for (int j = threadIdx.x; j < 2 * MAX_TABLES; j += BLOCK) sums[j] = 0;
     __syncthreads();
-    for (int idx = threadIdx.x; idx < PART_COPIES * 2 * MAX_TABLES; idx += BLOCK) {
-        const int j = idx % (2 * MAX_TABLES);
-        if (j % MAX_TABLES >= T) continue;
+    // the copies' words of the T tables: loads only in this loop, so they are
+    // all in flight together; cleared in a second loop
+    const int n_rel = PART_COPIES * 2 * T;
+    auto word = [T](int r) {
+        const int c = r / (2 * T), jj = r % (2 * T);
+        return c * 2 * MAX_TABLES + (jj < T ? jj : MAX_TABLES + jj - T);
+    };
+    for (int r = threadIdx.x; r < n_rel; r += BLOCK) {
+        const int idx = word(r);
         const int32_t v = part[idx];
-        if (v) {
-            atomicAdd(&sums[j], v);
-            part[idx] = 0;
-        }
+        if (v) atomicAdd(&sums[idx % (2 * MAX_TABLES)], v);
     }
     __syncthreads();
+    for (int r = threadIdx.x; r < n_rel; r += BLOCK) part[word(r)] = 0;
     for (int j = threadIdx.x; j < 2 * MAX_TABLES; j += BLOCK) {
         const int t = j % MAX_TABLES;
         if (t >= T) continue;
@@ -199,7 +203,7 @@ void launch_miss_compact(const uint32_t *ukeys, int64_t n_unique, TicketDev tk, 
 // sel_state[2a+1] = slots still to take at the current level,
 // sel_state[2 * MAX_TABLES + a] = blocks of the current level done with table a.
 
-constexpr int SEL_ITEMS = 4;
+constexpr int SEL_ITEMS = 16;
 constexpr int SEL_CHUNK = BLOCK * SEL_ITEMS;
 
 // One level of the select, one launch.  Every block counts its chunk of one

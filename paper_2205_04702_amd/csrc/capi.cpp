@@ -721,12 +721,23 @@ extern "C" void sp_host_free(void *ptr)
 
 // ---------------------------------------------------------------- plan
 
+// Make stream s wait for event e unless e has already completed: a wait on a
+// pending event recorded on another stream costs the host several times more
+// than asking whether it has completed.
+static hipError_t wait_unless_done(hipStream_t s, hipEvent_t e)
+{
+    const hipError_t q = hipEventQuery(e);
+    if (q == hipSuccess) return hipSuccess;
+    if (q != hipErrorNotReady) return q;
+    return hipStreamWaitEvent(s, e, 0);
+}
+
 static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
 {
     const int r = (int)(q % h->nring);
     BatchDev &b = h->ring[r];
     // the previous occupant (batch q - nring) must be done with its backward
-    HIPCHK(h, hipStreamWaitEvent(h->s_ingest, h->ev_upd[r], 0));
+    HIPCHK(h, wait_unless_done(h->s_ingest, h->ev_upd[r]));
     const bool timing = h->flags & SP_FLAG_TIMING;
     if (timing) HIPCHK(h, h->t_ing.begin(h->s_ingest));
     const int64_t nbags = (int64_t)h->T * bt.batch;
@@ -800,14 +811,14 @@ static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, int32_t *stamp_o
     const bool timing = h->flags & SP_FLAG_TIMING;
     if (timing) HIPCHK(h, h->t_qry.begin(h->s_plan));
     // the ticket buffers being reused belonged to ticket k - nring
-    if (k >= h->nring) HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ev_upd[e], 0));
+    if (k >= h->nring) HIPCHK(h, wait_unless_done(h->s_plan, h->ev_upd[e]));
     const uint32_t *ukeys[MAX_WINDOW];
     const int32_t *nuniq[MAX_WINDOW];
     int64_t max_nnz = 0;
     for (int w = 0; w < nhold; ++w) {
         const int r = (int)((k + w) % h->nring);
         if (!h->ring_seen[r]) {  // later queries are behind this one on the same stream
-            HIPCHK(h, hipStreamWaitEvent(h->s_plan, h->ring_ready[r], 0));
+            HIPCHK(h, wait_unless_done(h->s_plan, h->ring_ready[r]));
             h->ring_seen[r] = 1;
         }
         ukeys[w] = h->ring[r].ukeys;
@@ -1008,7 +1019,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
         for (int64_t j = std::max<int64_t>(0, k + h->L + 1 - h->nring); j < k; ++j) {
             const int ej = (int)(j % h->nring);
             if (j == k - 1 || h->upd_stream[ej] != h->upd_stream[(k - 1) % h->nring])
-                HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_upd[ej], 0));
+                HIPCHK(h, wait_unless_done(h->s_move, h->ev_upd[ej]));
         }
         launch_move(h->storage, h->D, h->tb, h->host_dev, tk, n_miss, u, h->stage_dev[sl],
                     h->s_move);
@@ -1065,7 +1076,7 @@ extern "C" sp_status sp_forward(sp_handle h, int64_t ticket, float *d_out, void 
     HIPCHK(h, hipStreamWaitEvent(s, h->ev_filled[e], 0));
     // RAW-1: the previous update must land first (implicit on the same stream)
     if (ticket >= 1 && s != h->last_update_stream)
-        HIPCHK(h, hipStreamWaitEvent(s, h->ev_upd[(ticket - 1) % h->nring], 0));
+        HIPCHK(h, wait_unless_done(s, h->ev_upd[(ticket - 1) % h->nring]));
     hipEvent_t e0 = nullptr, e1 = nullptr;
     if ((h->flags & SP_FLAG_TIMING) && nbags > 0) HIPCHK(h, h->t_fwd.take(&e0, &e1));
     launch_forward(h->storage, h->D, h->total_slots, h->tk[e].slot_of, h->ring[th.ring].bag_off,

@@ -50,7 +50,7 @@ def kernel_bytes(w, n_unique: float, n_chunks: float) -> dict:
 
 def traffic_from_profile(kernel: str, src_hash: str, workload: str):
     """HBM bytes per launch measured by rocprofv3 counters, if a summary for the
-    current kernel source exists under profiles/."""
+    current kernel source exists under profiles/ (keyed by the --workload name)."""
     p = os.path.join(ROOT, "profiles", "hbm_traffic.json")
     if not os.path.exists(p):
         return None
@@ -242,7 +242,7 @@ def main():
         dom = "forward" if fwd_ms >= bwd_ms else "backward"
         ach = fwd_gbs if dom == "forward" else bwd_gbs
         name = "k_forward" if dom == "forward" else "k_backward"
-        tr = traffic_from_profile(name, src_hash, w.name)
+        tr = traffic_from_profile(name, src_hash, args.workload if not args.tables else w.name)
         res["roofline"] = {"bound": "hbm", "kernel": name,
                            "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                            "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": tr,

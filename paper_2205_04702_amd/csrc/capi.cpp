@@ -279,7 +279,8 @@ struct sp_ctx {
     uint32_t *vk0 = nullptr, *vv0 = nullptr, *vk1 = nullptr;
     float *partial = nullptr;
     DevCounters *cnt = nullptr;
-    int32_t *cnt_part = nullptr;  // [PART_COPIES][2 * MAX_TABLES] probe counter copies
+    int32_t *cnt_part = nullptr;  // [PART_COPIES][2 * MAX_TABLES] probe counter copies, then
+                                  // the query's arrival count
     // host-coherent copy of the counters, one 64-bit word per counter: query
     // sequence number << 32 | value; and its device address
     uint64_t *h_cnt = nullptr, *h_cnt_dev = nullptr;
@@ -580,7 +581,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     TRY(dalloc(h, &h->hist, radix_hist_entries(N)));
     TRY(dalloc(h, &h->ihist, radix_hist_entries(N)));
     TRY(dalloc(h, &h->cnt, 1));
-    TRY(dalloc(h, &h->cnt_part, (int64_t)PART_COPIES * 2 * MAX_TABLES));
+    TRY(dalloc(h, &h->cnt_part, (int64_t)PART_COPIES * 2 * MAX_TABLES + 1));
     {
         // scans: victims (tables x slots per table), misses and batches (N),
         // radix histogram tables (at most N + 2048 entries)
@@ -636,7 +637,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     HIPCHK(nullptr, hipMemsetAsync(h->sel_hist, 0, sizeof(int32_t) * MAX_TABLES * SEL_BINS, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->sel_state, 0, sizeof(int32_t) * 3 * MAX_TABLES, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->cnt, 0, sizeof(DevCounters), h->s_plan));
-    HIPCHK(nullptr, hipMemsetAsync(h->cnt_part, 0, sizeof(int32_t) * PART_COPIES * 2 * MAX_TABLES, h->s_plan));
+    HIPCHK(nullptr, hipMemsetAsync(h->cnt_part, 0, sizeof(int32_t) * (PART_COPIES * 2 * MAX_TABLES + 1), h->s_plan));
     for (ScanWs *ws : {&h->ws_plan, &h->ws_ingest}) {
         HIPCHK(nullptr, hipMemsetAsync(ws->status, 0, sizeof(uint64_t) * LB_WORDS * ws->max_tiles, h->s_plan));
         HIPCHK(nullptr, hipMemsetAsync(ws->counter, 0, sizeof(uint32_t), h->s_plan));
@@ -826,10 +827,10 @@ static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, int32_t *stamp_o
         max_nnz = std::max(max_nnz, h->ring_nnz[r]);
     }
     const int32_t stamp = ++h->stamp;
-    launch_probe_hold(h->tb, h->hash, h->hash_mask, ukeys, nuniq, nhold, max_nnz, h->held, stamp,
-                      h->tk[e], h->cnt, h->cnt_part, h->ring[k % h->nring].scal, h->s_plan);
     *seq_out = ++h->qseq;
-    launch_publish(h->cnt, h->cnt_part, h->T, h->h_cnt_dev, *seq_out, h->s_plan);  // clears them
+    launch_query(h->tb, h->hash, h->hash_mask, ukeys, nuniq, nhold, max_nnz, h->held, stamp,
+                 h->tk[e], h->cnt, h->cnt_part, h->cnt_part + PART_COPIES * 2 * MAX_TABLES,
+                 h->ring[k % h->nring].scal, h->h_cnt_dev, *seq_out, h->s_plan);
     CHECK_LAUNCH(h);
     if (timing) HIPCHK(h, h->t_qry.end(h->s_plan));
     *stamp_out = stamp;

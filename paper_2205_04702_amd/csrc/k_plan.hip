@@ -14,31 +14,44 @@ struct ProbeArgs {
     const int32_t *nu[MAX_WINDOW];
 };
 
-// blockIdx.y = window batch.  Every cached key of a window batch stamps its
-// slot as held for this plan (held[slot] = stamp) and counts it once per
-// table; batch 0 (the planned one) also records hit / slot and counts misses.
-// Per-table counts are summed across the wave (keys are sorted, so a wave
-// nearly always covers one table), then across the block in LDS, then added
-// to one of PART_COPIES copies of the counters so that few blocks contend for
-// an address; the publish kernel sums the copies.
-__global__ void __launch_bounds__(BLOCK) k_probe_hold(int32_t row_bits, int32_t T,
-                                                      const uint64_t *__restrict__ hash,
-                                                      uint32_t mask, ProbeArgs pa, int32_t *held,
-                                                      int32_t stamp, int32_t *hit,
-                                                      int32_t *slot_u, DevCounters *cnt,
-                                                      int32_t *part, const int32_t *scal0)
+// The query of one plan, one launch.  blockIdx.y = window batch.  Every
+// cached key of a window batch stamps its slot as held for this plan
+// (held[slot] = stamp) and counts it once per table; batch 0 (the planned
+// one) also records hit / slot and counts misses.  Per-table counts are summed
+// across the wave (keys are sorted, so a wave nearly always covers one table),
+// then across the block in LDS, then added to one of PART_COPIES copies of the
+// counters so that few blocks contend for an address.
+//
+// Every add a block makes returns its old value, and each thread tests the
+// values before the block's barrier, so all of a block's adds have been
+// performed when the block arrives.  The last block to arrive then publishes:
+// it sums the copies (device-scope atomic loads) and writes every counter word
+// to pinned, device-mapped, host-coherent memory as one 64-bit store tagged
+// with the query's sequence number.  The host polls until every word carries
+// it; no copy command, fence or stream synchronisation is involved, and each
+// word is whole when seen.  It then clears the copies, the per-plan counters
+// and the arrival count for the next query.
+__global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
+                                                 const uint64_t *__restrict__ hash, uint32_t mask,
+                                                 ProbeArgs pa, int32_t *held, int32_t stamp,
+                                                 int32_t *hit, int32_t *slot_u, DevCounters *cnt,
+                                                 int32_t *part, int32_t *arrived,
+                                                 const int32_t *scal0, uint64_t *host_mapped,
+                                                 uint32_t seq)
 {
     __shared__ int32_t c_miss[MAX_TABLES], c_held[MAX_TABLES];
+    __shared__ int32_t last_s;
     for (int t = threadIdx.x; t < T; t += BLOCK) c_miss[t] = c_held[t] = 0;
     __syncthreads();
     const int w = blockIdx.y;
     const int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    int32_t seen = 0;  // returned old values; tested below so the adds complete first
     if (w == 0 && i == 0) {
-        cnt->n_unique = scal0[0];
-        cnt->n_chunks = scal0[1];
-        cnt->n_multi = scal0[3];
+        seen |= atomicExch(&cnt->n_unique, scal0[0]) == INT32_MIN;
+        seen |= atomicExch(&cnt->n_chunks, scal0[1]) == INT32_MIN;
+        seen |= atomicExch(&cnt->n_multi, scal0[3]) == INT32_MIN;
     }
-    if (i == 0 && pa.nu[w][2]) atomicOr(&cnt->err, pa.nu[w][2]);  // the batch's input errors
+    if (i == 0 && pa.nu[w][2]) seen |= atomicOr(&cnt->err, pa.nu[w][2]) == INT32_MIN;
     const bool valid = i < *pa.nu[w];
     int t = 0;
     bool miss = false, fresh = false;
@@ -69,40 +82,21 @@ __global__ void __launch_bounds__(BLOCK) k_probe_hold(int32_t row_bits, int32_t 
     }
     __syncthreads();
     int32_t *p = part + (int64_t)((blockIdx.y * gridDim.x + blockIdx.x) % PART_COPIES) * 2 * MAX_TABLES;
-    for (int t = threadIdx.x; t < T; t += BLOCK) {
-        if (c_miss[t]) atomicAdd(&p[t], c_miss[t]);
-        if (c_held[t]) atomicAdd(&p[MAX_TABLES + t], c_held[t]);
+    for (int tt = threadIdx.x; tt < T; tt += BLOCK) {
+        if (c_miss[tt]) seen |= atomicAdd(&p[tt], c_miss[tt]);
+        if (c_held[tt]) seen |= atomicAdd(&p[MAX_TABLES + tt], c_held[tt]);
     }
-}
+    if (seen < 0) cnt->pad2[0] = seen;  // never taken (counts are not negative)
+    __syncthreads();
+    if (threadIdx.x == 0)
+        last_s = atomicAdd(arrived, 1) == (int32_t)(gridDim.x * gridDim.y) - 1;
+    __syncthreads();
+    if (!last_s) return;  // uniform per block
 
-void launch_probe_hold(const Tables &tb, const uint64_t *hash, uint32_t mask,
-                       const uint32_t *const *ukeys, const int32_t *const *nuniq, int nwin,
-                       int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk,
-                       DevCounters *cnt, int32_t *part, const int32_t *scal0, hipStream_t s)
-{
-    ProbeArgs pa{};
-    for (int w = 0; w < nwin; ++w) pa.uk[w] = ukeys[w], pa.nu[w] = nuniq[w];
-    // at least one block per batch so that every batch's error word is read
-    const int64_t n = max_unique > 0 ? max_unique : 1;
-    hipLaunchKernelGGL(k_probe_hold, dim3((unsigned)((n + BLOCK - 1) / BLOCK), nwin), dim3(BLOCK),
-                       0, s, tb.row_bits, tb.T, hash, mask, pa, held, stamp, tk.hit, tk.slot_u,
-                       cnt, part, scal0);
-}
-
-// Sum the probe's counter copies into the plan counters (clearing the copies),
-// then write the counters to pinned, device-mapped, host-coherent memory, each
-// as one 64-bit store tagged with the query's sequence number: the host polls
-// until every word carries it, with no copy command and no fence, and each
-// word is whole when seen.  Then clear the per-plan counters for the next
-// query.
-__global__ void __launch_bounds__(BLOCK) k_publish(DevCounters *cnt, int32_t *part, int32_t T,
-                                                   uint64_t *host_mapped, uint32_t seq)
-{
+    // ---- last block: publish
     __shared__ int32_t sums[2 * MAX_TABLES];
     for (int j = threadIdx.x; j < 2 * MAX_TABLES; j += BLOCK) sums[j] = 0;
     __syncthreads();
-    // the copies' words of the T tables: loads only in this loop, so they are
-    // all in flight together; cleared in a second loop
     const int n_rel = PART_COPIES * 2 * T;
     auto word = [T](int r) {
         const int c = r / (2 * T), jj = r % (2 * T);
@@ -110,29 +104,40 @@ __global__ void __launch_bounds__(BLOCK) k_publish(DevCounters *cnt, int32_t *pa
     };
     for (int r = threadIdx.x; r < n_rel; r += BLOCK) {
         const int idx = word(r);
-        const int32_t v = part[idx];
+        const int32_t v = __hip_atomic_load(&part[idx], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (v) atomicAdd(&sums[idx % (2 * MAX_TABLES)], v);
     }
     __syncthreads();
-    for (int r = threadIdx.x; r < n_rel; r += BLOCK) part[word(r)] = 0;
-    for (int j = threadIdx.x; j < 2 * MAX_TABLES; j += BLOCK) {
-        const int t = j % MAX_TABLES;
-        if (t >= T) continue;
-        if (j < MAX_TABLES) cnt->miss[t] = sums[j];
-        else cnt->held[t] = sums[j];
-    }
-    __syncthreads();
     int32_t *src = reinterpret_cast<int32_t *>(cnt);
-    for (int i = threadIdx.x; i < COUNTER_WORDS; i += BLOCK) {
-        host_mapped[i] = ((uint64_t)seq << 32) | (uint32_t)src[i];
-        if (i < COUNTERS_CLEARED) src[i] = 0;
+    constexpr int MISS0 = (int)(offsetof(DevCounters, miss) / sizeof(int32_t));
+    constexpr int HELD0 = (int)(offsetof(DevCounters, held) / sizeof(int32_t));
+    for (int k = threadIdx.x; k < COUNTER_WORDS; k += BLOCK) {
+        int32_t v;
+        if (k >= MISS0 && k < MISS0 + MAX_TABLES) v = k - MISS0 < T ? sums[k - MISS0] : 0;
+        else if (k >= HELD0 && k < HELD0 + MAX_TABLES) v = k - HELD0 < T ? sums[MAX_TABLES + k - HELD0] : 0;
+        else v = __hip_atomic_load(&src[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        host_mapped[k] = ((uint64_t)seq << 32) | (uint32_t)v;
+        if (k < COUNTERS_CLEARED)
+            __hip_atomic_store(&src[k], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+    for (int r = threadIdx.x; r < n_rel; r += BLOCK)
+        __hip_atomic_store(&part[word(r)], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x == 0) __hip_atomic_store(arrived, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-void launch_publish(DevCounters *cnt, int32_t *part, int32_t T, uint64_t *host_mapped,
-                    uint32_t seq, hipStream_t s)
+void launch_query(const Tables &tb, const uint64_t *hash, uint32_t mask,
+                  const uint32_t *const *ukeys, const int32_t *const *nuniq, int nwin,
+                  int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk,
+                  DevCounters *cnt, int32_t *part, int32_t *arrived, const int32_t *scal0,
+                  uint64_t *host_mapped, uint32_t seq, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_publish, dim3(1), dim3(BLOCK), 0, s, cnt, part, T, host_mapped, seq);
+    ProbeArgs pa{};
+    for (int w = 0; w < nwin; ++w) pa.uk[w] = ukeys[w], pa.nu[w] = nuniq[w];
+    // at least one block per batch so that every batch's error word is read
+    const int64_t n = max_unique > 0 ? max_unique : 1;
+    hipLaunchKernelGGL(k_query, dim3((unsigned)((n + BLOCK - 1) / BLOCK), nwin), dim3(BLOCK), 0, s,
+                       tb.row_bits, tb.T, hash, mask, pa, held, stamp, tk.hit, tk.slot_u, cnt,
+                       part, arrived, scal0, host_mapped, seq);
 }
 
 // ---------------------------------------------------------------- hash rebuild

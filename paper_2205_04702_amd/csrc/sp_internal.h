@@ -124,14 +124,14 @@ struct RadixPlan {
 RadixPlan radix_plan(int64_t n, int bits);
 
 // k_plan.hip
-void launch_probe_hold(const Tables &tb, const uint64_t *hash, uint32_t mask,
-                       const uint32_t *const *ukeys, const int32_t *const *nuniq, int nwin,
-                       int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk,
-                       DevCounters *cnt, int32_t *part, const int32_t *scal0, hipStream_t s);
-// Sums the probe's counter copies, publishes the counters (word i of
-// host_mapped = seq << 32 | counter word i), clears them.
-void launch_publish(DevCounters *cnt, int32_t *part, int32_t T, uint64_t *host_mapped,
-                    uint32_t seq, hipStream_t s);
+// The query: hold marks, hits and per-table counts of one plan, published to
+// host_mapped (word i = seq << 32 | counter word i) by the last block.
+void launch_query(const Tables &tb, const uint64_t *hash, uint32_t mask,
+                  const uint32_t *const *ukeys, const int32_t *const *nuniq, int nwin,
+                  int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk,
+                  DevCounters *cnt, int32_t *part, int32_t *arrived, const int32_t *scal0,
+                  uint64_t *host_mapped, uint32_t seq, hipStream_t s);
+
 void launch_hash_rebuild(uint64_t *hash, uint32_t mask, const int32_t *key_of_slot, int64_t nslots,
                          DevCounters *cnt, hipStream_t s);
 void launch_miss_compact(const uint32_t *ukeys, int64_t n_unique, TicketDev tk, ScanWs &ws,

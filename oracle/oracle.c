@@ -13,9 +13,10 @@
  *       (Sec. II-B "Forward propagation" and "Backpropagation"; plain SGD as
  *        stated in Sec. VI, the method leaves the optimiser unchanged).
  *   O2  reference planner for the GPU scratchpad: Hit-Map query, hold set
- *       from the look-forward window, LRU victims among unheld slots, Hit-Map
- *       update (Sec. IV-C hazard windows, Sec. IV-D Algorithm 1, LRU default
- *       of Sec. VI-E).
+ *       from the look-forward window, victims among unheld slots by the
+ *       replacement policy (LRU, the default, or LFU or random eviction, the
+ *       alternatives of Sec. VI-E), Hit-Map update (Sec. IV-C hazard windows,
+ *       Sec. IV-D Algorithm 1).
  *
  * Batch layout (both parts): one mini-batch is a table-major CSR.  ids[] holds
  * table 0's row IDs first, then table 1's, ...; bag g = t*B + b spans
@@ -31,6 +32,11 @@
 #define ORC_OK 0
 #define ORC_ERR_INVALID (-1)
 #define ORC_ERR_CAPACITY (-3)
+
+/* replacement policies (Sec. VI-E) */
+#define ORC_POLICY_LRU 0
+#define ORC_POLICY_LFU 1
+#define ORC_POLICY_RANDOM 2
 
 int orc_max_threads(void)
 {
@@ -145,30 +151,71 @@ void orc_train_step(int32_t T, int32_t B, int32_t D, float *const *tables,
 /* ------------------------------------------------------------------------- O2 */
 
 /*
+ * SplitMix64 (Steele, Lea and Flood, "Fast splittable pseudorandom number
+ * generators", OOPSLA 2014): the state advances by the golden-ratio gamma and
+ * each output is the state passed through the variant-13 64-bit finaliser.
+ * orc_splitmix64_nth returns output number n (n >= 1) of the generator
+ * started from state `seed`, i.e. the finaliser applied to seed + n * gamma.
+ */
+uint64_t orc_splitmix64_nth(uint64_t seed, uint64_t n)
+{
+    uint64_t z = seed + n * 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+/*
+ * Random-eviction priority of global slot g at plan u: a slot that never
+ * held a row gets 0 (free slots are used before anything is evicted); any
+ * other gets 1 + the top 24 bits of output number u * 2^31 + g + 1 of the
+ * seeded SplitMix64 stream, a fresh draw for every plan.  The victims are
+ * the unheld slots with the smallest (priority, slot): a uniformly random
+ * choice among the occupied candidates, up to ties of the 24-bit draws,
+ * which go to the lower slot.
+ */
+uint32_t orc_random_priority(uint64_t seed, int32_t u, int64_t g, int32_t last_use)
+{
+    if (last_use < 0) return 0;
+    uint64_t n = ((uint64_t)(uint32_t)u << 31) + (uint64_t)g + 1;
+    return 1u + (uint32_t)(orc_splitmix64_nth(seed, n) >> 40);
+}
+
+/*
  * Planner state per table t (Sec. IV-D, "GPU scratchpad design"):
  *   key_of_slot[s]  row cached in slot s, or -1 if the slot never held one;
  *   slot_of_row[r]  slot caching row r, or -1 (the Hit-Map, kept as a plain
  *                   array indexed by row);
  *   last_use[s]     index of the last plan whose current batch used slot s,
- *                   -1 for a slot that never held a row.
+ *                   -1 for a slot that never held a row;
+ *   uses[s]         plans whose current batch used slot s since its current
+ *                   row was placed there (the placing plan included), 0 for a
+ *                   slot that never held a row: the LFU frequency.
  */
 typedef struct {
     int32_t T;
+    int32_t policy;
+    uint64_t seed;
     int64_t *rows, *slots, *slot_base;
-    int32_t **key_of_slot, **last_use, **slot_of_row;
+    int32_t **key_of_slot, **last_use, **slot_of_row, **uses;
     int32_t u; /* plans committed so far = index of the next plan */
 } orc_planner;
 
-orc_planner *orc_planner_create(int32_t T, const int64_t *rows, const int64_t *slots)
+orc_planner *orc_planner_create(int32_t T, const int64_t *rows, const int64_t *slots,
+                                int32_t policy, uint64_t seed)
 {
+    if (policy < ORC_POLICY_LRU || policy > ORC_POLICY_RANDOM) return NULL;
     orc_planner *p = (orc_planner *)calloc(1, sizeof(orc_planner));
     p->T = T;
+    p->policy = policy;
+    p->seed = seed;
     p->rows = (int64_t *)malloc(sizeof(int64_t) * T);
     p->slots = (int64_t *)malloc(sizeof(int64_t) * T);
     p->slot_base = (int64_t *)malloc(sizeof(int64_t) * (T + 1));
     p->key_of_slot = (int32_t **)malloc(sizeof(int32_t *) * T);
     p->last_use = (int32_t **)malloc(sizeof(int32_t *) * T);
     p->slot_of_row = (int32_t **)malloc(sizeof(int32_t *) * T);
+    p->uses = (int32_t **)malloc(sizeof(int32_t *) * T);
     p->slot_base[0] = 0;
     for (int32_t t = 0; t < T; ++t) {
         p->rows[t] = rows[t];
@@ -177,6 +224,7 @@ orc_planner *orc_planner_create(int32_t T, const int64_t *rows, const int64_t *s
         p->key_of_slot[t] = (int32_t *)malloc(sizeof(int32_t) * slots[t]);
         p->last_use[t] = (int32_t *)malloc(sizeof(int32_t) * slots[t]);
         p->slot_of_row[t] = (int32_t *)malloc(sizeof(int32_t) * rows[t]);
+        p->uses[t] = (int32_t *)calloc((size_t)slots[t], sizeof(int32_t));
         for (int64_t s = 0; s < slots[t]; ++s) p->key_of_slot[t][s] = -1, p->last_use[t][s] = -1;
         for (int64_t r = 0; r < rows[t]; ++r) p->slot_of_row[t][r] = -1;
     }
@@ -191,7 +239,9 @@ void orc_planner_destroy(orc_planner *p)
         free(p->key_of_slot[t]);
         free(p->last_use[t]);
         free(p->slot_of_row[t]);
+        free(p->uses[t]);
     }
+    free(p->uses);
     free(p->key_of_slot);
     free(p->last_use);
     free(p->slot_of_row);
@@ -205,8 +255,9 @@ int32_t orc_planner_step(const orc_planner *p) { return p->u; }
 
 /* Read access to the committed state, for invariant checks. */
 void orc_planner_state(const orc_planner *p, int32_t t, int32_t *key_of_slot,
-                       int32_t *last_use, int32_t *slot_of_row)
+                       int32_t *last_use, int32_t *slot_of_row, int32_t *uses)
 {
+    if (uses) memcpy(uses, p->uses[t], sizeof(int32_t) * p->slots[t]);
     if (key_of_slot) memcpy(key_of_slot, p->key_of_slot[t], sizeof(int32_t) * p->slots[t]);
     if (last_use) memcpy(last_use, p->last_use[t], sizeof(int32_t) * p->slots[t]);
     if (slot_of_row) memcpy(slot_of_row, p->slot_of_row[t], sizeof(int32_t) * p->rows[t]);
@@ -218,16 +269,30 @@ static int orc_cmp_i32(const void *a, const void *b)
     return (x > y) - (x < y);
 }
 
+/* A candidate slot and its eviction priority: smaller goes first. */
 typedef struct {
-    int32_t last_use;
+    int64_t prio;
     int32_t slot;
 } orc_cand;
 
 static int orc_cmp_cand(const void *a, const void *b)
 {
     const orc_cand *x = (const orc_cand *)a, *y = (const orc_cand *)b;
-    if (x->last_use != y->last_use) return x->last_use < y->last_use ? -1 : 1;
+    if (x->prio != y->prio) return x->prio < y->prio ? -1 : 1;
     return (x->slot > y->slot) - (x->slot < y->slot);
+}
+
+/* Eviction priority of slot s of table t under the planner's policy:
+ * LRU the last use (never used = -1, first), LFU the use count (never used =
+ * 0, first), random the seeded draw of orc_random_priority. */
+static int64_t orc_priority(const orc_planner *p, int32_t t, int64_t s)
+{
+    switch (p->policy) {
+    case ORC_POLICY_LFU: return p->uses[t][s];
+    case ORC_POLICY_RANDOM:
+        return orc_random_priority(p->seed, p->u, p->slot_base[t] + s, p->last_use[t][s]);
+    default: return p->last_use[t][s];
+    }
 }
 
 /* Sorted unique rows of table t in one batch; returns the count. */
@@ -255,8 +320,10 @@ static int32_t orc_find(const int32_t *sorted, int32_t n, int32_t key)
 /*
  * Held slots of table t for this plan (Sec. IV-C, "Removing RAW-4" and
  * "Putting everything together"): a slot is held when the row it caches is
- * used by any batch of the window (the batch being planned and its visible
- * successors).  Rows not resident hold nothing.  held[] is zeroed here.
+ * used by any batch of the window (the batch being planned, its visible
+ * successors and, when the caller passes them, earlier batches still in
+ * flight: the past window).  Rows not resident hold nothing.  held[] is
+ * zeroed here.
  */
 static void orc_mark_held(const orc_planner *p, int32_t t, int32_t nwin,
                           const int32_t *const *win_ids, const int32_t *const *win_off,
@@ -273,18 +340,22 @@ static void orc_mark_held(const orc_planner *p, int32_t t, int32_t nwin,
 }
 
 /*
- * Plan the batch win[0] with look-forward window win[0..nwin-1].
+ * Plan the batch win[0] with hold window win[0..nwin-1] (its look-forward
+ * successors, and any past batches the caller wants held, in any order after
+ * win[0]).
  *
  * For each table t (Algorithm 1, canonicalised):
  *   U      sorted unique rows of win[0] in table t; inv[j] indexes U;
  *   hit    U[i] is cached (Hit-Map query, Step C);
  *   M      the missing rows of U in ascending order;
  *   C      unheld slots (never used, or caching a row no window batch uses);
- *   V      the |M| slots of C with the smallest (last_use, slot): the LRU
- *          choice of ChooseVictim, oldest first, ties by slot index;
+ *   V      the |M| slots of C with the smallest (priority, slot), in that
+ *          order: ChooseVictim under the policy (orc_priority), ties by slot
+ *          index;
  *   M[i] is placed in V[i]; V[i]'s previous row (if any) is evicted and
- *   leaves the Hit-Map;
- *   every slot of U gets last_use = u; slot_of[j] = slot of ids[j].
+ *   leaves the Hit-Map; V[i]'s use count restarts at 0;
+ *   every slot of U gets last_use = u and one more use; slot_of[j] = slot of
+ *   ids[j].
  * If any table has |M| > |C| the plan fails with ORC_ERR_CAPACITY and no
  * state changes (the worst-case sizing of Sec. IV-D is not met).
  *
@@ -364,7 +435,7 @@ int32_t orc_planner_plan(orc_planner *p, int32_t nwin, const int32_t *const *win
         int64_t nc = 0;
         for (int64_t s = 0; s < p->slots[t]; ++s)
             if (!held[s]) {
-                cand[nc].last_use = p->last_use[t][s];
+                cand[nc].prio = orc_priority(p, t, s);
                 cand[nc].slot = (int32_t)s;
                 ++nc;
             }
@@ -381,11 +452,13 @@ int32_t orc_planner_plan(orc_planner *p, int32_t nwin, const int32_t *const *win
             }
             p->key_of_slot[t][v] = m_row[mbase + i];
             p->slot_of_row[t][m_row[mbase + i]] = v;
+            p->uses[t][v] = 0;
         }
         for (int32_t i = 0; i < nu; ++i) {
             int32_t s = p->slot_of_row[t][U[i]];
             slot_u[ubase + i] = (int32_t)(p->slot_base[t] + s);
             p->last_use[t][s] = p->u;
+            p->uses[t][s] += 1;
         }
         for (int32_t j = j0; j < j1; ++j) slot_of[j] = slot_u[inv[j]];
         nU += nu;

@@ -4,7 +4,9 @@ TEST INFRASTRUCTURE ONLY: imported by the tests, the smoke check and the
 benchmark's CPU-baseline leg, never by the product library.
 
   forward / backward_sgd / train_step   uncached embedding-bag SGD (O1)
-  Planner                               reference scratchpad planner (O2)
+  Planner                               reference scratchpad planner (O2), with the
+                                        LRU, LFU and random replacement policies
+                                        (Sec. VI-E) and an optional past window
   CachedSimulator                       O2's plans applied to a CPU copy of the
                                         scratchpad, trained with O1's arithmetic (O3)
 
@@ -24,6 +26,7 @@ _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 OK, ERR_INVALID, ERR_CAPACITY = 0, -1, -3
+POLICIES = {"lru": 0, "lfu": 1, "random": 2}  # replacement policies of Sec. VI-E
 
 _i32p = np.ctypeslib.ndpointer(dtype=np.int32, flags="C_CONTIGUOUS")
 _i64p = np.ctypeslib.ndpointer(dtype=np.int64, flags="C_CONTIGUOUS")
@@ -43,11 +46,16 @@ def lib():
                                        _f32p, C.c_float]
         L.orc_max_threads.restype = C.c_int
         L.orc_planner_create.restype = C.c_void_p
-        L.orc_planner_create.argtypes = [C.c_int32, _i64p, _i64p]
+        L.orc_planner_create.argtypes = [C.c_int32, _i64p, _i64p, C.c_int32, C.c_uint64]
+        L.orc_splitmix64_nth.restype = C.c_uint64
+        L.orc_splitmix64_nth.argtypes = [C.c_uint64, C.c_uint64]
+        L.orc_random_priority.restype = C.c_uint32
+        L.orc_random_priority.argtypes = [C.c_uint64, C.c_int32, C.c_int64, C.c_int32]
         L.orc_planner_destroy.argtypes = [C.c_void_p]
         L.orc_planner_step.argtypes = [C.c_void_p]
         L.orc_planner_step.restype = C.c_int32
-        L.orc_planner_state.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p]
+        L.orc_planner_state.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
+                                        C.c_void_p]
         L.orc_planner_plan.restype = C.c_int32
         L.orc_planner_plan.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_int32,
                                        _i32p, _i32p, _i32p, _u8p, _i32p, _i32p, _i32p, _i32p,
@@ -58,6 +66,16 @@ def lib():
 
 def max_threads() -> int:
     return int(lib().orc_max_threads())
+
+
+def splitmix64_nth(seed: int, n: int) -> int:
+    """Output number n (n >= 1) of SplitMix64 started from state `seed`."""
+    return int(lib().orc_splitmix64_nth(C.c_uint64(seed), C.c_uint64(n)))
+
+
+def random_priority(seed: int, u: int, g: int, last_use: int) -> int:
+    """Random-eviction priority of global slot g at plan u (0 for a never-used slot)."""
+    return int(lib().orc_random_priority(C.c_uint64(seed), u, g, last_use))
 
 
 def _ptr_array(arrays):
@@ -113,14 +131,20 @@ class PlanResult:
 
 
 class Planner:
-    """Reference planner (O2).  plan() returns a PlanResult or raises PlanError."""
+    """Reference planner (O2).  plan() returns a PlanResult or raises PlanError.
 
-    def __init__(self, rows, slots):
+    policy: "lru" (the default of Sec. VI-E), "lfu" or "random"; seed feeds the
+    random policy's draws.
+    """
+
+    def __init__(self, rows, slots, policy: str = "lru", seed: int = 0):
         self.T = len(rows)
         self.rows = np.asarray(rows, dtype=np.int64)
         self.slots = np.asarray(slots, dtype=np.int64)
         self.slot_base = np.concatenate([[0], np.cumsum(self.slots)]).astype(np.int64)
-        self._h = lib().orc_planner_create(self.T, self.rows, self.slots)
+        self.policy, self.seed = policy, int(seed)
+        self._h = lib().orc_planner_create(self.T, self.rows, self.slots, POLICIES[policy],
+                                           C.c_uint64(self.seed))
 
     def __del__(self):
         h, self._h = getattr(self, "_h", None), None
@@ -135,11 +159,19 @@ class Planner:
         kos = np.empty(int(self.slots[t]), np.int32)
         lu = np.empty(int(self.slots[t]), np.int32)
         sor = np.empty(int(self.rows[t]), np.int32)
-        lib().orc_planner_state(self._h, t, kos.ctypes.data, lu.ctypes.data, sor.ctypes.data)
+        lib().orc_planner_state(self._h, t, kos.ctypes.data, lu.ctypes.data, sor.ctypes.data, None)
         return kos, lu, sor
 
-    def plan(self, window, B: int) -> PlanResult:
-        """window: list of (ids, bag_off) for the planned batch and its visible successors."""
+    def uses(self, t: int):
+        """Per-slot use counts of table t (the LFU frequency)."""
+        n = np.empty(int(self.slots[t]), np.int32)
+        lib().orc_planner_state(self._h, t, None, None, None, n.ctypes.data)
+        return n
+
+    def plan(self, window, B: int, past=()) -> PlanResult:
+        """window: list of (ids, bag_off) for the planned batch and its visible successors;
+        past: earlier batches whose cached rows are held as well (the past window)."""
+        window = list(window) + list(past)
         ids_l = [np.ascontiguousarray(w[0], np.int32) for w in window]
         off_l = [np.ascontiguousarray(w[1], np.int32) for w in window]
         nnz = int(off_l[0][-1])
@@ -180,11 +212,12 @@ class CachedSimulator:
     they are modified in place (write-backs, flush).
     """
 
-    def __init__(self, host_tables, slots, check_residency: bool = True):
+    def __init__(self, host_tables, slots, check_residency: bool = True, policy: str = "lru",
+                 seed: int = 0):
         self.host = host_tables
         self.D = host_tables[0].shape[1]
         rows = [t.shape[0] for t in host_tables]
-        self.planner = Planner(rows, slots)
+        self.planner = Planner(rows, slots, policy, seed)
         self.storage = np.zeros((int(self.planner.slot_base[-1]), self.D), np.float32)
         self.check = check_residency
         self.writebacks = 0
@@ -193,8 +226,8 @@ class CachedSimulator:
         b = self.planner.slot_base
         return [self.storage[b[t]:b[t + 1]] for t in range(len(self.host))]
 
-    def step(self, window, B: int, grad, lr: float, want_out: bool = False):
-        p = self.planner.plan(window, B)
+    def step(self, window, B: int, grad, lr: float, want_out: bool = False, past=()):
+        p = self.planner.plan(window, B, past)
         base = self.planner.slot_base
         # write back evicted rows (they were trained, so they are dirty), then fill misses
         for i in range(p.m_row.size):

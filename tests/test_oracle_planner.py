@@ -28,8 +28,11 @@ def snapshot(planner):
     return [planner.state(t) for t in range(planner.T)]
 
 
-def check_plan(planner, pre, post, window, B, p, u):
-    """Verify plan p (already applied: pre -> post) against the stated properties."""
+def check_plan(planner, pre, post, window, B, p, u, prio=None):
+    """Verify plan p (already applied: pre -> post) against the stated properties.
+
+    window holds every batch whose rows are held (the planned one first); prio[t]
+    gives each slot's eviction priority before the plan (default: last use, LRU)."""
     ids, off = window[0]
     T = planner.T
     base = planner.slot_base
@@ -56,11 +59,12 @@ def check_plan(planner, pre, post, window, B, p, u):
         for wi, wo in window:
             win_rows.update(int(r) for r in wi[int(wo[t * B]):int(wo[(t + 1) * B])])
         held = {int(sor0[r]) for r in win_rows if sor0[r] >= 0}
-        cand = sorted((int(lu0[s]), s) for s in range(S) if s not in held)
+        pr = lu0 if prio is None else prio[t]
+        cand = sorted((int(pr[s]), s) for s in range(S) if s not in held)
         victims = [int(v) - int(base[t]) for v in p.v_slot[m_off:m_off + k]]
         assert len(set(victims)) == k
-        # exactly the k smallest unheld slots by (last_use, slot), in that order
-        assert [(int(lu0[v]), v) for v in victims] == cand[:k]
+        # exactly the k smallest unheld slots by (priority, slot), in that order
+        assert [(int(pr[v]), v) for v in victims] == cand[:k]
         assert np.array_equal(p.v_old_row[m_off:m_off + k], kos0[victims])
         assert np.array_equal(p.v_old_use[m_off:m_off + k], lu0[victims])
         for old in kos0[victims]:

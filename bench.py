@@ -97,6 +97,10 @@ def main():
     ap.add_argument("--tables", type=int, default=0, metavar="N",
                     help="run only the workload's first N tables (one GPU's share when the "
                          "pinned host tables of the whole workload exceed what one process maps)")
+    ap.add_argument("--policy", choices=["lru", "lfu", "random"], default="lru",
+                    help="replacement policy (LRU is the method's default)")
+    ap.add_argument("--hold-past", type=int, default=0, metavar="P",
+                    help="also hold the rows of the P batches planned before each plan")
     ap.add_argument("--host-ids", action="store_true",
                     help="hand the batch IDs over from host memory (PCIe-inclusive variant)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -145,7 +149,7 @@ def main():
     timed = not args.no_timing
     every = max(1, args.time_every)
     ctx = sp.ScratchPipe(w.rows, w.dim, w.slots, L, host, max_batch=w.batch, max_ids=w.nnz,
-                         flags=0)
+                         flags=0, policy=args.policy, hold_past=args.hold_past)
     out = torch.empty((w.tables * w.batch, w.dim), dtype=torch.float32, device=dev)
 
     host_s = [0.0, 0.0, 0.0]  # host time inside plan / forward / backward calls
@@ -207,7 +211,9 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {**w.describe(), "ids": "host" if args.host_ids else "hbm"},
+        "config": {**w.describe(), "ids": "host" if args.host_ids else "hbm",
+                   **({"policy": args.policy} if args.policy != "lru" else {}),
+                   **({"hold_past": args.hold_past} if args.hold_past else {})},
     }
     detail = {"miss_rate": round(d["misses"] / max(d["unique"], 1), 4),
               "unique_per_step": round(n_unique, 1),

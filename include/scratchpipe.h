@@ -44,6 +44,23 @@ typedef int32_t sp_status;
 #define SP_ERR_HIP (-5)         /* a HIP runtime call failed (sticky)                  */
 #define SP_ERR_STATE (-6)       /* context unusable (after SP_ERR_HIP) or null handle  */
 
+/* sp_config.policy: how victims are chosen among unheld slots (Sec. VI-E
+ * names LRU as the default and random eviction and LFU as alternatives).
+ * Every policy takes the slots with the smallest (priority, slot):
+ *   LRU     priority = last plan that used the slot (never used: first)
+ *   LFU     priority = plans that used the slot since its current row was
+ *           placed there, the placing plan included (never used: 0, first)
+ *   RANDOM  priority = 0 for a never-used slot, else 1 + the top 24 bits of
+ *           output number u * 2^31 + g + 1 of a SplitMix64 stream started at
+ *           sp_config.seed (u = plan index, g = global slot): a fresh uniform
+ *           draw per slot and plan */
+#define SP_POLICY_LRU 0
+#define SP_POLICY_LFU 1
+#define SP_POLICY_RANDOM 2
+
+/* sp_config.hold_past at most: earlier batches a plan may hold as well */
+#define SP_MAX_HOLD_PAST 4
+
 /* sp_config.flags */
 #define SP_FLAG_DEBUG_SYNC 0x1u /* synchronise the device at the end of every call     */
 #define SP_FLAG_TIMING 0x2u     /* time forward/backward/plan/fill kernels with events */
@@ -64,6 +81,13 @@ typedef struct {
     int64_t max_ids;            /* largest nnz any batch will have (all tables)        */
     uint32_t flags;             /* SP_FLAG_*                                           */
     int32_t device;             /* HIP device ordinal                                  */
+    int32_t policy;             /* SP_POLICY_* (0 = LRU)                               */
+    int32_t hold_past;          /* 0..SP_MAX_HOLD_PAST, and lookahead + 1 + hold_past
+                                   <= 16: a plan also holds the rows of this many
+                                   batches planned before it (the past window of
+                                   Sec. IV-C), so no row a recent batch used is
+                                   evicted; 0 = look-forward window only          */
+    uint64_t seed;              /* SP_POLICY_RANDOM's stream                           */
 } sp_config;
 
 typedef struct {
@@ -153,12 +177,13 @@ sp_status sp_create(const sp_config *config, sp_handle *out);
  * all of that call's batches are read again on the next call).  Window
  * buffers may be reused when the call returns.  The plan queries the Hit-Map
  * for window[0]'s unique keys, holds
- * every cached slot used by any window batch, takes for each table's misses
- * the least-recently-used unheld slots (oldest first, ties by slot; the
- * ascending misses take them in that order), updates Hit-Map, slot keys and
- * last-use, and enqueues the evicted rows' write-back and the misses' fill
- * (Sec. IV-C "Putting everything together", Sec. IV-D Algorithm 1; LRU from
- * Sec. VI-E).  The host waits once for per-table counts.
+ * every cached slot used by any window batch (and by the hold_past batches
+ * planned before this one), takes for each table's misses the unheld slots
+ * that come first under the policy (smallest priority first, ties by slot;
+ * the ascending misses take them in that order), updates Hit-Map, slot keys,
+ * last-use and use counts, and enqueues the evicted rows' write-back and the
+ * misses' fill (Sec. IV-C "Putting everything together", Sec. IV-D
+ * Algorithm 1; policies from Sec. VI-E).  The host waits once for per-table counts.
  * Requires the previous ticket's sp_backward_update to have been issued.
  * Transactional: on SP_ERR_INVALID_ARG (ID out of range, bad offsets, sizes
  * above the config) or SP_ERR_CAPACITY (misses > unheld slots in some table)

@@ -231,6 +231,8 @@ class ScatterPool {
 struct sp_ctx {
     // configuration
     int T = 0, D = 0, L = 0, device = 0;
+    int policy = POLICY_LRU, P = 0;  // replacement policy, past batches held
+    uint64_t seed = 0;
     uint32_t flags = 0;
     int32_t max_batch = 0;
     int64_t max_ids = 0;
@@ -242,6 +244,7 @@ struct sp_ctx {
     // device state
     float *storage = nullptr;
     int32_t *key_of_slot = nullptr, *last_use = nullptr, *held = nullptr;
+    int32_t *uses = nullptr;  // per-slot use counts, LFU only
     uint64_t *hash = nullptr;
     uint32_t hash_mask = 0;
     int64_t hash_used = 0;
@@ -478,6 +481,9 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     h->T = T;
     h->D = c->dim;
     h->L = c->lookahead;
+    h->policy = c->policy;
+    h->P = c->hold_past;
+    h->seed = c->seed;
     h->device = c->device;
     h->flags = c->flags;
     h->max_batch = c->max_batch;
@@ -519,15 +525,16 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     TRY(dalloc(h, &h->key_of_slot, S));
     TRY(dalloc(h, &h->last_use, S));
     TRY(dalloc(h, &h->held, S));
+    if (h->policy == POLICY_LFU) TRY(dalloc(h, &h->uses, S));
     int64_t cap = 1024;
     while (cap < 2 * S) cap <<= 1;
     if (cap > (int64_t)1 << 32) return fail(nullptr, SP_ERR_INVALID_ARG, "too many slots");
     h->hash_mask = (uint32_t)(cap - 1);
     TRY(dalloc(h, &h->hash, cap));
 
-    // batches k-1 (training) .. k+L+1 (prepared ahead) plus one of slack
-    // batches k-1 (training) .. k+L+SP_MAX_AHEAD (prepared) plus one of slack
-    h->nring = h->L + 3 + SP_MAX_AHEAD;
+    // batches k-max(1, P) (training, or held as past) .. k+L+SP_MAX_AHEAD
+    // (prepared) plus one of slack
+    h->nring = h->L + 3 + SP_MAX_AHEAD + std::max(0, h->P - 1);
     h->ring.resize(h->nring);
     h->ring_batch.assign(h->nring, -1);
     h->ring_nnz.assign(h->nring, 0);
@@ -631,6 +638,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     // initial state: nothing cached
     HIPCHK(nullptr, hipMemsetAsync(h->key_of_slot, 0xFF, sizeof(int32_t) * S, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->last_use, 0xFF, sizeof(int32_t) * S, h->s_plan));
+    if (h->uses) HIPCHK(nullptr, hipMemsetAsync(h->uses, 0, sizeof(int32_t) * S, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->held, 0, sizeof(int32_t) * S, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->hash, 0xFF, sizeof(uint64_t) * cap, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->storage, 0, sizeof(float) * S * h->D, h->s_plan));
@@ -661,6 +669,11 @@ extern "C" sp_status sp_create(const sp_config *c, sp_handle *out)
         return fail(nullptr, SP_ERR_INVALID_ARG, "dim %d must be a power of two in 4..256", D);
     if (c->lookahead < 0 || c->lookahead >= MAX_WINDOW)
         return fail(nullptr, SP_ERR_INVALID_ARG, "lookahead %d not in 0..%d", c->lookahead, MAX_WINDOW - 1);
+    if (c->policy < POLICY_LRU || c->policy > POLICY_RANDOM)
+        return fail(nullptr, SP_ERR_INVALID_ARG, "unknown policy %d", c->policy);
+    if (c->hold_past < 0 || c->hold_past > SP_MAX_HOLD_PAST || c->lookahead + 1 + c->hold_past > MAX_WINDOW)
+        return fail(nullptr, SP_ERR_INVALID_ARG, "hold_past %d not in 0..%d with lookahead + 1 + hold_past <= %d",
+                    c->hold_past, SP_MAX_HOLD_PAST, MAX_WINDOW);
     if (c->max_batch < 0 || c->max_ids < 0 || c->max_ids > INT32_MAX - 1)
         return fail(nullptr, SP_ERR_INVALID_ARG, "bad max_batch / max_ids");
     if ((int64_t)T * c->max_batch + 1 > INT32_MAX) return fail(nullptr, SP_ERR_INVALID_ARG, "too many bags");
@@ -826,9 +839,19 @@ static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, int32_t *stamp_o
         nuniq[w] = h->ring[r].scal;
         max_nnz = std::max(max_nnz, h->ring_nnz[r]);
     }
+    // the past window: batches planned before k stay in the ring (nring covers them)
+    int nwin = nhold;
+    for (int64_t q = k - 1; q >= 0 && q >= k - h->P; --q, ++nwin) {
+        const int r = (int)(q % h->nring);
+        if (h->ring_batch[r] != q)
+            return fail(h, SP_ERR_HIP, "internal: past batch %lld is not in the window ring", (long long)q);
+        ukeys[nwin] = h->ring[r].ukeys;
+        nuniq[nwin] = h->ring[r].scal;
+        max_nnz = std::max(max_nnz, h->ring_nnz[r]);
+    }
     const int32_t stamp = ++h->stamp;
     *seq_out = ++h->qseq;
-    launch_query(h->tb, h->hash, h->hash_mask, ukeys, nuniq, nhold, max_nnz, h->held, stamp,
+    launch_query(h->tb, h->hash, h->hash_mask, ukeys, nuniq, nwin, max_nnz, h->held, stamp,
                  h->tk[e], h->cnt, h->cnt_part, h->cnt_part + PART_COPIES * 2 * MAX_TABLES,
                  h->ring[k % h->nring].scal, h->h_cnt_dev, *seq_out, h->s_plan);
     CHECK_LAUNCH(h);
@@ -968,17 +991,20 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
             }
             vb += c.miss[t];
         }
-        const int nb = std::max(1, bits_for((uint64_t)u));
-        a.lu_bits = nb;
+        // priority values: LRU last use + 1 <= u, LFU uses <= u + 1, random <= 2^24
+        const int nb = h->policy == POLICY_RANDOM ? 25
+                       : std::max(1, bits_for((uint64_t)u + (h->policy == POLICY_LFU)));
+        a.prio_bits = nb;
         a.act_bits = bits_for((uint64_t)(a.nact - 1));
         a.stamp = stamp;
+        a.prio = Prio{h->policy == POLICY_LFU ? h->uses : h->last_use, h->policy, (uint32_t)u, h->seed};
         const int levels = (nb + SEL_BITS - 1) / SEL_BITS;
-        launch_select_victims(a, levels, maxS, h->held, h->last_use, h->sel_state, h->sel_hist, h->vk0,
+        launch_select_victims(a, levels, maxS, h->held, h->sel_state, h->sel_hist, h->vk0,
                               h->vv0, h->vk1, (uint32_t *)nullptr, n_miss, h->hist, h->ws_plan,
                               tk.v_slot, &h->cnt->err_sticky, h->s_plan);
     }
     launch_commit(h->tb, h->hash, h->hash_mask, tk, b0, n_miss, th.n_unique, th.nnz, h->key_of_slot,
-                  h->last_use, u, h->cnt, h->s_plan);
+                  h->last_use, h->uses, u, h->cnt, h->s_plan);
     CHECK_LAUNCH(h);
     if (h->ws_plan.overflow) return fail(h, SP_ERR_HIP, "internal: scan workspace too small");
     HIPCHK(h, hipEventRecord(h->ev_planned[e], h->s_plan));

@@ -1,7 +1,8 @@
-// Planner kernels: Hit-Map query, hold marking over the look-forward window,
-// LRU victim choice among unheld slots, and the Hit-Map / slot-metadata commit
-// (Sec. IV-C "Putting everything together", Sec. IV-D Algorithm 1; LRU is the
-// default replacement policy of Sec. VI-E).
+// Planner kernels: Hit-Map query, hold marking over the hold window, victim
+// choice among unheld slots by the replacement policy, and the Hit-Map /
+// slot-metadata commit (Sec. IV-C "Putting everything together", Sec. IV-D
+// Algorithm 1; LRU is the default replacement policy of Sec. VI-E, LFU and
+// random eviction its alternatives).
 #include "sp_device.h"
 #include "sp_internal.h"
 
@@ -196,15 +197,17 @@ void launch_miss_compact(const uint32_t *ukeys, int64_t n_unique, TicketDev tk, 
                        MissOut{ukeys, tk.m_key, tk.m_uidx}, ws, s);
 }
 
-// ---------------------------------------------------------------- LRU victims
+// ---------------------------------------------------------------- victims
 //
-// For each table with k misses: the k smallest (last_use + 1, slot) among its
-// unheld slots (last_use = -1 for a never-used slot, so those go first).
-// A radix select on last_use + 1 (SEL_BITS per level, most significant first)
-// finds the threshold value v* and how many slots equal to v* to take (r); a
-// segmented scan then compacts, in slot order, every unheld slot below v* and
-// the first r equal to it; a stable radix sort on (table, last_use + 1) puts
-// them in LRU order with ties in slot order.  sel_state[2a] = v* prefix,
+// For each table with k misses: the k smallest (priority, slot) among its
+// unheld slots, the priority being the policy's (Prio: last use + 1 for LRU,
+// so never-used slots go first; use count for LFU; a fresh random draw for
+// random eviction).  A radix select on the priority (SEL_BITS per level, most
+// significant first) finds the threshold value v* and how many slots equal to
+// v* to take (r); a segmented scan then compacts, in slot order, every unheld
+// slot below v* and the first r equal to it; a stable radix sort on (table,
+// priority) puts them in priority order with ties in slot order.
+// sel_state[2a] = v* prefix,
 // sel_state[2a+1] = slots still to take at the current level,
 // sel_state[2 * MAX_TABLES + a] = blocks of the current level done with table a.
 
@@ -212,7 +215,7 @@ constexpr int SEL_ITEMS = 16;
 constexpr int SEL_CHUNK = BLOCK * SEL_ITEMS;
 
 // One level of the select, one launch.  Every block counts its chunk of one
-// active table's unheld slots by the current SEL_BITS of last_use + 1 (among
+// active table's unheld slots by the current SEL_BITS of the priority (among
 // slots matching the prefix found so far) and adds the counts to the table's
 // histogram.  The last block of a table to arrive then fixes the next SEL_BITS
 // of v* and the slots still to take, and leaves the histogram and its arrival
@@ -224,7 +227,7 @@ constexpr int SEL_CHUNK = BLOCK * SEL_ITEMS;
 // entries invalid (-1) before the compaction fills them, and clear (all
 // tables together) the n_zero counters the global victim sort accumulates into.
 __global__ void __launch_bounds__(BLOCK) k_sel_level(SelArgs a, int shift, int first,
-                                                     const int32_t *held, const int32_t *last_use,
+                                                     const int32_t *held,
                                                      int32_t *st, int32_t *hist, int32_t *arrived,
                                                      int32_t *victims, uint32_t *zero,
                                                      int64_t n_zero)
@@ -246,12 +249,12 @@ __global__ void __launch_bounds__(BLOCK) k_sel_level(SelArgs a, int shift, int f
         for (int r = 0; r < SEL_ITEMS; ++r) {  // all loads in flight together
             const int64_t s = s0 + (int64_t)r * BLOCK + threadIdx.x;
             hv[r] = s < S ? held[base + s] : a.stamp;
-            lv[r] = s < S ? last_use[base + s] : 0;
+            lv[r] = s < S ? a.prio.src[base + s] : 0;
         }
 #pragma unroll
         for (int r = 0; r < SEL_ITEMS; ++r) {
             if (hv[r] != a.stamp) {
-                const uint32_t key = (uint32_t)(lv[r] + 1);
+                const uint32_t key = a.prio.key(lv[r], base + s0 + (int64_t)r * BLOCK + threadIdx.x);
                 if (((uint64_t)key >> (shift + SEL_BITS)) == want)
                     atomicAdd(&h[(key >> shift) & (SEL_BINS - 1)], 1);
             }
@@ -310,21 +313,23 @@ struct SegAct {
 
 // (below v*) << 32 | (equal to v*) for an unheld slot, 0 for a held one.
 struct VictimFlag {
-    const int32_t *held, *last_use, *st;
+    const int32_t *held, *st;
+    Prio prio;
     int32_t stamp;
     __device__ uint64_t operator()(int64_t g, int y) const
     {
         if (held[g] == stamp) return 0;
-        uint32_t key = (uint32_t)(last_use[g] + 1), vstar = (uint32_t)st[2 * y];
+        uint32_t key = prio(g), vstar = (uint32_t)st[2 * y];
         if (key < vstar) return 1ull << 32;
         return key == vstar ? 1ull : 0ull;
     }
 };
 
 struct VictimOut {
-    const int32_t *last_use, *st;
+    const int32_t *st;
+    Prio prio;
     int32_t vbase[MAX_TABLES], k[MAX_TABLES];
-    int32_t lu_bits;
+    int32_t prio_bits;
     uint32_t *vk, *vv;
     uint32_t *hist0;                 // first sort pass's counters (digit-major), or null
     uint32_t digit_mask, tile_len, tiles;
@@ -346,18 +351,18 @@ struct VictimOut {
         else return;
         if (pos >= (uint32_t)k[y]) return;  // never write past the table's victims
         const int64_t idx = vbase[y] + pos;
-        const uint32_t key = ((uint32_t)y << lu_bits) | (uint32_t)(last_use[g] + 1);
+        const uint32_t key = ((uint32_t)y << prio_bits) | prio(g);
         vk[idx] = key;
         vv[idx] = (uint32_t)g;
         if (hist0) atomicAdd(&hist0[(key & digit_mask) * tiles + (uint32_t)idx / tile_len], 1u);
     }
 };
 
-// ---------------------------------------------------------------- LRU order in LDS
+// ---------------------------------------------------------------- victim order in LDS
 //
 // When every active table has at most VS_MAX victims, one block per table puts
-// its compacted victims (slot order) into LRU order: a stable LSD radix sort on
-// last_use + 1 in LDS, 8-bit digits.  Within a round of VS_THREADS keys, lanes
+// its compacted victims (slot order) into priority order: a stable LSD radix
+// sort on the priority in LDS, 8-bit digits.  Within a round of VS_THREADS keys, lanes
 // of a wave with the same digit find each other with ballots; the lowest of
 // them records the wave's count stamped with the round, so no clearing is
 // needed between rounds.
@@ -376,7 +381,7 @@ __global__ void __launch_bounds__(VS_THREADS) k_victim_sort(SelArgs a, const uin
     const int n = a.k[y] < VS_MAX ? a.k[y] : VS_MAX;
     const int64_t off = a.vbase[y];
     const int tid = threadIdx.x, w = wave_id(), lane = lane_id();
-    const uint32_t kmask = a.lu_bits >= 32 ? ~0u : ((1u << a.lu_bits) - 1u);
+    const uint32_t kmask = a.prio_bits >= 32 ? ~0u : ((1u << a.prio_bits) - 1u);
     for (int i = tid; i < n; i += VS_THREADS) {
         kb[0][i] = vk[off + i] & kmask;
         vb[0][i] = vv[off + i];
@@ -385,7 +390,7 @@ __global__ void __launch_bounds__(VS_THREADS) k_victim_sort(SelArgs a, const uin
     const uint64_t lt = lanemask_lt();
     int cur = 0;
     uint32_t stamp = 0;
-    for (int shift = 0; shift < a.lu_bits; shift += 8) {
+    for (int shift = 0; shift < a.prio_bits; shift += 8) {
         if (tid < 256) base[tid] = 0;
         __syncthreads();
         for (int i = tid; i < n; i += VS_THREADS) atomicAdd(&base[(kb[cur][i] >> shift) & 255u], 1u);
@@ -441,18 +446,18 @@ __global__ void __launch_bounds__(VS_THREADS) k_victim_sort(SelArgs a, const uin
 }
 
 void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int32_t *held,
-                           const int32_t *last_use, int32_t *sel_state, int32_t *sel_hist,
+                           int32_t *sel_state, int32_t *sel_hist,
                            uint32_t *vk0, uint32_t *vv0, uint32_t *vk1, uint32_t *vv1,
                            int64_t n_victims, uint32_t *hist, ScanWs &ws, int32_t *v_slot,
                            int32_t *err, hipStream_t s)
 {
     if (a.nact <= 0 || n_victims <= 0) return;
     // small victim sets are ordered per table in LDS; otherwise one global
-    // sort on (table, last_use + 1), whose compaction lands where the sort's
-    // last pass will end in v_slot
+    // sort on (table, priority), whose compaction lands where the sort's last
+    // pass will end in v_slot
     bool small = true;
     for (int y = 0; y < a.nact; ++y) small = small && a.k[y] <= VS_MAX;
-    const int bits = a.act_bits + a.lu_bits;
+    const int bits = a.act_bits + a.prio_bits;
     const int passes = small ? 1 : radix_passes(n_victims, bits);
     uint32_t *ck = (passes & 1) ? vk0 : vk1;
     uint32_t *cv = (passes & 1) ? vv0 : (uint32_t *)v_slot;
@@ -466,7 +471,7 @@ void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int
     for (int l = 0; l < levels; ++l) {
         int shift = (levels - 1 - l) * SEL_BITS;
         hipLaunchKernelGGL(k_sel_level, dim3(chunks, a.nact), dim3(BLOCK), 0, s, a, shift,
-                           (int)(l == 0), held, last_use, sel_state, sel_hist,
+                           (int)(l == 0), held, sel_state, sel_hist,
                            sel_state + 2 * MAX_TABLES, (int32_t *)cv, hist,
                            prehist ? rp.table * rp.passes : (int64_t)0);
     }
@@ -480,16 +485,16 @@ void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int
         out.last[y] = a.base[y] + a.S[y] - 1;
     }
     out.err = err;
-    out.last_use = last_use;
+    out.prio = a.prio;
     out.st = sel_state;
-    out.lu_bits = a.lu_bits;
+    out.prio_bits = a.prio_bits;
     out.vk = ck;
     out.vv = cv;
     out.hist0 = prehist ? hist : nullptr;
     out.digit_mask = prehist ? (1u << rp.dbits) - 1u : 0u;
     out.tile_len = prehist ? (uint32_t)(BLOCK * rp.items) : 1u;
     out.tiles = prehist ? (uint32_t)rp.tiles : 0u;
-    seg_scan<uint64_t>(seg, a.nact, maxS, VictimFlag{held, last_use, sel_state, a.stamp}, out, ws,
+    seg_scan<uint64_t>(seg, a.nact, maxS, VictimFlag{held, sel_state, a.prio, a.stamp}, out, ws,
                        s);
     if (small) {
         hipLaunchKernelGGL(k_victim_sort, dim3(a.nact), dim3(VS_THREADS), 0, s, a,
@@ -504,8 +509,9 @@ void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int
 
 // Threads [0, n_miss): miss i goes to victim slot v = v_slot[i]: record the
 // slot's previous occupant and its last use, erase that key from the Hit-Map,
-// enter the new key, then touch the slot (last_use = u) and point every
-// position of the key at it.  Erases and inserts may interleave across
+// enter the new key, then touch the slot (last_use = u; with use counts, the
+// new row's count starts at this plan's use) and point every position of the
+// key at it.  Erases and inserts may interleave across
 // threads: inserts only claim EMPTY or erased entries, so they never disturb
 // a live key another thread is erasing, and the keys inserted are known to be
 // absent.  Threads [n_miss, n_miss + max(n_unique, nnz)): touch the slots of
@@ -516,7 +522,7 @@ __global__ void __launch_bounds__(BLOCK) k_commit(uint64_t *hash, uint32_t mask,
                                                   const uint32_t *perm, int64_t n_miss,
                                                   int64_t n_unique, int64_t nnz, int64_t nslots,
                                                   int32_t *key_of_slot, int32_t *last_use,
-                                                  int32_t u, int32_t *err)
+                                                  int32_t *uses, int32_t u, int32_t *err)
 {
     const int64_t t = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
     if (t < n_miss) {
@@ -538,6 +544,7 @@ __global__ void __launch_bounds__(BLOCK) k_commit(uint64_t *hash, uint32_t mask,
         if (!hash_insert(hash, mask, key, v)) atomicOr(err, ERR_HASH_FULL);
         tk.slot_u[ui] = v;
         last_use[v] = u;
+        if (uses) uses[v] = 1;
         const int32_t p0 = seg_off[ui], p1 = seg_off[ui + 1];
         for (int32_t p = p0; p < p1; ++p) {
             const uint32_t j = perm[p];
@@ -548,7 +555,10 @@ __global__ void __launch_bounds__(BLOCK) k_commit(uint64_t *hash, uint32_t mask,
     const int64_t j = t - n_miss;
     if (j < n_unique && tk.hit[j]) {
         const int32_t v = tk.slot_u[j];
-        if ((uint32_t)v < (uint64_t)nslots) last_use[v] = u;
+        if ((uint32_t)v < (uint64_t)nslots) {
+            last_use[v] = u;
+            if (uses) uses[v] += 1;  // one thread per unique key, so one per slot
+        }
     }
     if (j < nnz) {
         const int32_t i = inv[j];
@@ -559,8 +569,8 @@ __global__ void __launch_bounds__(BLOCK) k_commit(uint64_t *hash, uint32_t mask,
 
 void launch_commit(const Tables &tb, uint64_t *hash, uint32_t mask, TicketDev tk,
                    const BatchDev &b, int64_t n_miss, int64_t n_unique, int64_t nnz,
-                   int32_t *key_of_slot, int32_t *last_use, int32_t u, DevCounters *cnt,
-                   hipStream_t s)
+                   int32_t *key_of_slot, int32_t *last_use, int32_t *uses, int32_t u,
+                   DevCounters *cnt, hipStream_t s)
 {
     const int64_t n = n_miss + (nnz > n_unique ? nnz : n_unique);
     if (n <= 0) return;
@@ -568,7 +578,7 @@ void launch_commit(const Tables &tb, uint64_t *hash, uint32_t mask, TicketDev tk
     hipLaunchKernelGGL(k_commit, dim3((unsigned)((n + BLOCK - 1) / BLOCK)), dim3(BLOCK), 0, s,
                        hash, mask, tk, (const int32_t *)b.inv, (const int32_t *)b.seg_off,
                        (const uint32_t *)b.perm, n_miss, n_unique, nnz, nslots, key_of_slot,
-                       last_use, u, &cnt->err_sticky);
+                       last_use, uses, u, &cnt->err_sticky);
 }
 
 }  // namespace sp

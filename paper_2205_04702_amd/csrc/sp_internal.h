@@ -82,12 +82,42 @@ struct TicketDev {
     int32_t *v_old_key, *v_old_lu;   // [n_miss] previous occupant / last use of that slot
 };
 
+// Replacement policies (Sec. VI-E): the values of SP_POLICY_*.
+constexpr int POLICY_LRU = 0, POLICY_LFU = 1, POLICY_RANDOM = 2;
+
+// Eviction priority of a slot: smaller goes first, ties by slot.  src[g] is
+// the slot's last use (LRU, random) or use count (LFU).
+//   LRU     last use + 1 (a never-used slot: 0)
+//   LFU     uses of the slot's current row (never used: 0)
+//   random  0 for a never-used slot, else 1 + the top 24 bits of SplitMix64
+//           output number u * 2^31 + g + 1 of the stream started at `seed`
+//           (Steele, Lea and Flood, OOPSLA 2014): a fresh draw per plan.
+struct Prio {
+    const int32_t *src;
+    int32_t policy;
+    uint32_t u;
+    uint64_t seed;
+    __host__ __device__ uint32_t key(int32_t v, int64_t g) const
+    {
+        if (policy == POLICY_LFU) return (uint32_t)v;
+        if (policy != POLICY_RANDOM) return (uint32_t)(v + 1);
+        if (v < 0) return 0u;
+        uint64_t z = seed + (((uint64_t)u << 31) + (uint64_t)g + 1) * 0x9E3779B97F4A7C15ull;
+        z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+        z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+        z ^= z >> 31;
+        return 1u + (uint32_t)(z >> 40);
+    }
+    __device__ uint32_t operator()(int64_t g) const { return key(src[g], g); }
+};
+
 // Victim selection arguments (active tables = those with misses).
 struct SelArgs {
     int32_t nact;
-    int32_t lu_bits;                 // bits of (last_use + 1) values
+    int32_t prio_bits;               // bits of the priority values
     int32_t act_bits;                // bits of the active-table index in sort keys
     int32_t stamp;
+    Prio prio;
     int32_t t[MAX_TABLES];
     int32_t k[MAX_TABLES];           // misses
     int64_t base[MAX_TABLES];        // first global slot of the table
@@ -136,17 +166,17 @@ void launch_hash_rebuild(uint64_t *hash, uint32_t mask, const int32_t *key_of_sl
                          DevCounters *cnt, hipStream_t s);
 void launch_miss_compact(const uint32_t *ukeys, int64_t n_unique, TicketDev tk, ScanWs &ws,
                          hipStream_t s);
-void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int32_t *held,
-                           const int32_t *last_use, int32_t *sel_state, int32_t *sel_hist,
+void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int32_t *held, int32_t *sel_state, int32_t *sel_hist,
                            uint32_t *vk0, uint32_t *vv0, uint32_t *vk1, uint32_t *vv1,
                            int64_t n_victims, uint32_t *hist, ScanWs &ws, int32_t *v_slot,
                            int32_t *err, hipStream_t s);
 // Misses into their victim slots, Hit-Map and slot metadata updated, every
 // slot the batch uses touched (last_use = u), slot_of filled.
+// uses: per-slot use counts (LFU), or null when the policy does not keep them
 void launch_commit(const Tables &tb, uint64_t *hash, uint32_t mask, TicketDev tk,
                    const BatchDev &b, int64_t n_miss, int64_t n_unique, int64_t nnz,
-                   int32_t *key_of_slot, int32_t *last_use, int32_t u, DevCounters *cnt,
-                   hipStream_t s);
+                   int32_t *key_of_slot, int32_t *last_use, int32_t *uses, int32_t u,
+                   DevCounters *cnt, hipStream_t s);
 
 // k_train.hip
 void launch_move(float *storage, int dim, const Tables &tb, float *const *host_dev, TicketDev tk,

@@ -26,6 +26,8 @@ SP_ERR_STATE = -6
 SP_FLAG_DEBUG_SYNC = 0x1
 SP_FLAG_TIMING = 0x2
 SP_MAX_AHEAD = 2  # batches after the hold window that sp_plan sorts early
+SP_MAX_HOLD_PAST = 4
+POLICIES = {"lru": 0, "lfu": 1, "random": 2}  # SP_POLICY_*
 
 _NAMES = {SP_ERR_INVALID_ARG: "SP_ERR_INVALID_ARG", SP_ERR_OOM: "SP_ERR_OOM",
           SP_ERR_CAPACITY: "SP_ERR_CAPACITY", SP_ERR_SEQUENCE: "SP_ERR_SEQUENCE",
@@ -42,7 +44,8 @@ class sp_config(C.Structure):
     _fields_ = [("num_tables", C.c_int32), ("rows", C.POINTER(C.c_int64)), ("dim", C.c_int32),
                 ("slots", C.POINTER(C.c_int64)), ("lookahead", C.c_int32),
                 ("host_tables", C.POINTER(C.c_void_p)), ("max_batch", C.c_int32),
-                ("max_ids", C.c_int64), ("flags", C.c_uint32), ("device", C.c_int32)]
+                ("max_ids", C.c_int64), ("flags", C.c_uint32), ("device", C.c_int32),
+                ("policy", C.c_int32), ("hold_past", C.c_int32), ("seed", C.c_uint64)]
 
 
 class sp_batch(C.Structure):
@@ -248,10 +251,14 @@ def _stream_handle(stream) -> int:
 
 
 class ScratchPipe:
-    """One scratchpad context over pinned host tables (see include/scratchpipe.h)."""
+    """One scratchpad context over pinned host tables (see include/scratchpipe.h).
+
+    policy: "lru", "lfu" or "random"; hold_past: earlier batches held as well;
+    seed: the random policy's stream."""
 
     def __init__(self, rows, dim, slots, lookahead, host_tables: HostTables, max_batch, max_ids,
-                 flags: int = 0, device: int = 0):
+                 flags: int = 0, device: int = 0, policy: str = "lru", hold_past: int = 0,
+                 seed: int = 0):
         self.T = len(rows)
         self.dim = dim
         self._rows = (C.c_int64 * self.T)(*[int(r) for r in rows])
@@ -259,7 +266,8 @@ class ScratchPipe:
         self._tabs = (C.c_void_p * self.T)(*host_tables.ptrs)
         cfg = sp_config(num_tables=self.T, rows=self._rows, dim=dim, slots=self._slots,
                         lookahead=lookahead, host_tables=self._tabs, max_batch=max_batch,
-                        max_ids=max_ids, flags=flags, device=device)
+                        max_ids=max_ids, flags=flags, device=device, policy=POLICIES[policy],
+                        hold_past=hold_past, seed=seed)
         self.handle = sp_create(cfg)
         self._desc_cache = {}
 

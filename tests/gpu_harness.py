@@ -35,7 +35,8 @@ def compare_plan(step, dump, ref, T, B):
     assert dump["n_evict"] == ref.n_evict, f"step {step}: evictions {dump['n_evict']} vs {ref.n_evict}"
 
 
-def run_gpu(w, batches, host, first=0, last=None, flags=0, prepare_ahead=0):
+def run_gpu(w, batches, host, first=0, last=None, flags=0, prepare_ahead=0, policy="lru",
+            hold_past=0, seed=0):
     """Train batches[first:last] on the GPU only (fresh context over `host`), then flush.
     prepare_ahead: how many batches after each window to hand over for early sorting."""
     import torch
@@ -44,7 +45,8 @@ def run_gpu(w, batches, host, first=0, last=None, flags=0, prepare_ahead=0):
     last = n if last is None else last
     T, B, D, L = w.tables, w.batch, w.dim, w.lookahead
     max_ids = max(int(b[0].size) for b in batches)
-    sp = ScratchPipe(w.rows, D, w.slots, L, host, max_batch=B, max_ids=max(max_ids, 1), flags=flags)
+    sp = ScratchPipe(w.rows, D, w.slots, L, host, max_batch=B, max_ids=max(max_ids, 1), flags=flags,
+                     policy=policy, hold_past=hold_past, seed=seed)
     try:
         out = torch.zeros((T * B, D), dtype=torch.float32, device=dev)
         for u in range(first, last):
@@ -77,11 +79,13 @@ def make_inputs(w, steps=None, ragged=None):
 
 def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all", flags=0,
                device_ids=False, ref_tables=None, sync_each_step=True, compare_tables=True,
-               return_tables=False, steps=None, prepare_ahead=0):
+               return_tables=False, steps=None, prepare_ahead=0, policy="lru", hold_past=0,
+               seed=0):
     """Train w on the GPU and with the oracle; assert parity; return a summary.
 
     prepare_ahead: also hand the GPU that many batches after the window
-    (prepared in advance, not held); the oracle always sees the plain window."""
+    (prepared in advance, not held); the oracle always sees the plain window.
+    policy, hold_past, seed: replacement policy and past window of both planners."""
     import torch
     dev = torch.device("cuda:0")
     if batches is None:
@@ -93,7 +97,7 @@ def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all"
     for t in range(T):
         wl.init_table(w, t, out=host[t])
     ref = ref_tables if ref_tables is not None else [wl.init_table(w, t) for t in range(T)]
-    planner = oracle.Planner(w.rows, w.slots)
+    planner = oracle.Planner(w.rows, w.slots, policy, seed)
     touched = [np.zeros(r, bool) for r in w.rows]
     dev_batches = None
     if device_ids:
@@ -101,7 +105,8 @@ def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all"
     plan_set = set(range(n)) if check_plan_steps == "all" else set(check_plan_steps)
     fwd_set = set(range(n)) if check_fwd_steps == "all" else set(check_fwd_steps)
     worst_fwd = 0.0
-    sp = ScratchPipe(w.rows, D, w.slots, L, host, max_batch=B, max_ids=max(max_ids, 1), flags=flags)
+    sp = ScratchPipe(w.rows, D, w.slots, L, host, max_batch=B, max_ids=max(max_ids, 1), flags=flags,
+                     policy=policy, hold_past=hold_past, seed=seed)
     try:
         out = torch.zeros((T * B, D), dtype=torch.float32, device=dev)
         for u in range(n):
@@ -111,7 +116,8 @@ def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all"
                                  if q < n]
             ticket = sp.plan([src[q] for q in gpu_idx])
             assert ticket == u
-            p = planner.plan([batches[q] for q in win_idx], B)
+            p = planner.plan([batches[q] for q in win_idx], B,
+                             past=batches[max(0, u - hold_past):u])
             if u in plan_set:
                 compare_plan(u, sp.debug_plan(ticket, max(int(batches[u][0].size), 1)), p, T, B)
             sp.forward(ticket, out)
@@ -167,7 +173,8 @@ def row_values(t, rows, dim):
     return ((h - 1001) * (0.05 / 1002)).astype(np.float32)
 
 
-def run_sampled_parity(w, steps, *, check_plan_steps, check_fwd_steps, say=print):
+def run_sampled_parity(w, steps, *, check_plan_steps, check_fwd_steps, say=print, policy="lru",
+                       hold_past=0, seed=0):
     """A full-size workload driven as the benchmark drives it (IDs in device memory, the two
     batches after the window handed over early) for `steps` steps.
 
@@ -207,15 +214,17 @@ def run_sampled_parity(w, steps, *, check_plan_steps, check_fwd_steps, say=print
         return np.concatenate(parts), off
 
     dev_batches = [(torch.from_numpy(i).to(dev), torch.from_numpy(o).to(dev)) for i, o in batches]
-    planner = oracle.Planner(w.rows, w.slots)
+    planner = oracle.Planner(w.rows, w.slots, policy, seed)
     max_ids = max(int(b[0].size) for b in batches)
-    sp = ScratchPipe(w.rows, D, w.slots, L, host, max_batch=B, max_ids=max_ids)
+    sp = ScratchPipe(w.rows, D, w.slots, L, host, max_batch=B, max_ids=max_ids, policy=policy,
+                     hold_past=hold_past, seed=seed)
     worst_fwd = 0.0
     try:
         out = torch.zeros((T * B, D), dtype=torch.float32, device=dev)
         for u in range(steps):
             ticket = sp.plan([dev_batches[q] for q in range(u, u + L + 1 + ahead)])
-            p = planner.plan([batches[q] for q in range(u, u + L + 1)], B)
+            p = planner.plan([batches[q] for q in range(u, u + L + 1)], B,
+                             past=batches[max(0, u - hold_past):u])
             if u in check_plan_steps:
                 compare_plan(u, sp.debug_plan(ticket, int(batches[u][0].size)), p, T, B)
             sp.forward(ticket, out)

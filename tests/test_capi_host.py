@@ -49,6 +49,7 @@ int main(void) {
   printf("sp_config %zu\\nsp_batch %zu\\nsp_stats %zu\\nsp_plan_dump %zu\\n",
          sizeof(sp_config), sizeof(sp_batch), sizeof(sp_stats), sizeof(sp_plan_dump));
   P(sp_config, max_ids); P(sp_config, flags); P(sp_config, device); P(sp_config, host_tables);
+  P(sp_config, policy); P(sp_config, hold_past); P(sp_config, seed);
   P(sp_batch, nnz); P(sp_batch, on_device); P(sp_stats, ms_forward); P(sp_stats, timed_fill);
   P(sp_plan_dump, hit); P(sp_plan_dump, nnz);
   return 0; }
@@ -86,6 +87,11 @@ def _cfg(**over):
     (dict(lookahead=16), "lookahead"),
     (dict(max_ids=-5), "max_"),
     (dict(flags=0x80), "flags"),
+    (dict(policy=3), "policy"),
+    (dict(policy=-1), "policy"),
+    (dict(hold_past=-1), "hold_past"),
+    (dict(hold_past=5), "hold_past"),
+    (dict(lookahead=12, hold_past=4), "hold_past"),
 ])
 def test_create_rejects_bad_configs(over, needle):
     cfg, keep = _cfg(**over)

@@ -149,7 +149,8 @@ def main():
     timed = not args.no_timing
     every = max(1, args.time_every)
     ctx = sp.ScratchPipe(w.rows, w.dim, w.slots, L, host, max_batch=w.batch, max_ids=w.nnz,
-                         flags=0, policy=args.policy, hold_past=args.hold_past)
+                         flags=0, policy=args.policy, hold_past=args.hold_past,
+                         max_table_ids=w.batch * max(w.pooling))
     out = torch.empty((w.tables * w.batch, w.dim), dtype=torch.float32, device=dev)
 
     host_s = [0.0, 0.0, 0.0]  # host time inside plan / forward / backward calls

@@ -88,6 +88,12 @@ typedef struct {
                                    Sec. IV-C), so no row a recent batch used is
                                    evicted; 0 = look-forward window only          */
     uint64_t seed;              /* SP_POLICY_RANDOM's stream                           */
+    int64_t max_table_ids;      /* 0, or the most IDs one table has in any batch: a
+                                   batch with a table above it is rejected
+                                   (SP_ERR_INVALID_ARG).  With max_table_ids and
+                                   max_batch both <= 8192 each table of a batch is
+                                   sorted and deduplicated by one workgroup in LDS,
+                                   the whole batch in one launch                    */
 } sp_config;
 
 typedef struct {

@@ -235,7 +235,7 @@ struct sp_ctx {
     uint64_t seed = 0;
     uint32_t flags = 0;
     int32_t max_batch = 0;
-    int64_t max_ids = 0;
+    int64_t max_ids = 0, max_table_ids = 0, nchunk_max = 0;
     int key_bits = 0, chunk = 0;
     Tables tb{};
     int64_t slots[MAX_TABLES]{}, total_slots = 0, maxS = 0;
@@ -287,6 +287,11 @@ struct sp_ctx {
     // host-coherent copy of the counters, one 64-bit word per counter: query
     // sequence number << 32 | value; and its device address
     uint64_t *h_cnt = nullptr, *h_cnt_dev = nullptr;
+    // ingests in LDS report that they have read the caller's arrays through
+    // word h_cnt[COUNTER_WORDS]: blocks count themselves in cons_counter
+    uint32_t *cons_counter = nullptr;
+    uint32_t cons_issued = 0, cons_seq = 0;
+    bool wait_cons_event = false, wait_cons_word = false;  // for the sp_plan call in progress
     uint32_t qseq = 0;        // sequence number of the last query issued
     uint32_t spec_seq = 0;    // that of the early query
 
@@ -488,6 +493,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     h->flags = c->flags;
     h->max_batch = c->max_batch;
     h->max_ids = c->max_ids;
+    h->max_table_ids = c->max_table_ids;
     h->chunk = chunk_positions(h->D);
     int64_t max_rows = 1;
     h->tb.T = T;
@@ -521,6 +527,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
 
     const int64_t S = h->total_slots, N = h->max_ids, TB1 = (int64_t)T * h->max_batch + 1;
     const int64_t nchunk_max = N + N / h->chunk + 1;
+    h->nchunk_max = nchunk_max;
     TRY(dalloc(h, &h->storage, S * h->D));
     TRY(dalloc(h, &h->key_of_slot, S));
     TRY(dalloc(h, &h->last_use, S));
@@ -560,7 +567,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
         TRY(dalloc(h, &b.seg_off, N + 1));
         TRY(dalloc(h, &b.seg_chunk0, N));
         TRY(dalloc(h, &b.chunk_desc, nchunk_max));
-        TRY(dalloc(h, &b.multi, N / (h->chunk + 1) + 2));
+        TRY(dalloc(h, &b.multi, multi_capacity(N, h->chunk)));
         TRY(dalloc(h, &b.scal, T + 3));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ring_ready[r], hipEventDisableTiming));
     }
@@ -611,7 +618,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     }
     {
         void *p = nullptr;
-        const size_t bytes = sizeof(uint64_t) * COUNTER_WORDS;
+        const size_t bytes = sizeof(uint64_t) * (COUNTER_WORDS + 1);
         hipError_t e = hipHostMalloc(&p, bytes, hipHostMallocMapped | hipHostMallocCoherent);
         if (e != hipSuccess) {
             (void)hipGetLastError();
@@ -623,6 +630,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
         HIPCHK(nullptr, hipHostGetDevicePointer((void **)&h->h_cnt_dev, p, 0));
     }
 
+    TRY(dalloc(h, &h->cons_counter, 1));
     HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_consumed, hipEventDisableTiming));
     HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_plan, hipStreamNonBlocking));
     HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_ingest, hipStreamNonBlocking));
@@ -636,6 +644,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     HIPCHK(nullptr, h->t_qry.init());
 
     // initial state: nothing cached
+    HIPCHK(nullptr, hipMemsetAsync(h->cons_counter, 0, sizeof(uint32_t), h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->key_of_slot, 0xFF, sizeof(int32_t) * S, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->last_use, 0xFF, sizeof(int32_t) * S, h->s_plan));
     if (h->uses) HIPCHK(nullptr, hipMemsetAsync(h->uses, 0, sizeof(int32_t) * S, h->s_plan));
@@ -674,6 +683,7 @@ extern "C" sp_status sp_create(const sp_config *c, sp_handle *out)
     if (c->hold_past < 0 || c->hold_past > SP_MAX_HOLD_PAST || c->lookahead + 1 + c->hold_past > MAX_WINDOW)
         return fail(nullptr, SP_ERR_INVALID_ARG, "hold_past %d not in 0..%d with lookahead + 1 + hold_past <= %d",
                     c->hold_past, SP_MAX_HOLD_PAST, MAX_WINDOW);
+    if (c->max_table_ids < 0) return fail(nullptr, SP_ERR_INVALID_ARG, "max_table_ids %lld < 0", (long long)c->max_table_ids);
     if (c->max_batch < 0 || c->max_ids < 0 || c->max_ids > INT32_MAX - 1)
         return fail(nullptr, SP_ERR_INVALID_ARG, "bad max_batch / max_ids");
     if ((int64_t)T * c->max_batch + 1 > INT32_MAX) return fail(nullptr, SP_ERR_INVALID_ARG, "too many bags");
@@ -765,8 +775,25 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
         ids = b.ids;
         off = b.bag_off;
     }
-    launch_ingest(h->tb, b, ids, off, bt.batch, bt.nnz, h->key_bits, h->chunk, h->itmp_k,
-                  h->itmp_v, h->ihist, h->ws_ingest, h->ev_consumed, h->s_ingest);
+    IngestCons ic{h->cons_counter, 0, h->h_cnt_dev + COUNTER_WORDS, 0};
+    if (bt.nnz > 0 && ingest_in_lds(h->max_table_ids, bt.batch)) {
+        // one launch; it reports when it has read its inputs (device arrays
+        // are the caller's; host arrays were copied into the ring above)
+        h->cons_issued += (uint32_t)h->T;
+        ic.target = h->cons_issued;
+        ic.seq = ++h->cons_seq;
+        if (bt.on_device) {
+            h->wait_cons_word = true;
+        } else {
+            HIPCHK(h, hipEventRecord(h->ev_consumed, h->s_ingest));
+            h->wait_cons_event = true;
+        }
+    } else {
+        h->wait_cons_event = true;  // recorded by launch_ingest once the inputs are read
+    }
+    launch_ingest(h->tb, b, ids, off, bt.batch, bt.nnz, h->key_bits, h->chunk, h->max_table_ids,
+                  h->max_ids, h->nchunk_max, h->itmp_k, h->itmp_v, h->ihist, h->ws_ingest,
+                  h->ev_consumed, ic, h->s_ingest);
     CHECK_LAUNCH(h);
     if (h->ws_ingest.overflow) return fail(h, SP_ERR_HIP, "internal: scan workspace too small");
     HIPCHK(h, hipEventRecord(h->ring_ready[r], h->s_ingest));
@@ -776,6 +803,27 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
     h->ring_nnz[r] = bt.nnz;
     h->ring_B[r] = bt.batch;
     return SP_OK;
+}
+
+// Wait until the ingests this sp_plan call enqueued have read the caller's
+// window arrays: the general path's event, and the word an ingest in LDS
+// writes once its blocks have read their inputs (stream order makes the last
+// one enough).  Stream errors end the wait; they surface on the next call
+// that checks the stream.
+static void wait_inputs_read(sp_ctx *h)
+{
+    if (h->wait_cons_event) (void)hipEventSynchronize(h->ev_consumed);
+    if (h->wait_cons_word) {
+        const volatile uint64_t *w = h->h_cnt + COUNTER_WORDS;
+        for (int64_t spin = 0; (uint32_t)*w != h->cons_seq; ++spin) {
+            if ((spin & 1023) == 1023 && hipStreamQuery(h->s_ingest) != hipErrorNotReady) {
+                (void)hipGetLastError();
+                break;  // idle (the word is final) or failed
+            }
+            __builtin_ia32_pause();
+        }
+    }
+    h->wait_cons_event = h->wait_cons_word = false;
 }
 
 // Wait until the query with sequence number seq has published every counter
@@ -889,15 +937,10 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     // query that needs them; the prepared-ahead batch goes after the query
     // has been enqueued, so its launches overlap the query on the GPU
     double tA = host_ms();
-    bool consumed = false;
     struct ConsumedGuard {  // the window buffers are the caller's again when we return
         sp_ctx *h;
-        const bool *flag;
-        ~ConsumedGuard()
-        {
-            if (*flag) (void)hipEventSynchronize(h->ev_consumed);
-        }
-    } guard{h, &consumed};
+        ~ConsumedGuard() { wait_inputs_read(h); }
+    } guard{h};
     for (int w = 0; w < n; ++w) {
         const int64_t q = k + w;
         const int r = (int)(q % h->nring);
@@ -905,7 +948,6 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
             return fail(h, SP_ERR_INVALID_ARG, "batch %lld changed shape between windows", (long long)q);
         if (w < nhold && h->ring_batch[r] != q) {
             TRY(ingest(h, window[w], q));
-            consumed = true;
         }
     }
 
@@ -925,7 +967,6 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     for (int w = nhold; w < n; ++w) {
         if (h->ring_batch[(k + w) % h->nring] != k + w) {
             TRY(ingest(h, window[w], k + w));
-            consumed = true;
         }
     }
     double tD = host_ms();
@@ -934,10 +975,12 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     TRY(wait_counts(h, seq, &c));
     double tE = host_ms();
     h->host_ms[2] += tE - tD;
-    if (c.err & (ERR_ID_RANGE | ERR_OFFSETS)) {
+    if (c.err & (ERR_ID_RANGE | ERR_OFFSETS | ERR_TABLE_IDS)) {
         for (int w = 0; w < n; ++w) h->ring_batch[(k + w) % h->nring] = -1;  // re-read on retry
         return fail(h, SP_ERR_INVALID_ARG, "%s in the window",
-                    (c.err & ERR_ID_RANGE) ? "row ID out of range" : "malformed bag offsets");
+                    (c.err & ERR_ID_RANGE)  ? "row ID out of range"
+                    : (c.err & ERR_OFFSETS) ? "malformed bag offsets"
+                                            : "a table with more IDs than max_table_ids");
     }
     if (c.err_sticky)
         return fail(h, SP_ERR_HIP, "internal planner inconsistency (flags %d) in an earlier plan",

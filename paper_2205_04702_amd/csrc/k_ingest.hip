@@ -35,12 +35,14 @@ void launch_zero_i32(int32_t *p, int64_t n, hipStream_t s) { launch_fill_i32(p, 
 //  * bag g < nbags: validate the offsets (non-decreasing, from 0 to nnz;
 //    ERR_OFFSETS otherwise, ranges clamped into [0, nnz)), write bag_of[j] = g
 //    for the bag's positions and copy the offsets into the window ring (when
-//    they are read from the caller's device memory).
+//    they are read from the caller's device memory); the first bag of each
+//    table also checks the table's ID count against max_table_ids (when set,
+//    ERR_TABLE_IDS).
 __global__ void __launch_bounds__(BLOCK) k_prepare(Tables tb, const int32_t *ids,
                                                    const int32_t *bag_off, int32_t *bag_off_copy,
                                                    int32_t B, int64_t nnz, int64_t nbags,
-                                                   uint32_t *keys, uint32_t *pos, int32_t *bag_of,
-                                                   int32_t *err)
+                                                   int64_t max_table_ids, uint32_t *keys,
+                                                   uint32_t *pos, int32_t *bag_of, int32_t *err)
 {
     const int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
     if (i < nnz) {
@@ -71,6 +73,9 @@ __global__ void __launch_bounds__(BLOCK) k_prepare(Tables tb, const int32_t *ids
             hi = hi < lo ? lo : (hi > nnz ? nnz : hi);
         }
         for (int64_t j = lo; j < hi; ++j) bag_of[j] = (int32_t)i;
+        if (max_table_ids > 0 && i % B == 0 &&
+            (int64_t)bag_off[i + B] - bag_off[i] > max_table_ids)
+            atomicOr(err, ERR_TABLE_IDS);
     }
 }
 
@@ -390,16 +395,272 @@ struct ChunkOut {
     }
 };
 
+// ---------------------------------------------------------------- whole tables in LDS
+//
+// When every table of a batch has at most IG_MAX IDs and the batch at most
+// IG_MAX bags per table, one launch does all of the above: one block per
+// table (blocks take tables in the order they start, from an atomic counter)
+// validates the table's offsets and IDs, sorts its entries (row << 26 | bag
+// << 13 | position, positions and bags local to the table) by row in LDS,
+// finds the runs of equal rows and their backward chunks, then publishes its
+// unique-key, chunk and long-run counts and its error bits (epoch-tagged, as
+// the single-pass scan does).  It adds up the counts of the tables before it,
+// which have all started, to place its outputs; the last table's block also
+// writes the batch totals.  The global order is the same as the general
+// path's: keys are table-major, so table t's sorted positions are its own
+// span of the batch.  Once a block has read all of its inputs it counts
+// itself in *cons; the block that completes the count (cons_target) writes
+// cons_seq to the host-coherent word cons_word, which tells the host that the
+// caller's arrays are no longer needed, long before the kernel ends.
+constexpr int IG_THREADS = 1024;
+constexpr int IG_WAVES = IG_THREADS / WAVE;
+constexpr int IG_ITEMS = 8;
+constexpr int IG_SHIFT_BAG = 13, IG_SHIFT_ROW = 26;
+static_assert(IG_THREADS * IG_ITEMS == IG_MAX, "one item per thread per round");
+
+__global__ void __launch_bounds__(IG_THREADS) k_ingest_table(Tables tb, const int32_t *ids,
+                                                             const int32_t *bag_off,
+                                                             int32_t *bag_off_copy, int32_t B,
+                                                             int64_t nnz, int32_t chunk,
+                                                             int64_t max_table_ids, BatchDev b,
+                                                             int64_t cap_u, int64_t cap_c,
+                                                             ScanDev d, uint32_t *cons,
+                                                             uint32_t cons_target,
+                                                             uint64_t *cons_word, uint32_t cons_seq)
+{
+    __shared__ uint64_t buf[2][IG_MAX];
+    __shared__ uint32_t wc[IG_WAVES][256];
+    __shared__ uint32_t base[256];
+    __shared__ uint32_t lds[IG_WAVES];
+    __shared__ uint32_t id_s, multi_s;
+    __shared__ int32_t err_s;
+    __shared__ uint32_t before_s[4];
+    const int tid = threadIdx.x;
+    if (tid == 0) {
+        id_s = atomicAdd(d.counter, 1u) - d.base;
+        multi_s = 0;
+        err_s = 0;
+    }
+    __syncthreads();
+    const int t = (int)id_s;
+    auto inputs_read = [&]() {  // thread 0, after every read of ids and bag_off
+        if (atomicAdd(cons, 1u) + 1u == cons_target)
+            __hip_atomic_store(cons_word, (uint64_t)cons_seq, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_SYSTEM);
+    };
+    if (t >= tb.T) {  // the counter and the host disagree: give up loudly
+        if (tid == 0) {
+            atomicOr(d.err, ERR_PLAN);
+            inputs_read();
+        }
+        return;
+    }
+    const int64_t nbags = (int64_t)tb.T * B;
+    // ---- offsets of the table's bags: validate, copy into the ring
+    int32_t err = 0;
+    for (int lb = tid; lb < B; lb += IG_THREADS) {
+        const int64_t g = (int64_t)t * B + lb;
+        const int64_t lo = bag_off[g], hi = bag_off[g + 1];
+        if (bag_off_copy != bag_off) {
+            bag_off_copy[g] = (int32_t)lo;
+            if (g == nbags - 1) bag_off_copy[g + 1] = (int32_t)hi;
+        }
+        if (lo > hi || lo < 0 || hi > nnz || (g == 0 && lo != 0) || (g == nbags - 1 && hi != nnz))
+            err |= ERR_OFFSETS;
+    }
+    int64_t j0 = bag_off[(int64_t)t * B], j1 = bag_off[(int64_t)(t + 1) * B];
+    j0 = j0 < 0 ? 0 : (j0 > nnz ? nnz : j0);
+    j1 = j1 < j0 ? j0 : (j1 > nnz ? nnz : j1);
+    int n = (int)(j1 - j0 < IG_MAX ? j1 - j0 : IG_MAX);
+    if (j1 - j0 > max_table_ids) err |= ERR_TABLE_IDS;  // the rest is left out; the plan fails
+    // ---- entries by position, then each bag marks its positions
+    const int rb = tb.row_bits;
+    for (int i = tid; i < n; i += IG_THREADS) {
+        int32_t row = ids[j0 + i];
+        if (row < 0 || (int64_t)row >= tb.rows[t]) {
+            err |= ERR_ID_RANGE;
+            row = 0;
+        }
+        buf[0][i] = ((uint64_t)(uint32_t)row << IG_SHIFT_ROW) | (uint64_t)i;
+    }
+    __syncthreads();
+    for (int lb = tid; lb < B; lb += IG_THREADS) {
+        const int64_t g = (int64_t)t * B + lb;
+        int64_t lo = bag_off[g] - j0, hi = bag_off[g + 1] - j0;
+        lo = lo < 0 ? 0 : lo;
+        hi = hi > n ? n : hi;
+        for (int64_t i = lo; i < hi; ++i) buf[0][i] |= (uint64_t)lb << IG_SHIFT_BAG;
+    }
+    if (err) atomicOr(&err_s, err);
+    __syncthreads();
+    if (tid == 0) inputs_read();
+    uint64_t *srt = lds_radix_sort<IG_THREADS>(buf[0], buf[1], n, IG_SHIFT_ROW, rb, wc, base, lds);
+    // the other buffer holds each run's first sorted index and its first chunk
+    uint32_t *run0 = reinterpret_cast<uint32_t *>(srt == buf[0] ? buf[1] : buf[0]);
+    uint32_t *chunk0 = run0 + IG_MAX;
+
+    // ---- runs of equal rows (blocked: thread tid owns items tid*8 .. tid*8+7)
+    const int i0 = tid * IG_ITEMS;
+    uint32_t heads = 0;
+    uint64_t e[IG_ITEMS];
+#pragma unroll
+    for (int q = 0; q < IG_ITEMS; ++q) {
+        const int i = i0 + q;
+        e[q] = i < n ? srt[i] : 0ull;
+        const bool h = i < n && (i == 0 || (srt[i - 1] >> IG_SHIFT_ROW) != (e[q] >> IG_SHIFT_ROW));
+        heads |= (uint32_t)h << q;
+    }
+    uint32_t nU;
+    const uint32_t seg_first = block_excl_scan_n<IG_THREADS>((uint32_t)__popc(heads), lds, nU);
+    {
+        uint32_t sg = seg_first;
+#pragma unroll
+        for (int q = 0; q < IG_ITEMS; ++q)
+            if ((heads >> q) & 1u) run0[sg++] = (uint32_t)(i0 + q);
+    }
+    __syncthreads();
+    // chunks per run (blocked over runs)
+    uint32_t nch[IG_ITEMS], csum = 0, msum = 0;
+#pragma unroll
+    for (int q = 0; q < IG_ITEMS; ++q) {
+        const uint32_t sr = (uint32_t)(i0 + q);
+        nch[q] = 0;
+        if (sr < nU) {
+            const uint32_t len = (sr + 1 < nU ? run0[sr + 1] : (uint32_t)n) - run0[sr];
+            nch[q] = (len + (uint32_t)chunk - 1) / (uint32_t)chunk;
+            csum += nch[q];
+            msum += nch[q] > 1;
+        }
+    }
+    uint32_t nC;
+    uint32_t cb = block_excl_scan_n<IG_THREADS>(csum, lds, nC);
+    uint32_t nM;
+    (void)block_excl_scan_n<IG_THREADS>(msum, lds, nM);
+#pragma unroll
+    for (int q = 0; q < IG_ITEMS; ++q) {
+        const uint32_t sr = (uint32_t)(i0 + q);
+        if (sr < nU) chunk0[sr] = cb;
+        cb += nch[q];
+    }
+
+    // ---- publish this table's counts, add up those of the tables before it
+    uint64_t *st = d.status + (int64_t)t * LB_WORDS;
+    if (tid == 0) {
+        const uint32_t mine[4] = {nU, nC, nM, (uint32_t)err_s};
+#pragma unroll
+        for (int c = 0; c < 4; ++c) lb_publish<uint32_t>(st + c, d.epoch, mine[c]);
+    }
+    if (tid < WAVE) {
+        uint32_t v[4] = {0, 0, 0, 0};
+        if (tid < t) {  // T <= 64: one lane per earlier table
+            const uint64_t *w = d.status + (int64_t)tid * LB_WORDS;
+            int spins = 0;
+            bool ok = false;
+            while (!ok) {
+                ok = true;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) ok = lb_read<uint32_t>(w + c, d.epoch, v[c]) && ok;
+                if (!ok && ++spins > LB_SPIN) {  // counted as zero; result flagged wrong
+                    atomicOr(d.err, ERR_PLAN);
+                    v[0] = v[1] = v[2] = v[3] = 0;
+                    break;
+                }
+                if (!ok) __builtin_amdgcn_s_sleep(1);
+            }
+        }
+        const uint32_t u0 = wave_sum(v[0]), c0 = wave_sum(v[1]), m0 = wave_sum(v[2]);
+        uint32_t eo = v[3];
+#pragma unroll
+        for (int o = WAVE / 2; o > 0; o >>= 1) eo |= __shfl_xor(eo, o, WAVE);
+        if (tid == 0) {
+            before_s[0] = u0;
+            before_s[1] = c0;
+            before_s[2] = m0;
+            before_s[3] = eo;
+        }
+    }
+    __syncthreads();
+    const uint32_t U0 = before_s[0], C0 = before_s[1], M0 = before_s[2];
+
+    // ---- outputs: positions
+    uint32_t sg = seg_first;
+#pragma unroll
+    for (int q = 0; q < IG_ITEMS; ++q) {
+        const int i = i0 + q;
+        if (i >= n) break;
+        const uint32_t row = (uint32_t)(e[q] >> IG_SHIFT_ROW);
+        const int32_t bag = (int32_t)((e[q] >> IG_SHIFT_BAG) & ((1u << (IG_SHIFT_ROW - IG_SHIFT_BAG)) - 1u));
+        const int64_t pos = j0 + (int64_t)(e[q] & ((1u << IG_SHIFT_BAG) - 1u));
+        const int64_t gi = j0 + i;
+        if ((heads >> q) & 1u) {
+            if ((int64_t)U0 + sg < cap_u) {
+                b.ukeys[U0 + sg] = ((uint32_t)t << rb) | row;
+                b.seg_off[U0 + sg] = (int32_t)gi;
+            }
+            ++sg;
+        }
+        b.perm[gi] = (uint32_t)pos;
+        b.sbag[gi] = (int32_t)((int64_t)t * B + bag);
+        b.inv[pos] = (int32_t)(U0 + sg - 1);
+    }
+    // ---- outputs: runs and their backward chunks
+#pragma unroll
+    for (int q = 0; q < IG_ITEMS; ++q) {
+        const uint32_t sr = (uint32_t)(i0 + q);
+        if (sr >= nU) break;
+        const int64_t gs = (int64_t)U0 + sr;
+        const int64_t c0 = (int64_t)C0 + chunk0[sr];
+        if (gs >= cap_u) break;
+        b.seg_chunk0[gs] = (int32_t)c0;
+        const int32_t s0 = (int32_t)(j0 + run0[sr]);
+        const int32_t s1 = (int32_t)(j0 + (sr + 1 < nU ? run0[sr + 1] : (uint32_t)n));
+        for (uint32_t c = 0; c < nch[q] && c0 + c < cap_c; ++c) {
+            const int32_t p0 = s0 + (int32_t)c * chunk;
+            b.chunk_desc[c0 + c] = make_int4(p0, p0 + chunk < s1 ? p0 + chunk : s1, (int32_t)gs,
+                                             (int32_t)nch[q]);
+        }
+        if (nch[q] > 1) {
+            const uint32_t m = M0 + atomicAdd(&multi_s, 1u);  // list order is irrelevant
+            if ((int64_t)m < multi_capacity(cap_u, chunk)) b.multi[m] = (int32_t)gs;
+        }
+    }
+    if (t == tb.T - 1 && tid == 0) {  // the batch totals
+        const uint32_t U = U0 + nU;
+        if ((int64_t)U < cap_u + 1) b.seg_off[U] = (int32_t)nnz;
+        b.scal[0] = (int32_t)U;
+        b.scal[1] = (int32_t)(C0 + nC);
+        b.scal[2] = (int32_t)(before_s[3] | (uint32_t)err_s);
+        b.scal[3] = (int32_t)(M0 + nM);
+    }
+}
+
 // Sort, deduplicate and split into backward chunks one batch of the window.
 // ids / bag_off may be the caller's device arrays (read once, here) or the
 // ring's own copies; the ring always ends up with the offsets.  Input errors
 // are recorded in the batch's own scal[2].
 void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, const int32_t *bag_off,
-                   int32_t B, int64_t nnz, int key_bits, int chunk, uint32_t *tmp_k,
-                   uint32_t *tmp_v, uint32_t *hist, ScanWs &ws, hipEvent_t consumed,
+                   int32_t B, int64_t nnz, int key_bits, int chunk, int64_t max_table_ids,
+                   int64_t cap_u, int64_t cap_c, uint32_t *tmp_k, uint32_t *tmp_v,
+                   uint32_t *hist, ScanWs &ws, hipEvent_t consumed, const IngestCons &ic,
                    hipStream_t s)
 {
     const int64_t nbags = (int64_t)tb.T * B;
+    if (nnz > 0 && ingest_in_lds(max_table_ids, B)) {
+        if (tb.T > ws.max_tiles) {
+            ws.overflow = true;
+            return;
+        }
+        if (ws.epoch == 0xFFFFFFFFu) {  // epochs wrapped: forget every published word
+            (void)hipMemsetAsync(ws.status, 0, sizeof(uint64_t) * LB_WORDS * ws.max_tiles, s);
+            ws.epoch = 0;
+        }
+        ScanDev d{ws.status, ws.counter, ws.err, ws.issued, ++ws.epoch, (uint32_t)tb.T, 1};
+        ws.issued += (uint32_t)tb.T;
+        hipLaunchKernelGGL(k_ingest_table, dim3((unsigned)tb.T), dim3(IG_THREADS), 0, s, tb, ids,
+                           bag_off, b.bag_off, B, nnz, chunk, max_table_ids, b, cap_u, cap_c, d,
+                           ic.counter, ic.target, ic.word, ic.seq);
+        return;
+    }
     launch_zero_i32(b.scal, 4, s);
     // place the keys so that the final sort pass lands in skeys/perm
     const int passes = radix_passes(nnz, key_bits);
@@ -408,11 +669,11 @@ void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, cons
     const int64_t nthr = nnz > nbags ? nnz : nbags;
     if (nthr > 0)
         hipLaunchKernelGGL(k_prepare, dim3((unsigned)((nthr + BLOCK - 1) / BLOCK)), dim3(BLOCK), 0,
-                           s, tb, ids, bag_off, b.bag_off, B, nnz, nbags, k0, v0, b.bag_of,
-                           b.scal + 2);
+                           s, tb, ids, bag_off, b.bag_off, B, nnz, nbags, max_table_ids, k0, v0,
+                           b.bag_of, b.scal + 2);
     else if (bag_off != b.bag_off)
-        hipMemcpyAsync(b.bag_off, bag_off, sizeof(int32_t), hipMemcpyDeviceToDevice, s);
-    hipEventRecord(consumed, s);  // the caller's arrays are not read after this point
+        (void)hipMemcpyAsync(b.bag_off, bag_off, sizeof(int32_t), hipMemcpyDeviceToDevice, s);
+    (void)hipEventRecord(consumed, s);  // the caller's arrays are not read after this point
     if (nnz > 0) {
         bool in_k1 = false;
         launch_radix_sort(k0, v0, k1, v1, nnz, key_bits, hist, ws, &in_k1, s, false);

@@ -57,6 +57,19 @@ constexpr int COUNTERS_CLEARED = (int)(offsetof(DevCounters, err_sticky) / sizeo
 constexpr int PART_COPIES = 64;  // copies of the per-table counters the probe adds into
 constexpr int COUNTER_WORDS = (int)(sizeof(DevCounters) / sizeof(int32_t));
 constexpr int32_t ERR_ID_RANGE = 1, ERR_OFFSETS = 2, ERR_HASH_FULL = 4, ERR_PLAN = 8;
+constexpr int32_t ERR_TABLE_IDS = 16;  // a table has more IDs than the configured bound
+
+// Entries of a batch's list of runs longer than one chunk: such a run has at
+// least chunk + 1 positions.
+__host__ __device__ inline int64_t multi_capacity(int64_t max_ids, int chunk) { return max_ids / (chunk + 1) + 2; }
+
+// Batches whose tables each have at most IG_MAX IDs (and at most IG_MAX bags)
+// are ingested by one launch, one workgroup per table, entirely in LDS.
+constexpr int IG_MAX = 8192;
+inline bool ingest_in_lds(int64_t max_table_ids, int64_t B)
+{
+    return max_table_ids > 0 && max_table_ids <= IG_MAX && B <= IG_MAX;
+}
 
 // One window-ring entry: a batch as it arrived plus its sort/dedup products.
 struct BatchDev {
@@ -133,9 +146,21 @@ inline int chunk_positions(int /*dim*/) { return 16; }
 // k_ingest.hip
 void launch_zero_i32(int32_t *p, int64_t n, hipStream_t s);
 void launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
+// How an ingest in LDS reports that it has read its inputs: blocks count
+// themselves in *counter (it only grows); the one that reaches target writes
+// seq to the host-coherent *word.
+struct IngestCons {
+    uint32_t *counter;
+    uint32_t target;
+    uint64_t *word;
+    uint32_t seq;
+};
+// Ingest one batch.  In LDS (ingest_in_lds and nnz > 0) the inputs are known
+// read when *ic.word reads ic.seq; otherwise when `consumed` completes.
 void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, const int32_t *bag_off,
-                   int32_t B, int64_t nnz, int key_bits, int chunk, uint32_t *tmp_k,
-                   uint32_t *tmp_v, uint32_t *hist, ScanWs &ws, hipEvent_t consumed,
+                   int32_t B, int64_t nnz, int key_bits, int chunk, int64_t max_table_ids,
+                   int64_t cap_u, int64_t cap_c, uint32_t *tmp_k, uint32_t *tmp_v,
+                   uint32_t *hist, ScanWs &ws, hipEvent_t consumed, const IngestCons &ic,
                    hipStream_t s);
 
 void launch_radix_sort(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *v1, int64_t n,

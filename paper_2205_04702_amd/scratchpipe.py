@@ -45,7 +45,8 @@ class sp_config(C.Structure):
                 ("slots", C.POINTER(C.c_int64)), ("lookahead", C.c_int32),
                 ("host_tables", C.POINTER(C.c_void_p)), ("max_batch", C.c_int32),
                 ("max_ids", C.c_int64), ("flags", C.c_uint32), ("device", C.c_int32),
-                ("policy", C.c_int32), ("hold_past", C.c_int32), ("seed", C.c_uint64)]
+                ("policy", C.c_int32), ("hold_past", C.c_int32), ("seed", C.c_uint64),
+                ("max_table_ids", C.c_int64)]
 
 
 class sp_batch(C.Structure):
@@ -254,11 +255,12 @@ class ScratchPipe:
     """One scratchpad context over pinned host tables (see include/scratchpipe.h).
 
     policy: "lru", "lfu" or "random"; hold_past: earlier batches held as well;
-    seed: the random policy's stream."""
+    seed: the random policy's stream; max_table_ids: 0 or the most IDs any one
+    table has in a batch (a promise that is checked)."""
 
     def __init__(self, rows, dim, slots, lookahead, host_tables: HostTables, max_batch, max_ids,
                  flags: int = 0, device: int = 0, policy: str = "lru", hold_past: int = 0,
-                 seed: int = 0):
+                 seed: int = 0, max_table_ids: int = 0):
         self.T = len(rows)
         self.dim = dim
         self._rows = (C.c_int64 * self.T)(*[int(r) for r in rows])
@@ -267,7 +269,7 @@ class ScratchPipe:
         cfg = sp_config(num_tables=self.T, rows=self._rows, dim=dim, slots=self._slots,
                         lookahead=lookahead, host_tables=self._tabs, max_batch=max_batch,
                         max_ids=max_ids, flags=flags, device=device, policy=POLICIES[policy],
-                        hold_past=hold_past, seed=seed)
+                        hold_past=hold_past, seed=seed, max_table_ids=max_table_ids)
         self.handle = sp_create(cfg)
         self._desc_cache = {}
 

@@ -35,8 +35,18 @@ def compare_plan(step, dump, ref, T, B):
     assert dump["n_evict"] == ref.n_evict, f"step {step}: evictions {dump['n_evict']} vs {ref.n_evict}"
 
 
+def table_bound(w, batches):
+    """The most IDs any one table has in any of the batches."""
+    B = w.batch
+    return max(int(np.max(np.diff(np.asarray(off)[::B]))) for _, off in batches) if batches else 0
+
+
+def _bound(w, batches, max_table_ids):
+    return table_bound(w, batches) if max_table_ids == "auto" else int(max_table_ids)
+
+
 def run_gpu(w, batches, host, first=0, last=None, flags=0, prepare_ahead=0, policy="lru",
-            hold_past=0, seed=0):
+            hold_past=0, seed=0, max_table_ids="auto"):
     """Train batches[first:last] on the GPU only (fresh context over `host`), then flush.
     prepare_ahead: how many batches after each window to hand over for early sorting."""
     import torch
@@ -46,7 +56,8 @@ def run_gpu(w, batches, host, first=0, last=None, flags=0, prepare_ahead=0, poli
     T, B, D, L = w.tables, w.batch, w.dim, w.lookahead
     max_ids = max(int(b[0].size) for b in batches)
     sp = ScratchPipe(w.rows, D, w.slots, L, host, max_batch=B, max_ids=max(max_ids, 1), flags=flags,
-                     policy=policy, hold_past=hold_past, seed=seed)
+                     policy=policy, hold_past=hold_past, seed=seed,
+                     max_table_ids=_bound(w, batches, max_table_ids))
     try:
         out = torch.zeros((T * B, D), dtype=torch.float32, device=dev)
         for u in range(first, last):
@@ -80,12 +91,14 @@ def make_inputs(w, steps=None, ragged=None):
 def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all", flags=0,
                device_ids=False, ref_tables=None, sync_each_step=True, compare_tables=True,
                return_tables=False, steps=None, prepare_ahead=0, policy="lru", hold_past=0,
-               seed=0):
+               seed=0, max_table_ids="auto"):
     """Train w on the GPU and with the oracle; assert parity; return a summary.
 
     prepare_ahead: also hand the GPU that many batches after the window
     (prepared in advance, not held); the oracle always sees the plain window.
-    policy, hold_past, seed: replacement policy and past window of both planners."""
+    policy, hold_past, seed: replacement policy and past window of both planners.
+    max_table_ids: the bound handed to the library ("auto": the batches' own maximum,
+    which sorts tables of up to 8192 IDs in LDS; 0: no bound, the general path)."""
     import torch
     dev = torch.device("cuda:0")
     if batches is None:
@@ -106,7 +119,8 @@ def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all"
     fwd_set = set(range(n)) if check_fwd_steps == "all" else set(check_fwd_steps)
     worst_fwd = 0.0
     sp = ScratchPipe(w.rows, D, w.slots, L, host, max_batch=B, max_ids=max(max_ids, 1), flags=flags,
-                     policy=policy, hold_past=hold_past, seed=seed)
+                     policy=policy, hold_past=hold_past, seed=seed,
+                     max_table_ids=_bound(w, batches, max_table_ids))
     try:
         out = torch.zeros((T * B, D), dtype=torch.float32, device=dev)
         for u in range(n):
@@ -174,7 +188,7 @@ def row_values(t, rows, dim):
 
 
 def run_sampled_parity(w, steps, *, check_plan_steps, check_fwd_steps, say=print, policy="lru",
-                       hold_past=0, seed=0):
+                       hold_past=0, seed=0, max_table_ids="auto"):
     """A full-size workload driven as the benchmark drives it (IDs in device memory, the two
     batches after the window handed over early) for `steps` steps.
 
@@ -217,7 +231,8 @@ def run_sampled_parity(w, steps, *, check_plan_steps, check_fwd_steps, say=print
     planner = oracle.Planner(w.rows, w.slots, policy, seed)
     max_ids = max(int(b[0].size) for b in batches)
     sp = ScratchPipe(w.rows, D, w.slots, L, host, max_batch=B, max_ids=max_ids, policy=policy,
-                     hold_past=hold_past, seed=seed)
+                     hold_past=hold_past, seed=seed,
+                     max_table_ids=_bound(w, batches, max_table_ids))
     worst_fwd = 0.0
     try:
         out = torch.zeros((T * B, D), dtype=torch.float32, device=dev)

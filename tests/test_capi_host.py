@@ -49,7 +49,7 @@ int main(void) {
   printf("sp_config %zu\\nsp_batch %zu\\nsp_stats %zu\\nsp_plan_dump %zu\\n",
          sizeof(sp_config), sizeof(sp_batch), sizeof(sp_stats), sizeof(sp_plan_dump));
   P(sp_config, max_ids); P(sp_config, flags); P(sp_config, device); P(sp_config, host_tables);
-  P(sp_config, policy); P(sp_config, hold_past); P(sp_config, seed);
+  P(sp_config, policy); P(sp_config, hold_past); P(sp_config, seed); P(sp_config, max_table_ids);
   P(sp_batch, nnz); P(sp_batch, on_device); P(sp_stats, ms_forward); P(sp_stats, timed_fill);
   P(sp_plan_dump, hit); P(sp_plan_dump, nnz);
   return 0; }
@@ -92,6 +92,7 @@ def _cfg(**over):
     (dict(hold_past=-1), "hold_past"),
     (dict(hold_past=5), "hold_past"),
     (dict(lookahead=12, hold_past=4), "hold_past"),
+    (dict(max_table_ids=-1), "max_table_ids"),
 ])
 def test_create_rejects_bad_configs(over, needle):
     cfg, keep = _cfg(**over)

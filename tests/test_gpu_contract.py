@@ -79,22 +79,31 @@ def _big_batch(w):
     return ids, off
 
 
-@pytest.mark.parametrize("lookahead", [0, 2])
-def test_rejected_plans_leave_state_unchanged(harness, lookahead):
+def _fat_table(w, n):
+    """Table 0: n IDs in its first bag, the other bags empty; table 1: one ID per bag."""
+    ids = np.concatenate([np.arange(n, dtype=np.int32) % w.rows[0], np.zeros(w.batch, np.int32)])
+    off = np.concatenate([[0], np.full(w.batch - 1, n), n + np.arange(1, w.batch + 1)])
+    return ids, off.astype(np.int32)
+
+
+@pytest.mark.parametrize("lookahead,bound", [(0, 0), (2, 0), (0, 512), (2, 512)])
+def test_rejected_plans_leave_state_unchanged(harness, lookahead, bound):
     """Rejected plans (row out of range, negative row, offsets not increasing,
-    more misses than unheld slots) change nothing: continuing afterwards
-    matches the oracle, which saw only the accepted plans.  New content enters
-    through the window's last batch, the one seen for the first time."""
+    more misses than unheld slots, and with a bound on IDs per table a table
+    above it) change nothing: continuing afterwards matches the oracle, which
+    saw only the accepted plans.  New content enters through the window's last
+    batch, the one seen for the first time.  bound 512 sorts each table in LDS."""
     import torch
     from oracle import oracle
     w = wl.custom(rows=[1500, 2500], dim=32, batch=24, pooling=[3, 2], slots=[300, 260],
                   lookahead=lookahead, steps=16, dist=("zipf", 1.0), seed=31)
-    _say(f"case transactional errors L={lookahead}")
+    _say(f"case transactional errors L={lookahead} bound={bound}")
     batches = harness.make_inputs(w)
     host = harness.fresh_host(w)
     ref = [wl.init_table(w, t) for t in range(w.tables)]
     planner = oracle.Planner(w.rows, w.slots)
-    ctx = spm.ScratchPipe(w.rows, w.dim, w.slots, w.lookahead, host, w.batch, 4096)
+    ctx = spm.ScratchPipe(w.rows, w.dim, w.slots, w.lookahead, host, w.batch, 4096,
+                          max_table_ids=bound)
     out = torch.zeros((w.tables * w.batch, w.dim), device="cuda:0")
     L = w.lookahead
     try:
@@ -106,7 +115,7 @@ def test_rejected_plans_leave_state_unchanged(harness, lookahead):
                     win[:-1] + [_bad_ids(tail, w, 1, w.rows[1])],          # row out of range
                     win[:-1] + [_bad_ids(tail, w, 0, -3)],                  # negative row
                     win[:-1] + [(tail[0], tail[1][::-1].copy())],          # offsets decreasing
-                ]
+                ] + ([win[:-1] + [_fat_table(w, bound + 1)]] if bound else [])  # over the bound
                 for bw in bad_windows:
                     with pytest.raises(spm.SPError) as e:
                         ctx.plan(bw)

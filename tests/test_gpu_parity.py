@@ -25,11 +25,13 @@ def _say(msg):
     print(msg, flush=True)
 
 
-def test_tiny_all_steps(harness):
-    """4 x 20k x 32, B=128, 4 IDs per bag, 2048 slots, lookahead 2, 50 steps."""
+@pytest.mark.parametrize("bound", ["auto", 0])
+def test_tiny_all_steps(harness, bound):
+    """4 x 20k x 32, B=128, 4 IDs per bag, 2048 slots, lookahead 2, 50 steps; tables
+    sorted in LDS (bound: the batches' own) and by the general multi-launch path (0)."""
     w = wl.get_workload("tiny")
-    _say(f"case tiny {w.describe()}")
-    r = harness.run_parity(w)
+    _say(f"case tiny {w.describe()} bound {bound}")
+    r = harness.run_parity(w, max_table_ids=bound)
     st = r["stats"]
     assert st["plans"] == 50 and st["misses"] > 0 and st["evictions"] > 0
     _say(f"tiny worst fwd {r['worst_fwd']:.2e} table {r['worst_table']:.2e} stats {st}")
@@ -100,6 +102,32 @@ def test_device_resident_ids_match_host_ids(harness):
     _say("case device ids")
     a = harness.run_parity(w, return_tables=True)
     b = harness.run_parity(w, device_ids=True, return_tables=True)
+    for x, y in zip(a["tables"], b["tables"]):
+        assert np.array_equal(x, y)
+
+
+@pytest.mark.parametrize("shape", ["ragged", "8192-ids", "8192-bags"])
+def test_ingest_in_lds_matches_general_path(harness, shape):
+    """Batches whose tables fit one workgroup are sorted and deduplicated in LDS, one
+    launch per batch; the general path uses several launches over the whole batch.  Both
+    must give the oracle's plans, and bit-identical tables.  Edge cases: ragged and empty
+    bags, tables at the 8192-ID limit with hot runs split into chunks, 8192 bags."""
+    if shape == "ragged":
+        w = wl.custom(rows=[900, 1400, 700], dim=16, batch=64, pooling=3, slots=[600, 800, 500],
+                      lookahead=2, steps=14, seed=17)
+        batches = [wl.ragged_batch(w, s, 7, empty_frac=0.25) for s in range(w.steps)]
+    elif shape == "8192-ids":
+        w = wl.custom(rows=[200_000] * 2, dim=16, batch=1024, pooling=8, slots=[20_000] * 2,
+                      lookahead=1, steps=6, dist=("zipf", 1.1), seed=18)
+        batches = harness.make_inputs(w)
+    else:
+        w = wl.custom(rows=[100_000] * 2, dim=8, batch=8192, pooling=1, slots=[20_000] * 2,
+                      lookahead=1, steps=6, dist=("zipf", 1.05), seed=19)
+        batches = harness.make_inputs(w)
+    _say(f"case ingest paths {shape} bound {harness.table_bound(w, batches)}")
+    assert harness.table_bound(w, batches) <= 8192
+    a = harness.run_parity(w, batches, return_tables=True)
+    b = harness.run_parity(w, batches, return_tables=True, max_table_ids=0)
     for x, y in zip(a["tables"], b["tables"]):
         assert np.array_equal(x, y)
 

@@ -228,6 +228,10 @@ class ScatterPool {
 
 }  // namespace
 
+// staging slots of evicted rows (fill of plan p, copy of plan p - 1 and the
+// host scatter of plan p - 2 can all be in flight)
+constexpr int NSTAGE = 3;
+
 struct sp_ctx {
     // configuration
     int T = 0, D = 0, L = 0, device = 0;
@@ -297,13 +301,17 @@ struct sp_ctx {
 
     // write-back staging (two in flight)
     int64_t stage_rows = 0;
-    float *stage_dev[2]{}, *stage_host[2]{};  // n rows, then their n previous keys
-    hipEvent_t ev_d2h[2]{};
+    // staging of evicted rows, plan p in slot p % NSTAGE: n rows, then their n
+    // previous keys.  Plan p's copy to the host is issued by plan p + 1 (or by
+    // flush), when its fill has nearly always finished: copy_pending = p
+    float *stage_dev[NSTAGE]{}, *stage_host[NSTAGE]{};
+    hipEvent_t ev_d2h[NSTAGE]{};
+    int64_t copy_pending = -1, copy_n = 0;
 
     // plan stream: query, hold, victims, commit; ingest stream: sorting and
     // deduplicating batches as they become visible; move stream: write-back
     // staging, miss fills and the device-to-host copy of evicted rows
-    hipStream_t s_plan = nullptr, s_ingest = nullptr, s_move = nullptr;
+    hipStream_t s_plan = nullptr, s_ingest = nullptr, s_move = nullptr, s_copy = nullptr;
 
     // write-back thread
     std::thread worker;
@@ -463,7 +471,7 @@ static void release(sp_ctx *h)
         for (auto &e : *v)
             if (e) hipEventDestroy(e);
     if (h->ev_consumed) hipEventDestroy(h->ev_consumed);
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < NSTAGE; ++i)
         if (h->ev_d2h[i]) hipEventDestroy(h->ev_d2h[i]);
     h->t_fwd.destroy();
     h->t_bwd.destroy();
@@ -475,6 +483,7 @@ static void release(sp_ctx *h)
     if (h->s_plan) hipStreamDestroy(h->s_plan);
     if (h->s_ingest) hipStreamDestroy(h->s_ingest);
     if (h->s_move) hipStreamDestroy(h->s_move);
+    if (h->s_copy) hipStreamDestroy(h->s_copy);
     for (void *p : h->dev_allocs) hipFree(p);
     for (void *p : h->pinned_allocs) hipHostFree(p);
     delete h;
@@ -611,7 +620,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     TRY(dalloc(h, &h->sel_hist, (int64_t)MAX_TABLES * SEL_BINS));
     TRY(dalloc(h, &h->partial, nchunk_max * h->D));
     h->stage_rows = std::min<int64_t>(N, S);
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < NSTAGE; ++i) {
         TRY(dalloc(h, &h->stage_dev[i], h->stage_rows * (h->D + 1)));
         TRY(palloc(h, &h->stage_host[i], h->stage_rows * (h->D + 1)));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_d2h[i], hipEventDisableTiming));
@@ -635,6 +644,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_plan, hipStreamNonBlocking));
     HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_ingest, hipStreamNonBlocking));
     HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_move, hipStreamNonBlocking));
+    HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_copy, hipStreamNonBlocking));
     HIPCHK(nullptr, h->t_fwd.init());
     HIPCHK(nullptr, h->t_bwd.init());
     HIPCHK(nullptr, h->t_cmb.init());
@@ -802,6 +812,37 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
     h->ring_batch[r] = q;
     h->ring_nnz[r] = bt.nnz;
     h->ring_B[r] = bt.batch;
+    return SP_OK;
+}
+
+// Issue the pending write-back copy (plan p = copy_pending) on the copy
+// stream and hand its rows to the write-back thread.  The host staging slot
+// was last used by plan p - NSTAGE, whose scatter is joined first.
+static sp_status issue_copy(sp_ctx *h)
+{
+    const int64_t p = h->copy_pending;
+    if (p < 0) return SP_OK;
+    const int sl = (int)(p % NSTAGE);
+    if (p >= NSTAGE) TRY(join_jobs(h, p - NSTAGE));
+    Job job;
+    job.ticket = p;
+    const int64_t n = h->copy_n;
+    if (n > 0) {
+        HIPCHK(h, wait_unless_done(h->s_copy, h->ev_filled[p % h->nring]));
+        HIPCHK(h, hipMemcpyAsync(h->stage_host[sl], h->stage_dev[sl],
+                                 sizeof(float) * n * (h->D + 1), hipMemcpyDeviceToHost, h->s_copy));
+        HIPCHK(h, hipEventRecord(h->ev_d2h[sl], h->s_copy));
+        job.ev = h->ev_d2h[sl];
+        job.rows = h->stage_host[sl];
+        job.keys = (const int32_t *)(h->stage_host[sl] + n * h->D);
+        job.n = n;
+    }
+    {
+        std::lock_guard<std::mutex> lk(h->mu);
+        h->jobs.push_back(job);
+    }
+    h->cv.notify_one();
+    h->copy_pending = -1;
     return SP_OK;
 }
 
@@ -1071,13 +1112,14 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     for (const auto &d : h->deadlines)
         if (d.second <= k) need = std::max(need, d.first);
     if (need >= 0) {
+        if (h->copy_pending >= 0 && h->copy_pending <= need) TRY(issue_copy(h));
         TRY(join_jobs(h, need));
         while (!h->deadlines.empty() && h->deadlines.front().first <= need) h->deadlines.pop_front();
     }
-    const int sl = (int)(k & 1);
-    // host staging of plan k-2 is free again once its rows are scattered; the
-    // device staging is, by stream order (its copy ran on this stream)
-    if (k >= 2) TRY(join_jobs(h, k - 2));
+    const int sl = (int)(k % NSTAGE);
+    // the device staging slot is free once plan k - NSTAGE's copy has run
+    // (issued two plans ago)
+    if (k >= NSTAGE) HIPCHK(h, wait_unless_done(h->s_move, h->ev_d2h[sl]));
     HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_planned[e], 0));
     if (timing) HIPCHK(h, h->t_fill.begin(h->s_move));
     if (n_miss > 0) {
@@ -1085,10 +1127,14 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
         // has run.  Update j freed ring entry j % nring for batch j + nring,
         // whose ingest waited for it; this plan's query is behind every batch
         // up to k+L, so updates up to k+L-nring are behind this stream
-        // already.  The rest are waited for, one wait when they share a stream.
-        for (int64_t j = std::max<int64_t>(0, k + h->L + 1 - h->nring); j < k; ++j) {
+        // already.  Batches k-P .. k-1 of the past window cannot have used a
+        // victim's row (their rows are held), and the fill writes only victim
+        // slots, so their updates need no wait.  The rest are waited for, one
+        // wait when they share a stream.
+        const int64_t last = k - 1 - h->P;
+        for (int64_t j = std::max<int64_t>(0, k + h->L + 1 - h->nring); j <= last; ++j) {
             const int ej = (int)(j % h->nring);
-            if (j == k - 1 || h->upd_stream[ej] != h->upd_stream[(k - 1) % h->nring])
+            if (j == last || h->upd_stream[ej] != h->upd_stream[last % h->nring])
                 HIPCHK(h, wait_unless_done(h->s_move, h->ev_upd[ej]));
         }
         launch_move(h->storage, h->D, h->tb, h->host_dev, tk, n_miss, u, h->stage_dev[sl],
@@ -1097,23 +1143,11 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     }
     HIPCHK(h, hipEventRecord(h->ev_filled[e], h->s_move));
     if (timing) HIPCHK(h, h->t_fill.end(h->s_move));
-    Job job;
-    job.ticket = k;
-    if (n_miss > 0) {
-        HIPCHK(h, hipMemcpyAsync(h->stage_host[sl], h->stage_dev[sl],
-                                 sizeof(float) * n_miss * (h->D + 1), hipMemcpyDeviceToHost,
-                                 h->s_move));
-        HIPCHK(h, hipEventRecord(h->ev_d2h[sl], h->s_move));
-        job.ev = h->ev_d2h[sl];
-        job.rows = h->stage_host[sl];
-        job.keys = (const int32_t *)(h->stage_host[sl] + n_miss * h->D);
-        job.n = n_miss;
-    }
-    {
-        std::lock_guard<std::mutex> lk(h->mu);
-        h->jobs.push_back(job);
-    }
-    h->cv.notify_one();
+    // the previous plan's write-back copy, on its own stream, so that it
+    // overlaps this fill (they use the host link in opposite directions)
+    TRY(issue_copy(h));
+    h->copy_pending = k;
+    h->copy_n = n_miss;
     h->deadlines.emplace_back(k, k + nhold);
 
     h->host_ms[4] += host_ms() - tF;
@@ -1191,6 +1225,7 @@ extern "C" sp_status sp_backward_update(sp_handle h, int64_t ticket, const float
 extern "C" sp_status sp_flush(sp_handle h)
 {
     TRY(usable(h));
+    TRY(issue_copy(h));
     HIPCHK(h, hipDeviceSynchronize());
     TRY(join_jobs(h, h->planned - 1));
     h->deadlines.clear();

@@ -75,7 +75,8 @@ __global__ void __launch_bounds__(BLOCK) k_forward(const float4 *__restrict__ st
                                                    int64_t nbags, int64_t nslots,
                                                    float4 *__restrict__ out)
 {
-    const int64_t g = (int64_t)blockIdx.x * (BLOCK / WAVE) + wave_id();
+    // consecutive bags (one table's) on one XCD: the table's hot rows share its L2
+    const int64_t g = xcd_block(blockIdx.x, gridDim.x) * (BLOCK / WAVE) + wave_id();
     if (g >= nbags) return;
     float4 acc = gather_sum<LPR, 4>(storage, nslots, slot_of, bag_off[g], bag_off[g + 1]);
     acc = reduce_rows<LPR>(acc);
@@ -113,7 +114,9 @@ __global__ void __launch_bounds__(BLOCK) k_backward(float4 *__restrict__ storage
                                                     int64_t nbags, int64_t nslots, float lr,
                                                     float4 *__restrict__ partial)
 {
-    const int64_t t = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    // consecutive chunks (one table's) on one XCD: the table's bag gradients
+    // share its L2
+    const int64_t t = xcd_block(blockIdx.x, gridDim.x) * BLOCK + threadIdx.x;
     const int64_t ch = t / LPR;
     const int c = (int)(t % LPR);
     if (ch >= n_chunks) return;  // whole lane groups leave together

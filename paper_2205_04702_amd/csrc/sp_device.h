@@ -14,6 +14,18 @@ __device__ __forceinline__ int lane_id() { return threadIdx.x & (WAVE - 1); }
 __device__ __forceinline__ int wave_id() { return threadIdx.x / WAVE; }
 __device__ __forceinline__ uint64_t lanemask_lt() { return (1ull << lane_id()) - 1ull; }
 
+// The hardware hands the blocks of a launch to the 8 XCDs in turn (block b to
+// XCD b % 8), and each XCD has its own L2.  This maps block b to a logical
+// block so that XCD x works through the x-th eighth of the logical blocks: work
+// that is contiguous in logical order (one table's bags, chunks or rows) then
+// shares one L2.  A bijection on [0, n).
+constexpr int XCDS = 8;
+__device__ __forceinline__ int64_t xcd_block(int64_t b, int64_t n)
+{
+    const int64_t x = b % XCDS, i = b / XCDS, q = n / XCDS, rem = n % XCDS;
+    return x * q + (x < rem ? x : rem) + i;
+}
+
 template <typename T>
 __device__ __forceinline__ T wave_incl_scan(T v)
 {

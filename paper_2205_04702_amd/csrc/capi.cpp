@@ -608,7 +608,9 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     {
         // scans: victims (tables x slots per table), misses and batches (N),
         // radix histogram tables (at most N + 2048 entries)
-        const int64_t tiles = std::max(scan_tiles(T, h->maxS), scan_tiles(1, N + 4096)) + 2;
+        // (and the query's tiles of unique keys)
+        const int64_t tiles = std::max({scan_tiles(T, h->maxS), scan_tiles(1, N + 4096),
+                                        (N + QUERY_TILE - 1) / QUERY_TILE}) + 2;
         for (ScanWs *ws : {&h->ws_plan, &h->ws_ingest}) {
             ws->max_tiles = tiles;
             TRY(dalloc(h, &ws->status, LB_WORDS * tiles));
@@ -942,8 +944,9 @@ static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, int32_t *stamp_o
     *seq_out = ++h->qseq;
     launch_query(h->tb, h->hash, h->hash_mask, ukeys, nuniq, nwin, max_nnz, h->held, stamp,
                  h->tk[e], h->cnt, h->cnt_part, h->cnt_part + PART_COPIES * 2 * MAX_TABLES,
-                 h->ring[k % h->nring].scal, h->h_cnt_dev, *seq_out, h->s_plan);
+                 h->ring[k % h->nring].scal, h->h_cnt_dev, *seq_out, h->ws_plan, h->s_plan);
     CHECK_LAUNCH(h);
+    if (h->ws_plan.overflow) return fail(h, SP_ERR_HIP, "internal: scan workspace too small");
     if (timing) HIPCHK(h, h->t_qry.end(h->s_plan));
     *stamp_out = stamp;
     return SP_OK;
@@ -1059,7 +1062,6 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
             ++h->st.hash_rebuilds;
         }
         h->hash_used += n_miss;
-        launch_miss_compact(b0.ukeys, th.n_unique, tk, h->ws_plan, h->s_plan);
         SelArgs a{};
         int32_t vb = 0;
         int64_t maxS = 0;

@@ -10,6 +10,8 @@ namespace sp {
 
 // ---------------------------------------------------------------- query + hold
 
+static_assert(QUERY_TILE == BLOCK, "one unique key per query thread");
+
 struct ProbeArgs {
     const uint32_t *uk[MAX_WINDOW];
     const int32_t *nu[MAX_WINDOW];
@@ -18,7 +20,10 @@ struct ProbeArgs {
 // The query of one plan, one launch.  blockIdx.y = window batch.  Every
 // cached key of a window batch stamps its slot as held for this plan
 // (held[slot] = stamp) and counts it once per table; batch 0 (the planned
-// one) also records hit / slot and counts misses.  Per-table counts are summed
+// one) also records hit / slot, counts misses and compacts them in ascending
+// key order into m_key / m_uidx with a single-pass scan (its blocks take
+// their tiles of keys from an atomic counter, so a tile only looks back at
+// tiles whose blocks have started).  Per-table counts are summed
 // across the wave (keys are sorted, so a wave nearly always covers one table),
 // then across the block in LDS, then added to one of PART_COPIES copies of the
 // counters so that few blocks contend for an address.
@@ -38,14 +43,23 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
                                                  int32_t *hit, int32_t *slot_u, DevCounters *cnt,
                                                  int32_t *part, int32_t *arrived,
                                                  const int32_t *scal0, uint64_t *host_mapped,
-                                                 uint32_t seq)
+                                                 uint32_t seq, uint32_t *m_key, int32_t *m_uidx,
+                                                 ScanDev d)
 {
     __shared__ int32_t c_miss[MAX_TABLES], c_held[MAX_TABLES];
     __shared__ int32_t last_s;
-    for (int t = threadIdx.x; t < T; t += BLOCK) c_miss[t] = c_held[t] = 0;
-    __syncthreads();
+    __shared__ uint32_t tile_s, pref_s;
+    __shared__ uint32_t lds_scan[BLOCK / WAVE];
     const int w = blockIdx.y;
-    const int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    for (int t = threadIdx.x; t < T; t += BLOCK) c_miss[t] = c_held[t] = 0;
+    if (w == 0 && threadIdx.x == 0) tile_s = atomicAdd(d.counter, 1u) - d.base;
+    __syncthreads();
+    const int64_t xb = w == 0 ? (int64_t)tile_s : (int64_t)blockIdx.x;
+    if (xb >= (int64_t)gridDim.x) {  // the counter and the host disagree: give up loudly
+        if (threadIdx.x == 0) atomicOr(d.err, ERR_PLAN);
+        return;
+    }
+    const int64_t i = xb * BLOCK + threadIdx.x;
     int32_t seen = 0;  // returned old values; tested below so the adds complete first
     if (w == 0 && i == 0) {
         seen |= atomicExch(&cnt->n_unique, scal0[0]) == INT32_MIN;
@@ -56,8 +70,9 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
     const bool valid = i < *pa.nu[w];
     int t = 0;
     bool miss = false, fresh = false;
+    uint32_t key = 0;
     if (valid) {
-        const uint32_t key = pa.uk[w][i];
+        key = pa.uk[w][i];
         t = (int)(key >> row_bits);
         const int32_t slot = hash_find_ro(hash, mask, key);  // the map is not written here
         if (w == 0) {
@@ -66,6 +81,19 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
             miss = slot < 0;
         }
         if (slot >= 0) fresh = atomicExch(&held[slot], stamp) != stamp;
+    }
+    if (w == 0 && xb * BLOCK < (int64_t)*pa.nu[0]) {  // uniform per block
+        uint32_t tot;
+        const uint32_t ex = block_excl_scan((uint32_t)miss, lds_scan, tot);
+        if (threadIdx.x < WAVE) {
+            const uint32_t pre = lb_lookback<uint32_t>(d, (uint32_t)xb, (int)xb, tot);
+            if (threadIdx.x == 0) pref_s = pre;
+        }
+        __syncthreads();
+        if (miss) {
+            m_key[pref_s + ex] = key;
+            m_uidx[pref_s + ex] = (int32_t)i;
+        }
     }
     uint64_t todo = __ballot(valid);
     while (todo) {
@@ -130,15 +158,26 @@ void launch_query(const Tables &tb, const uint64_t *hash, uint32_t mask,
                   const uint32_t *const *ukeys, const int32_t *const *nuniq, int nwin,
                   int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk,
                   DevCounters *cnt, int32_t *part, int32_t *arrived, const int32_t *scal0,
-                  uint64_t *host_mapped, uint32_t seq, hipStream_t s)
+                  uint64_t *host_mapped, uint32_t seq, ScanWs &ws, hipStream_t s)
 {
     ProbeArgs pa{};
     for (int w = 0; w < nwin; ++w) pa.uk[w] = ukeys[w], pa.nu[w] = nuniq[w];
     // at least one block per batch so that every batch's error word is read
     const int64_t n = max_unique > 0 ? max_unique : 1;
-    hipLaunchKernelGGL(k_query, dim3((unsigned)((n + BLOCK - 1) / BLOCK), nwin), dim3(BLOCK), 0, s,
-                       tb.row_bits, tb.T, hash, mask, pa, held, stamp, tk.hit, tk.slot_u, cnt,
-                       part, arrived, scal0, host_mapped, seq);
+    const int64_t gx = (n + BLOCK - 1) / BLOCK;
+    if (gx > ws.max_tiles) {
+        ws.overflow = true;
+        return;
+    }
+    if (ws.epoch == 0xFFFFFFFFu) {  // epochs wrapped: forget every published word
+        (void)hipMemsetAsync(ws.status, 0, sizeof(uint64_t) * LB_WORDS * ws.max_tiles, s);
+        ws.epoch = 0;
+    }
+    ScanDev d{ws.status, ws.counter, ws.err, ws.issued, ++ws.epoch, (uint32_t)gx, (int32_t)gx};
+    ws.issued += (uint32_t)gx;  // the planned batch's row of blocks takes tiles
+    hipLaunchKernelGGL(k_query, dim3((unsigned)gx, nwin), dim3(BLOCK), 0, s, tb.row_bits, tb.T,
+                       hash, mask, pa, held, stamp, tk.hit, tk.slot_u, cnt, part, arrived, scal0,
+                       host_mapped, seq, tk.m_key, tk.m_uidx, d);
 }
 
 // ---------------------------------------------------------------- hash rebuild
@@ -167,34 +206,6 @@ void launch_hash_rebuild(uint64_t *hash, uint32_t mask, const int32_t *key_of_sl
     if (nslots > 0)
         hipLaunchKernelGGL(k_hash_reinsert, dim3((unsigned)((nslots + BLOCK - 1) / BLOCK)),
                            dim3(BLOCK), 0, s, hash, mask, key_of_slot, nslots, &cnt->err_sticky);
-}
-
-// ---------------------------------------------------------------- misses
-
-struct MissFlag {
-    const int32_t *hit;
-    __device__ uint32_t operator()(int64_t i, int) const { return hit[i] == 0; }
-};
-struct MissOut {
-    const uint32_t *ukeys;
-    uint32_t *m_key;
-    int32_t *m_uidx;
-    __device__ void operator()(int64_t i, uint32_t e, uint32_t v, int) const
-    {
-        if (v) {
-            m_key[e] = ukeys[i];
-            m_uidx[e] = (int32_t)i;
-        }
-    }
-};
-
-// Misses in ascending key order (the unique keys are sorted), so table t's
-// misses start at the sum of the miss counts of tables < t.
-void launch_miss_compact(const uint32_t *ukeys, int64_t n_unique, TicketDev tk, ScanWs &ws,
-                         hipStream_t s)
-{
-    seg_scan<uint32_t>(SegN{n_unique}, 1, n_unique, MissFlag{tk.hit},
-                       MissOut{ukeys, tk.m_key, tk.m_uidx}, ws, s);
 }
 
 // ---------------------------------------------------------------- victims

@@ -160,6 +160,49 @@ __device__ __forceinline__ bool lb_read(const uint64_t *w, uint32_t epoch, T &v)
     return ok;
 }
 
+// The look-back of tile `id`, the x-th tile of its segment, whose own sum is
+// `total`: publishes the sum, adds the sums published by earlier tiles of the
+// segment until it meets an inclusive prefix, then publishes its own inclusive
+// prefix.  Returns the exclusive prefix.  Called by the 64 lanes of one wave.
+template <typename T>
+__device__ T lb_lookback(const ScanDev &d, uint32_t id, int x, T total)
+{
+    const int lane = lane_id();
+    uint64_t *st = d.status + (int64_t)id * LB_WORDS;
+    T prefix = 0;
+    if (x == 0) {
+        if (lane == 0) lb_publish(st + 2, d.epoch, total);
+        return prefix;
+    }
+    if (lane == 0) lb_publish(st, d.epoch, total);
+    const int64_t first = (int64_t)id - x;  // the segment's first tile
+    int64_t t = (int64_t)id - 1 - lane;
+    int spins = 0;
+    while (true) {
+        T pv = 0;
+        int state = 2;  // lanes before the segment act as a zero inclusive prefix
+        if (t >= first) {
+            const uint64_t *w = d.status + t * LB_WORDS;
+            state = lb_read(w + 2, d.epoch, pv) ? 2 : (lb_read(w, d.epoch, pv) ? 1 : 0);
+        }
+        const uint64_t incl = __ballot(state == 2);
+        const int stop = incl ? __ffsll((unsigned long long)incl) - 1 : WAVE;
+        const uint64_t need = stop >= WAVE - 1 ? ~0ull : ((2ull << stop) - 1ull);
+        if (__ballot(state == 0) & need) {
+            if (++spins <= LB_SPIN) {
+                __builtin_amdgcn_s_sleep(1);
+                continue;
+            }
+            if (lane == 0) atomicOr(d.err, ERR_PLAN);  // counted as zero; result flagged wrong
+        }
+        prefix += wave_sum(lane <= stop && state != 0 ? pv : T(0));
+        if (stop < WAVE) break;
+        t -= WAVE;
+    }
+    if (lane == 0) lb_publish(st + 2, d.epoch, prefix + total);
+    return prefix;
+}
+
 template <class Seg, class Val, class Out, typename T>
 __global__ void __launch_bounds__(BLOCK) k_scan_lookback(Seg seg, Val val, Out out, ScanDev d)
 {
@@ -187,41 +230,9 @@ __global__ void __launch_bounds__(BLOCK) k_scan_lookback(Seg seg, Val val, Out o
     }
     T total;
     const T excl = block_excl_scan(sum, lds, total);
-    uint64_t *st = d.status + (int64_t)id * LB_WORDS;
     if (threadIdx.x < WAVE) {
-        const int lane = threadIdx.x;
-        T prefix = 0;
-        if (x == 0) {
-            if (lane == 0) lb_publish(st + 2, d.epoch, total);
-        } else {
-            if (lane == 0) lb_publish(st, d.epoch, total);
-            const int64_t first = (int64_t)id - x;  // the segment's first tile
-            int64_t t = (int64_t)id - 1 - lane;
-            int spins = 0;
-            while (true) {
-                T pv = 0;
-                int state = 2;  // lanes before the segment act as a zero inclusive prefix
-                if (t >= first) {
-                    const uint64_t *w = d.status + t * LB_WORDS;
-                    state = lb_read(w + 2, d.epoch, pv) ? 2 : (lb_read(w, d.epoch, pv) ? 1 : 0);
-                }
-                const uint64_t incl = __ballot(state == 2);
-                const int stop = incl ? __ffsll((unsigned long long)incl) - 1 : WAVE;
-                const uint64_t need = stop >= WAVE - 1 ? ~0ull : ((2ull << stop) - 1ull);
-                if (__ballot(state == 0) & need) {
-                    if (++spins <= LB_SPIN) {
-                        __builtin_amdgcn_s_sleep(1);
-                        continue;
-                    }
-                    if (lane == 0) atomicOr(d.err, ERR_PLAN);  // counted as zero; result flagged wrong
-                }
-                prefix += wave_sum(lane <= stop && state != 0 ? pv : T(0));
-                if (stop < WAVE) break;
-                t -= WAVE;
-            }
-            if (lane == 0) lb_publish(st + 2, d.epoch, prefix + total);
-        }
-        if (lane == 0) prefix_s = prefix;
+        const T prefix = lb_lookback(d, id, x, total);
+        if (threadIdx.x == 0) prefix_s = prefix;
     }
     __syncthreads();
     T run = prefix_s + excl;

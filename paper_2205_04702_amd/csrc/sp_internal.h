@@ -8,6 +8,7 @@ namespace sp {
 
 constexpr int MAX_TABLES = 64;
 constexpr int MAX_WINDOW = 16;   // batches one plan may look at (lookahead <= 15)
+constexpr int QUERY_TILE = 256;  // unique keys per block of the query (one per thread)
 constexpr int SEL_BITS = 11;     // digit width of the LRU radix select
 constexpr int SEL_BINS = 1 << SEL_BITS;
 
@@ -179,18 +180,17 @@ struct RadixPlan {
 RadixPlan radix_plan(int64_t n, int bits);
 
 // k_plan.hip
-// The query: hold marks, hits and per-table counts of one plan, published to
-// host_mapped (word i = seq << 32 | counter word i) by the last block.
+// The query: hold marks, hits, the misses in ascending key order (tk.m_key,
+// tk.m_uidx) and per-table counts of one plan, published to host_mapped
+// (word i = seq << 32 | counter word i) by the last block.
 void launch_query(const Tables &tb, const uint64_t *hash, uint32_t mask,
                   const uint32_t *const *ukeys, const int32_t *const *nuniq, int nwin,
                   int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk,
                   DevCounters *cnt, int32_t *part, int32_t *arrived, const int32_t *scal0,
-                  uint64_t *host_mapped, uint32_t seq, hipStream_t s);
+                  uint64_t *host_mapped, uint32_t seq, ScanWs &ws, hipStream_t s);
 
 void launch_hash_rebuild(uint64_t *hash, uint32_t mask, const int32_t *key_of_slot, int64_t nslots,
                          DevCounters *cnt, hipStream_t s);
-void launch_miss_compact(const uint32_t *ukeys, int64_t n_unique, TicketDev tk, ScanWs &ws,
-                         hipStream_t s);
 void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int32_t *held, int32_t *sel_state, int32_t *sel_hist,
                            uint32_t *vk0, uint32_t *vv0, uint32_t *vk1, uint32_t *vv1,
                            int64_t n_victims, uint32_t *hist, ScanWs &ws, int32_t *v_slot,

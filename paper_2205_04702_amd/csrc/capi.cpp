@@ -228,6 +228,9 @@ class ScatterPool {
 
 }  // namespace
 
+// words of sp_ctx::sem, one cache line apart
+constexpr int SEM_PLANNED = 0, SEM_FILLED = 8, SEM_WORDS = 16;
+
 // staging slots of evicted rows (fill of plan p, copy of plan p - 1 and the
 // host scatter of plan p - 2 can all be in flight)
 constexpr int NSTAGE = 3;
@@ -266,7 +269,13 @@ struct sp_ctx {
     // so ev_upd[r] (backward of the entry's ticket issued) also frees ring[r]
     std::vector<TicketDev> tk;
     std::vector<TicketHost> tkh;
-    std::vector<hipEvent_t> ev_planned, ev_filled, ev_upd;
+    std::vector<hipEvent_t> ev_filled, ev_upd;
+    // stream-ordered counters in device memory for the two waits that are
+    // nearly always still pending when they are enqueued (a value wait costs
+    // the host a fraction of a wait on an unfinished event): sem[SEM_PLANNED]
+    // reaches k + 1 when plan k's commit has run, sem[SEM_FILLED] when its
+    // fill has
+    uint64_t *sem = nullptr;
     std::vector<hipStream_t> upd_stream;    // stream each ticket's backward ran on
     int64_t planned = 0, forwarded = 0, updated = 0;
     int32_t stamp = 0;
@@ -467,7 +476,7 @@ static void release(sp_ctx *h)
     }
     h->scatter.stop();
     (void)hipDeviceSynchronize();
-    for (auto *v : {&h->ring_ready, &h->ev_planned, &h->ev_filled, &h->ev_upd})
+    for (auto *v : {&h->ring_ready, &h->ev_filled, &h->ev_upd})
         for (auto &e : *v)
             if (e) hipEventDestroy(e);
     if (h->ev_consumed) hipEventDestroy(h->ev_consumed);
@@ -559,7 +568,6 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     h->ring_seen.assign(h->nring, 0);
     h->tk.assign(h->nring, TicketDev{});
     h->tkh.assign(h->nring, TicketHost{});
-    h->ev_planned.assign(h->nring, nullptr);
     h->ev_filled.assign(h->nring, nullptr);
     h->ev_upd.assign(h->nring, nullptr);
     h->upd_stream.assign(h->nring, nullptr);
@@ -590,7 +598,6 @@ static sp_status build(sp_ctx *h, const sp_config *c)
         TRY(dalloc(h, &t.v_slot, N));
         TRY(dalloc(h, &t.v_old_key, N));
         TRY(dalloc(h, &t.v_old_lu, N));
-        HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_planned[k], hipEventDisableTiming));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_filled[k], hipEventDisableTiming));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_upd[k], hipEventDisableTiming));
     }
@@ -642,6 +649,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     }
 
     TRY(dalloc(h, &h->cons_counter, 1));
+    TRY(dalloc(h, &h->sem, SEM_WORDS));
     HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_consumed, hipEventDisableTiming));
     HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_plan, hipStreamNonBlocking));
     HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_ingest, hipStreamNonBlocking));
@@ -657,6 +665,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
 
     // initial state: nothing cached
     HIPCHK(nullptr, hipMemsetAsync(h->cons_counter, 0, sizeof(uint32_t), h->s_plan));
+    HIPCHK(nullptr, hipMemsetAsync(h->sem, 0, sizeof(uint64_t) * SEM_WORDS, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->key_of_slot, 0xFF, sizeof(int32_t) * S, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->last_use, 0xFF, sizeof(int32_t) * S, h->s_plan));
     if (h->uses) HIPCHK(nullptr, hipMemsetAsync(h->uses, 0, sizeof(int32_t) * S, h->s_plan));
@@ -1093,7 +1102,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
                   h->last_use, h->uses, u, h->cnt, h->s_plan);
     CHECK_LAUNCH(h);
     if (h->ws_plan.overflow) return fail(h, SP_ERR_HIP, "internal: scan workspace too small");
-    HIPCHK(h, hipEventRecord(h->ev_planned[e], h->s_plan));
+    HIPCHK(h, hipStreamWriteValue64(h->s_plan, h->sem + SEM_PLANNED, (uint64_t)k + 1, 0));
     if (timing) HIPCHK(h, h->t_plan.end(h->s_plan));
     double tF = host_ms();
     h->host_ms[3] += tF - tE;
@@ -1122,7 +1131,8 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     // the device staging slot is free once plan k - NSTAGE's copy has run
     // (issued two plans ago)
     if (k >= NSTAGE) HIPCHK(h, wait_unless_done(h->s_move, h->ev_d2h[sl]));
-    HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_planned[e], 0));
+    HIPCHK(h, hipStreamWaitValue64(h->s_move, h->sem + SEM_PLANNED, (uint64_t)k + 1,
+                                   hipStreamWaitValueGte, ~0ull));
     if (timing) HIPCHK(h, h->t_fill.begin(h->s_move));
     if (n_miss > 0) {
         // RAW-2/3: a victim's row is final once the last update that used it
@@ -1144,6 +1154,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
         CHECK_LAUNCH(h);
     }
     HIPCHK(h, hipEventRecord(h->ev_filled[e], h->s_move));
+    HIPCHK(h, hipStreamWriteValue64(h->s_move, h->sem + SEM_FILLED, (uint64_t)k + 1, 0));
     if (timing) HIPCHK(h, h->t_fill.end(h->s_move));
     // the previous plan's write-back copy, on its own stream, so that it
     // overlaps this fill (they use the host link in opposite directions)
@@ -1179,7 +1190,8 @@ extern "C" sp_status sp_forward(sp_handle h, int64_t ticket, float *d_out, void 
     const int64_t nbags = (int64_t)h->T * th.B;
     if (nbags > 0 && !d_out) return fail(h, SP_ERR_INVALID_ARG, "null d_out");
     hipStream_t s = (hipStream_t)stream;
-    HIPCHK(h, hipStreamWaitEvent(s, h->ev_filled[e], 0));
+    HIPCHK(h, hipStreamWaitValue64(s, h->sem + SEM_FILLED, (uint64_t)ticket + 1,
+                                   hipStreamWaitValueGte, ~0ull));
     // RAW-1: the previous update must land first (implicit on the same stream)
     if (ticket >= 1 && s != h->last_update_stream)
         HIPCHK(h, wait_unless_done(s, h->ev_upd[(ticket - 1) % h->nring]));

@@ -108,6 +108,9 @@ def main():
     ap.add_argument("--no-timing", action="store_true", help="do not time kernels with events")
     ap.add_argument("--time-every", type=int, default=8, metavar="K",
                     help="time the kernels of every K-th step with events (the rest run untimed)")
+    ap.add_argument("--event-waits", action="store_true",
+                    help="wait on events instead of stream values (for profilers that run one "
+                         "dispatch at a time, such as counter collection)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="after the timed region, run a plain elementwise copy (torch.neg) of MIB "
                          "MiB three times: the reference kernel for scaling HBM byte counters")
@@ -149,7 +152,7 @@ def main():
     timed = not args.no_timing
     every = max(1, args.time_every)
     ctx = sp.ScratchPipe(w.rows, w.dim, w.slots, L, host, max_batch=w.batch, max_ids=w.nnz,
-                         flags=0, policy=args.policy, hold_past=args.hold_past,
+                         flags=sp.SP_FLAG_EVENT_WAITS if args.event_waits else 0, policy=args.policy, hold_past=args.hold_past,
                          max_table_ids=w.batch * max(w.pooling))
     out = torch.empty((w.tables * w.batch, w.dim), dtype=torch.float32, device=dev)
 
@@ -159,8 +162,11 @@ def main():
     def step(u):
         # hold window u..u+L, plus the next batches handed over early for sorting;
         # kernel events on a sample of the steps only (they cost host time)
+        base = sp.SP_FLAG_EVENT_WAITS if args.event_waits else 0
         if timed:
-            ctx.set_flags(sp.SP_FLAG_TIMING if u % every == 0 else 0)
+            ctx.set_flags(base | (sp.SP_FLAG_TIMING if u % every == 0 else 0))
+        elif base:
+            ctx.set_flags(base)
         t0 = time.perf_counter()
         tk = ctx.plan([batches[q] for q in range(u, min(u + L + ahead, nb - 1) + 1)])
         t1 = time.perf_counter()

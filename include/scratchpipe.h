@@ -64,6 +64,10 @@ typedef int32_t sp_status;
 /* sp_config.flags */
 #define SP_FLAG_DEBUG_SYNC 0x1u /* synchronise the device at the end of every call     */
 #define SP_FLAG_TIMING 0x2u     /* time forward/backward/plan/fill kernels with events */
+#define SP_FLAG_EVENT_WAITS 0x4u /* wait on events where the library otherwise waits on
+                                    stream values (hipStreamWaitValue64); for tools
+                                    that run one dispatch at a time, under which a
+                                    value wait would wait for a dispatch held back */
 
 typedef struct sp_ctx *sp_handle;
 

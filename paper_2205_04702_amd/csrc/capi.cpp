@@ -228,6 +228,8 @@ class ScatterPool {
 
 }  // namespace
 
+constexpr uint32_t SP_FLAGS_ALL = SP_FLAG_DEBUG_SYNC | SP_FLAG_TIMING | SP_FLAG_EVENT_WAITS;
+
 // words of sp_ctx::sem, one cache line apart
 constexpr int SEM_PLANNED = 0, SEM_FILLED = 8, SEM_WORDS = 16;
 
@@ -269,12 +271,12 @@ struct sp_ctx {
     // so ev_upd[r] (backward of the entry's ticket issued) also frees ring[r]
     std::vector<TicketDev> tk;
     std::vector<TicketHost> tkh;
-    std::vector<hipEvent_t> ev_filled, ev_upd;
+    std::vector<hipEvent_t> ev_planned, ev_filled, ev_upd;
     // stream-ordered counters in device memory for the two waits that are
     // nearly always still pending when they are enqueued (a value wait costs
     // the host a fraction of a wait on an unfinished event): sem[SEM_PLANNED]
     // reaches k + 1 when plan k's commit has run, sem[SEM_FILLED] when its
-    // fill has
+    // fill has.  The events are recorded as well, for SP_FLAG_EVENT_WAITS.
     uint64_t *sem = nullptr;
     std::vector<hipStream_t> upd_stream;    // stream each ticket's backward ran on
     int64_t planned = 0, forwarded = 0, updated = 0;
@@ -476,7 +478,7 @@ static void release(sp_ctx *h)
     }
     h->scatter.stop();
     (void)hipDeviceSynchronize();
-    for (auto *v : {&h->ring_ready, &h->ev_filled, &h->ev_upd})
+    for (auto *v : {&h->ring_ready, &h->ev_planned, &h->ev_filled, &h->ev_upd})
         for (auto &e : *v)
             if (e) hipEventDestroy(e);
     if (h->ev_consumed) hipEventDestroy(h->ev_consumed);
@@ -568,6 +570,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     h->ring_seen.assign(h->nring, 0);
     h->tk.assign(h->nring, TicketDev{});
     h->tkh.assign(h->nring, TicketHost{});
+    h->ev_planned.assign(h->nring, nullptr);
     h->ev_filled.assign(h->nring, nullptr);
     h->ev_upd.assign(h->nring, nullptr);
     h->upd_stream.assign(h->nring, nullptr);
@@ -598,6 +601,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
         TRY(dalloc(h, &t.v_slot, N));
         TRY(dalloc(h, &t.v_old_key, N));
         TRY(dalloc(h, &t.v_old_lu, N));
+        HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_planned[k], hipEventDisableTiming));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_filled[k], hipEventDisableTiming));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_upd[k], hipEventDisableTiming));
     }
@@ -718,7 +722,7 @@ extern "C" sp_status sp_create(const sp_config *c, sp_handle *out)
         total += c->slots[t];
     }
     if (total > INT32_MAX) return fail(nullptr, SP_ERR_INVALID_ARG, "total slots exceed 2^31-1");
-    if (c->flags & ~(SP_FLAG_DEBUG_SYNC | SP_FLAG_TIMING)) return fail(nullptr, SP_ERR_INVALID_ARG, "unknown flags");
+    if (c->flags & ~SP_FLAGS_ALL) return fail(nullptr, SP_ERR_INVALID_ARG, "unknown flags");
     int ndev = 0;
     if (hipGetDeviceCount(&ndev) != hipSuccess || c->device < 0 || c->device >= ndev) {
         (void)hipGetLastError();
@@ -1103,6 +1107,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     CHECK_LAUNCH(h);
     if (h->ws_plan.overflow) return fail(h, SP_ERR_HIP, "internal: scan workspace too small");
     HIPCHK(h, hipStreamWriteValue64(h->s_plan, h->sem + SEM_PLANNED, (uint64_t)k + 1, 0));
+    HIPCHK(h, hipEventRecord(h->ev_planned[e], h->s_plan));
     if (timing) HIPCHK(h, h->t_plan.end(h->s_plan));
     double tF = host_ms();
     h->host_ms[3] += tF - tE;
@@ -1131,8 +1136,11 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     // the device staging slot is free once plan k - NSTAGE's copy has run
     // (issued two plans ago)
     if (k >= NSTAGE) HIPCHK(h, wait_unless_done(h->s_move, h->ev_d2h[sl]));
-    HIPCHK(h, hipStreamWaitValue64(h->s_move, h->sem + SEM_PLANNED, (uint64_t)k + 1,
-                                   hipStreamWaitValueGte, ~0ull));
+    if (h->flags & SP_FLAG_EVENT_WAITS)
+        HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_planned[e], 0));
+    else
+        HIPCHK(h, hipStreamWaitValue64(h->s_move, h->sem + SEM_PLANNED, (uint64_t)k + 1,
+                                       hipStreamWaitValueGte, ~0ull));
     if (timing) HIPCHK(h, h->t_fill.begin(h->s_move));
     if (n_miss > 0) {
         // RAW-2/3: a victim's row is final once the last update that used it
@@ -1190,8 +1198,11 @@ extern "C" sp_status sp_forward(sp_handle h, int64_t ticket, float *d_out, void 
     const int64_t nbags = (int64_t)h->T * th.B;
     if (nbags > 0 && !d_out) return fail(h, SP_ERR_INVALID_ARG, "null d_out");
     hipStream_t s = (hipStream_t)stream;
-    HIPCHK(h, hipStreamWaitValue64(s, h->sem + SEM_FILLED, (uint64_t)ticket + 1,
-                                   hipStreamWaitValueGte, ~0ull));
+    if (h->flags & SP_FLAG_EVENT_WAITS)
+        HIPCHK(h, hipStreamWaitEvent(s, h->ev_filled[e], 0));
+    else
+        HIPCHK(h, hipStreamWaitValue64(s, h->sem + SEM_FILLED, (uint64_t)ticket + 1,
+                                       hipStreamWaitValueGte, ~0ull));
     // RAW-1: the previous update must land first (implicit on the same stream)
     if (ticket >= 1 && s != h->last_update_stream)
         HIPCHK(h, wait_unless_done(s, h->ev_upd[(ticket - 1) % h->nring]));
@@ -1269,7 +1280,7 @@ extern "C" sp_status sp_flush(sp_handle h)
 extern "C" sp_status sp_set_flags(sp_handle h, uint32_t flags)
 {
     TRY(usable(h));
-    if (flags & ~(SP_FLAG_DEBUG_SYNC | SP_FLAG_TIMING)) return fail(h, SP_ERR_INVALID_ARG, "unknown flags");
+    if (flags & ~SP_FLAGS_ALL) return fail(h, SP_ERR_INVALID_ARG, "unknown flags");
     h->flags = flags;
     return SP_OK;
 }

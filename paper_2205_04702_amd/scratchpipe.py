@@ -25,6 +25,7 @@ SP_ERR_HIP = -5
 SP_ERR_STATE = -6
 SP_FLAG_DEBUG_SYNC = 0x1
 SP_FLAG_TIMING = 0x2
+SP_FLAG_EVENT_WAITS = 0x4
 SP_MAX_AHEAD = 2  # batches after the hold window that sp_plan sorts early
 SP_MAX_HOLD_PAST = 4
 POLICIES = {"lru": 0, "lfu": 1, "random": 2}  # SP_POLICY_*

@@ -190,13 +190,16 @@ def test_bad_prepared_batch_fails_the_plan_that_holds_it(harness, ahead):
 def test_overlapped_equals_serialized_bit_for_bit(harness):
     """The overlapped schedule (plan of the next batch while this one trains,
     fills and write-backs on side streams) gives exactly the tables of a run
-    with a device synchronisation after every call, and of a second run."""
+    with a device synchronisation after every call, of runs with batches
+    handed over early, of a run that waits on events instead of stream values,
+    and of a second run."""
     w = wl.custom(rows=[3000, 5000, 2000], dim=64, batch=64, pooling=[4, 6, 2],
                   slots=[800, 1200, 500], lookahead=3, steps=30, dist=("zipf", 1.05), seed=41)
     _say("case overlap vs serialised")
     batches = harness.make_inputs(w)
     results = []
-    for flags, ahead in ((0, 0), (spm.SP_FLAG_DEBUG_SYNC, 0), (0, 1), (0, 2), (0, 0)):
+    for flags, ahead in ((0, 0), (spm.SP_FLAG_DEBUG_SYNC, 0), (0, 1), (0, 2),
+                         (spm.SP_FLAG_EVENT_WAITS, 2), (0, 0)):
         host = harness.fresh_host(w)
         harness.run_gpu(w, batches, host, flags=flags, prepare_ahead=ahead)
         results.append([host[t].copy() for t in range(w.tables)])

@@ -250,6 +250,14 @@ def main():
                        "forward_GBps_unique": round(fwd_gbs, 1),
                        "forward_GBps_requested": round(kb["forward_requested"] / (fwd_ms * 1e-3) / 1e9, 1),
                        "backward_GBps": round(bwd_gbs, 1)})
+        # the fill is bound by the host link, not by HBM: its misses' rows
+        # cross the link once per fill (timed with the same events)
+        fill_ms = d["ms_fill"] / max(d["timed_fill"], 1)
+        if fill_ms > 0:
+            link = d["bytes_fill"] / max(d["plans"], 1) / (fill_ms * 1e-3) / 1e9
+            detail["host_link"] = {"kernel": "k_move", "achieved_GBps": round(link, 1),
+                                   "nominal_GBps": 64.0, "unit": "GB/s host to device",
+                                   "frac_nominal": round(link / 64.0, 3)}
         src = open(os.path.join(ROOT, "paper_2205_04702_amd", "csrc", "k_train.hip"), "rb").read()
         src_hash = hashlib.sha256(src).hexdigest()
         dom = "forward" if fwd_ms >= bwd_ms else "backward"

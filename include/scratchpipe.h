@@ -124,9 +124,10 @@ typedef struct {
     int64_t pinned_bytes;       /* pinned staging held by the context                   */
     /* SP_FLAG_TIMING only: summed time in ms and number of timed launches.
      * forward, backward (per-chunk kernel) and combine (runs split over several
-     * chunks, launched only when there are any) are kernel execution times;
-     * plan (the commit sequence: victims, Hit-Map, slot metadata) and fill
-     * (evicted-row staging and miss fill) span their launch sequences. */
+     * chunks, launched only when there are any) and fill (evicted-row
+     * staging and miss fill, plans with misses only) are kernel execution
+     * times; plan (the commit sequence: victims, Hit-Map, slot metadata)
+     * spans its launch sequence. */
     double ms_forward, ms_backward, ms_combine, ms_plan, ms_fill;
     int64_t timed_forward, timed_backward, timed_combine, timed_plan, timed_fill;
     /* host time spent inside sp_plan, in ms: enqueueing ingest, enqueueing the

@@ -1141,7 +1141,6 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     else
         HIPCHK(h, hipStreamWaitValue64(h->s_move, h->sem + SEM_PLANNED, (uint64_t)k + 1,
                                        hipStreamWaitValueGte, ~0ull));
-    if (timing) HIPCHK(h, h->t_fill.begin(h->s_move));
     if (n_miss > 0) {
         // RAW-2/3: a victim's row is final once the last update that used it
         // has run.  Update j freed ring entry j % nring for batch j + nring,
@@ -1157,13 +1156,14 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
             if (j == last || h->upd_stream[ej] != h->upd_stream[last % h->nring])
                 HIPCHK(h, wait_unless_done(h->s_move, h->ev_upd[ej]));
         }
+        if (timing) HIPCHK(h, h->t_fill.begin(h->s_move));  // the fill kernel itself
         launch_move(h->storage, h->D, h->tb, h->host_dev, tk, n_miss, u, h->stage_dev[sl],
                     h->s_move);
         CHECK_LAUNCH(h);
+        if (timing) HIPCHK(h, h->t_fill.end(h->s_move));
     }
     HIPCHK(h, hipEventRecord(h->ev_filled[e], h->s_move));
     HIPCHK(h, hipStreamWriteValue64(h->s_move, h->sem + SEM_FILLED, (uint64_t)k + 1, 0));
-    if (timing) HIPCHK(h, h->t_fill.end(h->s_move));
     // the previous plan's write-back copy, on its own stream, so that it
     // overlaps this fill (they use the host link in opposite directions)
     TRY(issue_copy(h));

@@ -139,6 +139,9 @@ typedef struct {
      * its stream reaches it, waits for ingests included) */
     double ms_ingest, ms_query;
     int64_t timed_ingest, timed_query;
+    /* host time, in ms, that sp_plan spends before returning waiting until its
+     * ingests have read the caller's window arrays */
+    double host_ms_inputs;
 } sp_stats;
 
 /* Per-plan decisions copied to the host for checking.  The caller allocates

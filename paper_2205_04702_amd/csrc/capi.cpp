@@ -236,6 +236,9 @@ constexpr int SEM_PLANNED = 0, SEM_FILLED = 8, SEM_WORDS = 16;
 // staging slots of evicted rows (fill of plan p, copy of plan p - 1 and the
 // host scatter of plan p - 2 can all be in flight)
 constexpr int NSTAGE = 3;
+// write-back copies above this size go on the ingest stream, where they
+// overlap the next fill; smaller ones go on the copy stream
+constexpr int64_t SMALL_COPY_BYTES = 8ll << 20;
 
 struct sp_ctx {
     // configuration
@@ -321,7 +324,11 @@ struct sp_ctx {
 
     // plan stream: query, hold, victims, commit; ingest stream: sorting and
     // deduplicating batches as they become visible; move stream: write-back
-    // staging, miss fills and the device-to-host copy of evicted rows
+    // staging and miss fills; copy stream: the device-to-host copy of evicted
+    // rows when it is small.  A process gets few hardware queues (four by
+    // default) and streams beyond them share one, in order: the copy stream
+    // may land behind the fill.  A large copy therefore goes on the ingest
+    // stream, where it overlaps the next fill.
     hipStream_t s_plan = nullptr, s_ingest = nullptr, s_move = nullptr, s_copy = nullptr;
 
     // write-back thread
@@ -340,7 +347,8 @@ struct sp_ctx {
     sp_stats st{};
     Timer t_fwd, t_bwd, t_cmb, t_plan, t_fill, t_ing, t_qry;
     int64_t dev_bytes = 0, pinned_bytes = 0;
-    double host_ms[5] = {0, 0, 0, 0, 0};  // ingest, query, wait, commit, mover (sp_plan)
+    // sp_plan: ingest, query, wait, commit, mover, waiting for inputs to be read
+    double host_ms[6] = {0, 0, 0, 0, 0, 0};
     std::vector<void *> dev_allocs, pinned_allocs;
     std::string err;
     bool broken = false;
@@ -830,10 +838,10 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
     return SP_OK;
 }
 
-// Issue the pending write-back copy (plan p = copy_pending) on the copy
-// stream and hand its rows to the write-back thread.  The host staging slot
-// was last used by plan p - NSTAGE, whose scatter is joined first.
-static sp_status issue_copy(sp_ctx *h)
+// Issue the pending write-back copy (plan p = copy_pending) on stream s and
+// hand its rows to the write-back thread.  The host staging slot was last
+// used by plan p - NSTAGE, whose scatter is joined first.
+static sp_status issue_copy(sp_ctx *h, hipStream_t s)
 {
     const int64_t p = h->copy_pending;
     if (p < 0) return SP_OK;
@@ -843,10 +851,10 @@ static sp_status issue_copy(sp_ctx *h)
     job.ticket = p;
     const int64_t n = h->copy_n;
     if (n > 0) {
-        HIPCHK(h, wait_unless_done(h->s_copy, h->ev_filled[p % h->nring]));
+        HIPCHK(h, wait_unless_done(s, h->ev_filled[p % h->nring]));
         HIPCHK(h, hipMemcpyAsync(h->stage_host[sl], h->stage_dev[sl],
-                                 sizeof(float) * n * (h->D + 1), hipMemcpyDeviceToHost, h->s_copy));
-        HIPCHK(h, hipEventRecord(h->ev_d2h[sl], h->s_copy));
+                                 sizeof(float) * n * (h->D + 1), hipMemcpyDeviceToHost, s));
+        HIPCHK(h, hipEventRecord(h->ev_d2h[sl], s));
         job.ev = h->ev_d2h[sl];
         job.rows = h->stage_host[sl];
         job.keys = (const int32_t *)(h->stage_host[sl] + n * h->D);
@@ -868,6 +876,7 @@ static sp_status issue_copy(sp_ctx *h)
 // that checks the stream.
 static void wait_inputs_read(sp_ctx *h)
 {
+    const double t0 = host_ms();
     if (h->wait_cons_event) (void)hipEventSynchronize(h->ev_consumed);
     if (h->wait_cons_word) {
         const volatile uint64_t *w = h->h_cnt + COUNTER_WORDS;
@@ -880,6 +889,7 @@ static void wait_inputs_read(sp_ctx *h)
         }
     }
     h->wait_cons_event = h->wait_cons_word = false;
+    h->host_ms[5] += host_ms() - t0;
 }
 
 // Wait until the query with sequence number seq has published every counter
@@ -1109,6 +1119,12 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     HIPCHK(h, hipStreamWriteValue64(h->s_plan, h->sem + SEM_PLANNED, (uint64_t)k + 1, 0));
     HIPCHK(h, hipEventRecord(h->ev_planned[e], h->s_plan));
     if (timing) HIPCHK(h, h->t_plan.end(h->s_plan));
+    // a large write-back copy of the previous plan goes on the ingest stream
+    // behind this call's ingests (its fill has normally finished by now): it
+    // then overlaps this plan's fill (the two use the host link in opposite
+    // directions) and is well under way when the next call's ingest comes
+    if (h->copy_pending >= 0 && h->copy_n * (h->D + 1) * (int64_t)sizeof(float) > SMALL_COPY_BYTES)
+        TRY(issue_copy(h, h->s_ingest));
     double tF = host_ms();
     h->host_ms[3] += tF - tE;
     // ---- the next plan's query, when its whole window is known: batches
@@ -1128,7 +1144,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     for (const auto &d : h->deadlines)
         if (d.second <= k) need = std::max(need, d.first);
     if (need >= 0) {
-        if (h->copy_pending >= 0 && h->copy_pending <= need) TRY(issue_copy(h));
+        if (h->copy_pending >= 0 && h->copy_pending <= need) TRY(issue_copy(h, h->s_copy));
         TRY(join_jobs(h, need));
         while (!h->deadlines.empty() && h->deadlines.front().first <= need) h->deadlines.pop_front();
     }
@@ -1164,9 +1180,9 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     }
     HIPCHK(h, hipEventRecord(h->ev_filled[e], h->s_move));
     HIPCHK(h, hipStreamWriteValue64(h->s_move, h->sem + SEM_FILLED, (uint64_t)k + 1, 0));
-    // the previous plan's write-back copy, on its own stream, so that it
-    // overlaps this fill (they use the host link in opposite directions)
-    TRY(issue_copy(h));
+    // a small one goes on the copy stream now: it ends long before the next
+    // fill, even where its queue is the move stream's
+    TRY(issue_copy(h, h->s_copy));
     h->copy_pending = k;
     h->copy_n = n_miss;
     h->deadlines.emplace_back(k, k + nhold);
@@ -1250,7 +1266,7 @@ extern "C" sp_status sp_backward_update(sp_handle h, int64_t ticket, const float
 extern "C" sp_status sp_flush(sp_handle h)
 {
     TRY(usable(h));
-    TRY(issue_copy(h));
+    TRY(issue_copy(h, h->s_copy));
     HIPCHK(h, hipDeviceSynchronize());
     TRY(join_jobs(h, h->planned - 1));
     h->deadlines.clear();
@@ -1319,6 +1335,7 @@ extern "C" sp_status sp_get_stats(sp_handle h, sp_stats *out)
     s.host_ms_wait = h->host_ms[2];
     s.host_ms_commit = h->host_ms[3];
     s.host_ms_mover = h->host_ms[4];
+    s.host_ms_inputs = h->host_ms[5];
     s.timed_plan = h->t_plan.count;
     s.timed_fill = h->t_fill.count;
     s.ms_ingest = h->t_ing.ms;

@@ -430,7 +430,6 @@ __global__ void __launch_bounds__(IG_THREADS) k_ingest_table(Tables tb, const in
 {
     __shared__ uint64_t buf[2][IG_MAX];
     __shared__ uint32_t wc[IG_WAVES][256];
-    __shared__ uint32_t base[256];
     __shared__ uint32_t lds[IG_WAVES];
     __shared__ uint32_t id_s, multi_s;
     __shared__ int32_t err_s;
@@ -494,7 +493,7 @@ __global__ void __launch_bounds__(IG_THREADS) k_ingest_table(Tables tb, const in
     if (err) atomicOr(&err_s, err);
     __syncthreads();
     if (tid == 0) inputs_read();
-    uint64_t *srt = lds_radix_sort<IG_THREADS>(buf[0], buf[1], n, IG_SHIFT_ROW, rb, wc, base, lds);
+    uint64_t *srt = lds_radix_sort<IG_THREADS, IG_ITEMS>(buf[0], buf[1], n, IG_SHIFT_ROW, rb, wc, lds);
     // the other buffer holds each run's first sorted index and its first chunk
     uint32_t *run0 = reinterpret_cast<uint32_t *>(srt == buf[0] ? buf[1] : buf[0]);
     uint32_t *chunk0 = run0 + IG_MAX;

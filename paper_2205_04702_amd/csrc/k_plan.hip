@@ -372,11 +372,8 @@ struct VictimOut {
 // ---------------------------------------------------------------- victim order in LDS
 //
 // When every active table has at most VS_MAX victims, one block per table puts
-// its compacted victims (slot order) into priority order: a stable LSD radix
-// sort on the priority in LDS, 8-bit digits.  Within a round of VS_THREADS keys, lanes
-// of a wave with the same digit find each other with ballots; the lowest of
-// them records the wave's count stamped with the round, so no clearing is
-// needed between rounds.
+// its compacted victims (slot order) into priority order: the stable LDS radix
+// sort on entries (priority << 32 | slot), keyed on the priority bits only.
 constexpr int VS_THREADS = 1024;
 constexpr int VS_WAVES = VS_THREADS / WAVE;
 constexpr int VS_MAX = 2048;
@@ -384,76 +381,20 @@ constexpr int VS_MAX = 2048;
 __global__ void __launch_bounds__(VS_THREADS) k_victim_sort(SelArgs a, const uint32_t *vk,
                                                           const uint32_t *vv, int32_t *v_slot)
 {
-    __shared__ uint32_t kb[2][VS_MAX], vb[2][VS_MAX];
+    __shared__ uint64_t eb[2][VS_MAX];
     __shared__ uint32_t wc[VS_WAVES][256];
-    __shared__ uint32_t base[256];
     __shared__ uint32_t lds[VS_WAVES];
     const int y = blockIdx.x;
     const int n = a.k[y] < VS_MAX ? a.k[y] : VS_MAX;
     const int64_t off = a.vbase[y];
-    const int tid = threadIdx.x, w = wave_id(), lane = lane_id();
+    const int tid = threadIdx.x;
     const uint32_t kmask = a.prio_bits >= 32 ? ~0u : ((1u << a.prio_bits) - 1u);
-    for (int i = tid; i < n; i += VS_THREADS) {
-        kb[0][i] = vk[off + i] & kmask;
-        vb[0][i] = vv[off + i];
-    }
-    for (int i = tid; i < VS_WAVES * 256; i += VS_THREADS) (&wc[0][0])[i] = 0;
-    const uint64_t lt = lanemask_lt();
-    int cur = 0;
-    uint32_t stamp = 0;
-    for (int shift = 0; shift < a.prio_bits; shift += 8) {
-        if (tid < 256) base[tid] = 0;
-        __syncthreads();
-        for (int i = tid; i < n; i += VS_THREADS) atomicAdd(&base[(kb[cur][i] >> shift) & 255u], 1u);
-        __syncthreads();
-        uint32_t tot;
-        const uint32_t ex = block_excl_scan_n<VS_THREADS>(tid < 256 ? base[tid] : 0u, lds, tot);
-        if (tid < 256) base[tid] = ex;
-        __syncthreads();
-        for (int r0 = 0; r0 < n; r0 += VS_THREADS) {
-            stamp += 1u << 16;
-            const int i = r0 + tid;
-            const bool valid = i < n;
-            const uint32_t key = valid ? kb[cur][i] : 0u, val = valid ? vb[cur][i] : 0u;
-            const uint32_t d = (key >> shift) & 255u;
-            uint64_t peers = __ballot(valid);
-            for (int b = 0; b < 8; ++b) {
-                const uint32_t bit = (d >> b) & 1u;
-                const uint64_t bb = __ballot(bit);
-                peers &= bit ? bb : ~bb;
-            }
-            const int leader = valid ? __ffsll((unsigned long long)peers) - 1 : lane;
-            const bool is_leader = valid && leader == lane;
-            if (is_leader) wc[w][d] = stamp | (uint32_t)__popcll(peers);
-            __syncthreads();
-            uint32_t start = 0, total = 0;
-            bool last_wave = false;
-            if (is_leader) {
-                uint32_t before = 0;
-                last_wave = true;
-                for (int q = 0; q < VS_WAVES; ++q) {
-                    const uint32_t e = wc[q][d];
-                    const uint32_t c = (e & 0xFFFF0000u) == stamp ? (e & 0xFFFFu) : 0u;
-                    if (q < w) before += c;
-                    if (q > w && c) last_wave = false;
-                    total += c;
-                }
-                start = base[d] + before;
-            }
-            start = __shfl(start, leader, WAVE);
-            __syncthreads();  // every leader has read base[d]
-            if (is_leader && last_wave) base[d] += total;
-            if (valid) {
-                uint32_t p = start + (uint32_t)__popcll(peers & lt);
-                p = p < (uint32_t)n ? p : (uint32_t)(n - 1);
-                kb[cur ^ 1][p] = key;
-                vb[cur ^ 1][p] = val;
-            }
-            __syncthreads();
-        }
-        cur ^= 1;
-    }
-    for (int i = tid; i < n; i += VS_THREADS) v_slot[off + i] = (int32_t)vb[cur][i];
+    for (int i = tid; i < n; i += VS_THREADS)
+        eb[0][i] = (uint64_t)(vk[off + i] & kmask) << 32 | vv[off + i];
+    __syncthreads();
+    const uint64_t *srt = lds_radix_sort<VS_THREADS, VS_MAX / VS_THREADS>(
+        eb[0], eb[1], n, 32, a.prio_bits, wc, lds);
+    for (int i = tid; i < n; i += VS_THREADS) v_slot[off + i] = (int32_t)(uint32_t)srt[i];
 }
 
 void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int32_t *held,

@@ -86,15 +86,16 @@ __global__ void __launch_bounds__(BLOCK) k_forward(const float4 *__restrict__ st
 
 // ---------------------------------------------------------------- backward + SGD
 
-__device__ __forceinline__ void sgd_row(float4 *w, float4 g, float lr)
+__device__ __forceinline__ float4 sgd_step(float4 x, float4 g, float lr)
 {
-    float4 x = *w;
     x.x = fmaf(-lr, g.x, x.x);
     x.y = fmaf(-lr, g.y, x.y);
     x.z = fmaf(-lr, g.z, x.z);
     x.w = fmaf(-lr, g.w, x.w);
-    *w = x;
+    return x;
 }
+
+__device__ __forceinline__ void sgd_row(float4 *w, float4 g, float lr) { *w = sgd_step(*w, g, lr); }
 
 // Gradient coalescing and SGD (Sec. II-B "Backpropagation").  The sorted
 // positions of one batch form runs of equal keys; each run is cut into chunks
@@ -124,6 +125,11 @@ __global__ void __launch_bounds__(BLOCK) k_backward(float4 *__restrict__ storage
     const int64_t p0 = d.x, p1 = d.y;
     const int32_t slot = slot_u[d.z];
     const int64_t nch = d.w;
+    // a one-chunk run reads its Storage row beside its gradient rows rather
+    // than after them: one memory round trip less on the lane's path
+    const bool direct = nch == 1 && (uint32_t)slot < (uint64_t)nslots;
+    float4 *const w = storage + (direct ? (int64_t)slot * LPR + c : 0);
+    const float4 w0 = direct ? *w : make_float4(0.f, 0.f, 0.f, 0.f);
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     int64_t p = p0;
     for (; p + 4 <= p1; p += 4) {
@@ -146,8 +152,8 @@ __global__ void __launch_bounds__(BLOCK) k_backward(float4 *__restrict__ storage
     }
     if (nch > 1) {
         partial[ch * LPR + c] = acc;
-    } else if ((uint32_t)slot < (uint64_t)nslots) {
-        sgd_row(storage + (int64_t)slot * LPR + c, acc, lr);
+    } else if (direct) {
+        *w = sgd_step(w0, acc, lr);
     }
 }
 

@@ -267,43 +267,40 @@ inline void seg_scan(Seg seg, int nseg, int64_t max_len, Val val, Out out, ScanW
 
 // ---------------------------------------------------------------- radix sort in LDS
 //
-// Stable LSD radix sort of n entries (n <= NT * 65535) held in LDS, by bits
+// Stable LSD radix sort of n entries (n <= NT * ITEMS) held in LDS, by bits
 // [lo, lo + bits) of the entry, 8-bit digits, by a block of NT threads.  a
 // holds the input and b is scratch of the same size; the return value is the
-// buffer that holds the result.  Per pass: a digit histogram, its exclusive
-// scan (base[d] = first output index of digit d), then rounds of NT entries in
-// input order.  Within a round, lanes of a wave with the same digit find each
-// other with one ballot per digit bit; the lowest of them records the wave's
-// count stamped with the round, so counts of earlier rounds read as zero and
-// wc never needs clearing after the first.  The last wave holding a digit
-// advances base[d] past the round's entries of that digit.  wc is
-// [NT / WAVE][256], base [256], lds [NT / WAVE]; every thread must call it.
-template <int NT, typename E>
+// buffer that holds the result.  Wave w ranks its own contiguous share of the
+// entries, 64 at a time in input order: lanes with the same digit find each
+// other with one ballot per digit bit, and the lowest of them advances the
+// wave's running count of that digit, wc[w][d].  One block scan over the digit
+// totals then gives every (wave, digit) its first output index, so a digit's
+// entries land in wave order and, within a wave, in input order: the pass is
+// stable with five barriers whatever n is.  wc is [NT / WAVE][256] and lds
+// [NT / WAVE]; every thread must call it.
+template <int NT, int ITEMS, typename E>
 __device__ E *lds_radix_sort(E *a, E *b, int n, int lo, int bits, uint32_t (*wc)[256],
-                             uint32_t *base, uint32_t *lds)
+                             uint32_t *lds)
 {
     constexpr int NW = NT / WAVE;
+    static_assert(ITEMS * WAVE <= 65536, "ranks within a wave take 16 bits");
     const int tid = threadIdx.x, w = wave_id(), lane = lane_id();
-    for (int i = tid; i < NW * 256; i += NT) (&wc[0][0])[i] = 0;
     const uint64_t lt = lanemask_lt();
-    uint32_t stamp = 0;
+    const int per = ((n + NW - 1) / NW + WAVE - 1) / WAVE * WAVE;  // entries per wave
+    const int i0 = w * per;
     for (int shift = lo; shift < lo + bits; shift += 8) {
         const int dbits = lo + bits - shift < 8 ? lo + bits - shift : 8;
         const uint32_t dmask = (1u << dbits) - 1u;
-        if (tid < 256) base[tid] = 0;
+        for (int i = tid; i < NW * 256; i += NT) (&wc[0][0])[i] = 0;
         __syncthreads();
-        for (int i = tid; i < n; i += NT) atomicAdd(&base[(uint32_t)(a[i] >> shift) & dmask], 1u);
-        __syncthreads();
-        uint32_t tot;
-        const uint32_t ex = block_excl_scan_n<NT>(tid < 256 ? base[tid] : 0u, lds, tot);
-        if (tid < 256) base[tid] = ex;
-        __syncthreads();
-        for (int r0 = 0; r0 < n; r0 += NT) {
-            stamp += 1u << 16;
-            const int i = r0 + tid;
+        uint32_t rk[ITEMS];  // digit << 16 | rank of the entry among the wave's entries
+#pragma unroll
+        for (int g = 0; g < ITEMS; ++g) {
+            rk[g] = 0;
+            if (g * WAVE >= per) break;  // uniform over the wave
+            const int i = i0 + g * WAVE + lane;
             const bool valid = i < n;
-            const E e = valid ? a[i] : E(0);
-            const uint32_t d = (uint32_t)(e >> shift) & dmask;
+            const uint32_t d = valid ? (uint32_t)(a[i] >> shift) & dmask : 0u;
             uint64_t peers = __ballot(valid);
             for (int q = 0; q < dbits; ++q) {
                 const uint32_t bit = (d >> q) & 1u;
@@ -311,33 +308,40 @@ __device__ E *lds_radix_sort(E *a, E *b, int n, int lo, int bits, uint32_t (*wc)
                 peers &= bit ? bb : ~bb;
             }
             const int leader = valid ? __ffsll((unsigned long long)peers) - 1 : lane;
-            const bool is_leader = valid && leader == lane;
-            if (is_leader) wc[w][d] = stamp | (uint32_t)__popcll(peers);
-            __syncthreads();
-            uint32_t start = 0, total = 0;
-            bool last_wave = false;
-            if (is_leader) {
-                uint32_t before = 0;
-                last_wave = true;
-                for (int q = 0; q < NW; ++q) {
-                    const uint32_t c4 = wc[q][d];
-                    const uint32_t c = (c4 & 0xFFFF0000u) == stamp ? (c4 & 0xFFFFu) : 0u;
-                    if (q < w) before += c;
-                    if (q > w && c) last_wave = false;
-                    total += c;
-                }
-                start = base[d] + before;
+            uint32_t before = 0;
+            if (valid && leader == lane) {
+                before = wc[w][d];
+                wc[w][d] = before + (uint32_t)__popcll(peers);
             }
-            start = __shfl(start, leader, WAVE);
-            __syncthreads();  // every leader has read base[d]
-            if (is_leader && last_wave) base[d] += total;
-            if (valid) {
-                uint32_t p = start + (uint32_t)__popcll(peers & lt);
-                p = p < (uint32_t)n ? p : (uint32_t)(n - 1);  // never write past the buffer
-                b[p] = e;
-            }
-            __syncthreads();
+            before = __shfl(before, leader, WAVE);
+            rk[g] = d << 16 | (before + (uint32_t)__popcll(peers & lt));
         }
+        __syncthreads();
+        uint32_t cnt = 0;
+        if (tid < 256)
+            for (int q = 0; q < NW; ++q) cnt += wc[q][tid];
+        uint32_t tot;
+        const uint32_t ex = block_excl_scan_n<NT>(cnt, lds, tot);
+        if (tid < 256) {
+            uint32_t run = ex;
+            for (int q = 0; q < NW; ++q) {
+                const uint32_t c = wc[q][tid];
+                wc[q][tid] = run;
+                run += c;
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int g = 0; g < ITEMS; ++g) {
+            if (g * WAVE >= per) break;
+            const int i = i0 + g * WAVE + lane;
+            if (i < n) {
+                uint32_t p = wc[w][rk[g] >> 16] + (rk[g] & 0xFFFFu);
+                p = p < (uint32_t)n ? p : (uint32_t)(n - 1);  // never write past the buffer
+                b[p] = a[i];
+            }
+        }
+        __syncthreads();
         E *t = a;
         a = b;
         b = t;

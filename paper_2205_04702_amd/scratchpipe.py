@@ -65,12 +65,14 @@ _STAT_CNT = ["timed_forward", "timed_backward", "timed_combine", "timed_plan", "
 _STAT_HOST = ["host_ms_ingest", "host_ms_query", "host_ms_wait", "host_ms_commit", "host_ms_mover"]
 _STAT_F64B = ["ms_ingest", "ms_query"]
 _STAT_CNTB = ["timed_ingest", "timed_query"]
+_STAT_HOSTB = ["host_ms_inputs"]
 
 
 class sp_stats(C.Structure):
     _fields_ = ([(n, C.c_int64) for n in _STAT_I64] + [(n, C.c_double) for n in _STAT_F64]
                 + [(n, C.c_int64) for n in _STAT_CNT] + [(n, C.c_double) for n in _STAT_HOST]
-                + [(n, C.c_double) for n in _STAT_F64B] + [(n, C.c_int64) for n in _STAT_CNTB])
+                + [(n, C.c_double) for n in _STAT_F64B] + [(n, C.c_int64) for n in _STAT_CNTB]
+                + [(n, C.c_double) for n in _STAT_HOSTB])
 
 
 _DUMP_I32 = ["u_table", "u_row", "inv", "m_table", "m_row", "v_slot", "v_old_row", "v_old_use",

@@ -51,6 +51,7 @@ int main(void) {
   P(sp_config, max_ids); P(sp_config, flags); P(sp_config, device); P(sp_config, host_tables);
   P(sp_config, policy); P(sp_config, hold_past); P(sp_config, seed); P(sp_config, max_table_ids);
   P(sp_batch, nnz); P(sp_batch, on_device); P(sp_stats, ms_forward); P(sp_stats, timed_fill);
+  P(sp_stats, timed_query); P(sp_stats, host_ms_inputs);
   P(sp_plan_dump, hit); P(sp_plan_dump, nnz);
   return 0; }
 """)

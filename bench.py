@@ -111,6 +111,10 @@ def main():
     ap.add_argument("--event-waits", action="store_true",
                     help="wait on events instead of stream values (for profilers that run one "
                          "dispatch at a time, such as counter collection)")
+    ap.add_argument("--serialize", action="store_true",
+                    help="synchronise the device at the end of every call, so each kernel runs "
+                         "alone (kernel times without overlap; throughput is then not the "
+                         "pipelined one)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="after the timed region, run a plain elementwise copy (torch.neg) of MIB "
                          "MiB three times: the reference kernel for scaling HBM byte counters")
@@ -145,14 +149,19 @@ def main():
         batches = [(torch.from_numpy(i).to(dev), torch.from_numpy(o).to(dev)) for i, o in host_batches]
     grads = [torch.from_numpy(wl.grads(w, s)).to(dev) for s in range(W + K)]
     host = sp.HostTables(w.rows, w.dim)
-    for t in range(w.tables):
-        wl.init_table(w, t, out=host[t])
+    # tables are independent streams: fill them on a few threads (numpy's
+    # generators release the GIL)
+    import concurrent.futures as cf
+    with cf.ThreadPoolExecutor(max_workers=max(1, min(16, w.tables, os.cpu_count() or 1))) as ex:
+        list(ex.map(lambda t: wl.init_table(w, t, out=host[t]), range(w.tables)))
     log(f"[bench] inputs ready in {time.perf_counter() - t0:.1f}s")
 
     timed = not args.no_timing
     every = max(1, args.time_every)
+    base_flags = ((sp.SP_FLAG_EVENT_WAITS if args.event_waits else 0)
+                  | (sp.SP_FLAG_DEBUG_SYNC if args.serialize else 0))
     ctx = sp.ScratchPipe(w.rows, w.dim, w.slots, L, host, max_batch=w.batch, max_ids=w.nnz,
-                         flags=sp.SP_FLAG_EVENT_WAITS if args.event_waits else 0, policy=args.policy, hold_past=args.hold_past,
+                         flags=base_flags, policy=args.policy, hold_past=args.hold_past,
                          max_table_ids=w.batch * max(w.pooling))
     out = torch.empty((w.tables * w.batch, w.dim), dtype=torch.float32, device=dev)
 
@@ -162,7 +171,7 @@ def main():
     def step(u):
         # hold window u..u+L, plus the next batches handed over early for sorting;
         # kernel events on a sample of the steps only (they cost host time)
-        base = sp.SP_FLAG_EVENT_WAITS if args.event_waits else 0
+        base = base_flags
         if timed:
             ctx.set_flags(base | (sp.SP_FLAG_TIMING if u % every == 0 else 0))
         elif base:
@@ -220,7 +229,8 @@ def main():
         "data": "synthetic",
         "config": {**w.describe(), "ids": "host" if args.host_ids else "hbm",
                    **({"policy": args.policy} if args.policy != "lru" else {}),
-                   **({"hold_past": args.hold_past} if args.hold_past else {})},
+                   **({"hold_past": args.hold_past} if args.hold_past else {}),
+                   **({"serialized": True} if args.serialize else {})},
     }
     detail = {"miss_rate": round(d["misses"] / max(d["unique"], 1), 4),
               "unique_per_step": round(n_unique, 1),

@@ -81,7 +81,9 @@ typedef struct {
                                    memory from sp_host_alloc (or hipHostMalloc with the
                                    mapped flag); caller-owned, must outlive the context;
                                    read on misses, written on evictions and flush      */
-    int32_t max_batch;          /* largest B any batch will have                       */
+    int32_t max_batch;          /* largest B any batch will have; T * max_batch * dim * 4
+                                   (the bytes of one [T*B][D] gradient) must stay
+                                   below 4 GiB                                         */
     int64_t max_ids;            /* largest nnz any batch will have (all tables)        */
     uint32_t flags;             /* SP_FLAG_*                                           */
     int32_t device;             /* HIP device ordinal                                  */

@@ -720,6 +720,9 @@ extern "C" sp_status sp_create(const sp_config *c, sp_handle *out)
     if (c->max_batch < 0 || c->max_ids < 0 || c->max_ids > INT32_MAX - 1)
         return fail(nullptr, SP_ERR_INVALID_ARG, "bad max_batch / max_ids");
     if ((int64_t)T * c->max_batch + 1 > INT32_MAX) return fail(nullptr, SP_ERR_INVALID_ARG, "too many bags");
+    // the backward addresses the [T*B][D] gradients with 32-bit byte offsets
+    if ((int64_t)T * c->max_batch * D * 4 > (int64_t)UINT32_MAX)
+        return fail(nullptr, SP_ERR_INVALID_ARG, "num_tables * max_batch * dim * 4 bytes exceeds 4 GiB");
     int64_t total = 0;
     for (int t = 0; t < T; ++t) {
         if (c->rows[t] < 1 || c->rows[t] > ((int64_t)1 << 25))

@@ -78,7 +78,9 @@ __global__ void __launch_bounds__(BLOCK) k_forward(const float4 *__restrict__ st
     // consecutive bags (one table's) on one XCD: the table's hot rows share its L2
     const int64_t g = xcd_block(blockIdx.x, gridDim.x) * (BLOCK / WAVE) + wave_id();
     if (g >= nbags) return;
-    float4 acc = gather_sum<LPR, 4>(storage, nslots, slot_of, bag_off[g], bag_off[g + 1]);
+    // at least 8 rows in flight per wave (a wave covers 64/LPR rows per load)
+    constexpr int UNROLL = LPR >= 32 ? 8 : 4;
+    float4 acc = gather_sum<LPR, UNROLL>(storage, nslots, slot_of, bag_off[g], bag_off[g + 1]);
     acc = reduce_rows<LPR>(acc);
     const int lane = lane_id();
     if (lane < LPR) out[g * LPR + lane] = acc;
@@ -105,6 +107,8 @@ __device__ __forceinline__ void sgd_row(float4 *w, float4 g, float lr) { *w = sg
 //  * a run of one chunk updates its Storage row directly: W -= lr * g;
 //  * a longer run stores per-chunk partial sums, which k_bwd_combine adds in
 //    chunk order before updating the row (the kernel boundary orders the two).
+constexpr int BWD_INFLIGHT = 8;  // gradient rows in flight per lane
+
 template <int LPR>
 __global__ void __launch_bounds__(BLOCK) k_backward(float4 *__restrict__ storage,
                                                     const int4 *__restrict__ chunk_desc,
@@ -130,25 +134,41 @@ __global__ void __launch_bounds__(BLOCK) k_backward(float4 *__restrict__ storage
     const bool direct = nch == 1 && (uint32_t)slot < (uint64_t)nslots;
     float4 *const w = storage + (direct ? (int64_t)slot * LPR + c : 0);
     const float4 w0 = direct ? *w : make_float4(0.f, 0.f, 0.f, 0.f);
+    // A chunk's bag indices arrive in one coalesced load (lane c of the group
+    // holds positions c, c+LPR, ...) and are broadcast by shuffles, so its
+    // gradient rows are requested BWD_INFLIGHT at a time without waiting on
+    // further index loads.  Sums stay in position order.
+    constexpr int PER_LANE = BWD_CHUNK / LPR > 0 ? BWD_CHUNK / LPR : 1;
+    const int gbase = lane_id() - c;
+    // 32-bit byte offsets from the uniform base (the gradient array is far
+    // below 4 GiB): one address register per load in flight
+    const char *__restrict__ gbytes = reinterpret_cast<const char *>(grad);
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    int64_t p = p0;
-    for (; p + 4 <= p1; p += 4) {
-        int32_t b[4];
-        float4 v[4];
+    for (int64_t base = p0; base < p1; base += BWD_CHUNK) {
+        const int n = (int)(p1 - base < BWD_CHUNK ? p1 - base : BWD_CHUNK);
+        int32_t mine[PER_LANE];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            b[q] = sbag[p + q];
-            b[q] = (uint32_t)b[q] < (uint64_t)nbags ? b[q] : 0;
+        for (int l = 0; l < PER_LANE; ++l) {
+            const int k = l * LPR + c;
+            const int32_t b = k < n ? sbag[base + k] : 0;
+            mine[l] = (uint32_t)b < (uint64_t)nbags ? b : 0;
         }
 #pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] = grad[(int64_t)b[q] * LPR + c];
+        for (int k0 = 0; k0 < BWD_CHUNK; k0 += BWD_INFLIGHT) {
+            if (k0 >= n) break;  // uniform within the lane group
+            float4 v[BWD_INFLIGHT];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) acc = f4_add(acc, v[q]);
-    }
-    for (; p < p1; ++p) {
-        int32_t b = sbag[p];
-        b = (uint32_t)b < (uint64_t)nbags ? b : 0;
-        acc = f4_add(acc, grad[(int64_t)b * LPR + c]);
+            for (int q = 0; q < BWD_INFLIGHT; ++q) {
+                const int k = k0 + q;
+                // every lane of the group takes part in the shuffle; only the load is predicated
+                const int32_t b = __shfl(mine[k / LPR], gbase + k % LPR, WAVE);
+                const uint32_t off = (uint32_t)b * (uint32_t)(LPR * 16) + (uint32_t)c * 16u;
+                v[q] = k < n ? *reinterpret_cast<const float4 *>(gbytes + off)
+                             : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+#pragma unroll
+            for (int q = 0; q < BWD_INFLIGHT; ++q) acc = f4_add(acc, v[q]);
+        }
     }
     if (nch > 1) {
         partial[ch * LPR + c] = acc;

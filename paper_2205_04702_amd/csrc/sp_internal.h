@@ -141,7 +141,8 @@ struct SelArgs {
 
 // Positions per backward chunk: one lane group sums at most this many
 // gradient rows before a run is split across groups.
-inline int chunk_positions(int /*dim*/) { return 16; }
+constexpr int BWD_CHUNK = 16;
+inline int chunk_positions(int /*dim*/) { return BWD_CHUNK; }
 
 // ---------------------------------------------------------------- launchers
 // k_ingest.hip

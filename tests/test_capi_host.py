@@ -94,6 +94,7 @@ def _cfg(**over):
     (dict(hold_past=5), "hold_past"),
     (dict(lookahead=12, hold_past=4), "hold_past"),
     (dict(max_table_ids=-1), "max_table_ids"),
+    (dict(dim=256, max_batch=1 << 21), "4 GiB"),  # gradients addressed with 32-bit offsets
 ])
 def test_create_rejects_bad_configs(over, needle):
     cfg, keep = _cfg(**over)

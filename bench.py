@@ -64,6 +64,24 @@ def traffic_from_profile(kernel: str, src_hash: str, workload: str):
     return None
 
 
+def access_ceiling(w, n_rows: int) -> dict | None:
+    """Bare random-row read-modify-write, random-row gather and sequential copy at the
+    workload's shape (Storage slots, distinct rows per step, row width, bags), timed by
+    the ceiling probe built beside the library.  The fraction of these that a training
+    kernel reaches says how close it is to what HBM gives its access pattern."""
+    import subprocess
+    exe = os.path.join(ROOT, "paper_2205_04702_amd", "ceiling")
+    if not os.path.exists(exe):
+        log("[bench] no ceiling probe built; skipping it")
+        return None
+    cmd = [exe, str(sum(w.slots)), str(max(1, n_rows)), str(w.dim), str(w.tables * w.batch), "1024"]
+    r = subprocess.run(cmd, capture_output=True, text=True, timeout=120)
+    if r.returncode != 0:
+        log(f"[bench] ceiling probe failed ({r.returncode}): {r.stderr.strip()}")
+        return None
+    return json.loads(r.stdout.strip().splitlines()[-1])
+
+
 def cpu_baseline(w, seconds: float = 15.0, max_steps: int | None = None) -> dict:
     """The uncached CPU oracle trainer on the same inputs, bounded in time."""
     from oracle import oracle
@@ -115,6 +133,8 @@ def main():
                     help="synchronise the device at the end of every call, so each kernel runs "
                          "alone (kernel times without overlap; throughput is then not the "
                          "pipelined one)")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the access-pattern ceiling probe run after the timed region")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="after the timed region, run a plain elementwise copy (torch.neg) of MIB "
                          "MiB three times: the reference kernel for scaling HBM byte counters")
@@ -279,6 +299,15 @@ def main():
                            "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": tr,
                            "bytes_per_launch": int(kb[dom]),
                            "ms_per_launch": round(fwd_ms if dom == "forward" else bwd_ms, 5)}
+    if not args.no_ceiling and "roofline" in res:
+        ceil = access_ceiling(w, int(round(n_unique)))
+        if ceil:
+            detail["ceiling"] = ceil
+            pat = "gather" if res["roofline"]["kernel"] == "k_forward" else "rmw"
+            c_gbs = ceil[pat]["GBps"]
+            res["roofline"]["pattern_ceiling"] = {
+                "pattern": pat, "GBps": c_gbs, "frac": round(res["roofline"]["achieved"] / c_gbs, 4),
+                "copy_GBps": ceil["copy"]["GBps"]}
     res["detail"] = detail
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle")

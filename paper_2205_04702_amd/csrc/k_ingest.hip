@@ -336,7 +336,11 @@ void launch_radix_sort(uint32_t *k0, uint32_t *v0, uint32_t *k1, uint32_t *v1, i
 
 struct HeadFlag {
     const uint32_t *k;
-    __device__ uint32_t operator()(int64_t i, int) const { return i == 0 || k[i] != k[i - 1]; }
+    __device__ uint32_t operator()(int64_t i, int) const
+    {
+        const uint32_t a = k[i], b = k[i > 0 ? i - 1 : i];  // both loads, no branch
+        return i == 0 || a != b;
+    }
 };
 
 // Segment (run of equal keys) bookkeeping for sorted position i.

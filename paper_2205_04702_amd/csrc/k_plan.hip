@@ -329,10 +329,11 @@ struct VictimFlag {
     int32_t stamp;
     __device__ uint64_t operator()(int64_t g, int y) const
     {
-        if (held[g] == stamp) return 0;
-        uint32_t key = prio(g), vstar = (uint32_t)st[2 * y];
-        if (key < vstar) return 1ull << 32;
-        return key == vstar ? 1ull : 0ull;
+        // every load unconditional (the scan batches them across items)
+        const int32_t h = held[g], src = prio.src[g];
+        const uint32_t key = prio.key(src, g), vstar = (uint32_t)st[2 * y];
+        const uint64_t f = key < vstar ? (1ull << 32) : (key == vstar ? 1ull : 0ull);
+        return h == stamp ? 0ull : f;
     }
 };
 

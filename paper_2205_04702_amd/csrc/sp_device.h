@@ -223,9 +223,14 @@ __global__ void __launch_bounds__(BLOCK) k_scan_lookback(Seg seg, Val val, Out o
     const int64_t i0 = tbase + (int64_t)threadIdx.x * LB_ITEMS;
     T v[LB_ITEMS];
     T sum = 0;
+    // values are read at an index clamped into the segment and masked after:
+    // with no branch around them, every item's loads are in flight together
+    // (val must be branch-free and have no side effects)
 #pragma unroll
     for (int q = 0; q < LB_ITEMS; ++q) {
-        v[q] = i0 + q < end ? val(i0 + q, y) : T(0);
+        const int64_t i = i0 + q;
+        const T x = val(i < end ? i : end - 1, y);
+        v[q] = i < end ? x : T(0);
         sum += v[q];
     }
     T total;

@@ -111,16 +111,17 @@ struct Prio {
     int32_t policy;
     uint32_t u;
     uint64_t seed;
+    // Written without branches, so that loops over slots keep their loads in
+    // flight together: every case is computed and the policy's is selected.
     __host__ __device__ uint32_t key(int32_t v, int64_t g) const
     {
-        if (policy == POLICY_LFU) return (uint32_t)v;
-        if (policy != POLICY_RANDOM) return (uint32_t)(v + 1);
-        if (v < 0) return 0u;
         uint64_t z = seed + (((uint64_t)u << 31) + (uint64_t)g + 1) * 0x9E3779B97F4A7C15ull;
         z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
         z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
         z ^= z >> 31;
-        return 1u + (uint32_t)(z >> 40);
+        const uint32_t rnd = v < 0 ? 0u : 1u + (uint32_t)(z >> 40);
+        const uint32_t other = policy == POLICY_LFU ? (uint32_t)v : (uint32_t)(v + 1);
+        return policy == POLICY_RANDOM ? rnd : other;
     }
     __device__ uint32_t operator()(int64_t g) const { return key(src[g], g); }
 };

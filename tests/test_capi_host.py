@@ -131,3 +131,16 @@ def test_null_handle_calls_report_state_error():
 def test_worst_case_storage_helper_matches_paper():
     """Sec. VI-D: (8 x 20 x 2048 x 128 x 4 B) x 6 = 960 MiB."""
     assert sp.worst_case_scratchpad_bytes(8, 20, 2048, 128, 6) == 960 * 2 ** 20
+
+
+def test_ceiling_probe_is_built_and_checks_its_arguments():
+    """The access-pattern ceiling probe the benchmark runs: built beside the library,
+    it rejects shapes it cannot sample (more rows than slots, odd widths) before
+    touching the GPU."""
+    import subprocess
+    exe = os.path.join(os.path.dirname(sp.__file__), "ceiling")
+    assert os.access(exe, os.X_OK)
+    for args in (["10", "20", "64", "5", "1"], ["100", "20", "12", "5", "1"], ["100", "20", "64", "0", "1"]):
+        r = subprocess.run([exe, *args], capture_output=True, text=True)
+        assert r.returncode == 2 and "bad arguments" in r.stderr
+    assert subprocess.run([exe], capture_output=True).returncode == 2

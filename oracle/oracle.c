@@ -318,6 +318,27 @@ static int32_t orc_find(const int32_t *sorted, int32_t n, int32_t key)
 }
 
 /*
+ * Rows of table t that a prefetching plan also fills (the earlier fill of
+ * future misses that Sec. IV-C's multi-stage overlap allows): the sorted
+ * unique rows of the next batch that are neither cached nor among the
+ * planned batch's rows U (those are filled as its own misses).  Returns the
+ * count; P needs room for the next batch's IDs of table t.
+ */
+static int32_t orc_prefetch_rows(const orc_planner *p, int32_t t, const int32_t *pf_ids,
+                                 const int32_t *pf_off, int32_t B, const int32_t *U, int32_t nu,
+                                 int32_t *P)
+{
+    int32_t j0 = pf_off[(int64_t)t * B], j1 = pf_off[(int64_t)(t + 1) * B];
+    int32_t n = orc_unique_rows(pf_ids, j0, j1, P), k = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        int32_t at = orc_find(U, nu, P[i]);
+        int32_t in_u = at < nu && U[at] == P[i];
+        if (p->slot_of_row[t][P[i]] < 0 && !in_u) P[k++] = P[i];
+    }
+    return k;
+}
+
+/*
  * Held slots of table t for this plan (Sec. IV-C, "Removing RAW-4" and
  * "Putting everything together"): a slot is held when the row it caches is
  * used by any batch of the window (the batch being planned, its visible
@@ -359,6 +380,13 @@ static void orc_mark_held(const orc_planner *p, int32_t t, int32_t nwin,
  * If any table has |M| > |C| the plan fails with ORC_ERR_CAPACITY and no
  * state changes (the worst-case sizing of Sec. IV-D is not met).
  *
+ * Prefetch (orc_planner_plan_pf with a next batch): M is extended, per table,
+ * by the next batch's rows that are neither cached nor in U
+ * (orc_prefetch_rows), ascending, after the planned batch's misses; they take
+ * the next victims in the same order.  A prefetched row is placed with
+ * last_use = u and no use (it is not part of this plan's batch); it has no
+ * slot_of entry.  The capacity check counts both kinds of misses.
+ *
  * Outputs (caller allocates; capacity NNZ of win[0] unless noted, slots are
  * global = slot_base[t] + local slot):
  *   u_table,u_row [nU]   U over all tables, ascending (table, row)
@@ -372,31 +400,39 @@ static void orc_mark_held(const orc_planner *p, int32_t t, int32_t nwin,
  *   slot_of [NNZ]        slot of ids[j] after the plan
  *   counts[3]            nU, nM, number of evictions of occupied slots
  */
-int32_t orc_planner_plan(orc_planner *p, int32_t nwin, const int32_t *const *win_ids,
-                         const int32_t *const *win_off, int32_t B,
-                         int32_t *u_table, int32_t *u_row, int32_t *inv, uint8_t *hit,
-                         int32_t *m_table, int32_t *m_row, int32_t *v_slot,
-                         int32_t *v_old_row, int32_t *v_old_use, int32_t *slot_u,
-                         int32_t *slot_of, int64_t *counts)
+static int32_t orc_batch_valid(const orc_planner *p, const int32_t *ids, const int32_t *off, int32_t B)
+{
+    if (off[0] != 0) return 0;
+    for (int64_t g = 0; g < (int64_t)p->T * B; ++g)
+        if (off[g + 1] < off[g]) return 0;
+    for (int32_t t = 0; t < p->T; ++t)
+        for (int32_t j = off[(int64_t)t * B]; j < off[(int64_t)(t + 1) * B]; ++j)
+            if (ids[j] < 0 || ids[j] >= p->rows[t]) return 0;
+    return 1;
+}
+
+static int32_t orc_plan_core(orc_planner *p, int32_t nwin, const int32_t *const *win_ids,
+                             const int32_t *const *win_off, int32_t B, const int32_t *pf_ids,
+                             const int32_t *pf_off, int32_t *u_table, int32_t *u_row,
+                             int32_t *inv, uint8_t *hit, int32_t *m_table, int32_t *m_row,
+                             int32_t *v_slot, int32_t *v_old_row, int32_t *v_old_use,
+                             int32_t *slot_u, int32_t *slot_of, int64_t *counts)
 {
     const int32_t T = p->T;
     const int32_t *ids = win_ids[0], *off = win_off[0];
     if (nwin < 1) return ORC_ERR_INVALID;
 
-    /* validate every window batch before anything else */
-    for (int32_t w = 0; w < nwin; ++w) {
-        if (win_off[w][0] != 0) return ORC_ERR_INVALID;
-        for (int64_t g = 0; g < (int64_t)T * B; ++g)
-            if (win_off[w][g + 1] < win_off[w][g]) return ORC_ERR_INVALID;
-        for (int32_t t = 0; t < T; ++t)
-            for (int32_t j = win_off[w][(int64_t)t * B]; j < win_off[w][(int64_t)(t + 1) * B]; ++j)
-                if (win_ids[w][j] < 0 || win_ids[w][j] >= p->rows[t]) return ORC_ERR_INVALID;
-    }
+    /* validate every window batch (and the prefetched one) before anything else */
+    for (int32_t w = 0; w < nwin; ++w)
+        if (!orc_batch_valid(p, win_ids[w], win_off[w], B)) return ORC_ERR_INVALID;
+    if (pf_ids && !orc_batch_valid(p, pf_ids, pf_off, B)) return ORC_ERR_INVALID;
 
     int64_t maxS = 0;
     for (int32_t t = 0; t < T; ++t) if (p->slots[t] > maxS) maxS = p->slots[t];
     int32_t nnz = off[(int64_t)T * B];
+    int32_t pf_nnz = pf_ids ? pf_off[(int64_t)T * B] : 0;
     int32_t *U = (int32_t *)malloc(sizeof(int32_t) * (size_t)(nnz > 0 ? nnz : 1));
+    int32_t *P = (int32_t *)malloc(sizeof(int32_t) * (size_t)(pf_nnz > 0 ? pf_nnz : 1));
     uint8_t *held = (uint8_t *)malloc((size_t)(maxS > 0 ? maxS : 1));
     orc_cand *cand = (orc_cand *)malloc(sizeof(orc_cand) * (size_t)(maxS > 0 ? maxS : 1));
     int32_t status = ORC_OK;
@@ -407,13 +443,14 @@ int32_t orc_planner_plan(orc_planner *p, int32_t nwin, const int32_t *const *win
         int32_t nu = orc_unique_rows(ids, j0, j1, U);
         int64_t nmiss = 0, ncand = 0;
         for (int32_t i = 0; i < nu; ++i) nmiss += p->slot_of_row[t][U[i]] < 0;
+        if (pf_ids) nmiss += orc_prefetch_rows(p, t, pf_ids, pf_off, B, U, nu, P);
         orc_mark_held(p, t, nwin, win_ids, win_off, B, held);
         for (int64_t s = 0; s < p->slots[t]; ++s) ncand += !held[s];
         if (nmiss > ncand) status = ORC_ERR_CAPACITY;
     }
 
     /* pass 2: commit */
-    int64_t nU = 0, nM = 0, nEv = 0;
+    int64_t nU = 0, nM = 0, nEv = 0, nPf = 0;
     for (int32_t t = 0; t < T && status == ORC_OK; ++t) {
         int32_t j0 = off[(int64_t)t * B], j1 = off[(int64_t)(t + 1) * B];
         int32_t nu = orc_unique_rows(ids, j0, j1, U);
@@ -431,6 +468,16 @@ int32_t orc_planner_plan(orc_planner *p, int32_t nwin, const int32_t *const *win
                 m_row[mbase + nmiss] = U[i];
                 ++nmiss;
             }
+        const int64_t nown = nmiss;  /* the planned batch's own misses come first */
+        if (pf_ids) {
+            int32_t npf = orc_prefetch_rows(p, t, pf_ids, pf_off, B, U, nu, P);
+            for (int32_t i = 0; i < npf; ++i) {
+                m_table[mbase + nmiss] = t;
+                m_row[mbase + nmiss] = P[i];
+                ++nmiss;
+            }
+            nPf += npf;
+        }
         orc_mark_held(p, t, nwin, win_ids, win_off, B, held);
         int64_t nc = 0;
         for (int64_t s = 0; s < p->slots[t]; ++s)
@@ -453,6 +500,7 @@ int32_t orc_planner_plan(orc_planner *p, int32_t nwin, const int32_t *const *win
             p->key_of_slot[t][v] = m_row[mbase + i];
             p->slot_of_row[t][m_row[mbase + i]] = v;
             p->uses[t][v] = 0;
+            if (i >= nown) p->last_use[t][v] = p->u;  /* prefetched: placed now, not used */
         }
         for (int32_t i = 0; i < nu; ++i) {
             int32_t s = p->slot_of_row[t][U[i]];
@@ -468,10 +516,41 @@ int32_t orc_planner_plan(orc_planner *p, int32_t nwin, const int32_t *const *win
         counts[0] = nU;
         counts[1] = nM;
         counts[2] = nEv;
+        counts[3] = nPf;
         p->u += 1;
     }
     free(cand);
     free(held);
+    free(P);
     free(U);
     return status;
+}
+
+/* Plan without prefetch; counts[3] as described above. */
+int32_t orc_planner_plan(orc_planner *p, int32_t nwin, const int32_t *const *win_ids,
+                         const int32_t *const *win_off, int32_t B,
+                         int32_t *u_table, int32_t *u_row, int32_t *inv, uint8_t *hit,
+                         int32_t *m_table, int32_t *m_row, int32_t *v_slot,
+                         int32_t *v_old_row, int32_t *v_old_use, int32_t *slot_u,
+                         int32_t *slot_of, int64_t *counts)
+{
+    int64_t c4[4] = {0, 0, 0, 0};
+    int32_t st = orc_plan_core(p, nwin, win_ids, win_off, B, NULL, NULL, u_table, u_row, inv, hit,
+                               m_table, m_row, v_slot, v_old_row, v_old_use, slot_u, slot_of, c4);
+    if (st == ORC_OK) memcpy(counts, c4, sizeof(int64_t) * 3);
+    return st;
+}
+
+/* Plan that also prefetches the next batch (pf_ids/pf_off, NULL for none);
+ * m_* and v_* need room for the NNZ of both batches; counts[4] = nU, nM
+ * (prefetched included), evictions, prefetched rows. */
+int32_t orc_planner_plan_pf(orc_planner *p, int32_t nwin, const int32_t *const *win_ids,
+                            const int32_t *const *win_off, int32_t B, const int32_t *pf_ids,
+                            const int32_t *pf_off, int32_t *u_table, int32_t *u_row,
+                            int32_t *inv, uint8_t *hit, int32_t *m_table, int32_t *m_row,
+                            int32_t *v_slot, int32_t *v_old_row, int32_t *v_old_use,
+                            int32_t *slot_u, int32_t *slot_of, int64_t *counts)
+{
+    return orc_plan_core(p, nwin, win_ids, win_off, B, pf_ids, pf_off, u_table, u_row, inv, hit,
+                         m_table, m_row, v_slot, v_old_row, v_old_use, slot_u, slot_of, counts);
 }

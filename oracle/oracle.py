@@ -56,6 +56,10 @@ def lib():
         L.orc_planner_step.restype = C.c_int32
         L.orc_planner_state.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
                                         C.c_void_p]
+        L.orc_planner_plan_pf.restype = C.c_int32
+        L.orc_planner_plan_pf.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_int32,
+                                          _i32p, _i32p, _i32p, _i32p, _i32p, _u8p, _i32p, _i32p,
+                                          _i32p, _i32p, _i32p, _i32p, _i32p, _i64p]
         L.orc_planner_plan.restype = C.c_int32
         L.orc_planner_plan.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_int32,
                                        _i32p, _i32p, _i32p, _u8p, _i32p, _i32p, _i32p, _i32p,
@@ -124,25 +128,28 @@ class PlanResult:
     """One plan's decisions; field meanings follow orc_planner_plan."""
 
     __slots__ = ("u_table", "u_row", "inv", "hit", "m_table", "m_row", "v_slot", "v_old_row",
-                 "v_old_use", "slot_u", "slot_of", "n_evict")
+                 "v_old_use", "slot_u", "slot_of", "n_evict", "n_prefetch")
 
     def keys(self):
-        return [s for s in self.__slots__ if s != "n_evict"]
+        return [s for s in self.__slots__ if s not in ("n_evict", "n_prefetch")]
 
 
 class Planner:
     """Reference planner (O2).  plan() returns a PlanResult or raises PlanError.
 
     policy: "lru" (the default of Sec. VI-E), "lfu" or "random"; seed feeds the
-    random policy's draws.
+    random policy's draws.  prefetch: each plan also fills the rows of the first
+    successor batch of its window that are neither cached nor in the planned
+    batch (orc_planner_plan_pf); they follow the planned batch's misses, per table.
     """
 
-    def __init__(self, rows, slots, policy: str = "lru", seed: int = 0):
+    def __init__(self, rows, slots, policy: str = "lru", seed: int = 0, prefetch: bool = False):
         self.T = len(rows)
         self.rows = np.asarray(rows, dtype=np.int64)
         self.slots = np.asarray(slots, dtype=np.int64)
         self.slot_base = np.concatenate([[0], np.cumsum(self.slots)]).astype(np.int64)
         self.policy, self.seed = policy, int(seed)
+        self.prefetch = bool(prefetch)
         self._h = lib().orc_planner_create(self.T, self.rows, self.slots, POLICIES[policy],
                                            C.c_uint64(self.seed))
 
@@ -171,23 +178,34 @@ class Planner:
     def plan(self, window, B: int, past=()) -> PlanResult:
         """window: list of (ids, bag_off) for the planned batch and its visible successors;
         past: earlier batches whose cached rows are held as well (the past window)."""
+        pf = window[1] if self.prefetch and len(window) >= 2 else None
         window = list(window) + list(past)
         ids_l = [np.ascontiguousarray(w[0], np.int32) for w in window]
         off_l = [np.ascontiguousarray(w[1], np.int32) for w in window]
         nnz = int(off_l[0][-1])
         cap = max(nnz, 1)
+        mcap = cap + (int(ids_l[1].size) if pf is not None else 0)
         r = PlanResult()
         r.u_table, r.u_row, r.inv = (np.empty(cap, np.int32) for _ in range(3))
         r.hit = np.empty(cap, np.uint8)
-        (r.m_table, r.m_row, r.v_slot, r.v_old_row, r.v_old_use, r.slot_u,
-         r.slot_of) = (np.empty(cap, np.int32) for _ in range(7))
-        counts = np.zeros(3, np.int64)
-        st = lib().orc_planner_plan(self._h, len(window), _ptr_array(ids_l), _ptr_array(off_l), B,
-                                    r.u_table, r.u_row, r.inv, r.hit, r.m_table, r.m_row, r.v_slot,
-                                    r.v_old_row, r.v_old_use, r.slot_u, r.slot_of, counts)
+        r.slot_u, r.slot_of = np.empty(cap, np.int32), np.empty(cap, np.int32)
+        (r.m_table, r.m_row, r.v_slot, r.v_old_row,
+         r.v_old_use) = (np.empty(mcap, np.int32) for _ in range(5))
+        counts = np.zeros(4, np.int64)
+        if pf is None:
+            st = lib().orc_planner_plan(self._h, len(window), _ptr_array(ids_l), _ptr_array(off_l),
+                                        B, r.u_table, r.u_row, r.inv, r.hit, r.m_table, r.m_row,
+                                        r.v_slot, r.v_old_row, r.v_old_use, r.slot_u, r.slot_of,
+                                        counts)
+        else:
+            st = lib().orc_planner_plan_pf(self._h, len(window), _ptr_array(ids_l),
+                                           _ptr_array(off_l), B, ids_l[1], off_l[1], r.u_table,
+                                           r.u_row, r.inv, r.hit, r.m_table, r.m_row, r.v_slot,
+                                           r.v_old_row, r.v_old_use, r.slot_u, r.slot_of, counts)
         if st != OK:
             raise PlanError(st)
         nU, nM = int(counts[0]), int(counts[1])
+        r.n_prefetch = int(counts[3])
         for f in ("u_table", "u_row", "hit", "slot_u"):
             setattr(r, f, getattr(r, f)[:nU].copy())
         for f in ("m_table", "m_row", "v_slot", "v_old_row", "v_old_use"):
@@ -213,11 +231,11 @@ class CachedSimulator:
     """
 
     def __init__(self, host_tables, slots, check_residency: bool = True, policy: str = "lru",
-                 seed: int = 0):
+                 seed: int = 0, prefetch: bool = False):
         self.host = host_tables
         self.D = host_tables[0].shape[1]
         rows = [t.shape[0] for t in host_tables]
-        self.planner = Planner(rows, slots, policy, seed)
+        self.planner = Planner(rows, slots, policy, seed, prefetch)
         self.storage = np.zeros((int(self.planner.slot_base[-1]), self.D), np.float32)
         self.check = check_residency
         self.writebacks = 0

@@ -1,0 +1,260 @@
+"""Pins for the oracle planner's prefetch mode (earlier fill of future misses).
+
+With prefetch, a plan also fills the rows of the first successor batch of its
+window that are neither cached nor in the planned batch (the multi-stage
+overlap of Sec. IV-C lets a row be brought in before the batch that needs it
+is planned).  Nothing here re-implements the planner: each plan is checked
+against properties recomputed from the state before it:
+  * the planned batch's dedup, hits and misses are unchanged by prefetching;
+  * the misses are, per table, the planned batch's misses ascending, then the
+    next batch's rows that are neither cached nor planned, ascending (set
+    arithmetic with numpy);
+  * victims are the smallest unheld (last use, slot) and no window row is
+    evicted (as without prefetch);
+  * after the plan every row of both the planned and the next batch is cached;
+  * prefetched slots carry the plan's index as last use; slots of the planned
+    batch are touched; all others keep their last use;
+  * the capacity check counts both kinds of misses (independent count);
+  * the next plan of the same stream of batches has no misses of its own;
+  * with slots >= rows every row is filled exactly once, at the first plan
+    that sees it in its planned or next batch (closed form);
+  * with no successor in the window (lookahead 0) prefetch changes nothing;
+  * scratchpad training with prefetch equals uncached training bit for bit.
+"""
+import itertools
+
+import numpy as np
+import pytest
+
+from paper_2205_04702_amd import workload as wl
+
+
+def snapshot(planner):
+    return [planner.state(t) for t in range(planner.T)]
+
+
+def rows_of(batch, t, B):
+    ids, off = batch
+    return np.asarray(ids[int(off[t * B]):int(off[(t + 1) * B])])
+
+
+def expected_misses(pre, window, B, t):
+    """(own misses, prefetched rows) of table t from the state before the plan."""
+    sor0 = pre[t][2]
+    U = np.unique(rows_of(window[0], t, B))
+    own = U[sor0[U] < 0]
+    if len(window) < 2:
+        return own, np.zeros(0, own.dtype)
+    nxt = np.unique(rows_of(window[1], t, B))
+    pf = nxt[(sor0[nxt] < 0) & ~np.isin(nxt, U)]
+    return own, pf
+
+
+def capacity_short_pf(planner, pre, window, B):
+    for t in range(planner.T):
+        own, pf = expected_misses(pre, window, B, t)
+        sor0 = pre[t][2]
+        win_rows = set()
+        for b in window:
+            win_rows.update(int(r) for r in rows_of(b, t, B))
+        held = {int(sor0[r]) for r in win_rows if sor0[r] >= 0}
+        if own.size + pf.size > int(planner.slots[t]) - len(held):
+            return True
+    return False
+
+
+def check_plan_pf(planner, pre, post, window, B, p, u):
+    T = planner.T
+    base = planner.slot_base
+    u_off = m_off = 0
+    for t in range(T):
+        kos0, lu0, sor0 = pre[t]
+        kos1, lu1, sor1 = post[t]
+        S = int(planner.slots[t])
+        rows_b = rows_of(window[0], t, B)
+        U = np.unique(rows_b)
+        nU = U.size
+        assert np.array_equal(p.u_row[u_off:u_off + nU], U)
+        assert np.array_equal(p.hit[u_off:u_off + nU].astype(bool), sor0[U] >= 0)
+        own, pf = expected_misses(pre, window, B, t)
+        k = own.size + pf.size
+        assert np.array_equal(p.m_table[m_off:m_off + k], np.full(k, t))
+        assert np.array_equal(p.m_row[m_off:m_off + own.size], own)
+        assert np.array_equal(p.m_row[m_off + own.size:m_off + k], pf)
+        win_rows = set()
+        for b in window:
+            win_rows.update(int(r) for r in rows_of(b, t, B))
+        held = {int(sor0[r]) for r in win_rows if sor0[r] >= 0}
+        cand = sorted((int(lu0[s]), s) for s in range(S) if s not in held)
+        victims = [int(v) - int(base[t]) for v in p.v_slot[m_off:m_off + k]]
+        assert [(int(lu0[v]), v) for v in victims] == cand[:k]
+        assert np.array_equal(p.v_old_row[m_off:m_off + k], kos0[victims])
+        for old in kos0[victims]:
+            assert old < 0 or int(old) not in win_rows, "evicted a held row"
+        for i, v in enumerate(victims):
+            assert kos1[v] == p.m_row[m_off + i] and sor1[p.m_row[m_off + i]] == v
+        # both batches resident afterwards
+        assert np.all(sor1[rows_b] >= 0)
+        if len(window) > 1:
+            assert np.all(sor1[rows_of(window[1], t, B)] >= 0)
+        local = p.slot_of[int(window[0][1][t * B]):int(window[0][1][(t + 1) * B])] - int(base[t])
+        assert np.array_equal(kos1[local], rows_b)
+        touched = np.zeros(S, bool)
+        touched[sor1[U]] = True
+        pf_slots = np.asarray(victims[own.size:], np.int64)
+        assert np.all(lu1[touched] == u)
+        assert np.all(lu1[pf_slots] == u)
+        rest = ~touched
+        rest[pf_slots] = False
+        assert np.array_equal(lu1[rest], lu0[rest])
+        occ = np.nonzero(kos1 >= 0)[0]
+        assert np.array_equal(sor1[kos1[occ]], occ)
+        u_off += nU
+        m_off += k
+    assert m_off == p.m_row.size
+    assert p.n_prefetch == sum(expected_misses(pre, window, B, t)[1].size for t in range(T))
+
+
+def run_checked_pf(oracle, w, batches, past=0):
+    planner = oracle.Planner(w.rows, w.slots, prefetch=True)
+    n = len(batches)
+    for u in range(n):
+        win = [batches[q] for q in range(u, min(u + w.lookahead, n - 1) + 1)]
+        pre = snapshot(planner)
+        short = capacity_short_pf(planner, pre, win, w.batch)
+        try:
+            p = planner.plan(win, w.batch)
+        except oracle.PlanError as e:
+            assert e.status == oracle.ERR_CAPACITY and short
+            assert all(np.array_equal(x, y) for a, b in zip(pre, snapshot(planner)) for x, y in zip(a, b))
+            return False
+        assert not short
+        check_plan_pf(planner, pre, snapshot(planner), win, w.batch, p, u)
+    return True
+
+
+@pytest.mark.parametrize("case", range(8))
+def test_random_runs_hold_every_property(oracle, case):
+    rng = np.random.default_rng(700 + case)
+    T = int(rng.integers(1, 4))
+    rows = [int(rng.integers(20, 120)) for _ in range(T)]
+    L = int(rng.integers(1, 4))
+    B = int(rng.integers(2, 7))
+    P = [int(rng.integers(1, 4)) for _ in range(T)]
+    slots = [min(r, (L + 2) * B * p + int(rng.integers(0, 20))) for r, p in zip(rows, P)]
+    dist = tuple(("zipf", 1.1) if rng.random() < 0.5 else ("uniform",) for _ in range(T))
+    w = wl.custom(rows=rows, dim=4, batch=B, pooling=P, slots=slots, lookahead=L, steps=25,
+                  dist=dist, seed=case)
+    batches = [wl.batch(w, s) for s in range(w.steps)]
+    assert run_checked_pf(oracle, w, batches)
+
+
+def test_exhaustive_tiny_spaces(oracle):
+    """Every sequence of three single-table batches over 3 rows, every slot count and
+    lookahead 0-2, with prefetch: each plan satisfies every property or fails for
+    capacity exactly when the independent count says it must."""
+    bags = [(a,) for a in range(3)] + list(itertools.product(range(3), repeat=2))
+    runs = failed = 0
+    for seq in itertools.product(bags, repeat=3):
+        batches = [(np.array(b, np.int32), np.array([0, len(b)], np.int32)) for b in seq]
+        for S in (1, 2, 3):
+            for L in (0, 1, 2):
+                w = wl.custom(rows=[3], dim=1, batch=1, pooling=1, slots=[S], lookahead=L,
+                              steps=3)
+                ok = run_checked_pf(oracle, w, batches)
+                runs += 1
+                failed += not ok
+    assert runs == 12 ** 3 * 9 and 0 < failed < runs
+
+
+def test_next_plan_has_no_misses_of_its_own(oracle):
+    w = wl.custom(rows=[200, 300], dim=4, batch=6, pooling=[3, 2], slots=[80, 90], lookahead=2,
+                  steps=20, dist=(("zipf", 1.05), ("uniform",)), seed=5)
+    batches = [wl.batch(w, s) for s in range(w.steps)]
+    planner = oracle.Planner(w.rows, w.slots, prefetch=True)
+    prefetched = 0
+    for u in range(w.steps):
+        p = planner.plan(batches[u:u + w.lookahead + 1], w.batch)
+        if u > 0:
+            assert p.hit.all(), "a row of the planned batch was not prefetched"
+        prefetched += p.n_prefetch
+    assert prefetched > 0
+
+
+def test_enough_slots_fills_each_row_once_at_first_sight(oracle):
+    """slots >= rows: plan u fills exactly the rows first seen in batch u or u+1."""
+    w = wl.custom(rows=[50, 80], dim=2, batch=8, pooling=3, slots=[50, 80], lookahead=2,
+                  steps=15, dist=("zipf", 1.0), seed=9)
+    planner = oracle.Planner(w.rows, w.slots, prefetch=True)
+    batches = [wl.batch(w, s) for s in range(w.steps)]
+    seen = [set() for _ in range(w.tables)]
+    for u in range(w.steps):
+        p = planner.plan(batches[u:u + w.lookahead + 1], w.batch)
+        expect = []
+        for t in range(w.tables):
+            cur = set(int(r) for r in rows_of(batches[u], t, w.batch))
+            nxt = set(int(r) for r in rows_of(batches[u + 1], t, w.batch)) if u + 1 < w.steps else set()
+            expect += [(t, r) for r in sorted(cur - seen[t])]
+            expect += [(t, r) for r in sorted(nxt - cur - seen[t])]
+            seen[t] |= cur | nxt
+        assert list(zip(p.m_table.tolist(), p.m_row.tolist())) == expect
+        assert p.n_evict == 0
+
+
+def test_without_a_successor_prefetch_changes_nothing(oracle):
+    """Lookahead 0: the window has no next batch, so every plan equals the plain one."""
+    w = wl.custom(rows=[60, 40], dim=2, batch=5, pooling=[2, 3], slots=[20, 25], lookahead=0,
+                  steps=20, dist=(("zipf", 1.05), ("uniform",)), seed=4)
+    batches = [wl.batch(w, s) for s in range(w.steps)]
+    a = oracle.Planner(w.rows, w.slots)
+    b = oracle.Planner(w.rows, w.slots, prefetch=True)
+    for u in range(w.steps):
+        pa, pb = a.plan(batches[u:u + 1], w.batch), b.plan(batches[u:u + 1], w.batch)
+        for f in pa.keys():
+            assert np.array_equal(getattr(pa, f), getattr(pb, f)), f
+        assert pb.n_prefetch == 0
+
+
+def test_capacity_counts_prefetched_rows(oracle):
+    # one table of 4 slots: batch {0,1} with next batch {2,3} fits exactly; next {2,3,4} does not
+    planner = oracle.Planner([10], [4], prefetch=True)
+    b01 = (np.array([0, 1], np.int32), np.array([0, 2], np.int32))
+    b23 = (np.array([2, 3], np.int32), np.array([0, 2], np.int32))
+    b234 = (np.array([2, 3, 4], np.int32), np.array([0, 3], np.int32))
+    pre = snapshot(planner)
+    with pytest.raises(oracle.PlanError) as e:
+        planner.plan([b01, b234], 1)
+    assert e.value.status == oracle.ERR_CAPACITY
+    assert all(np.array_equal(x, y) for a, b in zip(pre, snapshot(planner)) for x, y in zip(a, b))
+    p = planner.plan([b01, b23], 1)
+    assert p.m_row.tolist() == [0, 1, 2, 3] and p.n_prefetch == 2
+    assert p.v_slot.tolist() == [0, 1, 2, 3]
+    # the prefetched rows are hits for the next plan, and nothing is filled
+    p = planner.plan([b23], 1)
+    assert p.hit.all() and p.m_row.size == 0
+
+
+@pytest.mark.parametrize("name,slots,L,ragged", [
+    ("small-cache", [30, 40], 1, False),
+    ("deep-window", [60, 70], 3, False),
+    ("ragged", [45, 55], 2, True),
+    ("no-lookahead", [16, 20], 0, False),
+])
+def test_cached_training_equals_uncached_bit_for_bit(oracle, name, slots, L, ragged):
+    w = wl.custom(rows=[100, 150], dim=6, batch=5, pooling=[2, 3], slots=slots, lookahead=L,
+                  steps=30, dist=(("zipf", 1.05), ("uniform",)), seed=11)
+    batches = [wl.ragged_batch(w, s, 5) if ragged else wl.batch(w, s) for s in range(w.steps)]
+    plain = [wl.init_table(w, t) for t in range(w.tables)]
+    host = [t.copy() for t in plain]
+    sim = oracle.CachedSimulator(host, w.slots, prefetch=True)
+    pf = 0
+    for u in range(w.steps):
+        g = wl.grads(w, u)
+        o_plain = oracle.train_step(plain, *batches[u], w.batch, g, w.lr, want_out=True)
+        p, o_sim = sim.step(batches[u:u + L + 1], w.batch, g, w.lr, want_out=True)
+        pf += p.n_prefetch
+        assert np.array_equal(o_plain, o_sim)
+    sim.flush()
+    for t in range(w.tables):
+        assert np.array_equal(plain[t], host[t])
+    assert (pf > 0) == (L > 0)

@@ -100,6 +100,15 @@ typedef struct {
                                    max_batch both <= 8192 each table of a batch is
                                    sorted and deduplicated by one workgroup in LDS,
                                    the whole batch in one launch                    */
+    int32_t prefetch;           /* 0, or 1: each plan also fills the rows of the next
+                                   batch of its window (window[1], when lookahead >= 1
+                                   and it is given) that are neither cached nor in the
+                                   planned batch: the earlier fill of future misses
+                                   that the multi-stage overlap of Sec. IV-C allows.
+                                   Per table the planned batch's misses come first,
+                                   then the prefetched rows, each ascending; the
+                                   capacity check counts both, so SP_ERR_CAPACITY can
+                                   come one plan earlier than without prefetch      */
 } sp_config;
 
 typedef struct {
@@ -144,6 +153,10 @@ typedef struct {
     /* host time, in ms, that sp_plan spends before returning waiting until its
      * ingests have read the caller's window arrays */
     double host_ms_inputs;
+    /* prefetch mode: rows filled for the next batch (included in misses,
+     * evictions and bytes_fill, not in hits: hits count the planned batch's
+     * keys found cached, prefetched ones included) */
+    int64_t prefetched;
 } sp_stats;
 
 /* Per-plan decisions copied to the host for checking.  The caller allocates
@@ -158,7 +171,11 @@ typedef struct {
  *                                        slot each one gets, the row evicted
  *                                        from it (-1 if none) and that slot's
  *                                        previous last-use plan index (-1 if
- *                                        never used) */
+ *                                        never used).  In prefetch mode these
+ *                                        hold, per table, the planned batch's
+ *                                        misses then the prefetched rows, and
+ *                                        need room for the nnz of the planned
+ *                                        and the next batch together */
 typedef struct {
     int32_t *u_table, *u_row, *inv, *m_table, *m_row, *v_slot, *v_old_row, *v_old_use;
     int32_t *slot_u, *slot_of;

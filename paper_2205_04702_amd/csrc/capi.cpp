@@ -257,6 +257,10 @@ struct sp_ctx {
     float *storage = nullptr;
     int32_t *key_of_slot = nullptr, *last_use = nullptr, *held = nullptr;
     int32_t *uses = nullptr;  // per-slot use counts, LFU only
+    bool prefetch = false;    // plans also fill the next batch's missing rows
+    uint32_t *pf_own_key = nullptr;  // prefetch mode: the planned batch's own misses,
+    int32_t *pf_own_uidx = nullptr;  // as the query compacts them
+    int32_t *pf_flag = nullptr;      // next batch's unique keys to prefetch
     uint64_t *hash = nullptr;
     uint32_t hash_mask = 0;
     int64_t hash_used = 0;
@@ -516,6 +520,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     h->L = c->lookahead;
     h->policy = c->policy;
     h->P = c->hold_past;
+    h->prefetch = c->prefetch != 0;
     h->seed = c->seed;
     h->device = c->device;
     h->flags = c->flags;
@@ -554,6 +559,8 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     }
 
     const int64_t S = h->total_slots, N = h->max_ids, TB1 = (int64_t)T * h->max_batch + 1;
+    // misses of one plan: the planned batch's, plus the next batch's when prefetching
+    const int64_t NM = h->prefetch ? 2 * N : N;
     const int64_t nchunk_max = N + N / h->chunk + 1;
     h->nchunk_max = nchunk_max;
     TRY(dalloc(h, &h->storage, S * h->D));
@@ -604,11 +611,11 @@ static sp_status build(sp_ctx *h, const sp_config *c)
         TRY(dalloc(h, &t.hit, N));
         TRY(dalloc(h, &t.slot_u, N));
         TRY(dalloc(h, &t.slot_of, N));
-        TRY(dalloc(h, &t.m_key, N));
-        TRY(dalloc(h, &t.m_uidx, N));
-        TRY(dalloc(h, &t.v_slot, N));
-        TRY(dalloc(h, &t.v_old_key, N));
-        TRY(dalloc(h, &t.v_old_lu, N));
+        TRY(dalloc(h, &t.m_key, NM));
+        TRY(dalloc(h, &t.m_uidx, NM));
+        TRY(dalloc(h, &t.v_slot, NM));
+        TRY(dalloc(h, &t.v_old_key, NM));
+        TRY(dalloc(h, &t.v_old_lu, NM));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_planned[k], hipEventDisableTiming));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_filled[k], hipEventDisableTiming));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_upd[k], hipEventDisableTiming));
@@ -617,18 +624,23 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     TRY(dalloc(h, &h->tmp_v, N));
     TRY(dalloc(h, &h->itmp_k, N));
     TRY(dalloc(h, &h->itmp_v, N));
-    TRY(dalloc(h, &h->vk0, N));
-    TRY(dalloc(h, &h->vv0, N));
-    TRY(dalloc(h, &h->vk1, N));
-    TRY(dalloc(h, &h->hist, radix_hist_entries(N)));
+    TRY(dalloc(h, &h->vk0, NM));
+    TRY(dalloc(h, &h->vv0, NM));
+    TRY(dalloc(h, &h->vk1, NM));
+    TRY(dalloc(h, &h->hist, radix_hist_entries(NM)));
+    if (h->prefetch) {
+        TRY(dalloc(h, &h->pf_own_key, N));
+        TRY(dalloc(h, &h->pf_own_uidx, N));
+        TRY(dalloc(h, &h->pf_flag, N));
+    }
     TRY(dalloc(h, &h->ihist, radix_hist_entries(N)));
     TRY(dalloc(h, &h->cnt, 1));
-    TRY(dalloc(h, &h->cnt_part, (int64_t)PART_COPIES * 2 * MAX_TABLES + 1));
+    TRY(dalloc(h, &h->cnt_part, (int64_t)PART_COPIES * PART_WORDS + 1));
     {
         // scans: victims (tables x slots per table), misses and batches (N),
         // radix histogram tables (at most N + 2048 entries)
         // (and the query's tiles of unique keys)
-        const int64_t tiles = std::max({scan_tiles(T, h->maxS), scan_tiles(1, N + 4096),
+        const int64_t tiles = std::max({scan_tiles(T, h->maxS), scan_tiles(1, NM + 4096),
                                         (N + QUERY_TILE - 1) / QUERY_TILE}) + 2;
         for (ScanWs *ws : {&h->ws_plan, &h->ws_ingest}) {
             ws->max_tiles = tiles;
@@ -640,7 +652,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     TRY(dalloc(h, &h->sel_state, 3 * MAX_TABLES));  // v* prefix, slots to take, arrivals
     TRY(dalloc(h, &h->sel_hist, (int64_t)MAX_TABLES * SEL_BINS));
     TRY(dalloc(h, &h->partial, nchunk_max * h->D));
-    h->stage_rows = std::min<int64_t>(N, S);
+    h->stage_rows = std::min<int64_t>(NM, S);
     for (int i = 0; i < NSTAGE; ++i) {
         TRY(dalloc(h, &h->stage_dev[i], h->stage_rows * (h->D + 1)));
         TRY(palloc(h, &h->stage_host[i], h->stage_rows * (h->D + 1)));
@@ -687,7 +699,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     HIPCHK(nullptr, hipMemsetAsync(h->sel_hist, 0, sizeof(int32_t) * MAX_TABLES * SEL_BINS, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->sel_state, 0, sizeof(int32_t) * 3 * MAX_TABLES, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->cnt, 0, sizeof(DevCounters), h->s_plan));
-    HIPCHK(nullptr, hipMemsetAsync(h->cnt_part, 0, sizeof(int32_t) * (PART_COPIES * 2 * MAX_TABLES + 1), h->s_plan));
+    HIPCHK(nullptr, hipMemsetAsync(h->cnt_part, 0, sizeof(int32_t) * (PART_COPIES * PART_WORDS + 1), h->s_plan));
     for (ScanWs *ws : {&h->ws_plan, &h->ws_ingest}) {
         HIPCHK(nullptr, hipMemsetAsync(ws->status, 0, sizeof(uint64_t) * LB_WORDS * ws->max_tiles, h->s_plan));
         HIPCHK(nullptr, hipMemsetAsync(ws->counter, 0, sizeof(uint32_t), h->s_plan));
@@ -717,6 +729,7 @@ extern "C" sp_status sp_create(const sp_config *c, sp_handle *out)
         return fail(nullptr, SP_ERR_INVALID_ARG, "hold_past %d not in 0..%d with lookahead + 1 + hold_past <= %d",
                     c->hold_past, SP_MAX_HOLD_PAST, MAX_WINDOW);
     if (c->max_table_ids < 0) return fail(nullptr, SP_ERR_INVALID_ARG, "max_table_ids %lld < 0", (long long)c->max_table_ids);
+    if (c->prefetch != 0 && c->prefetch != 1) return fail(nullptr, SP_ERR_INVALID_ARG, "prefetch %d not 0 or 1", c->prefetch);
     if (c->max_batch < 0 || c->max_ids < 0 || c->max_ids > INT32_MAX - 1)
         return fail(nullptr, SP_ERR_INVALID_ARG, "bad max_batch / max_ids");
     if ((int64_t)T * c->max_batch + 1 > INT32_MAX) return fail(nullptr, SP_ERR_INVALID_ARG, "too many bags");
@@ -968,8 +981,10 @@ static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, int32_t *stamp_o
     }
     const int32_t stamp = ++h->stamp;
     *seq_out = ++h->qseq;
+    const PrefetchDev pf{(int32_t)(h->prefetch && nhold >= 2), h->pf_own_key, h->pf_own_uidx,
+                         h->pf_flag};
     launch_query(h->tb, h->hash, h->hash_mask, ukeys, nuniq, nwin, max_nnz, h->held, stamp,
-                 h->tk[e], h->cnt, h->cnt_part, h->cnt_part + PART_COPIES * 2 * MAX_TABLES,
+                 h->tk[e], pf, h->cnt, h->cnt_part, h->cnt_part + PART_COPIES * PART_WORDS,
                  h->ring[k % h->nring].scal, h->h_cnt_dev, *seq_out, h->ws_plan, h->s_plan);
     CHECK_LAUNCH(h);
     if (h->ws_plan.overflow) return fail(h, SP_ERR_HIP, "internal: scan workspace too small");
@@ -1055,17 +1070,23 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     if (c.err_sticky)
         return fail(h, SP_ERR_HIP, "internal planner inconsistency (flags %d) in an earlier plan",
                     c.err_sticky);
-    int64_t n_miss = 0, margin = INT64_MAX;
+    // prefetch mode: the next batch's rows to fetch count as misses too
+    const bool pf_on = h->prefetch && nhold >= 2;
+    if (!pf_on)
+        for (int t = 0; t < h->T; ++t) c.pf[t] = 0;
+    int64_t n_miss = 0, n_own = 0, margin = INT64_MAX;
     for (int t = 0; t < h->T; ++t) {
         const int64_t free_slots = h->slots[t] - c.held[t];
-        margin = std::min<int64_t>(margin, free_slots - c.miss[t]);
-        if (c.miss[t] > free_slots) {
+        const int64_t need = (int64_t)c.miss[t] + c.pf[t];
+        margin = std::min<int64_t>(margin, free_slots - need);
+        if (need > free_slots) {
             for (int w = 0; w < n; ++w) h->ring_batch[(k + w) % h->nring] = -1;  // re-read on retry
             return fail(h, SP_ERR_CAPACITY,
-                        "table %d: %d misses but only %lld unheld slots (plan %lld)", t, c.miss[t],
-                        (long long)free_slots, (long long)k);
+                        "table %d: %lld misses (%d to prefetch) but only %lld unheld slots (plan %lld)",
+                        t, (long long)need, c.pf[t], (long long)free_slots, (long long)k);
         }
-        n_miss += c.miss[t];
+        n_miss += need;
+        n_own += c.miss[t];
     }
 
     // ---- phase 2: commit
@@ -1092,16 +1113,16 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
         int32_t vb = 0;
         int64_t maxS = 0;
         for (int t = 0; t < h->T; ++t) {
-            if (c.miss[t] > 0) {
+            if (c.miss[t] + c.pf[t] > 0) {
                 int y = a.nact++;
                 a.t[y] = t;
-                a.k[y] = c.miss[t];
+                a.k[y] = c.miss[t] + c.pf[t];
                 a.base[y] = h->tb.slot_base[t];
                 a.S[y] = h->slots[t];
                 a.vbase[y] = vb;
                 maxS = std::max<int64_t>(maxS, h->slots[t]);
             }
-            vb += c.miss[t];
+            vb += c.miss[t] + c.pf[t];
         }
         // priority values: LRU last use + 1 <= u, LFU uses <= u + 1, random <= 2^24
         const int nb = h->policy == POLICY_RANDOM ? 25
@@ -1114,9 +1135,17 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
         launch_select_victims(a, levels, maxS, h->held, h->sel_state, h->sel_hist, h->vk0,
                               h->vv0, h->vk1, (uint32_t *)nullptr, n_miss, h->hist, h->ws_plan,
                               tk.v_slot, &h->cnt->err_sticky, h->s_plan);
+        if (pf_on) {
+            // the miss list in victim order: per table own misses, then the next
+            // batch's rows to prefetch (the query left the own misses aside)
+            const int r1 = (int)((k + 1) % h->nring);
+            launch_pf_arrange(h->tb, PrefetchDev{1, h->pf_own_key, h->pf_own_uidx, h->pf_flag},
+                              n_own, h->ring[r1].scal, h->ring_nnz[r1], h->ring[r1].ukeys, c.miss,
+                              c.pf, tk, n_miss, &h->cnt->err_sticky, h->ws_plan, h->s_plan);
+        }
     }
     launch_commit(h->tb, h->hash, h->hash_mask, tk, b0, n_miss, th.n_unique, th.nnz, h->key_of_slot,
-                  h->last_use, h->uses, u, h->cnt, h->s_plan);
+                  h->last_use, h->uses, u, pf_on, h->cnt, h->s_plan);
     CHECK_LAUNCH(h);
     if (h->ws_plan.overflow) return fail(h, SP_ERR_HIP, "internal: scan workspace too small");
     HIPCHK(h, hipStreamWriteValue64(h->s_plan, h->sem + SEM_PLANNED, (uint64_t)k + 1, 0));
@@ -1143,6 +1172,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     // ---- mover (own stream): write-back of evicted rows and fill of misses;
     // the next plan's query does not wait for it
     // RAW-4: rows evicted by plan p may be refilled from plan p + n_p on
+    // (n_p - 1 with prefetch, which fills the batch after the planned one)
     int64_t need = -1;
     for (const auto &d : h->deadlines)
         if (d.second <= k) need = std::max(need, d.first);
@@ -1188,7 +1218,10 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     TRY(issue_copy(h, h->s_copy));
     h->copy_pending = k;
     h->copy_n = n_miss;
-    h->deadlines.emplace_back(k, k + nhold);
+    // an evicted row is in no batch of this plan's window, so the first plan
+    // that can fill it again is the one whose planned batch (or, prefetching,
+    // next batch) is the first after the window
+    h->deadlines.emplace_back(k, k + nhold - (pf_on ? 1 : 0));
 
     h->host_ms[4] += host_ms() - tF;
     h->planned = k + 1;
@@ -1196,7 +1229,8 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     h->st.lookups += th.nnz;
     h->st.unique += th.n_unique;
     h->st.misses += n_miss;
-    h->st.hits += th.n_unique - n_miss;
+    h->st.hits += th.n_unique - n_own;
+    h->st.prefetched += n_miss - n_own;
     h->st.bytes_fill += n_miss * h->D * (int64_t)sizeof(float);
     h->st.min_capacity_margin = std::min(h->st.min_capacity_margin, margin);
     if (ticket) *ticket = k;
@@ -1339,6 +1373,7 @@ extern "C" sp_status sp_get_stats(sp_handle h, sp_stats *out)
     s.host_ms_commit = h->host_ms[3];
     s.host_ms_mover = h->host_ms[4];
     s.host_ms_inputs = h->host_ms[5];
+    s.prefetched = h->st.prefetched;
     s.timed_plan = h->t_plan.count;
     s.timed_fill = h->t_fill.count;
     s.ms_ingest = h->t_ing.ms;

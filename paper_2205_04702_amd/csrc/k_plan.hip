@@ -37,21 +37,39 @@ struct ProbeArgs {
 // it; no copy command, fence or stream synchronisation is involved, and each
 // word is whole when seen.  It then clears the copies, the per-plan counters
 // and the arrival count for the next query.
+//
+// Prefetch mode: batch 0's misses go to pf.own_key / pf.own_uidx instead, and
+// batch 1 (the next one) flags each unique key that is not cached and not a
+// key of batch 0 (a binary search of batch 0's sorted keys) and counts them
+// per table, so the plan can fill them too.
+// Whether key is among the n sorted keys a[0..n).
+__device__ __forceinline__ bool in_sorted(const uint32_t *__restrict__ a, int32_t n, uint32_t key)
+{
+    int32_t lo = 0, hi = n;
+    while (lo < hi) {
+        const int32_t mid = lo + (hi - lo) / 2;
+        if (a[mid] < key) lo = mid + 1;
+        else hi = mid;
+    }
+    return lo < n && a[lo] == key;
+}
+
 __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
                                                  const uint64_t *__restrict__ hash, uint32_t mask,
-                                                 ProbeArgs pa, int32_t *held, int32_t stamp,
+                                                 ProbeArgs pa, PrefetchDev pf, int32_t *held,
+                                                 int32_t stamp,
                                                  int32_t *hit, int32_t *slot_u, DevCounters *cnt,
                                                  int32_t *part, int32_t *arrived,
                                                  const int32_t *scal0, uint64_t *host_mapped,
                                                  uint32_t seq, uint32_t *m_key, int32_t *m_uidx,
                                                  ScanDev d)
 {
-    __shared__ int32_t c_miss[MAX_TABLES], c_held[MAX_TABLES];
+    __shared__ int32_t c_miss[MAX_TABLES], c_held[MAX_TABLES], c_pf[MAX_TABLES];
     __shared__ int32_t last_s;
     __shared__ uint32_t tile_s, pref_s;
     __shared__ uint32_t lds_scan[BLOCK / WAVE];
     const int w = blockIdx.y;
-    for (int t = threadIdx.x; t < T; t += BLOCK) c_miss[t] = c_held[t] = 0;
+    for (int t = threadIdx.x; t < T; t += BLOCK) c_miss[t] = c_held[t] = c_pf[t] = 0;
     if (w == 0 && threadIdx.x == 0) tile_s = atomicAdd(d.counter, 1u) - d.base;
     __syncthreads();
     const int64_t xb = w == 0 ? (int64_t)tile_s : (int64_t)blockIdx.x;
@@ -69,7 +87,7 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
     if (i == 0 && pa.nu[w][2]) seen |= atomicOr(&cnt->err, pa.nu[w][2]) == INT32_MIN;
     const bool valid = i < *pa.nu[w];
     int t = 0;
-    bool miss = false, fresh = false;
+    bool miss = false, fresh = false, fetch = false;
     uint32_t key = 0;
     if (valid) {
         key = pa.uk[w][i];
@@ -81,6 +99,10 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
             miss = slot < 0;
         }
         if (slot >= 0) fresh = atomicExch(&held[slot], stamp) != stamp;
+        if (w == 1 && pf.on) {
+            fetch = slot < 0 && !in_sorted(pa.uk[0], *pa.nu[0], key);
+            pf.flag[i] = fetch;
+        }
     }
     if (w == 0 && xb * BLOCK < (int64_t)*pa.nu[0]) {  // uniform per block
         uint32_t tot;
@@ -91,8 +113,10 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
         }
         __syncthreads();
         if (miss) {
-            m_key[pref_s + ex] = key;
-            m_uidx[pref_s + ex] = (int32_t)i;
+            uint32_t *const mk = pf.on ? pf.own_key : m_key;
+            int32_t *const mu = pf.on ? pf.own_uidx : m_uidx;
+            mk[pref_s + ex] = key;
+            mu[pref_s + ex] = (int32_t)i;
         }
     }
     uint64_t todo = __ballot(valid);
@@ -103,17 +127,20 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
         const uint64_t same = __ballot(mine);
         const int nm = __popcll(__ballot(mine && miss));
         const int nh = __popcll(__ballot(mine && fresh));
+        const int nf = __popcll(__ballot(mine && fetch));
         if (lane_id() == leader) {
             if (nm) atomicAdd(&c_miss[tl], nm);
             if (nh) atomicAdd(&c_held[tl], nh);
+            if (nf) atomicAdd(&c_pf[tl], nf);
         }
         todo &= ~same;
     }
     __syncthreads();
-    int32_t *p = part + (int64_t)((blockIdx.y * gridDim.x + blockIdx.x) % PART_COPIES) * 2 * MAX_TABLES;
+    int32_t *p = part + (int64_t)((blockIdx.y * gridDim.x + blockIdx.x) % PART_COPIES) * PART_WORDS;
     for (int tt = threadIdx.x; tt < T; tt += BLOCK) {
         if (c_miss[tt]) seen |= atomicAdd(&p[tt], c_miss[tt]);
         if (c_held[tt]) seen |= atomicAdd(&p[MAX_TABLES + tt], c_held[tt]);
+        if (c_pf[tt]) seen |= atomicAdd(&p[2 * MAX_TABLES + tt], c_pf[tt]);
     }
     if (seen < 0) cnt->pad2[0] = seen;  // never taken (counts are not negative)
     __syncthreads();
@@ -123,27 +150,29 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
     if (!last_s) return;  // uniform per block
 
     // ---- last block: publish
-    __shared__ int32_t sums[2 * MAX_TABLES];
-    for (int j = threadIdx.x; j < 2 * MAX_TABLES; j += BLOCK) sums[j] = 0;
+    __shared__ int32_t sums[PART_WORDS];
+    for (int j = threadIdx.x; j < PART_WORDS; j += BLOCK) sums[j] = 0;
     __syncthreads();
-    const int n_rel = PART_COPIES * 2 * T;
-    auto word = [T](int r) {
-        const int c = r / (2 * T), jj = r % (2 * T);
-        return c * 2 * MAX_TABLES + (jj < T ? jj : MAX_TABLES + jj - T);
+    const int n_rel = PART_COPIES * 3 * T;
+    auto word = [T](int r) {  // the r-th live word: copy c, array a (miss, held, pf), table
+        const int c = r / (3 * T), jj = r % (3 * T), a = jj / T;
+        return c * PART_WORDS + a * MAX_TABLES + (jj - a * T);
     };
     for (int r = threadIdx.x; r < n_rel; r += BLOCK) {
         const int idx = word(r);
         const int32_t v = __hip_atomic_load(&part[idx], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (v) atomicAdd(&sums[idx % (2 * MAX_TABLES)], v);
+        if (v) atomicAdd(&sums[idx % PART_WORDS], v);
     }
     __syncthreads();
     int32_t *src = reinterpret_cast<int32_t *>(cnt);
     constexpr int MISS0 = (int)(offsetof(DevCounters, miss) / sizeof(int32_t));
     constexpr int HELD0 = (int)(offsetof(DevCounters, held) / sizeof(int32_t));
+    constexpr int PF0 = (int)(offsetof(DevCounters, pf) / sizeof(int32_t));
     for (int k = threadIdx.x; k < COUNTER_WORDS; k += BLOCK) {
         int32_t v;
         if (k >= MISS0 && k < MISS0 + MAX_TABLES) v = k - MISS0 < T ? sums[k - MISS0] : 0;
         else if (k >= HELD0 && k < HELD0 + MAX_TABLES) v = k - HELD0 < T ? sums[MAX_TABLES + k - HELD0] : 0;
+        else if (k >= PF0 && k < PF0 + MAX_TABLES) v = k - PF0 < T ? sums[2 * MAX_TABLES + k - PF0] : 0;
         else v = __hip_atomic_load(&src[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         host_mapped[k] = ((uint64_t)seq << 32) | (uint32_t)v;
         if (k < COUNTERS_CLEARED)
@@ -156,10 +185,11 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
 
 void launch_query(const Tables &tb, const uint64_t *hash, uint32_t mask,
                   const uint32_t *const *ukeys, const int32_t *const *nuniq, int nwin,
-                  int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk,
+                  int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk, PrefetchDev pf,
                   DevCounters *cnt, int32_t *part, int32_t *arrived, const int32_t *scal0,
                   uint64_t *host_mapped, uint32_t seq, ScanWs &ws, hipStream_t s)
 {
+    if (nwin < 2) pf.on = 0;  // no next batch in the window
     ProbeArgs pa{};
     for (int w = 0; w < nwin; ++w) pa.uk[w] = ukeys[w], pa.nu[w] = nuniq[w];
     // at least one block per batch so that every batch's error word is read
@@ -176,7 +206,7 @@ void launch_query(const Tables &tb, const uint64_t *hash, uint32_t mask,
     ScanDev d{ws.status, ws.counter, ws.err, ws.issued, ++ws.epoch, (uint32_t)gx, (int32_t)gx};
     ws.issued += (uint32_t)gx;  // the planned batch's row of blocks takes tiles
     hipLaunchKernelGGL(k_query, dim3((unsigned)gx, nwin), dim3(BLOCK), 0, s, tb.row_bits, tb.T,
-                       hash, mask, pa, held, stamp, tk.hit, tk.slot_u, cnt, part, arrived, scal0,
+                       hash, mask, pa, pf, held, stamp, tk.hit, tk.slot_u, cnt, part, arrived, scal0,
                        host_mapped, seq, tk.m_key, tk.m_uidx, d);
 }
 
@@ -475,14 +505,17 @@ __global__ void __launch_bounds__(BLOCK) k_commit(uint64_t *hash, uint32_t mask,
                                                   const uint32_t *perm, int64_t n_miss,
                                                   int64_t n_unique, int64_t nnz, int64_t nslots,
                                                   int32_t *key_of_slot, int32_t *last_use,
-                                                  int32_t *uses, int32_t u, int32_t *err)
+                                                  int32_t *uses, int32_t u, int32_t prefetch,
+                                                  int32_t *err)
 {
     const int64_t t = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
     if (t < n_miss) {
         const int64_t i = t;
         const int32_t v = tk.v_slot[i];
         const int32_t ui = tk.m_uidx[i];
-        if ((uint32_t)v >= (uint64_t)nslots || (uint32_t)ui >= (uint64_t)n_unique) {
+        // a prefetched row (prefetch mode, m_uidx = -1) is placed but not used
+        const bool fetched = prefetch && ui == -1;
+        if ((uint32_t)v >= (uint64_t)nslots || (!fetched && (uint32_t)ui >= (uint64_t)n_unique)) {
             atomicOr(err, ERR_PLAN);
             tk.v_old_key[i] = -1;
             tk.v_old_lu[i] = -1;
@@ -495,9 +528,10 @@ __global__ void __launch_bounds__(BLOCK) k_commit(uint64_t *hash, uint32_t mask,
         const uint32_t key = tk.m_key[i];
         key_of_slot[v] = (int32_t)key;
         if (!hash_insert(hash, mask, key, v)) atomicOr(err, ERR_HASH_FULL);
-        tk.slot_u[ui] = v;
         last_use[v] = u;
-        if (uses) uses[v] = 1;
+        if (uses) uses[v] = fetched ? 0 : 1;
+        if (fetched) return;
+        tk.slot_u[ui] = v;
         const int32_t p0 = seg_off[ui], p1 = seg_off[ui + 1];
         for (int32_t p = p0; p < p1; ++p) {
             const uint32_t j = perm[p];
@@ -523,7 +557,7 @@ __global__ void __launch_bounds__(BLOCK) k_commit(uint64_t *hash, uint32_t mask,
 void launch_commit(const Tables &tb, uint64_t *hash, uint32_t mask, TicketDev tk,
                    const BatchDev &b, int64_t n_miss, int64_t n_unique, int64_t nnz,
                    int32_t *key_of_slot, int32_t *last_use, int32_t *uses, int32_t u,
-                   DevCounters *cnt, hipStream_t s)
+                   bool prefetch, DevCounters *cnt, hipStream_t s)
 {
     const int64_t n = n_miss + (nnz > n_unique ? nnz : n_unique);
     if (n <= 0) return;
@@ -531,7 +565,106 @@ void launch_commit(const Tables &tb, uint64_t *hash, uint32_t mask, TicketDev tk
     hipLaunchKernelGGL(k_commit, dim3((unsigned)((n + BLOCK - 1) / BLOCK)), dim3(BLOCK), 0, s,
                        hash, mask, tk, (const int32_t *)b.inv, (const int32_t *)b.seg_off,
                        (const uint32_t *)b.perm, n_miss, n_unique, nnz, nslots, key_of_slot,
-                       last_use, uses, u, &cnt->err_sticky);
+                       last_use, uses, u, (int32_t)prefetch, &cnt->err_sticky);
+}
+
+// ---------------------------------------------------------------- prefetch arrangement
+//
+// One single-pass scan over a virtual range: indices [0, n_own) are the
+// planned batch's own misses (ascending, all tables), indices n_own + j are
+// the next batch's unique keys j, valued 1 when flagged for prefetch.  The
+// scan's prefix at a flagged key counts the flagged keys before it, all
+// tables included, so per table (keys are ascending by table) it is the
+// table's first prefetched entry plus the key's rank among them.
+
+struct PfSeg {
+    int64_t n_own;
+    const int32_t *n_next;
+    __device__ int64_t beg(int) const { return 0; }
+    __device__ int64_t end(int) const { return n_own + *n_next; }
+};
+
+struct PfVal {
+    int64_t n_own;
+    const int32_t *flag;
+    __device__ uint32_t operator()(int64_t i, int) const
+    {
+        const int64_t j = i - n_own;
+        const int32_t f = flag[j > 0 ? j : 0];  // loaded without a branch
+        return i >= n_own && f ? 1u : 0u;
+    }
+};
+
+struct PfOut {
+    int64_t n_own, n_miss;
+    int32_t row_bits, T;
+    const uint32_t *own_key, *next_keys;
+    const int32_t *own_uidx;
+    uint32_t *m_key;
+    int32_t *m_uidx, *err;
+    int32_t pf_first[MAX_TABLES];    // prefetched keys of the tables before t
+    int32_t vbase[MAX_TABLES];       // first miss (and victim) of table t
+    int32_t own[MAX_TABLES];         // own misses of table t
+    __device__ void operator()(int64_t i, uint32_t e, uint32_t v, int) const
+    {
+        uint32_t key;
+        int32_t uidx;
+        int64_t dst;
+        if (i < n_own) {
+            key = own_key[i];
+            uidx = own_uidx[i];
+            const int t = (int)(key >> row_bits);
+            if (t >= T) {
+                atomicOr(err, ERR_PLAN);
+                return;
+            }
+            dst = i + pf_first[t];
+        } else {
+            if (!v) return;
+            key = next_keys[i - n_own];
+            uidx = -1;
+            const int t = (int)(key >> row_bits);
+            if (t >= T) {
+                atomicOr(err, ERR_PLAN);
+                return;
+            }
+            dst = (int64_t)vbase[t] + own[t] + ((int64_t)e - pf_first[t]);
+        }
+        if (dst < 0 || dst >= n_miss) {  // the counts and the lists disagree
+            atomicOr(err, ERR_PLAN);
+            return;
+        }
+        m_key[dst] = key;
+        m_uidx[dst] = uidx;
+    }
+};
+
+void launch_pf_arrange(const Tables &tb, PrefetchDev pf, int64_t n_own, const int32_t *n_next,
+                       int64_t max_next, const uint32_t *next_ukeys, const int32_t *own,
+                       const int32_t *pf_count, TicketDev tk, int64_t n_miss, int32_t *err,
+                       ScanWs &ws, hipStream_t s)
+{
+    PfOut o{};
+    o.n_own = n_own;
+    o.n_miss = n_miss;
+    o.row_bits = tb.row_bits;
+    o.T = tb.T;
+    o.own_key = pf.own_key;
+    o.own_uidx = pf.own_uidx;
+    o.next_keys = next_ukeys;
+    o.m_key = tk.m_key;
+    o.m_uidx = tk.m_uidx;
+    o.err = err;
+    int32_t pfa = 0, vb = 0;
+    for (int t = 0; t < tb.T; ++t) {
+        o.pf_first[t] = pfa;
+        o.vbase[t] = vb;
+        o.own[t] = own[t];
+        pfa += pf_count[t];
+        vb += own[t] + pf_count[t];
+    }
+    seg_scan<uint32_t>(PfSeg{n_own, n_next}, 1, n_own + (next_ukeys ? max_next : 0),
+                       PfVal{n_own, pf.flag}, o, ws, s);
 }
 
 }  // namespace sp

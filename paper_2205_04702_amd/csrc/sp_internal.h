@@ -51,11 +51,13 @@ struct DevCounters {
     int32_t n_multi;             // its runs longer than one chunk
     int32_t miss[MAX_TABLES];
     int32_t held[MAX_TABLES];
+    int32_t pf[MAX_TABLES];      // rows of the next batch to prefetch (prefetch mode)
     int32_t err_sticky;          // ERR_HASH_FULL / ERR_PLAN from any earlier commit
     int32_t pad2[3];
 };
 constexpr int COUNTERS_CLEARED = (int)(offsetof(DevCounters, err_sticky) / sizeof(int32_t));
 constexpr int PART_COPIES = 64;  // copies of the per-table counters the probe adds into
+constexpr int PART_WORDS = 3 * MAX_TABLES;  // one copy: miss, held and prefetch counts
 constexpr int COUNTER_WORDS = (int)(sizeof(DevCounters) / sizeof(int32_t));
 constexpr int32_t ERR_ID_RANGE = 1, ERR_OFFSETS = 2, ERR_HASH_FULL = 4, ERR_PLAN = 8;
 constexpr int32_t ERR_TABLE_IDS = 16;  // a table has more IDs than the configured bound
@@ -185,9 +187,18 @@ RadixPlan radix_plan(int64_t n, int bits);
 // The query: hold marks, hits, the misses in ascending key order (tk.m_key,
 // tk.m_uidx) and per-table counts of one plan, published to host_mapped
 // (word i = seq << 32 | counter word i) by the last block.
+// Prefetch mode: the query compacts the planned batch's own misses into
+// own_key / own_uidx and flags (flag[j] = 1) the next batch's unique keys to
+// prefetch; the arrangement then writes both into the ticket's miss list.
+struct PrefetchDev {
+    int32_t on;
+    uint32_t *own_key;
+    int32_t *own_uidx;
+    int32_t *flag;
+};
 void launch_query(const Tables &tb, const uint64_t *hash, uint32_t mask,
                   const uint32_t *const *ukeys, const int32_t *const *nuniq, int nwin,
-                  int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk,
+                  int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk, PrefetchDev pf,
                   DevCounters *cnt, int32_t *part, int32_t *arrived, const int32_t *scal0,
                   uint64_t *host_mapped, uint32_t seq, ScanWs &ws, hipStream_t s);
 
@@ -203,7 +214,14 @@ void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int
 void launch_commit(const Tables &tb, uint64_t *hash, uint32_t mask, TicketDev tk,
                    const BatchDev &b, int64_t n_miss, int64_t n_unique, int64_t nnz,
                    int32_t *key_of_slot, int32_t *last_use, int32_t *uses, int32_t u,
-                   DevCounters *cnt, hipStream_t s);
+                   bool prefetch, DevCounters *cnt, hipStream_t s);
+// Prefetch mode: the ticket's miss list, per table the planned batch's own
+// misses (ascending) then the next batch's flagged keys (ascending), at
+// vbase[t] = first victim of table t; prefetched entries get m_uidx = -1.
+void launch_pf_arrange(const Tables &tb, PrefetchDev pf, int64_t n_own, const int32_t *n_next,
+                       int64_t max_next, const uint32_t *next_ukeys, const int32_t *own,
+                       const int32_t *pf_count, TicketDev tk, int64_t n_miss, int32_t *err,
+                       ScanWs &ws, hipStream_t s);
 
 // k_train.hip
 void launch_move(float *storage, int dim, const Tables &tb, float *const *host_dev, TicketDev tk,

@@ -47,7 +47,7 @@ class sp_config(C.Structure):
                 ("host_tables", C.POINTER(C.c_void_p)), ("max_batch", C.c_int32),
                 ("max_ids", C.c_int64), ("flags", C.c_uint32), ("device", C.c_int32),
                 ("policy", C.c_int32), ("hold_past", C.c_int32), ("seed", C.c_uint64),
-                ("max_table_ids", C.c_int64)]
+                ("max_table_ids", C.c_int64), ("prefetch", C.c_int32)]
 
 
 class sp_batch(C.Structure):
@@ -66,13 +66,14 @@ _STAT_HOST = ["host_ms_ingest", "host_ms_query", "host_ms_wait", "host_ms_commit
 _STAT_F64B = ["ms_ingest", "ms_query"]
 _STAT_CNTB = ["timed_ingest", "timed_query"]
 _STAT_HOSTB = ["host_ms_inputs"]
+_STAT_I64B = ["prefetched"]
 
 
 class sp_stats(C.Structure):
     _fields_ = ([(n, C.c_int64) for n in _STAT_I64] + [(n, C.c_double) for n in _STAT_F64]
                 + [(n, C.c_int64) for n in _STAT_CNT] + [(n, C.c_double) for n in _STAT_HOST]
                 + [(n, C.c_double) for n in _STAT_F64B] + [(n, C.c_int64) for n in _STAT_CNTB]
-                + [(n, C.c_double) for n in _STAT_HOSTB])
+                + [(n, C.c_double) for n in _STAT_HOSTB] + [(n, C.c_int64) for n in _STAT_I64B])
 
 
 _DUMP_I32 = ["u_table", "u_row", "inv", "m_table", "m_row", "v_slot", "v_old_row", "v_old_use",
@@ -169,9 +170,13 @@ def sp_set_flags(handle: int, flags: int) -> None:
     _check(load().sp_set_flags(handle, flags), handle)
 
 
-def sp_debug_plan(handle: int, ticket: int, nnz_cap: int) -> dict:
+def sp_debug_plan(handle: int, ticket: int, nnz_cap: int, miss_cap: int | None = None) -> dict:
+    """miss_cap: room for the miss arrays (in prefetch mode the nnz of the planned and
+    the next batch together); nnz_cap by default."""
     cap = max(int(nnz_cap), 1)
-    arrays = {n: np.empty(cap, np.int32) for n in _DUMP_I32}
+    mcap = max(int(miss_cap if miss_cap is not None else nnz_cap), 1)
+    misses = ("m_table", "m_row", "v_slot", "v_old_row", "v_old_use")
+    arrays = {n: np.empty(mcap if n in misses else cap, np.int32) for n in _DUMP_I32}
     hit = np.empty(cap, np.uint8)
     d = sp_plan_dump()
     for n in _DUMP_I32:
@@ -259,12 +264,15 @@ class ScratchPipe:
 
     policy: "lru", "lfu" or "random"; hold_past: earlier batches held as well;
     seed: the random policy's stream; max_table_ids: 0 or the most IDs any one
-    table has in a batch (a promise that is checked)."""
+    table has in a batch (a promise that is checked); prefetch: plans also fill
+    the next batch's missing rows."""
 
     def __init__(self, rows, dim, slots, lookahead, host_tables: HostTables, max_batch, max_ids,
                  flags: int = 0, device: int = 0, policy: str = "lru", hold_past: int = 0,
-                 seed: int = 0, max_table_ids: int = 0):
+                 seed: int = 0, max_table_ids: int = 0, prefetch: bool = False):
         self.T = len(rows)
+        self.prefetch = bool(prefetch)
+        self.max_ids = int(max_ids)
         self.dim = dim
         self._rows = (C.c_int64 * self.T)(*[int(r) for r in rows])
         self._slots = (C.c_int64 * self.T)(*[int(s) for s in slots])
@@ -272,7 +280,8 @@ class ScratchPipe:
         cfg = sp_config(num_tables=self.T, rows=self._rows, dim=dim, slots=self._slots,
                         lookahead=lookahead, host_tables=self._tabs, max_batch=max_batch,
                         max_ids=max_ids, flags=flags, device=device, policy=POLICIES[policy],
-                        hold_past=hold_past, seed=seed, max_table_ids=max_table_ids)
+                        hold_past=hold_past, seed=seed, max_table_ids=max_table_ids,
+                        prefetch=int(self.prefetch))
         self.handle = sp_create(cfg)
         self._desc_cache = {}
 
@@ -322,7 +331,9 @@ class ScratchPipe:
         sp_set_flags(self.handle, flags)
 
     def debug_plan(self, ticket: int, nnz: int) -> dict:
-        return sp_debug_plan(self.handle, ticket, nnz)
+        # prefetch mode: misses of the planned and the next batch (each at most max_ids)
+        return sp_debug_plan(self.handle, ticket, nnz,
+                             nnz + self.max_ids if self.prefetch else nnz)
 
     def close(self) -> None:
         if getattr(self, "handle", None):

@@ -91,14 +91,15 @@ def make_inputs(w, steps=None, ragged=None):
 def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all", flags=0,
                device_ids=False, ref_tables=None, sync_each_step=True, compare_tables=True,
                return_tables=False, steps=None, prepare_ahead=0, policy="lru", hold_past=0,
-               seed=0, max_table_ids="auto"):
+               seed=0, max_table_ids="auto", prefetch=False):
     """Train w on the GPU and with the oracle; assert parity; return a summary.
 
     prepare_ahead: also hand the GPU that many batches after the window
     (prepared in advance, not held); the oracle always sees the plain window.
     policy, hold_past, seed: replacement policy and past window of both planners.
     max_table_ids: the bound handed to the library ("auto": the batches' own maximum,
-    which sorts tables of up to 8192 IDs in LDS; 0: no bound, the general path)."""
+    which sorts tables of up to 8192 IDs in LDS; 0: no bound, the general path).
+    prefetch: both planners also fill the next batch's missing rows."""
     import torch
     dev = torch.device("cuda:0")
     if batches is None:
@@ -110,7 +111,7 @@ def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all"
     for t in range(T):
         wl.init_table(w, t, out=host[t])
     ref = ref_tables if ref_tables is not None else [wl.init_table(w, t) for t in range(T)]
-    planner = oracle.Planner(w.rows, w.slots, policy, seed)
+    planner = oracle.Planner(w.rows, w.slots, policy, seed, prefetch)
     touched = [np.zeros(r, bool) for r in w.rows]
     dev_batches = None
     if device_ids:
@@ -120,7 +121,7 @@ def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all"
     worst_fwd = 0.0
     sp = ScratchPipe(w.rows, D, w.slots, L, host, max_batch=B, max_ids=max(max_ids, 1), flags=flags,
                      policy=policy, hold_past=hold_past, seed=seed,
-                     max_table_ids=_bound(w, batches, max_table_ids))
+                     max_table_ids=_bound(w, batches, max_table_ids), prefetch=prefetch)
     try:
         out = torch.zeros((T * B, D), dtype=torch.float32, device=dev)
         for u in range(n):
@@ -188,7 +189,7 @@ def row_values(t, rows, dim):
 
 
 def run_sampled_parity(w, steps, *, check_plan_steps, check_fwd_steps, say=print, policy="lru",
-                       hold_past=0, seed=0, max_table_ids="auto"):
+                       hold_past=0, seed=0, max_table_ids="auto", prefetch=False):
     """A full-size workload driven as the benchmark drives it (IDs in device memory, the two
     batches after the window handed over early) for `steps` steps.
 
@@ -228,11 +229,11 @@ def run_sampled_parity(w, steps, *, check_plan_steps, check_fwd_steps, say=print
         return np.concatenate(parts), off
 
     dev_batches = [(torch.from_numpy(i).to(dev), torch.from_numpy(o).to(dev)) for i, o in batches]
-    planner = oracle.Planner(w.rows, w.slots, policy, seed)
+    planner = oracle.Planner(w.rows, w.slots, policy, seed, prefetch)
     max_ids = max(int(b[0].size) for b in batches)
     sp = ScratchPipe(w.rows, D, w.slots, L, host, max_batch=B, max_ids=max_ids, policy=policy,
                      hold_past=hold_past, seed=seed,
-                     max_table_ids=_bound(w, batches, max_table_ids))
+                     max_table_ids=_bound(w, batches, max_table_ids), prefetch=prefetch)
     worst_fwd = 0.0
     try:
         out = torch.zeros((T * B, D), dtype=torch.float32, device=dev)

@@ -1,0 +1,88 @@
+"""Parity of the HIP planner's prefetch mode (needs an MI355X).
+
+With prefetch each plan also fills the rows of the next batch of its window
+that are neither cached nor in the planned batch: an earlier fill of future
+misses, which the multi-stage overlap of Sec. IV-C allows.  Plans (the miss
+list with the planned batch's misses then the prefetched rows per table, the
+victims, old rows and last uses, hits, slots) must match the oracle planner run
+in the same mode bit for bit; outputs and tables within 1e-5 per row as in the
+other parity tests.
+"""
+import pytest
+
+from paper_2205_04702_amd import workload as wl
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def harness():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from tests import gpu_harness
+    return gpu_harness
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+@pytest.mark.parametrize("policy", ["lru", "lfu", "random"])
+def test_tiny_all_steps(harness, policy):
+    """4 x 20k x 32, B=128, 4 IDs per bag, 2048 slots, lookahead 2, 50 steps."""
+    w = wl.get_workload("tiny")
+    _say(f"case prefetch tiny policy {policy}")
+    r = harness.run_parity(w, policy=policy, seed=5, prefetch=True)
+    st = r["stats"]
+    assert st["evictions"] > 0 and st["prefetched"] > 0
+
+
+def test_ragged_and_empty_bags_general_ingest(harness):
+    """Ragged bags with empty ones, sorted by the general (multi-launch) ingest path."""
+    w = wl.custom(rows=[3000, 5000], dim=16, batch=64, pooling=[3, 5], slots=[700, 900],
+                  lookahead=2, steps=20, dist=(("zipf", 1.05), ("uniform",)), seed=6)
+    batches = [wl.ragged_batch(w, s, max_len=8, empty_frac=0.25) for s in range(w.steps)]
+    _say("case prefetch ragged general ingest")
+    r = harness.run_parity(w, batches, prefetch=True, max_table_ids=0)
+    assert r["stats"]["prefetched"] > 0
+
+
+def test_no_lookahead_means_no_prefetch(harness):
+    w = wl.custom(rows=[4000] * 2, dim=32, batch=64, pooling=4, slots=[600] * 2, lookahead=0,
+                  steps=20, dist=("zipf", 1.05), seed=7)
+    _say("case prefetch lookahead 0")
+    r = harness.run_parity(w, prefetch=True)
+    assert r["stats"]["prefetched"] == 0 and r["stats"]["evictions"] > 0
+
+
+def test_past_window_and_prepared_batches(harness):
+    """A past window of 2 (its batches follow the hold window in the query) and two
+    batches handed over early from device memory."""
+    w = wl.custom(rows=[50_000] * 3, dim=32, batch=128, pooling=4, slots=[4096] * 3,
+                  lookahead=2, steps=30, dist=("zipf", 1.05), seed=4)
+    _say("case prefetch past window 2")
+    r = harness.run_parity(w, hold_past=2, prepare_ahead=2, device_ids=True, prefetch=True)
+    assert r["stats"]["prefetched"] > 0 and r["stats"]["evictions"] > 0
+
+
+def test_large_victim_sets(harness):
+    """Over 2048 victims per table per plan (own and prefetched misses together): the
+    victims are ordered by the global radix sort."""
+    w = wl.custom(rows=[1_000_000] * 2, dim=16, batch=1024, pooling=4, slots=[30_000] * 2,
+                  lookahead=1, steps=12, dist=("uniform",), seed=8)
+    _say("case prefetch large victim sets")
+    r = harness.run_parity(w, seed=3, sync_each_step=False, prefetch=True)
+    st = r["stats"]
+    assert st["evictions"] > 4 * 2 * 2048 and st["prefetched"] > 0
+
+
+def test_zipf_8x1M_sampled(harness):
+    """The benchmark workload with prefetch, driven as the benchmark drives it, 40 steps."""
+    w = wl.get_workload("zipf-8x1M")
+    _say("case prefetch zipf-8x1M")
+    sample = [0, 1, 2, 13, 25, 38, 39]
+    r = harness.run_sampled_parity(w, 40, check_plan_steps=sample, check_fwd_steps=sample,
+                                   say=_say, prefetch=True)
+    _say(f"zipf-8x1M prefetch: worst fwd {r['worst_fwd']:.2e} table {r['worst_table']:.2e} "
+         f"misses {r['stats']['misses']} prefetched {r['stats']['prefetched']}")

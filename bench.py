@@ -119,6 +119,8 @@ def main():
                     help="replacement policy (LRU is the method's default)")
     ap.add_argument("--hold-past", type=int, default=0, metavar="P",
                     help="also hold the rows of the P batches planned before each plan")
+    ap.add_argument("--prefetch", action="store_true",
+                    help="each plan also fills the next batch's missing rows")
     ap.add_argument("--host-ids", action="store_true",
                     help="hand the batch IDs over from host memory (PCIe-inclusive variant)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -182,6 +184,7 @@ def main():
                   | (sp.SP_FLAG_DEBUG_SYNC if args.serialize else 0))
     ctx = sp.ScratchPipe(w.rows, w.dim, w.slots, L, host, max_batch=w.batch, max_ids=w.nnz,
                          flags=base_flags, policy=args.policy, hold_past=args.hold_past,
+                         prefetch=args.prefetch,
                          max_table_ids=w.batch * max(w.pooling))
     out = torch.empty((w.tables * w.batch, w.dim), dtype=torch.float32, device=dev)
 
@@ -250,11 +253,15 @@ def main():
         "config": {**w.describe(), "ids": "host" if args.host_ids else "hbm",
                    **({"policy": args.policy} if args.policy != "lru" else {}),
                    **({"hold_past": args.hold_past} if args.hold_past else {}),
-                   **({"serialized": True} if args.serialize else {})},
+                   **({"serialized": True} if args.serialize else {}),
+                   **({"prefetch": True} if args.prefetch else {})},
     }
-    detail = {"miss_rate": round(d["misses"] / max(d["unique"], 1), 4),
+    # the planned batches' own misses; with prefetch, fills also cover the next batches
+    detail = {"miss_rate": round((d["misses"] - d.get("prefetched", 0)) / max(d["unique"], 1), 4),
+              "fills_per_step": round(d["misses"] / K, 1),
               "unique_per_step": round(n_unique, 1),
               "evictions_per_step": round(d["evictions"] / K, 1),
+              "prefetched_per_step": round(d.get("prefetched", 0) / K, 1),
               "fill_GBps": round(d["bytes_fill"] / dt / 1e9, 3),
               "writeback_GBps": round(d["bytes_writeback"] / dt / 1e9, 3),
               "host_ms_per_step": {"plan": round(host_s[0] * 1e3 / K, 4),

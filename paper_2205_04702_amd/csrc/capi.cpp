@@ -130,6 +130,7 @@ struct Job {
 
 struct TicketHost {
     int64_t nnz = 0, n_unique = 0, n_chunks = 0, n_multi = 0, n_miss = 0;
+    int64_t n_own = 0;  // misses of the planned batch itself (n_miss less prefetched rows)
     int32_t B = 0;
     int ring = 0;
     int nwin = 0;
@@ -1098,6 +1099,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     th.n_chunks = c.n_chunks;
     th.n_multi = c.n_multi;
     th.n_miss = n_miss;
+    th.n_own = n_own;
     th.ring = r0;
     th.nwin = nhold;
 
@@ -1251,11 +1253,28 @@ extern "C" sp_status sp_forward(sp_handle h, int64_t ticket, float *d_out, void 
     const int64_t nbags = (int64_t)h->T * th.B;
     if (nbags > 0 && !d_out) return fail(h, SP_ERR_INVALID_ARG, "null d_out");
     hipStream_t s = (hipStream_t)stream;
-    if (h->flags & SP_FLAG_EVENT_WAITS)
-        HIPCHK(h, hipStreamWaitEvent(s, h->ev_filled[e], 0));
-    else
-        HIPCHK(h, hipStreamWaitValue64(s, h->sem + SEM_FILLED, (uint64_t)ticket + 1,
-                                       hipStreamWaitValueGte, ~0ull));
+    // The batch's rows are resident once the fills that brought them are done:
+    // this plan's, if the batch had misses of its own (its fill also follows
+    // the commit that wrote slot_of); otherwise earlier ones only (with
+    // prefetch the previous plan's), and the commit is waited for by itself.
+    // This plan's fill writes only victim slots, which hold no row of the
+    // batch, so the forward and the update then overlap it.
+    const bool ev = h->flags & SP_FLAG_EVENT_WAITS;
+    if (th.n_own > 0 || ticket == 0) {
+        if (ev) HIPCHK(h, hipStreamWaitEvent(s, h->ev_filled[e], 0));
+        else HIPCHK(h, hipStreamWaitValue64(s, h->sem + SEM_FILLED, (uint64_t)ticket + 1,
+                                            hipStreamWaitValueGte, ~0ull));
+    } else {
+        if (ev) {
+            HIPCHK(h, hipStreamWaitEvent(s, h->ev_planned[e], 0));
+            HIPCHK(h, hipStreamWaitEvent(s, h->ev_filled[(ticket - 1) % h->nring], 0));
+        } else {
+            HIPCHK(h, hipStreamWaitValue64(s, h->sem + SEM_PLANNED, (uint64_t)ticket + 1,
+                                           hipStreamWaitValueGte, ~0ull));
+            HIPCHK(h, hipStreamWaitValue64(s, h->sem + SEM_FILLED, (uint64_t)ticket,
+                                           hipStreamWaitValueGte, ~0ull));
+        }
+    }
     // RAW-1: the previous update must land first (implicit on the same stream)
     if (ticket >= 1 && s != h->last_update_stream)
         HIPCHK(h, wait_unless_done(s, h->ev_upd[(ticket - 1) % h->nring]));

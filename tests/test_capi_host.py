@@ -95,6 +95,8 @@ def _cfg(**over):
     (dict(lookahead=12, hold_past=4), "hold_past"),
     (dict(max_table_ids=-1), "max_table_ids"),
     (dict(dim=256, max_batch=1 << 21), "4 GiB"),  # gradients addressed with 32-bit offsets
+    (dict(prefetch=2), "prefetch"),
+    (dict(prefetch=-1), "prefetch"),
 ])
 def test_create_rejects_bad_configs(over, needle):
     cfg, keep = _cfg(**over)

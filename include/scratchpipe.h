@@ -216,7 +216,10 @@ sp_status sp_create(const sp_config *config, sp_handle *out);
  * the ascending misses take them in that order), updates Hit-Map, slot keys,
  * last-use and use counts, and enqueues the evicted rows' write-back and the
  * misses' fill (Sec. IV-C "Putting everything together", Sec. IV-D
- * Algorithm 1; policies from Sec. VI-E).  The host waits once for per-table counts.
+ * Algorithm 1; policies from Sec. VI-E).  With sp_config.prefetch the misses
+ * also include window[1]'s rows that are neither cached nor in window[0]
+ * (after window[0]'s own misses, per table).  The host waits once for
+ * per-table counts.
  * Requires the previous ticket's sp_backward_update to have been issued.
  * Transactional: on SP_ERR_INVALID_ARG (ID out of range, bad offsets, sizes
  * above the config) or SP_ERR_CAPACITY (misses > unheld slots in some table)
@@ -228,7 +231,10 @@ sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int64_t *ticke
  * Pooled forward of a planned batch: d_out[t*B+b][:] = sum of the Storage rows
  * of bag (t,b) (Sec. II-B "Forward propagation", sum reduction; empty bag ->
  * zeros).  Enqueued on `stream` (a hipStream_t; NULL = default stream) after
- * the ticket's fill.  `ticket` must be the latest plan, not yet forwarded.
+ * the ticket's fill, or, when the batch had no misses of its own (all its
+ * rows cached before this plan, as with prefetch), after the ticket's commit
+ * and the previous ticket's fill: this plan's fill touches none of its rows.
+ * `ticket` must be the latest plan, not yet forwarded.
  * d_out: caller-owned device fp32 [T][B][D].  Errors: SP_ERR_SEQUENCE,
  * SP_ERR_INVALID_ARG (null d_out with B*T > 0).
  */

@@ -46,7 +46,7 @@ def _bound(w, batches, max_table_ids):
 
 
 def run_gpu(w, batches, host, first=0, last=None, flags=0, prepare_ahead=0, policy="lru",
-            hold_past=0, seed=0, max_table_ids="auto"):
+            hold_past=0, seed=0, max_table_ids="auto", prefetch=False):
     """Train batches[first:last] on the GPU only (fresh context over `host`), then flush.
     prepare_ahead: how many batches after each window to hand over for early sorting."""
     import torch
@@ -57,7 +57,7 @@ def run_gpu(w, batches, host, first=0, last=None, flags=0, prepare_ahead=0, poli
     max_ids = max(int(b[0].size) for b in batches)
     sp = ScratchPipe(w.rows, D, w.slots, L, host, max_batch=B, max_ids=max(max_ids, 1), flags=flags,
                      policy=policy, hold_past=hold_past, seed=seed,
-                     max_table_ids=_bound(w, batches, max_table_ids))
+                     max_table_ids=_bound(w, batches, max_table_ids), prefetch=prefetch)
     try:
         out = torch.zeros((T * B, D), dtype=torch.float32, device=dev)
         for u in range(first, last):

@@ -86,3 +86,71 @@ def test_zipf_8x1M_sampled(harness):
                                    say=_say, prefetch=True)
     _say(f"zipf-8x1M prefetch: worst fwd {r['worst_fwd']:.2e} table {r['worst_table']:.2e} "
          f"misses {r['stats']['misses']} prefetched {r['stats']['prefetched']}")
+
+
+def test_overlapped_equals_serialized_bit_for_bit(harness):
+    """With prefetch the forward and update of a batch run beside its plan's fill: the
+    overlapped schedule gives exactly the tables of runs synchronised after every call,
+    with batches handed over early, and waiting on events instead of stream values."""
+    import numpy as np
+    from paper_2205_04702_amd import scratchpipe as spm
+    w = wl.custom(rows=[3000, 5000, 2000], dim=64, batch=64, pooling=[4, 6, 2],
+                  slots=[900, 1400, 600], lookahead=3, steps=30, dist=("zipf", 1.05), seed=41)
+    _say("case prefetch overlap vs serialised")
+    batches = harness.make_inputs(w)
+    results = []
+    for flags, ahead in ((0, 0), (spm.SP_FLAG_DEBUG_SYNC, 0), (0, 2), (spm.SP_FLAG_EVENT_WAITS, 2)):
+        host = harness.fresh_host(w)
+        st = harness.run_gpu(w, batches, host, flags=flags, prepare_ahead=ahead, prefetch=True)
+        assert st["prefetched"] > 0 and st["evictions"] > 0
+        results.append([host[t].copy() for t in range(w.tables)])
+        host.close()
+    for r in results[1:]:
+        for x, y in zip(results[0], r):
+            assert np.array_equal(x, y)
+
+
+def test_capacity_error_from_the_prefetched_rows_changes_nothing(harness):
+    """A next batch whose new rows do not fit beside the planned batch's is rejected
+    (SP_ERR_CAPACITY) as the oracle rejects it; continuing with the regular window then
+    matches the oracle, which saw only the accepted plans."""
+    import numpy as np
+    import torch
+    from oracle import oracle
+    from paper_2205_04702_amd import scratchpipe as spm
+    w = wl.custom(rows=[1500, 2500], dim=32, batch=24, pooling=[3, 2], slots=[300, 260],
+                  lookahead=1, steps=12, dist=("zipf", 1.0), seed=31)
+    _say("case prefetch capacity error")
+    batches = harness.make_inputs(w)
+    host = harness.fresh_host(w)
+    ref = [wl.init_table(w, t) for t in range(w.tables)]
+    planner = oracle.Planner(w.rows, w.slots, prefetch=True)
+    ctx = spm.ScratchPipe(w.rows, w.dim, w.slots, w.lookahead, host, w.batch, 4096, prefetch=True)
+    # table 1 of the substitute next batch: one bag of slots + 5 distinct rows
+    big_rows = np.arange(1000, 1000 + w.slots[1] + 5, dtype=np.int32)
+    big_ids = np.concatenate([np.zeros(w.batch * 3, np.int32), big_rows])
+    big_off = np.concatenate([np.arange(0, 3 * w.batch + 1, 3),
+                              np.full(w.batch, 3 * w.batch + big_rows.size)]).astype(np.int32)
+    out = torch.zeros((w.tables * w.batch, w.dim), device="cuda:0")
+    try:
+        for u in range(w.steps):
+            win = batches[u:min(u + 1, w.steps - 1) + 1]
+            if u in (2, 6) and len(win) == 2:
+                with pytest.raises(spm.SPError) as e:
+                    ctx.plan([win[0], (big_ids, big_off)])
+                assert e.value.status == spm.SP_ERR_CAPACITY
+                with pytest.raises(oracle.PlanError):
+                    planner.plan([win[0], (big_ids, big_off)], w.batch)
+            t = ctx.plan(win)
+            p = planner.plan(win, w.batch)
+            harness.compare_plan(u, ctx.debug_plan(t, int(win[0][0].size)), p, w.tables, w.batch)
+            ctx.forward(t, out)
+            g = wl.grads(w, u)
+            ctx.backward_update(t, torch.from_numpy(g).to("cuda:0"), w.lr)
+            oracle.train_step(ref, *batches[u], w.batch, g, w.lr)
+        ctx.flush()
+        for t in range(w.tables):
+            assert harness.row_rel_err(host[t], ref[t]).max() <= harness.REL_TOL
+    finally:
+        ctx.close()
+        host.close()

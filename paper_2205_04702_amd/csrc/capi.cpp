@@ -131,6 +131,7 @@ struct Job {
 struct TicketHost {
     int64_t nnz = 0, n_unique = 0, n_chunks = 0, n_multi = 0, n_miss = 0;
     int64_t n_own = 0;  // misses of the planned batch itself (n_miss less prefetched rows)
+    bool ev_planned = false;  // the plan recorded ev_planned (event-wait mode at plan time)
     int32_t B = 0;
     int ring = 0;
     int nwin = 0;
@@ -1151,7 +1152,9 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     CHECK_LAUNCH(h);
     if (h->ws_plan.overflow) return fail(h, SP_ERR_HIP, "internal: scan workspace too small");
     HIPCHK(h, hipStreamWriteValue64(h->s_plan, h->sem + SEM_PLANNED, (uint64_t)k + 1, 0));
-    HIPCHK(h, hipEventRecord(h->ev_planned[e], h->s_plan));
+    // the event only serves event-wait mode; value waits on SEM_PLANNED always work
+    th.ev_planned = (h->flags & SP_FLAG_EVENT_WAITS) != 0;
+    if (th.ev_planned) HIPCHK(h, hipEventRecord(h->ev_planned[e], h->s_plan));
     if (timing) HIPCHK(h, h->t_plan.end(h->s_plan));
     // a large write-back copy of the previous plan goes on the ingest stream
     // behind this call's ingests (its fill has normally finished by now): it
@@ -1187,7 +1190,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     // the device staging slot is free once plan k - NSTAGE's copy has run
     // (issued two plans ago)
     if (k >= NSTAGE) HIPCHK(h, wait_unless_done(h->s_move, h->ev_d2h[sl]));
-    if (h->flags & SP_FLAG_EVENT_WAITS)
+    if (th.ev_planned)
         HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_planned[e], 0));
     else
         HIPCHK(h, hipStreamWaitValue64(h->s_move, h->sem + SEM_PLANNED, (uint64_t)k + 1,
@@ -1265,7 +1268,7 @@ extern "C" sp_status sp_forward(sp_handle h, int64_t ticket, float *d_out, void 
         else HIPCHK(h, hipStreamWaitValue64(s, h->sem + SEM_FILLED, (uint64_t)ticket + 1,
                                             hipStreamWaitValueGte, ~0ull));
     } else {
-        if (ev) {
+        if (ev && th.ev_planned) {
             HIPCHK(h, hipStreamWaitEvent(s, h->ev_planned[e], 0));
             HIPCHK(h, hipStreamWaitEvent(s, h->ev_filled[(ticket - 1) % h->nring], 0));
         } else {

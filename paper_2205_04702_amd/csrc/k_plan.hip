@@ -511,8 +511,11 @@ __global__ void __launch_bounds__(BLOCK) k_commit(uint64_t *hash, uint32_t mask,
     const int64_t t = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
     if (t < n_miss) {
         const int64_t i = t;
+        // independent loads first: later stores could alias them, so the
+        // compiler would otherwise keep each behind the stores before it
         const int32_t v = tk.v_slot[i];
         const int32_t ui = tk.m_uidx[i];
+        const uint32_t key = tk.m_key[i];
         // a prefetched row (prefetch mode, m_uidx = -1) is placed but not used
         const bool fetched = prefetch && ui == -1;
         if ((uint32_t)v >= (uint64_t)nslots || (!fetched && (uint32_t)ui >= (uint64_t)n_unique)) {
@@ -522,17 +525,17 @@ __global__ void __launch_bounds__(BLOCK) k_commit(uint64_t *hash, uint32_t mask,
             return;
         }
         const int32_t old = key_of_slot[v];
+        const int32_t old_lu = last_use[v];
+        const int32_t p0 = fetched ? 0 : seg_off[ui], p1 = fetched ? 0 : seg_off[ui + 1];
         tk.v_old_key[i] = old;
-        tk.v_old_lu[i] = last_use[v];
+        tk.v_old_lu[i] = old_lu;
         if (old >= 0) hash_erase(hash, mask, (uint32_t)old);
-        const uint32_t key = tk.m_key[i];
         key_of_slot[v] = (int32_t)key;
         if (!hash_insert(hash, mask, key, v)) atomicOr(err, ERR_HASH_FULL);
         last_use[v] = u;
         if (uses) uses[v] = fetched ? 0 : 1;
         if (fetched) return;
         tk.slot_u[ui] = v;
-        const int32_t p0 = seg_off[ui], p1 = seg_off[ui + 1];
         for (int32_t p = p0; p < p1; ++p) {
             const uint32_t j = perm[p];
             if (j < (uint64_t)nnz) tk.slot_of[j] = v;

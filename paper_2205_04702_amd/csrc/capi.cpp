@@ -234,6 +234,11 @@ constexpr uint32_t SP_FLAGS_ALL = SP_FLAG_DEBUG_SYNC | SP_FLAG_TIMING | SP_FLAG_
 
 // words of sp_ctx::sem, one cache line apart
 constexpr int SEM_PLANNED = 0, SEM_FILLED = 8, SEM_WORDS = 16;
+// then, per ring entry e (8 words apart), ticket + 1 of the last update of a
+// ticket in entry e: monotonic, since entry e is reused by ticket j + nring
+// only after update j has run (its query waits for it)
+constexpr int SEM_UPD = SEM_WORDS;
+static int sem_words(int nring) { return SEM_UPD + 8 * nring; }
 
 // staging slots of evicted rows (fill of plan p, copy of plan p - 1 and the
 // host scatter of plan p - 2 can all be in flight)
@@ -288,6 +293,7 @@ struct sp_ctx {
     // fill has.  The events are recorded as well, for SP_FLAG_EVENT_WAITS.
     uint64_t *sem = nullptr;
     std::vector<hipStream_t> upd_stream;    // stream each ticket's backward ran on
+    std::vector<char> upd_val;              // its update wrote its SEM_UPD word
     int64_t planned = 0, forwarded = 0, updated = 0;
     int32_t stamp = 0;
     // query of plan spec_ticket over spec_nhold batches, issued early by the
@@ -591,6 +597,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     h->ev_filled.assign(h->nring, nullptr);
     h->ev_upd.assign(h->nring, nullptr);
     h->upd_stream.assign(h->nring, nullptr);
+    h->upd_val.assign(h->nring, 0);
     for (int r = 0; r < h->nring; ++r) {
         BatchDev &b = h->ring[r];
         TRY(dalloc(h, &b.ids, N));
@@ -675,7 +682,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     }
 
     TRY(dalloc(h, &h->cons_counter, 1));
-    TRY(dalloc(h, &h->sem, SEM_WORDS));
+    TRY(dalloc(h, &h->sem, sem_words(h->nring)));
     HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_consumed, hipEventDisableTiming));
     HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_plan, hipStreamNonBlocking));
     HIPCHK(nullptr, hipStreamCreateWithFlags(&h->s_ingest, hipStreamNonBlocking));
@@ -691,7 +698,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
 
     // initial state: nothing cached
     HIPCHK(nullptr, hipMemsetAsync(h->cons_counter, 0, sizeof(uint32_t), h->s_plan));
-    HIPCHK(nullptr, hipMemsetAsync(h->sem, 0, sizeof(uint64_t) * SEM_WORDS, h->s_plan));
+    HIPCHK(nullptr, hipMemsetAsync(h->sem, 0, sizeof(uint64_t) * sem_words(h->nring), h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->key_of_slot, 0xFF, sizeof(int32_t) * S, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->last_use, 0xFF, sizeof(int32_t) * S, h->s_plan));
     if (h->uses) HIPCHK(nullptr, hipMemsetAsync(h->uses, 0, sizeof(int32_t) * S, h->s_plan));
@@ -1204,11 +1211,18 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
         // victim's row (their rows are held), and the fill writes only victim
         // slots, so their updates need no wait.  The rest are waited for, one
         // wait when they share a stream.
+        // (a value wait: a wait on a pending event costs the host far more)
         const int64_t last = k - 1 - h->P;
         for (int64_t j = std::max<int64_t>(0, k + h->L + 1 - h->nring); j <= last; ++j) {
             const int ej = (int)(j % h->nring);
-            if (j == last || h->upd_stream[ej] != h->upd_stream[last % h->nring])
-                HIPCHK(h, wait_unless_done(h->s_move, h->ev_upd[ej]));
+            if (j != last && h->upd_stream[ej] == h->upd_stream[last % h->nring]) continue;
+            if (hipEventQuery(h->ev_upd[ej]) == hipSuccess) continue;  // already done
+            (void)hipGetLastError();
+            if (!h->upd_val[ej])  // that update wrote no word (event-wait mode then)
+                HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_upd[ej], 0));
+            else
+                HIPCHK(h, hipStreamWaitValue64(h->s_move, h->sem + SEM_UPD + 8 * ej, (uint64_t)j + 1,
+                                               hipStreamWaitValueGte, ~0ull));
         }
         if (timing) HIPCHK(h, h->t_fill.begin(h->s_move));  // the fill kernel itself
         launch_move(h->storage, h->D, h->tb, h->host_dev, tk, n_miss, u, h->stage_dev[sl],
@@ -1311,6 +1325,9 @@ extern "C" sp_status sp_backward_update(sp_handle h, int64_t ticket, const float
                     h->partial, s, ev);
     CHECK_LAUNCH(h);
     HIPCHK(h, hipEventRecord(h->ev_upd[e], s));  // also frees ring entry e of the window
+    h->upd_val[e] = !(h->flags & SP_FLAG_EVENT_WAITS);
+    if (h->upd_val[e])  // for the value wait of a later fill
+        HIPCHK(h, hipStreamWriteValue64(s, h->sem + SEM_UPD + 8 * e, (uint64_t)ticket + 1, 0));
     h->upd_stream[e] = s;
     h->last_update_stream = s;
     h->updated = ticket + 1;

@@ -65,3 +65,16 @@ def test_mixed_full_size(harness):
     uniform and half Zipf 1.2, 40 GB Storage budget, L=6: 5 steps."""
     st = _run(harness, "mixed", 5, (0, 4))
     assert st["misses"] > 0
+
+
+def test_zipf_26x4M_full_size_prefetch(harness):
+    """26 x 4M with prefetch: every plan also fills the next batch's missing rows; 32 steps
+    with bit-exact plans (own misses, then prefetched rows, per table) and sampled forwards."""
+    w = wl.get_workload("zipf-26x4M")
+    _say(f"case zipf-26x4M prefetch, 32 steps {w.describe()}")
+    r = harness.run_sampled_parity(w, 32, check_plan_steps=set(range(32)),
+                                   check_fwd_steps={0, 16, 31}, say=_say, prefetch=True)
+    st = r["stats"]
+    _say(f"zipf-26x4M prefetch: worst fwd {r['worst_fwd']:.2e} table {r['worst_table']:.2e} "
+         f"fills {st['misses']} prefetched {st['prefetched']} evictions {st['evictions']}")
+    assert st["evictions"] > 0 and st["prefetched"] > 0

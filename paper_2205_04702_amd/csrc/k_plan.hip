@@ -17,6 +17,19 @@ struct ProbeArgs {
     const int32_t *nu[MAX_WINDOW];
 };
 
+// a[w] for a block-uniform w, chosen among the kernel-argument words without
+// indexing them by a register (which makes the compiler fetch them through
+// memory, one dependent round trip before the real loads can start)
+template <typename P>
+__device__ __forceinline__ P pick_uniform(const P (&a)[MAX_WINDOW], int w)
+{
+    P r = a[0];
+#pragma unroll
+    for (int q = 1; q < MAX_WINDOW; ++q)
+        if (w == q) r = a[q];
+    return r;
+}
+
 // The query of one plan, one launch.  blockIdx.y = window batch.  Every
 // cached key of a window batch stamps its slot as held for this plan
 // (held[slot] = stamp) and counts it once per table; batch 0 (the planned
@@ -84,13 +97,15 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
         seen |= atomicExch(&cnt->n_chunks, scal0[1]) == INT32_MIN;
         seen |= atomicExch(&cnt->n_multi, scal0[3]) == INT32_MIN;
     }
-    if (i == 0 && pa.nu[w][2]) seen |= atomicOr(&cnt->err, pa.nu[w][2]) == INT32_MIN;
-    const bool valid = i < *pa.nu[w];
+    const uint32_t *const ukw = pick_uniform(pa.uk, w);
+    const int32_t *const nuw = pick_uniform(pa.nu, w);
+    if (i == 0 && nuw[2]) seen |= atomicOr(&cnt->err, nuw[2]) == INT32_MIN;
+    const bool valid = i < *nuw;
     int t = 0;
     bool miss = false, fresh = false, fetch = false;
     uint32_t key = 0;
     if (valid) {
-        key = pa.uk[w][i];
+        key = ukw[i];
         t = (int)(key >> row_bits);
         const int32_t slot = hash_find_ro(hash, mask, key);  // the map is not written here
         if (w == 0) {

@@ -1,17 +1,29 @@
 """Embedding-training throughput of the HIP scratchpad on one MI355X.
 
-One step = sp_plan (window ingest, dedup, Hit-Map query, hold, LRU victims,
-commit, miss fill and evicted-row write-back) + sp_forward (pooled gather) +
-sp_backward_update (gradient coalescing and in-place SGD) for one mini-batch
-of the synthetic workload.  Batch IDs and upstream gradients are generated
-before timing and are resident in HBM when the timed region starts; the
-embedding tables live in pinned host memory and only the scratchpad is in HBM.
+One step = sp_plan (window ingest with the batch IDs handed over from host
+memory, dedup, Hit-Map query, hold, LRU victims, commit, miss fill and
+evicted-row write-back) + sp_forward (pooled gather) + sp_backward_update
+(gradient coalescing and in-place SGD) for one mini-batch of the synthetic
+workload.  The embedding tables live in host memory and only the scratchpad
+is in HBM.  Upstream gradients are generated on the device before timing.
 
-Prints one JSON line (rank 0).
+Before the timed steps the scratchpad is filled until every slot holds a row
+(untimed fill-up steps, so the timed steps evict and write back as in steady
+state), then `--warmup` more untimed steps run.  The timed region is
+bracketed by a device synchronisation and sp_sync (every write-back of the
+steps so far has landed in the host tables) on both sides.
+
+The default workload is the largest one: 26 tables x 10M rows x 128 (133 GB
+of host tables, batch 4096, pooling 40, Zipf 0.9, 200k slots per table,
+lookahead 4), with the staged fill (host gather into pinned staging, then
+copies), since one process can pin only about 64 GiB.
+
+Prints one JSON line.
 """
 from __future__ import annotations
 
 import argparse
+import concurrent.futures as cf
 import hashlib
 import json
 import os
@@ -23,7 +35,9 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+HOST_LINK_NOMINAL_GBS = 64.0  # PCIe Gen5 x16, per direction
+PINNED_LIMIT_BYTES = 48 << 30  # tables above this use the staged fill by default
 
 
 def log(*a):
@@ -50,7 +64,7 @@ def kernel_bytes(w, n_unique: float, n_chunks: float) -> dict:
 
 def traffic_from_profile(kernel: str, src_hash: str, workload: str):
     """HBM bytes per launch measured by rocprofv3 counters, if a summary for the
-    current kernel source exists under profiles/ (keyed by the --workload name)."""
+    current kernel source exists under profiles/ (keyed by the workload name)."""
     p = os.path.join(ROOT, "profiles", "hbm_traffic.json")
     if not os.path.exists(p):
         return None
@@ -64,70 +78,72 @@ def traffic_from_profile(kernel: str, src_hash: str, workload: str):
     return None
 
 
-def access_ceiling(w, n_rows: int) -> dict | None:
-    """Bare random-row read-modify-write, random-row gather and sequential copy at the
-    workload's shape (Storage slots, distinct rows per step, row width, bags), timed by
-    the ceiling probe built beside the library.  The fraction of these that a training
-    kernel reaches says how close it is to what HBM gives its access pattern."""
-    import subprocess
-    exe = os.path.join(ROOT, "paper_2205_04702_amd", "ceiling")
-    if not os.path.exists(exe):
-        log("[bench] no ceiling probe built; skipping it")
-        return None
-    cmd = [exe, str(sum(w.slots)), str(max(1, n_rows)), str(w.dim), str(w.tables * w.batch), "1024"]
-    r = subprocess.run(cmd, capture_output=True, text=True, timeout=120)
-    if r.returncode != 0:
-        log(f"[bench] ceiling probe failed ({r.returncode}): {r.stderr.strip()}")
-        return None
-    return json.loads(r.stdout.strip().splitlines()[-1])
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
-def cpu_baseline(w, seconds: float = 15.0, max_steps: int | None = None) -> dict:
-    """The uncached CPU oracle trainer on the same inputs, bounded in time."""
+def cpu_baseline(w, tables, batches, seconds: float) -> dict:
+    """The uncached CPU oracle trainer on the same workload and tables, bounded in
+    time (input generation excluded)."""
     from oracle import oracle
     from paper_2205_04702_amd import workload as wl
-    tables = [wl.init_table(w, t) for t in range(w.tables)]
     cores = min(oracle.max_threads(), w.tables)
-    # one step to size the sample
-    ids, off = wl.batch(w, 0)
+    ids, off = batches[0]
     g = wl.grads(w, 0)
     t0 = time.perf_counter()
     oracle.train_step(tables, ids, off, w.batch, g, w.lr, want_out=True)
     one = time.perf_counter() - t0
-    n = max(1, min(int(seconds / max(one, 1e-6)), max_steps or w.steps))
-    inputs = [(wl.batch(w, s), wl.grads(w, s)) for s in range(1, n + 1)]
+    n = max(1, min(int(seconds / max(one, 1e-6)), len(batches) - 1))
+    inputs = [(batches[s], wl.grads(w, s)) for s in range(1, n + 1)]
     t0 = time.perf_counter()
     for (ids, off), g in inputs:
         oracle.train_step(tables, ids, off, w.batch, g, w.lr, want_out=True)
     dt = time.perf_counter() - t0
     return {"value": round(w.batch * n / dt, 1), "unit": "samples/s", "cores": cores,
             "kind": "oracle",
-            "sample": f"steps 1..{n} of {w.name} (forward + coalesced SGD, fp64 accumulation, "
-                      f"OpenMP over tables), input generation excluded"}
+            "sample": f"steps 1..{n} of {w.name}, all {w.tables} tables (forward + coalesced "
+                      f"SGD, fp64 accumulation, OpenMP over tables, {cores} threads), input "
+                      f"generation excluded",
+            "affinity_cpus": len(os.sched_getaffinity(0)), "cpu_model": cpu_model()}
 
 
 def main():
-    ap = argparse.ArgumentParser(description=__doc__)
+    ap = argparse.ArgumentParser(description=__doc__,
+                                 formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="zipf-8x1M")
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="zipf-26x10M")
     ap.add_argument("--tables", type=int, default=0, metavar="N",
-                    help="run only the workload's first N tables (one GPU's share when the "
-                         "pinned host tables of the whole workload exceed what one process maps)")
+                    help="run only the workload's first N tables")
+    ap.add_argument("--fill", choices=["auto", "mapped", "staged"], default="auto",
+                    help="how missing rows reach HBM: zero-copy from pinned, mapped tables, or "
+                         "host gather into pinned staging then copies (auto: staged when the "
+                         "tables exceed 48 GiB)")
+    ap.add_argument("--ids", choices=["host", "hbm"], default="host",
+                    help="hand the batch IDs over from host memory (as the method does every "
+                         "step) or from device memory")
+    ap.add_argument("--fillup", type=int, default=-1, metavar="N",
+                    help="untimed steps before the warm-up (-1: until every slot holds a row, "
+                         "none when the slots hold every table)")
     ap.add_argument("--policy", choices=["lru", "lfu", "random"], default="lru",
                     help="replacement policy (LRU is the method's default)")
     ap.add_argument("--hold-past", type=int, default=0, metavar="P",
                     help="also hold the rows of the P batches planned before each plan")
-    ap.add_argument("--prefetch", action="store_true",
-                    help="each plan also fills the next batch's missing rows")
-    ap.add_argument("--host-ids", action="store_true",
-                    help="hand the batch IDs over from host memory (PCIe-inclusive variant)")
+    ap.add_argument("--prefetch", type=int, default=0, metavar="D",
+                    help="each plan also fills the missing rows of the next D batches")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-timing", action="store_true", help="do not time kernels with events")
-    ap.add_argument("--time-every", type=int, default=8, metavar="K",
-                    help="time the kernels of every K-th step with events (the rest run untimed)")
+    ap.add_argument("--time-every", type=int, default=0, metavar="K",
+                    help="time the kernels of every K-th step with events (0: every step when "
+                         "a step moves more than 100 MB, else every 8th)")
     ap.add_argument("--event-waits", action="store_true",
                     help="wait on events instead of stream values (for profilers that run one "
                          "dispatch at a time, such as counter collection)")
@@ -135,8 +151,6 @@ def main():
                     help="synchronise the device at the end of every call, so each kernel runs "
                          "alone (kernel times without overlap; throughput is then not the "
                          "pipelined one)")
-    ap.add_argument("--no-ceiling", action="store_true",
-                    help="skip the access-pattern ceiling probe run after the timed region")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="after the timed region, run a plain elementwise copy (torch.neg) of MIB "
                          "MiB three times: the reference kernel for scaling HBM byte counters")
@@ -159,48 +173,78 @@ def main():
         n = args.tables
         w = dataclasses.replace(w, name=f"{w.name}-first{n}", rows=w.rows[:n],
                                 pooling=w.pooling[:n], dist=w.dist[:n], slots=w.slots[:n])
+    table_bytes = sum(w.rows) * w.dim * 4
+    fill = args.fill if args.fill != "auto" else (
+        "staged" if table_bytes > PINNED_LIMIT_BYTES else "mapped")
+    evicts = sum(w.slots) < sum(w.rows)
+    if args.fillup >= 0:
+        fillup_max = args.fillup
+    else:
+        # enough steps to place a row in every slot at the first batch's miss count
+        fillup_max = 0 if not evicts else 200
     W, K, L = args.warmup, args.steps, w.lookahead
     ahead = sp.SP_MAX_AHEAD
-    nb = W + K + L + 1 + ahead  # the window of the last step plus the batches prepared after it
-    log(f"[bench] workload {w.name}: generating {nb} batches and {W + K} gradient tensors")
+    nsteps = fillup_max + W + K
+    nb_needed = lambda steps: steps + L + 1 + ahead  # noqa: E731  (windows of the last step)
+
     t0 = time.perf_counter()
-    host_batches = [wl.batch(w, s) for s in range(nb)]
-    if args.host_ids:
-        batches = host_batches
-    else:
-        batches = [(torch.from_numpy(i).to(dev), torch.from_numpy(o).to(dev)) for i, o in host_batches]
-    grads = [torch.from_numpy(wl.grads(w, s)).to(dev) for s in range(W + K)]
-    host = sp.HostTables(w.rows, w.dim)
-    # tables are independent streams: fill them on a few threads (numpy's
-    # generators release the GIL)
-    import concurrent.futures as cf
+    host = sp.host_tables(w.rows, w.dim, fill)
+    # tables are independent streams: fill them on threads (numpy's generators
+    # release the GIL)
     with cf.ThreadPoolExecutor(max_workers=max(1, min(16, w.tables, os.cpu_count() or 1))) as ex:
         list(ex.map(lambda t: wl.init_table(w, t, out=host[t]), range(w.tables)))
-    log(f"[bench] inputs ready in {time.perf_counter() - t0:.1f}s")
+    log(f"[bench] workload {w.name}: {table_bytes / 1e9:.1f} GB of {fill} host tables "
+        f"ready in {time.perf_counter() - t0:.1f}s")
 
+    # batches are generated as the steps need them, outside the timed region
+    host_batches: list = []
+    dev_batches: list = []
+    pool = cf.ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1))
+
+    def ensure_batches(n, chunk=1):
+        if n <= len(host_batches):
+            return
+        n = max(n, len(host_batches) + chunk)
+        new = list(pool.map(lambda s: wl.batch(w, s), range(len(host_batches), n)))
+        host_batches.extend(new)
+        if args.ids == "hbm":
+            dev_batches.extend((torch.from_numpy(i).to(dev), torch.from_numpy(o).to(dev))
+                               for i, o in new)
+
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(w.seed)
+    grads: list = []
+
+    def ensure_grads(n):
+        while len(grads) < n:
+            g = torch.randn((w.tables * w.batch, w.dim), generator=gen, device=dev)
+            if w.grad_sigma != 1.0:
+                g *= w.grad_sigma
+            grads.append(g)
+
+    every = args.time_every or (1 if w.nnz * w.dim * 4 > 100e6 else 8)
     timed = not args.no_timing
-    every = max(1, args.time_every)
     base_flags = ((sp.SP_FLAG_EVENT_WAITS if args.event_waits else 0)
                   | (sp.SP_FLAG_DEBUG_SYNC if args.serialize else 0))
     ctx = sp.ScratchPipe(w.rows, w.dim, w.slots, L, host, max_batch=w.batch, max_ids=w.nnz,
                          flags=base_flags, policy=args.policy, hold_past=args.hold_past,
-                         prefetch=args.prefetch,
+                         prefetch=args.prefetch, fill=fill,
                          max_table_ids=w.batch * max(w.pooling))
     out = torch.empty((w.tables * w.batch, w.dim), dtype=torch.float32, device=dev)
 
     host_s = [0.0, 0.0, 0.0]  # host time inside plan / forward / backward calls
     stream = torch.cuda.current_stream().cuda_stream  # forward and backward run here
+    src = dev_batches if args.ids == "hbm" else host_batches
 
-    def step(u):
+    def step(u, last_batch):
         # hold window u..u+L, plus the next batches handed over early for sorting;
         # kernel events on a sample of the steps only (they cost host time)
-        base = base_flags
         if timed:
-            ctx.set_flags(base | (sp.SP_FLAG_TIMING if u % every == 0 else 0))
-        elif base:
-            ctx.set_flags(base)
+            ctx.set_flags(base_flags | (sp.SP_FLAG_TIMING if u % every == 0 else 0))
+        elif base_flags:
+            ctx.set_flags(base_flags)
         t0 = time.perf_counter()
-        tk = ctx.plan([batches[q] for q in range(u, min(u + L + ahead, nb - 1) + 1)])
+        tk = ctx.plan([src[q] for q in range(u, min(u + L + ahead, last_batch) + 1)])
         t1 = time.perf_counter()
         ctx.forward(tk, out, stream)
         t2 = time.perf_counter()
@@ -210,17 +254,38 @@ def main():
         host_s[1] += t2 - t1
         host_s[2] += t3 - t2
 
-    for u in range(W):
-        step(u)
+    # ---- untimed: fill-up until every slot holds a row, then warm-up
+    t0 = time.perf_counter()
+    u = 0
+    fillup = 0
+    total_slots = sum(w.slots)
+    while fillup < fillup_max:
+        ensure_batches(nb_needed(u + 1), chunk=16)
+        ensure_grads(u + 1)
+        step(u, len(host_batches) - 1)
+        u += 1
+        fillup += 1
+        if ctx.stats()["misses"] >= total_slots:
+            break
+    log(f"[bench] fill-up: {fillup} steps ({time.perf_counter() - t0:.1f}s)")
+    ensure_batches(nb_needed(u + W + K))
+    ensure_grads(u + W + K)
+    last = len(host_batches) - 1
+    for _ in range(W):
+        step(u, last)
+        u += 1
     torch.cuda.synchronize()
+    ctx.sync()
     s0 = ctx.stats()
     log(f"[bench] warmup {W} steps done")
-    torch.cuda.synchronize()
     host_s[:] = [0.0, 0.0, 0.0]
+    first_timed = u
     t0 = time.perf_counter()
-    for u in range(W, W + K):
-        step(u)
+    for _ in range(K):
+        step(u, last)
+        u += 1
     torch.cuda.synchronize()
+    ctx.sync()
     dt = time.perf_counter() - t0
     s1 = ctx.stats()
     if args.calibrate_copy > 0:
@@ -231,7 +296,6 @@ def main():
         torch.cuda.synchronize()
         del x, y
     ctx.close()
-    host.close()
     log(f"[bench] timed {K} steps in {dt:.3f}s")
 
     d = {k: s1[k] - s0[k] for k in s1 if isinstance(s1[k], (int, float))}
@@ -250,13 +314,14 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {**w.describe(), "ids": "host" if args.host_ids else "hbm",
+        "config": {**w.describe(), "ids": args.ids, "fill": fill,
+                   "timed_steps": [first_timed, first_timed + K - 1], "fillup_steps": fillup,
                    **({"policy": args.policy} if args.policy != "lru" else {}),
                    **({"hold_past": args.hold_past} if args.hold_past else {}),
                    **({"serialized": True} if args.serialize else {}),
-                   **({"prefetch": True} if args.prefetch else {})},
+                   **({"prefetch": args.prefetch} if args.prefetch else {})},
     }
-    # the planned batches' own misses; with prefetch, fills also cover the next batches
+    # the planned batches' own misses; with prefetch, fills also cover later batches
     detail = {"miss_rate": round((d["misses"] - d.get("prefetched", 0)) / max(d["unique"], 1), 4),
               "fills_per_step": round(d["misses"] / K, 1),
               "unique_per_step": round(n_unique, 1),
@@ -268,57 +333,59 @@ def main():
                                    "forward": round(host_s[1] * 1e3 / K, 4),
                                    "backward": round(host_s[2] * 1e3 / K, 4),
                                    **{k[8:]: round(d[k] / K, 4) for k in d if k.startswith("host_ms_")}}}
-    if not args.no_timing and d["timed_forward"] > 0:
+    if timed and d["timed_forward"] > 0:
         # kernel execution times from start/stop events of the launches themselves
         fwd_ms = d["ms_forward"] / d["timed_forward"]
         bwd_ms = d["ms_backward"] / max(d["timed_backward"], 1)
+        cmb_ms = d["ms_combine"] / max(d["timed_combine"], 1)
         n_chunks = d["chunks"] / max(d["updates"], 1)
         kb = kernel_bytes(w, n_unique, n_chunks)
-        fwd_gbs = kb["forward"] / (fwd_ms * 1e-3) / 1e9
-        bwd_gbs = kb["backward"] / (bwd_ms * 1e-3) / 1e9
-        detail.update({"forward_ms": round(fwd_ms, 5), "backward_ms": round(bwd_ms, 5),
-                       "combine_ms": round(d["ms_combine"] / max(d["timed_combine"], 1), 5),
-                       "combine_launches": d["timed_combine"],
+        src_hash = hashlib.sha256(open(os.path.join(ROOT, "paper_2205_04702_amd", "csrc",
+                                                    "k_train.hip"), "rb").read()).hexdigest()
+        wname = w.name if args.tables else args.workload
+        kern = {}
+        for name, key, ms in (("k_forward", "forward", fwd_ms), ("k_backward", "backward", bwd_ms)):
+            gbs = kb[key] / (ms * 1e-3) / 1e9
+            kern[name] = {"achieved": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4),
+                          "bytes_per_launch": int(kb[key]), "ms_per_launch": round(ms, 5),
+                          "traffic": traffic_from_profile(name, src_hash, wname)}
+        kern["k_forward"]["requested_GBps"] = round(kb["forward_requested"] / (fwd_ms * 1e-3) / 1e9, 1)
+        # the dominant kernel: the one with more time per step
+        dom = "k_forward" if fwd_ms >= bwd_ms else "k_backward"
+        res["roofline"] = {"bound": "hbm", "kernel": dom, "achieved": kern[dom]["achieved"],
+                           "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": kern[dom]["frac"],
+                           "traffic": kern[dom]["traffic"],
+                           "bytes_per_launch": kern[dom]["bytes_per_launch"],
+                           "ms_per_launch": kern[dom]["ms_per_launch"],
+                           "kernels": kern, "timed_launches": int(d["timed_forward"])}
+        detail.update({"combine_ms": round(cmb_ms, 5), "combine_launches": d["timed_combine"],
                        "plan_ms": round(d["ms_plan"] / max(d["timed_plan"], 1), 5),
                        "fill_ms": round(d["ms_fill"] / max(d["timed_fill"], 1), 5),
                        "ingest_ms": round(d["ms_ingest"] / max(d["timed_ingest"], 1), 5),
                        "query_ms": round(d["ms_query"] / max(d["timed_query"], 1), 5),
-                       "chunks_per_step": round(n_chunks, 1),
-                       "forward_GBps_unique": round(fwd_gbs, 1),
-                       "forward_GBps_requested": round(kb["forward_requested"] / (fwd_ms * 1e-3) / 1e9, 1),
-                       "backward_GBps": round(bwd_gbs, 1)})
-        # the fill is bound by the host link, not by HBM: its misses' rows
-        # cross the link once per fill (timed with the same events)
-        fill_ms = d["ms_fill"] / max(d["timed_fill"], 1)
+                       "chunks_per_step": round(n_chunks, 1)})
+        # the host link: fills host -> device (the zero-copy move kernel, or the
+        # staged fill's copies), write-backs device -> host over the whole step
+        fill_ms = (d["ms_h2d"] / max(d["timed_h2d"], 1)) if fill == "staged" else \
+            d["ms_fill"] / max(d["timed_fill"], 1)
+        link = {"unit": "GB/s", "nominal_GBps": HOST_LINK_NOMINAL_GBS,
+                "h2d_bytes_per_step": int(d["bytes_fill"] / K),
+                "d2h_bytes_per_step": int(d["bytes_writeback"] / K),
+                "h2d_step_average_GBps": round(d["bytes_fill"] / dt / 1e9, 2),
+                "d2h_step_average_GBps": round(d["bytes_writeback"] / dt / 1e9, 2)}
         if fill_ms > 0:
-            link = d["bytes_fill"] / max(d["plans"], 1) / (fill_ms * 1e-3) / 1e9
-            detail["host_link"] = {"kernel": "k_move", "achieved_GBps": round(link, 1),
-                                   "nominal_GBps": 64.0, "unit": "GB/s host to device",
-                                   "frac_nominal": round(link / 64.0, 3)}
-        src = open(os.path.join(ROOT, "paper_2205_04702_amd", "csrc", "k_train.hip"), "rb").read()
-        src_hash = hashlib.sha256(src).hexdigest()
-        dom = "forward" if fwd_ms >= bwd_ms else "backward"
-        ach = fwd_gbs if dom == "forward" else bwd_gbs
-        name = "k_forward" if dom == "forward" else "k_backward"
-        tr = traffic_from_profile(name, src_hash, args.workload if not args.tables else w.name)
-        res["roofline"] = {"bound": "hbm", "kernel": name,
-                           "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                           "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": tr,
-                           "bytes_per_launch": int(kb[dom]),
-                           "ms_per_launch": round(fwd_ms if dom == "forward" else bwd_ms, 5)}
-    if not args.no_ceiling and "roofline" in res:
-        ceil = access_ceiling(w, int(round(n_unique)))
-        if ceil:
-            detail["ceiling"] = ceil
-            pat = "gather" if res["roofline"]["kernel"] == "k_forward" else "rmw"
-            c_gbs = ceil[pat]["GBps"]
-            res["roofline"]["pattern_ceiling"] = {
-                "pattern": pat, "GBps": c_gbs, "frac": round(res["roofline"]["achieved"] / c_gbs, 4),
-                "copy_GBps": ceil["copy"]["GBps"]}
+            g = d["bytes_fill"] / max(d["plans"], 1) / (fill_ms * 1e-3) / 1e9
+            link.update({"h2d_during_fill_GBps": round(g, 2),
+                         "h2d_fill_span_ms": round(fill_ms, 4),
+                         "h2d_span": "host-to-device copies of gathered rows" if fill == "staged"
+                         else "zero-copy move kernel"})
+        detail["host_link"] = link
     res["detail"] = detail
     if not args.no_cpu_baseline:
-        log("[bench] timing the CPU oracle")
-        res["cpu_baseline"] = cpu_baseline(w, seconds=args.cpu_seconds)
+        log("[bench] timing the CPU oracle on the same tables")
+        res["cpu_baseline"] = cpu_baseline(w, host.arrays, host_batches, args.cpu_seconds)
+    host.close()
+    pool.shutdown()
     print(json.dumps(res), flush=True)
 
 

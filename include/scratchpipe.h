@@ -68,6 +68,21 @@ typedef int32_t sp_status;
                                     stream values (hipStreamWaitValue64); for tools
                                     that run one dispatch at a time, under which a
                                     value wait would wait for a dispatch held back */
+#define SP_FLAG_POISON 0x8u     /* debugging aid, read by sp_create: Storage starts as
+                                    NaN instead of zeros, and with the staged fill the
+                                    device staging of filled rows is set to NaN once
+                                    the fill has used it, so a read of a slot before
+                                    its fill landed, or of stale staging, shows up as
+                                    NaN in outputs and tables                        */
+
+/* sp_config.fill: how missing rows reach the scratchpad (Sec. IV-B) */
+#define SP_FILL_MAPPED 0 /* the move kernel reads them straight from pinned,
+                            device-mapped host tables over the host link          */
+#define SP_FILL_STAGED 1 /* host threads gather them from the tables into pinned
+                            staging ([Collect]), copies take them to the device in
+                            pieces as they are gathered ([Exchange]) and the move
+                            kernel writes them into their slots ([Insert]); the
+                            tables may then be any host memory                    */
 
 typedef struct sp_ctx *sp_handle;
 
@@ -77,10 +92,12 @@ typedef struct {
     int32_t dim;                /* D, fp32 elements per row; multiple of 4, <= 256     */
     const int64_t *slots;       /* [T] scratchpad slots per table, 1 .. rows[t]         */
     int32_t lookahead;          /* L >= 0: successor batches a plan may hold           */
-    float *const *host_tables;  /* [T] row-major [rows][D] fp32 tables in pinned host
-                                   memory from sp_host_alloc (or hipHostMalloc with the
-                                   mapped flag); caller-owned, must outlive the context;
-                                   read on misses, written on evictions and flush      */
+    float *const *host_tables;  /* [T] row-major [rows][D] fp32 host tables, caller-owned,
+                                   must outlive the context; read on misses, written on
+                                   evictions and flush.  SP_FILL_MAPPED: pinned,
+                                   device-mapped memory from sp_host_alloc (or
+                                   hipHostMalloc with the mapped flag); SP_FILL_STAGED:
+                                   any host memory                                   */
     int32_t max_batch;          /* largest B any batch will have; T * max_batch * dim * 4
                                    (the bytes of one [T*B][D] gradient) must stay
                                    below 4 GiB                                         */
@@ -109,6 +126,7 @@ typedef struct {
                                    then the prefetched rows, each ascending; the
                                    capacity check counts both, so SP_ERR_CAPACITY can
                                    come one plan earlier than without prefetch      */
+    int32_t fill;               /* SP_FILL_MAPPED (0) or SP_FILL_STAGED               */
 } sp_config;
 
 typedef struct {
@@ -157,6 +175,12 @@ typedef struct {
      * evictions and bytes_fill, not in hits: hits count the planned batch's
      * keys found cached, prefetched ones included) */
     int64_t prefetched;
+    /* SP_FILL_STAGED: host time of the fill thread gathering missing rows into
+     * pinned staging, and host time the calling thread spent waiting for the
+     * fill thread to enqueue a plan's fill (ms); SP_FLAG_TIMING: the span of a
+     * plan's host-to-device copies of gathered rows, first start to last end */
+    double host_ms_gather, host_ms_fill_join, ms_h2d;
+    int64_t timed_h2d;
 } sp_stats;
 
 /* Per-plan decisions copied to the host for checking.  The caller allocates
@@ -187,8 +211,11 @@ typedef struct {
  * Create a context: allocates Storage (sum(slots) x D fp32), the Hit-Map hash,
  * per-slot metadata, the window ring and staging buffers on config->device,
  * and two library streams at default priority.  Nothing is cached initially.
- * Errors: SP_ERR_INVALID_ARG (config out of range, host table not pinned and
- * mapped), SP_ERR_OOM, SP_ERR_HIP.  *out is set only on success.
+ * Errors: SP_ERR_INVALID_ARG (config out of range; with SP_FILL_MAPPED a host
+ * table that is not pinned and mapped), SP_ERR_OOM, SP_ERR_HIP.  *out is set
+ * only on success; on failure everything allocated so far is freed.  For
+ * testing that path, the environment variable SP_FAIL_ALLOC_AFTER=n makes the
+ * allocation after the first n of this call fail with SP_ERR_OOM.
  * (Sec. IV-D "GPU scratchpad design": Storage and Hit-Map.)
  */
 sp_status sp_create(const sp_config *config, sp_handle *out);
@@ -257,6 +284,14 @@ sp_status sp_backward_update(sp_handle h, int64_t ticket, const float *d_grad, f
  * be written back, Sec. IV-B; flush applies that to all entries.)
  */
 sp_status sp_flush(sp_handle h);
+
+/*
+ * Wait until every effect of the calls so far is complete: all device work
+ * (the library's and the device) has finished and every row evicted so far
+ * has been written back to its host table.  Unlike sp_flush it writes no
+ * cached row back.  Training may continue afterwards.
+ */
+sp_status sp_sync(sp_handle h);
 
 /* Counters since sp_create (synchronises pending timing events). */
 sp_status sp_get_stats(sp_handle h, sp_stats *out);

@@ -1,5 +1,4 @@
-"""Compile the HIP scratchpad library for gfx950 into paper_2205_04702_amd/libscratchpipe.so,
-and the access-pattern ceiling probe into paper_2205_04702_amd/ceiling."""
+"""Compile the HIP scratchpad library for gfx950 into paper_2205_04702_amd/libscratchpipe.so."""
 import concurrent.futures as cf
 import os
 import subprocess
@@ -9,7 +8,6 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libscratchpipe.so")
-CEILING = os.path.join(HERE, "ceiling")
 SOURCES = ["k_ingest.hip", "k_plan.hip", "k_train.hip", "capi.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -36,25 +34,10 @@ def _compile(src: str, verbose: bool) -> str:
     return out
 
 
-def build_ceiling(verbose: bool = False) -> str:
-    """The access-pattern ceiling probe the benchmark reports beside the roofline
-    (a stand-alone program; the library does not use it)."""
-    cmd = [HIPCC, *COMMON, "-x", "hip", os.path.join(CSRC, "ceiling.hip"), "-o", CEILING + ".tmp"]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        raise RuntimeError(f"compile of ceiling.hip failed:\n{r.stderr}")
-    os.replace(CEILING + ".tmp", CEILING)
-    return CEILING
-
-
 def build(verbose: bool = False) -> str:
     os.makedirs(OBJ, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=len(SOURCES) + 1) as ex:
-        probe = ex.submit(build_ceiling, verbose)
+    with cf.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
         objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-        probe.result()
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", LIB + ".tmp", *objs,
            "-lpthread"]
     if verbose:

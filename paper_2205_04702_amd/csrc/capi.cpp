@@ -19,12 +19,14 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <chrono>
 #include <condition_variable>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
 #include <deque>
+#include <functional>
 #include <mutex>
 #include <string>
 #include <thread>
@@ -137,36 +139,66 @@ struct TicketHost {
     int nwin = 0;
 };
 
-thread_local std::string g_create_error;
+// A wait of the move stream: on an event, or (ev null) until *addr >= val.
+struct Wait {
+    hipEvent_t ev = nullptr;
+    uint64_t *addr = nullptr;
+    uint64_t val = 0;
+};
 
-// Host threads that copy evicted rows from the pinned staging buffer into the
-// host tables (the CPU-side [Insert] of Sec. IV-B).  Rows land at random
-// places in tables far larger than any cache, so the copy is latency-bound
-// and spreads over several threads.
-class ScatterPool {
+// Everything a plan's fill needs on the move stream: what to wait for, then
+// the move kernel (stage each victim's old row, write the missing row into
+// its slot), then the fill's event and value.  The caller builds it; the
+// mapped fill enqueues it at once, the staged fill hands it to the fill
+// thread, which first gathers and copies the rows.
+struct MoveJob {
+    int64_t k = 0, n = 0;  // plan, rows to place
+    int sl = 0, e = 0;     // staging slot, ticket entry
+    int32_t u = 0;
+    bool timing = false;
+    int nwait = 0;
+    Wait wait[MAX_WINDOW + 8];
+};
+
+thread_local std::string g_create_error;
+// allocations sp_create may still make before one is made to fail (testing
+// aid: SP_FAIL_ALLOC_AFTER); negative = no limit
+thread_local int64_t g_alloc_budget = -1;
+
+// Host threads that split row copies between them: the scatter of evicted
+// rows from pinned staging into the host tables (the CPU-side [Insert] of
+// Sec. IV-B) and, with the staged fill, the gather of missing rows from the
+// host tables into pinned staging ([Collect]).  Rows sit at random places in
+// tables far larger than any cache, so the copies are latency-bound and
+// spread over several threads.  The calling thread takes part; work is
+// handed out in pieces of `grain` items from a shared counter.  One caller at
+// a time (each user owns its pool).
+class Pool {
   public:
-    void start(int nthreads, float *const *tables, int dim, int row_bits)
+    void start(int helpers)
     {
-        tables_ = tables;
-        dim_ = dim;
-        row_bits_ = row_bits;
-        for (int i = 0; i < nthreads; ++i) threads_.emplace_back([this, i, nthreads] { loop(i, nthreads); });
+        for (int i = 0; i < helpers; ++i) threads_.emplace_back([this] { loop(); });
     }
-    // Scatter n staged rows (row i goes to the table row named by keys[i];
-    // negative keys are skipped).  Returns the number of rows written.
-    int64_t run(const float *rows, const int32_t *keys, int64_t n)
+    // fn(b, e) over [0, n) in pieces; returns when every piece has run.
+    template <typename F>
+    void run(int64_t n, int64_t grain, F &&fn)
     {
-        if (threads_.empty() || n < 2048) return slice(rows, keys, 0, n);
-        std::unique_lock<std::mutex> lk(m_);
-        rows_ = rows;
-        keys_ = keys;
-        n_ = n;
-        written_ = 0;
-        pending_ = (int)threads_.size();
-        ++gen_;
+        if (n <= 0) return;
+        if (threads_.empty() || n <= grain) {
+            fn((int64_t)0, n);
+            return;
+        }
+        Work w{[&fn](int64_t b, int64_t e) { fn(b, e); }, n, grain};
+        {
+            std::lock_guard<std::mutex> lk(m_);
+            work_ = &w;
+            ++gen_;
+        }
         cv_start_.notify_all();
-        cv_done_.wait(lk, [&] { return pending_ == 0; });
-        return written_;
+        take(w);
+        std::unique_lock<std::mutex> lk(m_);
+        work_ = nullptr;  // helpers that have not joined yet stay out
+        cv_done_.wait(lk, [&] { return w.busy == 0; });
     }
     void stop()
     {
@@ -178,59 +210,78 @@ class ScatterPool {
         for (auto &t : threads_) t.join();
         threads_.clear();
     }
+    int helpers() const { return (int)threads_.size(); }
 
   private:
-    int64_t slice(const float *rows, const int32_t *keys, int64_t b, int64_t e) const
+    struct Work {
+        std::function<void(int64_t, int64_t)> fn;
+        int64_t n, grain;
+        std::atomic<int64_t> next{0};
+        int busy = 0;  // helpers inside take(), under m_
+    };
+    static void take(Work &w)
     {
-        const uint32_t mask = (1u << row_bits_) - 1u;
-        const size_t row_bytes = sizeof(float) * (size_t)dim_;
-        int64_t w = 0;
-        for (int64_t i = b; i < e; ++i) {
-            const int32_t key = keys[i];
-            if (key < 0) continue;
-            memcpy(tables_[key >> row_bits_] + (int64_t)(key & mask) * dim_, rows + i * dim_,
-                   row_bytes);
-            ++w;
+        for (;;) {
+            const int64_t b = w.next.fetch_add(w.grain);
+            if (b >= w.n) return;
+            w.fn(b, std::min(w.n, b + w.grain));
         }
-        return w;
     }
-    void loop(int id, int nthreads)
+    void loop()
     {
         int64_t seen = 0;
         for (;;) {
-            const float *rows;
-            const int32_t *keys;
-            int64_t n;
+            Work *w;
             {
                 std::unique_lock<std::mutex> lk(m_);
                 cv_start_.wait(lk, [&] { return gen_ != seen || stop_; });
                 if (stop_) return;
                 seen = gen_;
-                rows = rows_;
-                keys = keys_;
-                n = n_;
+                w = work_;
+                if (!w) continue;
+                ++w->busy;
             }
-            const int64_t w = slice(rows, keys, n * id / nthreads, n * (id + 1) / nthreads);
+            take(*w);
             std::lock_guard<std::mutex> lk(m_);
-            written_ += w;
-            if (--pending_ == 0) cv_done_.notify_one();
+            if (--w->busy == 0) cv_done_.notify_all();
         }
     }
     std::vector<std::thread> threads_;
     std::mutex m_;
     std::condition_variable cv_start_, cv_done_;
-    float *const *tables_ = nullptr;
-    int dim_ = 0, row_bits_ = 0;
-    const float *rows_ = nullptr;
-    const int32_t *keys_ = nullptr;
-    int64_t n_ = 0, written_ = 0, gen_ = 0;
-    int pending_ = 0;
+    Work *work_ = nullptr;
+    int64_t gen_ = 0;
     bool stop_ = false;
 };
 
+// Copy rows between host tables and a staging buffer: staging row i holds
+// table row keys[i] (table key >> row_bits, row key & mask); negative keys,
+// and keys outside the tables, are skipped.  to_tables: scatter staging ->
+// tables, else gather.  Returns the rows copied.
+int64_t copy_rows(float *const *tables, const Tables &tb, int dim, float *stage,
+                  const int32_t *keys, int64_t b, int64_t e, bool to_tables)
+{
+    const uint32_t mask = (1u << tb.row_bits) - 1u;
+    const size_t row_bytes = sizeof(float) * (size_t)dim;
+    int64_t w = 0;
+    for (int64_t i = b; i < e; ++i) {
+        const int32_t key = keys[i];
+        if (key < 0) continue;
+        const int t = key >> tb.row_bits;
+        const int64_t r = key & mask;
+        if (t >= tb.T || r >= tb.rows[t]) continue;
+        float *row = tables[t] + r * dim;
+        if (to_tables) memcpy(row, stage + i * dim, row_bytes);
+        else memcpy(stage + i * dim, row, row_bytes);
+        ++w;
+    }
+    return w;
+}
+
 }  // namespace
 
-constexpr uint32_t SP_FLAGS_ALL = SP_FLAG_DEBUG_SYNC | SP_FLAG_TIMING | SP_FLAG_EVENT_WAITS;
+constexpr uint32_t SP_FLAGS_ALL =
+    SP_FLAG_DEBUG_SYNC | SP_FLAG_TIMING | SP_FLAG_EVENT_WAITS | SP_FLAG_POISON;
 
 // words of sp_ctx::sem, one cache line apart
 constexpr int SEM_PLANNED = 0, SEM_FILLED = 8, SEM_WORDS = 16;
@@ -353,7 +404,39 @@ struct sp_ctx {
     hipError_t worker_err = hipSuccess;
     std::deque<std::pair<int64_t, int64_t>> deadlines;  // (ticket, first plan that may refill)
     int64_t wb_evictions = 0, wb_bytes = 0;
-    ScatterPool scatter;
+    Pool scatter;
+
+    // staged fill (SP_FILL_STAGED): a plan's missing keys come to the host
+    // (h_mkey, copied behind the victim choice), host threads gather their
+    // rows from the tables into pinned staging (h_fill) and copies take them
+    // to the device (d_fill) piece by piece as they are gathered; the move
+    // kernel then writes them into their slots.  The fill thread does this
+    // per plan, in plan order, and enqueues everything of a plan's fill on the
+    // move stream, where the calling thread then enqueues nothing.  Staging
+    // slot k % NSTAGE, like the write-back's.
+    bool staged = false;
+    int32_t *h_mkey[NSTAGE]{};
+    float *h_fill[NSTAGE]{}, *d_fill[NSTAGE]{};
+    hipEvent_t ev_mkey[NSTAGE]{}, ev_fill_h2d[NSTAGE]{};
+    bool fill_h2d_used[NSTAGE]{};
+    std::thread filler;
+    std::mutex fmu;
+    std::condition_variable fcv, fcv_done;
+    std::deque<MoveJob> fjobs;
+    int64_t fill_enqueued = 0;  // plans whose fill is fully enqueued: tickets below this
+    bool fstop = false;
+    std::string fill_err;       // first error of the fill thread (then the context is broken)
+    Pool gather;
+    double gather_ms = 0, fill_join_ms = 0;
+    Timer t_h2d;
+    bool poison = false;
+
+    // pinned copies of window arrays handed over in host memory, per ring
+    // entry: the caller's arrays are copied here on the host, then to the
+    // device asynchronously (ev_ids: that copy has run)
+    std::vector<int32_t *> h_ids, h_off;
+    std::vector<hipEvent_t> ev_ids;
+    std::vector<char> ids_pending;
 
     // bookkeeping
     sp_stats st{};
@@ -403,10 +486,22 @@ static sp_status usable(sp_ctx *h)
     return SP_OK;
 }
 
+// True when the allocation budget of SP_FAIL_ALLOC_AFTER is spent.
+static bool injected_alloc_failure()
+{
+    if (g_alloc_budget == 0) return true;
+    if (g_alloc_budget > 0) --g_alloc_budget;
+    return false;
+}
+
 template <typename T>
 static sp_status dalloc(sp_ctx *h, T **p, int64_t count)
 {
     size_t bytes = (size_t)std::max<int64_t>(count, 1) * sizeof(T);
+    if (injected_alloc_failure()) {
+        *p = nullptr;
+        return fail(h, SP_ERR_OOM, "hipMalloc(%zu) failed: injected (SP_FAIL_ALLOC_AFTER)", bytes);
+    }
     hipError_t e = hipMalloc((void **)p, bytes);
     if (e != hipSuccess) {
         *p = nullptr;
@@ -422,6 +517,10 @@ template <typename T>
 static sp_status palloc(sp_ctx *h, T **p, int64_t count)
 {
     size_t bytes = (size_t)std::max<int64_t>(count, 1) * sizeof(T);
+    if (injected_alloc_failure()) {
+        *p = nullptr;
+        return fail(h, SP_ERR_OOM, "hipHostMalloc(%zu) failed: injected (SP_FAIL_ALLOC_AFTER)", bytes);
+    }
     hipError_t e = hipHostMalloc((void **)p, bytes, hipHostMallocDefault);
     if (e != hipSuccess) {
         *p = nullptr;
@@ -460,7 +559,12 @@ static void worker_main(sp_ctx *h)
                 std::lock_guard<std::mutex> lk(h->mu);
                 h->worker_err = e;
             } else {
-                ev = h->scatter.run(j.rows, j.keys, j.n);
+                std::atomic<int64_t> wr{0};
+                h->scatter.run(j.n, 512, [&](int64_t b, int64_t e2) {
+                    wr += copy_rows(h->host, h->tb, h->D, const_cast<float *>(j.rows), j.keys,
+                                    b, e2, true);
+                });
+                ev = wr.load();
             }
         }
         {
@@ -483,11 +587,134 @@ static sp_status join_jobs(sp_ctx *h, int64_t upto)
     return SP_OK;
 }
 
+// ---------------------------------------------------------------- fill
+
+// Enqueue a plan's fill on the move stream: its waits, the move kernel
+// (rows from the mapped host tables, or from `staged` device rows), then the
+// fill's event and counter value.  Called by the calling thread (mapped fill)
+// or the fill thread (staged fill), never by both for one context.
+static hipError_t enqueue_move(sp_ctx *h, const MoveJob &j, const float *staged)
+{
+    hipStream_t s = h->s_move;
+    hipError_t r = hipSuccess;
+    for (int i = 0; i < j.nwait && r == hipSuccess; ++i) {
+        const Wait &w = j.wait[i];
+        r = w.ev ? hipStreamWaitEvent(s, w.ev, 0)
+                 : hipStreamWaitValue64(s, w.addr, w.val, hipStreamWaitValueGte, ~0ull);
+    }
+    if (r != hipSuccess) return r;
+    if (j.n > 0) {
+        if (j.timing && (r = h->t_fill.begin(s)) != hipSuccess) return r;  // the kernel itself
+        launch_move(h->storage, h->D, h->tb, h->host_dev, h->tk[j.e], j.n, j.u, h->stage_dev[j.sl],
+                    staged, s);
+        if ((r = hipGetLastError()) != hipSuccess) return r;
+        if (j.timing && (r = h->t_fill.end(s)) != hipSuccess) return r;
+        if (staged && h->poison)  // the staging is spent: any later read of it shows
+            launch_fill_i32((int32_t *)h->d_fill[j.sl], j.n * h->D, 0x7FC00000, s);
+    }
+    if ((r = hipEventRecord(h->ev_filled[j.e], s)) != hipSuccess) return r;
+    return hipStreamWriteValue64(s, h->sem + SEM_FILLED, (uint64_t)j.k + 1, 0);
+}
+
+// Bytes of gathered rows per host-to-device copy of the staged fill: the copy
+// of one piece runs while the next is gathered.
+constexpr int64_t FILL_PIECE_BYTES = 8ll << 20;
+
+// The staged fill of one plan, on the fill thread: wait for the missing keys
+// on the host, gather their rows piece by piece into pinned staging and
+// enqueue each piece's copy to the device, then the move.
+static hipError_t staged_move(sp_ctx *h, const MoveJob &j)
+{
+    const int sl = j.sl;
+    hipError_t r = hipSuccess;
+    if (j.n > 0) {
+        if ((r = hipEventSynchronize(h->ev_mkey[sl])) != hipSuccess) return r;
+        // the copies out of this pinned staging slot (plan k - NSTAGE) have run
+        if (h->fill_h2d_used[sl] && (r = hipEventSynchronize(h->ev_fill_h2d[sl])) != hipSuccess)
+            return r;
+        const double t0 = host_ms();
+        const int D = h->D;
+        const int64_t piece = std::max<int64_t>(1, FILL_PIECE_BYTES / (4 * (int64_t)D));
+        float *const hs = h->h_fill[sl];
+        if (j.timing && (r = h->t_h2d.begin(h->s_move)) != hipSuccess) return r;
+        for (int64_t b = 0; b < j.n && r == hipSuccess; b += piece) {
+            const int64_t e = std::min(j.n, b + piece);
+            h->gather.run(e - b, 256, [&](int64_t b0, int64_t e0) {
+                copy_rows(h->host, h->tb, D, hs, h->h_mkey[sl], b + b0, b + e0, false);
+            });
+            r = hipMemcpyAsync(h->d_fill[sl] + b * D, hs + b * D, sizeof(float) * (e - b) * D,
+                               hipMemcpyHostToDevice, h->s_move);
+        }
+        if (r != hipSuccess) return r;
+        if (j.timing && (r = h->t_h2d.end(h->s_move)) != hipSuccess) return r;
+        if ((r = hipEventRecord(h->ev_fill_h2d[sl], h->s_move)) != hipSuccess) return r;
+        h->fill_h2d_used[sl] = true;
+        h->gather_ms += host_ms() - t0;
+    }
+    return enqueue_move(h, j, h->d_fill[sl]);
+}
+
+static void filler_main(sp_ctx *h)
+{
+    (void)hipSetDevice(h->device);
+    for (;;) {
+        MoveJob j;
+        {
+            std::unique_lock<std::mutex> lk(h->fmu);
+            h->fcv.wait(lk, [&] { return !h->fjobs.empty() || h->fstop; });
+            if (h->fjobs.empty()) return;
+            j = h->fjobs.front();
+        }
+        hipError_t r = hipSuccess;
+        bool failed;
+        {
+            std::lock_guard<std::mutex> lk(h->fmu);
+            failed = !h->fill_err.empty();
+        }
+        if (!failed) r = staged_move(h, j);
+        {
+            std::lock_guard<std::mutex> lk(h->fmu);
+            if (r != hipSuccess && h->fill_err.empty())
+                h->fill_err = std::string("fill of plan ") + std::to_string(j.k) + ": " +
+                              hipGetErrorString(r);
+            h->fjobs.pop_front();
+            h->fill_enqueued = j.k + 1;
+        }
+        h->fcv_done.notify_all();
+    }
+}
+
+// Wait until the fill thread has enqueued the fill of plan k (staged fill;
+// nothing to wait for otherwise).
+static sp_status join_fill(sp_ctx *h, int64_t k)
+{
+    if (!h->staged || k < 0) return SP_OK;
+    const double t0 = host_ms();
+    std::unique_lock<std::mutex> lk(h->fmu);
+    h->fcv_done.wait(lk, [&] { return h->fill_enqueued > k || !h->fill_err.empty(); });
+    h->fill_join_ms += host_ms() - t0;
+    if (!h->fill_err.empty()) {
+        const std::string m = h->fill_err;
+        lk.unlock();
+        return fail(h, SP_ERR_HIP, "%s", m.c_str());
+    }
+    return SP_OK;
+}
+
 // ---------------------------------------------------------------- create / destroy
 
 static void release(sp_ctx *h)
 {
     if (!h) return;
+    if (h->filler.joinable()) {  // it enqueues what is queued, then ends
+        {
+            std::lock_guard<std::mutex> lk(h->fmu);
+            h->fstop = true;
+        }
+        h->fcv.notify_all();
+        h->filler.join();
+    }
+    h->gather.stop();
     if (h->worker.joinable()) {
         {
             std::lock_guard<std::mutex> lk(h->mu);
@@ -503,7 +730,11 @@ static void release(sp_ctx *h)
             if (e) hipEventDestroy(e);
     if (h->ev_consumed) hipEventDestroy(h->ev_consumed);
     for (int i = 0; i < NSTAGE; ++i)
-        if (h->ev_d2h[i]) hipEventDestroy(h->ev_d2h[i]);
+        for (hipEvent_t e : {h->ev_d2h[i], h->ev_mkey[i], h->ev_fill_h2d[i]})
+            if (e) hipEventDestroy(e);
+    for (hipEvent_t e : h->ev_ids)
+        if (e) hipEventDestroy(e);
+    h->t_h2d.destroy();
     h->t_fwd.destroy();
     h->t_bwd.destroy();
     h->t_cmb.destroy();
@@ -551,9 +782,12 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     h->key_bits = bits_for((uint64_t)(T - 1)) + h->tb.row_bits;
     if (h->key_bits > 31) return fail(nullptr, SP_ERR_INVALID_ARG, "tables x rows need %d key bits (max 31)", h->key_bits);
 
+    h->staged = c->fill == SP_FILL_STAGED;
+    h->poison = (c->flags & SP_FLAG_POISON) != 0;
     HIPCHK(nullptr, hipSetDevice(h->device));
     for (int t = 0; t < T; ++t) {
         h->host[t] = c->host_tables[t];
+        if (h->staged) continue;  // read on the host only
         hipPointerAttribute_t attr;
         hipError_t e = hipPointerGetAttributes(&attr, (const void *)c->host_tables[t]);
         void *dp = nullptr;
@@ -615,6 +849,15 @@ static sp_status build(sp_ctx *h, const sp_config *c)
         TRY(dalloc(h, &b.scal, T + 3));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ring_ready[r], hipEventDisableTiming));
     }
+    h->h_ids.assign(h->nring, nullptr);
+    h->h_off.assign(h->nring, nullptr);
+    h->ev_ids.assign(h->nring, nullptr);
+    h->ids_pending.assign(h->nring, 0);
+    for (int r = 0; r < h->nring; ++r) {
+        TRY(palloc(h, &h->h_ids[r], N));
+        TRY(palloc(h, &h->h_off[r], TB1));
+        HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_ids[r], hipEventDisableTiming));
+    }
     for (int k = 0; k < h->nring; ++k) {
         TicketDev &t = h->tk[k];
         TRY(dalloc(h, &t.hit, N));
@@ -666,10 +909,19 @@ static sp_status build(sp_ctx *h, const sp_config *c)
         TRY(dalloc(h, &h->stage_dev[i], h->stage_rows * (h->D + 1)));
         TRY(palloc(h, &h->stage_host[i], h->stage_rows * (h->D + 1)));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_d2h[i], hipEventDisableTiming));
+        if (h->staged) {  // at most min(misses, slots) rows per plan, like the write-back
+            TRY(palloc(h, &h->h_mkey[i], h->stage_rows));
+            TRY(palloc(h, &h->h_fill[i], h->stage_rows * h->D));
+            TRY(dalloc(h, &h->d_fill[i], h->stage_rows * h->D));
+            HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_mkey[i], hipEventDisableTiming));
+            HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_fill_h2d[i], hipEventDisableTiming));
+        }
     }
     {
         void *p = nullptr;
         const size_t bytes = sizeof(uint64_t) * (COUNTER_WORDS + 1);
+        if (injected_alloc_failure())
+            return fail(h, SP_ERR_OOM, "hipHostMalloc(counters) failed: injected (SP_FAIL_ALLOC_AFTER)");
         hipError_t e = hipHostMalloc(&p, bytes, hipHostMallocMapped | hipHostMallocCoherent);
         if (e != hipSuccess) {
             (void)hipGetLastError();
@@ -695,6 +947,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     HIPCHK(nullptr, h->t_fill.init());
     HIPCHK(nullptr, h->t_ing.init());
     HIPCHK(nullptr, h->t_qry.init());
+    HIPCHK(nullptr, h->t_h2d.init());
 
     // initial state: nothing cached
     HIPCHK(nullptr, hipMemsetAsync(h->cons_counter, 0, sizeof(uint32_t), h->s_plan));
@@ -704,7 +957,8 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     if (h->uses) HIPCHK(nullptr, hipMemsetAsync(h->uses, 0, sizeof(int32_t) * S, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->held, 0, sizeof(int32_t) * S, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->hash, 0xFF, sizeof(uint64_t) * cap, h->s_plan));
-    HIPCHK(nullptr, hipMemsetAsync(h->storage, 0, sizeof(float) * S * h->D, h->s_plan));
+    // all-ones words are NaN: under SP_FLAG_POISON a read of a never-filled slot shows
+    HIPCHK(nullptr, hipMemsetAsync(h->storage, h->poison ? 0xFF : 0, sizeof(float) * S * h->D, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->sel_hist, 0, sizeof(int32_t) * MAX_TABLES * SEL_BINS, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->sel_state, 0, sizeof(int32_t) * 3 * MAX_TABLES, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->cnt, 0, sizeof(DevCounters), h->s_plan));
@@ -715,9 +969,15 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     }
     HIPCHK(nullptr, hipStreamSynchronize(h->s_plan));
     h->st.min_capacity_margin = INT64_MAX;
-    const unsigned hw = std::thread::hardware_concurrency();
-    h->scatter.start((int)std::min(8u, std::max(1u, hw / 2)), h->host, h->D, h->tb.row_bits);
+    // host copy threads: the write-back scatter and (staged fill) the gather
+    // each take about half of the cores, their calling threads included
+    const int hw = (int)std::max(2u, std::thread::hardware_concurrency());
+    h->scatter.start(std::max(1, std::min(8, hw / 2) - 1));
     h->worker = std::thread(worker_main, h);
+    if (h->staged) {
+        h->gather.start(std::max(1, std::min(8, hw / 2) - 1));
+        h->filler = std::thread(filler_main, h);
+    }
     return SP_OK;
 }
 
@@ -739,6 +999,8 @@ extern "C" sp_status sp_create(const sp_config *c, sp_handle *out)
                     c->hold_past, SP_MAX_HOLD_PAST, MAX_WINDOW);
     if (c->max_table_ids < 0) return fail(nullptr, SP_ERR_INVALID_ARG, "max_table_ids %lld < 0", (long long)c->max_table_ids);
     if (c->prefetch != 0 && c->prefetch != 1) return fail(nullptr, SP_ERR_INVALID_ARG, "prefetch %d not 0 or 1", c->prefetch);
+    if (c->fill != SP_FILL_MAPPED && c->fill != SP_FILL_STAGED)
+        return fail(nullptr, SP_ERR_INVALID_ARG, "fill %d not SP_FILL_MAPPED or SP_FILL_STAGED", c->fill);
     if (c->max_batch < 0 || c->max_ids < 0 || c->max_ids > INT32_MAX - 1)
         return fail(nullptr, SP_ERR_INVALID_ARG, "bad max_batch / max_ids");
     if ((int64_t)T * c->max_batch + 1 > INT32_MAX) return fail(nullptr, SP_ERR_INVALID_ARG, "too many bags");
@@ -761,8 +1023,13 @@ extern "C" sp_status sp_create(const sp_config *c, sp_handle *out)
         (void)hipGetLastError();
         return fail(nullptr, SP_ERR_INVALID_ARG, "device %d not available (%d devices)", c->device, ndev);
     }
+    {  // testing aid: fail the allocation after the first n
+        const char *f = getenv("SP_FAIL_ALLOC_AFTER");
+        g_alloc_budget = f && *f ? std::max<int64_t>(0, strtoll(f, nullptr, 10)) : -1;
+    }
     sp_ctx *h = new sp_ctx();
     sp_status s = build(h, c);
+    g_alloc_budget = -1;
     if (s != SP_OK) {
         if (!h->err.empty()) g_create_error = h->err;
         release(h);
@@ -824,29 +1091,33 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
     if (timing) HIPCHK(h, h->t_ing.begin(h->s_ingest));
     const int64_t nbags = (int64_t)h->T * bt.batch;
     const int32_t *ids = bt.ids, *off = bt.bag_off;
-    if (!bt.on_device) {  // host arrays: copy into the ring first
+    if (!bt.on_device) {
+        // host arrays: copied on the host into this entry's pinned buffers
+        // (the caller's arrays are free again right after), then to the ring
+        // asynchronously.  The buffers' previous copy (batch q - nring, or
+        // this batch before a rejected plan) has long run.
+        if (h->ids_pending[r]) HIPCHK(h, hipEventSynchronize(h->ev_ids[r]));
+        if (bt.nnz > 0) memcpy(h->h_ids[r], bt.ids, sizeof(int32_t) * bt.nnz);
+        memcpy(h->h_off[r], bt.bag_off, sizeof(int32_t) * (nbags + 1));
         if (bt.nnz > 0)
-            HIPCHK(h, hipMemcpyAsync(b.ids, bt.ids, sizeof(int32_t) * bt.nnz, hipMemcpyHostToDevice,
-                                     h->s_ingest));
-        HIPCHK(h, hipMemcpyAsync(b.bag_off, bt.bag_off, sizeof(int32_t) * (nbags + 1),
+            HIPCHK(h, hipMemcpyAsync(b.ids, h->h_ids[r], sizeof(int32_t) * bt.nnz,
+                                     hipMemcpyHostToDevice, h->s_ingest));
+        HIPCHK(h, hipMemcpyAsync(b.bag_off, h->h_off[r], sizeof(int32_t) * (nbags + 1),
                                  hipMemcpyHostToDevice, h->s_ingest));
+        HIPCHK(h, hipEventRecord(h->ev_ids[r], h->s_ingest));
+        h->ids_pending[r] = 1;
         ids = b.ids;
         off = b.bag_off;
     }
     IngestCons ic{h->cons_counter, 0, h->h_cnt_dev + COUNTER_WORDS, 0};
     if (bt.nnz > 0 && ingest_in_lds(h->max_table_ids, bt.batch)) {
-        // one launch; it reports when it has read its inputs (device arrays
-        // are the caller's; host arrays were copied into the ring above)
+        // one launch; it reports when it has read its inputs, which matters
+        // only for the caller's device arrays
         h->cons_issued += (uint32_t)h->T;
         ic.target = h->cons_issued;
         ic.seq = ++h->cons_seq;
-        if (bt.on_device) {
-            h->wait_cons_word = true;
-        } else {
-            HIPCHK(h, hipEventRecord(h->ev_consumed, h->s_ingest));
-            h->wait_cons_event = true;
-        }
-    } else {
+        if (bt.on_device) h->wait_cons_word = true;
+    } else if (bt.on_device) {
         h->wait_cons_event = true;  // recorded by launch_ingest once the inputs are read
     }
     launch_ingest(h->tb, b, ids, off, bt.batch, bt.nnz, h->key_bits, h->chunk, h->max_table_ids,
@@ -871,6 +1142,7 @@ static sp_status issue_copy(sp_ctx *h, hipStream_t s)
     const int64_t p = h->copy_pending;
     if (p < 0) return SP_OK;
     const int sl = (int)(p % NSTAGE);
+    TRY(join_fill(h, p));  // ev_filled of plan p is recorded
     if (p >= NSTAGE) TRY(join_jobs(h, p - NSTAGE));
     Job job;
     job.ticket = p;
@@ -1153,6 +1425,15 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
                               n_own, h->ring[r1].scal, h->ring_nnz[r1], h->ring[r1].ukeys, c.miss,
                               c.pf, tk, n_miss, &h->cnt->err_sticky, h->ws_plan, h->s_plan);
         }
+        if (h->staged) {
+            // the missing keys go to the host for the gather; their pinned slot
+            // was last read by the fill of plan k - NSTAGE
+            const int sl = (int)(k % NSTAGE);
+            TRY(join_fill(h, k - NSTAGE));
+            HIPCHK(h, hipMemcpyAsync(h->h_mkey[sl], tk.m_key, sizeof(uint32_t) * n_miss,
+                                     hipMemcpyDeviceToHost, h->s_plan));
+            HIPCHK(h, hipEventRecord(h->ev_mkey[sl], h->s_plan));
+        }
     }
     launch_commit(h->tb, h->hash, h->hash_mask, tk, b0, n_miss, th.n_unique, th.nnz, h->key_of_slot,
                   h->last_use, h->uses, u, pf_on, h->cnt, h->s_plan);
@@ -1194,14 +1475,26 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
         while (!h->deadlines.empty() && h->deadlines.front().first <= need) h->deadlines.pop_front();
     }
     const int sl = (int)(k % NSTAGE);
+    MoveJob mj;
+    mj.k = k;
+    mj.n = n_miss;
+    mj.sl = sl;
+    mj.e = e;
+    mj.u = u;
+    mj.timing = timing;
     // the device staging slot is free once plan k - NSTAGE's copy has run
     // (issued two plans ago)
-    if (k >= NSTAGE) HIPCHK(h, wait_unless_done(h->s_move, h->ev_d2h[sl]));
-    if (th.ev_planned)
-        HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_planned[e], 0));
-    else
-        HIPCHK(h, hipStreamWaitValue64(h->s_move, h->sem + SEM_PLANNED, (uint64_t)k + 1,
-                                       hipStreamWaitValueGte, ~0ull));
+    if (k >= NSTAGE && hipEventQuery(h->ev_d2h[sl]) != hipSuccess) {
+        (void)hipGetLastError();
+        mj.wait[mj.nwait++].ev = h->ev_d2h[sl];
+    }
+    if (th.ev_planned) {
+        mj.wait[mj.nwait++].ev = h->ev_planned[e];
+    } else {
+        Wait &w = mj.wait[mj.nwait++];
+        w.addr = h->sem + SEM_PLANNED;
+        w.val = (uint64_t)k + 1;
+    }
     if (n_miss > 0) {
         // RAW-2/3: a victim's row is final once the last update that used it
         // has run.  Update j freed ring entry j % nring for batch j + nring,
@@ -1218,20 +1511,26 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
             if (j != last && h->upd_stream[ej] == h->upd_stream[last % h->nring]) continue;
             if (hipEventQuery(h->ev_upd[ej]) == hipSuccess) continue;  // already done
             (void)hipGetLastError();
-            if (!h->upd_val[ej])  // that update wrote no word (event-wait mode then)
-                HIPCHK(h, hipStreamWaitEvent(h->s_move, h->ev_upd[ej], 0));
-            else
-                HIPCHK(h, hipStreamWaitValue64(h->s_move, h->sem + SEM_UPD + 8 * ej, (uint64_t)j + 1,
-                                               hipStreamWaitValueGte, ~0ull));
+            if (mj.nwait == (int)(sizeof mj.wait / sizeof mj.wait[0]))
+                return fail(h, SP_ERR_HIP, "internal: too many waits for the fill");
+            Wait &w = mj.wait[mj.nwait++];
+            if (!h->upd_val[ej]) {  // that update wrote no word (event-wait mode then)
+                w.ev = h->ev_upd[ej];
+            } else {
+                w.addr = h->sem + SEM_UPD + 8 * ej;
+                w.val = (uint64_t)j + 1;
+            }
         }
-        if (timing) HIPCHK(h, h->t_fill.begin(h->s_move));  // the fill kernel itself
-        launch_move(h->storage, h->D, h->tb, h->host_dev, tk, n_miss, u, h->stage_dev[sl],
-                    h->s_move);
-        CHECK_LAUNCH(h);
-        if (timing) HIPCHK(h, h->t_fill.end(h->s_move));
     }
-    HIPCHK(h, hipEventRecord(h->ev_filled[e], h->s_move));
-    HIPCHK(h, hipStreamWriteValue64(h->s_move, h->sem + SEM_FILLED, (uint64_t)k + 1, 0));
+    if (h->staged) {
+        {
+            std::lock_guard<std::mutex> lk(h->fmu);
+            h->fjobs.push_back(mj);
+        }
+        h->fcv.notify_one();
+    } else {
+        HIPCHK(h, enqueue_move(h, mj, nullptr));
+    }
     // a small one goes on the copy stream now: it ends long before the next
     // fill, even where its queue is the move stream's
     TRY(issue_copy(h, h->s_copy));
@@ -1277,6 +1576,8 @@ extern "C" sp_status sp_forward(sp_handle h, int64_t ticket, float *d_out, void 
     // This plan's fill writes only victim slots, which hold no row of the
     // batch, so the forward and the update then overlap it.
     const bool ev = h->flags & SP_FLAG_EVENT_WAITS;
+    // staged fill: the fill waited for must be enqueued before anything waits on it
+    TRY(join_fill(h, th.n_own > 0 || ticket == 0 ? ticket : ticket - 1));
     if (th.n_own > 0 || ticket == 0) {
         if (ev) HIPCHK(h, hipStreamWaitEvent(s, h->ev_filled[e], 0));
         else HIPCHK(h, hipStreamWaitValue64(s, h->sem + SEM_FILLED, (uint64_t)ticket + 1,
@@ -1342,6 +1643,7 @@ extern "C" sp_status sp_backward_update(sp_handle h, int64_t ticket, const float
 extern "C" sp_status sp_flush(sp_handle h)
 {
     TRY(usable(h));
+    TRY(join_fill(h, h->planned - 1));
     TRY(issue_copy(h, h->s_copy));
     HIPCHK(h, hipDeviceSynchronize());
     TRY(join_jobs(h, h->planned - 1));
@@ -1369,6 +1671,17 @@ extern "C" sp_status sp_flush(sp_handle h)
     return SP_OK;
 }
 
+extern "C" sp_status sp_sync(sp_handle h)
+{
+    TRY(usable(h));
+    TRY(join_fill(h, h->planned - 1));
+    TRY(issue_copy(h, h->s_copy));
+    HIPCHK(h, hipDeviceSynchronize());
+    TRY(join_jobs(h, h->planned - 1));
+    h->deadlines.clear();  // every write-back has landed
+    return SP_OK;
+}
+
 extern "C" sp_status sp_set_flags(sp_handle h, uint32_t flags)
 {
     TRY(usable(h));
@@ -1381,7 +1694,9 @@ extern "C" sp_status sp_get_stats(sp_handle h, sp_stats *out)
 {
     TRY(usable(h));
     if (!out) return fail(h, SP_ERR_INVALID_ARG, "null stats");
+    TRY(join_fill(h, h->planned - 1));  // the fill thread's timers and counts are final
     HIPCHK(h, hipDeviceSynchronize());
+    HIPCHK(h, h->t_h2d.flush());
     HIPCHK(h, h->t_fwd.flush());
     HIPCHK(h, h->t_bwd.flush());
     HIPCHK(h, h->t_cmb.flush());
@@ -1419,6 +1734,10 @@ extern "C" sp_status sp_get_stats(sp_handle h, sp_stats *out)
     s.ms_query = h->t_qry.ms;
     s.timed_ingest = h->t_ing.count;
     s.timed_query = h->t_qry.count;
+    s.host_ms_gather = h->gather_ms;
+    s.host_ms_fill_join = h->fill_join_ms;
+    s.ms_h2d = h->t_h2d.ms;
+    s.timed_h2d = h->t_h2d.count;
     *out = s;
     return SP_OK;
 }

@@ -221,20 +221,24 @@ __global__ void __launch_bounds__(BLOCK) k_bwd_combine(float4 *__restrict__ stor
 // ---------------------------------------------------------------- evict / fill
 
 // Victim i: copy the row its slot held (if any) to staging row i for the
-// write-back, then fill the slot with the missing row m_key[i] read straight
-// from the pinned host table (zero-copy over the host link).  The same lanes
-// read the old row before writing the new one.  Every victim's previous key
-// is stored after the n staging rows, so rows and keys leave the device in
-// one copy.  The grid is kept small and each lane group keeps MOVE_ROWS
-// victims in flight: waves waiting on the host link then occupy few compute
-// units, and the kernels running beside this one keep the rest.
+// write-back, then fill the slot with the missing row m_key[i]: read straight
+// from the pinned host table (zero-copy over the host link), or, with the
+// staged fill, from row i of the rows already copied to the device.  The same
+// lanes read the old row before writing the new one.  Every victim's previous
+// key is stored after the n staging rows, so rows and keys leave the device
+// in one copy.  For the zero-copy fill the grid is kept small and each lane
+// group keeps MOVE_ROWS victims in flight: waves waiting on the host link
+// then occupy few compute units, and the kernels running beside this one
+// keep the rest.  The staged fill only moves rows within HBM and takes a
+// full grid.
 constexpr int MOVE_MAX_BLOCKS = 64;
 constexpr int MOVE_ROWS = 4;
 
 template <int LPR>
 __global__ void __launch_bounds__(BLOCK) k_move(float4 *__restrict__ storage, Tables tb,
                                                 HostRows hr, TicketDev tk, int64_t n,
-                                                int64_t nslots, float4 *__restrict__ stage)
+                                                int64_t nslots, float4 *__restrict__ stage,
+                                                const float4 *__restrict__ staged)
 {
     const int c = (int)(threadIdx.x % LPR);
     const int64_t groups = (int64_t)gridDim.x * (BLOCK / LPR);
@@ -255,7 +259,8 @@ __global__ void __launch_bounds__(BLOCK) k_move(float4 *__restrict__ storage, Ta
                 const uint32_t key = tk.m_key[i];
                 const int tab = (int)(key >> tb.row_bits);
                 const int64_t row = key & row_mask;
-                if (tab < tb.T && row < tb.rows[tab]) src[q] = hr.p[tab] + row * LPR + c;
+                if (staged) src[q] = staged + i * LPR + c;
+                else if (tab < tb.T && row < tb.rows[tab]) src[q] = hr.p[tab] + row * LPR + c;
                 if ((uint32_t)v[q] >= (uint64_t)nslots) v[q] = -1;
             }
         }
@@ -302,16 +307,17 @@ static dim3 grid_waves(int64_t n)
 }
 
 void launch_move(float *storage, int dim, const Tables &tb, float *const *host_dev, TicketDev tk,
-                 int64_t n_miss, int32_t u, float *stage, hipStream_t s)
+                 int64_t n_miss, int32_t u, float *stage, const float *staged, hipStream_t s)
 {
     if (n_miss <= 0) return;
     const int D4 = dim / 4;
     HostRows hr{};
     for (int t = 0; t < tb.T; ++t) hr.p[t] = (const float4 *)host_dev[t];
-    dim3 grid = grid_rows(n_miss, D4);
-    grid.x = grid.x < (unsigned)MOVE_MAX_BLOCKS ? grid.x : (unsigned)MOVE_MAX_BLOCKS;
+    // each lane group places MOVE_ROWS victims per pass
+    dim3 grid = grid_rows((n_miss + MOVE_ROWS - 1) / MOVE_ROWS, D4);
+    if (!staged) grid.x = grid.x < (unsigned)MOVE_MAX_BLOCKS ? grid.x : (unsigned)MOVE_MAX_BLOCKS;
     SP_DISPATCH_LPR(D4, k_move, grid, (float4 *)storage, tb, hr, tk, n_miss,
-                    tb.slot_base[tb.T], (float4 *)stage);
+                    tb.slot_base[tb.T], (float4 *)stage, (const float4 *)staged);
 }
 
 // Launches that may carry start/stop events: the events then time the kernel's

@@ -224,8 +224,11 @@ void launch_pf_arrange(const Tables &tb, PrefetchDev pf, int64_t n_own, const in
                        ScanWs &ws, hipStream_t s);
 
 // k_train.hip
+// Victim i: stage its slot's old row (if any) in stage row i, then write the
+// missing row m_key[i] into the slot: from `staged` row i when given (the
+// staged fill), else straight from the mapped host table.
 void launch_move(float *storage, int dim, const Tables &tb, float *const *host_dev, TicketDev tk,
-                 int64_t n_miss, int32_t u, float *stage, hipStream_t s);
+                 int64_t n_miss, int32_t u, float *stage, const float *staged, hipStream_t s);
 void launch_forward(const float *storage, int dim, int64_t nslots, const int32_t *slot_of,
                     const int32_t *bag_off, int64_t nbags, float *out, hipStream_t s,
                     hipEvent_t e0, hipEvent_t e1);

@@ -26,6 +26,10 @@ SP_ERR_STATE = -6
 SP_FLAG_DEBUG_SYNC = 0x1
 SP_FLAG_TIMING = 0x2
 SP_FLAG_EVENT_WAITS = 0x4
+SP_FLAG_POISON = 0x8
+SP_FILL_MAPPED = 0
+SP_FILL_STAGED = 1
+FILLS = {"mapped": SP_FILL_MAPPED, "staged": SP_FILL_STAGED}
 SP_MAX_AHEAD = 2  # batches after the hold window that sp_plan sorts early
 SP_MAX_HOLD_PAST = 4
 POLICIES = {"lru": 0, "lfu": 1, "random": 2}  # SP_POLICY_*
@@ -47,7 +51,7 @@ class sp_config(C.Structure):
                 ("host_tables", C.POINTER(C.c_void_p)), ("max_batch", C.c_int32),
                 ("max_ids", C.c_int64), ("flags", C.c_uint32), ("device", C.c_int32),
                 ("policy", C.c_int32), ("hold_past", C.c_int32), ("seed", C.c_uint64),
-                ("max_table_ids", C.c_int64), ("prefetch", C.c_int32)]
+                ("max_table_ids", C.c_int64), ("prefetch", C.c_int32), ("fill", C.c_int32)]
 
 
 class sp_batch(C.Structure):
@@ -67,13 +71,16 @@ _STAT_F64B = ["ms_ingest", "ms_query"]
 _STAT_CNTB = ["timed_ingest", "timed_query"]
 _STAT_HOSTB = ["host_ms_inputs"]
 _STAT_I64B = ["prefetched"]
+_STAT_F64C = ["host_ms_gather", "host_ms_fill_join", "ms_h2d"]
+_STAT_I64C = ["timed_h2d"]
 
 
 class sp_stats(C.Structure):
     _fields_ = ([(n, C.c_int64) for n in _STAT_I64] + [(n, C.c_double) for n in _STAT_F64]
                 + [(n, C.c_int64) for n in _STAT_CNT] + [(n, C.c_double) for n in _STAT_HOST]
                 + [(n, C.c_double) for n in _STAT_F64B] + [(n, C.c_int64) for n in _STAT_CNTB]
-                + [(n, C.c_double) for n in _STAT_HOSTB] + [(n, C.c_int64) for n in _STAT_I64B])
+                + [(n, C.c_double) for n in _STAT_HOSTB] + [(n, C.c_int64) for n in _STAT_I64B]
+                + [(n, C.c_double) for n in _STAT_F64C] + [(n, C.c_int64) for n in _STAT_I64C])
 
 
 _DUMP_I32 = ["u_table", "u_row", "inv", "m_table", "m_row", "v_slot", "v_old_row", "v_old_use",
@@ -101,6 +108,7 @@ def load():
         L.sp_forward.argtypes = [h, C.c_int64, C.c_void_p, C.c_void_p]
         L.sp_backward_update.argtypes = [h, C.c_int64, C.c_void_p, C.c_float, C.c_void_p]
         L.sp_flush.argtypes = [h]
+        L.sp_sync.argtypes = [h]
         L.sp_get_stats.argtypes = [h, C.POINTER(sp_stats)]
         L.sp_set_flags.argtypes = [h, C.c_uint32]
         L.sp_debug_plan.argtypes = [h, C.c_int64, C.POINTER(sp_plan_dump)]
@@ -111,7 +119,7 @@ def load():
         L.sp_host_alloc.argtypes = [C.c_size_t, C.POINTER(C.c_void_p)]
         L.sp_host_free.argtypes = [C.c_void_p]
         L.sp_host_free.restype = None
-        for n in ("sp_create", "sp_plan", "sp_forward", "sp_backward_update", "sp_flush",
+        for n in ("sp_create", "sp_plan", "sp_forward", "sp_backward_update", "sp_flush", "sp_sync",
                   "sp_get_stats", "sp_set_flags", "sp_debug_plan", "sp_host_alloc"):
             getattr(L, n).restype = C.c_int32
         _lib = L
@@ -158,6 +166,10 @@ def sp_backward_update(handle: int, ticket: int, d_grad: int, lr: float, stream:
 
 def sp_flush(handle: int) -> None:
     _check(load().sp_flush(handle), handle)
+
+
+def sp_sync(handle: int) -> None:
+    _check(load().sp_sync(handle), handle)
 
 
 def sp_get_stats(handle: int) -> dict:
@@ -240,6 +252,31 @@ class HostTables:
         self.ptrs = []
 
 
+class PageableTables:
+    """fp32 host tables in ordinary (pageable) memory, for the staged fill: numpy
+    arrays, allocated lazily by the OS (pages appear when first written)."""
+
+    def __init__(self, rows, dim: int):
+        self.arrays = [np.empty((int(r), dim), dtype=np.float32) for r in rows]
+        self.ptrs = [int(a.ctypes.data) for a in self.arrays]
+
+    def __getitem__(self, t):
+        return self.arrays[t]
+
+    def __len__(self):
+        return len(self.arrays)
+
+    def close(self):
+        self.arrays = []
+        self.ptrs = []
+
+
+def host_tables(rows, dim: int, fill: str = "mapped"):
+    """Host tables for a context: pinned and device-mapped for the mapped fill,
+    ordinary memory for the staged fill."""
+    return PageableTables(rows, dim) if fill == "staged" else HostTables(rows, dim)
+
+
 def _ptr(x) -> int:
     if x is None:
         return 0
@@ -265,11 +302,13 @@ class ScratchPipe:
     policy: "lru", "lfu" or "random"; hold_past: earlier batches held as well;
     seed: the random policy's stream; max_table_ids: 0 or the most IDs any one
     table has in a batch (a promise that is checked); prefetch: plans also fill
-    the next batch's missing rows."""
+    the next batch's missing rows; fill: "mapped" (zero-copy from pinned,
+    device-mapped tables) or "staged" (host gather, then copies)."""
 
-    def __init__(self, rows, dim, slots, lookahead, host_tables: HostTables, max_batch, max_ids,
+    def __init__(self, rows, dim, slots, lookahead, host_tables, max_batch, max_ids,
                  flags: int = 0, device: int = 0, policy: str = "lru", hold_past: int = 0,
-                 seed: int = 0, max_table_ids: int = 0, prefetch: bool = False):
+                 seed: int = 0, max_table_ids: int = 0, prefetch: bool = False,
+                 fill: str = "mapped"):
         self.T = len(rows)
         self.prefetch = bool(prefetch)
         self.max_ids = int(max_ids)
@@ -281,7 +320,7 @@ class ScratchPipe:
                         lookahead=lookahead, host_tables=self._tabs, max_batch=max_batch,
                         max_ids=max_ids, flags=flags, device=device, policy=POLICIES[policy],
                         hold_past=hold_past, seed=seed, max_table_ids=max_table_ids,
-                        prefetch=int(self.prefetch))
+                        prefetch=int(self.prefetch), fill=FILLS[fill])
         self.handle = sp_create(cfg)
         self._desc_cache = {}
 
@@ -323,6 +362,9 @@ class ScratchPipe:
 
     def flush(self) -> None:
         sp_flush(self.handle)
+
+    def sync(self) -> None:
+        sp_sync(self.handle)
 
     def stats(self) -> dict:
         return sp_get_stats(self.handle)

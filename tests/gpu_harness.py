@@ -5,7 +5,7 @@ import numpy as np
 
 from oracle import oracle
 from paper_2205_04702_amd import workload as wl
-from paper_2205_04702_amd.scratchpipe import HostTables, ScratchPipe
+from paper_2205_04702_amd.scratchpipe import ScratchPipe, host_tables
 
 PLAN_FIELDS = ("u_table", "u_row", "inv", "hit", "m_table", "m_row", "v_slot", "v_old_row",
                "v_old_use", "slot_u", "slot_of")
@@ -46,7 +46,7 @@ def _bound(w, batches, max_table_ids):
 
 
 def run_gpu(w, batches, host, first=0, last=None, flags=0, prepare_ahead=0, policy="lru",
-            hold_past=0, seed=0, max_table_ids="auto", prefetch=False):
+            hold_past=0, seed=0, max_table_ids="auto", prefetch=False, fill="mapped"):
     """Train batches[first:last] on the GPU only (fresh context over `host`), then flush.
     prepare_ahead: how many batches after each window to hand over for early sorting."""
     import torch
@@ -57,7 +57,7 @@ def run_gpu(w, batches, host, first=0, last=None, flags=0, prepare_ahead=0, poli
     max_ids = max(int(b[0].size) for b in batches)
     sp = ScratchPipe(w.rows, D, w.slots, L, host, max_batch=B, max_ids=max(max_ids, 1), flags=flags,
                      policy=policy, hold_past=hold_past, seed=seed,
-                     max_table_ids=_bound(w, batches, max_table_ids), prefetch=prefetch)
+                     max_table_ids=_bound(w, batches, max_table_ids), prefetch=prefetch, fill=fill)
     try:
         out = torch.zeros((T * B, D), dtype=torch.float32, device=dev)
         for u in range(first, last):
@@ -72,8 +72,8 @@ def run_gpu(w, batches, host, first=0, last=None, flags=0, prepare_ahead=0, poli
         sp.close()
 
 
-def fresh_host(w):
-    host = HostTables(w.rows, w.dim)
+def fresh_host(w, fill="mapped"):
+    host = host_tables(w.rows, w.dim, fill)
     for t in range(w.tables):
         wl.init_table(w, t, out=host[t])
     return host
@@ -91,7 +91,7 @@ def make_inputs(w, steps=None, ragged=None):
 def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all", flags=0,
                device_ids=False, ref_tables=None, sync_each_step=True, compare_tables=True,
                return_tables=False, steps=None, prepare_ahead=0, policy="lru", hold_past=0,
-               seed=0, max_table_ids="auto", prefetch=False):
+               seed=0, max_table_ids="auto", prefetch=False, fill="mapped"):
     """Train w on the GPU and with the oracle; assert parity; return a summary.
 
     prepare_ahead: also hand the GPU that many batches after the window
@@ -99,7 +99,8 @@ def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all"
     policy, hold_past, seed: replacement policy and past window of both planners.
     max_table_ids: the bound handed to the library ("auto": the batches' own maximum,
     which sorts tables of up to 8192 IDs in LDS; 0: no bound, the general path).
-    prefetch: both planners also fill the next batch's missing rows."""
+    prefetch: both planners also fill the next batch's missing rows.
+    fill: how the GPU brings missing rows in ("mapped" or "staged")."""
     import torch
     dev = torch.device("cuda:0")
     if batches is None:
@@ -107,7 +108,7 @@ def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all"
     n = len(batches)
     T, B, D, L = w.tables, w.batch, w.dim, w.lookahead
     max_ids = max(int(b[0].size) for b in batches)
-    host = HostTables(w.rows, D)
+    host = host_tables(w.rows, D, fill)
     for t in range(T):
         wl.init_table(w, t, out=host[t])
     ref = ref_tables if ref_tables is not None else [wl.init_table(w, t) for t in range(T)]
@@ -121,7 +122,7 @@ def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all"
     worst_fwd = 0.0
     sp = ScratchPipe(w.rows, D, w.slots, L, host, max_batch=B, max_ids=max(max_ids, 1), flags=flags,
                      policy=policy, hold_past=hold_past, seed=seed,
-                     max_table_ids=_bound(w, batches, max_table_ids), prefetch=prefetch)
+                     max_table_ids=_bound(w, batches, max_table_ids), prefetch=prefetch, fill=fill)
     try:
         out = torch.zeros((T * B, D), dtype=torch.float32, device=dev)
         for u in range(n):
@@ -189,9 +190,11 @@ def row_values(t, rows, dim):
 
 
 def run_sampled_parity(w, steps, *, check_plan_steps, check_fwd_steps, say=print, policy="lru",
-                       hold_past=0, seed=0, max_table_ids="auto", prefetch=False):
-    """A full-size workload driven as the benchmark drives it (IDs in device memory, the two
-    batches after the window handed over early) for `steps` steps.
+                       hold_past=0, seed=0, max_table_ids="auto", prefetch=False, fill="mapped",
+                       host_ids=False):
+    """A full-size workload driven as the benchmark drives it (the two batches after the
+    window handed over early; IDs in device memory, or host memory with host_ids) for
+    `steps` steps.
 
     Only rows that the trained batches read are initialised (plus sentinel rows elsewhere);
     the oracle trains compact copies of exactly those rows (uncached training touches no
@@ -207,7 +210,7 @@ def run_sampled_parity(w, steps, *, check_plan_steps, check_fwd_steps, say=print
     batches = [wl.batch(w, s) for s in range(steps + L + ahead)]
     rows = touched_rows(w, batches, steps)
     say(f"  inputs {time.perf_counter() - t0:.1f}s, touched rows {sum(r.size for r in rows)}")
-    host = HostTables(w.rows, D)
+    host = host_tables(w.rows, D, fill)
     ref = []
     sentinels = []
     for t in range(T):
@@ -228,12 +231,13 @@ def run_sampled_parity(w, steps, *, check_plan_steps, check_fwd_steps, say=print
             parts.append(np.searchsorted(rows[t], seg).astype(np.int32))
         return np.concatenate(parts), off
 
-    dev_batches = [(torch.from_numpy(i).to(dev), torch.from_numpy(o).to(dev)) for i, o in batches]
+    dev_batches = batches if host_ids else \
+        [(torch.from_numpy(i).to(dev), torch.from_numpy(o).to(dev)) for i, o in batches]
     planner = oracle.Planner(w.rows, w.slots, policy, seed, prefetch)
     max_ids = max(int(b[0].size) for b in batches)
     sp = ScratchPipe(w.rows, D, w.slots, L, host, max_batch=B, max_ids=max_ids, policy=policy,
                      hold_past=hold_past, seed=seed,
-                     max_table_ids=_bound(w, batches, max_table_ids), prefetch=prefetch)
+                     max_table_ids=_bound(w, batches, max_table_ids), prefetch=prefetch, fill=fill)
     worst_fwd = 0.0
     try:
         out = torch.zeros((T * B, D), dtype=torch.float32, device=dev)

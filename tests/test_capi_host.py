@@ -52,7 +52,8 @@ int main(void) {
   P(sp_config, policy); P(sp_config, hold_past); P(sp_config, seed); P(sp_config, max_table_ids);
   P(sp_batch, nnz); P(sp_batch, on_device); P(sp_stats, ms_forward); P(sp_stats, timed_fill);
   P(sp_stats, timed_query); P(sp_stats, host_ms_inputs);
-  P(sp_plan_dump, hit); P(sp_plan_dump, nnz);
+  P(sp_plan_dump, hit); P(sp_plan_dump, nnz); P(sp_config, prefetch); P(sp_config, fill);
+  P(sp_stats, prefetched); P(sp_stats, host_ms_gather); P(sp_stats, timed_h2d);
   return 0; }
 """)
     exe = tmp_path / "layout"
@@ -97,6 +98,8 @@ def _cfg(**over):
     (dict(dim=256, max_batch=1 << 21), "4 GiB"),  # gradients addressed with 32-bit offsets
     (dict(prefetch=2), "prefetch"),
     (dict(prefetch=-1), "prefetch"),
+    (dict(fill=2), "fill"),
+    (dict(fill=-1), "fill"),
 ])
 def test_create_rejects_bad_configs(over, needle):
     cfg, keep = _cfg(**over)
@@ -126,6 +129,7 @@ def test_null_handle_calls_report_state_error():
     assert L.sp_forward(None, 0, None, None) == sp.SP_ERR_STATE
     assert L.sp_backward_update(None, 0, None, C.c_float(0.1), None) == sp.SP_ERR_STATE
     assert L.sp_flush(None) == sp.SP_ERR_STATE
+    assert L.sp_sync(None) == sp.SP_ERR_STATE
     assert L.sp_set_flags(None, 0) == sp.SP_ERR_STATE
     L.sp_destroy(None)
 
@@ -133,16 +137,3 @@ def test_null_handle_calls_report_state_error():
 def test_worst_case_storage_helper_matches_paper():
     """Sec. VI-D: (8 x 20 x 2048 x 128 x 4 B) x 6 = 960 MiB."""
     assert sp.worst_case_scratchpad_bytes(8, 20, 2048, 128, 6) == 960 * 2 ** 20
-
-
-def test_ceiling_probe_is_built_and_checks_its_arguments():
-    """The access-pattern ceiling probe the benchmark runs: built beside the library,
-    it rejects shapes it cannot sample (more rows than slots, odd widths) before
-    touching the GPU."""
-    import subprocess
-    exe = os.path.join(os.path.dirname(sp.__file__), "ceiling")
-    assert os.access(exe, os.X_OK)
-    for args in (["10", "20", "64", "5", "1"], ["100", "20", "12", "5", "1"], ["100", "20", "64", "0", "1"]):
-        r = subprocess.run([exe, *args], capture_output=True, text=True)
-        assert r.returncode == 2 and "bad arguments" in r.stderr
-    assert subprocess.run([exe], capture_output=True).returncode == 2

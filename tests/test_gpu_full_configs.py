@@ -31,13 +31,13 @@ def first_tables(w, n):
                                pooling=w.pooling[:n], dist=w.dist[:n], slots=w.slots[:n])
 
 
-def _run(harness, name, steps, fwd, tables=None):
+def _run(harness, name, steps, fwd, tables=None, **kw):
     w = wl.get_workload(name)
     if tables is not None:
         w = first_tables(w, tables)
-    _say(f"case {name} full size, {steps} steps {w.describe()}")
+    _say(f"case {name} full size, {steps} steps {w.describe()} {kw}")
     r = harness.run_sampled_parity(w, steps, check_plan_steps=set(range(steps)),
-                                   check_fwd_steps=set(fwd), say=_say)
+                                   check_fwd_steps=set(fwd), say=_say, **kw)
     st = r["stats"]
     _say(f"{name}: worst fwd {r['worst_fwd']:.2e} table {r['worst_table']:.2e} "
          f"misses {st['misses']} evictions {st['evictions']}")
@@ -53,10 +53,24 @@ def test_zipf_26x4M_full_size(harness):
 
 def test_zipf_26x10M_per_gpu_share(harness):
     """26 x 10M x 128, B=4096, pooling 40, Zipf 0.9, 200k slots, L=4, at the full per-table
-    shape.  All 26 tables need 133 GB of pinned, device-mapped host memory; one process can
-    map about 64 GiB here, which is the share of one GPU when the tables are split over
-    several (tables are independent units), so 12 tables (61 GB) run: 6 steps."""
+    shape, with the zero-copy fill: all 26 tables would need 133 GB of pinned,
+    device-mapped host memory, and one process can map about 64 GiB here, so the first 12
+    tables (61 GB) run: 6 steps."""
     st = _run(harness, "zipf-26x10M", 6, (0, 5), tables=12)
+    assert st["evictions"] > 0
+
+
+def test_zipf_26x10M_whole_staged(harness):
+    """All 26 tables of 26 x 10M x 128 (133 GB of ordinary host memory) with the staged
+    fill, IDs handed over from host memory as the benchmark does: 6 steps, the scratchpad
+    full and evicting from the third."""
+    st = _run(harness, "zipf-26x10M", 6, (0, 5), fill="staged", host_ids=True)
+    assert st["evictions"] > 0
+
+
+def test_zipf_26x4M_full_size_staged(harness):
+    """26 x 4M with the staged fill and host IDs, 32 steps (evicting after about 24)."""
+    st = _run(harness, "zipf-26x4M", 32, (0, 31), fill="staged", host_ids=True)
     assert st["evictions"] > 0
 
 

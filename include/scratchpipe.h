@@ -93,8 +93,9 @@ typedef struct {
     const int64_t *slots;       /* [T] scratchpad slots per table, 1 .. rows[t]         */
     int32_t lookahead;          /* L >= 0: successor batches a plan may hold           */
     float *const *host_tables;  /* [T] row-major [rows][D] fp32 host tables, caller-owned,
-                                   must outlive the context; read on misses, written on
-                                   evictions and flush.  SP_FILL_MAPPED: pinned,
+                                   must outlive the context, each 16-byte aligned; read
+                                   on misses, written on evictions and flush.
+                                   SP_FILL_MAPPED: pinned,
                                    device-mapped memory from sp_host_alloc (or
                                    hipHostMalloc with the mapped flag); SP_FILL_STAGED:
                                    any host memory                                   */

@@ -17,6 +17,7 @@
 //     not in batches p..p+n_p-1 (the hold window), so before the fill of plan k
 //     the host joins every write-back job with p + n_p <= k.
 #include <hip/hip_runtime.h>
+#include <immintrin.h>
 
 #include <algorithm>
 #include <atomic>
@@ -254,27 +255,54 @@ class Pool {
     bool stop_ = false;
 };
 
+// Copy one row of `bytes` (a multiple of 16, both ends 16-byte aligned) with
+// streaming stores: the destination is not read first and does not displace
+// the caches, since nothing reads it again soon (the copy engine reads the
+// staging; a table row is read again only when it misses much later).
+inline void stream_row(float *dst, const float *src, size_t bytes)
+{
+    const __m128i *s = reinterpret_cast<const __m128i *>(src);
+    __m128i *d = reinterpret_cast<__m128i *>(dst);
+    for (size_t k = 0; k < bytes / 16; ++k) _mm_stream_si128(d + k, _mm_loadu_si128(s + k));
+}
+
 // Copy rows between host tables and a staging buffer: staging row i holds
 // table row keys[i] (table key >> row_bits, row key & mask); negative keys,
 // and keys outside the tables, are skipped.  to_tables: scatter staging ->
-// tables, else gather.  Returns the rows copied.
+// tables, else gather.  The rows a few keys ahead are prefetched, so several
+// random rows are in flight per thread.  Returns the rows copied.
 int64_t copy_rows(float *const *tables, const Tables &tb, int dim, float *stage,
                   const int32_t *keys, int64_t b, int64_t e, bool to_tables)
 {
+    constexpr int AHEAD = 8;
     const uint32_t mask = (1u << tb.row_bits) - 1u;
     const size_t row_bytes = sizeof(float) * (size_t)dim;
-    int64_t w = 0;
-    for (int64_t i = b; i < e; ++i) {
-        const int32_t key = keys[i];
-        if (key < 0) continue;
+    auto row_of = [&](int32_t key) -> float * {
+        if (key < 0) return nullptr;
         const int t = key >> tb.row_bits;
         const int64_t r = key & mask;
-        if (t >= tb.T || r >= tb.rows[t]) continue;
-        float *row = tables[t] + r * dim;
-        if (to_tables) memcpy(row, stage + i * dim, row_bytes);
-        else memcpy(stage + i * dim, row, row_bytes);
+        if (t >= tb.T || r >= tb.rows[t]) return nullptr;
+        return tables[t] + r * dim;
+    };
+    for (int64_t i = b; i < std::min(e, b + AHEAD); ++i)
+        if (float *row = row_of(keys[i]))
+            for (size_t o = 0; o < row_bytes; o += 64)
+                _mm_prefetch(reinterpret_cast<const char *>(row) + o, _MM_HINT_T0);
+    int64_t w = 0;
+    for (int64_t i = b; i < e; ++i) {
+        if (i + AHEAD < e) {  // the table row (gather) or staging row (scatter) ahead
+            const char *pf = to_tables ? reinterpret_cast<const char *>(stage + (i + AHEAD) * dim)
+                                       : reinterpret_cast<const char *>(row_of(keys[i + AHEAD]));
+            if (pf)
+                for (size_t o = 0; o < row_bytes; o += 64) _mm_prefetch(pf + o, _MM_HINT_T0);
+        }
+        float *row = row_of(keys[i]);
+        if (!row) continue;
+        if (to_tables) stream_row(row, stage + i * dim, row_bytes);
+        else stream_row(stage + i * dim, row, row_bytes);
         ++w;
     }
+    _mm_sfence();  // the streamed rows are visible before the caller hands them on
     return w;
 }
 
@@ -1014,6 +1042,8 @@ extern "C" sp_status sp_create(const sp_config *c, sp_handle *out)
         if (c->slots[t] < 1 || c->slots[t] > c->rows[t])
             return fail(nullptr, SP_ERR_INVALID_ARG, "slots[%d]=%lld not in 1..rows", t, (long long)c->slots[t]);
         if (!c->host_tables[t]) return fail(nullptr, SP_ERR_INVALID_ARG, "host_tables[%d] is null", t);
+        if ((uintptr_t)c->host_tables[t] % 16)
+            return fail(nullptr, SP_ERR_INVALID_ARG, "host_tables[%d] is not 16-byte aligned", t);
         total += c->slots[t];
     }
     if (total > INT32_MAX) return fail(nullptr, SP_ERR_INVALID_ARG, "total slots exceed 2^31-1");

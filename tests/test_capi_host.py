@@ -109,6 +109,14 @@ def test_create_rejects_bad_configs(over, needle):
     assert needle in sp.sp_last_error(None)
 
 
+def test_create_rejects_unaligned_tables():
+    cfg, keep = _cfg()
+    keep[2][1] = 0x2004
+    h = C.c_void_p()
+    assert sp.load().sp_create(C.byref(cfg), C.byref(h)) == sp.SP_ERR_INVALID_ARG
+    assert "aligned" in sp.sp_last_error(None)
+
+
 def test_create_rejects_bad_table_sizes():
     cfg, keep = _cfg()
     keep[1][0] = 101  # slots > rows

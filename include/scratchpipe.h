@@ -279,6 +279,25 @@ sp_status sp_backward_update(sp_handle h, int64_t ticket, const float *d_grad, f
                              void *stream);
 
 /*
+ * For callers that cannot allocate device memory at call time or at all
+ * outside set-up (code under graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): sp_backward_update with the partial sums of runs
+ * split over several backward chunks kept in a fixed device array of 32 MiB
+ * instead of the context's buffer.  The array exists once per GPU for the
+ * life of the process; its address is taken in sp_create.  It holds the
+ * partials of at most 32 MiB / (4 * dim) backward chunks, one chunk per run
+ * of up to 16 positions of one key, so a batch with nnz * dim * 4 <= 32 MiB
+ * always fits; a ticket above that (with a split run) is rejected with
+ * SP_ERR_INVALID_ARG and nothing changes, and sp_backward_update can then be
+ * called for it.  Every call on one GPU uses the same array: calls that
+ * overlap on one GPU (contexts on different streams) race and must be
+ * ordered by the caller.  Otherwise as sp_backward_update; it allocates
+ * nothing.
+ */
+sp_status sp_backward_update_static(sp_handle h, int64_t ticket, const float *d_grad, float lr,
+                                    void *stream);
+
+/*
  * Synchronise everything and write every cached row back to its host table;
  * afterwards the host tables hold the trained model.  The scratchpad keeps
  * its contents, so training may continue.  (Evicted entries are dirty and must

@@ -390,6 +390,7 @@ struct sp_ctx {
     int32_t *sel_state = nullptr, *sel_hist = nullptr;
     uint32_t *vk0 = nullptr, *vv0 = nullptr, *vk1 = nullptr;
     float *partial = nullptr;
+    float *static_partial = nullptr;  // this device's fixed array (sp_backward_update_static)
     DevCounters *cnt = nullptr;
     int32_t *cnt_part = nullptr;  // [PART_COPIES][2 * MAX_TABLES] probe counter copies, then
                                   // the query's arrival count
@@ -615,6 +616,31 @@ static sp_status join_jobs(sp_ctx *h, int64_t upto)
     return SP_OK;
 }
 
+// ---------------------------------------------------------------- fixed scratch
+
+// Device address of the fixed partial-sum array on each device, taken once
+// per device with that device current (each device has its own copy).
+static std::mutex g_static_mu;
+static void *g_static_partial[256];
+
+static sp_status static_partial_for(sp_ctx *h, int device, float **out)
+{
+    if (device < 0 || device >= 256) return fail(h, SP_ERR_INVALID_ARG, "device %d out of range", device);
+    std::lock_guard<std::mutex> lk(g_static_mu);
+    if (!g_static_partial[device]) {
+        void *p = nullptr;
+        const hipError_t e = static_partial_address(&p);
+        if (e != hipSuccess || !p) {
+            (void)hipGetLastError();
+            return fail(h, SP_ERR_HIP, "hipGetSymbolAddress(fixed partial array): %s",
+                        hipGetErrorString(e));
+        }
+        g_static_partial[device] = p;
+    }
+    *out = (float *)g_static_partial[device];
+    return SP_OK;
+}
+
 // ---------------------------------------------------------------- fill
 
 // Enqueue a plan's fill on the move stream: its waits, the move kernel
@@ -813,6 +839,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     h->staged = c->fill == SP_FILL_STAGED;
     h->poison = (c->flags & SP_FLAG_POISON) != 0;
     HIPCHK(nullptr, hipSetDevice(h->device));
+    TRY(static_partial_for(h, h->device, &h->static_partial));
     for (int t = 0; t < T; ++t) {
         h->host[t] = c->host_tables[t];
         if (h->staged) continue;  // read on the host only
@@ -1636,8 +1663,11 @@ extern "C" sp_status sp_forward(sp_handle h, int64_t ticket, float *d_out, void 
     return SP_OK;
 }
 
-extern "C" sp_status sp_backward_update(sp_handle h, int64_t ticket, const float *d_grad, float lr,
-                                        void *stream)
+// Backward and update of a ticket, the split runs' partial sums in `partial`
+// (the context's buffer, or the fixed array of the static entry point, which
+// holds at most partial_bytes).
+static sp_status backward_update(sp_handle h, int64_t ticket, const float *d_grad, float lr,
+                                 void *stream, float *partial, int64_t partial_bytes)
 {
     TRY(usable(h));
     if (ticket != h->forwarded - 1 || h->updated != ticket)
@@ -1646,6 +1676,13 @@ extern "C" sp_status sp_backward_update(sp_handle h, int64_t ticket, const float
     const int e = (int)(ticket % h->nring);
     const TicketHost &th = h->tkh[e];
     if (th.nnz > 0 && !d_grad) return fail(h, SP_ERR_INVALID_ARG, "null d_grad");
+    // partials are indexed by chunk: room for every chunk of the ticket
+    if (th.n_multi > 0 && th.n_chunks * h->D * (int64_t)sizeof(float) > partial_bytes)
+        return fail(h, SP_ERR_INVALID_ARG,
+                    "ticket %lld has %lld backward chunks of %d floats: %lld bytes of partial sums, "
+                    "above the %lld available",
+                    (long long)ticket, (long long)th.n_chunks, h->D,
+                    (long long)(th.n_chunks * h->D * (int64_t)sizeof(float)), (long long)partial_bytes);
     hipStream_t s = (hipStream_t)stream;
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
     if ((h->flags & SP_FLAG_TIMING) && th.n_chunks > 0) HIPCHK(h, h->t_bwd.take(&ev[0], &ev[1]));
@@ -1653,7 +1690,7 @@ extern "C" sp_status sp_backward_update(sp_handle h, int64_t ticket, const float
         HIPCHK(h, h->t_cmb.take(&ev[2], &ev[3]));
     launch_backward(h->storage, h->D, h->total_slots, h->ring[th.ring], h->tk[e].slot_u,
                     th.n_chunks, th.n_multi, h->chunk, d_grad, (int64_t)h->T * th.B, lr,
-                    h->partial, s, ev);
+                    partial, s, ev);
     CHECK_LAUNCH(h);
     HIPCHK(h, hipEventRecord(h->ev_upd[e], s));  // also frees ring entry e of the window
     h->upd_val[e] = !(h->flags & SP_FLAG_EVENT_WAITS);
@@ -1666,6 +1703,21 @@ extern "C" sp_status sp_backward_update(sp_handle h, int64_t ticket, const float
     h->st.chunks += th.n_chunks;
     if (h->flags & SP_FLAG_DEBUG_SYNC) HIPCHK(h, hipDeviceSynchronize());
     return SP_OK;
+}
+
+extern "C" sp_status sp_backward_update(sp_handle h, int64_t ticket, const float *d_grad, float lr,
+                                        void *stream)
+{
+    if (!h) return SP_ERR_STATE;
+    return backward_update(h, ticket, d_grad, lr, stream, h->partial,
+                           h->nchunk_max * h->D * (int64_t)sizeof(float));
+}
+
+extern "C" sp_status sp_backward_update_static(sp_handle h, int64_t ticket, const float *d_grad,
+                                               float lr, void *stream)
+{
+    if (!h) return SP_ERR_STATE;
+    return backward_update(h, ticket, d_grad, lr, stream, h->static_partial, STATIC_PARTIAL_BYTES);
 }
 
 // ---------------------------------------------------------------- flush / stats / debug

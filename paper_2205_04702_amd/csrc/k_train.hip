@@ -282,6 +282,18 @@ __global__ void __launch_bounds__(BLOCK) k_move(float4 *__restrict__ storage, Ta
     }
 }
 
+// ---------------------------------------------------------------- fixed scratch
+
+// Partial sums of split runs for callers that cannot allocate: a fixed array
+// per GPU, held until the process ends.  Host code never uses its name as an
+// address; it takes the address hipGetSymbolAddress gives on each device.
+static __device__ __align__(256) float4 scratch[STATIC_PARTIAL_BYTES / sizeof(float4)];
+
+hipError_t static_partial_address(void **ptr)
+{
+    return hipGetSymbolAddress(ptr, HIP_SYMBOL(scratch));
+}
+
 // ---------------------------------------------------------------- dispatch
 
 #define SP_DISPATCH_LPR(D4, KERNEL, GRID, ...)                                                   \

@@ -232,6 +232,10 @@ void launch_move(float *storage, int dim, const Tables &tb, float *const *host_d
 void launch_forward(const float *storage, int dim, int64_t nslots, const int32_t *slot_of,
                     const int32_t *bag_off, int64_t nbags, float *out, hipStream_t s,
                     hipEvent_t e0, hipEvent_t e1);
+// The fixed partial-sum array of sp_backward_update_static: its bytes, and
+// its device address on the current device.
+constexpr int64_t STATIC_PARTIAL_BYTES = 32ll << 20;
+hipError_t static_partial_address(void **ptr);
 void launch_backward(float *storage, int dim, int64_t nslots, const BatchDev &b,
                      const int32_t *slot_u, int64_t n_chunks, int64_t n_multi, int chunk,
                      const float *grad, int64_t nbags, float lr, float *partial, hipStream_t s,

@@ -107,6 +107,7 @@ def load():
         L.sp_plan.argtypes = [h, C.POINTER(sp_batch), C.c_int32, C.POINTER(C.c_int64)]
         L.sp_forward.argtypes = [h, C.c_int64, C.c_void_p, C.c_void_p]
         L.sp_backward_update.argtypes = [h, C.c_int64, C.c_void_p, C.c_float, C.c_void_p]
+        L.sp_backward_update_static.argtypes = [h, C.c_int64, C.c_void_p, C.c_float, C.c_void_p]
         L.sp_flush.argtypes = [h]
         L.sp_sync.argtypes = [h]
         L.sp_get_stats.argtypes = [h, C.POINTER(sp_stats)]
@@ -119,7 +120,8 @@ def load():
         L.sp_host_alloc.argtypes = [C.c_size_t, C.POINTER(C.c_void_p)]
         L.sp_host_free.argtypes = [C.c_void_p]
         L.sp_host_free.restype = None
-        for n in ("sp_create", "sp_plan", "sp_forward", "sp_backward_update", "sp_flush", "sp_sync",
+        for n in ("sp_create", "sp_plan", "sp_forward", "sp_backward_update",
+                  "sp_backward_update_static", "sp_flush", "sp_sync",
                   "sp_get_stats", "sp_set_flags", "sp_debug_plan", "sp_host_alloc"):
             getattr(L, n).restype = C.c_int32
         _lib = L
@@ -162,6 +164,11 @@ def sp_forward(handle: int, ticket: int, d_out: int, stream: int) -> None:
 
 def sp_backward_update(handle: int, ticket: int, d_grad: int, lr: float, stream: int) -> None:
     _check(load().sp_backward_update(handle, ticket, d_grad, C.c_float(lr), stream), handle)
+
+
+def sp_backward_update_static(handle: int, ticket: int, d_grad: int, lr: float,
+                              stream: int) -> None:
+    _check(load().sp_backward_update_static(handle, ticket, d_grad, C.c_float(lr), stream), handle)
 
 
 def sp_flush(handle: int) -> None:
@@ -359,6 +366,9 @@ class ScratchPipe:
 
     def backward_update(self, ticket: int, grad, lr: float, stream=None) -> None:
         sp_backward_update(self.handle, ticket, _ptr(grad), lr, _stream_handle(stream))
+
+    def backward_update_static(self, ticket: int, grad, lr: float, stream=None) -> None:
+        sp_backward_update_static(self.handle, ticket, _ptr(grad), lr, _stream_handle(stream))
 
     def flush(self) -> None:
         sp_flush(self.handle)

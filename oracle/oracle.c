@@ -317,23 +317,38 @@ static int32_t orc_find(const int32_t *sorted, int32_t n, int32_t key)
     return lo;
 }
 
-/*
- * Rows of table t that a prefetching plan also fills (the earlier fill of
- * future misses that Sec. IV-C's multi-stage overlap allows): the sorted
- * unique rows of the next batch that are neither cached nor among the
- * planned batch's rows U (those are filled as its own misses).  Returns the
- * count; P needs room for the next batch's IDs of table t.
- */
-static int32_t orc_prefetch_rows(const orc_planner *p, int32_t t, const int32_t *pf_ids,
-                                 const int32_t *pf_off, int32_t B, const int32_t *U, int32_t nu,
-                                 int32_t *P)
+/* Whether row r is among the IDs of table t in batch (ids, off). */
+static int32_t orc_batch_has(const int32_t *ids, const int32_t *off, int32_t t, int32_t B, int32_t r)
 {
-    int32_t j0 = pf_off[(int64_t)t * B], j1 = pf_off[(int64_t)(t + 1) * B];
-    int32_t n = orc_unique_rows(pf_ids, j0, j1, P), k = 0;
-    for (int32_t i = 0; i < n; ++i) {
-        int32_t at = orc_find(U, nu, P[i]);
-        int32_t in_u = at < nu && U[at] == P[i];
-        if (p->slot_of_row[t][P[i]] < 0 && !in_u) P[k++] = P[i];
+    for (int32_t j = off[(int64_t)t * B]; j < off[(int64_t)(t + 1) * B]; ++j)
+        if (ids[j] == r) return 1;
+    return 0;
+}
+
+/*
+ * Rows of table t that a plan prefetching npf batches ahead also fills (the
+ * earlier fill of future misses that Sec. IV-C's multi-stage overlap allows):
+ * for each successor batch win[w], w = 1..npf in turn, its sorted unique rows
+ * that are neither cached nor in an earlier batch of the window (win[0] ..
+ * win[w-1]; rows of win[0] are filled as the planned batch's own misses,
+ * rows of a closer successor were taken with it).  Batch by batch, each
+ * ascending.  Returns the count; P needs room for the IDs of table t in
+ * win[1..npf], tmp for those of one batch.
+ */
+static int32_t orc_prefetch_rows(const orc_planner *p, int32_t t, int32_t npf,
+                                 const int32_t *const *win_ids, const int32_t *const *win_off,
+                                 int32_t B, int32_t *P, int32_t *tmp)
+{
+    int32_t k = 0;
+    for (int32_t w = 1; w <= npf; ++w) {
+        const int32_t *ids = win_ids[w], *off = win_off[w];
+        int32_t n = orc_unique_rows(ids, off[(int64_t)t * B], off[(int64_t)(t + 1) * B], tmp);
+        for (int32_t i = 0; i < n; ++i) {
+            int32_t earlier = 0;
+            for (int32_t e = 0; e < w && !earlier; ++e)
+                earlier = orc_batch_has(win_ids[e], win_off[e], t, B, tmp[i]);
+            if (p->slot_of_row[t][tmp[i]] < 0 && !earlier) P[k++] = tmp[i];
+        }
     }
     return k;
 }
@@ -380,12 +395,13 @@ static void orc_mark_held(const orc_planner *p, int32_t t, int32_t nwin,
  * If any table has |M| > |C| the plan fails with ORC_ERR_CAPACITY and no
  * state changes (the worst-case sizing of Sec. IV-D is not met).
  *
- * Prefetch (orc_planner_plan_pf with a next batch): M is extended, per table,
- * by the next batch's rows that are neither cached nor in U
- * (orc_prefetch_rows), ascending, after the planned batch's misses; they take
- * the next victims in the same order.  A prefetched row is placed with
- * last_use = u and no use (it is not part of this plan's batch); it has no
- * slot_of entry.  The capacity check counts both kinds of misses.
+ * Prefetch (orc_planner_plan_pf with npf >= 1 successors): M is extended,
+ * per table, by the rows of win[1..npf] that are neither cached nor in an
+ * earlier window batch (orc_prefetch_rows: batch by batch, each ascending),
+ * after the planned batch's misses; they take the next victims in the same
+ * order.  A prefetched row is placed with last_use = u and no use (it is not
+ * part of this plan's batch); it has no slot_of entry.  The capacity check
+ * counts both kinds of misses.
  *
  * Outputs (caller allocates; capacity NNZ of win[0] unless noted, slots are
  * global = slot_base[t] + local slot):
@@ -412,8 +428,8 @@ static int32_t orc_batch_valid(const orc_planner *p, const int32_t *ids, const i
 }
 
 static int32_t orc_plan_core(orc_planner *p, int32_t nwin, const int32_t *const *win_ids,
-                             const int32_t *const *win_off, int32_t B, const int32_t *pf_ids,
-                             const int32_t *pf_off, int32_t *u_table, int32_t *u_row,
+                             const int32_t *const *win_off, int32_t B, int32_t npf,
+                             int32_t *u_table, int32_t *u_row,
                              int32_t *inv, uint8_t *hit, int32_t *m_table, int32_t *m_row,
                              int32_t *v_slot, int32_t *v_old_row, int32_t *v_old_use,
                              int32_t *slot_u, int32_t *slot_of, int64_t *counts)
@@ -422,17 +438,23 @@ static int32_t orc_plan_core(orc_planner *p, int32_t nwin, const int32_t *const 
     const int32_t *ids = win_ids[0], *off = win_off[0];
     if (nwin < 1) return ORC_ERR_INVALID;
 
-    /* validate every window batch (and the prefetched one) before anything else */
+    /* validate every window batch before anything else */
+    if (npf < 0 || npf > nwin - 1) return ORC_ERR_INVALID;
     for (int32_t w = 0; w < nwin; ++w)
         if (!orc_batch_valid(p, win_ids[w], win_off[w], B)) return ORC_ERR_INVALID;
-    if (pf_ids && !orc_batch_valid(p, pf_ids, pf_off, B)) return ORC_ERR_INVALID;
 
     int64_t maxS = 0;
     for (int32_t t = 0; t < T; ++t) if (p->slots[t] > maxS) maxS = p->slots[t];
     int32_t nnz = off[(int64_t)T * B];
-    int32_t pf_nnz = pf_ids ? pf_off[(int64_t)T * B] : 0;
+    int32_t pf_nnz = 0, pf_max = 0;  /* IDs of the prefetched batches: all, the largest */
+    for (int32_t w = 1; w <= npf; ++w) {
+        int32_t n = win_off[w][(int64_t)T * B];
+        pf_nnz += n;
+        if (n > pf_max) pf_max = n;
+    }
     int32_t *U = (int32_t *)malloc(sizeof(int32_t) * (size_t)(nnz > 0 ? nnz : 1));
     int32_t *P = (int32_t *)malloc(sizeof(int32_t) * (size_t)(pf_nnz > 0 ? pf_nnz : 1));
+    int32_t *tmp = (int32_t *)malloc(sizeof(int32_t) * (size_t)(pf_max > 0 ? pf_max : 1));
     uint8_t *held = (uint8_t *)malloc((size_t)(maxS > 0 ? maxS : 1));
     orc_cand *cand = (orc_cand *)malloc(sizeof(orc_cand) * (size_t)(maxS > 0 ? maxS : 1));
     int32_t status = ORC_OK;
@@ -443,7 +465,7 @@ static int32_t orc_plan_core(orc_planner *p, int32_t nwin, const int32_t *const 
         int32_t nu = orc_unique_rows(ids, j0, j1, U);
         int64_t nmiss = 0, ncand = 0;
         for (int32_t i = 0; i < nu; ++i) nmiss += p->slot_of_row[t][U[i]] < 0;
-        if (pf_ids) nmiss += orc_prefetch_rows(p, t, pf_ids, pf_off, B, U, nu, P);
+        nmiss += orc_prefetch_rows(p, t, npf, win_ids, win_off, B, P, tmp);
         orc_mark_held(p, t, nwin, win_ids, win_off, B, held);
         for (int64_t s = 0; s < p->slots[t]; ++s) ncand += !held[s];
         if (nmiss > ncand) status = ORC_ERR_CAPACITY;
@@ -469,14 +491,14 @@ static int32_t orc_plan_core(orc_planner *p, int32_t nwin, const int32_t *const 
                 ++nmiss;
             }
         const int64_t nown = nmiss;  /* the planned batch's own misses come first */
-        if (pf_ids) {
-            int32_t npf = orc_prefetch_rows(p, t, pf_ids, pf_off, B, U, nu, P);
-            for (int32_t i = 0; i < npf; ++i) {
+        {
+            int32_t nfetch = orc_prefetch_rows(p, t, npf, win_ids, win_off, B, P, tmp);
+            for (int32_t i = 0; i < nfetch; ++i) {
                 m_table[mbase + nmiss] = t;
                 m_row[mbase + nmiss] = P[i];
                 ++nmiss;
             }
-            nPf += npf;
+            nPf += nfetch;
         }
         orc_mark_held(p, t, nwin, win_ids, win_off, B, held);
         int64_t nc = 0;
@@ -521,6 +543,7 @@ static int32_t orc_plan_core(orc_planner *p, int32_t nwin, const int32_t *const 
     }
     free(cand);
     free(held);
+    free(tmp);
     free(P);
     free(U);
     return status;
@@ -535,22 +558,23 @@ int32_t orc_planner_plan(orc_planner *p, int32_t nwin, const int32_t *const *win
                          int32_t *slot_of, int64_t *counts)
 {
     int64_t c4[4] = {0, 0, 0, 0};
-    int32_t st = orc_plan_core(p, nwin, win_ids, win_off, B, NULL, NULL, u_table, u_row, inv, hit,
+    int32_t st = orc_plan_core(p, nwin, win_ids, win_off, B, 0, u_table, u_row, inv, hit,
                                m_table, m_row, v_slot, v_old_row, v_old_use, slot_u, slot_of, c4);
     if (st == ORC_OK) memcpy(counts, c4, sizeof(int64_t) * 3);
     return st;
 }
 
-/* Plan that also prefetches the next batch (pf_ids/pf_off, NULL for none);
- * m_* and v_* need room for the NNZ of both batches; counts[4] = nU, nM
- * (prefetched included), evictions, prefetched rows. */
+/* Plan that also prefetches the first npf successors of the window (win[1..npf]
+ * must be look-forward batches; past batches follow them); m_* and v_* need
+ * room for the NNZ of win[0..npf] together; counts[4] = nU, nM (prefetched
+ * included), evictions, prefetched rows. */
 int32_t orc_planner_plan_pf(orc_planner *p, int32_t nwin, const int32_t *const *win_ids,
-                            const int32_t *const *win_off, int32_t B, const int32_t *pf_ids,
-                            const int32_t *pf_off, int32_t *u_table, int32_t *u_row,
+                            const int32_t *const *win_off, int32_t B, int32_t npf,
+                            int32_t *u_table, int32_t *u_row,
                             int32_t *inv, uint8_t *hit, int32_t *m_table, int32_t *m_row,
                             int32_t *v_slot, int32_t *v_old_row, int32_t *v_old_use,
                             int32_t *slot_u, int32_t *slot_of, int64_t *counts)
 {
-    return orc_plan_core(p, nwin, win_ids, win_off, B, pf_ids, pf_off, u_table, u_row, inv, hit,
+    return orc_plan_core(p, nwin, win_ids, win_off, B, npf, u_table, u_row, inv, hit,
                          m_table, m_row, v_slot, v_old_row, v_old_use, slot_u, slot_of, counts);
 }

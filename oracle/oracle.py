@@ -58,7 +58,7 @@ def lib():
                                         C.c_void_p]
         L.orc_planner_plan_pf.restype = C.c_int32
         L.orc_planner_plan_pf.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_int32,
-                                          _i32p, _i32p, _i32p, _i32p, _i32p, _u8p, _i32p, _i32p,
+                                          C.c_int32, _i32p, _i32p, _i32p, _u8p, _i32p, _i32p,
                                           _i32p, _i32p, _i32p, _i32p, _i32p, _i64p]
         L.orc_planner_plan.restype = C.c_int32
         L.orc_planner_plan.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_int32,
@@ -138,18 +138,19 @@ class Planner:
     """Reference planner (O2).  plan() returns a PlanResult or raises PlanError.
 
     policy: "lru" (the default of Sec. VI-E), "lfu" or "random"; seed feeds the
-    random policy's draws.  prefetch: each plan also fills the rows of the first
-    successor batch of its window that are neither cached nor in the planned
-    batch (orc_planner_plan_pf); they follow the planned batch's misses, per table.
+    random policy's draws.  prefetch: depth d (True = 1): each plan also fills the
+    rows of the first d successor batches of its window that are neither cached
+    nor in an earlier batch of the window (orc_planner_plan_pf); they follow the
+    planned batch's misses, per table, batch by batch.
     """
 
-    def __init__(self, rows, slots, policy: str = "lru", seed: int = 0, prefetch: bool = False):
+    def __init__(self, rows, slots, policy: str = "lru", seed: int = 0, prefetch=0):
         self.T = len(rows)
         self.rows = np.asarray(rows, dtype=np.int64)
         self.slots = np.asarray(slots, dtype=np.int64)
         self.slot_base = np.concatenate([[0], np.cumsum(self.slots)]).astype(np.int64)
         self.policy, self.seed = policy, int(seed)
-        self.prefetch = bool(prefetch)
+        self.prefetch = int(prefetch)
         self._h = lib().orc_planner_create(self.T, self.rows, self.slots, POLICIES[policy],
                                            C.c_uint64(self.seed))
 
@@ -178,13 +179,13 @@ class Planner:
     def plan(self, window, B: int, past=()) -> PlanResult:
         """window: list of (ids, bag_off) for the planned batch and its visible successors;
         past: earlier batches whose cached rows are held as well (the past window)."""
-        pf = window[1] if self.prefetch and len(window) >= 2 else None
+        npf = min(self.prefetch, len(window) - 1)  # successors in the look-forward window
         window = list(window) + list(past)
         ids_l = [np.ascontiguousarray(w[0], np.int32) for w in window]
         off_l = [np.ascontiguousarray(w[1], np.int32) for w in window]
         nnz = int(off_l[0][-1])
         cap = max(nnz, 1)
-        mcap = cap + (int(ids_l[1].size) if pf is not None else 0)
+        mcap = cap + sum(int(ids_l[w].size) for w in range(1, npf + 1))
         r = PlanResult()
         r.u_table, r.u_row, r.inv = (np.empty(cap, np.int32) for _ in range(3))
         r.hit = np.empty(cap, np.uint8)
@@ -192,14 +193,14 @@ class Planner:
         (r.m_table, r.m_row, r.v_slot, r.v_old_row,
          r.v_old_use) = (np.empty(mcap, np.int32) for _ in range(5))
         counts = np.zeros(4, np.int64)
-        if pf is None:
+        if npf == 0:
             st = lib().orc_planner_plan(self._h, len(window), _ptr_array(ids_l), _ptr_array(off_l),
                                         B, r.u_table, r.u_row, r.inv, r.hit, r.m_table, r.m_row,
                                         r.v_slot, r.v_old_row, r.v_old_use, r.slot_u, r.slot_of,
                                         counts)
         else:
             st = lib().orc_planner_plan_pf(self._h, len(window), _ptr_array(ids_l),
-                                           _ptr_array(off_l), B, ids_l[1], off_l[1], r.u_table,
+                                           _ptr_array(off_l), B, npf, r.u_table,
                                            r.u_row, r.inv, r.hit, r.m_table, r.m_row, r.v_slot,
                                            r.v_old_row, r.v_old_use, r.slot_u, r.slot_of, counts)
         if st != OK:
@@ -231,7 +232,7 @@ class CachedSimulator:
     """
 
     def __init__(self, host_tables, slots, check_residency: bool = True, policy: str = "lru",
-                 seed: int = 0, prefetch: bool = False):
+                 seed: int = 0, prefetch=0):
         self.host = host_tables
         self.D = host_tables[0].shape[1]
         rows = [t.shape[0] for t in host_tables]

@@ -1,17 +1,18 @@
 """Pins for the oracle planner's prefetch mode (earlier fill of future misses).
 
-With prefetch, a plan also fills the rows of the first successor batch of its
-window that are neither cached nor in the planned batch (the multi-stage
-overlap of Sec. IV-C lets a row be brought in before the batch that needs it
-is planned).  Nothing here re-implements the planner: each plan is checked
-against properties recomputed from the state before it:
+With prefetch depth d, a plan also fills the rows of the first d successor
+batches of its window that are neither cached nor in an earlier batch of the
+window (the multi-stage overlap of Sec. IV-C lets a row be brought in before
+the batch that needs it is planned).  Nothing here re-implements the planner:
+each plan is checked against properties recomputed from the state before it:
   * the planned batch's dedup, hits and misses are unchanged by prefetching;
-  * the misses are, per table, the planned batch's misses ascending, then the
-    next batch's rows that are neither cached nor planned, ascending (set
-    arithmetic with numpy);
+  * the misses are, per table, the planned batch's misses ascending, then for
+    each successor in turn its rows that are neither cached nor in an earlier
+    window batch, ascending (set arithmetic with numpy);
   * victims are the smallest unheld (last use, slot) and no window row is
     evicted (as without prefetch);
-  * after the plan every row of both the planned and the next batch is cached;
+  * after the plan every row of the planned batch and of its d successors is
+    cached;
   * prefetched slots carry the plan's index as last use; slots of the planned
     batch are touched; all others keep their last use;
   * the capacity check counts both kinds of misses (independent count);
@@ -38,21 +39,24 @@ def rows_of(batch, t, B):
     return np.asarray(ids[int(off[t * B]):int(off[(t + 1) * B])])
 
 
-def expected_misses(pre, window, B, t):
+def expected_misses(pre, window, B, t, depth=1):
     """(own misses, prefetched rows) of table t from the state before the plan."""
     sor0 = pre[t][2]
     U = np.unique(rows_of(window[0], t, B))
     own = U[sor0[U] < 0]
-    if len(window) < 2:
-        return own, np.zeros(0, own.dtype)
-    nxt = np.unique(rows_of(window[1], t, B))
-    pf = nxt[(sor0[nxt] < 0) & ~np.isin(nxt, U)]
+    seen = U
+    parts = []
+    for w in range(1, min(depth, len(window) - 1) + 1):
+        nxt = np.unique(rows_of(window[w], t, B))
+        parts.append(nxt[(sor0[nxt] < 0) & ~np.isin(nxt, seen)])
+        seen = np.union1d(seen, nxt)
+    pf = np.concatenate(parts) if parts else np.zeros(0, own.dtype)
     return own, pf
 
 
-def capacity_short_pf(planner, pre, window, B):
+def capacity_short_pf(planner, pre, window, B, depth=1):
     for t in range(planner.T):
-        own, pf = expected_misses(pre, window, B, t)
+        own, pf = expected_misses(pre, window, B, t, depth)
         sor0 = pre[t][2]
         win_rows = set()
         for b in window:
@@ -63,7 +67,7 @@ def capacity_short_pf(planner, pre, window, B):
     return False
 
 
-def check_plan_pf(planner, pre, post, window, B, p, u):
+def check_plan_pf(planner, pre, post, window, B, p, u, depth=1):
     T = planner.T
     base = planner.slot_base
     u_off = m_off = 0
@@ -76,7 +80,7 @@ def check_plan_pf(planner, pre, post, window, B, p, u):
         nU = U.size
         assert np.array_equal(p.u_row[u_off:u_off + nU], U)
         assert np.array_equal(p.hit[u_off:u_off + nU].astype(bool), sor0[U] >= 0)
-        own, pf = expected_misses(pre, window, B, t)
+        own, pf = expected_misses(pre, window, B, t, depth)
         k = own.size + pf.size
         assert np.array_equal(p.m_table[m_off:m_off + k], np.full(k, t))
         assert np.array_equal(p.m_row[m_off:m_off + own.size], own)
@@ -93,10 +97,10 @@ def check_plan_pf(planner, pre, post, window, B, p, u):
             assert old < 0 or int(old) not in win_rows, "evicted a held row"
         for i, v in enumerate(victims):
             assert kos1[v] == p.m_row[m_off + i] and sor1[p.m_row[m_off + i]] == v
-        # both batches resident afterwards
+        # the planned batch and its d successors resident afterwards
         assert np.all(sor1[rows_b] >= 0)
-        if len(window) > 1:
-            assert np.all(sor1[rows_of(window[1], t, B)] >= 0)
+        for w in range(1, min(depth, len(window) - 1) + 1):
+            assert np.all(sor1[rows_of(window[w], t, B)] >= 0)
         local = p.slot_of[int(window[0][1][t * B]):int(window[0][1][(t + 1) * B])] - int(base[t])
         assert np.array_equal(kos1[local], rows_b)
         touched = np.zeros(S, bool)
@@ -112,16 +116,16 @@ def check_plan_pf(planner, pre, post, window, B, p, u):
         u_off += nU
         m_off += k
     assert m_off == p.m_row.size
-    assert p.n_prefetch == sum(expected_misses(pre, window, B, t)[1].size for t in range(T))
+    assert p.n_prefetch == sum(expected_misses(pre, window, B, t, depth)[1].size for t in range(T))
 
 
-def run_checked_pf(oracle, w, batches, past=0):
-    planner = oracle.Planner(w.rows, w.slots, prefetch=True)
+def run_checked_pf(oracle, w, batches, depth=1):
+    planner = oracle.Planner(w.rows, w.slots, prefetch=depth)
     n = len(batches)
     for u in range(n):
         win = [batches[q] for q in range(u, min(u + w.lookahead, n - 1) + 1)]
         pre = snapshot(planner)
-        short = capacity_short_pf(planner, pre, win, w.batch)
+        short = capacity_short_pf(planner, pre, win, w.batch, depth)
         try:
             p = planner.plan(win, w.batch)
         except oracle.PlanError as e:
@@ -129,16 +133,17 @@ def run_checked_pf(oracle, w, batches, past=0):
             assert all(np.array_equal(x, y) for a, b in zip(pre, snapshot(planner)) for x, y in zip(a, b))
             return False
         assert not short
-        check_plan_pf(planner, pre, snapshot(planner), win, w.batch, p, u)
+        check_plan_pf(planner, pre, snapshot(planner), win, w.batch, p, u, depth)
     return True
 
 
-@pytest.mark.parametrize("case", range(8))
+@pytest.mark.parametrize("case", range(12))
 def test_random_runs_hold_every_property(oracle, case):
     rng = np.random.default_rng(700 + case)
     T = int(rng.integers(1, 4))
     rows = [int(rng.integers(20, 120)) for _ in range(T)]
     L = int(rng.integers(1, 4))
+    depth = 1 if case < 8 else int(rng.integers(1, L + 1))
     B = int(rng.integers(2, 7))
     P = [int(rng.integers(1, 4)) for _ in range(T)]
     slots = [min(r, (L + 2) * B * p + int(rng.integers(0, 20))) for r, p in zip(rows, P)]
@@ -146,25 +151,25 @@ def test_random_runs_hold_every_property(oracle, case):
     w = wl.custom(rows=rows, dim=4, batch=B, pooling=P, slots=slots, lookahead=L, steps=25,
                   dist=dist, seed=case)
     batches = [wl.batch(w, s) for s in range(w.steps)]
-    assert run_checked_pf(oracle, w, batches)
+    assert run_checked_pf(oracle, w, batches, depth)
 
 
 def test_exhaustive_tiny_spaces(oracle):
-    """Every sequence of three single-table batches over 3 rows, every slot count and
-    lookahead 0-2, with prefetch: each plan satisfies every property or fails for
-    capacity exactly when the independent count says it must."""
+    """Every sequence of three single-table batches over 3 rows, every slot count,
+    lookahead 0-2 and prefetch depth 1-2: each plan satisfies every property or fails
+    for capacity exactly when the independent count says it must."""
     bags = [(a,) for a in range(3)] + list(itertools.product(range(3), repeat=2))
     runs = failed = 0
     for seq in itertools.product(bags, repeat=3):
         batches = [(np.array(b, np.int32), np.array([0, len(b)], np.int32)) for b in seq]
         for S in (1, 2, 3):
-            for L in (0, 1, 2):
+            for L, depth in ((0, 1), (1, 1), (2, 1), (2, 2)):
                 w = wl.custom(rows=[3], dim=1, batch=1, pooling=1, slots=[S], lookahead=L,
                               steps=3)
-                ok = run_checked_pf(oracle, w, batches)
+                ok = run_checked_pf(oracle, w, batches, depth)
                 runs += 1
                 failed += not ok
-    assert runs == 12 ** 3 * 9 and 0 < failed < runs
+    assert runs == 12 ** 3 * 12 and 0 < failed < runs
 
 
 def test_next_plan_has_no_misses_of_its_own(oracle):
@@ -181,22 +186,24 @@ def test_next_plan_has_no_misses_of_its_own(oracle):
     assert prefetched > 0
 
 
-def test_enough_slots_fills_each_row_once_at_first_sight(oracle):
-    """slots >= rows: plan u fills exactly the rows first seen in batch u or u+1."""
-    w = wl.custom(rows=[50, 80], dim=2, batch=8, pooling=3, slots=[50, 80], lookahead=2,
+@pytest.mark.parametrize("depth", [1, 2, 3])
+def test_enough_slots_fills_each_row_once_at_first_sight(oracle, depth):
+    """slots >= rows: plan u fills exactly the rows first seen in batches u .. u+d,
+    batch by batch (closed form: each row crosses the host link once, at the first
+    plan whose prefetch range reaches it)."""
+    w = wl.custom(rows=[50, 80], dim=2, batch=8, pooling=3, slots=[50, 80], lookahead=3,
                   steps=15, dist=("zipf", 1.0), seed=9)
-    planner = oracle.Planner(w.rows, w.slots, prefetch=True)
+    planner = oracle.Planner(w.rows, w.slots, prefetch=depth)
     batches = [wl.batch(w, s) for s in range(w.steps)]
     seen = [set() for _ in range(w.tables)]
     for u in range(w.steps):
         p = planner.plan(batches[u:u + w.lookahead + 1], w.batch)
         expect = []
         for t in range(w.tables):
-            cur = set(int(r) for r in rows_of(batches[u], t, w.batch))
-            nxt = set(int(r) for r in rows_of(batches[u + 1], t, w.batch)) if u + 1 < w.steps else set()
-            expect += [(t, r) for r in sorted(cur - seen[t])]
-            expect += [(t, r) for r in sorted(nxt - cur - seen[t])]
-            seen[t] |= cur | nxt
+            for q in range(u, min(u + depth, w.steps - 1) + 1):
+                rows = set(int(r) for r in rows_of(batches[q], t, w.batch))
+                expect += [(t, r) for r in sorted(rows - seen[t])]
+                seen[t] |= rows
         assert list(zip(p.m_table.tolist(), p.m_row.tolist())) == expect
         assert p.n_evict == 0
 
@@ -234,19 +241,21 @@ def test_capacity_counts_prefetched_rows(oracle):
     assert p.hit.all() and p.m_row.size == 0
 
 
-@pytest.mark.parametrize("name,slots,L,ragged", [
-    ("small-cache", [30, 40], 1, False),
-    ("deep-window", [60, 70], 3, False),
-    ("ragged", [45, 55], 2, True),
-    ("no-lookahead", [16, 20], 0, False),
+@pytest.mark.parametrize("name,slots,L,ragged,depth", [
+    ("small-cache", [30, 40], 1, False, 1),
+    ("deep-window", [60, 70], 3, False, 1),
+    ("ragged", [45, 55], 2, True, 1),
+    ("no-lookahead", [16, 20], 0, False, 1),
+    ("deep-prefetch", [70, 80], 3, False, 3),
+    ("ragged-depth-2", [55, 65], 2, True, 2),
 ])
-def test_cached_training_equals_uncached_bit_for_bit(oracle, name, slots, L, ragged):
+def test_cached_training_equals_uncached_bit_for_bit(oracle, name, slots, L, ragged, depth):
     w = wl.custom(rows=[100, 150], dim=6, batch=5, pooling=[2, 3], slots=slots, lookahead=L,
                   steps=30, dist=(("zipf", 1.05), ("uniform",)), seed=11)
     batches = [wl.ragged_batch(w, s, 5) if ragged else wl.batch(w, s) for s in range(w.steps)]
     plain = [wl.init_table(w, t) for t in range(w.tables)]
     host = [t.copy() for t in plain]
-    sim = oracle.CachedSimulator(host, w.slots, prefetch=True)
+    sim = oracle.CachedSimulator(host, w.slots, prefetch=depth)
     pf = 0
     for u in range(w.steps):
         g = wl.grads(w, u)
@@ -258,3 +267,29 @@ def test_cached_training_equals_uncached_bit_for_bit(oracle, name, slots, L, rag
     for t in range(w.tables):
         assert np.array_equal(plain[t], host[t])
     assert (pf > 0) == (L > 0)
+
+
+def test_deeper_prefetch_spreads_the_first_fills(oracle):
+    """Hand-worked trace, one table of 8 slots, lookahead 2, batches {0}, {1}, {2},
+    {3}: depth 1 fills rows 0,1 then 2 then 3 (one plan ahead); depth 2 fills rows
+    0,1,2 at the first plan and then one new row per plan, two plans ahead."""
+    bs = [(np.array([r], np.int32), np.array([0, 1], np.int32)) for r in range(4)]
+    for depth, expect in ((1, [[0, 1], [2], [3], []]), (2, [[0, 1, 2], [3], [], []])):
+        planner = oracle.Planner([10], [8], prefetch=depth)
+        got = [planner.plan(bs[u:u + 3], 1).m_row.tolist() for u in range(4)]
+        assert got == expect, (depth, got)
+
+
+def test_depth_beyond_the_window_is_the_window(oracle):
+    """A depth above the window's successors prefetches only the batches given: plans
+    with depth 5 over windows of 3 batches equal plans with depth 2."""
+    w = wl.custom(rows=[90, 60], dim=2, batch=4, pooling=[3, 2], slots=[60, 50], lookahead=2,
+                  steps=16, dist=(("zipf", 1.05), ("uniform",)), seed=13)
+    batches = [wl.batch(w, s) for s in range(w.steps)]
+    a = oracle.Planner(w.rows, w.slots, prefetch=2)
+    b = oracle.Planner(w.rows, w.slots, prefetch=5)
+    for u in range(w.steps):
+        win = batches[u:u + 3]
+        pa, pb = a.plan(win, w.batch), b.plan(win, w.batch)
+        for f in pa.keys():
+            assert np.array_equal(getattr(pa, f), getattr(pb, f)), f

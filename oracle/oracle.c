@@ -38,6 +38,9 @@
 #define ORC_POLICY_LFU 1
 #define ORC_POLICY_RANDOM 2
 
+/* successor batches a plan may prefetch, at most */
+#define ORC_MAX_PF 15
+
 int orc_max_threads(void)
 {
 #ifdef _OPENMP
@@ -317,14 +320,6 @@ static int32_t orc_find(const int32_t *sorted, int32_t n, int32_t key)
     return lo;
 }
 
-/* Whether row r is among the IDs of table t in batch (ids, off). */
-static int32_t orc_batch_has(const int32_t *ids, const int32_t *off, int32_t t, int32_t B, int32_t r)
-{
-    for (int32_t j = off[(int64_t)t * B]; j < off[(int64_t)(t + 1) * B]; ++j)
-        if (ids[j] == r) return 1;
-    return 0;
-}
-
 /*
  * Rows of table t that a plan prefetching npf batches ahead also fills (the
  * earlier fill of future misses that Sec. IV-C's multi-stage overlap allows):
@@ -333,21 +328,31 @@ static int32_t orc_batch_has(const int32_t *ids, const int32_t *off, int32_t t, 
  * win[w-1]; rows of win[0] are filled as the planned batch's own misses,
  * rows of a closer successor were taken with it).  Batch by batch, each
  * ascending.  Returns the count; P needs room for the IDs of table t in
- * win[1..npf], tmp for those of one batch.
+ * win[1..npf]; tmp for those of table t in win[0..npf] (each batch's sorted
+ * unique rows, kept for the membership tests).
  */
 static int32_t orc_prefetch_rows(const orc_planner *p, int32_t t, int32_t npf,
                                  const int32_t *const *win_ids, const int32_t *const *win_off,
                                  int32_t B, int32_t *P, int32_t *tmp)
 {
     int32_t k = 0;
+    int32_t start[ORC_MAX_PF + 2], len[ORC_MAX_PF + 1];
+    start[0] = 0;
+    for (int32_t w = 0; w <= npf; ++w) {
+        const int32_t *off = win_off[w];
+        len[w] = orc_unique_rows(win_ids[w], off[(int64_t)t * B], off[(int64_t)(t + 1) * B],
+                                 tmp + start[w]);
+        start[w + 1] = start[w] + len[w];
+    }
     for (int32_t w = 1; w <= npf; ++w) {
-        const int32_t *ids = win_ids[w], *off = win_off[w];
-        int32_t n = orc_unique_rows(ids, off[(int64_t)t * B], off[(int64_t)(t + 1) * B], tmp);
-        for (int32_t i = 0; i < n; ++i) {
+        const int32_t *rows = tmp + start[w];
+        for (int32_t i = 0; i < len[w]; ++i) {
             int32_t earlier = 0;
-            for (int32_t e = 0; e < w && !earlier; ++e)
-                earlier = orc_batch_has(win_ids[e], win_off[e], t, B, tmp[i]);
-            if (p->slot_of_row[t][tmp[i]] < 0 && !earlier) P[k++] = tmp[i];
+            for (int32_t e = 0; e < w && !earlier; ++e) {
+                const int32_t at = orc_find(tmp + start[e], len[e], rows[i]);
+                earlier = at < len[e] && tmp[start[e] + at] == rows[i];
+            }
+            if (p->slot_of_row[t][rows[i]] < 0 && !earlier) P[k++] = rows[i];
         }
     }
     return k;
@@ -439,22 +444,18 @@ static int32_t orc_plan_core(orc_planner *p, int32_t nwin, const int32_t *const 
     if (nwin < 1) return ORC_ERR_INVALID;
 
     /* validate every window batch before anything else */
-    if (npf < 0 || npf > nwin - 1) return ORC_ERR_INVALID;
+    if (npf < 0 || npf > nwin - 1 || npf > ORC_MAX_PF) return ORC_ERR_INVALID;
     for (int32_t w = 0; w < nwin; ++w)
         if (!orc_batch_valid(p, win_ids[w], win_off[w], B)) return ORC_ERR_INVALID;
 
     int64_t maxS = 0;
     for (int32_t t = 0; t < T; ++t) if (p->slots[t] > maxS) maxS = p->slots[t];
     int32_t nnz = off[(int64_t)T * B];
-    int32_t pf_nnz = 0, pf_max = 0;  /* IDs of the prefetched batches: all, the largest */
-    for (int32_t w = 1; w <= npf; ++w) {
-        int32_t n = win_off[w][(int64_t)T * B];
-        pf_nnz += n;
-        if (n > pf_max) pf_max = n;
-    }
+    int32_t pf_nnz = 0;  /* IDs of the prefetched batches */
+    for (int32_t w = 1; w <= npf; ++w) pf_nnz += win_off[w][(int64_t)T * B];
     int32_t *U = (int32_t *)malloc(sizeof(int32_t) * (size_t)(nnz > 0 ? nnz : 1));
     int32_t *P = (int32_t *)malloc(sizeof(int32_t) * (size_t)(pf_nnz > 0 ? pf_nnz : 1));
-    int32_t *tmp = (int32_t *)malloc(sizeof(int32_t) * (size_t)(pf_max > 0 ? pf_max : 1));
+    int32_t *tmp = (int32_t *)malloc(sizeof(int32_t) * (size_t)(nnz + pf_nnz > 0 ? nnz + pf_nnz : 1));
     uint8_t *held = (uint8_t *)malloc((size_t)(maxS > 0 ? maxS : 1));
     orc_cand *cand = (orc_cand *)malloc(sizeof(orc_cand) * (size_t)(maxS > 0 ? maxS : 1));
     int32_t status = ORC_OK;

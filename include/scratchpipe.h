@@ -61,6 +61,9 @@ typedef int32_t sp_status;
 /* sp_config.hold_past at most: earlier batches a plan may hold as well */
 #define SP_MAX_HOLD_PAST 4
 
+/* sp_config.prefetch at most: successor batches a plan may fill ahead */
+#define SP_MAX_PREFETCH 4
+
 /* sp_config.flags */
 #define SP_FLAG_DEBUG_SYNC 0x1u /* synchronise the device at the end of every call     */
 #define SP_FLAG_TIMING 0x2u     /* time forward/backward/plan/fill kernels with events */
@@ -118,15 +121,17 @@ typedef struct {
                                    max_batch both <= 8192 each table of a batch is
                                    sorted and deduplicated by one workgroup in LDS,
                                    the whole batch in one launch                    */
-    int32_t prefetch;           /* 0, or 1: each plan also fills the rows of the next
-                                   batch of its window (window[1], when lookahead >= 1
-                                   and it is given) that are neither cached nor in the
-                                   planned batch: the earlier fill of future misses
-                                   that the multi-stage overlap of Sec. IV-C allows.
-                                   Per table the planned batch's misses come first,
-                                   then the prefetched rows, each ascending; the
-                                   capacity check counts both, so SP_ERR_CAPACITY can
-                                   come one plan earlier than without prefetch      */
+    int32_t prefetch;           /* depth d in 0 .. SP_MAX_PREFETCH (above lookahead it
+                                   acts as lookahead): each plan also fills the rows
+                                   of its next d window batches (window[1..d], those
+                                   given) that are
+                                   neither cached nor in an earlier window batch: the
+                                   earlier fill of future misses that the multi-stage
+                                   overlap of Sec. IV-C allows.  Per table the planned
+                                   batch's misses come first, then window[1]'s rows,
+                                   then window[2]'s, ..., each ascending; the capacity
+                                   check counts them all, so SP_ERR_CAPACITY can come
+                                   earlier than without prefetch.  0 = none        */
     int32_t fill;               /* SP_FILL_MAPPED (0) or SP_FILL_STAGED               */
 } sp_config;
 
@@ -200,7 +205,7 @@ typedef struct {
  *                                        hold, per table, the planned batch's
  *                                        misses then the prefetched rows, and
  *                                        need room for the nnz of the planned
- *                                        and the next batch together */
+ *                                        batch and its d successors together */
 typedef struct {
     int32_t *u_table, *u_row, *inv, *m_table, *m_row, *v_slot, *v_old_row, *v_old_use;
     int32_t *slot_u, *slot_of;
@@ -244,9 +249,9 @@ sp_status sp_create(const sp_config *config, sp_handle *out);
  * the ascending misses take them in that order), updates Hit-Map, slot keys,
  * last-use and use counts, and enqueues the evicted rows' write-back and the
  * misses' fill (Sec. IV-C "Putting everything together", Sec. IV-D
- * Algorithm 1; policies from Sec. VI-E).  With sp_config.prefetch the misses
- * also include window[1]'s rows that are neither cached nor in window[0]
- * (after window[0]'s own misses, per table).  The host waits once for
+ * Algorithm 1; policies from Sec. VI-E).  With sp_config.prefetch = d the
+ * misses also include the rows of window[1..d] that are neither cached nor in
+ * an earlier window batch (after window[0]'s own misses, per table).  The host waits once for
  * per-table counts.
  * Requires the previous ticket's sp_backward_update to have been issued.
  * Transactional: on SP_ERR_INVALID_ARG (ID out of range, bad offsets, sizes

@@ -343,10 +343,10 @@ struct sp_ctx {
     float *storage = nullptr;
     int32_t *key_of_slot = nullptr, *last_use = nullptr, *held = nullptr;
     int32_t *uses = nullptr;  // per-slot use counts, LFU only
-    bool prefetch = false;    // plans also fill the next batch's missing rows
+    int pf_depth = 0;         // plans also fill the missing rows of this many successors
     uint32_t *pf_own_key = nullptr;  // prefetch mode: the planned batch's own misses,
     int32_t *pf_own_uidx = nullptr;  // as the query compacts them
-    int32_t *pf_flag = nullptr;      // next batch's unique keys to prefetch
+    int32_t *pf_flag = nullptr;      // [pf_depth][max_ids] successors' unique keys to prefetch
     uint64_t *hash = nullptr;
     uint32_t hash_mask = 0;
     int64_t hash_used = 0;
@@ -813,7 +813,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     h->L = c->lookahead;
     h->policy = c->policy;
     h->P = c->hold_past;
-    h->prefetch = c->prefetch != 0;
+    h->pf_depth = std::min(c->prefetch, c->lookahead);  // only window batches are fetched
     h->seed = c->seed;
     h->device = c->device;
     h->flags = c->flags;
@@ -856,8 +856,8 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     }
 
     const int64_t S = h->total_slots, N = h->max_ids, TB1 = (int64_t)T * h->max_batch + 1;
-    // misses of one plan: the planned batch's, plus the next batch's when prefetching
-    const int64_t NM = h->prefetch ? 2 * N : N;
+    // misses of one plan: the planned batch's, plus its successors' when prefetching
+    const int64_t NM = (1 + (int64_t)h->pf_depth) * N;
     const int64_t nchunk_max = N + N / h->chunk + 1;
     h->nchunk_max = nchunk_max;
     TRY(dalloc(h, &h->storage, S * h->D));
@@ -935,10 +935,10 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     TRY(dalloc(h, &h->vv0, NM));
     TRY(dalloc(h, &h->vk1, NM));
     TRY(dalloc(h, &h->hist, radix_hist_entries(NM)));
-    if (h->prefetch) {
+    if (h->pf_depth > 0) {
         TRY(dalloc(h, &h->pf_own_key, N));
         TRY(dalloc(h, &h->pf_own_uidx, N));
-        TRY(dalloc(h, &h->pf_flag, N));
+        TRY(dalloc(h, &h->pf_flag, (int64_t)h->pf_depth * N));
     }
     TRY(dalloc(h, &h->ihist, radix_hist_entries(N)));
     TRY(dalloc(h, &h->cnt, 1));
@@ -1053,7 +1053,10 @@ extern "C" sp_status sp_create(const sp_config *c, sp_handle *out)
         return fail(nullptr, SP_ERR_INVALID_ARG, "hold_past %d not in 0..%d with lookahead + 1 + hold_past <= %d",
                     c->hold_past, SP_MAX_HOLD_PAST, MAX_WINDOW);
     if (c->max_table_ids < 0) return fail(nullptr, SP_ERR_INVALID_ARG, "max_table_ids %lld < 0", (long long)c->max_table_ids);
-    if (c->prefetch != 0 && c->prefetch != 1) return fail(nullptr, SP_ERR_INVALID_ARG, "prefetch %d not 0 or 1", c->prefetch);
+    static_assert(SP_MAX_PREFETCH == MAX_PF, "prefetch bound");
+    if (c->prefetch < 0 || c->prefetch > SP_MAX_PREFETCH)
+        return fail(nullptr, SP_ERR_INVALID_ARG, "prefetch %d not in 0..%d", c->prefetch,
+                    SP_MAX_PREFETCH);
     if (c->fill != SP_FILL_MAPPED && c->fill != SP_FILL_STAGED)
         return fail(nullptr, SP_ERR_INVALID_ARG, "fill %d not SP_FILL_MAPPED or SP_FILL_STAGED", c->fill);
     if (c->max_batch < 0 || c->max_ids < 0 || c->max_ids > INT32_MAX - 1)
@@ -1319,8 +1322,8 @@ static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, int32_t *stamp_o
     }
     const int32_t stamp = ++h->stamp;
     *seq_out = ++h->qseq;
-    const PrefetchDev pf{(int32_t)(h->prefetch && nhold >= 2), h->pf_own_key, h->pf_own_uidx,
-                         h->pf_flag};
+    const PrefetchDev pf{std::min(h->pf_depth, nhold - 1), h->pf_own_key, h->pf_own_uidx,
+                         h->pf_flag, h->max_ids};
     launch_query(h->tb, h->hash, h->hash_mask, ukeys, nuniq, nwin, max_nnz, h->held, stamp,
                  h->tk[e], pf, h->cnt, h->cnt_part, h->cnt_part + PART_COPIES * PART_WORDS,
                  h->ring[k % h->nring].scal, h->h_cnt_dev, *seq_out, h->ws_plan, h->s_plan);
@@ -1408,20 +1411,27 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     if (c.err_sticky)
         return fail(h, SP_ERR_HIP, "internal planner inconsistency (flags %d) in an earlier plan",
                     c.err_sticky);
-    // prefetch mode: the next batch's rows to fetch count as misses too
-    const bool pf_on = h->prefetch && nhold >= 2;
-    if (!pf_on)
-        for (int t = 0; t < h->T; ++t) c.pf[t] = 0;
+    // prefetch mode: the successors' rows to fetch count as misses too
+    const int pf_d = std::min(h->pf_depth, nhold - 1);
+    const bool pf_on = pf_d > 0;
+    int32_t pf_tot[MAX_TABLES];
+    for (int t = 0; t < h->T; ++t) {
+        pf_tot[t] = 0;
+        for (int w = 0; w < MAX_PF; ++w) {
+            if (w >= pf_d) c.pf[w][t] = 0;
+            pf_tot[t] += c.pf[w][t];
+        }
+    }
     int64_t n_miss = 0, n_own = 0, margin = INT64_MAX;
     for (int t = 0; t < h->T; ++t) {
         const int64_t free_slots = h->slots[t] - c.held[t];
-        const int64_t need = (int64_t)c.miss[t] + c.pf[t];
+        const int64_t need = (int64_t)c.miss[t] + pf_tot[t];
         margin = std::min<int64_t>(margin, free_slots - need);
         if (need > free_slots) {
             for (int w = 0; w < n; ++w) h->ring_batch[(k + w) % h->nring] = -1;  // re-read on retry
             return fail(h, SP_ERR_CAPACITY,
                         "table %d: %lld misses (%d to prefetch) but only %lld unheld slots (plan %lld)",
-                        t, (long long)need, c.pf[t], (long long)free_slots, (long long)k);
+                        t, (long long)need, pf_tot[t], (long long)free_slots, (long long)k);
         }
         n_miss += need;
         n_own += c.miss[t];
@@ -1452,16 +1462,16 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
         int32_t vb = 0;
         int64_t maxS = 0;
         for (int t = 0; t < h->T; ++t) {
-            if (c.miss[t] + c.pf[t] > 0) {
+            if (c.miss[t] + pf_tot[t] > 0) {
                 int y = a.nact++;
                 a.t[y] = t;
-                a.k[y] = c.miss[t] + c.pf[t];
+                a.k[y] = c.miss[t] + pf_tot[t];
                 a.base[y] = h->tb.slot_base[t];
                 a.S[y] = h->slots[t];
                 a.vbase[y] = vb;
                 maxS = std::max<int64_t>(maxS, h->slots[t]);
             }
-            vb += c.miss[t] + c.pf[t];
+            vb += c.miss[t] + pf_tot[t];
         }
         // priority values: LRU last use + 1 <= u, LFU uses <= u + 1, random <= 2^24
         const int nb = h->policy == POLICY_RANDOM ? 25
@@ -1475,12 +1485,21 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
                               h->vv0, h->vk1, (uint32_t *)nullptr, n_miss, h->hist, h->ws_plan,
                               tk.v_slot, &h->cnt->err_sticky, h->s_plan);
         if (pf_on) {
-            // the miss list in victim order: per table own misses, then the next
-            // batch's rows to prefetch (the query left the own misses aside)
-            const int r1 = (int)((k + 1) % h->nring);
-            launch_pf_arrange(h->tb, PrefetchDev{1, h->pf_own_key, h->pf_own_uidx, h->pf_flag},
-                              n_own, h->ring[r1].scal, h->ring_nnz[r1], h->ring[r1].ukeys, c.miss,
-                              c.pf, tk, n_miss, &h->cnt->err_sticky, h->ws_plan, h->s_plan);
+            // the miss list in victim order: per table own misses, then each
+            // successor's rows to prefetch (the query left the own misses aside)
+            const int32_t *n_next[MAX_PF] = {};
+            const uint32_t *next_keys[MAX_PF] = {};
+            int64_t max_next[MAX_PF] = {};
+            for (int w = 0; w < pf_d; ++w) {
+                const int r1 = (int)((k + 1 + w) % h->nring);
+                n_next[w] = h->ring[r1].scal;
+                next_keys[w] = h->ring[r1].ukeys;
+                max_next[w] = h->ring_nnz[r1];
+            }
+            launch_pf_arrange(h->tb,
+                              PrefetchDev{pf_d, h->pf_own_key, h->pf_own_uidx, h->pf_flag, h->max_ids},
+                              n_own, n_next, max_next, next_keys, c.miss, c.pf, tk, n_miss,
+                              &h->cnt->err_sticky, h->ws_plan, h->s_plan);
         }
         if (h->staged) {
             // the missing keys go to the host for the gather; their pinned slot
@@ -1522,7 +1541,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     // ---- mover (own stream): write-back of evicted rows and fill of misses;
     // the next plan's query does not wait for it
     // RAW-4: rows evicted by plan p may be refilled from plan p + n_p on
-    // (n_p - 1 with prefetch, which fills the batch after the planned one)
+    // (n_p - d with prefetch depth d, which fills the batches after the planned one)
     int64_t need = -1;
     for (const auto &d : h->deadlines)
         if (d.second <= k) need = std::max(need, d.first);
@@ -1596,7 +1615,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     // an evicted row is in no batch of this plan's window, so the first plan
     // that can fill it again is the one whose planned batch (or, prefetching,
     // next batch) is the first after the window
-    h->deadlines.emplace_back(k, k + nhold - (pf_on ? 1 : 0));
+    h->deadlines.emplace_back(k, k + nhold - pf_d);
 
     h->host_ms[4] += host_ms() - tF;
     h->planned = k + 1;

@@ -51,10 +51,10 @@ __device__ __forceinline__ P pick_uniform(const P (&a)[MAX_WINDOW], int w)
 // word is whole when seen.  It then clears the copies, the per-plan counters
 // and the arrival count for the next query.
 //
-// Prefetch mode: batch 0's misses go to pf.own_key / pf.own_uidx instead, and
-// batch 1 (the next one) flags each unique key that is not cached and not a
-// key of batch 0 (a binary search of batch 0's sorted keys) and counts them
-// per table, so the plan can fill them too.
+// Prefetch mode (depth d): batch 0's misses go to pf.own_key / pf.own_uidx
+// instead, and each successor w = 1..d flags every unique key that is not
+// cached and not a key of an earlier batch 0..w-1 (binary searches of their
+// sorted keys) and counts them per table, so the plan can fill them too.
 // Whether key is among the n sorted keys a[0..n).
 __device__ __forceinline__ bool in_sorted(const uint32_t *__restrict__ a, int32_t n, uint32_t key)
 {
@@ -77,7 +77,7 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
                                                  uint32_t seq, uint32_t *m_key, int32_t *m_uidx,
                                                  ScanDev d)
 {
-    __shared__ int32_t c_miss[MAX_TABLES], c_held[MAX_TABLES], c_pf[MAX_TABLES];
+    __shared__ int32_t c_miss[MAX_TABLES], c_held[MAX_TABLES], c_pf[MAX_TABLES];  // c_pf: row w's
     __shared__ int32_t last_s;
     __shared__ uint32_t tile_s, pref_s;
     __shared__ uint32_t lds_scan[BLOCK / WAVE];
@@ -114,9 +114,12 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
             miss = slot < 0;
         }
         if (slot >= 0) fresh = atomicExch(&held[slot], stamp) != stamp;
-        if (w == 1 && pf.on) {
-            fetch = slot < 0 && !in_sorted(pa.uk[0], *pa.nu[0], key);
-            pf.flag[i] = fetch;
+        if (w >= 1 && w <= pf.depth) {
+            fetch = slot < 0;
+#pragma unroll
+            for (int e = 0; e < MAX_PF; ++e)  // the earlier batches 0 .. w-1
+                if (e < w && fetch) fetch = !in_sorted(pa.uk[e], *pa.nu[e], key);
+            pf.flag[(int64_t)(w - 1) * pf.stride + i] = fetch;
         }
     }
     if (w == 0 && xb * BLOCK < (int64_t)*pa.nu[0]) {  // uniform per block
@@ -128,8 +131,8 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
         }
         __syncthreads();
         if (miss) {
-            uint32_t *const mk = pf.on ? pf.own_key : m_key;
-            int32_t *const mu = pf.on ? pf.own_uidx : m_uidx;
+            uint32_t *const mk = pf.depth > 0 ? pf.own_key : m_key;
+            int32_t *const mu = pf.depth > 0 ? pf.own_uidx : m_uidx;
             mk[pref_s + ex] = key;
             mu[pref_s + ex] = (int32_t)i;
         }
@@ -152,10 +155,11 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
     }
     __syncthreads();
     int32_t *p = part + (int64_t)((blockIdx.y * gridDim.x + blockIdx.x) % PART_COPIES) * PART_WORDS;
+    const int pfw = w >= 1 && w <= MAX_PF ? w - 1 : 0;  // this row's prefetch counts
     for (int tt = threadIdx.x; tt < T; tt += BLOCK) {
         if (c_miss[tt]) seen |= atomicAdd(&p[tt], c_miss[tt]);
         if (c_held[tt]) seen |= atomicAdd(&p[MAX_TABLES + tt], c_held[tt]);
-        if (c_pf[tt]) seen |= atomicAdd(&p[2 * MAX_TABLES + tt], c_pf[tt]);
+        if (c_pf[tt]) seen |= atomicAdd(&p[(2 + pfw) * MAX_TABLES + tt], c_pf[tt]);
     }
     if (seen < 0) cnt->pad2[0] = seen;  // never taken (counts are not negative)
     __syncthreads();
@@ -168,9 +172,10 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
     __shared__ int32_t sums[PART_WORDS];
     for (int j = threadIdx.x; j < PART_WORDS; j += BLOCK) sums[j] = 0;
     __syncthreads();
-    const int n_rel = PART_COPIES * 3 * T;
-    auto word = [T](int r) {  // the r-th live word: copy c, array a (miss, held, pf), table
-        const int c = r / (3 * T), jj = r % (3 * T), a = jj / T;
+    const int na = 2 + pf.depth;  // live arrays per copy: miss, held, one per successor
+    const int n_rel = PART_COPIES * na * T;
+    auto word = [T, na](int r) {  // the r-th live word: copy c, array a, table
+        const int c = r / (na * T), jj = r % (na * T), a = jj / T;
         return c * PART_WORDS + a * MAX_TABLES + (jj - a * T);
     };
     for (int r = threadIdx.x; r < n_rel; r += BLOCK) {
@@ -187,7 +192,8 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
         int32_t v;
         if (k >= MISS0 && k < MISS0 + MAX_TABLES) v = k - MISS0 < T ? sums[k - MISS0] : 0;
         else if (k >= HELD0 && k < HELD0 + MAX_TABLES) v = k - HELD0 < T ? sums[MAX_TABLES + k - HELD0] : 0;
-        else if (k >= PF0 && k < PF0 + MAX_TABLES) v = k - PF0 < T ? sums[2 * MAX_TABLES + k - PF0] : 0;
+        else if (k >= PF0 && k < PF0 + MAX_PF * MAX_TABLES)  // successor a, table tt
+            v = (k - PF0) % MAX_TABLES < T ? sums[2 * MAX_TABLES + (k - PF0)] : 0;
         else v = __hip_atomic_load(&src[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         host_mapped[k] = ((uint64_t)seq << 32) | (uint32_t)v;
         if (k < COUNTERS_CLEARED)
@@ -204,7 +210,10 @@ void launch_query(const Tables &tb, const uint64_t *hash, uint32_t mask,
                   DevCounters *cnt, int32_t *part, int32_t *arrived, const int32_t *scal0,
                   uint64_t *host_mapped, uint32_t seq, ScanWs &ws, hipStream_t s)
 {
-    if (nwin < 2) pf.on = 0;  // no next batch in the window
+    if (pf.depth > nwin - 1 || pf.depth > MAX_PF) {  // the caller limits it to the window
+        ws.overflow = true;
+        return;
+    }
     ProbeArgs pa{};
     for (int w = 0; w < nwin; ++w) pa.uk[w] = ukeys[w], pa.nu[w] = nuniq[w];
     // at least one block per batch so that every batch's error word is read
@@ -589,45 +598,57 @@ void launch_commit(const Tables &tb, uint64_t *hash, uint32_t mask, TicketDev tk
 // ---------------------------------------------------------------- prefetch arrangement
 //
 // One single-pass scan over a virtual range: indices [0, n_own) are the
-// planned batch's own misses (ascending, all tables), indices n_own + j are
-// the next batch's unique keys j, valued 1 when flagged for prefetch.  The
-// scan's prefix at a flagged key counts the flagged keys before it, all
-// tables included, so per table (keys are ascending by table) it is the
-// table's first prefetched entry plus the key's rank among them.
+// planned batch's own misses (ascending, all tables); then successor w's
+// segment of len[w] indices (a bound on its unique keys), index j valued 1
+// when its key j is flagged for prefetch.  The scan's prefix at a flagged key
+// counts the flagged keys before it: all of the earlier successors', then
+// those of the same successor in tables before t (keys are ascending by
+// table), then its rank in table t.  The host folds the first two and the
+// table's place into off[w][t], so the key goes to off[w][t] + prefix.
 
 struct PfSeg {
-    int64_t n_own;
-    const int32_t *n_next;
+    int64_t total;
     __device__ int64_t beg(int) const { return 0; }
-    __device__ int64_t end(int) const { return n_own + *n_next; }
+    __device__ int64_t end(int) const { return total; }
 };
 
 struct PfVal {
     int64_t n_own;
+    int32_t depth;
+    int64_t start[MAX_PF + 1];     // first index of each successor's segment, then the end
+    const int32_t *n_next[MAX_PF];  // unique keys of each successor
     const int32_t *flag;
+    int64_t stride;
     __device__ uint32_t operator()(int64_t i, int) const
     {
-        const int64_t j = i - n_own;
-        const int32_t f = flag[j > 0 ? j : 0];  // loaded without a branch
-        return i >= n_own && f ? 1u : 0u;
+        if (i < n_own) return 0u;
+        uint32_t f = 0;
+#pragma unroll
+        for (int w = 0; w < MAX_PF; ++w) {  // the segment holding i, without indexing by w
+            const int64_t j = i - start[w];
+            if (w < depth && j >= 0 && i < start[w + 1] && j < *n_next[w])
+                f = flag[(int64_t)w * stride + j] ? 1u : 0u;
+        }
+        return f;
     }
 };
 
 struct PfOut {
     int64_t n_own, n_miss;
-    int32_t row_bits, T;
-    const uint32_t *own_key, *next_keys;
+    int32_t row_bits, T, depth;
+    const uint32_t *own_key;
     const int32_t *own_uidx;
+    const uint32_t *next_keys[MAX_PF];
+    int64_t start[MAX_PF + 1];
     uint32_t *m_key;
     int32_t *m_uidx, *err;
-    int32_t pf_first[MAX_TABLES];    // prefetched keys of the tables before t
-    int32_t vbase[MAX_TABLES];       // first miss (and victim) of table t
-    int32_t own[MAX_TABLES];         // own misses of table t
+    int32_t pf_before[MAX_TABLES];      // prefetched keys of the tables before t (all successors)
+    int32_t off[MAX_PF][MAX_TABLES];    // successor w, table t: destination less the prefix
     __device__ void operator()(int64_t i, uint32_t e, uint32_t v, int) const
     {
-        uint32_t key;
+        uint32_t key = 0;
         int32_t uidx;
-        int64_t dst;
+        int64_t dst = -1;
         if (i < n_own) {
             key = own_key[i];
             uidx = own_uidx[i];
@@ -636,17 +657,19 @@ struct PfOut {
                 atomicOr(err, ERR_PLAN);
                 return;
             }
-            dst = i + pf_first[t];
+            dst = i + pf_before[t];
         } else {
             if (!v) return;
-            key = next_keys[i - n_own];
             uidx = -1;
-            const int t = (int)(key >> row_bits);
-            if (t >= T) {
-                atomicOr(err, ERR_PLAN);
-                return;
+#pragma unroll
+            for (int w = 0; w < MAX_PF; ++w) {
+                const int64_t j = i - start[w];
+                if (w < depth && j >= 0 && i < start[w + 1]) {
+                    key = next_keys[w][j];
+                    const int t = (int)(key >> row_bits);
+                    dst = t < T ? (int64_t)off[w][t] + e : -1;
+                }
             }
-            dst = (int64_t)vbase[t] + own[t] + ((int64_t)e - pf_first[t]);
         }
         if (dst < 0 || dst >= n_miss) {  // the counts and the lists disagree
             atomicOr(err, ERR_PLAN);
@@ -657,32 +680,63 @@ struct PfOut {
     }
 };
 
-void launch_pf_arrange(const Tables &tb, PrefetchDev pf, int64_t n_own, const int32_t *n_next,
-                       int64_t max_next, const uint32_t *next_ukeys, const int32_t *own,
-                       const int32_t *pf_count, TicketDev tk, int64_t n_miss, int32_t *err,
-                       ScanWs &ws, hipStream_t s)
+void launch_pf_arrange(const Tables &tb, PrefetchDev pf, int64_t n_own,
+                       const int32_t *const *n_next, const int64_t *max_next,
+                       const uint32_t *const *next_ukeys, const int32_t *own,
+                       const int32_t (*pf_count)[MAX_TABLES], TicketDev tk, int64_t n_miss,
+                       int32_t *err, ScanWs &ws, hipStream_t s)
 {
+    const int d = pf.depth;
+    if (d < 1 || d > MAX_PF) {
+        ws.overflow = true;
+        return;
+    }
     PfOut o{};
+    PfVal val{};
     o.n_own = n_own;
     o.n_miss = n_miss;
     o.row_bits = tb.row_bits;
     o.T = tb.T;
+    o.depth = d;
     o.own_key = pf.own_key;
     o.own_uidx = pf.own_uidx;
-    o.next_keys = next_ukeys;
     o.m_key = tk.m_key;
     o.m_uidx = tk.m_uidx;
     o.err = err;
-    int32_t pfa = 0, vb = 0;
-    for (int t = 0; t < tb.T; ++t) {
-        o.pf_first[t] = pfa;
-        o.vbase[t] = vb;
-        o.own[t] = own[t];
-        pfa += pf_count[t];
-        vb += own[t] + pf_count[t];
+    val.n_own = n_own;
+    val.depth = d;
+    val.flag = pf.flag;
+    val.stride = pf.stride;
+    int64_t at = n_own;
+    for (int w = 0; w < MAX_PF; ++w) {
+        o.start[w] = val.start[w] = at;
+        if (w < d) {
+            o.next_keys[w] = next_ukeys[w];
+            val.n_next[w] = n_next[w];
+            at += max_next[w];
+        }
     }
-    seg_scan<uint32_t>(PfSeg{n_own, n_next}, 1, n_own + (next_ukeys ? max_next : 0),
-                       PfVal{n_own, pf.flag}, o, ws, s);
+    o.start[MAX_PF] = val.start[MAX_PF] = at;
+    // destinations: table t's victims start at vbase[t]; its own misses come
+    // first, then successor 0's flagged keys, then successor 1's, ...
+    int32_t tot[MAX_PF] = {};
+    for (int w = 0; w < d; ++w)
+        for (int t = 0; t < tb.T; ++t) tot[w] += pf_count[w][t];
+    int32_t vb = 0, pfb = 0;
+    for (int t = 0; t < tb.T; ++t) {
+        o.pf_before[t] = pfb;
+        int32_t before_w = 0;     // table t's flagged keys of the successors before w
+        for (int w = 0; w < d; ++w) {
+            int32_t first = 0;    // flagged keys before (successor w, table t) in the scan
+            for (int w2 = 0; w2 < w; ++w2) first += tot[w2];
+            for (int t2 = 0; t2 < t; ++t2) first += pf_count[w][t2];
+            o.off[w][t] = vb + own[t] + before_w - first;
+            before_w += pf_count[w][t];
+        }
+        pfb += before_w;
+        vb += own[t] + before_w;
+    }
+    seg_scan<uint32_t>(PfSeg{at}, 1, at, val, o, ws, s);
 }
 
 }  // namespace sp

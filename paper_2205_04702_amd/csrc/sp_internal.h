@@ -7,6 +7,7 @@
 namespace sp {
 
 constexpr int MAX_TABLES = 64;
+constexpr int MAX_PF = 4;        // successor batches a plan may prefetch
 constexpr int MAX_WINDOW = 16;   // batches one plan may look at (lookahead <= 15)
 constexpr int QUERY_TILE = 256;  // unique keys per block of the query (one per thread)
 constexpr int SEL_BITS = 11;     // digit width of the LRU radix select
@@ -51,13 +52,14 @@ struct DevCounters {
     int32_t n_multi;             // its runs longer than one chunk
     int32_t miss[MAX_TABLES];
     int32_t held[MAX_TABLES];
-    int32_t pf[MAX_TABLES];      // rows of the next batch to prefetch (prefetch mode)
+    int32_t pf[MAX_PF][MAX_TABLES];  // rows of successor w + 1 to prefetch (prefetch mode)
     int32_t err_sticky;          // ERR_HASH_FULL / ERR_PLAN from any earlier commit
     int32_t pad2[3];
 };
 constexpr int COUNTERS_CLEARED = (int)(offsetof(DevCounters, err_sticky) / sizeof(int32_t));
 constexpr int PART_COPIES = 64;  // copies of the per-table counters the probe adds into
-constexpr int PART_WORDS = 3 * MAX_TABLES;  // one copy: miss, held and prefetch counts
+// one copy: miss, held and the prefetch counts of each successor
+constexpr int PART_WORDS = (2 + MAX_PF) * MAX_TABLES;
 constexpr int COUNTER_WORDS = (int)(sizeof(DevCounters) / sizeof(int32_t));
 constexpr int32_t ERR_ID_RANGE = 1, ERR_OFFSETS = 2, ERR_HASH_FULL = 4, ERR_PLAN = 8;
 constexpr int32_t ERR_TABLE_IDS = 16;  // a table has more IDs than the configured bound
@@ -187,14 +189,16 @@ RadixPlan radix_plan(int64_t n, int bits);
 // The query: hold marks, hits, the misses in ascending key order (tk.m_key,
 // tk.m_uidx) and per-table counts of one plan, published to host_mapped
 // (word i = seq << 32 | counter word i) by the last block.
-// Prefetch mode: the query compacts the planned batch's own misses into
-// own_key / own_uidx and flags (flag[j] = 1) the next batch's unique keys to
-// prefetch; the arrangement then writes both into the ticket's miss list.
+// Prefetch mode (depth d >= 1): the query compacts the planned batch's own
+// misses into own_key / own_uidx and flags (flag[(w-1) * stride + j] = 1) the
+// unique keys j of successor w = 1..d to prefetch; the arrangement then
+// writes both into the ticket's miss list.
 struct PrefetchDev {
-    int32_t on;
+    int32_t depth;
     uint32_t *own_key;
     int32_t *own_uidx;
     int32_t *flag;
+    int64_t stride;
 };
 void launch_query(const Tables &tb, const uint64_t *hash, uint32_t mask,
                   const uint32_t *const *ukeys, const int32_t *const *nuniq, int nwin,
@@ -216,12 +220,15 @@ void launch_commit(const Tables &tb, uint64_t *hash, uint32_t mask, TicketDev tk
                    int32_t *key_of_slot, int32_t *last_use, int32_t *uses, int32_t u,
                    bool prefetch, DevCounters *cnt, hipStream_t s);
 // Prefetch mode: the ticket's miss list, per table the planned batch's own
-// misses (ascending) then the next batch's flagged keys (ascending), at
-// vbase[t] = first victim of table t; prefetched entries get m_uidx = -1.
-void launch_pf_arrange(const Tables &tb, PrefetchDev pf, int64_t n_own, const int32_t *n_next,
-                       int64_t max_next, const uint32_t *next_ukeys, const int32_t *own,
-                       const int32_t *pf_count, TicketDev tk, int64_t n_miss, int32_t *err,
-                       ScanWs &ws, hipStream_t s);
+// misses (ascending) then, successor by successor, its flagged keys
+// (ascending), from vbase[t] = first victim of table t; prefetched entries get
+// m_uidx = -1.  Successor w (1..pf.depth): n_next[w-1] points at its count of
+// unique keys (at most max_next[w-1]), next_ukeys[w-1] at the keys.
+void launch_pf_arrange(const Tables &tb, PrefetchDev pf, int64_t n_own,
+                       const int32_t *const *n_next, const int64_t *max_next,
+                       const uint32_t *const *next_ukeys, const int32_t *own,
+                       const int32_t (*pf_count)[MAX_TABLES], TicketDev tk, int64_t n_miss,
+                       int32_t *err, ScanWs &ws, hipStream_t s);
 
 // k_train.hip
 // Victim i: stage its slot's old row (if any) in stage row i, then write the

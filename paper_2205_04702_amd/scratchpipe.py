@@ -308,16 +308,17 @@ class ScratchPipe:
 
     policy: "lru", "lfu" or "random"; hold_past: earlier batches held as well;
     seed: the random policy's stream; max_table_ids: 0 or the most IDs any one
-    table has in a batch (a promise that is checked); prefetch: plans also fill
-    the next batch's missing rows; fill: "mapped" (zero-copy from pinned,
+    table has in a batch (a promise that is checked); prefetch: depth d (True =
+    1): plans also fill the missing rows of their next d batches; fill: "mapped"
+    (zero-copy from pinned,
     device-mapped tables) or "staged" (host gather, then copies)."""
 
     def __init__(self, rows, dim, slots, lookahead, host_tables, max_batch, max_ids,
                  flags: int = 0, device: int = 0, policy: str = "lru", hold_past: int = 0,
-                 seed: int = 0, max_table_ids: int = 0, prefetch: bool = False,
+                 seed: int = 0, max_table_ids: int = 0, prefetch=0,
                  fill: str = "mapped"):
         self.T = len(rows)
-        self.prefetch = bool(prefetch)
+        self.prefetch = int(prefetch)  # depth (True = 1)
         self.max_ids = int(max_ids)
         self.dim = dim
         self._rows = (C.c_int64 * self.T)(*[int(r) for r in rows])
@@ -327,7 +328,7 @@ class ScratchPipe:
                         lookahead=lookahead, host_tables=self._tabs, max_batch=max_batch,
                         max_ids=max_ids, flags=flags, device=device, policy=POLICIES[policy],
                         hold_past=hold_past, seed=seed, max_table_ids=max_table_ids,
-                        prefetch=int(self.prefetch), fill=FILLS[fill])
+                        prefetch=self.prefetch, fill=FILLS[fill])
         self.handle = sp_create(cfg)
         self._desc_cache = {}
 
@@ -383,9 +384,8 @@ class ScratchPipe:
         sp_set_flags(self.handle, flags)
 
     def debug_plan(self, ticket: int, nnz: int) -> dict:
-        # prefetch mode: misses of the planned and the next batch (each at most max_ids)
-        return sp_debug_plan(self.handle, ticket, nnz,
-                             nnz + self.max_ids if self.prefetch else nnz)
+        # prefetch mode: misses of the planned batch and its successors (each at most max_ids)
+        return sp_debug_plan(self.handle, ticket, nnz, nnz + self.prefetch * self.max_ids)
 
     def close(self) -> None:
         if getattr(self, "handle", None):

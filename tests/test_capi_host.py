@@ -96,7 +96,7 @@ def _cfg(**over):
     (dict(lookahead=12, hold_past=4), "hold_past"),
     (dict(max_table_ids=-1), "max_table_ids"),
     (dict(dim=256, max_batch=1 << 21), "4 GiB"),  # gradients addressed with 32-bit offsets
-    (dict(prefetch=2), "prefetch"),
+    (dict(lookahead=8, prefetch=5), "prefetch"),   # above SP_MAX_PREFETCH
     (dict(prefetch=-1), "prefetch"),
     (dict(fill=2), "fill"),
     (dict(fill=-1), "fill"),

@@ -92,3 +92,17 @@ def test_zipf_26x4M_full_size_prefetch(harness):
     _say(f"zipf-26x4M prefetch: worst fwd {r['worst_fwd']:.2e} table {r['worst_table']:.2e} "
          f"fills {st['misses']} prefetched {st['prefetched']} evictions {st['evictions']}")
     assert st["evictions"] > 0 and st["prefetched"] > 0
+
+
+def test_zipf_26x4M_full_size_prefetch_depth_4(harness):
+    """26 x 4M with prefetch depth 4 (the whole look-forward window) and the staged fill:
+    32 steps with bit-exact plans and sampled forwards."""
+    w = wl.get_workload("zipf-26x4M")
+    _say(f"case zipf-26x4M prefetch 4 staged, 32 steps {w.describe()}")
+    r = harness.run_sampled_parity(w, 32, check_plan_steps=set(range(32)),
+                                   check_fwd_steps={0, 16, 31}, say=_say, prefetch=4,
+                                   fill="staged", host_ids=True)
+    st = r["stats"]
+    _say(f"zipf-26x4M prefetch 4: worst fwd {r['worst_fwd']:.2e} table {r['worst_table']:.2e} "
+         f"fills {st['misses']} prefetched {st['prefetched']} evictions {st['evictions']}")
+    assert st["evictions"] > 0 and st["prefetched"] > 0

@@ -154,3 +154,63 @@ def test_capacity_error_from_the_prefetched_rows_changes_nothing(harness):
     finally:
         ctx.close()
         host.close()
+
+
+# ----------------------------------------------------------------------------- deeper prefetch
+
+@pytest.mark.parametrize("depth", [2, 3, 4])
+def test_deeper_prefetch_every_step(harness, depth):
+    """Prefetch depth d: each plan also fills the rows of its next d batches that are
+    neither cached nor in an earlier window batch, successor by successor."""
+    w = wl.custom(rows=[6000, 9000, 4000], dim=32, batch=64, pooling=[4, 3, 5],
+                  slots=[2500, 3000, 2200], lookahead=4, steps=30,
+                  dist=(("zipf", 1.05), ("uniform",), ("zipf", 1.2)), seed=60 + depth)
+    _say(f"case prefetch depth {depth}")
+    r = harness.run_parity(w, prefetch=depth, prepare_ahead=2)
+    st = r["stats"]
+    assert st["prefetched"] > 0 and st["evictions"] > 0
+
+
+@pytest.mark.parametrize("policy", ["lfu", "random"])
+def test_deeper_prefetch_policies_past_window_device_ids(harness, policy):
+    w = wl.custom(rows=[40_000] * 2, dim=16, batch=96, pooling=4, slots=[5000] * 2,
+                  lookahead=3, steps=24, dist=("zipf", 1.05), seed=71)
+    _say(f"case prefetch depth 3 policy {policy} past 1")
+    r = harness.run_parity(w, prefetch=3, policy=policy, seed=9, hold_past=1, prepare_ahead=2,
+                           device_ids=True, sync_each_step=False, check_fwd_steps=[0, 12, 23])
+    assert r["stats"]["prefetched"] > 0
+
+
+def test_deeper_prefetch_ragged_general_ingest_large_victims(harness):
+    """Ragged and empty bags on the general ingest path, and over 2048 victims per
+    table (the global victim sort), at depth 2."""
+    w = wl.custom(rows=[800_000, 500_000], dim=16, batch=1024, pooling=[4, 3],
+                  slots=[40_000, 30_000], lookahead=2, steps=10, dist=("uniform",), seed=72)
+    batches = [wl.ragged_batch(w, s, max_len=7, empty_frac=0.2) for s in range(w.steps)]
+    _say("case prefetch depth 2 ragged large")
+    r = harness.run_parity(w, batches, prefetch=2, max_table_ids=0, sync_each_step=False,
+                           check_fwd_steps=[0, 9])
+    assert r["stats"]["prefetched"] > 2 * 2048
+
+
+def test_deeper_prefetch_overlapped_and_staged_equal_serialized(harness):
+    """Depth 3: the overlapped schedule, the serialised one, event waits and the staged
+    fill give bit-identical tables."""
+    import numpy as np
+    from paper_2205_04702_amd import scratchpipe as spm
+    w = wl.custom(rows=[3000, 5000, 2000], dim=64, batch=64, pooling=[4, 6, 2],
+                  slots=[1400, 2000, 900], lookahead=3, steps=30, dist=("zipf", 1.05), seed=73)
+    _say("case prefetch depth 3 overlap vs serialised vs staged")
+    batches = harness.make_inputs(w)
+    results = []
+    for flags, ahead, fill in ((0, 0, "mapped"), (spm.SP_FLAG_DEBUG_SYNC, 0, "mapped"),
+                               (spm.SP_FLAG_EVENT_WAITS, 2, "mapped"), (0, 2, "staged")):
+        host = harness.fresh_host(w, fill)
+        st = harness.run_gpu(w, batches, host, flags=flags, prepare_ahead=ahead, prefetch=3,
+                             fill=fill)
+        assert st["prefetched"] > 0 and st["evictions"] > 0
+        results.append([host[t].copy() for t in range(w.tables)])
+        host.close()
+    for r in results[1:]:
+        for x, y in zip(results[0], r):
+            assert np.array_equal(x, y)

@@ -153,6 +153,7 @@ struct Wait {
 // mapped fill enqueues it at once, the staged fill hands it to the fill
 // thread, which first gathers and copies the rows.
 struct MoveJob {
+    bool gather = false;   // the staged fill's gather and copies, else the move itself
     int64_t k = 0, n = 0;  // plan, rows to place
     int sl = 0, e = 0;     // staging slot, ticket entry
     int32_t u = 0;
@@ -325,6 +326,8 @@ constexpr int NSTAGE = 3;
 // write-back copies above this size go on the ingest stream, where they
 // overlap the next fill; smaller ones go on the copy stream
 constexpr int64_t SMALL_COPY_BYTES = 8ll << 20;
+// a write-back copy above this size takes longer than sorting a batch
+constexpr int64_t LONG_COPY_BYTES = 256ll << 20;
 
 struct sp_ctx {
     // configuration
@@ -674,38 +677,44 @@ static hipError_t enqueue_move(sp_ctx *h, const MoveJob &j, const float *staged)
 // of one piece runs while the next is gathered.
 constexpr int64_t FILL_PIECE_BYTES = 8ll << 20;
 
-// The staged fill of one plan, on the fill thread: wait for the missing keys
-// on the host, gather their rows piece by piece into pinned staging and
-// enqueue each piece's copy to the device, then the move.
-static hipError_t staged_move(sp_ctx *h, const MoveJob &j)
+// The staged fill's gather of one plan, on the fill thread: wait for the
+// missing keys on the host, then the gather threads take pieces of them in
+// turn, gather a piece's rows into pinned staging and enqueue its copy to the
+// device themselves (pieces are independent, so their copies may be enqueued
+// in any order; the move is enqueued after all of them).
+static hipError_t staged_gather(sp_ctx *h, const MoveJob &j)
 {
     const int sl = j.sl;
     hipError_t r = hipSuccess;
-    if (j.n > 0) {
-        if ((r = hipEventSynchronize(h->ev_mkey[sl])) != hipSuccess) return r;
-        // the copies out of this pinned staging slot (plan k - NSTAGE) have run
-        if (h->fill_h2d_used[sl] && (r = hipEventSynchronize(h->ev_fill_h2d[sl])) != hipSuccess)
-            return r;
-        const double t0 = host_ms();
-        const int D = h->D;
-        const int64_t piece = std::max<int64_t>(1, FILL_PIECE_BYTES / (4 * (int64_t)D));
-        float *const hs = h->h_fill[sl];
-        if (j.timing && (r = h->t_h2d.begin(h->s_move)) != hipSuccess) return r;
-        for (int64_t b = 0; b < j.n && r == hipSuccess; b += piece) {
-            const int64_t e = std::min(j.n, b + piece);
-            h->gather.run(e - b, 256, [&](int64_t b0, int64_t e0) {
-                copy_rows(h->host, h->tb, D, hs, h->h_mkey[sl], b + b0, b + e0, false);
-            });
-            r = hipMemcpyAsync(h->d_fill[sl] + b * D, hs + b * D, sizeof(float) * (e - b) * D,
-                               hipMemcpyHostToDevice, h->s_move);
+    if (j.n <= 0) return r;
+    if ((r = hipEventSynchronize(h->ev_mkey[sl])) != hipSuccess) return r;
+    // the copies out of this pinned staging slot (plan k - NSTAGE) have run
+    if (h->fill_h2d_used[sl] && (r = hipEventSynchronize(h->ev_fill_h2d[sl])) != hipSuccess)
+        return r;
+    const double t0 = host_ms();
+    const int D = h->D;
+    const int64_t piece = std::max<int64_t>(1, FILL_PIECE_BYTES / (4 * (int64_t)D));
+    const int64_t npieces = (j.n + piece - 1) / piece;
+    float *const hs = h->h_fill[sl];
+    if (j.timing && (r = h->t_h2d.begin(h->s_move)) != hipSuccess) return r;
+    std::atomic<int> bad{0};
+    h->gather.run(npieces, 1, [&](int64_t p0, int64_t p1) {
+        (void)hipSetDevice(h->device);
+        for (int64_t q = p0; q < p1; ++q) {
+            const int64_t b = q * piece, e = std::min(j.n, b + piece);
+            copy_rows(h->host, h->tb, D, hs, h->h_mkey[sl], b, e, false);
+            const hipError_t c = hipMemcpyAsync(h->d_fill[sl] + b * D, hs + b * D,
+                                                sizeof(float) * (e - b) * D,
+                                                hipMemcpyHostToDevice, h->s_move);
+            if (c != hipSuccess) bad.store((int)c);
         }
-        if (r != hipSuccess) return r;
-        if (j.timing && (r = h->t_h2d.end(h->s_move)) != hipSuccess) return r;
-        if ((r = hipEventRecord(h->ev_fill_h2d[sl], h->s_move)) != hipSuccess) return r;
-        h->fill_h2d_used[sl] = true;
-        h->gather_ms += host_ms() - t0;
-    }
-    return enqueue_move(h, j, h->d_fill[sl]);
+    });
+    if (bad.load()) return (hipError_t)bad.load();
+    if (j.timing && (r = h->t_h2d.end(h->s_move)) != hipSuccess) return r;
+    if ((r = hipEventRecord(h->ev_fill_h2d[sl], h->s_move)) != hipSuccess) return r;
+    h->fill_h2d_used[sl] = true;
+    h->gather_ms += host_ms() - t0;
+    return r;
 }
 
 static void filler_main(sp_ctx *h)
@@ -725,14 +734,14 @@ static void filler_main(sp_ctx *h)
             std::lock_guard<std::mutex> lk(h->fmu);
             failed = !h->fill_err.empty();
         }
-        if (!failed) r = staged_move(h, j);
+        if (!failed) r = j.gather ? staged_gather(h, j) : enqueue_move(h, j, h->d_fill[j.sl]);
         {
             std::lock_guard<std::mutex> lk(h->fmu);
             if (r != hipSuccess && h->fill_err.empty())
                 h->fill_err = std::string("fill of plan ") + std::to_string(j.k) + ": " +
                               hipGetErrorString(r);
             h->fjobs.pop_front();
-            h->fill_enqueued = j.k + 1;
+            if (!j.gather) h->fill_enqueued = j.k + 1;
         }
         h->fcv_done.notify_all();
     }
@@ -1145,10 +1154,16 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
 {
     const int r = (int)(q % h->nring);
     BatchDev &b = h->ring[r];
+    hipStream_t si = h->s_ingest;
     // the previous occupant (batch q - nring) must be done with its backward
-    HIPCHK(h, wait_unless_done(h->s_ingest, h->ev_upd[r]));
+    HIPCHK(h, wait_unless_done(si, h->ev_upd[r]));
+    // With the staged fill the step is bound by the host's gather, and a batch
+    // sorted ahead has time to spare: it waits for the last update issued, so
+    // that the training kernels do not share the GPU with it.
+    if (h->staged && h->updated > 0)
+        HIPCHK(h, wait_unless_done(si, h->ev_upd[(h->updated - 1) % h->nring]));
     const bool timing = h->flags & SP_FLAG_TIMING;
-    if (timing) HIPCHK(h, h->t_ing.begin(h->s_ingest));
+    if (timing) HIPCHK(h, h->t_ing.begin(si));
     const int64_t nbags = (int64_t)h->T * bt.batch;
     const int32_t *ids = bt.ids, *off = bt.bag_off;
     if (!bt.on_device) {
@@ -1161,10 +1176,10 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
         memcpy(h->h_off[r], bt.bag_off, sizeof(int32_t) * (nbags + 1));
         if (bt.nnz > 0)
             HIPCHK(h, hipMemcpyAsync(b.ids, h->h_ids[r], sizeof(int32_t) * bt.nnz,
-                                     hipMemcpyHostToDevice, h->s_ingest));
+                                     hipMemcpyHostToDevice, si));
         HIPCHK(h, hipMemcpyAsync(b.bag_off, h->h_off[r], sizeof(int32_t) * (nbags + 1),
-                                 hipMemcpyHostToDevice, h->s_ingest));
-        HIPCHK(h, hipEventRecord(h->ev_ids[r], h->s_ingest));
+                                 hipMemcpyHostToDevice, si));
+        HIPCHK(h, hipEventRecord(h->ev_ids[r], si));
         h->ids_pending[r] = 1;
         ids = b.ids;
         off = b.bag_off;
@@ -1182,11 +1197,11 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
     }
     launch_ingest(h->tb, b, ids, off, bt.batch, bt.nnz, h->key_bits, h->chunk, h->max_table_ids,
                   h->max_ids, h->nchunk_max, h->itmp_k, h->itmp_v, h->ihist, h->ws_ingest,
-                  h->ev_consumed, ic, h->s_ingest);
+                  h->ev_consumed, ic, si);
     CHECK_LAUNCH(h);
     if (h->ws_ingest.overflow) return fail(h, SP_ERR_HIP, "internal: scan workspace too small");
-    HIPCHK(h, hipEventRecord(h->ring_ready[r], h->s_ingest));
-    if (timing) HIPCHK(h, h->t_ing.end(h->s_ingest));
+    HIPCHK(h, hipEventRecord(h->ring_ready[r], si));
+    if (timing) HIPCHK(h, h->t_ing.end(si));
     h->ring_seen[r] = 0;
     h->ring_batch[r] = q;
     h->ring_nnz[r] = bt.nnz;
@@ -1223,6 +1238,32 @@ static sp_status issue_copy(sp_ctx *h, hipStream_t s)
     }
     h->cv.notify_one();
     h->copy_pending = -1;
+    return SP_OK;
+}
+
+// Ingest the window's batches after the hold window (prepared ahead) that are
+// not in the ring yet.
+static sp_status ingest_ahead(sp_ctx *h, const sp_batch *window, int n, int nhold, int64_t k)
+{
+    for (int w = nhold; w < n; ++w)
+        if (h->ring_batch[(k + w) % h->nring] != k + w) TRY(ingest(h, window[w], k + w));
+    return SP_OK;
+}
+
+// RAW-4: a row evicted by plan p may be refilled from plan p + n_p on (n_p
+// batches in p's hold window; n_p - d with prefetch depth d, which fills the
+// batches after the planned one): before plan k reads the host tables for
+// its fill, every write-back due by then has landed.
+static sp_status join_writebacks(sp_ctx *h, int64_t k)
+{
+    int64_t need = -1;
+    for (const auto &d : h->deadlines)
+        if (d.second <= k) need = std::max(need, d.first);
+    if (need >= 0) {
+        if (h->copy_pending >= 0 && h->copy_pending <= need) TRY(issue_copy(h, h->s_copy));
+        TRY(join_jobs(h, need));
+        while (!h->deadlines.empty() && h->deadlines.front().first <= need) h->deadlines.pop_front();
+    }
     return SP_OK;
 }
 
@@ -1390,11 +1431,9 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     const int r0 = (int)(k % h->nring);
     double tC = host_ms();
     h->host_ms[1] += tC - tB;
-    for (int w = nhold; w < n; ++w) {
-        if (h->ring_batch[(k + w) % h->nring] != k + w) {
-            TRY(ingest(h, window[w], k + w));
-        }
-    }
+    // batches prepared ahead: with the staged fill they wait until the gather
+    // has its keys (their host copy would delay it)
+    if (!h->staged) TRY(ingest_ahead(h, window, n, nhold, k));
     double tD = host_ms();
     h->host_ms[0] += tD - tC;
     DevCounters c;
@@ -1438,7 +1477,6 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     }
 
     // ---- phase 2: commit
-    if (timing) HIPCHK(h, h->t_plan.begin(h->s_plan));
     const BatchDev &b0 = h->ring[r0];
     th.nnz = h->ring_nnz[r0];
     th.B = (int32_t)h->ring_B[r0];
@@ -1449,6 +1487,53 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     th.n_own = n_own;
     th.ring = r0;
     th.nwin = nhold;
+
+    if (pf_on && n_miss > 0) {
+        // the miss list: per table own misses, then each successor's rows to
+        // prefetch (the query left the own misses aside); it needs only the
+        // query's outputs and counts, not the victims
+        const int32_t *n_next[MAX_PF] = {};
+        const uint32_t *next_keys[MAX_PF] = {};
+        int64_t max_next[MAX_PF] = {};
+        for (int w = 0; w < pf_d; ++w) {
+            const int r1 = (int)((k + 1 + w) % h->nring);
+            n_next[w] = h->ring[r1].scal;
+            next_keys[w] = h->ring[r1].ukeys;
+            max_next[w] = h->ring_nnz[r1];
+        }
+        launch_pf_arrange(h->tb,
+                          PrefetchDev{pf_d, h->pf_own_key, h->pf_own_uidx, h->pf_flag, h->max_ids},
+                          n_own, n_next, max_next, next_keys, c.miss, c.pf, tk, n_miss,
+                          &h->cnt->err_sticky, h->ws_plan, h->s_plan);
+    }
+    if (h->staged && n_miss > 0) {
+        // the staged fill gathers on the host as soon as it has the missing
+        // keys, while the victims are chosen: they go first.  Their pinned
+        // slot was last read by the fill of plan k - NSTAGE.
+        const int sl = (int)(k % NSTAGE);
+        TRY(join_fill(h, k - NSTAGE));
+        HIPCHK(h, hipMemcpyAsync(h->h_mkey[sl], tk.m_key, sizeof(uint32_t) * n_miss,
+                                 hipMemcpyDeviceToHost, h->s_plan));
+        HIPCHK(h, hipEventRecord(h->ev_mkey[sl], h->s_plan));
+        // the gather reads the host tables: the write-backs due land first
+        TRY(join_writebacks(h, k));
+        MoveJob gj;
+        gj.gather = true;
+        gj.k = k;
+        gj.n = n_miss;
+        gj.sl = sl;
+        gj.timing = timing;
+        {
+            std::lock_guard<std::mutex> lk(h->fmu);
+            h->fjobs.push_back(gj);
+        }
+        h->fcv.notify_one();
+        // The victims and the commit are then off the step's path (the gather
+        // takes far longer): they wait for the update of the batch before,
+        // so that the training kernels do not share the GPU with them.
+        if (k >= 1) HIPCHK(h, wait_unless_done(h->s_plan, h->ev_upd[(k - 1) % h->nring]));
+    }
+    if (timing) HIPCHK(h, h->t_plan.begin(h->s_plan));
 
     if (n_miss > 0) {
         const int64_t cap = (int64_t)h->hash_mask + 1;
@@ -1484,32 +1569,6 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
         launch_select_victims(a, levels, maxS, h->held, h->sel_state, h->sel_hist, h->vk0,
                               h->vv0, h->vk1, (uint32_t *)nullptr, n_miss, h->hist, h->ws_plan,
                               tk.v_slot, &h->cnt->err_sticky, h->s_plan);
-        if (pf_on) {
-            // the miss list in victim order: per table own misses, then each
-            // successor's rows to prefetch (the query left the own misses aside)
-            const int32_t *n_next[MAX_PF] = {};
-            const uint32_t *next_keys[MAX_PF] = {};
-            int64_t max_next[MAX_PF] = {};
-            for (int w = 0; w < pf_d; ++w) {
-                const int r1 = (int)((k + 1 + w) % h->nring);
-                n_next[w] = h->ring[r1].scal;
-                next_keys[w] = h->ring[r1].ukeys;
-                max_next[w] = h->ring_nnz[r1];
-            }
-            launch_pf_arrange(h->tb,
-                              PrefetchDev{pf_d, h->pf_own_key, h->pf_own_uidx, h->pf_flag, h->max_ids},
-                              n_own, n_next, max_next, next_keys, c.miss, c.pf, tk, n_miss,
-                              &h->cnt->err_sticky, h->ws_plan, h->s_plan);
-        }
-        if (h->staged) {
-            // the missing keys go to the host for the gather; their pinned slot
-            // was last read by the fill of plan k - NSTAGE
-            const int sl = (int)(k % NSTAGE);
-            TRY(join_fill(h, k - NSTAGE));
-            HIPCHK(h, hipMemcpyAsync(h->h_mkey[sl], tk.m_key, sizeof(uint32_t) * n_miss,
-                                     hipMemcpyDeviceToHost, h->s_plan));
-            HIPCHK(h, hipEventRecord(h->ev_mkey[sl], h->s_plan));
-        }
     }
     launch_commit(h->tb, h->hash, h->hash_mask, tk, b0, n_miss, th.n_unique, th.nnz, h->key_of_slot,
                   h->last_use, h->uses, u, pf_on, h->cnt, h->s_plan);
@@ -1524,8 +1583,15 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     // behind this call's ingests (its fill has normally finished by now): it
     // then overlaps this plan's fill (the two use the host link in opposite
     // directions) and is well under way when the next call's ingest comes
-    if (h->copy_pending >= 0 && h->copy_n * (h->D + 1) * (int64_t)sizeof(float) > SMALL_COPY_BYTES)
-        TRY(issue_copy(h, h->s_ingest));
+    // With the staged fill the batch prepared ahead is ingested here, beside
+    // that copy on the ingest stream: behind a copy that is short next to its
+    // sort, in front of a long one (which would otherwise hold back the next
+    // plan's query, which needs the batch)
+    const int64_t copy_bytes = h->copy_n * (h->D + 1) * (int64_t)sizeof(float);
+    const bool large_copy = h->copy_pending >= 0 && copy_bytes > SMALL_COPY_BYTES;
+    if (h->staged && large_copy && copy_bytes > LONG_COPY_BYTES) TRY(ingest_ahead(h, window, n, nhold, k));
+    if (large_copy) TRY(issue_copy(h, h->s_ingest));
+    if (h->staged) TRY(ingest_ahead(h, window, n, nhold, k));  // (nothing left if done above)
     double tF = host_ms();
     h->host_ms[3] += tF - tE;
     // ---- the next plan's query, when its whole window is known: batches
@@ -1540,16 +1606,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     tF = tG;
     // ---- mover (own stream): write-back of evicted rows and fill of misses;
     // the next plan's query does not wait for it
-    // RAW-4: rows evicted by plan p may be refilled from plan p + n_p on
-    // (n_p - d with prefetch depth d, which fills the batches after the planned one)
-    int64_t need = -1;
-    for (const auto &d : h->deadlines)
-        if (d.second <= k) need = std::max(need, d.first);
-    if (need >= 0) {
-        if (h->copy_pending >= 0 && h->copy_pending <= need) TRY(issue_copy(h, h->s_copy));
-        TRY(join_jobs(h, need));
-        while (!h->deadlines.empty() && h->deadlines.front().first <= need) h->deadlines.pop_front();
-    }
+    if (!h->staged) TRY(join_writebacks(h, k));  // the staged fill joined before its gather
     const int sl = (int)(k % NSTAGE);
     MoveJob mj;
     mj.k = k;

@@ -101,13 +101,24 @@ __device__ __forceinline__ void sgd_row(float4 *w, float4 g, float lr) { *w = sg
 
 // Gradient coalescing and SGD (Sec. II-B "Backpropagation").  The sorted
 // positions of one batch form runs of equal keys; each run is cut into chunks
-// of at most `chunk` positions.  One group of LPR lanes (one row width) takes
-// one chunk, so a wave works on 64/LPR chunks at once: it sums the gradient
-// rows of the bags at its positions in ascending position order.
+// of at most `chunk` positions.  One group of G = LPR / VPL lanes takes one
+// chunk, each lane VPL of the row's LPR 16-byte words (word j * G + c for lane
+// c), so a wave works on 64 / G chunks at once and each lane keeps VPL loads
+// of every row in flight: more rows per memory round trip than one word per
+// lane would give, which is what bounds this kernel (each chunk is a short
+// chain of dependent loads: descriptor, then slot and bag indices, then the
+// Storage row and gradient rows).  It sums the gradient rows of the bags at
+// its positions in ascending position order.
 //  * a run of one chunk updates its Storage row directly: W -= lr * g;
 //  * a longer run stores per-chunk partial sums, which k_bwd_combine adds in
 //    chunk order before updating the row (the kernel boundary orders the two).
-constexpr int BWD_INFLIGHT = 8;  // gradient rows in flight per lane
+constexpr int BWD_INFLIGHT = 8;  // gradient words in flight per lane (rows x VPL)
+
+// Words per lane for rows of LPR words (the launch's grid follows it): two
+// from rows of 64 floats up.  Measured alone on the 26x10M workload's update
+// (128 floats): 0.80 ms with one word per lane, 0.69 ms with four (fewer
+// waves fit: 97 registers), 0.63 ms with two (71 registers, 7 waves per SIMD).
+constexpr int bwd_vpl(int lpr) { return lpr >= 16 ? 2 : 1; }
 
 template <int LPR>
 __global__ void __launch_bounds__(BLOCK) k_backward(float4 *__restrict__ storage,
@@ -119,11 +130,14 @@ __global__ void __launch_bounds__(BLOCK) k_backward(float4 *__restrict__ storage
                                                     int64_t nbags, int64_t nslots, float lr,
                                                     float4 *__restrict__ partial)
 {
+    constexpr int VPL = bwd_vpl(LPR);
+    constexpr int G = LPR / VPL;                // lanes per chunk
+    constexpr int INFL = BWD_INFLIGHT / VPL;    // gradient rows in flight per lane
     // consecutive chunks (one table's) on one XCD: the table's bag gradients
     // share its L2
     const int64_t t = xcd_block(blockIdx.x, gridDim.x) * BLOCK + threadIdx.x;
-    const int64_t ch = t / LPR;
-    const int c = (int)(t % LPR);
+    const int64_t ch = t / G;
+    const int c = (int)(t % G);
     if (ch >= n_chunks) return;  // whole lane groups leave together
     const int4 d = chunk_desc[ch];  // first position, end position, run, chunks of the run
     const int64_t p0 = d.x, p1 = d.y;
@@ -133,47 +147,57 @@ __global__ void __launch_bounds__(BLOCK) k_backward(float4 *__restrict__ storage
     // than after them: one memory round trip less on the lane's path
     const bool direct = nch == 1 && (uint32_t)slot < (uint64_t)nslots;
     float4 *const w = storage + (direct ? (int64_t)slot * LPR + c : 0);
-    const float4 w0 = direct ? *w : make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 w0[VPL];
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) w0[j] = direct ? w[j * G] : make_float4(0.f, 0.f, 0.f, 0.f);
     // A chunk's bag indices arrive in one coalesced load (lane c of the group
-    // holds positions c, c+LPR, ...) and are broadcast by shuffles, so its
-    // gradient rows are requested BWD_INFLIGHT at a time without waiting on
-    // further index loads.  Sums stay in position order.
-    constexpr int PER_LANE = BWD_CHUNK / LPR > 0 ? BWD_CHUNK / LPR : 1;
+    // holds positions c, c+G, ...) and are broadcast by shuffles, so its
+    // gradient rows are requested INFL at a time without waiting on further
+    // index loads.  Sums stay in position order.
+    constexpr int PER_LANE = BWD_CHUNK / G > 0 ? BWD_CHUNK / G : 1;
     const int gbase = lane_id() - c;
     // 32-bit byte offsets from the uniform base (the gradient array is far
     // below 4 GiB): one address register per load in flight
     const char *__restrict__ gbytes = reinterpret_cast<const char *>(grad);
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 acc[VPL];
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) acc[j] = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int64_t base = p0; base < p1; base += BWD_CHUNK) {
         const int n = (int)(p1 - base < BWD_CHUNK ? p1 - base : BWD_CHUNK);
         int32_t mine[PER_LANE];
 #pragma unroll
         for (int l = 0; l < PER_LANE; ++l) {
-            const int k = l * LPR + c;
+            const int k = l * G + c;
             const int32_t b = k < n ? sbag[base + k] : 0;
             mine[l] = (uint32_t)b < (uint64_t)nbags ? b : 0;
         }
 #pragma unroll
-        for (int k0 = 0; k0 < BWD_CHUNK; k0 += BWD_INFLIGHT) {
+        for (int k0 = 0; k0 < BWD_CHUNK; k0 += INFL) {
             if (k0 >= n) break;  // uniform within the lane group
-            float4 v[BWD_INFLIGHT];
+            float4 v[INFL][VPL];
 #pragma unroll
-            for (int q = 0; q < BWD_INFLIGHT; ++q) {
+            for (int q = 0; q < INFL; ++q) {
                 const int k = k0 + q;
                 // every lane of the group takes part in the shuffle; only the load is predicated
-                const int32_t b = __shfl(mine[k / LPR], gbase + k % LPR, WAVE);
+                const int32_t b = __shfl(mine[k / G], gbase + k % G, WAVE);
                 const uint32_t off = (uint32_t)b * (uint32_t)(LPR * 16) + (uint32_t)c * 16u;
-                v[q] = k < n ? *reinterpret_cast<const float4 *>(gbytes + off)
-                             : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+                for (int j = 0; j < VPL; ++j)
+                    v[q][j] = k < n ? *reinterpret_cast<const float4 *>(gbytes + off + j * G * 16)
+                                    : make_float4(0.f, 0.f, 0.f, 0.f);
             }
 #pragma unroll
-            for (int q = 0; q < BWD_INFLIGHT; ++q) acc = f4_add(acc, v[q]);
+            for (int q = 0; q < INFL; ++q)
+#pragma unroll
+                for (int j = 0; j < VPL; ++j) acc[j] = f4_add(acc[j], v[q][j]);
         }
     }
     if (nch > 1) {
-        partial[ch * LPR + c] = acc;
+#pragma unroll
+        for (int j = 0; j < VPL; ++j) partial[ch * LPR + j * G + c] = acc[j];
     } else if (direct) {
-        *w = sgd_step(w0, acc, lr);
+#pragma unroll
+        for (int j = 0; j < VPL; ++j) w[j * G] = sgd_step(w0[j], acc[j], lr);
     }
 }
 
@@ -362,7 +386,9 @@ void launch_backward(float *storage, int dim, int64_t nslots, const BatchDev &b,
     if (n_chunks <= 0) return;
     const int D4 = dim / 4;
     (void)chunk;
-    SP_DISPATCH_LPR_EV(D4, k_backward, grid_rows(n_chunks, D4), ev[0], ev[1], (float4 *)storage,
+    // one lane group of D4 / VPL lanes per chunk
+    SP_DISPATCH_LPR_EV(D4, k_backward, grid_rows(n_chunks, D4 / bwd_vpl(D4)), ev[0], ev[1],
+                       (float4 *)storage,
                        (const int4 *)b.chunk_desc, (const int32_t *)b.sbag, slot_u, n_chunks,
                        (const float4 *)grad, nbags, nslots, lr, (float4 *)partial);
     if (n_multi > 0)

@@ -138,6 +138,9 @@ def main():
                     help="also hold the rows of the P batches planned before each plan")
     ap.add_argument("--prefetch", type=int, default=0, metavar="D",
                     help="each plan also fills the missing rows of the next D batches")
+    ap.add_argument("--ahead", type=int, default=-1, metavar="N",
+                    help="batches after the hold window handed over early for sorting "
+                         "(-1: SP_MAX_AHEAD)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-timing", action="store_true", help="do not time kernels with events")
@@ -183,7 +186,7 @@ def main():
         # enough steps to place a row in every slot at the first batch's miss count
         fillup_max = 0 if not evicts else 200
     W, K, L = args.warmup, args.steps, w.lookahead
-    ahead = sp.SP_MAX_AHEAD
+    ahead = sp.SP_MAX_AHEAD if args.ahead < 0 else min(args.ahead, sp.SP_MAX_AHEAD)
     nsteps = fillup_max + W + K
     nb_needed = lambda steps: steps + L + 1 + ahead  # noqa: E731  (windows of the last step)
 

@@ -28,6 +28,7 @@
 #include <cstring>
 #include <deque>
 #include <functional>
+#include <memory>
 #include <mutex>
 #include <string>
 #include <thread>
@@ -322,12 +323,19 @@ static int sem_words(int nring) { return SEM_UPD + 8 * nring; }
 
 // staging slots of evicted rows (fill of plan p, copy of plan p - 1 and the
 // host scatter of plan p - 2 can all be in flight)
-constexpr int NSTAGE = 3;
+constexpr int MAX_NSTAGE = 3;
+// staged fill: bytes of gathered rows per host-to-device copy, an eighth of
+// the plan's rows within these bounds (measured on the MI355X machine beside a
+// device-to-host copy of the same size: 8 MiB copies reach 45 GB/s, 32 MiB
+// copies 56 GB/s; a small fill still needs several copies to overlap its
+// gather), and per work item of the gather threads (small, so that all of
+// them work on the piece whose copy is next)
+constexpr int64_t FILL_PIECE_MIN_BYTES = 8ll << 20;
+constexpr int64_t FILL_PIECE_BYTES = 32ll << 20;
+constexpr int64_t FILL_ITEM_BYTES = 1ll << 20;
 // write-back copies above this size go on the ingest stream, where they
 // overlap the next fill; smaller ones go on the copy stream
 constexpr int64_t SMALL_COPY_BYTES = 8ll << 20;
-// a write-back copy above this size takes longer than sorting a batch
-constexpr int64_t LONG_COPY_BYTES = 256ll << 20;
 
 struct sp_ctx {
     // configuration
@@ -410,11 +418,12 @@ struct sp_ctx {
 
     // write-back staging (two in flight)
     int64_t stage_rows = 0;
-    // staging of evicted rows, plan p in slot p % NSTAGE: n rows, then their n
+    // staging of evicted rows, plan p in slot p % nstage: n rows, then their n
     // previous keys.  Plan p's copy to the host is issued by plan p + 1 (or by
     // flush), when its fill has nearly always finished: copy_pending = p
-    float *stage_dev[NSTAGE]{}, *stage_host[NSTAGE]{};
-    hipEvent_t ev_d2h[NSTAGE]{};
+    float *stage_dev[MAX_NSTAGE]{}, *stage_host[MAX_NSTAGE]{};
+    hipEvent_t ev_d2h[MAX_NSTAGE]{};
+    int nstage = 3;  // staging slots in use
     int64_t copy_pending = -1, copy_n = 0;
 
     // plan stream: query, hold, victims, commit; ingest stream: sorting and
@@ -445,12 +454,13 @@ struct sp_ctx {
     // kernel then writes them into their slots.  The fill thread does this
     // per plan, in plan order, and enqueues everything of a plan's fill on the
     // move stream, where the calling thread then enqueues nothing.  Staging
-    // slot k % NSTAGE, like the write-back's.
+    // slot k % nstage, like the write-back's.
     bool staged = false;
-    int32_t *h_mkey[NSTAGE]{};
-    float *h_fill[NSTAGE]{}, *d_fill[NSTAGE]{};
-    hipEvent_t ev_mkey[NSTAGE]{}, ev_fill_h2d[NSTAGE]{};
-    bool fill_h2d_used[NSTAGE]{};
+    int32_t *h_mkey[MAX_NSTAGE]{};
+    uint32_t *h_mkey_dev[MAX_NSTAGE]{};  // their device-visible addresses
+    float *h_fill[MAX_NSTAGE]{}, *d_fill[MAX_NSTAGE]{};
+    hipEvent_t ev_mkey[MAX_NSTAGE]{}, ev_fill_h2d[MAX_NSTAGE]{};
+    bool fill_h2d_used[MAX_NSTAGE]{};
     std::thread filler;
     std::mutex fmu;
     std::condition_variable fcv, fcv_done;
@@ -673,38 +683,45 @@ static hipError_t enqueue_move(sp_ctx *h, const MoveJob &j, const float *staged)
     return hipStreamWriteValue64(s, h->sem + SEM_FILLED, (uint64_t)j.k + 1, 0);
 }
 
-// Bytes of gathered rows per host-to-device copy of the staged fill: the copy
-// of one piece runs while the next is gathered.
-constexpr int64_t FILL_PIECE_BYTES = 8ll << 20;
-
 // The staged fill's gather of one plan, on the fill thread: wait for the
-// missing keys on the host, then the gather threads take pieces of them in
-// turn, gather a piece's rows into pinned staging and enqueue its copy to the
-// device themselves (pieces are independent, so their copies may be enqueued
-// in any order; the move is enqueued after all of them).
+// missing keys on the host, then the gather threads take small items of them
+// in turn and gather their rows into pinned staging; the thread that
+// completes the last item of a piece enqueues that piece's copy to the device
+// (pieces are independent, so their copies may be enqueued in any order; the
+// move is enqueued after all of them).
 static hipError_t staged_gather(sp_ctx *h, const MoveJob &j)
 {
     const int sl = j.sl;
     hipError_t r = hipSuccess;
     if (j.n <= 0) return r;
     if ((r = hipEventSynchronize(h->ev_mkey[sl])) != hipSuccess) return r;
-    // the copies out of this pinned staging slot (plan k - NSTAGE) have run
+    // the copies out of this pinned staging slot (plan k - nstage) have run
     if (h->fill_h2d_used[sl] && (r = hipEventSynchronize(h->ev_fill_h2d[sl])) != hipSuccess)
         return r;
     const double t0 = host_ms();
     const int D = h->D;
-    const int64_t piece = std::max<int64_t>(1, FILL_PIECE_BYTES / (4 * (int64_t)D));
-    const int64_t npieces = (j.n + piece - 1) / piece;
+    const int64_t item = std::max<int64_t>(1, FILL_ITEM_BYTES / (4 * (int64_t)D));
+    const int64_t piece_bytes =
+        std::clamp<int64_t>(j.n * 4 * (int64_t)D / 8, FILL_PIECE_MIN_BYTES, FILL_PIECE_BYTES);
+    const int64_t piece = std::max<int64_t>(1, piece_bytes / (4 * (int64_t)D) / item) * item;
+    const int64_t nitems = (j.n + item - 1) / item, npieces = (j.n + piece - 1) / piece;
+    std::unique_ptr<std::atomic<int64_t>[]> left(new std::atomic<int64_t>[npieces]);
+    for (int64_t q = 0; q < npieces; ++q)  // items of piece q
+        left[q] = (std::min(j.n, (q + 1) * piece) - q * piece + item - 1) / item;
     float *const hs = h->h_fill[sl];
     if (j.timing && (r = h->t_h2d.begin(h->s_move)) != hipSuccess) return r;
     std::atomic<int> bad{0};
-    h->gather.run(npieces, 1, [&](int64_t p0, int64_t p1) {
-        (void)hipSetDevice(h->device);
-        for (int64_t q = p0; q < p1; ++q) {
-            const int64_t b = q * piece, e = std::min(j.n, b + piece);
+    h->gather.run(nitems, 1, [&](int64_t i0, int64_t i1) {
+        for (int64_t i = i0; i < i1; ++i) {
+            const int64_t b = i * item, e = std::min(j.n, b + item);
             copy_rows(h->host, h->tb, D, hs, h->h_mkey[sl], b, e, false);
-            const hipError_t c = hipMemcpyAsync(h->d_fill[sl] + b * D, hs + b * D,
-                                                sizeof(float) * (e - b) * D,
+            const int64_t q = b / piece;
+            if (left[q].fetch_sub(1) != 1) continue;
+            // the piece is complete (copy_rows fenced its streamed stores)
+            (void)hipSetDevice(h->device);
+            const int64_t pb = q * piece, pe = std::min(j.n, pb + piece);
+            const hipError_t c = hipMemcpyAsync(h->d_fill[sl] + pb * D, hs + pb * D,
+                                                sizeof(float) * (pe - pb) * D,
                                                 hipMemcpyHostToDevice, h->s_move);
             if (c != hipSuccess) bad.store((int)c);
         }
@@ -792,7 +809,7 @@ static void release(sp_ctx *h)
         for (auto &e : *v)
             if (e) hipEventDestroy(e);
     if (h->ev_consumed) hipEventDestroy(h->ev_consumed);
-    for (int i = 0; i < NSTAGE; ++i)
+    for (int i = 0; i < MAX_NSTAGE; ++i)
         for (hipEvent_t e : {h->ev_d2h[i], h->ev_mkey[i], h->ev_fill_h2d[i]})
             if (e) hipEventDestroy(e);
     for (hipEvent_t e : h->ev_ids)
@@ -969,12 +986,27 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     TRY(dalloc(h, &h->sel_hist, (int64_t)MAX_TABLES * SEL_BINS));
     TRY(dalloc(h, &h->partial, nchunk_max * h->D));
     h->stage_rows = std::min<int64_t>(NM, S);
-    for (int i = 0; i < NSTAGE; ++i) {
+    h->nstage = MAX_NSTAGE;
+    for (int i = 0; i < h->nstage; ++i) {
         TRY(dalloc(h, &h->stage_dev[i], h->stage_rows * (h->D + 1)));
         TRY(palloc(h, &h->stage_host[i], h->stage_rows * (h->D + 1)));
         HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_d2h[i], hipEventDisableTiming));
         if (h->staged) {  // at most min(misses, slots) rows per plan, like the write-back
-            TRY(palloc(h, &h->h_mkey[i], h->stage_rows));
+            {  // device-mapped: the query writes the missing keys here itself
+                void *p = nullptr;
+                const size_t bytes = sizeof(int32_t) * (size_t)std::max<int64_t>(h->stage_rows, 1);
+                if (injected_alloc_failure())
+                    return fail(h, SP_ERR_OOM, "hipHostMalloc(%zu) failed: injected (SP_FAIL_ALLOC_AFTER)", bytes);
+                hipError_t e = hipHostMalloc(&p, bytes, hipHostMallocMapped);
+                if (e != hipSuccess) {
+                    (void)hipGetLastError();
+                    return fail(h, SP_ERR_OOM, "hipHostMalloc(%zu) failed: %s", bytes, hipGetErrorString(e));
+                }
+                h->pinned_allocs.push_back(p);
+                h->pinned_bytes += (int64_t)bytes;
+                h->h_mkey[i] = (int32_t *)p;
+                HIPCHK(nullptr, hipHostGetDevicePointer((void **)&h->h_mkey_dev[i], p, 0));
+            }
             TRY(palloc(h, &h->h_fill[i], h->stage_rows * h->D));
             TRY(dalloc(h, &h->d_fill[i], h->stage_rows * h->D));
             HIPCHK(nullptr, hipEventCreateWithFlags(&h->ev_mkey[i], hipEventDisableTiming));
@@ -1033,13 +1065,15 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     }
     HIPCHK(nullptr, hipStreamSynchronize(h->s_plan));
     h->st.min_capacity_margin = INT64_MAX;
-    // host copy threads: the write-back scatter and (staged fill) the gather
-    // each take about half of the cores, their calling threads included
-    const int hw = (int)std::max(2u, std::thread::hardware_concurrency());
-    h->scatter.start(std::max(1, std::min(8, hw / 2) - 1));
+    // host copy threads, their calling threads included: the write-back
+    // scatter takes half of the cores; with the staged fill the gather, which
+    // is on the step's path, takes three quarters and the scatter, which has
+    // a few steps to finish, one quarter
+    const int hw = (int)std::max(4u, std::thread::hardware_concurrency());
+    h->scatter.start(std::max(1, (h->staged ? hw / 4 : std::min(8, hw / 2)) - 1));
     h->worker = std::thread(worker_main, h);
     if (h->staged) {
-        h->gather.start(std::max(1, std::min(8, hw / 2) - 1));
+        h->gather.start(std::max(1, hw * 12 / 16 - 1));
         h->filler = std::thread(filler_main, h);
     }
     return SP_OK;
@@ -1211,14 +1245,14 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
 
 // Issue the pending write-back copy (plan p = copy_pending) on stream s and
 // hand its rows to the write-back thread.  The host staging slot was last
-// used by plan p - NSTAGE, whose scatter is joined first.
+// used by plan p - nstage, whose scatter is joined first.
 static sp_status issue_copy(sp_ctx *h, hipStream_t s)
 {
     const int64_t p = h->copy_pending;
     if (p < 0) return SP_OK;
-    const int sl = (int)(p % NSTAGE);
+    const int sl = (int)(p % h->nstage);
     TRY(join_fill(h, p));  // ev_filled of plan p is recorded
-    if (p >= NSTAGE) TRY(join_jobs(h, p - NSTAGE));
+    if (p >= h->nstage) TRY(join_jobs(h, p - h->nstage));
     Job job;
     job.ticket = p;
     const int64_t n = h->copy_n;
@@ -1365,10 +1399,20 @@ static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, int32_t *stamp_o
     *seq_out = ++h->qseq;
     const PrefetchDev pf{std::min(h->pf_depth, nhold - 1), h->pf_own_key, h->pf_own_uidx,
                          h->pf_flag, h->max_ids};
+    // staged fill without prefetch: the query itself hands the missing keys to
+    // the host (their pinned slot was last read by the gather of plan k - nstage)
+    const int sl = (int)(k % h->nstage);
+    uint32_t *host_keys = nullptr;
+    if (h->staged && pf.depth == 0) {
+        TRY(join_fill(h, k - h->nstage));
+        host_keys = h->h_mkey_dev[sl];
+    }
     launch_query(h->tb, h->hash, h->hash_mask, ukeys, nuniq, nwin, max_nnz, h->held, stamp,
                  h->tk[e], pf, h->cnt, h->cnt_part, h->cnt_part + PART_COPIES * PART_WORDS,
-                 h->ring[k % h->nring].scal, h->h_cnt_dev, *seq_out, h->ws_plan, h->s_plan);
+                 h->ring[k % h->nring].scal, h->h_cnt_dev, *seq_out, host_keys, h->stage_rows,
+                 h->ws_plan, h->s_plan);
     CHECK_LAUNCH(h);
+    if (host_keys) HIPCHK(h, hipEventRecord(h->ev_mkey[sl], h->s_plan));  // the keys are complete
     if (h->ws_plan.overflow) return fail(h, SP_ERR_HIP, "internal: scan workspace too small");
     if (timing) HIPCHK(h, h->t_qry.end(h->s_plan));
     *stamp_out = stamp;
@@ -1509,12 +1553,15 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     if (h->staged && n_miss > 0) {
         // the staged fill gathers on the host as soon as it has the missing
         // keys, while the victims are chosen: they go first.  Their pinned
-        // slot was last read by the fill of plan k - NSTAGE.
-        const int sl = (int)(k % NSTAGE);
-        TRY(join_fill(h, k - NSTAGE));
-        HIPCHK(h, hipMemcpyAsync(h->h_mkey[sl], tk.m_key, sizeof(uint32_t) * n_miss,
-                                 hipMemcpyDeviceToHost, h->s_plan));
-        HIPCHK(h, hipEventRecord(h->ev_mkey[sl], h->s_plan));
+        // slot was last read by the fill of plan k - nstage.  ev_mkey marks
+        // them complete.
+        const int sl = (int)(k % h->nstage);
+        if (pf_on) {  // (without prefetch the query wrote them there itself)
+            TRY(join_fill(h, k - h->nstage));
+            HIPCHK(h, hipMemcpyAsync(h->h_mkey[sl], tk.m_key, sizeof(uint32_t) * n_miss,
+                                     hipMemcpyDeviceToHost, h->s_plan));
+            HIPCHK(h, hipEventRecord(h->ev_mkey[sl], h->s_plan));
+        }
         // the gather reads the host tables: the write-backs due land first
         TRY(join_writebacks(h, k));
         MoveJob gj;
@@ -1583,15 +1630,12 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     // behind this call's ingests (its fill has normally finished by now): it
     // then overlaps this plan's fill (the two use the host link in opposite
     // directions) and is well under way when the next call's ingest comes
-    // With the staged fill the batch prepared ahead is ingested here, beside
-    // that copy on the ingest stream: behind a copy that is short next to its
-    // sort, in front of a long one (which would otherwise hold back the next
-    // plan's query, which needs the batch)
-    const int64_t copy_bytes = h->copy_n * (h->D + 1) * (int64_t)sizeof(float);
-    const bool large_copy = h->copy_pending >= 0 && copy_bytes > SMALL_COPY_BYTES;
-    if (h->staged && large_copy && copy_bytes > LONG_COPY_BYTES) TRY(ingest_ahead(h, window, n, nhold, k));
-    if (large_copy) TRY(issue_copy(h, h->s_ingest));
-    if (h->staged) TRY(ingest_ahead(h, window, n, nhold, k));  // (nothing left if done above)
+    if (h->copy_pending >= 0 && h->copy_n * (h->D + 1) * (int64_t)sizeof(float) > SMALL_COPY_BYTES)
+        TRY(issue_copy(h, h->s_ingest));
+    // With the staged fill the batches prepared ahead are ingested here, behind
+    // that copy on the ingest stream (the next plan's query needs only the
+    // batches of its window, ingested by earlier plans).
+    if (h->staged) TRY(ingest_ahead(h, window, n, nhold, k));
     double tF = host_ms();
     h->host_ms[3] += tF - tE;
     // ---- the next plan's query, when its whole window is known: batches
@@ -1607,7 +1651,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     // ---- mover (own stream): write-back of evicted rows and fill of misses;
     // the next plan's query does not wait for it
     if (!h->staged) TRY(join_writebacks(h, k));  // the staged fill joined before its gather
-    const int sl = (int)(k % NSTAGE);
+    const int sl = (int)(k % h->nstage);
     MoveJob mj;
     mj.k = k;
     mj.n = n_miss;
@@ -1615,9 +1659,9 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     mj.e = e;
     mj.u = u;
     mj.timing = timing;
-    // the device staging slot is free once plan k - NSTAGE's copy has run
+    // the device staging slot is free once plan k - nstage's copy has run
     // (issued two plans ago)
-    if (k >= NSTAGE && hipEventQuery(h->ev_d2h[sl]) != hipSuccess) {
+    if (k >= h->nstage && hipEventQuery(h->ev_d2h[sl]) != hipSuccess) {
         (void)hipGetLastError();
         mj.wait[mj.nwait++].ev = h->ev_d2h[sl];
     }

@@ -75,7 +75,7 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
                                                  int32_t *part, int32_t *arrived,
                                                  const int32_t *scal0, uint64_t *host_mapped,
                                                  uint32_t seq, uint32_t *m_key, int32_t *m_uidx,
-                                                 ScanDev d)
+                                                 uint32_t *host_keys, int64_t host_cap, ScanDev d)
 {
     __shared__ int32_t c_miss[MAX_TABLES], c_held[MAX_TABLES], c_pf[MAX_TABLES];  // c_pf: row w's
     __shared__ int32_t last_s;
@@ -135,6 +135,8 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
             int32_t *const mu = pf.depth > 0 ? pf.own_uidx : m_uidx;
             mk[pref_s + ex] = key;
             mu[pref_s + ex] = (int32_t)i;
+            // the staged fill's host threads read the misses from pinned memory
+            if (host_keys && pref_s + ex < (uint64_t)host_cap) host_keys[pref_s + ex] = key;
         }
     }
     uint64_t todo = __ballot(valid);
@@ -208,7 +210,8 @@ void launch_query(const Tables &tb, const uint64_t *hash, uint32_t mask,
                   const uint32_t *const *ukeys, const int32_t *const *nuniq, int nwin,
                   int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk, PrefetchDev pf,
                   DevCounters *cnt, int32_t *part, int32_t *arrived, const int32_t *scal0,
-                  uint64_t *host_mapped, uint32_t seq, ScanWs &ws, hipStream_t s)
+                  uint64_t *host_mapped, uint32_t seq, uint32_t *host_keys, int64_t host_cap,
+                  ScanWs &ws, hipStream_t s)
 {
     if (pf.depth > nwin - 1 || pf.depth > MAX_PF) {  // the caller limits it to the window
         ws.overflow = true;
@@ -231,7 +234,7 @@ void launch_query(const Tables &tb, const uint64_t *hash, uint32_t mask,
     ws.issued += (uint32_t)gx;  // the planned batch's row of blocks takes tiles
     hipLaunchKernelGGL(k_query, dim3((unsigned)gx, nwin), dim3(BLOCK), 0, s, tb.row_bits, tb.T,
                        hash, mask, pa, pf, held, stamp, tk.hit, tk.slot_u, cnt, part, arrived, scal0,
-                       host_mapped, seq, tk.m_key, tk.m_uidx, d);
+                       host_mapped, seq, tk.m_key, tk.m_uidx, host_keys, host_cap, d);
 }
 
 // ---------------------------------------------------------------- hash rebuild

@@ -188,7 +188,9 @@ RadixPlan radix_plan(int64_t n, int bits);
 // k_plan.hip
 // The query: hold marks, hits, the misses in ascending key order (tk.m_key,
 // tk.m_uidx) and per-table counts of one plan, published to host_mapped
-// (word i = seq << 32 | counter word i) by the last block.
+// (word i = seq << 32 | counter word i) by the last block.  Without prefetch,
+// host_keys (device-visible pinned memory, or null) also gets the first
+// host_cap missing keys, complete once the kernel is.
 // Prefetch mode (depth d >= 1): the query compacts the planned batch's own
 // misses into own_key / own_uidx and flags (flag[(w-1) * stride + j] = 1) the
 // unique keys j of successor w = 1..d to prefetch; the arrangement then
@@ -204,7 +206,8 @@ void launch_query(const Tables &tb, const uint64_t *hash, uint32_t mask,
                   const uint32_t *const *ukeys, const int32_t *const *nuniq, int nwin,
                   int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk, PrefetchDev pf,
                   DevCounters *cnt, int32_t *part, int32_t *arrived, const int32_t *scal0,
-                  uint64_t *host_mapped, uint32_t seq, ScanWs &ws, hipStream_t s);
+                  uint64_t *host_mapped, uint32_t seq, uint32_t *host_keys, int64_t host_cap,
+                  ScanWs &ws, hipStream_t s);
 
 void launch_hash_rebuild(uint64_t *hash, uint32_t mask, const int32_t *key_of_slot, int64_t nslots,
                          DevCounters *cnt, hipStream_t s);

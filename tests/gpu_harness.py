@@ -5,7 +5,7 @@ import numpy as np
 
 from oracle import oracle
 from paper_2205_04702_amd import workload as wl
-from paper_2205_04702_amd.scratchpipe import ScratchPipe, host_tables
+from paper_2205_04702_amd.scratchpipe import SP_MAX_AHEAD, ScratchPipe, host_tables
 
 PLAN_FIELDS = ("u_table", "u_row", "inv", "hit", "m_table", "m_row", "v_slot", "v_old_row",
                "v_old_use", "slot_u", "slot_of")
@@ -192,8 +192,8 @@ def row_values(t, rows, dim):
 def run_sampled_parity(w, steps, *, check_plan_steps, check_fwd_steps, say=print, policy="lru",
                        hold_past=0, seed=0, max_table_ids="auto", prefetch=False, fill="mapped",
                        host_ids=False):
-    """A full-size workload driven as the benchmark drives it (the two batches after the
-    window handed over early; IDs in device memory, or host memory with host_ids) for
+    """A full-size workload driven as the benchmark drives it (the SP_MAX_AHEAD batches
+    after the window handed over early; IDs in device memory, or host memory with host_ids) for
     `steps` steps.
 
     Only rows that the trained batches read are initialised (plus sentinel rows elsewhere);
@@ -206,7 +206,7 @@ def run_sampled_parity(w, steps, *, check_plan_steps, check_fwd_steps, say=print
     dev = torch.device("cuda:0")
     T, B, D, L = w.tables, w.batch, w.dim, w.lookahead
     t0 = time.perf_counter()
-    ahead = 2
+    ahead = SP_MAX_AHEAD
     batches = [wl.batch(w, s) for s in range(steps + L + ahead)]
     rows = touched_rows(w, batches, steps)
     say(f"  inputs {time.perf_counter() - t0:.1f}s, touched rows {sum(r.size for r in rows)}")

@@ -18,5 +18,18 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def build_sanitized(out_dir: str, verbose: bool = False) -> str:
+    """The oracle with AddressSanitizer and UndefinedBehaviorSanitizer (clang, whose
+    runtime the library's sanitizer build shares; without OpenMP, so sequential)."""
+    out = os.path.join(out_dir, "liboracle_asan.so")
+    cmd = ["/opt/rocm/llvm/bin/clang", "-O1", "-g", "-std=c11", "-fPIC", "-shared",
+           "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+           "-fno-omit-frame-pointer", "-shared-libasan", "-o", out, SRC]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    return out
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))

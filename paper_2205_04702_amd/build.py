@@ -47,5 +47,32 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def build_sanitized_host(out_dir: str, verbose: bool = False) -> str:
+    """The library with its host code built with AddressSanitizer and
+    UndefinedBehaviorSanitizer (device code as usual), for running the CPU tests
+    under the sanitizers; returns the path of the shared library."""
+    objs = []
+    flags = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+             "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host",
+             "-fno-omit-frame-pointer", "-g"]
+    for src in SOURCES:
+        out = os.path.join(out_dir, os.path.splitext(src)[0] + ".asan.o")
+        cmd = [HIPCC, *COMMON, *flags, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", out]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"sanitized compile of {src} failed:\n{r.stderr}")
+        objs.append(out)
+    lib = os.path.join(out_dir, "libscratchpipe_asan.so")
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-shared-libasan",
+           "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+           "-o", lib, *objs, "-lpthread"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    return lib
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))

@@ -298,3 +298,41 @@ def test_timing_can_be_sampled_per_step(harness):
         spm.sp_set_flags(0, 0)
     for x, y in zip(*results):
         assert np.array_equal(x, y)
+
+
+@pytest.mark.parametrize("fill", ["mapped", "staged"])
+def test_allocation_failure_is_reported_and_cleaned_up(harness, fill, monkeypatch):
+    """SP_FAIL_ALLOC_AFTER=n makes the allocation after the first n of sp_create fail:
+    every such failure must come back as SP_ERR_OOM (no context, nothing leaked: the
+    same create then succeeds), whichever allocation it hits."""
+    import ctypes as C
+    w = wl.custom(rows=[2000, 3000], dim=16, batch=16, pooling=2, slots=[200, 300],
+                  lookahead=2, steps=4, seed=5)
+    host = harness.fresh_host(w, fill)
+    L = spm.load()
+    rows = (C.c_int64 * 2)(*w.rows)
+    slots = (C.c_int64 * 2)(*w.slots)
+    tabs = (C.c_void_p * 2)(*host.ptrs)
+    cfg = spm.sp_config(num_tables=2, rows=rows, dim=16, slots=slots, lookahead=2,
+                        host_tables=tabs, max_batch=16, max_ids=64, flags=0, device=0,
+                        fill=spm.FILLS[fill])
+    try:
+        failures = 0
+        for n in (0, 1, 7, 30, 60, 90, 10_000):
+            monkeypatch.setenv("SP_FAIL_ALLOC_AFTER", str(n))
+            h = C.c_void_p()
+            st = L.sp_create(C.byref(cfg), C.byref(h))
+            if st == spm.SP_OK:  # n above the allocations the create makes
+                assert h.value
+                L.sp_destroy(h)
+                continue
+            failures += 1
+            assert st == spm.SP_ERR_OOM and not h.value
+            assert "injected" in spm.sp_last_error(None)
+        assert failures >= 5
+        monkeypatch.delenv("SP_FAIL_ALLOC_AFTER")
+        ctx = spm.ScratchPipe(w.rows, w.dim, w.slots, w.lookahead, host, max_batch=16,
+                              max_ids=64, fill=fill)
+        ctx.close()
+    finally:
+        host.close()

@@ -72,3 +72,39 @@ def test_zipf_8x1M_sampled(harness, policy):
                                    say=_say, policy=policy, seed=1)
     _say(f"zipf-8x1M {policy}: worst fwd {r['worst_fwd']:.2e} table {r['worst_table']:.2e} "
          f"misses {r['stats']['misses']} evictions {r['stats']['evictions']}")
+
+
+def test_hold_mask_fragment_of_the_paper(harness):
+    """The worked fragment of Sec. IV-D through the C ABI with a past window of three
+    batches: 3010 misses and 7089 hits in the second cycle, nothing is evicted before
+    the fifth cycle, whose miss evicts 2021; plans bit-exact against the oracle."""
+    import numpy as np
+    from tests.test_oracle_holdmask import CYCLES
+    w = wl.custom(rows=[10_000], dim=8, batch=1, pooling=2, slots=[3], lookahead=0, steps=5,
+                  seed=3)
+    _say("case hold-mask fragment, past window 3")
+    r = harness.run_parity(w, list(CYCLES), hold_past=3, max_table_ids=0)
+    assert r["stats"]["evictions"] == 1 and r["stats"]["misses"] == 4
+
+
+def test_hold_mask_fragment_fourth_cycle_miss_is_a_capacity_error(harness):
+    import torch
+    from paper_2205_04702_amd import scratchpipe as spm
+    from tests.test_oracle_holdmask import CYCLES, one_bag
+    w = wl.custom(rows=[10_000], dim=8, batch=1, pooling=2, slots=[3], lookahead=0, steps=5,
+                  seed=3)
+    _say("case hold-mask fragment, fourth-cycle miss")
+    host = harness.fresh_host(w)
+    ctx = spm.ScratchPipe(w.rows, w.dim, w.slots, 0, host, max_batch=1, max_ids=4, hold_past=3)
+    out = torch.zeros((1, w.dim), device="cuda:0")
+    try:
+        for b in CYCLES[:3]:
+            t = ctx.plan([b])
+            ctx.forward(t, out)
+            ctx.backward_update(t, torch.zeros((1, w.dim), device="cuda:0"), 0.01)
+        with pytest.raises(spm.SPError) as e:
+            ctx.plan([one_bag(4444)])
+        assert e.value.status == spm.SP_ERR_CAPACITY
+    finally:
+        ctx.close()
+        host.close()

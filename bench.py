@@ -37,7 +37,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 HOST_LINK_NOMINAL_GBS = 64.0  # PCIe Gen5 x16, per direction
-PINNED_LIMIT_BYTES = 48 << 30  # tables above this use the staged fill by default
+STAGED_ABOVE_BYTES = 8 << 30  # tables above this use the staged fill by default
 
 
 def log(*a):
@@ -125,7 +125,8 @@ def main():
     ap.add_argument("--fill", choices=["auto", "mapped", "staged"], default="auto",
                     help="how missing rows reach HBM: zero-copy from pinned, mapped tables, or "
                          "host gather into pinned staging then copies (auto: staged when the "
-                         "tables exceed 48 GiB)")
+                         "tables exceed 8 GiB; measured faster on 26x4M and the mixed "
+                         "workload, and the only way for tables beyond what one process pins)")
     ap.add_argument("--ids", choices=["host", "hbm"], default="host",
                     help="hand the batch IDs over from host memory (as the method does every "
                          "step) or from device memory")
@@ -141,6 +142,9 @@ def main():
     ap.add_argument("--ahead", type=int, default=-1, metavar="N",
                     help="batches after the hold window handed over early for sorting "
                          "(-1: SP_MAX_AHEAD)")
+    ap.add_argument("--general-ingest", action="store_true",
+                    help="promise no bound on IDs per table, so batches are sorted by the "
+                         "multi-launch path even where one workgroup per table would do")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-timing", action="store_true", help="do not time kernels with events")
@@ -178,7 +182,7 @@ def main():
                                 pooling=w.pooling[:n], dist=w.dist[:n], slots=w.slots[:n])
     table_bytes = sum(w.rows) * w.dim * 4
     fill = args.fill if args.fill != "auto" else (
-        "staged" if table_bytes > PINNED_LIMIT_BYTES else "mapped")
+        "staged" if table_bytes > STAGED_ABOVE_BYTES else "mapped")
     evicts = sum(w.slots) < sum(w.rows)
     if args.fillup >= 0:
         fillup_max = args.fillup
@@ -232,7 +236,7 @@ def main():
     ctx = sp.ScratchPipe(w.rows, w.dim, w.slots, L, host, max_batch=w.batch, max_ids=w.nnz,
                          flags=base_flags, policy=args.policy, hold_past=args.hold_past,
                          prefetch=args.prefetch, fill=fill,
-                         max_table_ids=w.batch * max(w.pooling))
+                         max_table_ids=0 if args.general_ingest else w.batch * max(w.pooling))
     out = torch.empty((w.tables * w.batch, w.dim), dtype=torch.float32, device=dev)
 
     host_s = [0.0, 0.0, 0.0]  # host time inside plan / forward / backward calls
@@ -349,9 +353,13 @@ def main():
         kern = {}
         for name, key, ms in (("k_forward", "forward", fwd_ms), ("k_backward", "backward", bwd_ms)):
             gbs = kb[key] / (ms * 1e-3) / 1e9
+            tr = traffic_from_profile(name, src_hash, wname)
             kern[name] = {"achieved": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4),
                           "bytes_per_launch": int(kb[key]), "ms_per_launch": round(ms, 5),
-                          "traffic": traffic_from_profile(name, src_hash, wname)}
+                          "traffic": tr}
+            if tr:  # the counted bytes (scaled FETCH_SIZE + WRITE_SIZE) over the same time
+                kern[name]["traffic_GBps"] = round(tr / (ms * 1e-3) / 1e9, 1)
+                kern[name]["traffic_frac"] = round(tr / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
         kern["k_forward"]["requested_GBps"] = round(kb["forward_requested"] / (fwd_ms * 1e-3) / 1e9, 1)
         # the dominant kernel: the one with more time per step
         dom = "k_forward" if fwd_ms >= bwd_ms else "k_backward"

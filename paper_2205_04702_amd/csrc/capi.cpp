@@ -972,9 +972,10 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     {
         // scans: victims (tables x slots per table), misses and batches (N),
         // radix histogram tables (at most N + 2048 entries)
-        // (and the query's tiles of unique keys)
+        // (and the query's tiles of unique keys, and the LDS ingest's workgroups)
         const int64_t tiles = std::max({scan_tiles(T, h->maxS), scan_tiles(1, NM + 4096),
-                                        (N + QUERY_TILE - 1) / QUERY_TILE}) + 2;
+                                        (N + QUERY_TILE - 1) / QUERY_TILE,
+                                        (int64_t)T * ingest_splits(T)}) + 2;
         for (ScanWs *ws : {&h->ws_plan, &h->ws_ingest}) {
             ws->max_tiles = tiles;
             TRY(dalloc(h, &ws->status, LB_WORDS * tiles));
@@ -1222,7 +1223,7 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
     if (bt.nnz > 0 && ingest_in_lds(h->max_table_ids, bt.batch)) {
         // one launch; it reports when it has read its inputs, which matters
         // only for the caller's device arrays
-        h->cons_issued += (uint32_t)h->T;
+        h->cons_issued += (uint32_t)(h->T * ingest_splits(h->T));
         ic.target = h->cons_issued;
         ic.seq = ++h->cons_seq;
         if (bt.on_device) h->wait_cons_word = true;

@@ -399,28 +399,35 @@ struct ChunkOut {
     }
 };
 
-// ---------------------------------------------------------------- whole tables in LDS
+// ---------------------------------------------------------------- tables in LDS, split by rows
 //
 // When every table of a batch has at most IG_MAX IDs and the batch at most
-// IG_MAX bags per table, one launch does all of the above: one block per
-// table (blocks take tables in the order they start, from an atomic counter)
-// validates the table's offsets and IDs, sorts its entries (row << 26 | bag
-// << 13 | position, positions and bags local to the table) by row in LDS,
-// finds the runs of equal rows and their backward chunks, then publishes its
-// unique-key, chunk and long-run counts and its error bits (epoch-tagged, as
-// the single-pass scan does).  It adds up the counts of the tables before it,
-// which have all started, to place its outputs; the last table's block also
-// writes the batch totals.  The global order is the same as the general
-// path's: keys are table-major, so table t's sorted positions are its own
-// span of the batch.  Once a block has read all of its inputs it counts
-// itself in *cons; the block that completes the count (cons_target) writes
-// cons_seq to the host-coherent word cons_word, which tells the host that the
-// caller's arrays are no longer needed, long before the kernel ends.
+// IG_MAX bags per table, one launch does all of the above.  Each table is
+// handled by S workgroups, each owning one contiguous range of its rows
+// (workgroups take (table, range) pairs in the order they start, from an
+// atomic counter).  A workgroup reads the table's offsets and IDs, keeps the
+// entries whose row falls in its range in position order (entry = row offset
+// << 26 | bag << 13 | position, positions and bags local to the table), sorts
+// them by row in LDS, finds the runs of equal rows and their backward chunks,
+// then publishes its entry, unique-key, chunk and long-run counts and its
+// error bits (epoch-tagged, as the single-pass scan does).  It adds up the
+// counts of every workgroup that started before it to place its outputs.
+// Keys are table-major and the ranges ascend, so this is the order of the
+// general path: a workgroup's sorted entries follow those of the ranges
+// before it within the table's span of the batch.  Once a workgroup has read
+// all of its inputs it counts itself in *cons; the one that completes the
+// count (cons_target) writes cons_seq to the host-coherent word cons_word,
+// which tells the host that the caller's arrays are no longer needed, long
+// before the kernel ends.  A workgroup can hold a whole table, so any
+// distribution of rows over the ranges is handled; an even one spreads the
+// sort over S compute units.
 constexpr int IG_THREADS = 1024;
 constexpr int IG_WAVES = IG_THREADS / WAVE;
 constexpr int IG_ITEMS = 8;
 constexpr int IG_SHIFT_BAG = 13, IG_SHIFT_ROW = 26;
+constexpr uint32_t IG_LOW = (1u << IG_SHIFT_BAG) - 1u;
 static_assert(IG_THREADS * IG_ITEMS == IG_MAX, "one item per thread per round");
+static_assert(MAX_TABLES * IG_SPLIT_MAX <= IG_THREADS, "one earlier workgroup per thread");
 
 __global__ void __launch_bounds__(IG_THREADS) k_ingest_table(Tables tb, const int32_t *ids,
                                                              const int32_t *bag_off,
@@ -428,24 +435,25 @@ __global__ void __launch_bounds__(IG_THREADS) k_ingest_table(Tables tb, const in
                                                              int64_t nnz, int32_t chunk,
                                                              int64_t max_table_ids, BatchDev b,
                                                              int64_t cap_u, int64_t cap_c,
-                                                             ScanDev d, uint32_t *cons,
+                                                             ScanDev d, int32_t S, uint32_t *cons,
                                                              uint32_t cons_target,
                                                              uint64_t *cons_word, uint32_t cons_seq)
 {
     __shared__ uint64_t buf[2][IG_MAX];
     __shared__ uint32_t wc[IG_WAVES][256];
     __shared__ uint32_t lds[IG_WAVES];
-    __shared__ uint32_t id_s, multi_s;
+    __shared__ uint32_t id_s, multi_s, m_s;
     __shared__ int32_t err_s;
-    __shared__ uint32_t before_s[4];
-    const int tid = threadIdx.x;
+    __shared__ uint32_t before_s[5];
+    const int tid = threadIdx.x, w = wave_id(), lane = lane_id();
     if (tid == 0) {
         id_s = atomicAdd(d.counter, 1u) - d.base;
         multi_s = 0;
         err_s = 0;
     }
     __syncthreads();
-    const int t = (int)id_s;
+    const uint32_t id = id_s;
+    const int t = (int)(id / (uint32_t)S), sub = (int)(id % (uint32_t)S);
     auto inputs_read = [&]() {  // thread 0, after every read of ids and bag_off
         if (atomicAdd(cons, 1u) + 1u == cons_target)
             __hip_atomic_store(cons_word, (uint64_t)cons_seq, __ATOMIC_RELAXED,
@@ -459,58 +467,105 @@ __global__ void __launch_bounds__(IG_THREADS) k_ingest_table(Tables tb, const in
         return;
     }
     const int64_t nbags = (int64_t)tb.T * B;
-    // ---- offsets of the table's bags: validate, copy into the ring
-    int32_t err = 0;
+    // ---- the table's span of the batch, then its IDs and offsets, all loads
+    // in flight together
+    int64_t j0 = bag_off[(int64_t)t * B], j1 = bag_off[(int64_t)(t + 1) * B];
+    j0 = j0 < 0 ? 0 : (j0 > nnz ? nnz : j0);
+    j1 = j1 < j0 ? j0 : (j1 > nnz ? nnz : j1);
+    const int n = (int)(j1 - j0 < IG_MAX ? j1 - j0 : IG_MAX);
+    // a table past the configured bound: the rest is left out and the plan fails
+    int32_t err = j1 - j0 > max_table_ids ? ERR_TABLE_IDS : 0;
+    int32_t rv[IG_ITEMS];
+#pragma unroll
+    for (int r = 0; r < IG_ITEMS; ++r) {
+        const int i = r * IG_THREADS + tid;
+        rv[r] = n > 0 ? ids[j0 + (i < n ? i : n - 1)] : 0;
+    }
+    // offsets: validate, mark the bag of every position; the first range's
+    // workgroup copies them into the ring
+    uint32_t *bag_at = reinterpret_cast<uint32_t *>(buf[1]);
     for (int lb = tid; lb < B; lb += IG_THREADS) {
         const int64_t g = (int64_t)t * B + lb;
         const int64_t lo = bag_off[g], hi = bag_off[g + 1];
-        if (bag_off_copy != bag_off) {
+        if (sub == 0 && bag_off_copy != bag_off) {
             bag_off_copy[g] = (int32_t)lo;
             if (g == nbags - 1) bag_off_copy[g + 1] = (int32_t)hi;
         }
         if (lo > hi || lo < 0 || hi > nnz || (g == 0 && lo != 0) || (g == nbags - 1 && hi != nnz))
             err |= ERR_OFFSETS;
+        const int64_t a = lo - j0 < 0 ? 0 : lo - j0, e = hi - j0 > n ? n : hi - j0;
+        for (int64_t i = a; i < e; ++i) bag_at[i] = (uint32_t)lb;
     }
-    int64_t j0 = bag_off[(int64_t)t * B], j1 = bag_off[(int64_t)(t + 1) * B];
-    j0 = j0 < 0 ? 0 : (j0 > nnz ? nnz : j0);
-    j1 = j1 < j0 ? j0 : (j1 > nnz ? nnz : j1);
-    int n = (int)(j1 - j0 < IG_MAX ? j1 - j0 : IG_MAX);
-    if (j1 - j0 > max_table_ids) err |= ERR_TABLE_IDS;  // the rest is left out; the plan fails
-    // ---- entries by position, then each bag marks its positions
-    const int rb = tb.row_bits;
-    for (int i = tid; i < n; i += IG_THREADS) {
-        int32_t row = ids[j0 + i];
-        if (row < 0 || (int64_t)row >= tb.rows[t]) {
+    // this workgroup's rows
+    const int64_t rows_t = tb.rows[t];
+    const int64_t span = (rows_t + S - 1) / S;
+    const int64_t r0 = (int64_t)sub * span;
+    const int64_t r1 = r0 + span < rows_t ? r0 + span : rows_t;
+    int rbits = 0;
+    while ((int64_t)1 << rbits < span) ++rbits;
+    __syncthreads();
+    // ---- keep the entries of this range, in position order: per round r the
+    // waves' counts are laid out (r, wave) and scanned by wave 0
+    const uint64_t lt = lanemask_lt();
+    uint32_t kept = 0, rank[IG_ITEMS];
+    uint32_t *cnt = &wc[0][0];
+#pragma unroll
+    for (int r = 0; r < IG_ITEMS; ++r) {
+        const int i = r * IG_THREADS + tid;
+        int32_t row = rv[r];
+        if (i < n && (row < 0 || (int64_t)row >= rows_t)) {
             err |= ERR_ID_RANGE;
             row = 0;
         }
-        buf[0][i] = ((uint64_t)(uint32_t)row << IG_SHIFT_ROW) | (uint64_t)i;
-    }
-    __syncthreads();
-    for (int lb = tid; lb < B; lb += IG_THREADS) {
-        const int64_t g = (int64_t)t * B + lb;
-        int64_t lo = bag_off[g] - j0, hi = bag_off[g + 1] - j0;
-        lo = lo < 0 ? 0 : lo;
-        hi = hi > n ? n : hi;
-        for (int64_t i = lo; i < hi; ++i) buf[0][i] |= (uint64_t)lb << IG_SHIFT_BAG;
+        rv[r] = row;
+        const bool keep = i < n && row >= r0 && row < r1;
+        const uint64_t bal = __ballot(keep);
+        kept |= (uint32_t)keep << r;
+        rank[r] = (uint32_t)__popcll(bal & lt);
+        if (lane == 0) cnt[r * IG_WAVES + w] = (uint32_t)__popcll(bal);
     }
     if (err) atomicOr(&err_s, err);
     __syncthreads();
     if (tid == 0) inputs_read();
-    uint64_t *srt = lds_radix_sort<IG_THREADS, IG_ITEMS>(buf[0], buf[1], n, IG_SHIFT_ROW, rb, wc, lds);
+    if (w == 0) {
+        static_assert(IG_ITEMS * IG_WAVES == 2 * WAVE, "two counts per lane");
+        const uint32_t c0 = cnt[2 * lane], c1 = cnt[2 * lane + 1];
+        const uint32_t incl = wave_incl_scan(c0 + c1);
+        cnt[2 * lane] = incl - c0 - c1;
+        cnt[2 * lane + 1] = incl - c1;
+        if (lane == WAVE - 1) m_s = incl;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < IG_ITEMS; ++r) {
+        if ((kept >> r) & 1u) {
+            const int i = r * IG_THREADS + tid;
+            uint32_t bag = bag_at[i];
+            bag = bag < (uint32_t)B ? bag : 0u;  // positions no bag covers: flagged above
+            buf[0][cnt[r * IG_WAVES + w] + rank[r]] =
+                ((uint64_t)(rv[r] - r0) << IG_SHIFT_ROW) | ((uint64_t)bag << IG_SHIFT_BAG) |
+                (uint64_t)i;
+        }
+    }
+    const int m = (int)m_s;
+    __syncthreads();
+    uint64_t *srt = lds_radix_sort<IG_THREADS, IG_ITEMS>(buf[0], buf[1], m, IG_SHIFT_ROW, rbits,
+                                                         wc, lds);
     // the other buffer holds each run's first sorted index and its first chunk
     uint32_t *run0 = reinterpret_cast<uint32_t *>(srt == buf[0] ? buf[1] : buf[0]);
     uint32_t *chunk0 = run0 + IG_MAX;
 
-    // ---- runs of equal rows (blocked: thread tid owns items tid*8 .. tid*8+7)
-    const int i0 = tid * IG_ITEMS;
+    // ---- runs of equal rows (blocked: thread tid owns items tid*K .. tid*K+K-1)
+    const int K = (m + IG_THREADS - 1) / IG_THREADS;
+    const int i0 = tid * K;
     uint32_t heads = 0;
     uint64_t e[IG_ITEMS];
 #pragma unroll
     for (int q = 0; q < IG_ITEMS; ++q) {
         const int i = i0 + q;
-        e[q] = i < n ? srt[i] : 0ull;
-        const bool h = i < n && (i == 0 || (srt[i - 1] >> IG_SHIFT_ROW) != (e[q] >> IG_SHIFT_ROW));
+        const bool in = q < K && i < m;
+        e[q] = in ? srt[i] : 0ull;
+        const bool h = in && (i == 0 || (srt[i - 1] >> IG_SHIFT_ROW) != (e[q] >> IG_SHIFT_ROW));
         heads |= (uint32_t)h << q;
     }
     uint32_t nU;
@@ -522,14 +577,14 @@ __global__ void __launch_bounds__(IG_THREADS) k_ingest_table(Tables tb, const in
             if ((heads >> q) & 1u) run0[sg++] = (uint32_t)(i0 + q);
     }
     __syncthreads();
-    // chunks per run (blocked over runs)
+    // chunks per run (blocked over runs the same way)
     uint32_t nch[IG_ITEMS], csum = 0, msum = 0;
 #pragma unroll
     for (int q = 0; q < IG_ITEMS; ++q) {
         const uint32_t sr = (uint32_t)(i0 + q);
         nch[q] = 0;
-        if (sr < nU) {
-            const uint32_t len = (sr + 1 < nU ? run0[sr + 1] : (uint32_t)n) - run0[sr];
+        if (q < K && sr < nU) {
+            const uint32_t len = (sr + 1 < nU ? run0[sr + 1] : (uint32_t)m) - run0[sr];
             nch[q] = (len + (uint32_t)chunk - 1) / (uint32_t)chunk;
             csum += nch[q];
             msum += nch[q] > 1;
@@ -542,59 +597,68 @@ __global__ void __launch_bounds__(IG_THREADS) k_ingest_table(Tables tb, const in
 #pragma unroll
     for (int q = 0; q < IG_ITEMS; ++q) {
         const uint32_t sr = (uint32_t)(i0 + q);
-        if (sr < nU) chunk0[sr] = cb;
+        if (q < K && sr < nU) chunk0[sr] = cb;
         cb += nch[q];
     }
 
-    // ---- publish this table's counts, add up those of the tables before it
-    uint64_t *st = d.status + (int64_t)t * LB_WORDS;
+    // ---- publish this workgroup's counts, add up those of every earlier one
+    uint64_t *st = d.status + (int64_t)id * LB_WORDS;
     if (tid == 0) {
-        const uint32_t mine[4] = {nU, nC, nM, (uint32_t)err_s};
+        const uint32_t mine[4] = {nU, nC, nM, (uint32_t)err_s << 16 | (uint32_t)m};
 #pragma unroll
         for (int c = 0; c < 4; ++c) lb_publish<uint32_t>(st + c, d.epoch, mine[c]);
     }
-    if (tid < WAVE) {
-        uint32_t v[4] = {0, 0, 0, 0};
-        if (tid < t) {  // T <= 64: one lane per earlier table
-            const uint64_t *w = d.status + (int64_t)tid * LB_WORDS;
-            int spins = 0;
-            bool ok = false;
-            while (!ok) {
-                ok = true;
+    uint32_t v[4] = {0, 0, 0, 0};
+    if (tid < (int)id) {  // one thread per earlier workgroup
+        const uint64_t *wd = d.status + (int64_t)tid * LB_WORDS;
+        int spins = 0;
+        bool ok = false;
+        while (!ok) {
+            ok = true;
 #pragma unroll
-                for (int c = 0; c < 4; ++c) ok = lb_read<uint32_t>(w + c, d.epoch, v[c]) && ok;
-                if (!ok && ++spins > LB_SPIN) {  // counted as zero; result flagged wrong
-                    atomicOr(d.err, ERR_PLAN);
-                    v[0] = v[1] = v[2] = v[3] = 0;
-                    break;
-                }
-                if (!ok) __builtin_amdgcn_s_sleep(1);
+            for (int c = 0; c < 4; ++c) ok = lb_read<uint32_t>(wd + c, d.epoch, v[c]) && ok;
+            if (!ok && ++spins > LB_SPIN) {  // counted as zero; result flagged wrong
+                atomicOr(d.err, ERR_PLAN);
+                v[0] = v[1] = v[2] = v[3] = 0;
+                break;
             }
-        }
-        const uint32_t u0 = wave_sum(v[0]), c0 = wave_sum(v[1]), m0 = wave_sum(v[2]);
-        uint32_t eo = v[3];
-#pragma unroll
-        for (int o = WAVE / 2; o > 0; o >>= 1) eo |= __shfl_xor(eo, o, WAVE);
-        if (tid == 0) {
-            before_s[0] = u0;
-            before_s[1] = c0;
-            before_s[2] = m0;
-            before_s[3] = eo;
+            if (!ok) __builtin_amdgcn_s_sleep(1);
         }
     }
-    __syncthreads();
+    {
+        // entries before this range within the table; error bits of them all
+        const uint32_t ent = tid >= t * S ? (v[3] & 0xFFFFu) : 0u;
+        uint32_t eo = v[3] >> 16;
+#pragma unroll
+        for (int o = WAVE / 2; o > 0; o >>= 1) eo |= __shfl_xor(eo, o, WAVE);
+        const uint32_t part[5] = {wave_sum(v[0]), wave_sum(v[1]), wave_sum(v[2]), eo,
+                                  wave_sum(ent)};
+        if (lane == 0)
+#pragma unroll
+            for (int c = 0; c < 5; ++c) wc[c][w] = part[c];
+        __syncthreads();
+        if (tid < 5) {
+            uint32_t acc = 0;
+            for (int q = 0; q < IG_WAVES; ++q) acc = tid == 3 ? (acc | wc[tid][q]) : acc + wc[tid][q];
+            before_s[tid] = acc;
+        }
+        __syncthreads();
+    }
     const uint32_t U0 = before_s[0], C0 = before_s[1], M0 = before_s[2];
+    const int64_t jb = j0 + (int64_t)before_s[4];  // this range's first sorted position
+    const int rb = tb.row_bits;
+    const int64_t n_multi = multi_capacity(cap_u, chunk);
 
     // ---- outputs: positions
     uint32_t sg = seg_first;
 #pragma unroll
     for (int q = 0; q < IG_ITEMS; ++q) {
         const int i = i0 + q;
-        if (i >= n) break;
-        const uint32_t row = (uint32_t)(e[q] >> IG_SHIFT_ROW);
-        const int32_t bag = (int32_t)((e[q] >> IG_SHIFT_BAG) & ((1u << (IG_SHIFT_ROW - IG_SHIFT_BAG)) - 1u));
-        const int64_t pos = j0 + (int64_t)(e[q] & ((1u << IG_SHIFT_BAG) - 1u));
-        const int64_t gi = j0 + i;
+        if (q >= K || i >= m) break;
+        const uint32_t row = (uint32_t)((e[q] >> IG_SHIFT_ROW) + (uint64_t)r0);
+        const int32_t bag = (int32_t)((e[q] >> IG_SHIFT_BAG) & IG_LOW);
+        const int64_t pos = j0 + (int64_t)(e[q] & IG_LOW);
+        const int64_t gi = jb + i;
         if ((heads >> q) & 1u) {
             if ((int64_t)U0 + sg < cap_u) {
                 b.ukeys[U0 + sg] = ((uint32_t)t << rb) | row;
@@ -610,24 +674,24 @@ __global__ void __launch_bounds__(IG_THREADS) k_ingest_table(Tables tb, const in
 #pragma unroll
     for (int q = 0; q < IG_ITEMS; ++q) {
         const uint32_t sr = (uint32_t)(i0 + q);
-        if (sr >= nU) break;
+        if (q >= K || sr >= nU) break;
         const int64_t gs = (int64_t)U0 + sr;
         const int64_t c0 = (int64_t)C0 + chunk0[sr];
         if (gs >= cap_u) break;
         b.seg_chunk0[gs] = (int32_t)c0;
-        const int32_t s0 = (int32_t)(j0 + run0[sr]);
-        const int32_t s1 = (int32_t)(j0 + (sr + 1 < nU ? run0[sr + 1] : (uint32_t)n));
+        const int32_t s0 = (int32_t)(jb + run0[sr]);
+        const int32_t s1 = (int32_t)(jb + (sr + 1 < nU ? run0[sr + 1] : (uint32_t)m));
         for (uint32_t c = 0; c < nch[q] && c0 + c < cap_c; ++c) {
             const int32_t p0 = s0 + (int32_t)c * chunk;
             b.chunk_desc[c0 + c] = make_int4(p0, p0 + chunk < s1 ? p0 + chunk : s1, (int32_t)gs,
                                              (int32_t)nch[q]);
         }
         if (nch[q] > 1) {
-            const uint32_t m = M0 + atomicAdd(&multi_s, 1u);  // list order is irrelevant
-            if ((int64_t)m < multi_capacity(cap_u, chunk)) b.multi[m] = (int32_t)gs;
+            const uint32_t mi = M0 + atomicAdd(&multi_s, 1u);  // list order is irrelevant
+            if ((int64_t)mi < n_multi) b.multi[mi] = (int32_t)gs;
         }
     }
-    if (t == tb.T - 1 && tid == 0) {  // the batch totals
+    if (id == (uint32_t)(tb.T * S - 1) && tid == 0) {  // the batch totals
         const uint32_t U = U0 + nU;
         if ((int64_t)U < cap_u + 1) b.seg_off[U] = (int32_t)nnz;
         b.scal[0] = (int32_t)U;
@@ -649,7 +713,9 @@ void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, cons
 {
     const int64_t nbags = (int64_t)tb.T * B;
     if (nnz > 0 && ingest_in_lds(max_table_ids, B)) {
-        if (tb.T > ws.max_tiles) {
+        const int S = ingest_splits(tb.T);
+        const int64_t grid = (int64_t)tb.T * S;
+        if (grid > ws.max_tiles) {
             ws.overflow = true;
             return;
         }
@@ -657,11 +723,11 @@ void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, cons
             (void)hipMemsetAsync(ws.status, 0, sizeof(uint64_t) * LB_WORDS * ws.max_tiles, s);
             ws.epoch = 0;
         }
-        ScanDev d{ws.status, ws.counter, ws.err, ws.issued, ++ws.epoch, (uint32_t)tb.T, 1};
-        ws.issued += (uint32_t)tb.T;
-        hipLaunchKernelGGL(k_ingest_table, dim3((unsigned)tb.T), dim3(IG_THREADS), 0, s, tb, ids,
+        ScanDev d{ws.status, ws.counter, ws.err, ws.issued, ++ws.epoch, (uint32_t)grid, 1};
+        ws.issued += (uint32_t)grid;
+        hipLaunchKernelGGL(k_ingest_table, dim3((unsigned)grid), dim3(IG_THREADS), 0, s, tb, ids,
                            bag_off, b.bag_off, B, nnz, chunk, max_table_ids, b, cap_u, cap_c, d,
-                           ic.counter, ic.target, ic.word, ic.seq);
+                           S, ic.counter, ic.target, ic.word, ic.seq);
         return;
     }
     launch_zero_i32(b.scal, 4, s);

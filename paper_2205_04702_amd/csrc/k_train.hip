@@ -255,6 +255,9 @@ __global__ void __launch_bounds__(BLOCK) k_bwd_combine(float4 *__restrict__ stor
 // then occupy few compute units, and the kernels running beside this one
 // keep the rest.  The staged fill only moves rows within HBM and takes a
 // full grid.
+typedef float v4f __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ v4f as_v4f(const float4 *p) { return *reinterpret_cast<const v4f *>(p); }
+
 constexpr int MOVE_MAX_BLOCKS = 64;
 constexpr int MOVE_ROWS = 4;
 
@@ -268,40 +271,63 @@ __global__ void __launch_bounds__(BLOCK) k_move(float4 *__restrict__ storage, Ta
     const int64_t groups = (int64_t)gridDim.x * (BLOCK / LPR);
     const int64_t g = ((int64_t)blockIdx.x * BLOCK + threadIdx.x) / LPR;
     const uint32_t row_mask = (1u << tb.row_bits) - 1u;
+    int32_t *const old_keys = reinterpret_cast<int32_t *>(stage + n * LPR);
     for (int64_t i0 = g; i0 < n; i0 += groups * MOVE_ROWS) {
+        // Straight-line code over the pass's MOVE_ROWS victims, with no branch
+        // around a load: an entry past n reads entry i0's indices, and one
+        // with nothing to read reads row 0 of the scratchpad and drops it.
+        // Each round of loads is then in flight together and the values stay
+        // in registers until the stores.
+        bool in[MOVE_ROWS];
         int32_t old[MOVE_ROWS], v[MOVE_ROWS];
-        const float4 *src[MOVE_ROWS];
+        uint32_t key[MOVE_ROWS];
 #pragma unroll
         for (int q = 0; q < MOVE_ROWS; ++q) {
             const int64_t i = i0 + q * groups;
-            old[q] = -1;
-            v[q] = -1;
-            src[q] = nullptr;
-            if (i < n) {
-                old[q] = tk.v_old_key[i];
-                v[q] = tk.v_slot[i];
-                const uint32_t key = tk.m_key[i];
-                const int tab = (int)(key >> tb.row_bits);
-                const int64_t row = key & row_mask;
-                if (staged) src[q] = staged + i * LPR + c;
-                else if (tab < tb.T && row < tb.rows[tab]) src[q] = hr.p[tab] + row * LPR + c;
-                if ((uint32_t)v[q] >= (uint64_t)nslots) v[q] = -1;
+            in[q] = i < n;
+            const int64_t ic = in[q] ? i : i0;
+            old[q] = tk.v_old_key[ic];
+            v[q] = tk.v_slot[ic];
+            key[q] = tk.m_key[ic];
+        }
+        const float4 *src[MOVE_ROWS];
+        if (staged) {
+#pragma unroll
+            for (int q = 0; q < MOVE_ROWS; ++q) src[q] = staged + (i0 + q * groups) * LPR + c;
+        } else {
+            int tab[MOVE_ROWS];
+            int64_t nrows[MOVE_ROWS];
+            const float4 *base[MOVE_ROWS];
+#pragma unroll
+            for (int q = 0; q < MOVE_ROWS; ++q) {
+                tab[q] = (int)(key[q] >> tb.row_bits);
+                const int tc = tab[q] < tb.T ? tab[q] : 0;
+                nrows[q] = tb.rows[tc];
+                base[q] = hr.p[tc];
+            }
+#pragma unroll
+            for (int q = 0; q < MOVE_ROWS; ++q) {
+                const int64_t row = key[q] & row_mask;
+                src[q] = tab[q] < tb.T && row < nrows[q] ? base[q] + row * LPR + c : nullptr;
             }
         }
-        float4 prev[MOVE_ROWS], next[MOVE_ROWS];
 #pragma unroll
-        for (int q = 0; q < MOVE_ROWS; ++q) {  // every load of the batch in flight together
-            if (v[q] >= 0 && old[q] >= 0) prev[q] = storage[(int64_t)v[q] * LPR + c];
-            if (v[q] >= 0 && src[q]) next[q] = *src[q];
+        for (int q = 0; q < MOVE_ROWS; ++q) {
+            if (!in[q] || (uint32_t)v[q] >= (uint64_t)nslots) v[q] = -1;
+            if (v[q] < 0) src[q] = nullptr;
+        }
+        v4f prev[MOVE_ROWS], next[MOVE_ROWS];
+#pragma unroll
+        for (int q = 0; q < MOVE_ROWS; ++q) {
+            prev[q] = as_v4f(storage + (v[q] >= 0 && old[q] >= 0 ? (int64_t)v[q] * LPR : 0) + c);
+            next[q] = as_v4f(src[q] ? src[q] : storage + c);
         }
 #pragma unroll
         for (int q = 0; q < MOVE_ROWS; ++q) {
             const int64_t i = i0 + q * groups;
-            if (i >= n) continue;
-            if (c == 0) reinterpret_cast<int32_t *>(stage + n * LPR)[i] = old[q];
-            if (v[q] < 0) continue;
-            if (old[q] >= 0) stage[i * LPR + c] = prev[q];
-            if (src[q]) storage[(int64_t)v[q] * LPR + c] = next[q];
+            if (in[q] && c == 0) old_keys[i] = old[q];
+            if (v[q] >= 0 && old[q] >= 0) *reinterpret_cast<v4f *>(stage + i * LPR + c) = prev[q];
+            if (src[q]) *reinterpret_cast<v4f *>(storage + (int64_t)v[q] * LPR + c) = next[q];
         }
     }
 }

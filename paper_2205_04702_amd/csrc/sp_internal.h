@@ -69,12 +69,16 @@ constexpr int32_t ERR_TABLE_IDS = 16;  // a table has more IDs than the configur
 __host__ __device__ inline int64_t multi_capacity(int64_t max_ids, int chunk) { return max_ids / (chunk + 1) + 2; }
 
 // Batches whose tables each have at most IG_MAX IDs (and at most IG_MAX bags)
-// are ingested by one launch, one workgroup per table, entirely in LDS.
+// are ingested by one launch entirely in LDS, ingest_splits(T) workgroups per
+// table, each owning a range of the table's rows (T * splits stays within the
+// 256 compute units).
 constexpr int IG_MAX = 8192;
+constexpr int IG_SPLIT_MAX = 16;
 inline bool ingest_in_lds(int64_t max_table_ids, int64_t B)
 {
     return max_table_ids > 0 && max_table_ids <= IG_MAX && B <= IG_MAX;
 }
+inline int ingest_splits(int T) { return T <= 16 ? 16 : (T <= 32 ? 8 : 4); }
 
 // One window-ring entry: a batch as it arrived plus its sort/dedup products.
 struct BatchDev {

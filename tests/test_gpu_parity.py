@@ -106,13 +106,25 @@ def test_device_resident_ids_match_host_ids(harness):
         assert np.array_equal(x, y)
 
 
-@pytest.mark.parametrize("shape", ["ragged", "8192-ids", "8192-bags"])
+@pytest.mark.parametrize("shape", ["ragged", "8192-ids", "8192-bags", "skewed-rows"])
 def test_ingest_in_lds_matches_general_path(harness, shape):
     """Batches whose tables fit one workgroup are sorted and deduplicated in LDS, one
-    launch per batch; the general path uses several launches over the whole batch.  Both
-    must give the oracle's plans, and bit-identical tables.  Edge cases: ragged and empty
-    bags, tables at the 8192-ID limit with hot runs split into chunks, 8192 bags."""
-    if shape == "ragged":
+    launch per batch, several workgroups per table, each over a range of the table's
+    rows; the general path uses several launches over the whole batch.  Both must give
+    the oracle's plans, and bit-identical tables.  Edge cases: ragged and empty bags,
+    tables at the 8192-ID limit with hot runs split into chunks, 8192 bags, and every
+    ID of a table in its first row range (one workgroup holds all 8192) beside a table
+    with fewer rows than there are ranges."""
+    if shape == "skewed-rows":
+        w = wl.custom(rows=[200_000, 5, 50_000], dim=16, batch=1024, pooling=8,
+                      slots=[20_000, 5, 5_000], lookahead=1, steps=6, dist=("zipf", 1.1),
+                      seed=20)
+        batches = []
+        for ids, off in harness.make_inputs(w):
+            ids = ids.copy()
+            ids[:1024 * 8] %= 9000  # table 0: rows below 9000 only
+            batches.append((ids, off))
+    elif shape == "ragged":
         w = wl.custom(rows=[900, 1400, 700], dim=16, batch=64, pooling=3, slots=[600, 800, 500],
                       lookahead=2, steps=14, seed=17)
         batches = [wl.ragged_batch(w, s, 7, empty_frac=0.25) for s in range(w.steps)]

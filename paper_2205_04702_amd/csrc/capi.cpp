@@ -1,11 +1,15 @@
 // C ABI of the scratchpad: context, window ring, plan/forward/backward state
 // machine, write-back thread and flush.  Kernels live in k_*.hip.
 //
-// Streams.  The caller's stream runs forward and backward.  The library's
-// plan stream runs window ingest, the plan and the miss fill; its copy stream
-// runs the device-to-host copy of evicted rows, which a host thread then
-// scatters into the host tables ([Collect] / [Exchange] / [Insert] of
-// Sec. IV-B, with the CPU-side insert done off the critical path).
+// Streams.  The caller's stream runs forward and backward.  The library has
+// four: the ingest stream sorts and deduplicates window batches (and carries
+// large write-back copies), the plan stream runs the query and the commit
+// sequence, the move stream runs the miss fill (and, with the staged fill,
+// the host-to-device copies of gathered rows), and the copy stream carries
+// small device-to-host copies of evicted rows.  Host threads gather missing
+// rows into pinned staging (staged fill) and scatter evicted rows into the
+// host tables ([Collect] / [Exchange] / [Insert] of Sec. IV-B, with the
+// CPU-side work done off the critical path).
 //
 // Ordering (the RAW dependences of Sec. IV-B, for one plan k in flight while
 // batch k-1 trains):
@@ -325,7 +329,7 @@ static int sem_words(int nring) { return SEM_UPD + 8 * nring; }
 // host scatter of plan p - 2 can all be in flight)
 constexpr int MAX_NSTAGE = 3;
 // staged fill: bytes of gathered rows per host-to-device copy, an eighth of
-// the plan's rows within these bounds (measured on the MI355X machine beside a
+// the plan's rows within these bounds (measured on an MI355X beside a
 // device-to-host copy of the same size: 8 MiB copies reach 45 GB/s, 32 MiB
 // copies 56 GB/s; a small fill still needs several copies to overlap its
 // gather), and per work item of the gather threads (small, so that all of

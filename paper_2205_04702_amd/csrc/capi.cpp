@@ -340,6 +340,8 @@ constexpr int64_t FILL_ITEM_BYTES = 1ll << 20;
 // write-back copies above this size go on the ingest stream, where they
 // overlap the next fill; smaller ones go on the copy stream
 constexpr int64_t SMALL_COPY_BYTES = 8ll << 20;
+// device-to-host copies of write-backs are issued in pieces of this size
+constexpr int64_t WB_PIECE_BYTES = 32ll << 20;
 
 struct sp_ctx {
     // configuration
@@ -352,6 +354,8 @@ struct sp_ctx {
     int key_bits = 0, chunk = 0;
     Tables tb{};
     int64_t slots[MAX_TABLES]{}, total_slots = 0, maxS = 0;
+    // per table: slots fresh[t] .. slots[t] - 1 have never held a row
+    int64_t fresh[MAX_TABLES]{};
     float *host[MAX_TABLES]{}, *host_dev[MAX_TABLES]{};
 
     // device state
@@ -1263,8 +1267,18 @@ static sp_status issue_copy(sp_ctx *h, hipStream_t s)
     const int64_t n = h->copy_n;
     if (n > 0) {
         HIPCHK(h, wait_unless_done(s, h->ev_filled[p % h->nring]));
-        HIPCHK(h, hipMemcpyAsync(h->stage_host[sl], h->stage_dev[sl],
-                                 sizeof(float) * n * (h->D + 1), hipMemcpyDeviceToHost, s));
+        // in pieces: the runtime copies device to host with a blit kernel
+        // that keeps a workgroup on every compute unit until it ends, and
+        // one copy of a large write-back runs for most of the step; pieces
+        // end often enough for the training kernels' workgroups to take
+        // those units (the 26x10M update: 0.63 ms beside pieces of 32 MiB,
+        // 0.74-0.84 ms beside one copy of 911 MB)
+        const int64_t bytes = (int64_t)sizeof(float) * n * (h->D + 1);
+        for (int64_t off = 0; off < bytes; off += WB_PIECE_BYTES)
+            HIPCHK(h, hipMemcpyAsync((char *)h->stage_host[sl] + off,
+                                     (const char *)h->stage_dev[sl] + off,
+                                     std::min(WB_PIECE_BYTES, bytes - off),
+                                     hipMemcpyDeviceToHost, s));
         HIPCHK(h, hipEventRecord(h->ev_d2h[sl], s));
         job.ev = h->ev_d2h[sl];
         job.rows = h->stage_host[sl];
@@ -1595,11 +1609,24 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
             ++h->st.hash_rebuilds;
         }
         h->hash_used += n_miss;
+        // every table's victims among its never-used slots: no select (with
+        // LFU and prefetch never-used slots are not known to come first)
+        bool fresh = !(h->policy == POLICY_LFU && pf_on);
+        for (int t = 0; t < h->T; ++t)
+            fresh = fresh && c.miss[t] + pf_tot[t] <= h->slots[t] - h->fresh[t];
         SelArgs a{};
+        FreshArgs f{};
         int32_t vb = 0;
-        int64_t maxS = 0;
+        int64_t maxS = 0, maxK = 0;
         for (int t = 0; t < h->T; ++t) {
-            if (c.miss[t] + pf_tot[t] > 0) {
+            const int64_t kt = c.miss[t] + pf_tot[t];
+            if (fresh && kt > 0) {
+                const int y = f.n++;
+                f.vbase[y] = vb;
+                f.k[y] = (int32_t)kt;
+                f.first[y] = h->tb.slot_base[t] + h->fresh[t];
+                maxK = std::max(maxK, kt);
+            } else if (kt > 0) {
                 int y = a.nact++;
                 a.t[y] = t;
                 a.k[y] = c.miss[t] + pf_tot[t];
@@ -1609,6 +1636,9 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
                 maxS = std::max<int64_t>(maxS, h->slots[t]);
             }
             vb += c.miss[t] + pf_tot[t];
+            // the first kt never-used slots are taken either way (all of them
+            // when there are fewer)
+            h->fresh[t] = std::min<int64_t>(h->slots[t], h->fresh[t] + kt);
         }
         // priority values: LRU last use + 1 <= u, LFU uses <= u + 1, random <= 2^24
         const int nb = h->policy == POLICY_RANDOM ? 25
@@ -1618,9 +1648,12 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
         a.stamp = stamp;
         a.prio = Prio{h->policy == POLICY_LFU ? h->uses : h->last_use, h->policy, (uint32_t)u, h->seed};
         const int levels = (nb + SEL_BITS - 1) / SEL_BITS;
-        launch_select_victims(a, levels, maxS, h->held, h->sel_state, h->sel_hist, h->vk0,
-                              h->vv0, h->vk1, (uint32_t *)nullptr, n_miss, h->hist, h->ws_plan,
-                              tk.v_slot, &h->cnt->err_sticky, h->s_plan);
+        if (fresh)
+            launch_fresh_victims(f, maxK, tk.v_slot, h->s_plan);
+        else
+            launch_select_victims(a, levels, maxS, h->held, h->sel_state, h->sel_hist, h->vk0,
+                                  h->vv0, h->vk1, (uint32_t *)nullptr, n_miss, h->hist,
+                                  h->ws_plan, tk.v_slot, &h->cnt->err_sticky, h->s_plan);
     }
     launch_commit(h->tb, h->hash, h->hash_mask, tk, b0, n_miss, th.n_unique, th.nnz, h->key_of_slot,
                   h->last_use, h->uses, u, pf_on, h->cnt, h->s_plan);

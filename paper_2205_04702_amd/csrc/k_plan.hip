@@ -455,6 +455,30 @@ __global__ void __launch_bounds__(VS_THREADS) k_victim_sort(SelArgs a, const uin
     for (int i = tid; i < n; i += VS_THREADS) v_slot[off + i] = (int32_t)(uint32_t)srt[i];
 }
 
+// Victims when every table's misses fit in its never-used slots.  Those slots
+// have priority 0 under every policy and come before every used slot (LFU
+// with prefetch excepted: a prefetched row not yet used also has 0 uses, and
+// the host then always selects), they are never held, and each plan takes
+// them in slot order; so they are always the last slots of each table, and
+// the k smallest (priority, slot) among unheld slots are simply the next k
+// of them.  This is the select's own result without the select.
+__global__ void __launch_bounds__(BLOCK) k_fresh_victims(FreshArgs f, int32_t *v_slot)
+{
+    const int y = blockIdx.y;
+    const int64_t k = f.k[y];
+    for (int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x; i < k;
+         i += (int64_t)gridDim.x * BLOCK)
+        v_slot[f.vbase[y] + i] = (int32_t)(f.first[y] + i);
+}
+
+void launch_fresh_victims(const FreshArgs &f, int64_t max_k, int32_t *v_slot, hipStream_t s)
+{
+    if (f.n <= 0 || max_k <= 0) return;
+    const int64_t gx = (max_k + BLOCK - 1) / BLOCK;
+    hipLaunchKernelGGL(k_fresh_victims, dim3((unsigned)(gx < 1024 ? gx : 1024), (unsigned)f.n),
+                       dim3(BLOCK), 0, s, f, v_slot);
+}
+
 void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int32_t *held,
                            int32_t *sel_state, int32_t *sel_hist,
                            uint32_t *vk0, uint32_t *vv0, uint32_t *vk1, uint32_t *vv1,

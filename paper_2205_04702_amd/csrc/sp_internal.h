@@ -148,6 +148,16 @@ struct SelArgs {
     int32_t vbase[MAX_TABLES];       // first victim index of the table
 };
 
+// Victims taken straight from the tables' never-used slots (fresh path):
+// table y's k[y] victims are global slots first[y] .. first[y] + k[y] - 1,
+// written from victim index vbase[y] on.
+struct FreshArgs {
+    int32_t n;
+    int32_t vbase[MAX_TABLES];
+    int32_t k[MAX_TABLES];
+    int64_t first[MAX_TABLES];
+};
+
 // Positions per backward chunk: one lane group sums at most this many
 // gradient rows before a run is split across groups.
 constexpr int BWD_CHUNK = 16;
@@ -215,6 +225,7 @@ void launch_query(const Tables &tb, const uint64_t *hash, uint32_t mask,
 
 void launch_hash_rebuild(uint64_t *hash, uint32_t mask, const int32_t *key_of_slot, int64_t nslots,
                          DevCounters *cnt, hipStream_t s);
+void launch_fresh_victims(const FreshArgs &f, int64_t max_k, int32_t *v_slot, hipStream_t s);
 void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int32_t *held, int32_t *sel_state, int32_t *sel_hist,
                            uint32_t *vk0, uint32_t *vv0, uint32_t *vk1, uint32_t *vv1,
                            int64_t n_victims, uint32_t *hist, ScanWs &ws, int32_t *v_slot,

@@ -140,7 +140,11 @@ typedef struct {
     int64_t nnz;                /* number of IDs, 0 .. max_ids                          */
     const int32_t *ids;         /* [nnz] row IDs, table-major                          */
     const int32_t *bag_off;     /* [T*B+1] bag offsets                                 */
-    int32_t on_device;          /* 0: ids/bag_off are host memory; 1: device memory    */
+    int32_t on_device;          /* 0: ids/bag_off are host memory; 1: device memory,
+                                   which must hold the batch when sp_plan is called: the
+                                   library reads it on its own stream, with no order
+                                   against the caller's streams (synchronise the stream
+                                   that wrote it first)                               */
 } sp_batch;
 
 typedef struct {

@@ -1670,10 +1670,11 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     // directions) and is well under way when the next call's ingest comes
     if (h->copy_pending >= 0 && h->copy_n * (h->D + 1) * (int64_t)sizeof(float) > SMALL_COPY_BYTES)
         TRY(issue_copy(h, h->s_ingest));
-    // With the staged fill the batches prepared ahead are ingested here, behind
-    // that copy on the ingest stream (the next plan's query needs only the
-    // batches of its window, ingested by earlier plans).
-    if (h->staged) TRY(ingest_ahead(h, window, n, nhold, k));
+    // With the staged fill the batches prepared ahead are ingested behind that
+    // copy on the ingest stream: here only the one the next plan's query holds
+    // (normally in the ring already), the rest at the end of this call, where
+    // the host's copy of the caller's arrays overlaps that query.
+    if (h->staged) TRY(ingest_ahead(h, window, std::min(n, nhold + 1), nhold, k));
     double tF = host_ms();
     h->host_ms[3] += tF - tE;
     // ---- the next plan's query, when its whole window is known: batches
@@ -1767,6 +1768,11 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     h->st.bytes_fill += n_miss * h->D * (int64_t)sizeof(float);
     h->st.min_capacity_margin = std::min(h->st.min_capacity_margin, margin);
     if (ticket) *ticket = k;
+    if (h->staged) {
+        const double t0 = host_ms();
+        TRY(ingest_ahead(h, window, n, nhold, k));
+        h->host_ms[0] += host_ms() - t0;
+    }
     if (h->flags & SP_FLAG_DEBUG_SYNC) HIPCHK(h, hipDeviceSynchronize());
     return SP_OK;
 }

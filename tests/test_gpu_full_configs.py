@@ -4,6 +4,7 @@ Each runs as the benchmark drives it, for a number of steps that reaches
 steady eviction, with bit-exact plans against the reference planner, sampled
 forward outputs, every touched row after flush, and untouched sentinel rows."""
 import dataclasses
+import os
 
 import pytest
 
@@ -106,3 +107,13 @@ def test_zipf_26x4M_full_size_prefetch_depth_4(harness):
     _say(f"zipf-26x4M prefetch 4: worst fwd {r['worst_fwd']:.2e} table {r['worst_table']:.2e} "
          f"fills {st['misses']} prefetched {st['prefetched']} evictions {st['evictions']}")
     assert st["evictions"] > 0 and st["prefetched"] > 0
+
+
+@pytest.mark.skipif(os.environ.get("SCRATCHPIPE_SLOW_TESTS") != "1",
+                    reason="about ten minutes; run with SCRATCHPIPE_SLOW_TESTS=1")
+def test_zipf_26x4M_all_500_steps_staged(harness):
+    """26 x 4M for all 500 steps of the configuration, with the staged fill and host IDs
+    as the benchmark drives it: every plan bit-exact, forward outputs at sampled steps,
+    and every touched row after flush within the tolerance after 500 SGD steps."""
+    st = _run(harness, "zipf-26x4M", 500, (0, 100, 250, 499), fill="staged", host_ids=True)
+    assert st["evictions"] > 0

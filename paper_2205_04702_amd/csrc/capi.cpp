@@ -1202,8 +1202,9 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
     HIPCHK(h, wait_unless_done(si, h->ev_upd[r]));
     // With the staged fill the step is bound by the host's gather, and a batch
     // sorted ahead has time to spare: it waits for the last update issued, so
-    // that the training kernels do not share the GPU with it.
-    if (h->staged && h->updated > 0)
+    // that the training kernels do not share the GPU with it.  Not one in the
+    // caller's device memory: sp_plan waits until its arrays have been read.
+    if (h->staged && h->updated > 0 && !bt.on_device)
         HIPCHK(h, wait_unless_done(si, h->ev_upd[(h->updated - 1) % h->nring]));
     const bool timing = h->flags & SP_FLAG_TIMING;
     if (timing) HIPCHK(h, h->t_ing.begin(si));
@@ -1668,6 +1669,13 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     // behind this call's ingests (its fill has normally finished by now): it
     // then overlaps this plan's fill (the two use the host link in opposite
     // directions) and is well under way when the next call's ingest comes
+    // (batches prepared ahead in the caller's device memory are ingested before
+    // it: sp_plan waits until their arrays have been read)
+    if (h->staged) {
+        bool dev = false;
+        for (int w = nhold; w < n; ++w) dev = dev || window[w].on_device;
+        if (dev) TRY(ingest_ahead(h, window, n, nhold, k));
+    }
     if (h->copy_pending >= 0 && h->copy_n * (h->D + 1) * (int64_t)sizeof(float) > SMALL_COPY_BYTES)
         TRY(issue_copy(h, h->s_ingest));
     // With the staged fill the batches prepared ahead are ingested behind that

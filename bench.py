@@ -78,6 +78,56 @@ def traffic_from_profile(kernel: str, src_hash: str, workload: str):
     return None
 
 
+def link_rates(mib: int = 1024, piece_mib: int = 32) -> dict:
+    """The host link as this step uses it: host-to-device and device-to-host copies
+    of `mib` MiB between pinned host memory and HBM, in pieces of `piece_mib` MiB as
+    the library issues them, each direction alone and both at once on two streams
+    (GB/s)."""
+    import torch
+    n, p = mib << 20, piece_mib << 20
+    h_in = torch.empty(n, dtype=torch.uint8, pin_memory=True)
+    h_out = torch.empty(n, dtype=torch.uint8, pin_memory=True)
+    d_in = torch.empty(n, dtype=torch.uint8, device="cuda")
+    d_out = torch.empty(n, dtype=torch.uint8, device="cuda")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+
+    def h2d():
+        with torch.cuda.stream(s1):
+            for o in range(0, n, p):
+                d_in[o:o + p].copy_(h_in[o:o + p], non_blocking=True)
+
+    def d2h():
+        with torch.cuda.stream(s2):
+            for o in range(0, n, p):
+                h_out[o:o + p].copy_(d_out[o:o + p], non_blocking=True)
+
+    def seconds(*fs):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for f in fs:
+            f()
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0
+
+    seconds(h2d, d2h)  # first use of the buffers
+    a, b, c = seconds(h2d), seconds(d2h), seconds(h2d, d2h)
+    return {"h2d_alone_GBps": round(n / a / 1e9, 2), "d2h_alone_GBps": round(n / b / 1e9, 2),
+            "both_GBps": round(2 * n / c / 1e9, 2)}
+
+
+def link_rates_in_child():
+    """link_rates() in a fresh child process.  In this one the library's four
+    streams and the caller's already share the GPU's four hardware queues, and the
+    two copy streams could land on one queue and run one after the other."""
+    import subprocess
+    r = subprocess.run([sys.executable, os.path.abspath(__file__), "--link-rates-only"],
+                       capture_output=True, text=True, timeout=300)
+    if r.returncode != 0:
+        log(f"[bench] host-link probe failed: {r.stderr.strip()[-300:]}")
+        return None
+    return json.loads(r.stdout.strip().splitlines()[-1])
+
+
 def cpu_model() -> str:
     try:
         for line in open("/proc/cpuinfo"):
@@ -145,6 +195,11 @@ def main():
     ap.add_argument("--general-ingest", action="store_true",
                     help="promise no bound on IDs per table, so batches are sorted by the "
                          "multi-launch path even where one workgroup per table would do")
+    ap.add_argument("--no-huge-pages", action="store_true",
+                    help="staged fill: do not advise the host tables for transparent huge pages")
+    ap.add_argument("--no-link-probe", action="store_true",
+                    help="skip the host-link measurement after the timed region")
+    ap.add_argument("--link-rates-only", action="store_true", help=argparse.SUPPRESS)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-timing", action="store_true", help="do not time kernels with events")
@@ -162,6 +217,9 @@ def main():
                     help="after the timed region, run a plain elementwise copy (torch.neg) of MIB "
                          "MiB three times: the reference kernel for scaling HBM byte counters")
     args = ap.parse_args()
+    if args.link_rates_only:  # the child of link_rates_in_child
+        print(json.dumps(link_rates()), flush=True)
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the scratchpad path has no multi-GPU mode "
@@ -195,7 +253,7 @@ def main():
     nb_needed = lambda steps: steps + L + 1 + ahead  # noqa: E731  (windows of the last step)
 
     t0 = time.perf_counter()
-    host = sp.host_tables(w.rows, w.dim, fill)
+    host = sp.host_tables(w.rows, w.dim, fill, huge_pages=not args.no_huge_pages)
     # tables are independent streams: fill them on threads (numpy's generators
     # release the GIL)
     with cf.ThreadPoolExecutor(max_workers=max(1, min(16, w.tables, os.cpu_count() or 1))) as ex:
@@ -322,6 +380,8 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {**w.describe(), "ids": args.ids, "fill": fill,
+                   **({"host_pages": "4k" if args.no_huge_pages else "huge (advised)"}
+                      if fill == "staged" else {}),
                    "timed_steps": [first_timed, first_timed + K - 1], "fillup_steps": fillup,
                    **({"policy": args.policy} if args.policy != "lru" else {}),
                    **({"hold_past": args.hold_past} if args.hold_past else {}),
@@ -390,6 +450,16 @@ def main():
                          "h2d_fill_span_ms": round(fill_ms, 4),
                          "h2d_span": "host-to-device copies of gathered rows" if fill == "staged"
                          else "zero-copy move kernel"})
+        if not args.no_link_probe:
+            # the step's floor on this link: its bytes in each direction at that
+            # direction's rate, and both together at the rate of both at once
+            r = link_rates_in_child()
+            if r:
+                h, o = link["h2d_bytes_per_step"], link["d2h_bytes_per_step"]
+                bound = max(h / r["h2d_alone_GBps"], o / r["d2h_alone_GBps"],
+                            (h + o) / r["both_GBps"]) / 1e6
+                link.update({"measured": r, "bound_ms_per_step": round(bound, 3),
+                             "step_frac_of_bound": round(bound / (dt * 1e3 / K), 4)})
         detail["host_link"] = link
     res["detail"] = detail
     if not args.no_cpu_baseline:

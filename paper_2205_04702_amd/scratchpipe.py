@@ -8,6 +8,7 @@ stream (torch.cuda.current_stream()) for forward/backward.
 from __future__ import annotations
 
 import ctypes as C
+import mmap
 import os
 
 import numpy as np
@@ -260,11 +261,28 @@ class HostTables:
 
 
 class PageableTables:
-    """fp32 host tables in ordinary (pageable) memory, for the staged fill: numpy
-    arrays, allocated lazily by the OS (pages appear when first written)."""
+    """fp32 host tables in ordinary (pageable) memory, for the staged fill, allocated
+    lazily by the OS (pages appear when first written).  With huge_pages (the
+    default) each table is an anonymous mapping advised for transparent huge pages
+    before any page is touched: the fill's host threads read and write rows at
+    random places in the tables, and 2 MB pages take most address translations off
+    that path.  Where the kernel does not allow it the advice changes nothing."""
 
-    def __init__(self, rows, dim: int):
-        self.arrays = [np.empty((int(r), dim), dtype=np.float32) for r in rows]
+    def __init__(self, rows, dim: int, huge_pages: bool = True):
+        self._maps = []
+        self.arrays = []
+        for r in rows:
+            n = int(r) * dim
+            if huge_pages and hasattr(mmap, "MADV_HUGEPAGE"):
+                m = mmap.mmap(-1, max(4 * n, 1), flags=mmap.MAP_PRIVATE | mmap.MAP_ANONYMOUS)
+                try:
+                    m.madvise(mmap.MADV_HUGEPAGE)
+                except OSError:
+                    pass
+                self._maps.append(m)
+                self.arrays.append(np.frombuffer(m, dtype=np.float32, count=n).reshape(int(r), dim))
+            else:
+                self.arrays.append(np.empty((int(r), dim), dtype=np.float32))
         self.ptrs = [int(a.ctypes.data) for a in self.arrays]
 
     def __getitem__(self, t):
@@ -276,12 +294,19 @@ class PageableTables:
     def close(self):
         self.arrays = []
         self.ptrs = []
+        for m in self._maps:
+            try:
+                m.close()
+            except BufferError:  # an array of it is still referenced: freed with it
+                pass
+        self._maps = []
 
 
-def host_tables(rows, dim: int, fill: str = "mapped"):
+def host_tables(rows, dim: int, fill: str = "mapped", huge_pages: bool = True):
     """Host tables for a context: pinned and device-mapped for the mapped fill,
-    ordinary memory for the staged fill."""
-    return PageableTables(rows, dim) if fill == "staged" else HostTables(rows, dim)
+    ordinary memory (in transparent huge pages unless huge_pages is false) for the
+    staged fill."""
+    return PageableTables(rows, dim, huge_pages) if fill == "staged" else HostTables(rows, dim)
 
 
 def _ptr(x) -> int:

@@ -145,3 +145,23 @@ def test_null_handle_calls_report_state_error():
 def test_worst_case_storage_helper_matches_paper():
     """Sec. VI-D: (8 x 20 x 2048 x 128 x 4 B) x 6 = 960 MiB."""
     assert sp.worst_case_scratchpad_bytes(8, 20, 2048, 128, 6) == 960 * 2 ** 20
+
+
+@pytest.mark.parametrize("huge", [True, False])
+def test_pageable_tables_for_the_staged_fill(huge):
+    """Ordinary host tables for the staged fill (in mappings advised for huge pages,
+    or plain arrays): fp32, row-major, writable, 16-byte aligned as sp_create requires,
+    each table its own allocation, and closing them twice is harmless."""
+    import numpy as np
+    t = sp.PageableTables([5, 1000, 1], 12, huge_pages=huge)
+    assert len(t) == 3
+    for i, rows in enumerate([5, 1000, 1]):
+        a = t[i]
+        assert a.shape == (rows, 12) and a.dtype == np.float32
+        assert a.flags.c_contiguous and a.flags.writeable
+        assert t.ptrs[i] == a.ctypes.data and t.ptrs[i] % 16 == 0
+        a[:] = i + 0.5
+    assert float(t[1].sum()) == 1.5 * 1000 * 12 and float(t[0][4, 11]) == 0.5
+    t.close()
+    t.close()
+    assert len(t) == 0

@@ -1,11 +1,13 @@
 """Embedding-training throughput of the HIP scratchpad on one MI355X.
 
-One step = sp_plan (window ingest with the batch IDs handed over from host
-memory, dedup, Hit-Map query, hold, LRU victims, commit, miss fill and
-evicted-row write-back) + sp_forward (pooled gather) + sp_backward_update
-(gradient coalescing and in-place SGD) for one mini-batch of the synthetic
-workload.  The embedding tables live in host memory and only the scratchpad
-is in HBM.  Upstream gradients are generated on the device before timing.
+One step = sp_plan (window ingest, dedup, Hit-Map query, hold, LRU victims,
+commit, miss fill and evicted-row write-back) + sp_forward (pooled gather) +
+sp_backward_update (gradient coalescing and in-place SGD) for one mini-batch
+of the synthetic workload.  The embedding tables live in host memory and only
+the scratchpad is in HBM.  The batches' IDs and the upstream gradients are
+generated in device memory before timing.  A second timed region then runs
+the next steps with the IDs handed over from host memory (copied to the
+device every step) and reports that rate beside the first.
 
 Before the timed steps the scratchpad is filled until every slot holds a row
 (untimed fill-up steps, so the timed steps evict and write back as in steady
@@ -177,9 +179,13 @@ def main():
                          "host gather into pinned staging then copies (auto: staged when the "
                          "tables exceed 8 GiB; measured faster on 26x4M and the mixed "
                          "workload, and the only way for tables beyond what one process pins)")
-    ap.add_argument("--ids", choices=["host", "hbm"], default="host",
-                    help="hand the batch IDs over from host memory (as the method does every "
-                         "step) or from device memory")
+    ap.add_argument("--ids", choices=["host", "hbm"], default="hbm",
+                    help="hand the batch IDs over from device memory (resident in HBM before "
+                         "the timed region) or from host memory, copied over the host link "
+                         "every step as the method's planner does")
+    ap.add_argument("--no-host-ids-rate", action="store_true",
+                    help="with --ids hbm, skip the second timed region that hands the same "
+                         "workload's next batches over from host memory")
     ap.add_argument("--fillup", type=int, default=-1, metavar="N",
                     help="untimed steps before the warm-up (-1: until every slot holds a row, "
                          "none when the slots hold every table)")
@@ -333,8 +339,10 @@ def main():
         if ctx.stats()["misses"] >= total_slots:
             break
     log(f"[bench] fill-up: {fillup} steps ({time.perf_counter() - t0:.1f}s)")
-    ensure_batches(nb_needed(u + W + K))
-    ensure_grads(u + W + K)
+    host_region = args.ids == "hbm" and not args.no_host_ids_rate
+    n_timed = K + (W + K if host_region else 0)
+    ensure_batches(nb_needed(u + W + n_timed))
+    ensure_grads(u + W + n_timed)
     last = len(host_batches) - 1
     for _ in range(W):
         step(u, last)
@@ -353,6 +361,34 @@ def main():
     ctx.sync()
     dt = time.perf_counter() - t0
     s1 = ctx.stats()
+    host_s_timed = list(host_s)
+    host_rate = None
+    if host_region:
+        # the next K steps with the IDs handed over from host memory: the rate
+        # that includes their copy over the host link every step (after W more
+        # untimed steps with them)
+        src = host_batches
+        for _ in range(W):
+            step(u, last)
+            u += 1
+        torch.cuda.synchronize()
+        ctx.sync()
+        s1h = ctx.stats()
+        first_host = u
+        t0 = time.perf_counter()
+        for _ in range(K):
+            step(u, last)
+            u += 1
+        torch.cuda.synchronize()
+        ctx.sync()
+        dth = time.perf_counter() - t0
+        s2 = ctx.stats()
+        host_rate = {"value": round(w.batch * K / dth, 1), "unit": "samples/s",
+                     "ms_per_step": round(dth * 1e3 / K, 4),
+                     "timed_steps": [first_host, first_host + K - 1],
+                     "evictions_per_step": round((s2["evictions"] - s1h["evictions"]) / K, 1),
+                     "ids": "host memory, copied to the device every step"}
+        log(f"[bench] timed {K} more steps with host IDs in {dth:.3f}s")
     if args.calibrate_copy > 0:
         x = torch.ones(args.calibrate_copy << 18, dtype=torch.float32, device=dev)
         y = torch.empty_like(x)
@@ -362,6 +398,7 @@ def main():
         del x, y
     ctx.close()
     log(f"[bench] timed {K} steps in {dt:.3f}s")
+    host_s[:] = host_s_timed
 
     d = {k: s1[k] - s0[k] for k in s1 if isinstance(s1[k], (int, float))}
     n_unique = d["unique"] / max(d["plans"], 1)
@@ -461,6 +498,8 @@ def main():
                 link.update({"measured": r, "bound_ms_per_step": round(bound, 3),
                              "step_frac_of_bound": round(bound / (dt * 1e3 / K), 4)})
         detail["host_link"] = link
+    if host_rate:
+        detail["host_ids_rate"] = host_rate
     res["detail"] = detail
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on the same tables")

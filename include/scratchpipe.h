@@ -140,11 +140,13 @@ typedef struct {
     int64_t nnz;                /* number of IDs, 0 .. max_ids                          */
     const int32_t *ids;         /* [nnz] row IDs, table-major                          */
     const int32_t *bag_off;     /* [T*B+1] bag offsets                                 */
-    int32_t on_device;          /* 0: ids/bag_off are host memory; 1: device memory,
-                                   which must hold the batch when sp_plan is called: the
-                                   library reads it on its own stream, with no order
-                                   against the caller's streams (synchronise the stream
-                                   that wrote it first)                               */
+    int32_t on_device;          /* 0: ids/bag_off are host memory, copied before sp_plan
+                                   returns; 1: device memory, which must hold the batch
+                                   when sp_plan is called (the library reads it on its
+                                   own stream, with no order against the caller's
+                                   streams: synchronise the stream that wrote it first)
+                                   and stay unchanged until an sp_plan call that holds
+                                   the batch (window index <= lookahead) has returned */
 } sp_batch;
 
 typedef struct {
@@ -245,8 +247,11 @@ sp_status sp_create(const sp_config *config, sp_handle *out);
  * enter the device window
  * ring once, when first seen, and are not read again: the same batch must be
  * passed with the same content every time it appears (after a failed plan
- * all of that call's batches are read again on the next call).  Window
- * buffers may be reused when the call returns.  The plan queries the Hit-Map
+ * all of that call's batches are read again on the next call).  Host window
+ * buffers may be reused when the call returns; device ones once a call that
+ * holds their batch has returned (a batch prepared ahead in device memory is
+ * read asynchronously, before the query of the first plan that holds it).
+ * The plan queries the Hit-Map
  * for window[0]'s unique keys, holds
  * every cached slot used by any window batch (and by the hold_past batches
  * planned before this one), takes for each table's misses the unheld slots

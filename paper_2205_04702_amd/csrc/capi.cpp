@@ -340,6 +340,10 @@ constexpr int64_t FILL_ITEM_BYTES = 1ll << 20;
 // write-back copies above this size go on the ingest stream, where they
 // overlap the next fill; smaller ones go on the copy stream
 constexpr int64_t SMALL_COPY_BYTES = 8ll << 20;
+// A write-back copy above this many bytes keeps the ingest stream busy for
+// most of a step (5 ms and more on the host link): batches prepared ahead are
+// then sorted behind the update instead of behind it.
+constexpr int64_t DEFER_BEHIND_COPY_BYTES = 256ll << 20;
 // device-to-host copies of write-backs are issued in pieces of this size
 constexpr int64_t WB_PIECE_BYTES = 32ll << 20;
 
@@ -421,6 +425,14 @@ struct sp_ctx {
     uint32_t *cons_counter = nullptr;
     uint32_t cons_issued = 0, cons_seq = 0;
     bool wait_cons_event = false, wait_cons_word = false;  // for the sp_plan call in progress
+    // staged fill: batches prepared ahead whose ingest sp_backward_update
+    // enqueues behind its update (host ones already in their pinned buffers)
+    struct Deferred {
+        sp_batch bt;
+        int64_t q;
+    };
+    std::vector<Deferred> deferred;
+    uint32_t wait_seq = 0;  // the word the last ingest from the caller's arrays writes
     uint32_t qseq = 0;        // sequence number of the last query issued
     uint32_t spec_seq = 0;    // that of the early query
 
@@ -1193,18 +1205,27 @@ static hipError_t wait_unless_done(hipStream_t s, hipEvent_t e)
     return hipStreamWaitEvent(s, e, 0);
 }
 
-static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
+// `ahead`: the batch is only prepared, held by a later plan (window index
+// above the lookahead).  Its arrays in the caller's device memory may be read
+// after this sp_plan call returns: the query of the first plan that holds the
+// batch waits for this ingest, and that plan waits for the query.
+// `prestaged`: a batch from host memory already copied into the entry's
+// pinned buffers (by defer_ahead).
+static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q, bool ahead,
+                        bool prestaged = false)
 {
     const int r = (int)(q % h->nring);
     BatchDev &b = h->ring[r];
     hipStream_t si = h->s_ingest;
+    // this call returns only once the caller's device arrays have been read
+    const bool caller_waits = bt.on_device && !ahead;
     // the previous occupant (batch q - nring) must be done with its backward
     HIPCHK(h, wait_unless_done(si, h->ev_upd[r]));
     // With the staged fill the step is bound by the host's gather, and a batch
     // sorted ahead has time to spare: it waits for the last update issued, so
-    // that the training kernels do not share the GPU with it.  Not one in the
-    // caller's device memory: sp_plan waits until its arrays have been read.
-    if (h->staged && h->updated > 0 && !bt.on_device)
+    // that the training kernels do not share the GPU with it.  Not one the
+    // host waits for.
+    if (h->staged && h->updated > 0 && !caller_waits)
         HIPCHK(h, wait_unless_done(si, h->ev_upd[(h->updated - 1) % h->nring]));
     const bool timing = h->flags & SP_FLAG_TIMING;
     if (timing) HIPCHK(h, h->t_ing.begin(si));
@@ -1215,9 +1236,11 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
         // (the caller's arrays are free again right after), then to the ring
         // asynchronously.  The buffers' previous copy (batch q - nring, or
         // this batch before a rejected plan) has long run.
-        if (h->ids_pending[r]) HIPCHK(h, hipEventSynchronize(h->ev_ids[r]));
-        if (bt.nnz > 0) memcpy(h->h_ids[r], bt.ids, sizeof(int32_t) * bt.nnz);
-        memcpy(h->h_off[r], bt.bag_off, sizeof(int32_t) * (nbags + 1));
+        if (!prestaged) {
+            if (h->ids_pending[r]) HIPCHK(h, hipEventSynchronize(h->ev_ids[r]));
+            if (bt.nnz > 0) memcpy(h->h_ids[r], bt.ids, sizeof(int32_t) * bt.nnz);
+            memcpy(h->h_off[r], bt.bag_off, sizeof(int32_t) * (nbags + 1));
+        }
         if (bt.nnz > 0)
             HIPCHK(h, hipMemcpyAsync(b.ids, h->h_ids[r], sizeof(int32_t) * bt.nnz,
                                      hipMemcpyHostToDevice, si));
@@ -1235,13 +1258,16 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q)
         h->cons_issued += (uint32_t)(h->T * ingest_splits(h->T));
         ic.target = h->cons_issued;
         ic.seq = ++h->cons_seq;
-        if (bt.on_device) h->wait_cons_word = true;
-    } else if (bt.on_device) {
+        if (caller_waits) {
+            h->wait_cons_word = true;
+            h->wait_seq = ic.seq;
+        }
+    } else if (caller_waits) {
         h->wait_cons_event = true;  // recorded by launch_ingest once the inputs are read
     }
     launch_ingest(h->tb, b, ids, off, bt.batch, bt.nnz, h->key_bits, h->chunk, h->max_table_ids,
                   h->max_ids, h->nchunk_max, h->itmp_k, h->itmp_v, h->ihist, h->ws_ingest,
-                  h->ev_consumed, ic, si);
+                  caller_waits ? h->ev_consumed : nullptr, ic, si);
     CHECK_LAUNCH(h);
     if (h->ws_ingest.overflow) return fail(h, SP_ERR_HIP, "internal: scan workspace too small");
     HIPCHK(h, hipEventRecord(h->ring_ready[r], si));
@@ -1300,7 +1326,44 @@ static sp_status issue_copy(sp_ctx *h, hipStream_t s)
 static sp_status ingest_ahead(sp_ctx *h, const sp_batch *window, int n, int nhold, int64_t k)
 {
     for (int w = nhold; w < n; ++w)
-        if (h->ring_batch[(k + w) % h->nring] != k + w) TRY(ingest(h, window[w], k + w));
+        if (h->ring_batch[(k + w) % h->nring] != k + w) TRY(ingest(h, window[w], k + w, true));
+    return SP_OK;
+}
+
+// Staged fill with a large write-back copy on the ingest stream: sorted behind
+// that copy, the batches prepared ahead would run as the step's training
+// kernels do.  Those that no query of this call or the next needs (window
+// index above lookahead + 1) are sorted behind the update of this plan's
+// ticket instead, where the step waits for the host's gather.  Host arrays
+// are copied into the entry's pinned buffers now (the caller's are free when
+// sp_plan returns); device ones are read then, before any plan that holds
+// them.
+static sp_status defer_ahead(sp_ctx *h, const sp_batch *window, int n, int from, int64_t k)
+{
+    for (int w = from; w < n; ++w) {
+        const sp_batch &bt = window[w];
+        const int64_t q = k + w;
+        const int r = (int)(q % h->nring);
+        if (h->ring_batch[r] == q) continue;
+        if (!bt.on_device) {
+            if (h->ids_pending[r]) HIPCHK(h, hipEventSynchronize(h->ev_ids[r]));
+            h->ids_pending[r] = 0;
+            if (bt.nnz > 0) memcpy(h->h_ids[r], bt.ids, sizeof(int32_t) * bt.nnz);
+            memcpy(h->h_off[r], bt.bag_off,
+                   sizeof(int32_t) * ((int64_t)h->T * bt.batch + 1));
+        }
+        h->deferred.push_back({bt, q});
+    }
+    return SP_OK;
+}
+
+// Enqueue the deferred ingests (behind the last update issued).
+static sp_status ingest_deferred(sp_ctx *h)
+{
+    const double t0 = host_ms();
+    for (const auto &d : h->deferred) TRY(ingest(h, d.bt, d.q, true, !d.bt.on_device));
+    h->deferred.clear();
+    h->host_ms[0] += host_ms() - t0;
     return SP_OK;
 }
 
@@ -1321,18 +1384,20 @@ static sp_status join_writebacks(sp_ctx *h, int64_t k)
     return SP_OK;
 }
 
-// Wait until the ingests this sp_plan call enqueued have read the caller's
-// window arrays: the general path's event, and the word an ingest in LDS
-// writes once its blocks have read their inputs (stream order makes the last
-// one enough).  Stream errors end the wait; they surface on the next call
-// that checks the stream.
+// Wait until the ingests of held batches that this sp_plan call enqueued have
+// read the caller's device arrays: the general path's event, and the word an
+// ingest in LDS writes once its blocks have read their inputs (stream order
+// makes the last one enough).  After a query this returns at once: the query
+// waited for those ingests.  Stream errors end the wait; they surface on the
+// next call that checks the stream.
 static void wait_inputs_read(sp_ctx *h)
 {
     const double t0 = host_ms();
     if (h->wait_cons_event) (void)hipEventSynchronize(h->ev_consumed);
     if (h->wait_cons_word) {
         const volatile uint64_t *w = h->h_cnt + COUNTER_WORDS;
-        for (int64_t spin = 0; (uint32_t)*w != h->cons_seq; ++spin) {
+        // words arrive in stream order; a later ingest's may already be there
+        for (int64_t spin = 0; (int32_t)((uint32_t)*w - h->wait_seq) < 0; ++spin) {
             if ((spin & 1023) == 1023 && hipStreamQuery(h->s_ingest) != hipErrorNotReady) {
                 (void)hipGetLastError();
                 break;  // idle (the word is final) or failed
@@ -1455,6 +1520,8 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
             return fail(h, SP_ERR_INVALID_ARG, "window[%d]: batch %d / nnz %lld outside the config or null pointer",
                         w, b.batch, (long long)b.nnz);
     }
+    // normally enqueued by the last sp_backward_update already
+    if (!h->deferred.empty()) TRY(ingest_deferred(h));
     const int64_t k = h->planned;
     const int32_t u = (int32_t)k;
     const int e = (int)(k % h->nring);
@@ -1478,7 +1545,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
         if (h->ring_batch[r] == q && (h->ring_nnz[r] != window[w].nnz || h->ring_B[r] != window[w].batch))
             return fail(h, SP_ERR_INVALID_ARG, "batch %lld changed shape between windows", (long long)q);
         if (w < nhold && h->ring_batch[r] != q) {
-            TRY(ingest(h, window[w], q));
+            TRY(ingest(h, window[w], q, false));
         }
     }
 
@@ -1669,15 +1736,8 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     // behind this call's ingests (its fill has normally finished by now): it
     // then overlaps this plan's fill (the two use the host link in opposite
     // directions) and is well under way when the next call's ingest comes
-    // (batches prepared ahead in the caller's device memory are ingested before
-    // it: sp_plan waits until their arrays have been read)
-    if (h->staged) {
-        bool dev = false;
-        for (int w = nhold; w < n; ++w) dev = dev || window[w].on_device;
-        if (dev) TRY(ingest_ahead(h, window, n, nhold, k));
-    }
-    if (h->copy_pending >= 0 && h->copy_n * (h->D + 1) * (int64_t)sizeof(float) > SMALL_COPY_BYTES)
-        TRY(issue_copy(h, h->s_ingest));
+    const int64_t copy_bytes = h->copy_pending >= 0 ? h->copy_n * (h->D + 1) * (int64_t)sizeof(float) : 0;
+    if (copy_bytes > SMALL_COPY_BYTES) TRY(issue_copy(h, h->s_ingest));
     // With the staged fill the batches prepared ahead are ingested behind that
     // copy on the ingest stream: here only the one the next plan's query holds
     // (normally in the ring already), the rest at the end of this call, where
@@ -1778,7 +1838,10 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     if (ticket) *ticket = k;
     if (h->staged) {
         const double t0 = host_ms();
-        TRY(ingest_ahead(h, window, n, nhold, k));
+        if (copy_bytes > DEFER_BEHIND_COPY_BYTES)
+            TRY(defer_ahead(h, window, n, nhold + 1, k));
+        else
+            TRY(ingest_ahead(h, window, n, nhold, k));
         h->host_ms[0] += host_ms() - t0;
     }
     if (h->flags & SP_FLAG_DEBUG_SYNC) HIPCHK(h, hipDeviceSynchronize());
@@ -1837,9 +1900,11 @@ extern "C" sp_status sp_forward(sp_handle h, int64_t ticket, float *d_out, void 
 
 // Backward and update of a ticket, the split runs' partial sums in `partial`
 // (the context's buffer, or the fixed array of the static entry point, which
-// holds at most partial_bytes).
+// holds at most partial_bytes).  `defer`: then enqueue the ingests that
+// sp_plan deferred (the static entry point leaves them to the next sp_plan and
+// enqueues nothing on the library's streams).
 static sp_status backward_update(sp_handle h, int64_t ticket, const float *d_grad, float lr,
-                                 void *stream, float *partial, int64_t partial_bytes)
+                                 void *stream, float *partial, int64_t partial_bytes, bool defer)
 {
     TRY(usable(h));
     if (ticket != h->forwarded - 1 || h->updated != ticket)
@@ -1873,6 +1938,7 @@ static sp_status backward_update(sp_handle h, int64_t ticket, const float *d_gra
     h->updated = ticket + 1;
     h->st.updates += 1;
     h->st.chunks += th.n_chunks;
+    if (defer) TRY(ingest_deferred(h));
     if (h->flags & SP_FLAG_DEBUG_SYNC) HIPCHK(h, hipDeviceSynchronize());
     return SP_OK;
 }
@@ -1882,14 +1948,15 @@ extern "C" sp_status sp_backward_update(sp_handle h, int64_t ticket, const float
 {
     if (!h) return SP_ERR_STATE;
     return backward_update(h, ticket, d_grad, lr, stream, h->partial,
-                           h->nchunk_max * h->D * (int64_t)sizeof(float));
+                           h->nchunk_max * h->D * (int64_t)sizeof(float), true);
 }
 
 extern "C" sp_status sp_backward_update_static(sp_handle h, int64_t ticket, const float *d_grad,
                                                float lr, void *stream)
 {
     if (!h) return SP_ERR_STATE;
-    return backward_update(h, ticket, d_grad, lr, stream, h->static_partial, STATIC_PARTIAL_BYTES);
+    return backward_update(h, ticket, d_grad, lr, stream, h->static_partial, STATIC_PARTIAL_BYTES,
+                           false);
 }
 
 // ---------------------------------------------------------------- flush / stats / debug

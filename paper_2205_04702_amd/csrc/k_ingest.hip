@@ -742,7 +742,7 @@ void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, cons
                            b.bag_of, b.scal + 2);
     else if (bag_off != b.bag_off)
         (void)hipMemcpyAsync(b.bag_off, bag_off, sizeof(int32_t), hipMemcpyDeviceToDevice, s);
-    (void)hipEventRecord(consumed, s);  // the caller's arrays are not read after this point
+    if (consumed) (void)hipEventRecord(consumed, s);  // the inputs are not read after this point
     if (nnz > 0) {
         bool in_k1 = false;
         launch_radix_sort(k0, v0, k1, v1, nnz, key_bits, hist, ws, &in_k1, s, false);

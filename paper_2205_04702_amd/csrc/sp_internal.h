@@ -177,7 +177,8 @@ struct IngestCons {
     uint32_t seq;
 };
 // Ingest one batch.  In LDS (ingest_in_lds and nnz > 0) the inputs are known
-// read when *ic.word reads ic.seq; otherwise when `consumed` completes.
+// read when *ic.word reads ic.seq; otherwise when `consumed` (if not null)
+// completes.
 void launch_ingest(const Tables &tb, const BatchDev &b, const int32_t *ids, const int32_t *bag_off,
                    int32_t B, int64_t nnz, int key_bits, int chunk, int64_t max_table_ids,
                    int64_t cap_u, int64_t cap_c, uint32_t *tmp_k, uint32_t *tmp_v,

@@ -364,7 +364,10 @@ class ScratchPipe:
                         on_device=_on_device(ids))
 
     def plan(self, window) -> int:
-        """window: [(ids, bag_off), ...] as int32 numpy arrays or int32 device tensors."""
+        """window: [(ids, bag_off), ...] as int32 numpy arrays or int32 device tensors.
+
+        Device tensors must hold their batch already and stay unchanged until a
+        plan that holds the batch (window index <= lookahead) has returned."""
         n = len(window)
         arr = (sp_batch * n)()
         keep = []

@@ -91,7 +91,8 @@ def make_inputs(w, steps=None, ragged=None):
 def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all", flags=0,
                device_ids=False, ref_tables=None, sync_each_step=True, compare_tables=True,
                return_tables=False, steps=None, prepare_ahead=0, policy="lru", hold_past=0,
-               seed=0, max_table_ids="auto", prefetch=False, fill="mapped"):
+               seed=0, max_table_ids="auto", prefetch=False, fill="mapped",
+               overwrite_held_ids=False):
     """Train w on the GPU and with the oracle; assert parity; return a summary.
 
     prepare_ahead: also hand the GPU that many batches after the window
@@ -100,7 +101,10 @@ def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all"
     max_table_ids: the bound handed to the library ("auto": the batches' own maximum,
     which sorts tables of up to 8192 IDs in LDS; 0: no bound, the general path).
     prefetch: both planners also fill the next batch's missing rows.
-    fill: how the GPU brings missing rows in ("mapped" or "staged")."""
+    fill: how the GPU brings missing rows in ("mapped" or "staged").
+    overwrite_held_ids: with device_ids, set every ID of the batches a plan held to
+    an out-of-range row once the plan returns (the library must not read a batch
+    again once a plan that holds it has returned)."""
     import torch
     dev = torch.device("cuda:0")
     if batches is None:
@@ -132,6 +136,9 @@ def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all"
                                  if q < n]
             ticket = sp.plan([src[q] for q in gpu_idx])
             assert ticket == u
+            if device_ids and overwrite_held_ids:
+                for q in win_idx:
+                    dev_batches[q][0].fill_(0x7FFFFFFF)
             p = planner.plan([batches[q] for q in win_idx], B,
                              past=batches[max(0, u - hold_past):u])
             if u in plan_set:

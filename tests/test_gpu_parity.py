@@ -152,9 +152,11 @@ def test_zipf_8x1M_full_size(harness):
     _say(f"case zipf-8x1M {w.describe()}")
     sample = [0, 1, 2, 3, 50, 101, 150, 198, 199]
     # as the benchmark drives it: IDs in device memory, the two batches after
-    # the window handed over early
+    # the window handed over early (read after sp_plan returns); the IDs of
+    # held batches are overwritten once their plan has returned
     r = harness.run_parity(w, check_plan_steps=sample, check_fwd_steps=sample,
-                           sync_each_step=False, prepare_ahead=2, device_ids=True)
+                           sync_each_step=False, prepare_ahead=2, device_ids=True,
+                           overwrite_held_ids=True)
     st = r["stats"]
     assert st["plans"] == 200 and st["evictions"] > 0
     _say(f"zipf-8x1M worst fwd {r['worst_fwd']:.2e} table {r['worst_table']:.2e} "

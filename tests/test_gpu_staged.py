@@ -52,16 +52,17 @@ def test_staged_every_row_width_ragged(harness, dim):
 @pytest.mark.parametrize("bound", ["auto", 0])
 def test_staged_device_ids_handed_over_ahead(harness, bound):
     """IDs in device memory, the two batches after the window handed over ahead and no
-    synchronisation between steps: device batches are ingested before the write-back
-    copy and without waiting for the last update, unlike host ones.  Both ingest paths
-    (in LDS, and general); the tables must equal the host-ID run's bit for bit."""
+    synchronisation between steps: batches prepared ahead are read after sp_plan has
+    returned, and once a plan that holds a batch has returned its IDs are overwritten
+    with an out-of-range row, which the library must never see.  Both ingest paths (in
+    LDS, and general); the tables must equal the host-ID run's bit for bit."""
     w = wl.custom(rows=[6000, 9000, 4000], dim=32, batch=64, pooling=6,
                   slots=[1500, 2000, 1200], lookahead=2, steps=30, dist=("zipf", 1.05),
                   seed=43)
     _say(f"case staged device IDs bound {bound}")
     a = harness.run_parity(w, fill="staged", device_ids=True, prepare_ahead=2,
                            sync_each_step=False, max_table_ids=bound, return_tables=True,
-                           check_fwd_steps=[0, 15, 29])
+                           check_fwd_steps=[0, 15, 29], overwrite_held_ids=True)
     b = harness.run_parity(w, fill="staged", prepare_ahead=2, sync_each_step=False,
                            max_table_ids=bound, return_tables=True, check_fwd_steps=[29])
     assert a["stats"]["evictions"] > 0

@@ -137,6 +137,11 @@ struct Job {
 };
 
 struct TicketHost {
+    QueryRows qr{};  // the rows of the plan's query (its entering batches, rebuild)
+    const uint32_t *uk[MAX_WINDOW] = {};  // the query's probe arrays
+    const int32_t *nu[MAX_WINDOW] = {};
+    int64_t ent_len[MAX_WINDOW] = {};  // per probe array: IDs (a bound on its unique keys)
+    int32_t stamp = 0;    // the query's stamp
     int64_t nnz = 0, n_unique = 0, n_chunks = 0, n_multi = 0, n_miss = 0;
     int64_t n_own = 0;  // misses of the planned batch itself (n_miss less prefetched rows)
     bool ev_planned = false;  // the plan recorded ev_planned (event-wait mode at plan time)
@@ -364,7 +369,15 @@ struct sp_ctx {
 
     // device state
     float *storage = nullptr;
-    int32_t *key_of_slot = nullptr, *last_use = nullptr, *held = nullptr;
+    int32_t *key_of_slot = nullptr, *last_use = nullptr;
+    int32_t *hold_to = nullptr;  // last plan holding each slot (-1: none)
+    int32_t *held = nullptr;     // stamp of the last query whose entering batches hold the slot
+    int32_t stamp = 0;           // of the last query
+    int64_t total_rows = 0;      // rows of all tables
+    int64_t *rbase = nullptr;    // [T + 1] first row index of each table (device)
+    int32_t *lastq = nullptr, *pend = nullptr;  // per row: see RowIndex
+    int32_t *hcnt = nullptr;     // [MAX_TABLES][HOLD_RING] slots per table and hold_to value
+    int64_t entered = -1;        // last batch whose slots an accepted plan has marked held
     int32_t *uses = nullptr;  // per-slot use counts, LFU only
     int pf_depth = 0;         // plans also fill the missing rows of this many successors
     uint32_t *pf_own_key = nullptr;  // prefetch mode: the planned batch's own misses,
@@ -397,12 +410,10 @@ struct sp_ctx {
     std::vector<hipStream_t> upd_stream;    // stream each ticket's backward ran on
     std::vector<char> upd_val;              // its update wrote its SEM_UPD word
     int64_t planned = 0, forwarded = 0, updated = 0;
-    int32_t stamp = 0;
     // query of plan spec_ticket over spec_nhold batches, issued early by the
-    // plan before it (-1: none); its hold marks carry spec_stamp
+    // plan before it (-1: none)
     int64_t spec_ticket = -1;
     int spec_nhold = 0;
-    int32_t spec_stamp = 0;
     hipStream_t last_update_stream = nullptr;
 
     // scratch of the plan stream and of the ingest stream
@@ -909,7 +920,13 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     TRY(dalloc(h, &h->storage, S * h->D));
     TRY(dalloc(h, &h->key_of_slot, S));
     TRY(dalloc(h, &h->last_use, S));
+    TRY(dalloc(h, &h->hold_to, S));
     TRY(dalloc(h, &h->held, S));
+    for (int t = 0; t < T; ++t) h->total_rows += h->tb.rows[t];
+    TRY(dalloc(h, &h->rbase, T + 1));
+    TRY(dalloc(h, &h->lastq, h->total_rows));
+    TRY(dalloc(h, &h->pend, h->total_rows));
+    TRY(dalloc(h, &h->hcnt, (int64_t)MAX_TABLES * HOLD_RING));
     if (h->policy == POLICY_LFU) TRY(dalloc(h, &h->uses, S));
     int64_t cap = 1024;
     while (cap < 2 * S) cap <<= 1;
@@ -942,6 +959,7 @@ static sp_status build(sp_ctx *h, const sp_config *c)
         TRY(dalloc(h, &b.perm, N));
         TRY(dalloc(h, &b.sbag, N));
         TRY(dalloc(h, &b.ukeys, N));
+        TRY(dalloc(h, &b.eslot, N));
         TRY(dalloc(h, &b.inv, N));
         TRY(dalloc(h, &b.seg_off, N + 1));
         TRY(dalloc(h, &b.seg_chunk0, N));
@@ -1072,7 +1090,16 @@ static sp_status build(sp_ctx *h, const sp_config *c)
     HIPCHK(nullptr, hipMemsetAsync(h->key_of_slot, 0xFF, sizeof(int32_t) * S, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->last_use, 0xFF, sizeof(int32_t) * S, h->s_plan));
     if (h->uses) HIPCHK(nullptr, hipMemsetAsync(h->uses, 0, sizeof(int32_t) * S, h->s_plan));
+    HIPCHK(nullptr, hipMemsetAsync(h->hold_to, 0xFF, sizeof(int32_t) * S, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->held, 0, sizeof(int32_t) * S, h->s_plan));
+    HIPCHK(nullptr, hipMemsetAsync(h->lastq, 0xFF, sizeof(int32_t) * h->total_rows, h->s_plan));
+    HIPCHK(nullptr, hipMemsetAsync(h->pend, 0, sizeof(int32_t) * h->total_rows, h->s_plan));
+    {
+        std::vector<int64_t> rb((size_t)T + 1, 0);
+        for (int t = 0; t < T; ++t) rb[t + 1] = rb[t] + h->tb.rows[t];
+        HIPCHK(nullptr, hipMemcpy(h->rbase, rb.data(), sizeof(int64_t) * (T + 1), hipMemcpyHostToDevice));
+    }
+    HIPCHK(nullptr, hipMemsetAsync(h->hcnt, 0, sizeof(int32_t) * MAX_TABLES * HOLD_RING, h->s_plan));
     HIPCHK(nullptr, hipMemsetAsync(h->hash, 0xFF, sizeof(uint64_t) * cap, h->s_plan));
     // all-ones words are NaN: under SP_FLAG_POISON a read of a never-filled slot shows
     HIPCHK(nullptr, hipMemsetAsync(h->storage, h->poison ? 0xFF : 0, sizeof(float) * S * h->D, h->s_plan));
@@ -1449,26 +1476,24 @@ static sp_status wait_counts(sp_ctx *h, uint32_t seq, DevCounters *c)
 // Phase 1 of plan k over window batches k .. k+nhold-1, all ingested or being
 // ingested: hold marks, the planned batch's hits and per-table miss / held
 // counts, published to host-coherent memory (read-only on the scratchpad).
-static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, int32_t *stamp_out,
-                               uint32_t *seq_out)
+static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, uint32_t *seq_out)
 {
     const int e = (int)(k % h->nring);
     const bool timing = h->flags & SP_FLAG_TIMING;
     if (timing) HIPCHK(h, h->t_qry.begin(h->s_plan));
     // the ticket buffers being reused belonged to ticket k - nring
     if (k >= h->nring) HIPCHK(h, wait_unless_done(h->s_plan, h->ev_upd[e]));
-    const uint32_t *ukeys[MAX_WINDOW];
-    const int32_t *nuniq[MAX_WINDOW];
-    int64_t max_nnz = 0;
+    TicketHost &th = h->tkh[e];
+    int64_t nnz[MAX_WINDOW] = {};
     for (int w = 0; w < nhold; ++w) {
         const int r = (int)((k + w) % h->nring);
         if (!h->ring_seen[r]) {  // later queries are behind this one on the same stream
             HIPCHK(h, wait_unless_done(h->s_plan, h->ring_ready[r]));
             h->ring_seen[r] = 1;
         }
-        ukeys[w] = h->ring[r].ukeys;
-        nuniq[w] = h->ring[r].scal;
-        max_nnz = std::max(max_nnz, h->ring_nnz[r]);
+        th.uk[w] = h->ring[r].ukeys;
+        th.nu[w] = h->ring[r].scal;
+        nnz[w] = h->ring_nnz[r];
     }
     // the past window: batches planned before k stay in the ring (nring covers them)
     int nwin = nhold;
@@ -1476,14 +1501,34 @@ static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, int32_t *stamp_o
         const int r = (int)(q % h->nring);
         if (h->ring_batch[r] != q)
             return fail(h, SP_ERR_HIP, "internal: past batch %lld is not in the window ring", (long long)q);
-        ukeys[nwin] = h->ring[r].ukeys;
-        nuniq[nwin] = h->ring[r].scal;
-        max_nnz = std::max(max_nnz, h->ring_nnz[r]);
+        th.uk[nwin] = h->ring[r].ukeys;
+        th.nu[nwin] = h->ring[r].scal;
+        nnz[nwin] = h->ring_nnz[r];
     }
-    const int32_t stamp = ++h->stamp;
-    *seq_out = ++h->qseq;
     const PrefetchDev pf{std::min(h->pf_depth, nhold - 1), h->pf_own_key, h->pf_own_uidx,
                          h->pf_flag, h->max_ids};
+    // rows: the planned batch, the successors to prefetch, and the batches
+    // entering the hold window.  A batch marked held by an earlier plan but no
+    // longer in the window (the caller shortened it) makes every hold be
+    // rebuilt from this window and the past ones.
+    QueryRows &qr = th.qr;
+    qr = QueryRows{};
+    qr.span = h->L + h->P;
+    qr.rebuild = h->entered > k + nhold - 1;
+    int64_t max_nnz = 0;
+    for (int w = 0; w < nwin; ++w) {
+        qr.qoff[w] = w < nhold ? w : -(w - nhold + 1);
+        qr.eslot[w] = h->ring[(k + qr.qoff[w]) % h->nring].eslot;
+        th.ent_len[w] = nnz[w];
+        const bool ent = qr.rebuild || (w < nhold && k + w > h->entered);
+        if (ent) qr.entrant |= 1u << w;
+        if (w == 0 || w <= pf.depth || ent) {
+            qr.idx[qr.n++] = w;
+            max_nnz = std::max(max_nnz, nnz[w]);
+        }
+    }
+    th.stamp = ++h->stamp;
+    *seq_out = ++h->qseq;
     // staged fill without prefetch: the query itself hands the missing keys to
     // the host (their pinned slot was last read by the gather of plan k - nstage)
     const int sl = (int)(k % h->nstage);
@@ -1492,15 +1537,15 @@ static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, int32_t *stamp_o
         TRY(join_fill(h, k - h->nstage));
         host_keys = h->h_mkey_dev[sl];
     }
-    launch_query(h->tb, h->hash, h->hash_mask, ukeys, nuniq, nwin, max_nnz, h->held, stamp,
-                 h->tk[e], pf, h->cnt, h->cnt_part, h->cnt_part + PART_COPIES * PART_WORDS,
-                 h->ring[k % h->nring].scal, h->h_cnt_dev, *seq_out, host_keys, h->stage_rows,
-                 h->ws_plan, h->s_plan);
+    launch_query(h->tb, h->hash, h->hash_mask, th.uk, th.nu, nwin, max_nnz, h->hold_to, h->held,
+                 th.stamp, h->hcnt, (int32_t)k, qr, RowIndex{h->rbase, h->lastq, h->pend}, h->tk[e],
+                 pf, h->cnt, h->cnt_part,
+                 h->cnt_part + PART_COPIES * PART_WORDS, h->ring[k % h->nring].scal, h->h_cnt_dev,
+                 *seq_out, host_keys, h->stage_rows, h->ws_plan, h->s_plan);
     CHECK_LAUNCH(h);
     if (host_keys) HIPCHK(h, hipEventRecord(h->ev_mkey[sl], h->s_plan));  // the keys are complete
     if (h->ws_plan.overflow) return fail(h, SP_ERR_HIP, "internal: scan workspace too small");
     if (timing) HIPCHK(h, h->t_qry.end(h->s_plan));
-    *stamp_out = stamp;
     return SP_OK;
 }
 
@@ -1556,9 +1601,8 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     bool spec = h->spec_ticket == k && h->spec_nhold == nhold;
     for (int w = 0; w < nhold && spec; ++w) spec = h->ring_batch[(k + w) % h->nring] == k + w;
     h->spec_ticket = -1;
-    int32_t stamp = h->spec_stamp;
     uint32_t seq = h->spec_seq;
-    if (!spec) TRY(enqueue_query(h, k, nhold, &stamp, &seq));
+    if (!spec) TRY(enqueue_query(h, k, nhold, &seq));
     const int r0 = (int)(k % h->nring);
     double tC = host_ms();
     h->host_ms[1] += tC - tB;
@@ -1668,6 +1712,29 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
         if (k >= 1) HIPCHK(h, wait_unless_done(h->s_plan, h->ev_upd[(k - 1) % h->nring]));
     }
     if (timing) HIPCHK(h, h->t_plan.begin(h->s_plan));
+    // the plan is accepted: the entering batches' cached slots become held.
+    // The commit marks them (the victims are chosen without them: the query
+    // stamped them); a rebuild drops every hold and marks them first.
+    HoldRows hr{};
+    for (int r = 0; r < th.qr.n; ++r) {
+        const int w = th.qr.idx[r];
+        if (!((th.qr.entrant >> w) & 1u)) continue;
+        const int y = hr.n++;
+        hr.uk[y] = th.uk[w];
+        hr.nu[y] = th.nu[w];
+        hr.es[y] = th.qr.eslot[w];
+        hr.nv_off[y] = th.qr.qoff[w] + h->P;
+        hr.q_off[y] = th.qr.qoff[w];
+        hr.start[y + 1] = hr.start[y] + th.ent_len[w];
+    }
+    const RowIndex ri{h->rbase, h->lastq, h->pend};
+    // the filled rows' holds from lastq / pend when at most one batch enters
+    const bool fast_hold = !th.qr.rebuild && hr.n <= 1;
+    const int32_t ent = hr.n == 1 ? hr.q_off[0] : 0;
+    if (th.qr.rebuild) {
+        launch_hold_rebuild(h->tb, hr, ri, h->hold_to, h->hcnt, u, h->s_plan);
+        hr = HoldRows{};
+    }
 
     if (n_miss > 0) {
         const int64_t cap = (int64_t)h->hash_mask + 1;
@@ -1713,19 +1780,28 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
                        : std::max(1, bits_for((uint64_t)u + (h->policy == POLICY_LFU)));
         a.prio_bits = nb;
         a.act_bits = bits_for((uint64_t)(a.nact - 1));
-        a.stamp = stamp;
+        a.plan = u;
+        a.stamp = th.stamp;
         a.prio = Prio{h->policy == POLICY_LFU ? h->uses : h->last_use, h->policy, (uint32_t)u, h->seed};
         const int levels = (nb + SEL_BITS - 1) / SEL_BITS;
         if (fresh)
             launch_fresh_victims(f, maxK, tk.v_slot, h->s_plan);
         else
-            launch_select_victims(a, levels, maxS, h->held, h->sel_state, h->sel_hist, h->vk0,
+            launch_select_victims(a, levels, maxS, h->hold_to, h->held, h->sel_state, h->sel_hist, h->vk0,
                                   h->vv0, h->vk1, (uint32_t *)nullptr, n_miss, h->hist,
                                   h->ws_plan, tk.v_slot, &h->cnt->err_sticky, h->s_plan);
     }
+    WindowKeys wk{};
+    wk.n = nhold;
+    wk.hold_past = h->P;
+    wk.fast = fast_hold;
+    wk.ent = ent;
+    wk.stamp = th.stamp;
+    for (int w = 0; w < nhold; ++w) wk.uk[w] = th.uk[w], wk.nu[w] = th.nu[w];
     launch_commit(h->tb, h->hash, h->hash_mask, tk, b0, n_miss, th.n_unique, th.nnz, h->key_of_slot,
-                  h->last_use, h->uses, u, pf_on, h->cnt, h->s_plan);
+                  h->last_use, h->uses, u, pf_on, wk, hr, ri, h->hold_to, h->hcnt, h->cnt, h->s_plan);
     CHECK_LAUNCH(h);
+    h->entered = th.qr.rebuild ? k + nhold - 1 : std::max(h->entered, k + nhold - 1);
     if (h->ws_plan.overflow) return fail(h, SP_ERR_HIP, "internal: scan workspace too small");
     HIPCHK(h, hipStreamWriteValue64(h->s_plan, h->sem + SEM_PLANNED, (uint64_t)k + 1, 0));
     // the event only serves event-wait mode; value waits on SEM_PLANNED always work
@@ -1748,7 +1824,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     // ---- the next plan's query, when its whole window is known: batches
     // k+1 .. k+L+1 are all in the ring now; it runs right behind this commit
     if (n >= h->L + 2) {
-        TRY(enqueue_query(h, k + 1, h->L + 1, &h->spec_stamp, &h->spec_seq));
+        TRY(enqueue_query(h, k + 1, h->L + 1, &h->spec_seq));
         h->spec_ticket = k + 1;
         h->spec_nhold = h->L + 1;
     }

@@ -30,13 +30,19 @@ __device__ __forceinline__ P pick_uniform(const P (&a)[MAX_WINDOW], int w)
     return r;
 }
 
-// The query of one plan, one launch.  blockIdx.y = window batch.  Every
-// cached key of a window batch stamps its slot as held for this plan
-// (held[slot] = stamp) and counts it once per table; batch 0 (the planned
-// one) also records hit / slot, counts misses and compacts them in ascending
-// key order into m_key / m_uidx with a single-pass scan (its blocks take
-// their tiles of keys from an atomic counter, so a tile only looks back at
-// tiles whose blocks have started).  Per-table counts are summed
+// The query of one plan, one launch.  blockIdx.y = row (QueryRows).  Batch 0
+// (the planned one) records hit / slot, counts misses and compacts them in
+// ascending key order into m_key / m_uidx with a single-pass scan (its blocks
+// take their tiles of keys from an atomic counter, so a tile only looks back
+// at tiles whose blocks have started).  A batch entering the hold window
+// records the slot of each of its keys (eslot) and stamps each cached slot
+// with this query's stamp (held[slot] = stamp, which the victim choice of
+// this plan treats as held); the first stamp of a slot counts it, per table,
+// when hold_to < plan: the slots the plan newly holds.  hold_to is not
+// written here, so a rejected plan changes nothing (its stamp is never
+// matched again); the commit raises it.  Held slots at this plan are those
+// newly held plus those whose hold_to lies in plan .. plan + span - 1,
+// counted in hcnt.  Per-table counts are summed
 // across the wave (keys are sorted, so a wave nearly always covers one table),
 // then across the block in LDS, then added to one of PART_COPIES copies of the
 // counters so that few blocks contend for an address.
@@ -49,7 +55,9 @@ __device__ __forceinline__ P pick_uniform(const P (&a)[MAX_WINDOW], int w)
 // with the query's sequence number.  The host polls until every word carries
 // it; no copy command, fence or stream synchronisation is involved, and each
 // word is whole when seen.  It then clears the copies, the per-plan counters
-// and the arrival count for the next query.
+// and the arrival count for the next query, and the hold count of value
+// plan + span (the first this plan's holds may take; its entry last counted
+// an expired value).
 //
 // Prefetch mode (depth d): batch 0's misses go to pf.own_key / pf.own_uidx
 // instead, and each successor w = 1..d flags every unique key that is not
@@ -69,8 +77,11 @@ __device__ __forceinline__ bool in_sorted(const uint32_t *__restrict__ a, int32_
 
 __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
                                                  const uint64_t *__restrict__ hash, uint32_t mask,
-                                                 ProbeArgs pa, PrefetchDev pf, int32_t *held,
-                                                 int32_t stamp,
+                                                 ProbeArgs pa, PrefetchDev pf,
+                                                 const int32_t *__restrict__ hold_to,
+                                                 int32_t *held, int32_t stamp,
+                                                 int32_t *hcnt, int32_t plan, QueryRows qr,
+                                                 RowIndex ri,
                                                  int32_t *hit, int32_t *slot_u, DevCounters *cnt,
                                                  int32_t *part, int32_t *arrived,
                                                  const int32_t *scal0, uint64_t *host_mapped,
@@ -81,7 +92,8 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
     __shared__ int32_t last_s;
     __shared__ uint32_t tile_s, pref_s;
     __shared__ uint32_t lds_scan[BLOCK / WAVE];
-    const int w = blockIdx.y;
+    const int w = pick_uniform(qr.idx, (int)blockIdx.y);
+    const bool entrant = (qr.entrant >> w) & 1u;
     for (int t = threadIdx.x; t < T; t += BLOCK) c_miss[t] = c_held[t] = c_pf[t] = 0;
     if (w == 0 && threadIdx.x == 0) tile_s = atomicAdd(d.counter, 1u) - d.base;
     __syncthreads();
@@ -113,7 +125,14 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
             slot_u[i] = slot;
             miss = slot < 0;
         }
-        if (slot >= 0) fresh = atomicExch(&held[slot], stamp) != stamp;
+        if (entrant) {
+            if (slot >= 0)
+                fresh = atomicExch(&held[slot], stamp) != stamp &&
+                        (qr.rebuild || hold_to[slot] < plan);
+            else if (t < T)
+                ri.pend[ri.rbase[t] + (key & ((1u << row_bits) - 1u))] = stamp;
+            pick_uniform(qr.eslot, w)[i] = slot;
+        }
         if (w >= 1 && w <= pf.depth) {
             fetch = slot < 0;
 #pragma unroll
@@ -193,7 +212,16 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
     for (int k = threadIdx.x; k < COUNTER_WORDS; k += BLOCK) {
         int32_t v;
         if (k >= MISS0 && k < MISS0 + MAX_TABLES) v = k - MISS0 < T ? sums[k - MISS0] : 0;
-        else if (k >= HELD0 && k < HELD0 + MAX_TABLES) v = k - HELD0 < T ? sums[MAX_TABLES + k - HELD0] : 0;
+        else if (k >= HELD0 && k < HELD0 + MAX_TABLES) {
+            const int t = k - HELD0;
+            v = 0;
+            if (t < T) {
+                v = sums[MAX_TABLES + t];
+                for (int j = 0; j < qr.span && !qr.rebuild; ++j)
+                    v += __hip_atomic_load(&hcnt[t * HOLD_RING + ((plan + j) & (HOLD_RING - 1))],
+                                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
         else if (k >= PF0 && k < PF0 + MAX_PF * MAX_TABLES)  // successor a, table tt
             v = (k - PF0) % MAX_TABLES < T ? sums[2 * MAX_TABLES + (k - PF0)] : 0;
         else v = __hip_atomic_load(&src[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -203,20 +231,31 @@ __global__ void __launch_bounds__(BLOCK) k_query(int32_t row_bits, int32_t T,
     }
     for (int r = threadIdx.x; r < n_rel; r += BLOCK)
         __hip_atomic_store(&part[word(r)], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (int t = threadIdx.x; t < T; t += BLOCK)
+        __hip_atomic_store(&hcnt[t * HOLD_RING + ((plan + qr.span) & (HOLD_RING - 1))], 0,
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (threadIdx.x == 0) __hip_atomic_store(arrived, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 void launch_query(const Tables &tb, const uint64_t *hash, uint32_t mask,
                   const uint32_t *const *ukeys, const int32_t *const *nuniq, int nwin,
-                  int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk, PrefetchDev pf,
+                  int64_t max_unique, const int32_t *hold_to, int32_t *held, int32_t stamp,
+                  int32_t *hcnt, int32_t plan, const QueryRows &qr, const RowIndex &ri,
+                  TicketDev tk, PrefetchDev pf,
                   DevCounters *cnt, int32_t *part, int32_t *arrived, const int32_t *scal0,
                   uint64_t *host_mapped, uint32_t seq, uint32_t *host_keys, int64_t host_cap,
                   ScanWs &ws, hipStream_t s)
 {
-    if (pf.depth > nwin - 1 || pf.depth > MAX_PF) {  // the caller limits it to the window
+    if (pf.depth > nwin - 1 || pf.depth > MAX_PF || qr.n < 1 || qr.n > nwin || qr.idx[0] != 0 ||
+        qr.span < 0 || qr.span >= HOLD_SPAN) {  // the caller keeps to these
         ws.overflow = true;
         return;
     }
+    for (int r = 0; r < qr.n; ++r)
+        if (qr.idx[r] < 0 || qr.idx[r] >= nwin) {
+            ws.overflow = true;
+            return;
+        }
     ProbeArgs pa{};
     for (int w = 0; w < nwin; ++w) pa.uk[w] = ukeys[w], pa.nu[w] = nuniq[w];
     // at least one block per batch so that every batch's error word is read
@@ -232,9 +271,105 @@ void launch_query(const Tables &tb, const uint64_t *hash, uint32_t mask,
     }
     ScanDev d{ws.status, ws.counter, ws.err, ws.issued, ++ws.epoch, (uint32_t)gx, (int32_t)gx};
     ws.issued += (uint32_t)gx;  // the planned batch's row of blocks takes tiles
-    hipLaunchKernelGGL(k_query, dim3((unsigned)gx, nwin), dim3(BLOCK), 0, s, tb.row_bits, tb.T,
-                       hash, mask, pa, pf, held, stamp, tk.hit, tk.slot_u, cnt, part, arrived, scal0,
-                       host_mapped, seq, tk.m_key, tk.m_uidx, host_keys, host_cap, d);
+    hipLaunchKernelGGL(k_query, dim3((unsigned)gx, (unsigned)qr.n), dim3(BLOCK), 0, s, tb.row_bits,
+                       tb.T, hash, mask, pa, pf, hold_to, held, stamp, hcnt, plan, qr, ri, tk.hit,
+                       tk.slot_u, cnt,
+                       part, arrived, scal0, host_mapped, seq, tk.m_key, tk.m_uidx, host_keys,
+                       host_cap, d);
+}
+
+// ---------------------------------------------------------------- holds
+
+// Adds per (table, value - plan) gathered in LDS, then into hcnt.
+__device__ __forceinline__ void hold_counts_flush(const int32_t *c, int32_t *hcnt, int32_t plan)
+{
+    for (int x = threadIdx.x; x < MAX_TABLES * HOLD_SPAN; x += BLOCK)
+        if (c[x])
+            atomicAdd(&hcnt[(x / HOLD_SPAN) * HOLD_RING + ((plan + x % HOLD_SPAN) & (HOLD_RING - 1))],
+                      c[x]);
+}
+
+// Thread j of a HoldRows section: its row's arrays and its key index.
+struct HoldRef {
+    const uint32_t *uk;
+    const int32_t *nu, *es;
+    int32_t off, qo;
+    int64_t i;
+};
+__device__ __forceinline__ HoldRef hold_ref(const HoldRows &hr, int64_t j)
+{
+    HoldRef h{hr.uk[0], hr.nu[0], hr.es[0], hr.nv_off[0], hr.q_off[0], j};
+#pragma unroll
+    for (int r = 1; r < MAX_WINDOW; ++r)  // selects, no indexing by a register
+        if (r < hr.n && j >= hr.start[r]) {
+            h.uk = hr.uk[r];
+            h.nu = hr.nu[r];
+            h.es = hr.es[r];
+            h.off = hr.nv_off[r];
+            h.qo = hr.q_off[r];
+            h.i = j - hr.start[r];
+        }
+    return h;
+}
+
+// One key of an entering batch: its slot (if cached) is held through the
+// batch (+ hold_past): hold_to rises to that value and, if it rose, the count
+// moves from the old value (if still live) to the new one.  Keys of two
+// entering batches may share a slot: atomicMax orders the raises, and each
+// raise moves the count exactly once.  A key not cached records the batch in
+// lastq.
+__device__ __forceinline__ void hold_key(const HoldRef &h, int32_t row_bits, int32_t T,
+                                         const RowIndex &ri, int32_t *hold_to, int32_t plan,
+                                         int32_t *c)
+{
+    if (h.i >= *h.nu) return;
+    const int32_t slot = h.es[h.i];
+    const uint32_t key = h.uk[h.i];
+    const int t = (int)(key >> row_bits);
+    if (t >= T) return;
+    if (slot < 0) {
+        atomicMax(&ri.lastq[ri.rbase[t] + (key & ((1u << row_bits) - 1u))], plan + h.qo);
+        return;
+    }
+    if (h.off < 0 || h.off >= HOLD_SPAN) return;
+    const int32_t old = atomicMax(&hold_to[slot], plan + h.off);
+    if (old < plan + h.off) {
+        if (old >= plan) atomicSub(&c[t * HOLD_SPAN + (old - plan)], 1);
+        atomicAdd(&c[t * HOLD_SPAN + h.off], 1);
+    }
+}
+
+__global__ void __launch_bounds__(BLOCK) k_hold(HoldRows hr, int32_t row_bits, int32_t T,
+                                                RowIndex ri, int32_t *hold_to, int32_t *hcnt,
+                                                int32_t plan)
+{
+    __shared__ int32_t c[MAX_TABLES * HOLD_SPAN];
+    for (int x = threadIdx.x; x < MAX_TABLES * HOLD_SPAN; x += BLOCK) c[x] = 0;
+    __syncthreads();
+    const int64_t j = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    if (j < hr.start[hr.n]) hold_key(hold_ref(hr, j), row_bits, T, ri, hold_to, plan, c);
+    __syncthreads();
+    hold_counts_flush(c, hcnt, plan);
+}
+
+__global__ void k_hold_clear(int32_t *hold_to, int64_t nslots, int32_t *hcnt)
+{
+    const int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
+    if (i < nslots) hold_to[i] = -1;
+    if (i < MAX_TABLES * HOLD_RING) hcnt[i] = 0;
+}
+
+void launch_hold_rebuild(const Tables &tb, const HoldRows &hr, const RowIndex &ri,
+                         int32_t *hold_to, int32_t *hcnt, int32_t plan, hipStream_t s)
+{
+    const int64_t ns = tb.slot_base[tb.T];
+    const int64_t n = ns > MAX_TABLES * HOLD_RING ? ns : MAX_TABLES * HOLD_RING;
+    hipLaunchKernelGGL(k_hold_clear, dim3((unsigned)((n + BLOCK - 1) / BLOCK)), dim3(BLOCK), 0, s,
+                       hold_to, ns, hcnt);
+    const int64_t m = hr.start[hr.n];
+    if (hr.n > 0 && m > 0)
+        hipLaunchKernelGGL(k_hold, dim3((unsigned)((m + BLOCK - 1) / BLOCK)), dim3(BLOCK), 0, s,
+                           hr, tb.row_bits, tb.T, ri, hold_to, hcnt, plan);
 }
 
 // ---------------------------------------------------------------- hash rebuild
@@ -295,7 +430,7 @@ constexpr int SEL_CHUNK = BLOCK * SEL_ITEMS;
 // entries invalid (-1) before the compaction fills them, and clear (all
 // tables together) the n_zero counters the global victim sort accumulates into.
 __global__ void __launch_bounds__(BLOCK) k_sel_level(SelArgs a, int shift, int first,
-                                                     const int32_t *held,
+                                                     const int32_t *hold_to, const int32_t *held,
                                                      int32_t *st, int32_t *hist, int32_t *arrived,
                                                      int32_t *victims, uint32_t *zero,
                                                      int64_t n_zero)
@@ -312,16 +447,17 @@ __global__ void __launch_bounds__(BLOCK) k_sel_level(SelArgs a, int shift, int f
     if (s0 < S) {
         const uint64_t want = (uint64_t)(uint32_t)prefix >> (shift + SEL_BITS);
         const int64_t base = a.base[ai];
-        int32_t hv[SEL_ITEMS], lv[SEL_ITEMS];
+        int32_t hv[SEL_ITEMS], sv[SEL_ITEMS], lv[SEL_ITEMS];
 #pragma unroll
         for (int r = 0; r < SEL_ITEMS; ++r) {  // all loads in flight together
             const int64_t s = s0 + (int64_t)r * BLOCK + threadIdx.x;
-            hv[r] = s < S ? held[base + s] : a.stamp;
+            hv[r] = s < S ? hold_to[base + s] : a.plan;
+            sv[r] = s < S ? held[base + s] : a.stamp;
             lv[r] = s < S ? a.prio.src[base + s] : 0;
         }
 #pragma unroll
         for (int r = 0; r < SEL_ITEMS; ++r) {
-            if (hv[r] != a.stamp) {
+            if (hv[r] < a.plan && sv[r] != a.stamp) {  // unheld
                 const uint32_t key = a.prio.key(lv[r], base + s0 + (int64_t)r * BLOCK + threadIdx.x);
                 if (((uint64_t)key >> (shift + SEL_BITS)) == want)
                     atomicAdd(&h[(key >> shift) & (SEL_BINS - 1)], 1);
@@ -381,16 +517,16 @@ struct SegAct {
 
 // (below v*) << 32 | (equal to v*) for an unheld slot, 0 for a held one.
 struct VictimFlag {
-    const int32_t *held, *st;
+    const int32_t *hold_to, *held, *st;
     Prio prio;
-    int32_t stamp;
+    int32_t plan, stamp;
     __device__ uint64_t operator()(int64_t g, int y) const
     {
         // every load unconditional (the scan batches them across items)
-        const int32_t h = held[g], src = prio.src[g];
+        const int32_t h = hold_to[g], hs = held[g], src = prio.src[g];
         const uint32_t key = prio.key(src, g), vstar = (uint32_t)st[2 * y];
         const uint64_t f = key < vstar ? (1ull << 32) : (key == vstar ? 1ull : 0ull);
-        return h == stamp ? 0ull : f;
+        return h >= plan || hs == stamp ? 0ull : f;
     }
 };
 
@@ -479,8 +615,8 @@ void launch_fresh_victims(const FreshArgs &f, int64_t max_k, int32_t *v_slot, hi
                        dim3(BLOCK), 0, s, f, v_slot);
 }
 
-void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int32_t *held,
-                           int32_t *sel_state, int32_t *sel_hist,
+void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int32_t *hold_to,
+                           const int32_t *held, int32_t *sel_state, int32_t *sel_hist,
                            uint32_t *vk0, uint32_t *vv0, uint32_t *vk1, uint32_t *vv1,
                            int64_t n_victims, uint32_t *hist, ScanWs &ws, int32_t *v_slot,
                            int32_t *err, hipStream_t s)
@@ -505,7 +641,7 @@ void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int
     for (int l = 0; l < levels; ++l) {
         int shift = (levels - 1 - l) * SEL_BITS;
         hipLaunchKernelGGL(k_sel_level, dim3(chunks, a.nact), dim3(BLOCK), 0, s, a, shift,
-                           (int)(l == 0), held, sel_state, sel_hist,
+                           (int)(l == 0), hold_to, held, sel_state, sel_hist,
                            sel_state + 2 * MAX_TABLES, (int32_t *)cv, hist,
                            prehist ? rp.table * rp.passes : (int64_t)0);
     }
@@ -528,7 +664,7 @@ void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int
     out.digit_mask = prehist ? (1u << rp.dbits) - 1u : 0u;
     out.tile_len = prehist ? (uint32_t)(BLOCK * rp.items) : 1u;
     out.tiles = prehist ? (uint32_t)rp.tiles : 0u;
-    seg_scan<uint64_t>(seg, a.nact, maxS, VictimFlag{held, sel_state, a.prio, a.stamp}, out, ws,
+    seg_scan<uint64_t>(seg, a.nact, maxS, VictimFlag{hold_to, held, sel_state, a.prio, a.plan, a.stamp}, out, ws,
                        s);
     if (small) {
         hipLaunchKernelGGL(k_victim_sort, dim3(a.nact), dim3(VS_THREADS), 0, s, a,
@@ -550,76 +686,163 @@ void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int
 // a live key another thread is erasing, and the keys inserted are known to be
 // absent.  Threads [n_miss, n_miss + max(n_unique, nnz)): touch the slots of
 // hits and point the positions of hit keys at them.  Victims are unheld and
-// hits are held, so the two groups never share a slot.
+// hits are held, so the two groups never share a slot.  A placed row is held
+// through the last window batch that has its key (binary searches of the
+// later batches' sorted keys), plus hold_past; its slot was unheld, so only
+// the new value is counted.
+__device__ __forceinline__ bool commit_fill(int64_t i, uint64_t *hash, uint32_t mask,
+                                            const TicketDev &tk, const int32_t *seg_off,
+                                            const uint32_t *perm, int64_t n_unique, int64_t nnz,
+                                            int64_t nslots, int32_t *key_of_slot,
+                                            int32_t *last_use, int32_t *uses, int32_t u,
+                                            int32_t prefetch, int32_t *err)
+{
+    // independent loads first: later stores could alias them, so the
+    // compiler would otherwise keep each behind the stores before it
+    const int32_t v = tk.v_slot[i];
+    const int32_t ui = tk.m_uidx[i];
+    const uint32_t key = tk.m_key[i];
+    // a prefetched row (prefetch mode, m_uidx = -1) is placed but not used
+    const bool fetched = prefetch && ui == -1;
+    if ((uint32_t)v >= (uint64_t)nslots || (!fetched && (uint32_t)ui >= (uint64_t)n_unique)) {
+        atomicOr(err, ERR_PLAN);
+        tk.v_old_key[i] = -1;
+        tk.v_old_lu[i] = -1;
+        return false;
+    }
+    const int32_t old = key_of_slot[v];
+    const int32_t old_lu = last_use[v];
+    const int32_t p0 = fetched ? 0 : seg_off[ui], p1 = fetched ? 0 : seg_off[ui + 1];
+    tk.v_old_key[i] = old;
+    tk.v_old_lu[i] = old_lu;
+    if (old >= 0) hash_erase(hash, mask, (uint32_t)old);
+    key_of_slot[v] = (int32_t)key;
+    if (!hash_insert(hash, mask, key, v)) atomicOr(err, ERR_HASH_FULL);
+    last_use[v] = u;
+    if (uses) uses[v] = fetched ? 0 : 1;
+    if (fetched) return true;
+    tk.slot_u[ui] = v;
+    for (int32_t p = p0; p < p1; ++p) {
+        const uint32_t j = perm[p];
+        if (j < (uint64_t)nnz) tk.slot_of[j] = v;
+    }
+    return true;
+}
+
+// The last window batch 1 .. n-1 whose sorted unique keys hold key (0 if
+// none).  The binary searches of all batches advance together, so their
+// loads are in flight at once and a miss waits for one search, not n - 1.
+__device__ __forceinline__ int32_t last_batch_with(const WindowKeys &wk, uint32_t key)
+{
+    int32_t lo[MAX_WINDOW], hi[MAX_WINDOW];
+#pragma unroll
+    for (int w = 0; w < MAX_WINDOW; ++w) {
+        lo[w] = 0;
+        hi[w] = w >= 1 && w < wk.n ? *wk.nu[w] : 0;
+    }
+    bool active = true;
+    while (active) {
+        active = false;
+#pragma unroll
+        for (int w = 1; w < MAX_WINDOW; ++w)
+            if (lo[w] < hi[w]) {
+                const int32_t mid = lo[w] + (hi[w] - lo[w]) / 2;
+                if (wk.uk[w][mid] < key) lo[w] = mid + 1;
+                else hi[w] = mid;
+                active = true;
+            }
+    }
+    int32_t q = 0;
+#pragma unroll
+    for (int w = 1; w < MAX_WINDOW; ++w)
+        if (w < wk.n && lo[w] < *wk.nu[w] && wk.uk[w][lo[w]] == key) q = w;
+    return q;
+}
+
 __global__ void __launch_bounds__(BLOCK) k_commit(uint64_t *hash, uint32_t mask, TicketDev tk,
                                                   const int32_t *inv, const int32_t *seg_off,
                                                   const uint32_t *perm, int64_t n_miss,
                                                   int64_t n_unique, int64_t nnz, int64_t nslots,
                                                   int32_t *key_of_slot, int32_t *last_use,
                                                   int32_t *uses, int32_t u, int32_t prefetch,
+                                                  WindowKeys wk, HoldRows hr, RowIndex ri,
+                                                  int64_t ent0, int32_t row_bits, int32_t T,
+                                                  int32_t *hold_to, int32_t *hcnt, int32_t plan,
                                                   int32_t *err)
 {
+    __shared__ int32_t c[MAX_TABLES * HOLD_SPAN];
+    // blocks that move hold counts (uniform per block): fills, entering keys
+    const int64_t b0 = (int64_t)blockIdx.x * BLOCK;
+    const bool fills = b0 < n_miss || b0 + BLOCK > ent0;
+    if (fills) {
+        for (int x = threadIdx.x; x < MAX_TABLES * HOLD_SPAN; x += BLOCK) c[x] = 0;
+        __syncthreads();
+    }
     const int64_t t = (int64_t)blockIdx.x * BLOCK + threadIdx.x;
     if (t < n_miss) {
-        const int64_t i = t;
-        // independent loads first: later stores could alias them, so the
-        // compiler would otherwise keep each behind the stores before it
-        const int32_t v = tk.v_slot[i];
-        const int32_t ui = tk.m_uidx[i];
-        const uint32_t key = tk.m_key[i];
-        // a prefetched row (prefetch mode, m_uidx = -1) is placed but not used
-        const bool fetched = prefetch && ui == -1;
-        if ((uint32_t)v >= (uint64_t)nslots || (!fetched && (uint32_t)ui >= (uint64_t)n_unique)) {
-            atomicOr(err, ERR_PLAN);
-            tk.v_old_key[i] = -1;
-            tk.v_old_lu[i] = -1;
-            return;
+        if (commit_fill(t, hash, mask, tk, seg_off, perm, n_unique, nnz, nslots, key_of_slot,
+                        last_use, uses, u, prefetch, err)) {
+            const uint32_t key = tk.m_key[t];
+            const int32_t v = tk.v_slot[t];
+            const int tt = (int)(key >> row_bits);
+            int32_t q = 0;  // the last window batch with the key
+            if (wk.fast && tt < T) {
+                const int64_t row = ri.rbase[tt] + (key & ((1u << row_bits) - 1u));
+                const int32_t lq = ri.lastq[row], pd = ri.pend[row];
+                if (lq > plan + wk.n - 1) {  // from a window since shortened
+                    q = last_batch_with(wk, key);
+                } else {
+                    q = lq >= plan ? lq - plan : 0;
+                    if (pd == wk.stamp && wk.ent > q) q = wk.ent;
+                }
+            } else {
+                q = last_batch_with(wk, key);
+            }
+            const int32_t off = q + wk.hold_past;
+            hold_to[v] = plan + off;
+            if (tt < T && off < HOLD_SPAN) atomicAdd(&c[tt * HOLD_SPAN + off], 1);
         }
-        const int32_t old = key_of_slot[v];
-        const int32_t old_lu = last_use[v];
-        const int32_t p0 = fetched ? 0 : seg_off[ui], p1 = fetched ? 0 : seg_off[ui + 1];
-        tk.v_old_key[i] = old;
-        tk.v_old_lu[i] = old_lu;
-        if (old >= 0) hash_erase(hash, mask, (uint32_t)old);
-        key_of_slot[v] = (int32_t)key;
-        if (!hash_insert(hash, mask, key, v)) atomicOr(err, ERR_HASH_FULL);
-        last_use[v] = u;
-        if (uses) uses[v] = fetched ? 0 : 1;
-        if (fetched) return;
-        tk.slot_u[ui] = v;
-        for (int32_t p = p0; p < p1; ++p) {
-            const uint32_t j = perm[p];
-            if (j < (uint64_t)nnz) tk.slot_of[j] = v;
+    } else if (t >= ent0) {
+        if (t - ent0 < hr.start[hr.n])
+            hold_key(hold_ref(hr, t - ent0), row_bits, T, ri, hold_to, plan, c);
+    } else {
+        const int64_t j = t - n_miss;
+        if (j < n_unique && tk.hit[j]) {
+            const int32_t v = tk.slot_u[j];
+            if ((uint32_t)v < (uint64_t)nslots) {
+                last_use[v] = u;
+                if (uses) uses[v] += 1;  // one thread per unique key, so one per slot
+            }
         }
-        return;
+        if (j < nnz) {
+            const int32_t i = inv[j];
+            if ((uint32_t)i >= (uint64_t)n_unique) tk.slot_of[j] = -1;
+            else if (tk.hit[i]) tk.slot_of[j] = tk.slot_u[i];
+        }
     }
-    const int64_t j = t - n_miss;
-    if (j < n_unique && tk.hit[j]) {
-        const int32_t v = tk.slot_u[j];
-        if ((uint32_t)v < (uint64_t)nslots) {
-            last_use[v] = u;
-            if (uses) uses[v] += 1;  // one thread per unique key, so one per slot
-        }
-    }
-    if (j < nnz) {
-        const int32_t i = inv[j];
-        if ((uint32_t)i >= (uint64_t)n_unique) tk.slot_of[j] = -1;
-        else if (tk.hit[i]) tk.slot_of[j] = tk.slot_u[i];
+    if (fills) {
+        __syncthreads();
+        hold_counts_flush(c, hcnt, plan);
     }
 }
 
 void launch_commit(const Tables &tb, uint64_t *hash, uint32_t mask, TicketDev tk,
                    const BatchDev &b, int64_t n_miss, int64_t n_unique, int64_t nnz,
                    int32_t *key_of_slot, int32_t *last_use, int32_t *uses, int32_t u,
-                   bool prefetch, DevCounters *cnt, hipStream_t s)
+                   bool prefetch, const WindowKeys &wk, const HoldRows &hr, const RowIndex &ri,
+                   int32_t *hold_to, int32_t *hcnt, DevCounters *cnt, hipStream_t s)
 {
-    const int64_t n = n_miss + (nnz > n_unique ? nnz : n_unique);
+    // threads: misses, then the planned batch's keys and positions, then the
+    // entering batches' keys
+    const int64_t ent0 = n_miss + (nnz > n_unique ? nnz : n_unique);
+    const int64_t n = ent0 + (hr.n > 0 ? hr.start[hr.n] : 0);
     if (n <= 0) return;
     const int64_t nslots = tb.slot_base[tb.T];
     hipLaunchKernelGGL(k_commit, dim3((unsigned)((n + BLOCK - 1) / BLOCK)), dim3(BLOCK), 0, s,
                        hash, mask, tk, (const int32_t *)b.inv, (const int32_t *)b.seg_off,
                        (const uint32_t *)b.perm, n_miss, n_unique, nnz, nslots, key_of_slot,
-                       last_use, uses, u, (int32_t)prefetch, &cnt->err_sticky);
+                       last_use, uses, u, (int32_t)prefetch, wk, hr, ri, ent0, tb.row_bits, tb.T,
+                       hold_to, hcnt, u, &cnt->err_sticky);
 }
 
 // ---------------------------------------------------------------- prefetch arrangement

@@ -13,6 +13,17 @@ constexpr int QUERY_TILE = 256;  // unique keys per block of the query (one per 
 constexpr int SEL_BITS = 11;     // digit width of the LRU radix select
 constexpr int SEL_BINS = 1 << SEL_BITS;
 
+// Holds.  hold_to[slot] is the last plan whose hold set contains the slot: a
+// slot is held at plan k when hold_to >= k.  A batch q's cached slots get
+// q + hold_past when q enters the hold window, a filled row gets the last
+// window batch holding its key plus hold_past, so every value lies within
+// k .. k + lookahead + hold_past (< HOLD_SPAN) at plan k.  hcnt[t][v %
+// HOLD_RING] counts table t's slots whose hold_to is v, for the live v.
+constexpr int HOLD_SPAN = 16;
+constexpr int HOLD_RING = 32;
+static_assert(MAX_WINDOW <= HOLD_SPAN, "lookahead + hold_past < MAX_WINDOW <= HOLD_SPAN");
+static_assert(HOLD_RING >= HOLD_SPAN + 2, "an expired count is cleared before its reuse");
+
 // Single-pass scan: indices per tile, published words per tile (sum and
 // inclusive prefix, two 32-bit halves each), tiles of nseg segments.
 constexpr int LB_TILE = 2048;
@@ -92,6 +103,8 @@ struct BatchDev {
     int4 *chunk_desc;                // [n_chunks] first pos, end pos, run, chunks of the run
     int32_t *multi;                  // [n_multi] runs longer than one chunk (any order)
     int32_t *scal;                   // [0] n_unique, [1] n_chunks, [2] ERR_* bits, [3] n_multi
+    int32_t *eslot;                  // [n_unique] slot of each unique key when the batch
+                                     // entered the hold window (-1: not cached)
 };
 
 // Per-plan device buffers.
@@ -134,12 +147,52 @@ struct Prio {
     __device__ uint32_t operator()(int64_t g) const { return key(src[g], g); }
 };
 
+// The rows of a plan's query.  Probe arrays: window batches 0 .. nhold-1,
+// then the past batches.  Row 0 is the planned batch (array index 0), rows
+// for the successors to prefetch (1 .. depth) and for the batches entering
+// the hold window (their cached keys are marked held by the commit sequence,
+// after the plan has been accepted) follow.  With `rebuild` every hold is
+// dropped and every window and past batch enters again.
+struct QueryRows {
+    int32_t n;                       // rows
+    int32_t idx[MAX_WINDOW];         // probe-array index of each row
+    int32_t qoff[MAX_WINDOW];        // per probe-array index: its batch less the planned one
+    uint32_t entrant;                // bit per probe-array index
+    int32_t rebuild;
+    int32_t span;                    // lookahead + hold_past
+    int32_t *eslot[MAX_WINDOW];      // per probe-array index: where an entrant's slots go
+};
+
+// The batches entering the hold window, as their slots are marked held:
+// row r's keys are covered by threads start[r] .. start[r+1] - 1.
+struct HoldRows {
+    int32_t n;
+    const uint32_t *uk[MAX_WINDOW];
+    const int32_t *nu[MAX_WINDOW];
+    const int32_t *es[MAX_WINDOW];
+    int32_t nv_off[MAX_WINDOW];      // batch + hold_past - plan
+    int32_t q_off[MAX_WINDOW];       // batch - plan
+    int64_t start[MAX_WINDOW + 1];
+};
+
+// Rows of all tables, one index each: table t's row r is rbase[t] + r.
+// lastq[row]: the last batch that entered the hold window with the row not
+// cached (-1: none), written once its plan is accepted; pend[row]: the stamp
+// of the last query whose entering batch has the row not cached.  A row
+// missing at plan k is in no earlier window batch's cached set, so these
+// two give the last window batch that has it without a search.
+struct RowIndex {
+    const int64_t *rbase;
+    int32_t *lastq, *pend;
+};
+
 // Victim selection arguments (active tables = those with misses).
 struct SelArgs {
     int32_t nact;
     int32_t prio_bits;               // bits of the priority values
     int32_t act_bits;                // bits of the active-table index in sort keys
-    int32_t stamp;
+    int32_t plan;                    // slots with hold_to >= plan are held,
+    int32_t stamp;                   // and those the plan's query stamped
     Prio prio;
     int32_t t[MAX_TABLES];
     int32_t k[MAX_TABLES];           // misses
@@ -219,25 +272,49 @@ struct PrefetchDev {
 };
 void launch_query(const Tables &tb, const uint64_t *hash, uint32_t mask,
                   const uint32_t *const *ukeys, const int32_t *const *nuniq, int nwin,
-                  int64_t max_unique, int32_t *held, int32_t stamp, TicketDev tk, PrefetchDev pf,
+                  int64_t max_unique, const int32_t *hold_to, int32_t *held, int32_t stamp,
+                  int32_t *hcnt, int32_t plan, const QueryRows &qr, const RowIndex &ri,
+                  TicketDev tk, PrefetchDev pf,
                   DevCounters *cnt, int32_t *part, int32_t *arrived, const int32_t *scal0,
                   uint64_t *host_mapped, uint32_t seq, uint32_t *host_keys, int64_t host_cap,
                   ScanWs &ws, hipStream_t s);
+// Every hold dropped, then the cached keys of hr's batches marked held:
+// hold_to = max(hold_to, batch + hold_past), with the counts moved (a plan
+// that rebuilds the holds, before its victims are chosen; otherwise the
+// commit marks them).
+void launch_hold_rebuild(const Tables &tb, const HoldRows &hr, const RowIndex &ri,
+                         int32_t *hold_to, int32_t *hcnt, int32_t plan, hipStream_t s);
 
 void launch_hash_rebuild(uint64_t *hash, uint32_t mask, const int32_t *key_of_slot, int64_t nslots,
                          DevCounters *cnt, hipStream_t s);
 void launch_fresh_victims(const FreshArgs &f, int64_t max_k, int32_t *v_slot, hipStream_t s);
-void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int32_t *held, int32_t *sel_state, int32_t *sel_hist,
+void launch_select_victims(const SelArgs &a, int levels, int64_t maxS, const int32_t *hold_to,
+                           const int32_t *held, int32_t *sel_state, int32_t *sel_hist,
                            uint32_t *vk0, uint32_t *vv0, uint32_t *vk1, uint32_t *vv1,
                            int64_t n_victims, uint32_t *hist, ScanWs &ws, int32_t *v_slot,
                            int32_t *err, hipStream_t s);
+// The window batches' sorted unique keys (0 = the planned batch), for the
+// hold of filled rows.  fast: at most one batch enters (at window index ent,
+// 0 if none) and the holds were not rebuilt, so lastq / pend (with this
+// plan's query stamp) answer; otherwise binary searches do.
+struct WindowKeys {
+    int32_t n;                       // nhold
+    int32_t hold_past;
+    int32_t fast, ent, stamp;
+    const uint32_t *uk[MAX_WINDOW];
+    const int32_t *nu[MAX_WINDOW];
+};
 // Misses into their victim slots, Hit-Map and slot metadata updated, every
-// slot the batch uses touched (last_use = u), slot_of filled.
+// slot the batch uses touched (last_use = u), slot_of filled.  A filled row is
+// held through the last window batch that has its key (plus hold_past), and
+// the cached keys of the entering batches hr (none after a rebuild) are
+// marked held.
 // uses: per-slot use counts (LFU), or null when the policy does not keep them
 void launch_commit(const Tables &tb, uint64_t *hash, uint32_t mask, TicketDev tk,
                    const BatchDev &b, int64_t n_miss, int64_t n_unique, int64_t nnz,
                    int32_t *key_of_slot, int32_t *last_use, int32_t *uses, int32_t u,
-                   bool prefetch, DevCounters *cnt, hipStream_t s);
+                   bool prefetch, const WindowKeys &wk, const HoldRows &hr, const RowIndex &ri,
+                   int32_t *hold_to, int32_t *hcnt, DevCounters *cnt, hipStream_t s);
 // Prefetch mode: the ticket's miss list, per table the planned batch's own
 // misses (ascending) then, successor by successor, its flagged keys
 // (ascending), from vbase[t] = first victim of table t; prefetched entries get

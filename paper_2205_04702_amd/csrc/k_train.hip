@@ -14,6 +14,25 @@ struct HostRows {
     const float4 *p[MAX_TABLES];  // device-visible pointers to the pinned host tables
 };
 
+// Loads and stores that do not keep the line in the caches: the update reads
+// and writes each Storage row once, and streamed rows would otherwise evict
+// the bag gradients it reads again for every chunk that uses them.
+typedef float nv4f __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ float4 nt_load(const float4 *p)
+{
+    const nv4f v = __builtin_nontemporal_load(reinterpret_cast<const nv4f *>(p));
+    return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void nt_store(float4 *p, float4 x)
+{
+    nv4f v;
+    v.x = x.x;
+    v.y = x.y;
+    v.z = x.z;
+    v.w = x.w;
+    __builtin_nontemporal_store(v, reinterpret_cast<nv4f *>(p));
+}
+
 __device__ __forceinline__ float4 f4_add(float4 a, float4 b)
 {
     return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
@@ -97,7 +116,6 @@ __device__ __forceinline__ float4 sgd_step(float4 x, float4 g, float lr)
     return x;
 }
 
-__device__ __forceinline__ void sgd_row(float4 *w, float4 g, float lr) { *w = sgd_step(*w, g, lr); }
 
 // Gradient coalescing and SGD (Sec. II-B "Backpropagation").  The sorted
 // positions of one batch form runs of equal keys; each run is cut into chunks
@@ -149,7 +167,7 @@ __global__ void __launch_bounds__(BLOCK) k_backward(float4 *__restrict__ storage
     float4 *const w = storage + (direct ? (int64_t)slot * LPR + c : 0);
     float4 w0[VPL];
 #pragma unroll
-    for (int j = 0; j < VPL; ++j) w0[j] = direct ? w[j * G] : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int j = 0; j < VPL; ++j) w0[j] = direct ? nt_load(w + j * G) : make_float4(0.f, 0.f, 0.f, 0.f);
     // A chunk's bag indices arrive in one coalesced load (lane c of the group
     // holds positions c, c+G, ...) and are broadcast by shuffles, so its
     // gradient rows are requested INFL at a time without waiting on further
@@ -197,7 +215,7 @@ __global__ void __launch_bounds__(BLOCK) k_backward(float4 *__restrict__ storage
         for (int j = 0; j < VPL; ++j) partial[ch * LPR + j * G + c] = acc[j];
     } else if (direct) {
 #pragma unroll
-        for (int j = 0; j < VPL; ++j) w[j * G] = sgd_step(w0[j], acc[j], lr);
+        for (int j = 0; j < VPL; ++j) nt_store(w + j * G, sgd_step(w0[j], acc[j], lr));
     }
 }
 
@@ -239,7 +257,10 @@ __global__ void __launch_bounds__(BLOCK) k_bwd_combine(float4 *__restrict__ stor
     float4 sum = red[0][c];
     for (int k = 1; k < G; ++k) sum = f4_add(sum, red[k][c]);
     const int32_t slot = slot_u[s];
-    if ((uint32_t)slot < (uint64_t)nslots) sgd_row(storage + (int64_t)slot * LPR + c, sum, lr);
+    if ((uint32_t)slot < (uint64_t)nslots) {
+        float4 *const w = storage + (int64_t)slot * LPR + c;
+        nt_store(w, sgd_step(nt_load(w), sum, lr));
+    }
 }
 
 // ---------------------------------------------------------------- evict / fill

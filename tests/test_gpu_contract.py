@@ -336,3 +336,44 @@ def test_allocation_failure_is_reported_and_cleaned_up(harness, fill, monkeypatc
         ctx.close()
     finally:
         host.close()
+
+
+@pytest.mark.parametrize("hold_past", [0, 1])
+def test_window_length_changes(harness, hold_past):
+    """Windows that shorten and lengthen from step to step: a window shorter
+    than what earlier plans held makes the plan rebuild every hold, and a
+    longer one has several batches enter the hold window at once.  Every plan
+    must equal the oracle's for the same windows, and the tables its
+    training."""
+    import torch
+    from oracle import oracle
+    w = wl.custom(rows=[1500, 2500, 900], dim=32, batch=24, pooling=[3, 2, 4],
+                  slots=[420, 380, 300], lookahead=3, steps=26, dist=("zipf", 1.0), seed=53)
+    _say(f"case window length changes, hold_past {hold_past}")
+    batches = harness.make_inputs(w)
+    host = harness.fresh_host(w)
+    ref = [wl.init_table(w, t) for t in range(w.tables)]
+    planner = oracle.Planner(w.rows, w.slots)
+    ctx = spm.ScratchPipe(w.rows, w.dim, w.slots, w.lookahead, host, w.batch, 4096,
+                          hold_past=hold_past)
+    out = torch.zeros((w.tables * w.batch, w.dim), device="cuda:0")
+    n = len(batches)
+    # window lengths (1 .. lookahead + 1): drops below what was held, regrowth
+    lengths = [4, 4, 1, 1, 4, 2, 4, 4, 3, 1, 4, 4, 2, 2, 4, 1, 3, 4, 4, 1, 4, 4, 4, 2, 4, 4]
+    try:
+        for u in range(w.steps):
+            win = batches[u:min(u + lengths[u], n)]
+            t = ctx.plan(win)
+            p = planner.plan(win, w.batch, past=batches[max(0, u - hold_past):u])
+            harness.compare_plan(u, ctx.debug_plan(t, int(win[0][0].size)), p, w.tables, w.batch)
+            ctx.forward(t, out)
+            g = wl.grads(w, u)
+            ctx.backward_update(t, torch.from_numpy(g).to("cuda:0"), w.lr)
+            oracle.train_step(ref, *batches[u], w.batch, g, w.lr)
+            _say(f"  step {u} window {len(win)} done")
+        ctx.flush()
+        for t in range(w.tables):
+            assert harness.row_rel_err(host[t], ref[t]).max() <= harness.REL_TOL
+    finally:
+        ctx.close()
+        host.close()

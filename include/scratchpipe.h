@@ -77,6 +77,12 @@ typedef int32_t sp_status;
                                     the fill has used it, so a read of a slot before
                                     its fill landed, or of stale staging, shows up as
                                     NaN in outputs and tables                        */
+#define SP_FLAG_DEFER_SORTS 0x10u /* debugging aid, staged fill: batches prepared ahead
+                                    are always sorted behind the update of the plan
+                                    that received them (sp_backward_update enqueues
+                                    them; the allocation-free variant leaves them to
+                                    the next sp_plan), as they are by default only
+                                    behind a write-back copy above 256 MiB           */
 
 /* sp_config.fill: how missing rows reach the scratchpad (Sec. IV-B) */
 #define SP_FILL_MAPPED 0 /* the move kernel reads them straight from pinned,

@@ -320,7 +320,7 @@ int64_t copy_rows(float *const *tables, const Tables &tb, int dim, float *stage,
 }  // namespace
 
 constexpr uint32_t SP_FLAGS_ALL =
-    SP_FLAG_DEBUG_SYNC | SP_FLAG_TIMING | SP_FLAG_EVENT_WAITS | SP_FLAG_POISON;
+    SP_FLAG_DEBUG_SYNC | SP_FLAG_TIMING | SP_FLAG_EVENT_WAITS | SP_FLAG_POISON | SP_FLAG_DEFER_SORTS;
 
 // words of sp_ctx::sem, one cache line apart
 constexpr int SEM_PLANNED = 0, SEM_FILLED = 8, SEM_WORDS = 16;
@@ -1914,7 +1914,7 @@ extern "C" sp_status sp_plan(sp_handle h, const sp_batch *window, int32_t n, int
     if (ticket) *ticket = k;
     if (h->staged) {
         const double t0 = host_ms();
-        if (copy_bytes > DEFER_BEHIND_COPY_BYTES)
+        if (copy_bytes > DEFER_BEHIND_COPY_BYTES || (h->flags & SP_FLAG_DEFER_SORTS))
             TRY(defer_ahead(h, window, n, nhold + 1, k));
         else
             TRY(ingest_ahead(h, window, n, nhold, k));

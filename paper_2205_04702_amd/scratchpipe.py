@@ -28,6 +28,7 @@ SP_FLAG_DEBUG_SYNC = 0x1
 SP_FLAG_TIMING = 0x2
 SP_FLAG_EVENT_WAITS = 0x4
 SP_FLAG_POISON = 0x8
+SP_FLAG_DEFER_SORTS = 0x10
 SP_FILL_MAPPED = 0
 SP_FILL_STAGED = 1
 FILLS = {"mapped": SP_FILL_MAPPED, "staged": SP_FILL_STAGED}

@@ -92,7 +92,7 @@ def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all"
                device_ids=False, ref_tables=None, sync_each_step=True, compare_tables=True,
                return_tables=False, steps=None, prepare_ahead=0, policy="lru", hold_past=0,
                seed=0, max_table_ids="auto", prefetch=False, fill="mapped",
-               overwrite_held_ids=False):
+               overwrite_held_ids=False, static_backward=False):
     """Train w on the GPU and with the oracle; assert parity; return a summary.
 
     prepare_ahead: also hand the GPU that many batches after the window
@@ -104,7 +104,8 @@ def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all"
     fill: how the GPU brings missing rows in ("mapped" or "staged").
     overwrite_held_ids: with device_ids, set every ID of the batches a plan held to
     an out-of-range row once the plan returns (the library must not read a batch
-    again once a plan that holds it has returned)."""
+    again once a plan that holds it has returned).
+    static_backward: update through the allocation-free sp_backward_update_static."""
     import torch
     dev = torch.device("cuda:0")
     if batches is None:
@@ -146,7 +147,7 @@ def run_parity(w, batches=None, *, check_plan_steps="all", check_fwd_steps="all"
             sp.forward(ticket, out)
             g = wl.grads(w, u)
             gd = torch.from_numpy(g).to(dev)
-            sp.backward_update(ticket, gd, w.lr)
+            (sp.backward_update_static if static_backward else sp.backward_update)(ticket, gd, w.lr)
             ids, off = batches[u]
             o_ref = oracle.train_step(ref, ids, off, B, g, w.lr, want_out=u in fwd_set)
             for t in range(T):

@@ -165,3 +165,19 @@ def test_pageable_tables_for_the_staged_fill(huge):
     t.close()
     t.close()
     assert len(t) == 0
+
+
+def test_header_constants_match_the_binding():
+    """Every integer #define of include/scratchpipe.h that the Python binding also
+    names has the same value there, and every SP_FLAG_* and SP_ERR_* is named."""
+    hdr = open(os.path.join(ROOT, "include", "scratchpipe.h")).read()
+    consts = {m.group(1): int(m.group(2), 0)
+              for m in re.finditer(r"^#define (SP_[A-Z_]+) \(?(-?(?:0x)?[0-9a-fA-F]+)u?\)?", hdr,
+                                   re.M)}
+    assert len(consts) >= 20
+    policies = {f"SP_POLICY_{k.upper()}": v for k, v in sp.POLICIES.items()}
+    for name, val in consts.items():
+        if name.startswith("SP_POLICY_"):
+            assert policies[name] == val, name
+        elif name.startswith(("SP_FLAG_", "SP_ERR_")) or hasattr(sp, name):
+            assert getattr(sp, name) == val, name

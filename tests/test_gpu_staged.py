@@ -70,6 +70,24 @@ def test_staged_device_ids_handed_over_ahead(harness, bound):
         assert np.array_equal(x, y)
 
 
+@pytest.mark.parametrize("device_ids,static", [(False, False), (True, False), (True, True)],
+                         ids=["host-ids", "device-ids", "device-ids-static-backward"])
+def test_staged_sorts_deferred_behind_the_update(harness, device_ids, static):
+    """SP_FLAG_DEFER_SORTS: the batches prepared ahead are sorted behind each update,
+    as they are by default behind a large write-back; with the allocation-free backward
+    they are left to the next plan.  Device IDs of held batches are overwritten once
+    their plan returns.  Plans, sampled outputs and tables must match the oracle."""
+    w = wl.custom(rows=[6000, 9000, 4000], dim=32, batch=64, pooling=6,
+                  slots=[1500, 2000, 1200], lookahead=2, steps=30, dist=("zipf", 1.05),
+                  seed=47)
+    _say(f"case staged deferred sorts device_ids={device_ids} static={static}")
+    r = harness.run_parity(w, fill="staged", device_ids=device_ids, prepare_ahead=2,
+                           sync_each_step=False, flags=sp.SP_FLAG_DEFER_SORTS,
+                           static_backward=static, overwrite_held_ids=device_ids,
+                           check_fwd_steps=[0, 15, 29])
+    assert r["stats"]["evictions"] > 0
+
+
 @pytest.mark.parametrize("prefetch", [False, True])
 def test_staged_prefetch_and_past_window(harness, prefetch):
     w = wl.custom(rows=[3000, 5000], dim=32, batch=48, pooling=[3, 5], slots=[900, 1400],

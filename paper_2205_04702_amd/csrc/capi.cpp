@@ -1474,8 +1474,9 @@ static sp_status wait_counts(sp_ctx *h, uint32_t seq, DevCounters *c)
 }
 
 // Phase 1 of plan k over window batches k .. k+nhold-1, all ingested or being
-// ingested: hold marks, the planned batch's hits and per-table miss / held
-// counts, published to host-coherent memory (read-only on the scratchpad).
+// ingested: the planned batch's hits, the stamps of the entering batches'
+// cached slots, and per-table miss / held counts, published to host-coherent
+// memory (Storage, the Hit-Map and the holds are not written).
 static sp_status enqueue_query(sp_ctx *h, int64_t k, int nhold, uint32_t *seq_out)
 {
     const int e = (int)(k % h->nring);

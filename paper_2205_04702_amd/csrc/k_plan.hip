@@ -1,4 +1,4 @@
-// Planner kernels: Hit-Map query, hold marking over the hold window, victim
+// Planner kernels: Hit-Map query, holds over the hold window, victim
 // choice among unheld slots by the replacement policy, and the Hit-Map /
 // slot-metadata commit (Sec. IV-C "Putting everything together", Sec. IV-D
 // Algorithm 1; LRU is the default replacement policy of Sec. VI-E, LFU and
@@ -38,7 +38,9 @@ __device__ __forceinline__ P pick_uniform(const P (&a)[MAX_WINDOW], int w)
 // records the slot of each of its keys (eslot) and stamps each cached slot
 // with this query's stamp (held[slot] = stamp, which the victim choice of
 // this plan treats as held); the first stamp of a slot counts it, per table,
-// when hold_to < plan: the slots the plan newly holds.  hold_to is not
+// when hold_to < plan: the slots the plan newly holds.  An uncached key of
+// such a batch writes the stamp to its row's pend entry, which tells this
+// plan's commit that the key is in the entering batch.  hold_to is not
 // written here, so a rejected plan changes nothing (its stamp is never
 // matched again); the commit raises it.  Held slots at this plan are those
 // newly held plus those whose hold_to lies in plan .. plan + span - 1,
@@ -56,8 +58,8 @@ __device__ __forceinline__ P pick_uniform(const P (&a)[MAX_WINDOW], int w)
 // it; no copy command, fence or stream synchronisation is involved, and each
 // word is whole when seen.  It then clears the copies, the per-plan counters
 // and the arrival count for the next query, and the hold count of value
-// plan + span (the first this plan's holds may take; its entry last counted
-// an expired value).
+// plan + span: no slot has that value yet (this plan's commit is the first
+// that may give it), and its entry last counted an expired value.
 //
 // Prefetch mode (depth d): batch 0's misses go to pf.own_key / pf.own_uidx
 // instead, and each successor w = 1..d flags every unique key that is not

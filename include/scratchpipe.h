@@ -227,8 +227,10 @@ typedef struct {
 
 /*
  * Create a context: allocates Storage (sum(slots) x D fp32), the Hit-Map hash,
- * per-slot metadata, the window ring and staging buffers on config->device,
- * and four library streams at default priority (plan, ingest, move and copy).
+ * per-slot metadata and holds, two int32 per row of every table (sum(rows) x 8
+ * bytes: the row index behind the holds of filled rows), the window ring and
+ * staging buffers on config->device, and four library streams at default
+ * priority (plan, ingest, move and copy).
  * Nothing is cached initially.
  * Errors: SP_ERR_INVALID_ARG (config out of range; with SP_FILL_MAPPED a host
  * table that is not pinned and mapped), SP_ERR_OOM, SP_ERR_HIP.  *out is set

@@ -387,6 +387,11 @@ def main():
                      "ms_per_step": round(dth * 1e3 / K, 4),
                      "timed_steps": [first_host, first_host + K - 1],
                      "evictions_per_step": round((s2["evictions"] - s1h["evictions"]) / K, 1),
+                     # later steps: where the budget holds every table, fewer
+                     # rows are seen for the first time, so fewer miss
+                     "miss_rate": round((s2["misses"] - s1h["misses"]
+                                         - (s2.get("prefetched", 0) - s1h.get("prefetched", 0)))
+                                        / max(s2["unique"] - s1h["unique"], 1), 4),
                      "ids": "host memory, copied to the device every step"}
         log(f"[bench] timed {K} more steps with host IDs in {dth:.3f}s")
     if args.calibrate_copy > 0:

@@ -343,6 +343,10 @@ constexpr int MAX_NSTAGE = 3;
 constexpr int64_t FILL_PIECE_MIN_BYTES = 8ll << 20;
 constexpr int64_t FILL_PIECE_BYTES = 32ll << 20;
 constexpr int64_t FILL_ITEM_BYTES = 1ll << 20;
+// Host ID arrays from this size on are copied into pinned memory by several
+// threads (one reaches a fraction of the host's memory bandwidth).
+constexpr int64_t IDCOPY_ABOVE_BYTES = 8ll << 20;
+constexpr int64_t IDCOPY_GRAIN_BYTES = 2ll << 20;
 // write-back copies above this size go on the ingest stream, where they
 // overlap the next fill; smaller ones go on the copy stream
 constexpr int64_t SMALL_COPY_BYTES = 8ll << 20;
@@ -504,6 +508,7 @@ struct sp_ctx {
     bool fstop = false;
     std::string fill_err;       // first error of the fill thread (then the context is broken)
     Pool gather;
+    Pool idcopy;  // copies of large host ID arrays into pinned memory (calling thread)
     double gather_ms = 0, fill_join_ms = 0;
     Timer t_h2d;
     bool poison = false;
@@ -839,6 +844,7 @@ static void release(sp_ctx *h)
         h->worker.join();
     }
     h->scatter.stop();
+    h->idcopy.stop();
     (void)hipDeviceSynchronize();
     for (auto *v : {&h->ring_ready, &h->ev_planned, &h->ev_filled, &h->ev_upd})
         for (auto &e : *v)
@@ -1128,6 +1134,9 @@ static sp_status build(sp_ctx *h, const sp_config *c)
         h->gather.start(std::max(1, hw * 12 / 16 - 1));
         h->filler = std::thread(filler_main, h);
     }
+    // batches of host IDs larger than a single thread copies quickly
+    if (h->max_ids * (int64_t)sizeof(int32_t) >= IDCOPY_ABOVE_BYTES)
+        h->idcopy.start(std::min(3, std::max(1, hw / 4)));
     return SP_OK;
 }
 
@@ -1236,6 +1245,22 @@ static hipError_t wait_unless_done(hipStream_t s, hipEvent_t e)
     return hipStreamWaitEvent(s, e, 0);
 }
 
+// A caller's host array into pinned memory, large ones over the ID copy
+// threads.
+static void copy_host(sp_ctx *h, void *dst, const void *src, int64_t bytes)
+{
+    if (bytes < 2 * IDCOPY_GRAIN_BYTES || h->idcopy.helpers() == 0) {
+        if (bytes > 0) memcpy(dst, src, (size_t)bytes);
+        return;
+    }
+    const int64_t pieces = (bytes + IDCOPY_GRAIN_BYTES - 1) / IDCOPY_GRAIN_BYTES;
+    h->idcopy.run(pieces, 1, [&](int64_t b, int64_t e) {
+        const int64_t o = b * IDCOPY_GRAIN_BYTES;
+        const int64_t n = std::min(bytes, e * IDCOPY_GRAIN_BYTES) - o;
+        memcpy((char *)dst + o, (const char *)src + o, (size_t)n);
+    });
+}
+
 // `ahead`: the batch is only prepared, held by a later plan (window index
 // above the lookahead).  Its arrays in the caller's device memory may be read
 // after this sp_plan call returns: the query of the first plan that holds the
@@ -1269,7 +1294,7 @@ static sp_status ingest(sp_ctx *h, const sp_batch &bt, int64_t q, bool ahead,
         // this batch before a rejected plan) has long run.
         if (!prestaged) {
             if (h->ids_pending[r]) HIPCHK(h, hipEventSynchronize(h->ev_ids[r]));
-            if (bt.nnz > 0) memcpy(h->h_ids[r], bt.ids, sizeof(int32_t) * bt.nnz);
+            copy_host(h, h->h_ids[r], bt.ids, (int64_t)sizeof(int32_t) * bt.nnz);
             memcpy(h->h_off[r], bt.bag_off, sizeof(int32_t) * (nbags + 1));
         }
         if (bt.nnz > 0)
@@ -1379,7 +1404,7 @@ static sp_status defer_ahead(sp_ctx *h, const sp_batch *window, int n, int from,
         if (!bt.on_device) {
             if (h->ids_pending[r]) HIPCHK(h, hipEventSynchronize(h->ev_ids[r]));
             h->ids_pending[r] = 0;
-            if (bt.nnz > 0) memcpy(h->h_ids[r], bt.ids, sizeof(int32_t) * bt.nnz);
+            copy_host(h, h->h_ids[r], bt.ids, (int64_t)sizeof(int32_t) * bt.nnz);
             memcpy(h->h_off[r], bt.bag_off,
                    sizeof(int32_t) * ((int64_t)h->T * bt.batch + 1));
         }

@@ -1,8 +1,8 @@
 /*
  * scratchpipe.h - C ABI of an MI355X embedding-training scratchpad.
  *
- * The library trains embedding tables that live in pinned host memory through
- * a GPU-resident cache (the "scratchpad": Storage plus Hit-Map, Sec. IV-D).
+ * The library trains embedding tables that live in host memory through a
+ * GPU-resident cache (the "scratchpad": Storage plus Hit-Map, Sec. IV-D).
  * Because the sparse IDs of upcoming mini-batches are already known from the
  * training data (Sec. IV-A), every batch is planned before it is trained: its
  * missing rows are brought in and victims are chosen only among slots that no
@@ -330,9 +330,9 @@ sp_status sp_flush(sp_handle h);
 
 /*
  * Wait until every effect of the calls so far is complete: all device work
- * (the library's and the device) has finished and every row evicted so far
- * has been written back to its host table.  Unlike sp_flush it writes no
- * cached row back.  Training may continue afterwards.
+ * (on the library's streams and the rest of the device) has finished and
+ * every row evicted so far has been written back to its host table.  Unlike
+ * sp_flush it writes no cached row back.  Training may continue afterwards.
  */
 sp_status sp_sync(sp_handle h);
 

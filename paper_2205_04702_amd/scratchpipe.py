@@ -330,14 +330,14 @@ def _stream_handle(stream) -> int:
 
 
 class ScratchPipe:
-    """One scratchpad context over pinned host tables (see include/scratchpipe.h).
+    """One scratchpad context over host tables (see include/scratchpipe.h).
 
     policy: "lru", "lfu" or "random"; hold_past: earlier batches held as well;
     seed: the random policy's stream; max_table_ids: 0 or the most IDs any one
     table has in a batch (a promise that is checked); prefetch: depth d (True =
-    1): plans also fill the missing rows of their next d batches; fill: "mapped"
-    (zero-copy from pinned,
-    device-mapped tables) or "staged" (host gather, then copies)."""
+    1): plans also fill the missing rows of their next d batches; fill:
+    "mapped" (zero-copy from pinned, device-mapped tables, HostTables) or
+    "staged" (host gather, then copies; any host tables, PageableTables)."""
 
     def __init__(self, rows, dim, slots, lookahead, host_tables, max_batch, max_ids,
                  flags: int = 0, device: int = 0, policy: str = "lru", hold_past: int = 0,
@@ -367,8 +367,10 @@ class ScratchPipe:
     def plan(self, window) -> int:
         """window: [(ids, bag_off), ...] as int32 numpy arrays or int32 device tensors.
 
-        Device tensors must hold their batch already and stay unchanged until a
-        plan that holds the batch (window index <= lookahead) has returned."""
+        Device tensors must hold their batch already (synchronise the stream that
+        wrote them first: the library reads them on its own stream) and stay
+        unchanged until a plan that holds the batch (window index <= lookahead)
+        has returned."""
         n = len(window)
         arr = (sp_batch * n)()
         keep = []

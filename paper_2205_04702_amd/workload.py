@@ -210,6 +210,27 @@ def ragged_batch(w: Workload, step: int, max_len: int, empty_frac: float = 0.1):
     return np.concatenate(parts).astype(np.int32), off.astype(np.int32)
 
 
+def thinned_batch(w: Workload, step: int, tables=None, max_ids: int | None = None):
+    """batch(w, step) with only the IDs of `tables` kept (the bags of the other
+    tables become empty; () gives a batch without any ID), then only the first
+    `max_ids` of those, in CSR order (later bags empty)."""
+    ids, off = batch(w, step)
+    B = w.batch
+    lens = np.diff(off.astype(np.int64))
+    if tables is not None:
+        for t in range(w.tables):
+            if t not in tables:
+                lens[t * B:(t + 1) * B] = 0
+    if max_ids is not None:
+        lens = np.minimum(lens, np.maximum(max_ids - (np.cumsum(lens) - lens), 0))
+    keep = np.zeros(ids.size, dtype=bool)
+    for g in np.nonzero(lens)[0]:
+        keep[int(off[g]):int(off[g]) + int(lens[g])] = True
+    new_off = np.zeros(lens.size + 1, dtype=np.int64)
+    np.cumsum(lens, out=new_off[1:])
+    return ids[keep].astype(np.int32), new_off.astype(np.int32)
+
+
 def grads(w: Workload, step: int) -> np.ndarray:
     """Upstream gradient of the pooled outputs, float32 [T, B, D], N(0, sigma^2)."""
     rng = np.random.default_rng([w.seed, _GRAD, step])

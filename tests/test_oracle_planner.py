@@ -157,6 +157,45 @@ def test_ragged_and_empty_bags(oracle):
     assert run_checked(oracle, w2, batches)
 
 
+def degenerate_batches(w):
+    """Batches without any ID (alone, and two in a row, so that the planned batch
+    and the batch entering the window are empty in turn), a batch with some tables
+    without IDs, and a batch of one ID, between ordinary ones."""
+    kinds = {3: ((), None), 5: ((1,), None), 7: ((), None), 8: ((), None), 10: (None, 1)}
+    return [wl.thinned_batch(w, s, *kinds.get(s, (None, None))) for s in range(w.steps)]
+
+
+@pytest.mark.parametrize("L", [0, 1, 2])
+def test_empty_batches_and_tables(oracle, L):
+    """Zero IDs planned, held or entering the window: every property holds, an
+    empty batch has no unique keys and no misses, and training through the
+    scratchpad equals uncached training bit for bit."""
+    w = wl.custom(rows=[50, 70, 40], dim=4, batch=5, pooling=[3, 2, 2], slots=[30, 40, 25],
+                  lookahead=L, steps=14, seed=21)
+    batches = degenerate_batches(w)
+    assert [int(b[0].size) for b in batches][3] == 0 and batches[10][0].size == 1
+    assert run_checked(oracle, w, batches)
+    planner = oracle.Planner(w.rows, w.slots)
+    for u in range(w.steps):
+        p = planner.plan(batches[u:u + L + 1], w.batch)
+        if batches[u][0].size == 0:
+            assert len(p.u_row) == 0 and len(p.m_row) == 0 and p.n_evict == 0
+    plain = [wl.init_table(w, t) for t in range(w.tables)]
+    host = [t.copy() for t in plain]
+    sim = oracle.CachedSimulator(host, w.slots)
+    for u in range(w.steps):
+        g = wl.grads(w, u)
+        o_plain = oracle.train_step(plain, *batches[u], w.batch, g, w.lr, want_out=True)
+        _, o_sim = sim.step(batches[u:u + L + 1], w.batch, g, w.lr, want_out=True)
+        assert np.array_equal(o_plain, o_sim)
+        if batches[u][0].size == 0:
+            assert not o_sim.any()
+    sim.flush()
+    for t in range(w.tables):
+        assert np.array_equal(plain[t], host[t])
+    assert sim.writebacks > 0
+
+
 def test_exhaustive_tiny_spaces(oracle):
     """Every sequence of three single-table batches over 3 rows (B=1, bags of 1-2 IDs),
     every slot count and lookahead 0-2: each plan either satisfies every property or

@@ -60,3 +60,32 @@ def test_named_workload_sizes():
     assert mx.tables == 64 and all(1 <= p <= 80 for p in mx.pooling)
     assert all(1000 <= r <= 2e7 for r in mx.rows) and all(s <= r for s, r in zip(mx.slots, mx.rows))
     assert sum(mx.slots) * 64 * 4 <= 40e9
+
+
+def test_thinned_batch_keeps_a_prefix_of_each_bag_of_the_kept_tables():
+    w = wl.get_workload("tiny")
+    B = w.batch
+    full_ids, full_off = wl.batch(w, 4)
+    for tables, max_ids in [((), None), ((1, 3), None), (None, 1), ((0, 2), 300), (None, None)]:
+        ids, off = wl.thinned_batch(w, 4, tables, max_ids)
+        assert ids.dtype == np.int32 and off.dtype == np.int32
+        assert off.size == w.tables * B + 1 and off[0] == 0 and off[-1] == ids.size
+        assert np.all(np.diff(off) >= 0)
+        kept = 0
+        for g in range(w.tables * B):
+            t = g // B
+            full = full_ids[full_off[g]:full_off[g + 1]]
+            got = ids[off[g]:off[g + 1]]
+            if tables is not None and t not in tables:
+                assert got.size == 0
+            else:
+                assert np.array_equal(got, full[:got.size])
+                room = full.size if max_ids is None else min(full.size, max(max_ids - kept, 0))
+                assert got.size == room
+            kept += got.size
+        if max_ids is not None:
+            assert ids.size == min(max_ids, sum(
+                int(full_off[(t + 1) * B] - full_off[t * B]) for t in range(w.tables)
+                if tables is None or t in tables))
+    ids, off = wl.thinned_batch(w, 4)
+    assert np.array_equal(ids, full_ids) and np.array_equal(off, full_off)

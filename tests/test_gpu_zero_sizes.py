@@ -1,8 +1,8 @@
 """Batches without IDs, tables without IDs and a one-ID batch on the GPU (needs an
 MI355X): planned, held, entering the window and prepared ahead, on both ingest
-paths, with host and device IDs, the staged fill and prefetch.  Plans must match
-the oracle bit for bit, empty batches' outputs must be zeros, and tables must
-match within 1e-5 per row."""
+paths, with host and device IDs, the staged fill, prefetch, a past window and
+the random policy.  Plans must match the oracle bit for bit, empty batches'
+outputs must be zeros, and tables must match within 1e-5 per row."""
 import pytest
 
 from paper_2205_04702_amd import scratchpipe as sp
@@ -29,7 +29,10 @@ def harness():
     dict(max_table_ids=0, device_ids=True),
     dict(fill="staged", prepare_ahead=2, flags=sp.SP_FLAG_DEFER_SORTS),
     dict(prefetch=1, prepare_ahead=2),
-], ids=["lds-host-ids", "general-device-ids", "staged-deferred", "prefetch"])
+    dict(hold_past=2, prepare_ahead=2),
+    dict(policy="random", seed=5, max_table_ids=0),
+], ids=["lds-host-ids", "general-device-ids", "staged-deferred", "prefetch", "past-window",
+        "random-policy"])
 def test_empty_batches_and_tables(harness, case):
     w = wl.get_workload("tiny")
     batches = [wl.thinned_batch(w, s, *KINDS.get(s, (None, None))) for s in range(16)]
